@@ -1,0 +1,725 @@
+/*
+ * mosaic_oracle.c -- plain, slow CPU reference of the MosaicKV compressed-cache
+ * hot path (arXiv 2607.00760).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path links, loads or calls
+ * this file; it is used by tests/, by __graft_entry__.smoke() and by the
+ * cpu_baseline leg of bench.py.  It shares no code, header, table or constant
+ * generator with the HIP library: only the dense K/V/q inputs and the
+ * rotation matrices (inputs of the method) are common.
+ *
+ * Build: gcc -O2 -std=c11 -ffp-contract=off -fno-fast-math -fPIC -shared
+ * (no SIMD intrinsics; fmaf is the C library's correctly rounded fused
+ * multiply-add).
+ *
+ * What is computed, in the paper's terms:
+ *  - Stage-1 per-vector channel compression (Sec. 4.2 "Stage-1"): rotate each
+ *    K/V vector by its window's SVD rotation (Sec. 2.3: K . R^T), keep the
+ *    top-r elements by magnitude, discard the rest.
+ *  - Element groups of 1/2/4 with one bitmap bit per group and packed
+ *    values (Sec. 5.1, packed KV format and variable-granularity bitmap).
+ *  - Per-segment strategy (Sec. 4.3 "Compression Strategy", Sec. 5.5):
+ *    highest compression rate, then largest group size, whose loss is below a
+ *    threshold; largest token block size whose intra-block key variance is
+ *    below a threshold.
+ *  - Stage-2 sequence compression (Sec. 4.2 "Stage-2"): block keys are the
+ *    mean of the block's keys, channel-compressed like K; blocks are scored
+ *    by q . block-key and the top-k blocks are kept.
+ *  - PackedAttention (Sec. 5.3): attention over the selected blocks' packed
+ *    K/V with the rotation merged into the single query / output vector.
+ *  - KV update buffer (Sec. 5.3) and heterogeneous double compression
+ *    buffering (Sec. 5.4): new tokens stay uncompressed in a 32-token buffer;
+ *    a full buffer is compressed with the previous segment's strategy
+ *    (provisional), and a completed segment is finalized with its own
+ *    strategy and recompressed in place.
+ *
+ * Where the paper is silent the readings are fixed here and listed in the
+ * repository's design notes: loss = relative dropped energy (R-3), group
+ * score = L1 of the group's magnitudes (R-2), candidate order rate-first
+ * (R-4), block variance relative to total energy (R-5), global top-k per
+ * (sequence, kv head) with k = ceil(rho * N_blocks) (R-7), GQA block score =
+ * max over the group's query heads (R-8), buffer tokens always attended
+ * dense and unrotated (R-9), provisional strategy = previous finalized
+ * segment or the default (R-10), prefill remainder handled as appends
+ * (R-11), y = x . R^T with row j of R the j-th rotated channel (R-12).
+ *
+ * Exactly-defined orders (so that integer and byte results are unique):
+ *  chain(a, b)  : acc = 0; for i ascending: acc = fmaf(a_i, b_i, acc)
+ *  tree(n)      : pairwise sum of adjacent elements, level by level
+ *                 (x0+x1), (x2+x3), ... until one value; n a power of two.
+ *  Every comparison that decides an index uses fp32 values and breaks ties
+ *  by the lowest index.
+ *
+ * Parity status: see the pin list in tests/test_oracle_pins.py.  The strategy
+ * thresholds' arithmetic (dropped-energy and block-variance tree sums) is
+ * pinned only by closed forms and limiting cases; between those it is the
+ * reading above ("parity unpinned" beyond its closed forms).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define D 128
+#define MAXG 16
+
+/* ------------------------------------------------------------------ */
+/* Public structures (mirrored by oracle/oracle.py with ctypes).       */
+/* ------------------------------------------------------------------ */
+typedef struct {
+    int32_t group;          /* G: query heads per kv head */
+    int32_t dtype;          /* 0 = fp16, 1 = bf16 */
+    int32_t seg_len;        /* S (64) */
+    int32_t rot_window;     /* W, multiple of S */
+    int32_t update_buf;     /* U (32) */
+    int32_t keep_cand[3];   /* kept channels r, tried in this order */
+    int32_t group_cand[3];  /* element group sizes g, tried in this order per r */
+    int32_t block_cand[3];  /* token block sizes B, tried in this order */
+    int32_t def_keep, def_group, def_block;
+    float tau_channel, tau_block;
+    int32_t select_num, select_den;  /* rho = num / den */
+    int32_t force_default;           /* 1: every segment uses the default */
+} orc_params;
+
+typedef struct {
+    uint32_t tok_off, sc_off, first_block;
+    uint8_t r, log2g, log2b, flags; /* flags bit0: provisional */
+} orc_desc;
+
+typedef struct {
+    orc_params P;
+    int32_t cap;         /* capacity in tokens */
+    int32_t nw;          /* rotation windows held */
+    int32_t L;           /* tokens in the cache */
+    int32_t nblk_final;  /* scoreable blocks in finalized segments */
+    uint32_t tok_tail, sc_tail; /* bytes used by finalized segments */
+    uint8_t *tok, *sc;
+    size_t tok_cap, sc_cap;
+    orc_desc *desc;
+    int32_t desc_cap;
+    uint16_t bufk[32 * D], bufv[32 * D];   /* update buffer (raw dtype bits) */
+    uint16_t stgk[64 * D], stgv[64 * D];   /* raw tokens of the trailing segment */
+    float *rk, *rv;      /* [nw][D][D] or NULL (identity) */
+} orc_pair;
+
+typedef struct {
+    int32_t L, n_final, prov, n_buf, n_desc, nblk_final, nblk;
+    uint32_t tok_tail, sc_tail;
+    uint64_t used_bytes;
+} orc_info;
+
+/* ------------------------------------------------------------------ */
+/* Element conversions (own implementations, round to nearest even).  */
+/* ------------------------------------------------------------------ */
+float orc_f16_to_f32(uint16_t h) {
+    uint32_t s = (uint32_t)(h & 0x8000) << 16;
+    uint32_t e = (h >> 10) & 0x1f, m = h & 0x3ff, u;
+    if (e == 0) {
+        if (m == 0) { u = s; }
+        else {
+            /* subnormal: m * 2^-24 is exact in fp32 */
+            float f = (float)m * 0x1p-24f;
+            memcpy(&u, &f, 4);
+            u |= s;
+        }
+    } else if (e == 31) {
+        u = s | 0x7f800000u | (m << 13);
+    } else {
+        u = s | ((e + 112) << 23) | (m << 13);
+    }
+    float f; memcpy(&f, &u, 4);
+    return f;
+}
+
+uint16_t orc_f32_to_f16(float f) {
+    uint32_t x; memcpy(&x, &f, 4);
+    uint32_t sign = (x >> 16) & 0x8000u, ax = x & 0x7fffffffu;
+    if (ax > 0x7f800000u) return (uint16_t)(sign | 0x7e00u);
+    if (ax >= 0x477ff000u) return (uint16_t)(sign | 0x7c00u);
+    if (ax < 0x38800000u) {                 /* below 2^-14: fp16 subnormal or 0 */
+        if (ax < 0x33000000u) return (uint16_t)sign;   /* <= 2^-25 rounds to 0 */
+        uint32_t e = ax >> 23, mant = (ax & 0x7fffffu) | 0x800000u;
+        uint32_t sh = 126u - e;              /* value / 2^-24 = mant >> sh */
+        uint32_t q = mant >> sh, rem = mant & ((1u << sh) - 1u), half = 1u << (sh - 1u);
+        if (rem > half || (rem == half && (q & 1u))) q++;
+        return (uint16_t)(sign | q);
+    }
+    uint32_t e = ax >> 23, m = ax & 0x7fffffu;
+    uint32_t h = ((e - 112u) << 10) | (m >> 13), rem = m & 0x1fffu;
+    if (rem > 0x1000u || (rem == 0x1000u && (h & 1u))) h++;
+    return (uint16_t)(sign | h);
+}
+
+float orc_bf16_to_f32(uint16_t b) {
+    uint32_t u = (uint32_t)b << 16; float f; memcpy(&f, &u, 4); return f;
+}
+
+uint16_t orc_f32_to_bf16(float f) {
+    uint32_t u; memcpy(&u, &f, 4);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+static float to_f32(uint16_t v, int dtype) { return dtype ? orc_bf16_to_f32(v) : orc_f16_to_f32(v); }
+static uint16_t from_f32(float v, int dtype) { return dtype ? orc_f32_to_bf16(v) : orc_f32_to_f16(v); }
+
+/* ------------------------------------------------------------------ */
+/* Ordered arithmetic helpers.                                         */
+/* ------------------------------------------------------------------ */
+/* pairwise adjacent tree sum over n (power of two) values */
+float orc_tree_sum(const float *a, int n) {
+    float buf[256];
+    memcpy(buf, a, (size_t)n * sizeof(float));
+    for (int w = n; w > 1; w >>= 1)
+        for (int i = 0; i < w / 2; ++i) buf[i] = buf[2 * i] + buf[2 * i + 1];
+    return buf[0];
+}
+
+/* Sec. 2.3: the cache is rotated as x . R^T; y[j] = chain_c(x[c], R[j][c]).
+   R == NULL is the identity (y = x exactly). */
+void orc_rotate(const float *x, const float *R, float *y) {
+    if (!R) { memcpy(y, x, D * sizeof(float)); return; }
+    for (int j = 0; j < D; ++j) {
+        float acc = 0.0f;
+        for (int c = 0; c < D; ++c) acc = fmaf(x[c], R[j * D + c], acc);
+        y[j] = acc;
+    }
+}
+
+/* Group importance (reading R-2): g = 1 is |y| exactly as in Sec. 4.2
+   ("largest absolute values"); groups of 2 and 4 sum magnitudes pairwise. */
+void orc_group_scores(const float *y, int g, float *s) {
+    int n = D / g;
+    for (int i = 0; i < n; ++i) {
+        if (g == 1) s[i] = fabsf(y[i]);
+        else if (g == 2) s[i] = fabsf(y[2 * i]) + fabsf(y[2 * i + 1]);
+        else s[i] = (fabsf(y[4 * i]) + fabsf(y[4 * i + 1])) + (fabsf(y[4 * i + 2]) + fabsf(y[4 * i + 3]));
+    }
+}
+
+typedef struct { float v; int32_t i; } vi_t;
+static int cmp_desc(const void *pa, const void *pb) {
+    const vi_t *a = (const vi_t *)pa, *b = (const vi_t *)pb;
+    if (a->v > b->v) return -1;
+    if (a->v < b->v) return 1;
+    return (a->i > b->i) - (a->i < b->i);
+}
+
+/* Top-k of n values by (value descending, index ascending): keep[i] = 1 for
+   the k selected.  A library sort is the selection step.  Returns 0, or -1
+   on a non-finite input. */
+int orc_topk_mask(const float *s, int n, int k, uint8_t *keep) {
+    vi_t *a = (vi_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(vi_t));
+    if (!a) return -2;
+    for (int i = 0; i < n; ++i) {
+        if (!isfinite(s[i])) { free(a); return -1; }
+        a[i].v = s[i]; a[i].i = i; keep[i] = 0;
+    }
+    qsort(a, (size_t)n, sizeof(vi_t), cmp_desc);
+    if (k > n) k = n;
+    for (int j = 0; j < k; ++j) keep[a[j].i] = 1;
+    free(a);
+    return 0;
+}
+
+/* kept-channel mask of one rotated vector for strategy (r, g) */
+static void keep_channels(const float *y, int r, int g, uint8_t *kch) {
+    float s[D]; uint8_t kg[D];
+    orc_group_scores(y, g, s);
+    orc_topk_mask(s, D / g, r / g, kg);
+    for (int c = 0; c < D; ++c) kch[c] = kg[c / g];
+}
+
+/* ------------------------------------------------------------------ */
+/* Packed KV format (Sec. 5.1).                                        */
+/* A packed vector = [bitmap: D/g bits as little-endian u32 words, bit */
+/* i = group i kept][values: the r kept elements in ascending channel  */
+/* order, fp32 -> dtype RNE].                                          */
+/* ------------------------------------------------------------------ */
+int orc_bitmap_bytes(int g) { return D / (8 * g); }
+int orc_vec_bytes(int r, int g, int elem_bytes) { return r * elem_bytes + D / (8 * g); }
+
+static void pack_bitmap(const uint8_t *kch, int g, uint8_t *out) {
+    int nbits = D / g, nwords = nbits / 32;
+    for (int w = 0; w < nwords; ++w) {
+        uint32_t word = 0;
+        for (int b = 0; b < 32; ++b)
+            if (kch[(w * 32 + b) * g]) word |= 1u << b;
+        out[4 * w + 0] = (uint8_t)(word & 0xff);
+        out[4 * w + 1] = (uint8_t)((word >> 8) & 0xff);
+        out[4 * w + 2] = (uint8_t)((word >> 16) & 0xff);
+        out[4 * w + 3] = (uint8_t)((word >> 24) & 0xff);
+    }
+}
+
+static void pack_values(const float *y, const uint8_t *kch, int dtype, uint8_t *out) {
+    int slot = 0;
+    for (int c = 0; c < D; ++c) {
+        if (!kch[c]) continue;
+        uint16_t h = from_f32(y[c], dtype);
+        out[2 * slot] = (uint8_t)(h & 0xff);
+        out[2 * slot + 1] = (uint8_t)(h >> 8);
+        slot++;
+    }
+}
+
+/* Public: pack one rotated vector (for layout tests). */
+void orc_pack_vector(const float *y, int r, int g, int dtype, uint8_t *out) {
+    uint8_t kch[D];
+    keep_channels(y, r, g, kch);
+    pack_bitmap(kch, g, out);
+    pack_values(y, kch, dtype, out + orc_bitmap_bytes(g));
+}
+
+static int ilog2(int v) { int l = 0; while ((1 << l) < v) ++l; return l; }
+
+/* ------------------------------------------------------------------ */
+/* Strategy selection (Sec. 4.3, Sec. 5.5; readings R-3..R-6).         */
+/* ------------------------------------------------------------------ */
+/* yk, yv: [n][D] rotated vectors of one segment (n == S == 64). */
+void orc_choose_strategy(const orc_params *P, const float *yk, const float *yv, int n,
+                         int *r_out, int *g_out, int *b_out) {
+    if (P->force_default) { *r_out = P->def_keep; *g_out = P->def_group; *b_out = P->def_block; return; }
+    float totk[64], totv[64], dk[9][64], dv[9][64];
+    for (int t = 0; t < n; ++t) {
+        float ek[D], ev[D];
+        for (int c = 0; c < D; ++c) { ek[c] = yk[t * D + c] * yk[t * D + c]; ev[c] = yv[t * D + c] * yv[t * D + c]; }
+        totk[t] = orc_tree_sum(ek, D); totv[t] = orc_tree_sum(ev, D);
+        for (int ci = 0; ci < 9; ++ci) {
+            int r = P->keep_cand[ci / 3], g = P->group_cand[ci % 3];
+            uint8_t kk[D], kv[D]; float mk[D], mv[D];
+            keep_channels(yk + t * D, r, g, kk); keep_channels(yv + t * D, r, g, kv);
+            for (int c = 0; c < D; ++c) { mk[c] = kk[c] ? 0.0f : ek[c]; mv[c] = kv[c] ? 0.0f : ev[c]; }
+            dk[ci][t] = orc_tree_sum(mk, D); dv[ci][t] = orc_tree_sum(mv, D);
+        }
+    }
+    float TK = orc_tree_sum(totk, n), TV = orc_tree_sum(totv, n);
+    int chosen = 8;
+    for (int ci = 0; ci < 9; ++ci) {
+        float DK = orc_tree_sum(dk[ci], n), DV = orc_tree_sum(dv[ci], n);
+        float lk = P->tau_channel * TK, lv = P->tau_channel * TV;
+        if (DK < lk && DV < lv) { chosen = ci; break; }
+    }
+    *r_out = P->keep_cand[chosen / 3]; *g_out = P->group_cand[chosen % 3];
+    int bsel = P->block_cand[2];
+    for (int bi = 0; bi < 3; ++bi) {
+        int B = P->block_cand[bi];
+        float d[64];
+        for (int b0 = 0; b0 < n; b0 += B) {
+            float mu[D];
+            for (int c = 0; c < D; ++c) {
+                float s = yk[b0 * D + c];
+                for (int t = b0 + 1; t < b0 + B; ++t) s = s + yk[t * D + c];
+                mu[c] = s * (1.0f / (float)B);
+            }
+            for (int t = b0; t < b0 + B; ++t) {
+                float e[D];
+                for (int c = 0; c < D; ++c) { float df = yk[t * D + c] - mu[c]; e[c] = df * df; }
+                d[t] = orc_tree_sum(e, D);
+            }
+        }
+        float VB = orc_tree_sum(d, n), lim = P->tau_block * TK;
+        if (VB < lim) { bsel = B; break; }
+    }
+    *b_out = bsel;
+}
+
+/* Block key of tokens [b0, b0+B): mean in fp32, ascending token order. */
+static void block_mean(const float *yk, int b0, int B, float *mu) {
+    for (int c = 0; c < D; ++c) {
+        float s = yk[b0 * D + c];
+        for (int t = b0 + 1; t < b0 + B; ++t) s = s + yk[t * D + c];
+        mu[c] = s * (1.0f / (float)B);
+    }
+}
+
+/* Encode n tokens (n = S or U) with strategy (r, g, B) into a token-arena
+   record and a score-arena record (Sec. 5.2 compressed KV encoding). */
+static void encode_segment(const float *yk, const float *yv, int n, int r, int g, int B, int dtype,
+                           uint8_t *tok, uint8_t *sc) {
+    int bmb = orc_bitmap_bytes(g), vb = r * 2, rec = bmb + vb;
+    uint8_t kch[D];
+    for (int b0 = 0, bi = 0; b0 < n; b0 += B, ++bi) {
+        uint8_t *blk = tok + (size_t)bi * B * 2 * rec;
+        uint8_t *kbm = blk, *kval = blk + B * bmb, *vbm = kval + B * vb, *vval = vbm + B * bmb;
+        for (int j = 0; j < B; ++j) {
+            const float *k = yk + (size_t)(b0 + j) * D, *v = yv + (size_t)(b0 + j) * D;
+            keep_channels(k, r, g, kch); pack_bitmap(kch, g, kbm + j * bmb); pack_values(k, kch, dtype, kval + j * vb);
+            keep_channels(v, r, g, kch); pack_bitmap(kch, g, vbm + j * bmb); pack_values(v, kch, dtype, vval + j * vb);
+        }
+        float mu[D];
+        block_mean(yk, b0, B, mu);
+        keep_channels(mu, r, g, kch);
+        pack_bitmap(kch, g, sc + (size_t)bi * rec);
+        pack_values(mu, kch, dtype, sc + (size_t)bi * rec + bmb);
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* Per-(sequence, kv head) cache state.                                */
+/* ------------------------------------------------------------------ */
+static int max_vec_bytes(const orc_params *P) {
+    int m = orc_vec_bytes(P->def_keep, P->def_group, 2);
+    for (int i = 0; i < 3; ++i) for (int j = 0; j < 3; ++j) {
+        int v = orc_vec_bytes(P->keep_cand[i], P->group_cand[j], 2);
+        if (v > m) m = v;
+    }
+    return m;
+}
+static int min_block(const orc_params *P) {
+    int m = P->def_block;
+    for (int i = 0; i < 3; ++i) if (P->block_cand[i] < m) m = P->block_cand[i];
+    return m;
+}
+
+orc_pair *orc_pair_new(const orc_params *P, int cap, const float *rk, const float *rv, int nw) {
+    orc_pair *p = (orc_pair *)calloc(1, sizeof(orc_pair));
+    if (!p) return NULL;
+    p->P = *P; p->cap = cap; p->nw = nw;
+    int mv = max_vec_bytes(P), mb = min_block(P);
+    int nseg = cap / P->seg_len + 2;
+    p->tok_cap = (size_t)nseg * P->seg_len * 2 * mv;
+    p->sc_cap = (size_t)nseg * (P->seg_len / mb) * mv;
+    p->desc_cap = nseg;
+    p->tok = (uint8_t *)calloc(p->tok_cap, 1);
+    p->sc = (uint8_t *)calloc(p->sc_cap, 1);
+    p->desc = (orc_desc *)calloc((size_t)nseg, sizeof(orc_desc));
+    if (rk && rv && nw > 0) {
+        p->rk = (float *)malloc((size_t)nw * D * D * sizeof(float));
+        p->rv = (float *)malloc((size_t)nw * D * D * sizeof(float));
+        memcpy(p->rk, rk, (size_t)nw * D * D * sizeof(float));
+        memcpy(p->rv, rv, (size_t)nw * D * D * sizeof(float));
+    }
+    return p;
+}
+
+void orc_pair_free(orc_pair *p) {
+    if (!p) return;
+    free(p->tok); free(p->sc); free(p->desc); free(p->rk); free(p->rv); free(p);
+}
+
+static const float *rot_of(const orc_pair *p, const float *R, int token_pos) {
+    if (!R) return NULL;
+    int w = token_pos / p->P.rot_window;
+    if (w >= p->nw) w = p->nw - 1;
+    return R + (size_t)w * D * D;
+}
+
+static void rotate_tokens(const orc_pair *p, const uint16_t *raw, int n, int pos0, const float *R, float *y) {
+    const float *Rw = rot_of(p, R, pos0);
+    for (int t = 0; t < n; ++t) {
+        float x[D];
+        for (int c = 0; c < D; ++c) x[c] = to_f32(raw[(size_t)t * D + c], p->P.dtype);
+        orc_rotate(x, Rw, y + (size_t)t * D);
+    }
+}
+
+static int state_nfinal(const orc_pair *p) { return p->L / p->P.seg_len; }
+static int state_prov(const orc_pair *p) { return (p->L % p->P.seg_len) >= p->P.update_buf; }
+static int state_nbuf(const orc_pair *p) { return (p->L % p->P.seg_len) - (state_prov(p) ? p->P.update_buf : 0); }
+
+/* finalize the trailing segment: staging holds S raw tokens */
+static void finalize_segment(orc_pair *p) {
+    const orc_params *P = &p->P;
+    int S = P->seg_len, nf = p->L / S - 1;   /* index of the segment being finalized */
+    float *yk = (float *)malloc((size_t)S * D * sizeof(float)), *yv = (float *)malloc((size_t)S * D * sizeof(float));
+    rotate_tokens(p, p->stgk, S, nf * S, p->rk, yk);
+    rotate_tokens(p, p->stgv, S, nf * S, p->rv, yv);
+    int r, g, B;
+    orc_choose_strategy(P, yk, yv, S, &r, &g, &B);
+    int rec = orc_vec_bytes(r, g, 2);
+    encode_segment(yk, yv, S, r, g, B, P->dtype, p->tok + p->tok_tail, p->sc + p->sc_tail);
+    orc_desc *d = &p->desc[nf];
+    d->tok_off = p->tok_tail; d->sc_off = p->sc_tail; d->first_block = (uint32_t)p->nblk_final;
+    d->r = (uint8_t)r; d->log2g = (uint8_t)ilog2(g); d->log2b = (uint8_t)ilog2(B); d->flags = 0;
+    p->tok_tail += (uint32_t)(S * 2 * rec);
+    p->sc_tail += (uint32_t)((S / B) * rec);
+    p->nblk_final += S / B;
+    free(yk); free(yv);
+}
+
+/* flush: the first U tokens of the trailing segment, compressed with the
+   previous finalized segment's strategy (Sec. 5.4) or the default */
+static void flush_provisional(orc_pair *p) {
+    const orc_params *P = &p->P;
+    int S = P->seg_len, U = P->update_buf, nf = p->L / S;
+    int r = P->def_keep, g = P->def_group, B = P->def_block;
+    if (nf > 0) { orc_desc *pd = &p->desc[nf - 1]; r = pd->r; g = 1 << pd->log2g; B = 1 << pd->log2b; }
+    float *yk = (float *)malloc((size_t)U * D * sizeof(float)), *yv = (float *)malloc((size_t)U * D * sizeof(float));
+    rotate_tokens(p, p->stgk, U, nf * S, p->rk, yk);
+    rotate_tokens(p, p->stgv, U, nf * S, p->rv, yv);
+    encode_segment(yk, yv, U, r, g, B, P->dtype, p->tok + p->tok_tail, p->sc + p->sc_tail);
+    orc_desc *d = &p->desc[nf];
+    d->tok_off = p->tok_tail; d->sc_off = p->sc_tail; d->first_block = (uint32_t)p->nblk_final;
+    d->r = (uint8_t)r; d->log2g = (uint8_t)ilog2(g); d->log2b = (uint8_t)ilog2(B); d->flags = 1;
+    free(yk); free(yv);
+}
+
+/* Append one token (Sec. 5.3 update buffer, Sec. 5.4 double buffering).
+   Returns 0, or -3 when the capacity is exhausted. */
+int orc_pair_append(orc_pair *p, const uint16_t *k, const uint16_t *v) {
+    const orc_params *P = &p->P;
+    if (p->L >= p->cap) return -3;
+    int S = P->seg_len, U = P->update_buf;
+    int m = p->L % S, nb = state_nbuf(p);
+    memcpy(p->bufk + (size_t)nb * D, k, D * 2); memcpy(p->bufv + (size_t)nb * D, v, D * 2);
+    memcpy(p->stgk + (size_t)m * D, k, D * 2); memcpy(p->stgv + (size_t)m * D, v, D * 2);
+    p->L++;
+    if (nb + 1 == U) {
+        if (p->L % S == 0) finalize_segment(p);
+        else flush_provisional(p);
+    }
+    return 0;
+}
+
+/* Prefill compression (Sec. 5.2): full segments encoded with their own
+   strategy; the remainder of L mod S tokens goes through the append path
+   (reading R-11).  k, v: [L][D] raw dtype bits. */
+int orc_pair_compress(orc_pair *p, const uint16_t *k, const uint16_t *v, int L) {
+    const orc_params *P = &p->P;
+    if (L > p->cap || L < 0) return -3;
+    p->L = 0; p->nblk_final = 0; p->tok_tail = 0; p->sc_tail = 0;
+    int S = P->seg_len, nfull = L / S;
+    for (int s = 0; s < nfull; ++s) {
+        memcpy(p->stgk, k + (size_t)s * S * D, (size_t)S * D * 2);
+        memcpy(p->stgv, v + (size_t)s * S * D, (size_t)S * D * 2);
+        p->L = (s + 1) * S;
+        finalize_segment(p);
+    }
+    p->L = nfull * S;
+    for (int t = nfull * S; t < L; ++t) orc_pair_append(p, k + (size_t)t * D, v + (size_t)t * D);
+    return 0;
+}
+
+void orc_pair_info(const orc_pair *p, orc_info *o) {
+    const orc_params *P = &p->P;
+    o->L = p->L; o->n_final = state_nfinal(p); o->prov = state_prov(p); o->n_buf = state_nbuf(p);
+    o->n_desc = o->n_final + o->prov; o->nblk_final = p->nblk_final;
+    o->nblk = p->nblk_final;
+    uint64_t used = (uint64_t)p->tok_tail + p->sc_tail + 16ull * (uint64_t)o->n_desc
+                  + (uint64_t)o->n_buf * 2 * D * 2;
+    if (o->prov) {
+        const orc_desc *d = &p->desc[o->n_final];
+        int B = 1 << d->log2b, rec = orc_vec_bytes(d->r, 1 << d->log2g, 2);
+        o->nblk += P->update_buf / B;
+        used += (uint64_t)P->update_buf * 2 * rec + (uint64_t)(P->update_buf / B) * rec;
+    }
+    o->tok_tail = p->tok_tail; o->sc_tail = p->sc_tail; o->used_bytes = used;
+}
+
+const uint8_t *orc_pair_tok(const orc_pair *p) { return p->tok; }
+const uint8_t *orc_pair_sc(const orc_pair *p) { return p->sc; }
+const orc_desc *orc_pair_desc(const orc_pair *p) { return p->desc; }
+const uint16_t *orc_pair_bufk(const orc_pair *p) { return p->bufk; }
+const uint16_t *orc_pair_bufv(const orc_pair *p) { return p->bufv; }
+const uint16_t *orc_pair_stgk(const orc_pair *p) { return p->stgk; }
+const uint16_t *orc_pair_stgv(const orc_pair *p) { return p->stgv; }
+
+/* ------------------------------------------------------------------ */
+/* Decode (Sec. 4.2 stage-2, Sec. 5.3 PackedAttention).                */
+/* ------------------------------------------------------------------ */
+static int desc_ntok(const orc_pair *p, const orc_desc *d) {
+    return (d->flags & 1) ? p->P.update_buf : p->P.seg_len;
+}
+
+/* q rotation merged into the single query vector (Sec. 5.3): fp32 chain,
+   used for block scores. */
+static void qrot32(const orc_pair *p, const uint16_t *qh, int pos, float *out) {
+    float x[D];
+    for (int c = 0; c < D; ++c) x[c] = to_f32(qh[c], p->P.dtype);
+    orc_rotate(x, rot_of(p, p->rk, pos), out);
+}
+
+/* Block scores s_b = max over the G heads of chain over kept slots of
+   (q_rot[c], value).  Returns the number of scoreable blocks. */
+int orc_pair_scores(const orc_pair *p, const uint16_t *q, float *scores, int cap) {
+    const orc_params *P = &p->P;
+    orc_info inf; orc_pair_info(p, &inf);
+    int G = P->group, nb = 0;
+    float qr[MAXG][D];
+    int cur_w = -1;
+    for (int di = 0; di < inf.n_desc; ++di) {
+        const orc_desc *d = &p->desc[di];
+        int pos = di * P->seg_len, w = pos / P->rot_window;
+        if (w != cur_w) { for (int h = 0; h < G; ++h) qrot32(p, q + (size_t)h * D, pos, qr[h]); cur_w = w; }
+        int g = 1 << d->log2g, B = 1 << d->log2b, r = d->r, rec = orc_vec_bytes(r, g, 2), bmb = orc_bitmap_bytes(g);
+        int nblk = desc_ntok(p, d) / B;
+        for (int j = 0; j < nblk; ++j) {
+            const uint8_t *rp = p->sc + d->sc_off + (size_t)j * rec;
+            float best = 0.0f;
+            for (int h = 0; h < G; ++h) {
+                float acc = 0.0f; int slot = 0;
+                for (int gi = 0; gi < D / g; ++gi) {
+                    if (!((rp[gi >> 3] >> (gi & 7)) & 1)) continue;
+                    for (int e = 0; e < g; ++e) {
+                        int c = gi * g + e;
+                        uint16_t hv = (uint16_t)(rp[bmb + 2 * slot] | (rp[bmb + 2 * slot + 1] << 8));
+                        acc = fmaf(qr[h][c], to_f32(hv, P->dtype), acc);
+                        slot++;
+                    }
+                }
+                best = (h == 0) ? acc : fmaxf(best, acc);
+            }
+            if (best == 0.0f) best = 0.0f;   /* -0 -> +0 */
+            if (nb < cap) scores[nb] = best;
+            nb++;
+        }
+    }
+    return nb;
+}
+
+int orc_select_count(int nblk, int num, int den) {
+    if (nblk <= 0) return 0;
+    long long k = ((long long)nblk * num + den - 1) / den;
+    if (k < 1) k = 1;
+    if (k > nblk) k = nblk;
+    return (int)k;
+}
+
+/* unpack one packed vector into dense fp64 (0 at dropped channels) */
+static void unpack64(const uint8_t *bm, const uint8_t *vals, int g, int dtype, double *out) {
+    int slot = 0;
+    for (int gi = 0; gi < D / g; ++gi) {
+        int kept = (bm[gi >> 3] >> (gi & 7)) & 1;
+        for (int e = 0; e < g; ++e) {
+            int c = gi * g + e;
+            if (kept) {
+                uint16_t hv = (uint16_t)(vals[2 * slot] | (vals[2 * slot + 1] << 8));
+                out[c] = (double)to_f32(hv, dtype); slot++;
+            } else out[c] = 0.0;
+        }
+    }
+}
+
+/* Full decode step for one (sequence, kv head): block scores, top-k,
+   attention over the selected blocks and the update buffer, back-rotation.
+   q: [G][D] raw; out: [G][D] fp64.  sel (optional, capacity cap): selected
+   block indices ascending.  Returns the number selected, or < 0 on error. */
+int orc_pair_decode(const orc_pair *p, const uint16_t *q, float scale, double *out, int32_t *sel, int cap) {
+    const orc_params *P = &p->P;
+    orc_info inf; orc_pair_info(p, &inf);
+    int G = P->group, nb = inf.nblk;
+    float *scores = (float *)malloc((size_t)(nb > 0 ? nb : 1) * sizeof(float));
+    uint8_t *keep = (uint8_t *)malloc((size_t)(nb > 0 ? nb : 1));
+    orc_pair_scores(p, q, scores, nb);
+    int k = orc_select_count(nb, P->select_num, P->select_den);
+    if (nb > 0 && orc_topk_mask(scores, nb, k, keep) != 0) { free(scores); free(keep); return -1; }
+    int ns = 0;
+    for (int b = 0; b < nb; ++b) if (keep[b]) { if (sel && ns < cap) sel[ns] = b; ns++; }
+
+    /* collect logits; tokens of selected blocks grouped by window */
+    int ntok_max = nb * 16 + P->update_buf + 1;
+    double *z = (double *)malloc((size_t)ntok_max * G * sizeof(double));
+    int *tw = (int *)malloc((size_t)ntok_max * sizeof(int));       /* window, -1 = buffer */
+    double *vv = (double *)malloc((size_t)ntok_max * D * sizeof(double));
+    int nt = 0;
+    double qd[MAXG][D];
+    for (int h = 0; h < G; ++h) for (int c = 0; c < D; ++c) qd[h][c] = (double)to_f32(q[h * D + c], P->dtype);
+    int bglob = 0, cur_w = -1;
+    double qr[MAXG][D];
+    for (int di = 0; di < inf.n_desc; ++di) {
+        const orc_desc *d = &p->desc[di];
+        int pos = di * P->seg_len, w = pos / P->rot_window;
+        if (w != cur_w) {   /* q . R_k^T in fp64 for this window */
+            const float *Rk = rot_of(p, p->rk, pos);
+            for (int h = 0; h < G; ++h) for (int j = 0; j < D; ++j) {
+                if (!Rk) { qr[h][j] = qd[h][j]; continue; }
+                double a = 0.0;
+                for (int c = 0; c < D; ++c) a += qd[h][c] * (double)Rk[j * D + c];
+                qr[h][j] = a;
+            }
+            cur_w = w;
+        }
+        int g = 1 << d->log2g, B = 1 << d->log2b, r = d->r, bmb = orc_bitmap_bytes(g), vb = 2 * r, rec = bmb + vb;
+        int nblk = desc_ntok(p, d) / B;
+        for (int j = 0; j < nblk; ++j, ++bglob) {
+            if (!keep[bglob]) continue;
+            const uint8_t *blk = p->tok + d->tok_off + (size_t)j * B * 2 * rec;
+            const uint8_t *kbm = blk, *kval = blk + B * bmb, *vbm = kval + B * vb, *vval = vbm + B * bmb;
+            for (int t = 0; t < B; ++t) {
+                double kd[D];
+                unpack64(kbm + t * bmb, kval + t * vb, g, P->dtype, kd);
+                unpack64(vbm + t * bmb, vval + t * vb, g, P->dtype, vv + (size_t)nt * D);
+                for (int h = 0; h < G; ++h) {
+                    double a = 0.0;
+                    for (int c = 0; c < D; ++c) a += qr[h][c] * kd[c];
+                    z[(size_t)nt * G + h] = (double)scale * a;
+                }
+                tw[nt] = w; nt++;
+            }
+        }
+    }
+    for (int i = 0; i < inf.n_buf; ++i) {
+        for (int h = 0; h < G; ++h) {
+            double a = 0.0;
+            for (int c = 0; c < D; ++c) a += qd[h][c] * (double)to_f32(p->bufk[i * D + c], P->dtype);
+            z[(size_t)nt * G + h] = (double)scale * a;
+        }
+        for (int c = 0; c < D; ++c) vv[(size_t)nt * D + c] = (double)to_f32(p->bufv[i * D + c], P->dtype);
+        tw[nt] = -1; nt++;
+    }
+    int nwin = p->nw > 0 ? p->nw : 1;
+    if (!p->rv) nwin = 1;
+    for (int h = 0; h < G; ++h) {
+        double *o = out + (size_t)h * D;
+        for (int j = 0; j < D; ++j) o[j] = 0.0;
+        if (nt == 0) continue;
+        double m = -INFINITY;
+        for (int t = 0; t < nt; ++t) if (z[(size_t)t * G + h] > m) m = z[(size_t)t * G + h];
+        double l = 0.0;
+        double *acc = (double *)calloc((size_t)(nwin + 1) * D, sizeof(double));
+        for (int t = 0; t < nt; ++t) {
+            double e = exp(z[(size_t)t * G + h] - m);
+            l += e;
+            int slotw = (tw[t] < 0) ? nwin : (p->rv ? (tw[t] < p->nw ? tw[t] : p->nw - 1) : 0);
+            for (int c = 0; c < D; ++c) acc[(size_t)slotw * D + c] += e * vv[(size_t)t * D + c];
+        }
+        for (int w = 0; w < nwin; ++w) {
+            const double *a = acc + (size_t)w * D;
+            if (!p->rv) { for (int j = 0; j < D; ++j) o[j] += a[j]; continue; }
+            const float *Rv = p->rv + (size_t)w * D * D;
+            for (int j = 0; j < D; ++j) {
+                double s = 0.0;
+                for (int c = 0; c < D; ++c) s += a[c] * (double)Rv[c * D + j];   /* x = y . R */
+                o[j] += s;
+            }
+        }
+        for (int j = 0; j < D; ++j) o[j] = (o[j] + acc[(size_t)nwin * D + j]) / l;
+        free(acc);
+    }
+    free(scores); free(keep); free(z); free(tw); free(vv);
+    return ns;
+}
+
+/* Dense attention of one GQA group (the uncompressed reference). */
+void orc_dense_attention(const uint16_t *q, const uint16_t *k, const uint16_t *v, int L, int G, int dtype,
+                         float scale, double *out) {
+    double *z = (double *)malloc((size_t)(L > 0 ? L : 1) * sizeof(double));
+    for (int h = 0; h < G; ++h) {
+        double qd[D];
+        for (int c = 0; c < D; ++c) qd[c] = (double)to_f32(q[h * D + c], dtype);
+        double m = -INFINITY;
+        for (int t = 0; t < L; ++t) {
+            double a = 0.0;
+            for (int c = 0; c < D; ++c) a += qd[c] * (double)to_f32(k[(size_t)t * D + c], dtype);
+            z[t] = (double)scale * a;
+            if (z[t] > m) m = z[t];
+        }
+        double l = 0.0, o[D];
+        for (int j = 0; j < D; ++j) o[j] = 0.0;
+        for (int t = 0; t < L; ++t) {
+            double e = exp(z[t] - m); l += e;
+            for (int j = 0; j < D; ++j) o[j] += e * (double)to_f32(v[(size_t)t * D + j], dtype);
+        }
+        for (int j = 0; j < D; ++j) out[h * D + j] = L > 0 ? o[j] / l : 0.0;
+    }
+    free(z);
+}
+
+/* Byte accounting per token of a full segment (for the ratio closed form):
+   2 packed vectors per token plus one block key per B tokens. */
+double orc_bytes_per_token(int r, int g, int B, int elem_bytes) {
+    double v = (double)orc_vec_bytes(r, g, elem_bytes);
+    return 2.0 * v + v / (double)B;
+}

@@ -1,0 +1,461 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Each test checks the oracle against something other than itself: library
+conversions, brute force on tiny inputs, closed forms, limiting cases of the
+thresholds, textbook dense attention, exact signed-permutation rotations and
+numbers the paper prints (tests/golden/paper_numbers.json).
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+
+D = 128
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_numbers.json")))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    O.build(force=False)
+
+
+def rng(seed):
+    return np.random.default_rng(seed)
+
+
+def to_bits(x, dtype):
+    t = torch.tensor(np.asarray(x, np.float32))
+    t = t.to(torch.bfloat16 if dtype == "bf16" else torch.float16)
+    return t.view(torch.int16).numpy().view(np.uint16)
+
+
+def from_bits(b, dtype):
+    t = torch.from_numpy(np.ascontiguousarray(b).view(np.int16))
+    return t.view(torch.bfloat16 if dtype == "bf16" else torch.float16).double().numpy()
+
+
+# ---------------------------------------------------------------- conversions
+def test_f16_rne_matches_numpy():
+    r = rng(0)
+    pats = r.integers(0, 2**32, 200000, dtype=np.uint64).astype(np.uint32)
+    x = pats.view(np.float32)
+    x = x[np.isfinite(x)]
+    edge = np.array([0.0, -0.0, 65504.0, 65519.99, 65520.0, 1e-8, 2.0**-25, 2.0**-24, 3 * 2.0**-26,
+                     2.0**-14, 2.0**-14 * (1 - 2.0**-11), 1.0 + 2.0**-11, 1.0 + 3 * 2.0**-11, -3.5e-6],
+                    np.float32)
+    scaled = (r.standard_normal(100000) * r.choice([1e-6, 1e-3, 1, 100, 3e4], 100000)).astype(np.float32)
+    for xs in (x[:50000], edge, scaled):
+        got = O.f32_to_f16_bits(xs)
+        with np.errstate(over="ignore"):
+            want = xs.astype(np.float16).view(np.uint16)
+        assert np.array_equal(got, want)
+
+
+def test_bf16_rne_matches_torch():
+    r = rng(1)
+    pats = r.integers(0, 2**32, 100000, dtype=np.uint64).astype(np.uint32)
+    x = pats.view(np.float32)
+    x = x[np.isfinite(x) & (np.abs(x) < 3.3e38)]
+    x = np.concatenate([x, np.array([1.0 + 2.0**-8, 1.0 + 3 * 2.0**-8, -0.0, 1e-40], np.float32)])
+    got = O.f32_to_bf16_bits(x)
+    want = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(got, want)
+
+
+def test_16bit_to_f32_all_patterns():
+    pats = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    f16 = O.f16_bits_to_f32(pats)
+    ref = pats.view(np.float16).astype(np.float32)
+    ok = np.isfinite(ref)
+    assert np.array_equal(f16[ok].view(np.uint32), ref[ok].view(np.uint32))
+    bf = O.bf16_bits_to_f32(pats)
+    refb = (pats.astype(np.uint32) << 16).view(np.float32)
+    okb = np.isfinite(refb)
+    assert np.array_equal(bf[okb].view(np.uint32), refb[okb].view(np.uint32))
+
+
+# ---------------------------------------------------------------- ordered sums
+def test_tree_sum_is_pairwise():
+    # exact on integers; and pairwise (not left-to-right) where rounding decides:
+    # (1+1) + (1+2^24) = 2 + 2^24 -> 16777218 ; left-to-right would give 16777220
+    a = np.array([1.0, 1.0, 1.0, 2.0**24], np.float32)
+    assert O.tree_sum(a) == np.float32(16777218.0)
+    ints = rng(2).integers(-1000, 1000, 128).astype(np.float32)
+    assert O.tree_sum(ints) == np.float32(ints.astype(np.int64).sum())
+
+
+# ---------------------------------------------------------------- rotation (Sec. 2.3)
+def test_rotation_identity_exact():
+    x = rng(3).standard_normal((5, D)).astype(np.float32)
+    assert np.array_equal(O.rotate(x, np.eye(D, dtype=np.float32)), x)
+    assert np.array_equal(O.rotate(x, None), x)
+
+
+def test_rotation_signed_permutation_exact():
+    r = rng(4)
+    perm = r.permutation(D)
+    sign = r.choice([-1.0, 1.0], D)
+    R = np.zeros((D, D), np.float32)
+    R[np.arange(D), perm] = sign            # row j picks channel perm[j]
+    x = r.standard_normal((3, D)).astype(np.float32)
+    y = O.rotate(x, R)
+    assert np.array_equal(y, (x[:, perm] * sign).astype(np.float32))
+
+
+def test_rotation_matches_matmul_and_norm():
+    r = rng(5)
+    Q, _ = np.linalg.qr(r.standard_normal((D, D)))
+    R = Q.astype(np.float32)
+    x = r.standard_normal((4, D)).astype(np.float32)
+    y = O.rotate(x, R)
+    ref = x.astype(np.float64) @ R.astype(np.float64).T
+    assert np.max(np.abs(y - ref)) < 1e-5
+    assert np.allclose(np.linalg.norm(y, axis=1), np.linalg.norm(x, axis=1), rtol=1e-5)
+
+
+# ---------------------------------------------------------------- top-k rule
+def _brute_topk(s, k):
+    """Max-sum subset of size k; ties -> lexicographically smallest index set."""
+    best, best_set = None, None
+    for sub in itertools.combinations(range(len(s)), k):
+        tot = sum(int(s[i]) for i in sub)
+        if best is None or tot > best:
+            best, best_set = tot, sub
+    return set(best_set)
+
+
+def test_topk_matches_brute_force():
+    r = rng(6)
+    for n in range(1, 10):
+        for _ in range(6):
+            s = r.integers(0, 4, n).astype(np.float32)   # many ties
+            for k in range(0, n + 1):
+                m = O.topk_mask(s, k)
+                assert set(np.nonzero(m)[0].tolist()) == (_brute_topk(s, k) if k else set())
+
+
+def test_topk_tie_storm_takes_lowest_indices():
+    m = O.topk_mask(np.ones(128, np.float32), 32)
+    assert np.array_equal(np.nonzero(m)[0], np.arange(32))
+    m = O.topk_mask(np.array([0.0, -0.0, 0.0, -0.0], np.float32), 2)   # -0 == +0
+    assert np.array_equal(np.nonzero(m)[0], [0, 1])
+
+
+def test_group_scores_closed_form():
+    y = np.zeros(D, np.float32)
+    y[:8] = [1, -2, 3, -4, 0.5, 0.25, -8, 16]
+    assert O.group_scores(y, 1)[:8].tolist() == [1, 2, 3, 4, 0.5, 0.25, 8, 16]
+    assert O.group_scores(y, 2)[:4].tolist() == [3, 7, 0.75, 24]
+    assert O.group_scores(y, 4)[:2].tolist() == [10, 24.75]
+
+
+# ---------------------------------------------------------------- packed format (Sec. 5.1)
+def _unpack(rec, r, g, dtype):
+    """Independent decoder of one packed vector -> (kept channel mask, values at kept)."""
+    nbits = D // g
+    words = rec[: nbits // 8].view(np.uint32) if nbits >= 32 else None
+    bits = np.array([(int(words[i // 32]) >> (i % 32)) & 1 for i in range(nbits)], bool)
+    kept = np.repeat(bits, g)
+    vals = rec[nbits // 8:].view(np.uint16)
+    assert vals.size == r
+    return kept, vals
+
+
+@pytest.mark.parametrize("r,g", [(16, 4), (16, 2), (16, 1), (32, 4), (32, 2), (32, 1), (48, 4), (48, 2), (48, 1)])
+@pytest.mark.parametrize("dtype", ["fp16", "bf16"])
+def test_pack_vector_roundtrip(r, g, dtype):
+    rr = rng(7 + r + g)
+    for _ in range(5):
+        y = (rr.standard_normal(D) * rr.choice([0.1, 1, 10], D)).astype(np.float32)
+        rec = O.pack_vector(y, r, g, dtype)
+        assert rec.size == r * 2 + D // (8 * g)
+        kept, vals = _unpack(rec, r, g, dtype)
+        # kept groups = top r/g by (L1 magnitude desc, index asc), computed with numpy
+        a = np.abs(y).reshape(-1, g)
+        sc = a[:, 0] if g == 1 else ((a[:, 0] + a[:, 1]) if g == 2 else (a[:, 0] + a[:, 1]) + (a[:, 2] + a[:, 3]))
+        order = np.lexsort((np.arange(sc.size), -sc))
+        want = np.zeros(sc.size, bool)
+        want[order[: r // g]] = True
+        assert np.array_equal(kept, np.repeat(want, g))
+        assert np.array_equal(vals, to_bits(y[kept], dtype))
+
+
+def test_bitmap_and_ratio_paper_numbers():
+    ex = GOLD["bitmap_example"]
+    e = ex["elem_bits"] // 8
+    r = int(round(D * (1 - ex["compression_rate"])))
+    dense = D * e
+    assert r * e / dense == ex["packed_fraction"]
+    assert O.bitmap_bytes(1) / dense == ex["bitmap_fraction"]
+    assert O.vec_bytes(r, 1, e) == r * e + O.bitmap_bytes(1)
+    full = GOLD["memory_reduction_vs_full"]
+    st = full["strategy"]
+    ratio = 2 * D * 2 / O.bytes_per_token(st["keep"], st["group"], st["block"], 2)
+    assert abs(ratio - full["value"]) < full["abs_tol"]
+    q = GOLD["memory_reduction_vs_quest"]
+    assert abs(ratio * (1 + q["quest_overhead"]) - q["value"]) < q["abs_tol"]
+
+
+def test_used_bytes_closed_form_forced_default():
+    P = O.Params(force_default=True, dtype="bf16")
+    pr = O.Pair(P, 640)
+    x = to_bits(rng(8).standard_normal((640, D)), "bf16")
+    pr.compress(x, x)
+    inf = pr.info()
+    per_seg = 64 * 2 * (32 * 2 + 16) + 8 * (32 * 2 + 16) + 16
+    assert inf.used_bytes == 10 * per_seg
+    assert all((d["r"], d["log2g"], d["log2b"]) == (32, 0, 3) for d in pr.descriptors())
+    ratio = 640 * 2 * D * 2 / inf.used_bytes
+    assert abs(ratio - 512 / (160 + 10 + 0.25)) < 1e-12
+
+
+# ---------------------------------------------------------------- strategy (Sec. 4.3 / 5.5)
+def test_strategy_all_ones_closed_form():
+    # all-equal magnitudes: kept = lowest groups, dropped fraction = (128 - r) / 128 exactly
+    y = np.ones((64, D), np.float32)
+    for tau, want in [(0.9, (16, 4)), (0.8, (32, 4)), (0.7, (48, 4)), (0.6, (48, 1))]:
+        r, g, B = O.choose_strategy(O.Params(tau_channel=tau, tau_block=0.5), y, y)
+        assert (r, g) == want
+        assert B == 16                      # identical tokens: zero intra-block variance
+    r, g, B = O.choose_strategy(O.Params(tau_channel=0.9, tau_block=0.0), y, y)
+    assert B == 4                           # tau 0: nothing is strictly below 0 -> fallback
+
+
+def test_strategy_one_hot_is_lossless():
+    y = np.zeros((64, D), np.float32)
+    y[np.arange(64), (np.arange(64) * 7) % D] = 3.0
+    r, g, B = O.choose_strategy(O.Params(tau_channel=1e-6), y, y)
+    assert (r, g) == (16, 4)
+
+
+def test_strategy_limits():
+    y = rng(9).standard_normal((64, D)).astype(np.float32)
+    assert O.choose_strategy(O.Params(tau_channel=np.inf, tau_block=np.inf), y, y) == (16, 4, 16)
+    assert O.choose_strategy(O.Params(tau_channel=0.0, tau_block=0.0), y, y) == (48, 1, 4)
+
+
+def test_block_size_closed_forms():
+    base = np.ones(D, np.float32)
+    # constant inside each 8-token group, sign flips between groups: B=16 mean is 0
+    # (variance = total energy), B=8 variance is 0
+    y = np.stack([base * (1 if (t // 8) % 2 == 0 else -1) for t in range(64)]).astype(np.float32)
+    assert O.choose_strategy(O.Params(tau_channel=0.9, tau_block=0.5), y, y)[2] == 8
+    # alternating sign every token: every block mean is 0 -> variance ratio exactly 1
+    y = np.stack([base * (1 if t % 2 == 0 else -1) for t in range(64)]).astype(np.float32)
+    assert O.choose_strategy(O.Params(tau_channel=0.9, tau_block=1.0), y, y)[2] == 4
+    assert O.choose_strategy(O.Params(tau_channel=0.9, tau_block=1.0001), y, y)[2] == 16
+
+
+def test_strategy_monotone_in_tau():
+    r = rng(10)
+    order = [(a, b) for a in (16, 32, 48) for b in (4, 2, 1)]
+    for trial in range(4):
+        scale = r.choice([1.0, 4.0, 16.0], D)
+        yk = (r.standard_normal((64, D)) * scale).astype(np.float32)
+        yv = (r.standard_normal((64, D)) * scale[::-1]).astype(np.float32)
+        prev_c, prev_b = None, None
+        for tau in (0.05, 0.1, 0.2, 0.3, 0.5, 0.8):
+            rr, g, B = O.choose_strategy(O.Params(tau_channel=tau, tau_block=tau + 0.4), yk, yv)
+            c = order.index((rr, g))
+            if prev_c is not None:
+                assert c <= prev_c and B >= prev_b
+            prev_c, prev_b = c, B
+
+
+def test_block_key_of_identical_tokens_is_the_token():
+    x = np.zeros(D, np.float32)
+    x[:40] = np.arange(40) * 0.25 - 3.0          # dyadic: block sums are exact
+    toks = np.tile(x, (64, 1))
+    bits = to_bits(toks, "fp16")
+    pr = O.Pair(O.Params(force_default=True), 64)
+    pr.compress(bits, bits)
+    sc = pr.score_arena()
+    rec = O.pack_vector(x, 32, 1, "fp16")
+    assert np.array_equal(sc.reshape(8, -1), np.tile(rec, (8, 1)))
+
+
+# ---------------------------------------------------------------- top-k count (Sec. 4.2 / 6.1)
+def test_select_count():
+    assert O.select_count(0, 1, 10) == 0
+    assert O.select_count(1, 1, 10) == 1
+    assert O.select_count(10, 1, 10) == 1
+    assert O.select_count(11, 1, 10) == 2
+    assert O.select_count(16384, 1, 10) == 1639
+    assert O.select_count(131072, 1, 10) == 13108
+    assert O.select_count(7, 1, 1) == 7
+
+
+# ---------------------------------------------------------------- decode vs dense attention
+def _numpy_attention(q, k, v, scale, dtype):
+    scale = float(np.float32(scale))            # the scale is an fp32 argument
+    qd, kd, vd = from_bits(q, dtype), from_bits(k, dtype), from_bits(v, dtype)
+    if kd.shape[0] == 0:
+        return np.zeros_like(qd)
+    z = (qd @ kd.T) * scale
+    z = z - z.max(axis=1, keepdims=True)
+    p = np.exp(z)
+    return (p @ vd) / p.sum(axis=1, keepdims=True)
+
+
+@pytest.mark.parametrize("dtype", ["fp16", "bf16"])
+@pytest.mark.parametrize("G", [4, 7])
+def test_everything_kept_equals_dense(dtype, G):
+    """r = D, rho = 1, identity rotation: the method reduces to dense attention."""
+    r = rng(11 + G)
+    for L in (0, 1, 31, 32, 33, 63, 64, 65, 100, 200, 257):
+        for B in (4, 16):
+            P = O.Params(group=G, dtype=dtype, force_default=True, default=(128, 1, B), select=(1, 1),
+                         rot_window=128)
+            k = to_bits(r.standard_normal((L, D)), dtype)
+            v = to_bits(r.standard_normal((L, D)), dtype)
+            q = to_bits(r.standard_normal((G, D)) * 2, dtype)
+            pr = O.Pair(P, max(L, 1))
+            pr.compress(k, v)
+            out, sel = pr.decode(q, 1 / math.sqrt(D))
+            ref = _numpy_attention(q, k, v, 1 / math.sqrt(D), dtype)
+            assert np.max(np.abs(out - ref)) < 1e-12, (L, B)
+            assert len(sel) == pr.info().nblk
+
+
+def test_signed_permutation_rotation_equals_dense():
+    """Exact rotations (signed permutations, one per window): the q rotation,
+    the packed rotated K/V and the back-rotation of the output must cancel."""
+    r = rng(12)
+    G, L, W = 4, 300, 128
+    nw = 3
+    Rk = np.zeros((nw, D, D), np.float32)
+    Rv = np.zeros((nw, D, D), np.float32)
+    for w in range(nw):
+        for R in (Rk[w], Rv[w]):
+            R[np.arange(D), r.permutation(D)] = r.choice([-1.0, 1.0], D)
+    P = O.Params(group=G, dtype="fp16", force_default=True, default=(128, 1, 8), select=(1, 1), rot_window=W)
+    k = to_bits(r.standard_normal((L, D)), "fp16")
+    v = to_bits(r.standard_normal((L, D)), "fp16")
+    q = to_bits(r.standard_normal((G, D)) * 2, "fp16")
+    pr = O.Pair(P, L, Rk, Rv)
+    pr.compress(k, v)
+    out, _ = pr.decode(q, 0.125)
+    ref = _numpy_attention(q, k, v, 0.125, "fp16")
+    assert np.max(np.abs(out - ref)) < 1e-12
+
+
+def test_orthogonal_rotation_close_to_dense():
+    r = rng(13)
+    G, L = 4, 256
+    Q1, _ = np.linalg.qr(r.standard_normal((D, D)))
+    Q2, _ = np.linalg.qr(r.standard_normal((D, D)))
+    P = O.Params(group=G, dtype="fp16", force_default=True, default=(128, 1, 8), select=(1, 1))
+    k = to_bits(r.standard_normal((L, D)), "fp16")
+    v = to_bits(r.standard_normal((L, D)), "fp16")
+    q = to_bits(r.standard_normal((G, D)), "fp16")
+    pr = O.Pair(P, L, Q1[None].astype(np.float32), Q2[None].astype(np.float32))
+    pr.compress(k, v)
+    out, _ = pr.decode(q, 1 / math.sqrt(D))
+    ref = _numpy_attention(q, k, v, 1 / math.sqrt(D), "fp16")
+    assert np.max(np.abs(out - ref)) < 3e-3        # only the fp16 rounding of rotated values
+
+
+def test_selection_is_topk_of_scores():
+    r = rng(14)
+    G, L = 4, 64 * 40 + 45
+    P = O.Params(group=G, dtype="bf16", tau_channel=0.3)
+    Q, _ = np.linalg.qr(r.standard_normal((D, D)))
+    R = Q.astype(np.float32)[None]
+    k = to_bits(r.standard_normal((L, D)), "bf16")
+    v = to_bits(r.standard_normal((L, D)), "bf16")
+    q = to_bits(r.standard_normal((G, D)), "bf16")
+    pr = O.Pair(P, L, R, R)
+    pr.compress(k, v)
+    s = pr.scores(q)
+    assert s.size == pr.info().nblk
+    kk = O.select_count(s.size, 1, 10)
+    order = np.lexsort((np.arange(s.size), -s.astype(np.float64)))
+    _, sel = pr.decode(q, 0.1)
+    assert np.array_equal(sel, np.sort(order[:kk]))
+
+
+def test_block_score_closed_form():
+    """Integer data, identity rotation, r = D: the chain is an exact integer
+    dot product, and the block score is the max over the group's heads."""
+    r = rng(15)
+    G = 4
+    P = O.Params(group=G, force_default=True, default=(128, 1, 4), select=(1, 1))
+    k = r.integers(-3, 4, (64, D)).astype(np.float32)
+    q = r.integers(-3, 4, (G, D)).astype(np.float32)
+    pr = O.Pair(P, 64)
+    pr.compress(to_bits(k, "fp16"), to_bits(k, "fp16"))
+    s = pr.scores(to_bits(q, "fp16"))
+    means = k.reshape(16, 4, D).mean(axis=1)           # exact (sums of small ints / 4)
+    want = (q.astype(np.float64) @ means.T.astype(np.float64)).max(axis=0)
+    assert np.array_equal(s.astype(np.float64), want)
+
+
+# ---------------------------------------------------------------- update buffer / double buffering
+def _state(pr):
+    i = pr.info()
+    bk, bv = pr.buffer()
+    sk, sv = pr.staging()
+    return (i.L, i.n_final, i.prov, i.n_buf, i.nblk, i.used_bytes, pr.token_arena().tobytes(),
+            pr.score_arena().tobytes(), pr.descriptor_bytes().tobytes(), bk.tobytes(), bv.tobytes(),
+            sk.tobytes(), sv.tobytes())
+
+
+@pytest.mark.parametrize("dtype", ["fp16", "bf16"])
+def test_prefill_equals_prefill_plus_appends(dtype):
+    r = rng(16)
+    Lmax = 64 * 5 + 40
+    Q, _ = np.linalg.qr(r.standard_normal((D, D)))
+    R = np.stack([Q, Q[::-1]]).astype(np.float32)
+    k = to_bits(r.standard_normal((Lmax, D)) * r.choice([1, 6], D), dtype)
+    v = to_bits(r.standard_normal((Lmax, D)), dtype)
+    P = O.Params(dtype=dtype, rot_window=128, tau_channel=0.25)
+    for L0, L in [(0, 70), (5, 64), (32, 97), (64, 200), (100, 257), (150, Lmax)]:
+        a = O.Pair(P, Lmax, R, R[::-1].copy())
+        a.compress(k[:L], v[:L])
+        b = O.Pair(P, Lmax, R, R[::-1].copy())
+        b.compress(k[:L0], v[:L0])
+        for t in range(L0, L):
+            b.append(k[t], v[t])
+        assert _state(a) == _state(b), (L0, L)
+
+
+def test_state_machine_counts_and_provisional_strategy():
+    r = rng(17)
+    P = O.Params(dtype="fp16", tau_channel=0.3, force_default=False)
+    k = to_bits(r.standard_normal((200, D)) * r.choice([1, 8], D), "fp16")
+    pr = O.Pair(P, 200)
+    pr.compress(k[:64], k[:64])
+    prev = pr.descriptors()[0]
+    for t in range(64, 200):
+        pr.append(k[t], k[t])
+        i = pr.info()
+        m = i.L % 64
+        assert (i.n_final, i.prov, i.n_buf) == (i.L // 64, int(m >= 32), m - 32 * int(m >= 32))
+        ds = pr.descriptors()
+        if i.prov:
+            d = ds[-1]
+            assert d["flags"] == 1
+            assert (d["r"], d["log2g"], d["log2b"]) == (prev["r"], prev["log2g"], prev["log2b"])
+            assert d["tok_off"] == i.tok_tail and d["first_block"] == i.nblk_final
+        elif m == 0:
+            prev = ds[-1]
+            assert prev["flags"] == 0
+    with pytest.raises(ValueError):
+        pr.append(k[0], k[0])                 # capacity exhausted
+
+
+def test_first_provisional_uses_default():
+    r = rng(18)
+    P = O.Params(dtype="fp16", default=(48, 2, 16))
+    k = to_bits(r.standard_normal((40, D)), "fp16")
+    pr = O.Pair(P, 64)
+    pr.compress(k, k)
+    d = pr.descriptors()
+    assert len(d) == 1 and d[0]["flags"] == 1 and (d[0]["r"], d[0]["log2g"], d[0]["log2b"]) == (48, 1, 4)
+    assert pr.info().n_buf == 8
