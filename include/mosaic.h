@@ -1,0 +1,217 @@
+/*
+ * mosaic.h -- C ABI of the MI355X (gfx950) MosaicKV hot path.
+ *
+ * MosaicKV (arXiv 2607.00760) keeps a long-context KV cache compressed in two
+ * dimensions.  Every K/V vector is rotated by its window's SVD rotation and
+ * keeps only its top-r elements (stage 1, Sec. 4.2).  Decode scores
+ * mean-of-block keys against the query and attends only the top-k blocks
+ * (stage 2, Sec. 4.2).  Each 64-token segment gets its own strategy: kept
+ * channels r, element group size g, token block size B (Sec. 4.3, Sec. 5.5).
+ * The strategy is stored in the packed KV format: packed values plus a
+ * position bitmap (Sec. 5.1).
+ *
+ * Conventions for every entry point:
+ *  - Pointers are DEVICE pointers unless the name ends in _host.
+ *  - The caller allocates and owns all device memory: inputs, the cache arena,
+ *    workspaces and outputs.  It keeps them alive until the enqueued work
+ *    completes.  The library never allocates device memory.  Only
+ *    mosaic_cache_stats synchronizes.
+ *  - `stream` is a hipStream_t (NULL = the null stream).  All work is enqueued
+ *    on it, in order.
+ *  - Validation happens before anything is enqueued.  On error nothing is
+ *    launched, the cache is unchanged, and mosaic_last_error() describes the
+ *    cause.
+ *  - head_dim is 128.  K, V and q share one element type: fp16 or bf16,
+ *    little-endian 16-bit.  Outputs are fp32.
+ *  - A cache holds num_seqs sequences x num_kv_heads kv heads.  Query head h
+ *    of a sequence reads kv head h / group_size (GQA).
+ */
+#ifndef MOSAIC_H
+#define MOSAIC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MOSAIC_OK = 0,
+    MOSAIC_ERR_INVALID = -1,     /* bad argument (NULL, shape, alignment, parameter) */
+    MOSAIC_ERR_UNSUPPORTED = -2, /* valid request outside what this build implements */
+    MOSAIC_ERR_CAPACITY = -3,    /* more tokens than the cache was created for */
+    MOSAIC_ERR_STATE = -4,       /* call out of order (e.g. decode before compress) */
+    MOSAIC_ERR_HIP = -5          /* a HIP runtime call failed */
+} mosaic_status;
+
+typedef enum { MOSAIC_FP16 = 0, MOSAIC_BF16 = 1 } mosaic_dtype;
+
+/* Method parameters.  The strategy set is Sec. 4.3: rotation, compression
+ * rate, element group size, sequence compression rate, token block size.
+ * The candidates are those of Sec. 5.5 (rates 87.5/75/62.5 % -> r = 16/32/48
+ * of 128 channels, g = 1/2/4, B = 4/8/16).  The defaults are those of
+ * Sec. 6.1 (25 % channels, block 8, 10 % of tokens). */
+typedef struct {
+    int32_t head_dim;          /* D, must be 128 */
+    int32_t num_kv_heads;      /* Hkv >= 1 */
+    int32_t group_size;        /* G = query heads per kv head, 1..8 */
+    int32_t dtype;             /* mosaic_dtype */
+    int32_t seg_len;           /* S: strategy segment length, must be 64 */
+    int32_t rot_window;        /* W: tokens sharing one rotation, multiple of S */
+    int32_t update_buf;        /* U: update-buffer tokens (Sec. 5.3), must be 32 */
+    int32_t keep_cand[3];      /* r candidates, tried in this order; multiple of g, <= 128 */
+    int32_t group_cand[3];     /* g candidates in {1, 2, 4}, tried in this order per r */
+    int32_t block_cand[3];     /* B candidates in {4, 8, 16}, tried in this order */
+    int32_t default_keep;      /* strategy of a provisional chunk with no finalized */
+    int32_t default_group;     /*   predecessor, and of every segment when */
+    int32_t default_block;     /*   force_default_strategy is set */
+    float tau_channel;         /* accept (r, g) if dropped energy < tau * energy, K and V */
+    float tau_block;           /* accept B if intra-block key variance < tau * energy */
+    int32_t select_num;        /* rho = select_num / select_den: blocks kept per */
+    int32_t select_den;        /*   (sequence, kv head) = ceil(rho * blocks) */
+    int32_t force_default_strategy; /* 1: skip the search, use the default */
+} mosaic_params;
+
+/* Fills *p with the paper's defaults (Sec. 5.5, Sec. 6.1): r in {16, 32, 48},
+ * g in {4, 2, 1}, B in {16, 8, 4}, default (32, 1, 8), S = 64, U = 32,
+ * W = 65536, tau = (0.30, 0.90), rho = 1/10, fp16, 8 kv heads, G = 4. */
+void mosaic_params_default(mosaic_params *p);
+
+typedef struct mosaic_cache mosaic_cache;  /* host bookkeeping + bound arena */
+
+/* Creates the host side of a cache for num_seqs sequences of up to max_tokens
+ * tokens each.  rotated = 1 if mosaic_compress will receive rotation matrices
+ * (Sec. 2.3); 0 for the identity rotation.  The handle owns host memory
+ * only.  Errors: INVALID (parameters), UNSUPPORTED (head_dim != 128,
+ * S != 64, U != 32), CAPACITY (a per-(sequence, kv head) arena would
+ * exceed 4 GiB). */
+mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
+                                  int32_t rotated, mosaic_cache **out);
+
+/* Bytes of device memory the cache needs (worst case over strategies).  The
+ * caller allocates it, 256-byte aligned, and binds it once. */
+mosaic_status mosaic_cache_arena_bytes(const mosaic_cache *cache, size_t *bytes);
+mosaic_status mosaic_cache_bind(mosaic_cache *cache, void *arena, size_t bytes);
+mosaic_status mosaic_cache_destroy(mosaic_cache *cache);
+
+/* Where each region lives inside the bound arena.  Every region holds one
+ * slot per (sequence, kv head) pair p = seq * num_kv_heads + kv_head, at
+ * off + p * stride.  Use it for inspection (tests, stats); the layout of a
+ * region's contents is the packed format of Sec. 5.1:
+ *   meta     : int32 tokens, int32 finalized blocks, uint32 token-arena
+ *              bytes, uint32 score-arena bytes (finalized segments)
+ *   desc     : 16-byte segment descriptors {uint32 token-arena offset,
+ *              uint32 score-arena offset, uint32 first block, uint8 r,
+ *              uint8 log2 g, uint8 log2 B, uint8 flags (bit 0 provisional)}
+ *   score    : block-key records [bitmap D/(8g) B][r values], block order
+ *   token    : per block [K bitmaps][K values][V bitmaps][V values]
+ *   buffer   : update buffer [2 (K, V)][U][D] raw elements (Sec. 5.3)
+ *   stage    : raw tokens of the trailing segment [2][S][D] (Sec. 5.4)
+ *   rot      : per window {R_k^T, R_v^T, R_v} fp32 [3][D][D]
+ */
+typedef struct {
+    uint64_t meta_off, meta_stride;
+    uint64_t desc_off, desc_stride;
+    uint64_t score_off, score_stride;
+    uint64_t token_off, token_stride;
+    uint64_t buf_off, buf_stride;
+    uint64_t stage_off, stage_stride;
+    uint64_t rot_off, rot_stride;
+    uint64_t total;
+    int32_t num_pairs, max_desc, num_windows, reserved;
+} mosaic_layout;
+mosaic_status mosaic_cache_layout(const mosaic_cache *cache, mosaic_layout *out);
+
+enum { MOSAIC_OP_COMPRESS = 0, MOSAIC_OP_APPEND = 1, MOSAIC_OP_DECODE = 2 };
+/* Workspace bytes an operation needs (0 if none).  Depends only on the
+ * cache's shape and capacity, so one allocation serves every call. */
+mosaic_status mosaic_workspace_bytes(const mosaic_cache *cache, int32_t op, size_t *bytes);
+
+/* Layout of the decode workspace (inspection): per pair p,
+ *   qrot  + p * qrot_stride  : fp32 [windows][D][GP] rotated queries
+ *   score + p * score_stride : fp32 [max_blocks] block scores
+ *   sel   + p * sel_stride   : int32 [max_blocks] selected blocks, ascending
+ *   wsel  + p * wsel_stride  : int32 [windows + 2]: first selected entry of
+ *                              each window, then k, then the block count */
+typedef struct {
+    uint64_t qrot_off, qrot_stride, score_off, score_stride, sel_off, sel_stride, wsel_off, wsel_stride;
+    uint64_t part_off, part_stride, tag_off, tag_stride, total;
+    int32_t max_blocks, max_splits, gp, reserved;
+} mosaic_ws_layout;
+mosaic_status mosaic_decode_ws_layout(const mosaic_cache *cache, mosaic_ws_layout *out);
+
+/* Prefill compression (Sec. 5.2 compressed KV encoding; strategy Sec. 4.3).
+ *   k, v      : [num_seqs][num_kv_heads][seq_stride][128], first
+ *               ctx_lens_host[s] tokens of sequence s valid.
+ *   rot_k/v   : [num_seqs][num_kv_heads][num_windows][128][128] fp32; row j
+ *               is rotated channel j, so y = x . R^T (Sec. 2.3).  Window w
+ *               covers tokens [w W, (w+1) W); num_windows = ceil(max_tokens
+ *               / W).  NULL (both) iff the cache was created with rotated = 0.
+ *   Full segments get their own strategy.  The remaining ctx_len mod S tokens
+ *   take the update path (buffer, provisional flush), as if appended.
+ * Replaces any previous contents.  ws may be NULL when the workspace size is 0.
+ * Errors: STATE (not bound), CAPACITY (ctx_len > max_tokens),
+ * INVALID (NULL, negative length, misaligned pointer, seq_stride < max ctx). */
+mosaic_status mosaic_compress(mosaic_cache *cache, const void *k, const void *v, int64_t seq_stride,
+                              const int32_t *ctx_lens_host, const float *rot_k, const float *rot_v,
+                              void *ws, size_t ws_bytes, void *stream);
+
+/* Appends one token to every sequence (Sec. 5.3 update buffer; Sec. 5.4
+ * heterogeneous double compression buffering).  k_new, v_new:
+ * [num_seqs][num_kv_heads][128].  When a sequence's buffer reaches U tokens,
+ * they are compressed with the previous finalized segment's strategy, as a
+ * provisional chunk.  When its trailing segment reaches S tokens, the
+ * segment gets its own strategy and is recompressed in place.
+ * Errors: STATE (not compressed yet), CAPACITY (a sequence is full). */
+mosaic_status mosaic_append(mosaic_cache *cache, const void *k_new, const void *v_new, void *stream);
+
+/* One decode step of PackedAttention (Sec. 5.3) for every sequence.  Steps:
+ * rotate q into each window (rotation merged into the query), score every
+ * block key (max over the GQA group's heads), keep the top ceil(rho * blocks)
+ * per (sequence, kv head) by (score desc, block index asc), attend the kept
+ * blocks' packed K/V plus the uncompressed update-buffer tokens, and rotate
+ * the output back with R_v.
+ *   q   : [num_seqs][num_kv_heads * group_size][128] (cache dtype)
+ *   out : [num_seqs][num_kv_heads * group_size][128] fp32
+ *   sm_scale: softmax scale (e.g. 1/sqrt(128)).
+ *   ws  : at least mosaic_workspace_bytes(MOSAIC_OP_DECODE) bytes.
+ * A sequence with no tokens gets a zero output.
+ * Errors: STATE, INVALID (NULL, small workspace). */
+mosaic_status mosaic_decode_attention(mosaic_cache *cache, const void *q, float *out, float sm_scale,
+                                      void *ws, size_t ws_bytes, void *stream);
+
+/* Uncompressed baseline: dense split-K decode attention over K/V laid out as
+ * for mosaic_compress (the "Full" baseline of Sec. 6.1).
+ *   ctx_lens: DEVICE int32 [num_seqs].  ws: mosaic_dense_workspace_bytes. */
+mosaic_status mosaic_dense_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t group_size,
+                                           int32_t max_ctx, size_t *bytes);
+mosaic_status mosaic_dense_decode_attention(const void *q, const void *k, const void *v, float *out,
+                                            int32_t num_seqs, int32_t num_kv_heads, int32_t group_size,
+                                            int32_t head_dim, int32_t dtype, int64_t seq_stride,
+                                            int32_t max_ctx, const int32_t *ctx_lens, float sm_scale,
+                                            void *ws, size_t ws_bytes, void *stream);
+
+/* Memory accounting of Sec. 6.3 (reads the device state: synchronizes the
+ * given stream).  used_bytes counts packed tokens, block keys, descriptors
+ * and live buffer tokens; rotation matrices are reported apart. */
+typedef struct {
+    int64_t tokens;            /* sum of sequence lengths */
+    int64_t dense_bytes;       /* 2 * tokens * 128 * 2 * num_kv_heads */
+    int64_t used_bytes;
+    int64_t rotation_bytes;    /* R_k and R_v of the windows in use, fp32 */
+    int64_t segments;          /* finalized segments */
+    int64_t strategy_hist[3][3][3]; /* finalized segments by (r, g, B) candidate index */
+} mosaic_stats;
+mosaic_status mosaic_cache_stats(const mosaic_cache *cache, mosaic_stats *out, void *stream);
+
+/* Host view of a sequence's length (no device access). */
+int32_t mosaic_seq_tokens(const mosaic_cache *cache, int32_t seq);
+
+/* Message of the last error on this thread ("" if none). */
+const char *mosaic_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOSAIC_H */

@@ -1,0 +1,218 @@
+"""MI355X (gfx950) MosaicKV hot path: compressed KV cache + decode attention.
+
+Thin Python layer over libmosaic (include/mosaic.h).  PyTorch provides device
+memory and the current HIP stream; every step of the method runs in the HIP
+kernels.  There is no CPU or PyTorch fallback: if the library is not built,
+using the cache raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from dataclasses import dataclass
+
+from ._lib import (OP_APPEND, OP_COMPRESS, OP_DECODE, MosaicError, MosaicLayout, MosaicParams, MosaicStats,
+                   MosaicWsLayout, check, load)
+
+__all__ = ["Params", "MosaicCache", "dense_decode", "MosaicError", "load"]
+
+D = 128
+
+
+@dataclass
+class Params:
+    """Method parameters (the strategy set of Sec. 4.3, candidates of Sec. 5.5,
+    defaults of Sec. 6.1)."""
+    num_kv_heads: int = 8
+    group_size: int = 4
+    dtype: str = "fp16"
+    rot_window: int = 65536
+    keep_cand: tuple = (16, 32, 48)
+    group_cand: tuple = (4, 2, 1)
+    block_cand: tuple = (16, 8, 4)
+    default: tuple = (32, 1, 8)
+    tau_channel: float = 0.30
+    tau_block: float = 0.90
+    select: tuple = (1, 10)
+    force_default: bool = False
+
+    def to_c(self) -> MosaicParams:
+        p = MosaicParams()
+        load().mosaic_params_default(C.byref(p))
+        p.num_kv_heads, p.group_size = self.num_kv_heads, self.group_size
+        p.dtype = 1 if self.dtype == "bf16" else 0
+        p.rot_window = self.rot_window
+        for i in range(3):
+            p.keep_cand[i], p.group_cand[i], p.block_cand[i] = self.keep_cand[i], self.group_cand[i], self.block_cand[i]
+        p.default_keep, p.default_group, p.default_block = self.default
+        p.tau_channel, p.tau_block = self.tau_channel, self.tau_block
+        p.select_num, p.select_den = self.select
+        p.force_default_strategy = 1 if self.force_default else 0
+        return p
+
+
+def _stream(device=None):
+    import torch
+    return C.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _ptr(t):
+    return C.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _check_tensor(t, name, dtype, device):
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a GPU")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, cache on {device}")
+
+
+class MosaicCache:
+    """One layer's compressed KV cache for `num_seqs` sequences."""
+
+    def __init__(self, params: Params, num_seqs: int, max_tokens: int, rotated: bool = True, device="cuda"):
+        import torch
+        self.lib = load()
+        self.params = params
+        self.num_seqs, self.max_tokens, self.rotated = num_seqs, max_tokens, bool(rotated)
+        self.device = torch.device(device)
+        if self.device.index is None:
+            self.device = torch.device("cuda", torch.cuda.current_device())
+        self.elem = torch.bfloat16 if params.dtype == "bf16" else torch.float16
+        self._p = params.to_c()
+        h = C.c_void_p()
+        check(self.lib.mosaic_cache_create(C.byref(self._p), num_seqs, max_tokens, int(self.rotated), C.byref(h)))
+        self._h = h
+        n = C.c_size_t()
+        check(self.lib.mosaic_cache_arena_bytes(self._h, C.byref(n)))
+        self.arena = torch.empty(n.value, dtype=torch.uint8, device=self.device)
+        check(self.lib.mosaic_cache_bind(self._h, _ptr(self.arena), n.value))
+        check(self.lib.mosaic_workspace_bytes(self._h, OP_DECODE, C.byref(n)))
+        self.workspace = torch.empty(max(n.value, 256), dtype=torch.uint8, device=self.device)
+        self.layout = MosaicLayout()
+        check(self.lib.mosaic_cache_layout(self._h, C.byref(self.layout)))
+        self.ws_layout = MosaicWsLayout()
+        check(self.lib.mosaic_decode_ws_layout(self._h, C.byref(self.ws_layout)))
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            try:
+                self.lib.mosaic_cache_destroy(h)
+            except Exception:
+                pass
+            self._h = None
+
+    @property
+    def num_pairs(self):
+        return self.num_seqs * self.params.num_kv_heads
+
+    def seq_tokens(self, s):
+        return int(self.lib.mosaic_seq_tokens(self._h, s))
+
+    def compress(self, k, v, ctx_lens, rot_k=None, rot_v=None):
+        """k, v: [num_seqs][Hkv][seq_stride][128] (cache dtype); ctx_lens: host ints;
+        rot_k/rot_v: [num_seqs][Hkv][num_windows][128][128] fp32 or None."""
+        import torch
+        _check_tensor(k, "k", self.elem, self.device)
+        _check_tensor(v, "v", self.elem, self.device)
+        if k.shape != v.shape or k.dim() != 4 or k.shape[0] != self.num_seqs or k.shape[1] != self.params.num_kv_heads \
+                or k.shape[3] != D:
+            raise ValueError(f"k/v shape {tuple(k.shape)} does not match the cache")
+        if rot_k is not None:
+            _check_tensor(rot_k, "rot_k", torch.float32, self.device)
+            _check_tensor(rot_v, "rot_v", torch.float32, self.device)
+            want = (self.num_seqs, self.params.num_kv_heads, self.layout.num_windows, D, D)
+            if tuple(rot_k.shape) != want or tuple(rot_v.shape) != want:
+                raise ValueError(f"rotation shape {tuple(rot_k.shape)} != {want}")
+        lens = (C.c_int32 * self.num_seqs)(*[int(x) for x in ctx_lens])
+        with torch.cuda.device(self.device):
+            check(self.lib.mosaic_compress(self._h, _ptr(k), _ptr(v), k.shape[2], lens, _ptr(rot_k), _ptr(rot_v),
+                                           None, 0, _stream(self.device)))
+        self._keep = (k, v, rot_k, rot_v)      # alive until the enqueued work completes
+
+    def append(self, k_new, v_new):
+        """k_new, v_new: [num_seqs][Hkv][128]."""
+        _check_tensor(k_new, "k_new", self.elem, self.device)
+        _check_tensor(v_new, "v_new", self.elem, self.device)
+        if tuple(k_new.shape) != (self.num_seqs, self.params.num_kv_heads, D) or k_new.shape != v_new.shape:
+            raise ValueError(f"k_new shape {tuple(k_new.shape)}")
+        import torch
+        with torch.cuda.device(self.device):
+            check(self.lib.mosaic_append(self._h, _ptr(k_new), _ptr(v_new), _stream(self.device)))
+        self._keep_app = (k_new, v_new)
+
+    def decode(self, q, sm_scale: float, out=None):
+        """q: [num_seqs][Hkv * G][128] -> fp32 [num_seqs][Hq][128]."""
+        import torch
+        _check_tensor(q, "q", self.elem, self.device)
+        hq = self.params.num_kv_heads * self.params.group_size
+        if tuple(q.shape) != (self.num_seqs, hq, D):
+            raise ValueError(f"q shape {tuple(q.shape)} != {(self.num_seqs, hq, D)}")
+        if out is None:
+            out = torch.empty((self.num_seqs, hq, D), dtype=torch.float32, device=self.device)
+        _check_tensor(out, "out", torch.float32, self.device)
+        with torch.cuda.device(self.device):
+            check(self.lib.mosaic_decode_attention(self._h, _ptr(q), _ptr(out), float(sm_scale), _ptr(self.workspace),
+                                                   self.workspace.numel(), _stream(self.device)))
+        return out
+
+    def stats(self) -> dict:
+        st = MosaicStats()
+        import torch
+        with torch.cuda.device(self.device):
+            check(self.lib.mosaic_cache_stats(self._h, C.byref(st), _stream(self.device)))
+        hist = {}
+        p = self.params
+        for ri in range(3):
+            for gi in range(3):
+                for bi in range(3):
+                    n = st.strategy_hist[ri * 9 + gi * 3 + bi]
+                    if n:
+                        hist[(p.keep_cand[ri], p.group_cand[gi], p.block_cand[bi])] = n
+        return dict(tokens=st.tokens, dense_bytes=st.dense_bytes, used_bytes=st.used_bytes,
+                    rotation_bytes=st.rotation_bytes, segments=st.segments, strategies=hist,
+                    ratio=(st.dense_bytes / st.used_bytes) if st.used_bytes else float("nan"))
+
+    # ---- inspection (tests): raw bytes of a pair's regions -------------------
+    def region(self, name: str, pair: int, nbytes: int | None = None):
+        off = getattr(self.layout, name + "_off")
+        stride = getattr(self.layout, name + "_stride")
+        n = stride if nbytes is None else nbytes
+        return self.arena[off + pair * stride: off + pair * stride + n]
+
+    def ws_region(self, name: str, pair: int, nbytes: int | None = None):
+        off = getattr(self.ws_layout, name + "_off")
+        stride = getattr(self.ws_layout, name + "_stride")
+        n = stride if nbytes is None else nbytes
+        return self.workspace[off + pair * stride: off + pair * stride + n]
+
+
+def dense_decode(q, k, v, ctx_lens_dev, sm_scale: float, max_ctx: int, group_size: int, out=None, ws=None):
+    """Uncompressed split-K decode attention (baseline).  q [S][Hq][128];
+    k, v [S][Hkv][seq_stride][128]; ctx_lens_dev int32 [S] on the GPU."""
+    import torch
+    lib = load()
+    S, Hkv, stride, _ = k.shape
+    _check_tensor(k, "k", None, None)
+    _check_tensor(v, "v", k.dtype, k.device)
+    _check_tensor(q, "q", k.dtype, k.device)
+    _check_tensor(ctx_lens_dev, "ctx_lens", torch.int32, k.device)
+    n = C.c_size_t()
+    check(lib.mosaic_dense_workspace_bytes(S, Hkv, group_size, max_ctx, C.byref(n)))
+    if ws is None or ws.numel() < n.value:
+        ws = torch.empty(max(n.value, 256), dtype=torch.uint8, device=k.device)
+    if out is None:
+        out = torch.empty((S, Hkv * group_size, D), dtype=torch.float32, device=k.device)
+    dt = 1 if k.dtype == torch.bfloat16 else 0
+    with torch.cuda.device(k.device):
+        check(lib.mosaic_dense_decode_attention(_ptr(q), _ptr(k), _ptr(v), _ptr(out), S, Hkv, group_size, D, dt, stride,
+                                                max_ctx, _ptr(ctx_lens_dev), float(sm_scale), _ptr(ws), ws.numel(),
+                                                _stream(k.device)))
+    return out

@@ -1,0 +1,406 @@
+// api.hip -- C ABI of libmosaic (see include/mosaic.h): argument validation,
+// host-side bookkeeping of sequence lengths (the paper's CPU-side management
+// of Sec. 5.4, reduced to deciding which kernels run), arena and workspace
+// layout, and kernel launches.  No C++ exception crosses the ABI.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/mosaic.h"
+#include "mosaic_internal.h"
+
+using namespace mosaic;
+
+namespace {
+
+thread_local std::string g_err;
+
+mosaic_status fail(mosaic_status st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return st;
+}
+
+mosaic_status ok() {
+    g_err.clear();
+    return MOSAIC_OK;
+}
+
+mosaic_status hip_fail(hipError_t e, const char *what) {
+    return fail(MOSAIC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
+int ilog2(int v) { int l = 0; while ((1 << l) < v) ++l; return l; }
+
+}  // namespace
+
+struct mosaic_cache {
+    mosaic_params P;
+    int num_seqs, max_tokens, rotated, npairs, GP, nw, max_desc, max_blocks, max_sel, max_splits;
+    int maxrec, minb;
+    mosaic_layout lay;
+    mosaic_ws_layout wsl;
+    uint64_t ctx_off;            // device int32 [num_seqs] (inside the arena)
+    uint8_t *arena;
+    bool compressed;
+    std::vector<int32_t> L;      // host mirror of each sequence's length
+    Geom geom() const {
+        Geom g{};
+        g.npairs = npairs; g.hkv = P.num_kv_heads; g.G = P.group_size; g.GP = GP; g.dtype = P.dtype;
+        g.W = P.rot_window; g.nw = nw; g.cap = max_tokens; g.max_desc = max_desc; g.rotated = rotated;
+        g.meta = arena + lay.meta_off; g.desc = arena + lay.desc_off; g.sc = arena + lay.score_off;
+        g.tok = arena + lay.token_off; g.buf = (uint16_t *)(arena + lay.buf_off);
+        g.stg = (uint16_t *)(arena + lay.stage_off); g.rot = (float *)(arena + lay.rot_off);
+        g.meta_stride = lay.meta_stride; g.desc_stride = lay.desc_stride; g.sc_stride = lay.score_stride;
+        g.tok_stride = lay.token_stride; g.buf_stride = lay.buf_stride; g.stg_stride = lay.stage_stride;
+        g.rot_stride = lay.rot_stride;
+        for (int i = 0; i < 3; ++i) {
+            g.keep_cand[i] = P.keep_cand[i]; g.group_cand[i] = P.group_cand[i]; g.block_cand[i] = P.block_cand[i];
+        }
+        g.def_keep = P.default_keep; g.def_group = P.default_group; g.def_block = P.default_block;
+        g.tau_ch = P.tau_channel; g.tau_blk = P.tau_block;
+        g.sel_num = P.select_num; g.sel_den = P.select_den; g.force = P.force_default_strategy;
+        return g;
+    }
+    WsGeom wsgeom(void *ws) const {
+        uint8_t *b = (uint8_t *)ws;
+        WsGeom w{};
+        w.qrot = (float *)(b + wsl.qrot_off); w.qrot_stride = wsl.qrot_stride;
+        w.score = (float *)(b + wsl.score_off); w.score_stride = wsl.score_stride;
+        w.sel = (int32_t *)(b + wsl.sel_off); w.sel_stride = wsl.sel_stride;
+        w.wsel = (int32_t *)(b + wsl.wsel_off); w.wsel_stride = wsl.wsel_stride;
+        w.part = (float *)(b + wsl.part_off); w.part_stride = wsl.part_stride;
+        w.tag = (int32_t *)(b + wsl.tag_off); w.tag_stride = wsl.tag_stride;
+        w.max_blocks = max_blocks; w.max_splits = max_splits;
+        return w;
+    }
+};
+
+extern "C" {
+
+void mosaic_params_default(mosaic_params *p) {
+    if (!p) return;
+    std::memset(p, 0, sizeof(*p));
+    p->head_dim = 128; p->num_kv_heads = 8; p->group_size = 4; p->dtype = MOSAIC_FP16;
+    p->seg_len = 64; p->rot_window = 65536; p->update_buf = 32;
+    p->keep_cand[0] = 16; p->keep_cand[1] = 32; p->keep_cand[2] = 48;
+    p->group_cand[0] = 4; p->group_cand[1] = 2; p->group_cand[2] = 1;
+    p->block_cand[0] = 16; p->block_cand[1] = 8; p->block_cand[2] = 4;
+    p->default_keep = 32; p->default_group = 1; p->default_block = 8;
+    p->tau_channel = 0.30f; p->tau_block = 0.90f;
+    p->select_num = 1; p->select_den = 10;
+    p->force_default_strategy = 0;
+}
+
+static mosaic_status check_params(const mosaic_params *p) {
+    if (p->head_dim != 128) return fail(MOSAIC_ERR_UNSUPPORTED, "head_dim %d: only 128 is supported", p->head_dim);
+    if (p->seg_len != SEG) return fail(MOSAIC_ERR_UNSUPPORTED, "seg_len %d: only 64 is supported", p->seg_len);
+    if (p->update_buf != UBUF) return fail(MOSAIC_ERR_UNSUPPORTED, "update_buf %d: only 32 is supported", p->update_buf);
+    if (p->num_kv_heads < 1) return fail(MOSAIC_ERR_INVALID, "num_kv_heads %d < 1", p->num_kv_heads);
+    if (p->group_size < 1 || p->group_size > 8) return fail(MOSAIC_ERR_INVALID, "group_size %d not in 1..8", p->group_size);
+    if (p->dtype != MOSAIC_FP16 && p->dtype != MOSAIC_BF16) return fail(MOSAIC_ERR_INVALID, "dtype %d", p->dtype);
+    if (p->rot_window < SEG || p->rot_window % SEG) return fail(MOSAIC_ERR_INVALID, "rot_window %d: multiple of 64 required", p->rot_window);
+    auto okg = [](int g) { return g == 1 || g == 2 || g == 4; };
+    auto okb = [](int b) { return b == 4 || b == 8 || b == 16; };
+    auto okr = [](int r, int g) { return r >= 2 && r <= 128 && r % g == 0 && r % 2 == 0; };
+    for (int i = 0; i < 3; ++i) {
+        if (!okg(p->group_cand[i])) return fail(MOSAIC_ERR_INVALID, "group_cand[%d] = %d not in {1,2,4}", i, p->group_cand[i]);
+        if (!okb(p->block_cand[i])) return fail(MOSAIC_ERR_INVALID, "block_cand[%d] = %d not in {4,8,16}", i, p->block_cand[i]);
+    }
+    for (int i = 0; i < 3; ++i)
+        for (int j = 0; j < 3; ++j)
+            if (!okr(p->keep_cand[i], p->group_cand[j]))
+                return fail(MOSAIC_ERR_INVALID, "keep_cand[%d] = %d: even, 2..128 and a multiple of every group size",
+                            i, p->keep_cand[i]);
+    if (!okg(p->default_group) || !okb(p->default_block) || !okr(p->default_keep, p->default_group))
+        return fail(MOSAIC_ERR_INVALID, "default strategy (%d, %d, %d) invalid", p->default_keep, p->default_group,
+                    p->default_block);
+    if (std::isnan(p->tau_channel) || std::isnan(p->tau_block) || p->tau_channel < 0 || p->tau_block < 0)
+        return fail(MOSAIC_ERR_INVALID, "thresholds must be >= 0");
+    if (p->select_num < 1 || p->select_den < 1) return fail(MOSAIC_ERR_INVALID, "select ratio %d/%d", p->select_num, p->select_den);
+    return MOSAIC_OK;
+}
+
+mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
+                                  int32_t rotated, mosaic_cache **out) {
+    if (!params || !out) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    mosaic_status st = check_params(params);
+    if (st != MOSAIC_OK) return st;
+    if (num_seqs < 1 || max_tokens < 1) return fail(MOSAIC_ERR_INVALID, "num_seqs %d, max_tokens %d", num_seqs, max_tokens);
+    mosaic_cache *c = new (std::nothrow) mosaic_cache();
+    if (!c) return fail(MOSAIC_ERR_INVALID, "out of host memory");
+    c->P = *params;
+    c->num_seqs = num_seqs; c->max_tokens = max_tokens; c->rotated = rotated ? 1 : 0;
+    c->npairs = num_seqs * params->num_kv_heads;
+    c->GP = params->group_size <= 4 ? 4 : 8;
+    c->nw = (max_tokens + params->rot_window - 1) / params->rot_window;
+    c->max_desc = max_tokens / SEG + 2;
+    int maxrec = 0, minb = params->default_block;
+    for (int i = 0; i < 3; ++i)
+        for (int j = 0; j < 3; ++j)
+            maxrec = std::max(maxrec, 2 * params->keep_cand[i] + 16 / params->group_cand[j]);
+    maxrec = std::max(maxrec, 2 * params->default_keep + 16 / params->default_group);
+    for (int i = 0; i < 3; ++i) minb = std::min(minb, params->block_cand[i]);
+    c->maxrec = maxrec; c->minb = minb;
+    const uint64_t tok_bytes = (uint64_t)c->max_desc * SEG * 2 * maxrec + 64;
+    const uint64_t sc_bytes = (uint64_t)c->max_desc * (SEG / minb) * maxrec + 64;
+    if (tok_bytes >= (1ull << 32)) {
+        delete c;
+        return fail(MOSAIC_ERR_CAPACITY, "max_tokens %d: a pair's token arena would exceed 4 GiB", max_tokens);
+    }
+    c->max_blocks = c->max_desc * (SEG / minb);
+    c->max_sel = (int)std::min<int64_t>(c->max_blocks, ((int64_t)c->max_blocks * params->select_num +
+                                                        params->select_den - 1) / params->select_den);
+    c->max_splits = (c->max_sel + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS + c->nw + 1;
+    // arena layout
+    mosaic_layout &l = c->lay;
+    std::memset(&l, 0, sizeof(l));
+    uint64_t off = 0;
+    auto region = [&](uint64_t &o, uint64_t &stride, uint64_t per_pair) {
+        stride = align256(per_pair);
+        o = off;
+        off = align256(off + stride * (uint64_t)c->npairs);
+    };
+    region(l.meta_off, l.meta_stride, sizeof(PairMeta));
+    region(l.desc_off, l.desc_stride, (uint64_t)c->max_desc * sizeof(Desc));
+    region(l.score_off, l.score_stride, sc_bytes);
+    region(l.token_off, l.token_stride, tok_bytes);
+    region(l.buf_off, l.buf_stride, 2ull * UBUF * D * 2);
+    region(l.stage_off, l.stage_stride, 2ull * SEG * D * 2);
+    region(l.rot_off, l.rot_stride, c->rotated ? (uint64_t)c->nw * 3 * D * D * 4 : 0);
+    c->ctx_off = off;
+    off = align256(off + (uint64_t)num_seqs * 4);
+    l.total = off;
+    l.num_pairs = c->npairs; l.max_desc = c->max_desc; l.num_windows = c->nw;
+    // decode workspace layout
+    mosaic_ws_layout &w = c->wsl;
+    std::memset(&w, 0, sizeof(w));
+    off = 0;
+    auto wregion = [&](uint64_t &o, uint64_t &stride, uint64_t per_pair) {
+        stride = align256(per_pair);
+        o = off;
+        off = align256(off + stride * (uint64_t)c->npairs);
+    };
+    wregion(w.qrot_off, w.qrot_stride, (uint64_t)c->nw * D * c->GP * 4);
+    wregion(w.score_off, w.score_stride, (uint64_t)c->max_blocks * 4);
+    wregion(w.sel_off, w.sel_stride, (uint64_t)c->max_blocks * 4);
+    wregion(w.wsel_off, w.wsel_stride, (uint64_t)(c->nw + 2) * 4);
+    wregion(w.part_off, w.part_stride, (uint64_t)c->max_splits * c->GP * (D + 2) * 4);
+    wregion(w.tag_off, w.tag_stride, (uint64_t)c->max_splits * 4);
+    w.total = off;
+    w.max_blocks = c->max_blocks; w.max_splits = c->max_splits; w.gp = c->GP;
+    c->arena = nullptr;
+    c->compressed = false;
+    c->L.assign(num_seqs, 0);
+    *out = c;
+    return ok();
+}
+
+mosaic_status mosaic_cache_arena_bytes(const mosaic_cache *c, size_t *bytes) {
+    if (!c || !bytes) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    *bytes = c->lay.total;
+    return ok();
+}
+
+mosaic_status mosaic_cache_bind(mosaic_cache *c, void *arena, size_t bytes) {
+    if (!c || !arena) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    if ((uintptr_t)arena % 256) return fail(MOSAIC_ERR_INVALID, "arena not 256-byte aligned");
+    if (bytes < c->lay.total) return fail(MOSAIC_ERR_INVALID, "arena %zu bytes < %llu required", bytes,
+                                          (unsigned long long)c->lay.total);
+    c->arena = (uint8_t *)arena;
+    c->compressed = false;
+    return ok();
+}
+
+mosaic_status mosaic_cache_destroy(mosaic_cache *c) {
+    delete c;
+    return ok();
+}
+
+mosaic_status mosaic_cache_layout(const mosaic_cache *c, mosaic_layout *out) {
+    if (!c || !out) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    *out = c->lay;
+    return ok();
+}
+
+mosaic_status mosaic_decode_ws_layout(const mosaic_cache *c, mosaic_ws_layout *out) {
+    if (!c || !out) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    *out = c->wsl;
+    return ok();
+}
+
+mosaic_status mosaic_workspace_bytes(const mosaic_cache *c, int32_t op, size_t *bytes) {
+    if (!c || !bytes) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    if (op == MOSAIC_OP_COMPRESS || op == MOSAIC_OP_APPEND) *bytes = 0;
+    else if (op == MOSAIC_OP_DECODE) *bytes = c->wsl.total;
+    else return fail(MOSAIC_ERR_INVALID, "unknown op %d", op);
+    return ok();
+}
+
+int32_t mosaic_seq_tokens(const mosaic_cache *c, int32_t seq) {
+    if (!c || seq < 0 || seq >= c->num_seqs) return -1;
+    return c->L[seq];
+}
+
+mosaic_status mosaic_compress(mosaic_cache *c, const void *k, const void *v, int64_t seq_stride,
+                              const int32_t *ctx_lens_host, const float *rot_k, const float *rot_v, void *ws,
+                              size_t ws_bytes, void *stream) {
+    (void)ws; (void)ws_bytes;
+    if (!c) return fail(MOSAIC_ERR_INVALID, "NULL cache");
+    if (!c->arena) return fail(MOSAIC_ERR_STATE, "cache not bound to an arena");
+    if (!k || !v || !ctx_lens_host) return fail(MOSAIC_ERR_INVALID, "NULL k, v or ctx_lens_host");
+    if (((uintptr_t)k | (uintptr_t)v) % 16) return fail(MOSAIC_ERR_INVALID, "k/v must be 16-byte aligned");
+    if (c->rotated && (!rot_k || !rot_v)) return fail(MOSAIC_ERR_INVALID, "cache is rotated: rot_k and rot_v required");
+    if (!c->rotated && (rot_k || rot_v)) return fail(MOSAIC_ERR_INVALID, "cache created without rotation");
+    if (c->rotated && (((uintptr_t)rot_k | (uintptr_t)rot_v) % 16)) return fail(MOSAIC_ERR_INVALID, "rot must be 16-byte aligned");
+    int maxL = 0, any_tail = 0;
+    for (int s = 0; s < c->num_seqs; ++s) {
+        const int L = ctx_lens_host[s];
+        if (L < 0) return fail(MOSAIC_ERR_INVALID, "ctx_lens[%d] = %d < 0", s, L);
+        if (L > c->max_tokens) return fail(MOSAIC_ERR_CAPACITY, "ctx_lens[%d] = %d > max_tokens %d", s, L, c->max_tokens);
+        maxL = std::max(maxL, L);
+        any_tail |= (L % SEG) != 0;
+    }
+    if (seq_stride < maxL || seq_stride < 1) return fail(MOSAIC_ERR_INVALID, "seq_stride %lld < longest context %d",
+                                                         (long long)seq_stride, maxL);
+    hipStream_t s = (hipStream_t)stream;
+    const Geom g = c->geom();
+    int32_t *ctx_dev = (int32_t *)(c->arena + c->ctx_off);
+    hipError_t e = hipMemcpyAsync(ctx_dev, ctx_lens_host, sizeof(int32_t) * c->num_seqs, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "copy of context lengths");
+    if (c->rotated && (e = launch_copy_rot(g, rot_k, rot_v, s)) != hipSuccess) return hip_fail(e, "rotation copy");
+    e = launch_compress(g, (const uint16_t *)k, (const uint16_t *)v, seq_stride, ctx_dev, maxL / SEG, any_tail, s);
+    if (e != hipSuccess) return hip_fail(e, "compress launch");
+    for (int q = 0; q < c->num_seqs; ++q) c->L[q] = ctx_lens_host[q];
+    c->compressed = true;
+    return ok();
+}
+
+mosaic_status mosaic_append(mosaic_cache *c, const void *k_new, const void *v_new, void *stream) {
+    if (!c) return fail(MOSAIC_ERR_INVALID, "NULL cache");
+    if (!c->arena || !c->compressed) return fail(MOSAIC_ERR_STATE, "append before compress");
+    if (!k_new || !v_new) return fail(MOSAIC_ERR_INVALID, "NULL k_new or v_new");
+    if (((uintptr_t)k_new | (uintptr_t)v_new) % 4) return fail(MOSAIC_ERR_INVALID, "k_new/v_new must be 4-byte aligned");
+    bool due = false;
+    for (int q = 0; q < c->num_seqs; ++q) {
+        if (c->L[q] + 1 > c->max_tokens) return fail(MOSAIC_ERR_CAPACITY, "sequence %d is full (%d tokens)", q, c->L[q]);
+        due |= ((c->L[q] + 1) % UBUF) == 0;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    const Geom g = c->geom();
+    hipError_t e = launch_append(g, (const uint16_t *)k_new, (const uint16_t *)v_new, s);
+    if (e != hipSuccess) return hip_fail(e, "append launch");
+    if (due && (e = launch_maintain(g, MAINT_APPEND, s)) != hipSuccess) return hip_fail(e, "flush/finalize launch");
+    for (int q = 0; q < c->num_seqs; ++q) c->L[q] += 1;
+    return ok();
+}
+
+mosaic_status mosaic_decode_attention(mosaic_cache *c, const void *q, float *out, float sm_scale, void *ws,
+                                      size_t ws_bytes, void *stream) {
+    if (!c) return fail(MOSAIC_ERR_INVALID, "NULL cache");
+    if (!c->arena || !c->compressed) return fail(MOSAIC_ERR_STATE, "decode before compress");
+    if (!q || !out || !ws) return fail(MOSAIC_ERR_INVALID, "NULL q, out or workspace");
+    if (ws_bytes < c->wsl.total) return fail(MOSAIC_ERR_INVALID, "workspace %zu bytes < %llu required", ws_bytes,
+                                             (unsigned long long)c->wsl.total);
+    if ((uintptr_t)ws % 256) return fail(MOSAIC_ERR_INVALID, "workspace not 256-byte aligned");
+    if (((uintptr_t)q % 4) || ((uintptr_t)out % 4)) return fail(MOSAIC_ERR_INVALID, "q/out misaligned");
+    if (!std::isfinite(sm_scale)) return fail(MOSAIC_ERR_INVALID, "sm_scale not finite");
+    int max_desc = 0, maxL = 0;
+    for (int q2 = 0; q2 < c->num_seqs; ++q2) {
+        const int L = c->L[q2];
+        max_desc = std::max(max_desc, L / SEG + ((L % SEG) >= UBUF ? 1 : 0));
+        maxL = std::max(maxL, L);
+    }
+    const int nwu = std::max(1, std::min(c->nw, (maxL + c->P.rot_window - 1) / c->P.rot_window));
+    hipError_t e = launch_decode(c->geom(), c->wsgeom(ws), (const uint16_t *)q, out, sm_scale, max_desc, nwu,
+                                 (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "decode launch");
+    return ok();
+}
+
+mosaic_status mosaic_dense_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t group_size,
+                                           int32_t max_ctx, size_t *bytes) {
+    if (!bytes) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    if (num_seqs < 1 || num_kv_heads < 1 || group_size < 1 || group_size > 8 || max_ctx < 0)
+        return fail(MOSAIC_ERR_INVALID, "bad shape");
+    *bytes = dense_part_bytes(num_seqs * num_kv_heads, group_size, max_ctx);
+    return ok();
+}
+
+mosaic_status mosaic_dense_decode_attention(const void *q, const void *k, const void *v, float *out, int32_t num_seqs,
+                                            int32_t num_kv_heads, int32_t group_size, int32_t head_dim, int32_t dtype,
+                                            int64_t seq_stride, int32_t max_ctx, const int32_t *ctx_lens,
+                                            float sm_scale, void *ws, size_t ws_bytes, void *stream) {
+    if (!q || !k || !v || !out || !ctx_lens || !ws) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    if (head_dim != 128) return fail(MOSAIC_ERR_UNSUPPORTED, "head_dim %d", head_dim);
+    if (dtype != MOSAIC_FP16 && dtype != MOSAIC_BF16) return fail(MOSAIC_ERR_INVALID, "dtype %d", dtype);
+    if (num_seqs < 1 || num_kv_heads < 1 || group_size < 1 || group_size > 8) return fail(MOSAIC_ERR_INVALID, "bad shape");
+    if (max_ctx < 0 || seq_stride < max_ctx) return fail(MOSAIC_ERR_INVALID, "seq_stride %lld < max_ctx %d",
+                                                         (long long)seq_stride, max_ctx);
+    if (((uintptr_t)k | (uintptr_t)v) % 16) return fail(MOSAIC_ERR_INVALID, "k/v must be 16-byte aligned");
+    const size_t need = dense_part_bytes(num_seqs * num_kv_heads, group_size, max_ctx);
+    if (ws_bytes < need) return fail(MOSAIC_ERR_INVALID, "workspace %zu < %zu", ws_bytes, need);
+    hipError_t e = launch_dense((const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, out, num_seqs,
+                                num_kv_heads, group_size, dtype, seq_stride, max_ctx, ctx_lens, sm_scale, (float *)ws, 0,
+                                (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "dense launch");
+    return ok();
+}
+
+mosaic_status mosaic_cache_stats(const mosaic_cache *c, mosaic_stats *out, void *stream) {
+    if (!c || !out) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    if (!c->arena || !c->compressed) return fail(MOSAIC_ERR_STATE, "stats before compress");
+    hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+    std::memset(out, 0, sizeof(*out));
+    std::vector<PairMeta> meta(c->npairs);
+    std::vector<Desc> desc((size_t)c->max_desc);
+    for (int p = 0; p < c->npairs; ++p) {
+        e = hipMemcpy(&meta[p], c->arena + c->lay.meta_off + (uint64_t)p * c->lay.meta_stride, sizeof(PairMeta),
+                      hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(e, "meta copy");
+    }
+    const int hkv = c->P.num_kv_heads;
+    for (int p = 0; p < c->npairs; ++p) {
+        const int L = meta[p].L, nf = L / SEG, rem = L % SEG, prov = rem >= UBUF, nbuf = rem - (prov ? UBUF : 0);
+        const int nd = nf + prov;
+        if (nd > 0) {
+            e = hipMemcpy(desc.data(), c->arena + c->lay.desc_off + (uint64_t)p * c->lay.desc_stride,
+                          sizeof(Desc) * nd, hipMemcpyDeviceToHost);
+            if (e != hipSuccess) return hip_fail(e, "descriptor copy");
+        }
+        int64_t used = (int64_t)meta[p].tok_tail + meta[p].sc_tail + 16ll * nd + (int64_t)nbuf * 2 * D * 2;
+        if (prov) {
+            const Desc &d = desc[nf];
+            const int rec = 2 * d.r + (16 >> d.log2g);
+            used += (int64_t)UBUF * 2 * rec + (int64_t)(UBUF >> d.log2b) * rec;
+        }
+        out->used_bytes += used;
+        out->tokens += (p % hkv == 0) ? L : 0;
+        out->segments += nf;
+        for (int s = 0; s < nf; ++s) {
+            int ri = -1, gi = -1, bi = -1;
+            for (int i = 0; i < 3; ++i) {
+                if (c->P.keep_cand[i] == desc[s].r && ri < 0) ri = i;
+                if (c->P.group_cand[i] == (1 << desc[s].log2g) && gi < 0) gi = i;
+                if (c->P.block_cand[i] == (1 << desc[s].log2b) && bi < 0) bi = i;
+            }
+            if (ri >= 0 && gi >= 0 && bi >= 0) out->strategy_hist[ri][gi][bi]++;
+        }
+        if (c->rotated) out->rotation_bytes += (int64_t)((L + c->P.rot_window - 1) / c->P.rot_window) * 2 * D * D * 4;
+    }
+    out->dense_bytes = out->tokens * 2 * D * 2 * hkv;
+    return ok();
+}
+
+const char *mosaic_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

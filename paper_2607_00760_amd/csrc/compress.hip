@@ -1,0 +1,511 @@
+// compress.hip -- gfx950 kernels of the MosaicKV compression pass.
+//
+//   Stage-1 per-vector channel compression (Sec. 4.2), the packed KV format
+//   with variable-granularity bitmaps (Sec. 5.1), compressed KV encoding with
+//   mean block keys (Sec. 5.2), per-segment strategy selection (Sec. 4.3,
+//   Sec. 5.5), the update buffer (Sec. 5.3) and heterogeneous double
+//   compression buffering (Sec. 5.4).
+//
+// Work decomposition: one 256-thread workgroup per 64-token segment.  Wave w
+// owns tokens [16w, 16w+16); lane l owns channels l and l+64, so a vector's
+// 128 channels live in one wave and channel trees, ranks, bitmaps and slot
+// numbers are wave-local (butterflies, ballots, mbcnt).  The rotation is an
+// fp32 fused-multiply-add chain over ascending input channels per output
+// channel (R^T staged in LDS, x broadcast from LDS), so every rotated value,
+// kept index and packed byte is reproducible bit for bit.
+#include "mosaic_internal.h"
+
+namespace mosaic {
+
+namespace {
+
+constexpr int TPW = 16;            // tokens per wave
+constexpr int NCAND = 9;
+
+struct SegSmem {
+    float rt[D * D];               // R^T of the matrix being applied (rt[c*D + j] = R[j][c])
+    float x[SEG * D];              // the segment's input tokens, fp32
+    float tot[2][SEG];             // per-token energy (K, V)
+    float drop[2][NCAND][SEG];     // per-token dropped energy per (r, g) candidate
+    float bvar[3][SEG];            // per-token deviation from its block mean, per B candidate
+    uint64_t keys[4][D];           // per-wave group keys of the vector being ranked
+    int strat[4];                  // chosen r, log2 g, log2 B
+};
+
+__device__ __forceinline__ int ilog2i(int v) { return 31 - __clz(v); }
+
+// Stage the tokens and (optionally) R^T, then y[i][0..1] = rotated channels
+// (l, l+64) of token 16w+i.  y = x . R^T as fp32 fmaf chains over ascending c.
+__device__ __forceinline__ void rotate_tile(const uint16_t *src, int ntok, const float *rt_g, int dtype,
+                            SegSmem &sm, float (&y)[TPW][2]) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int i = tid; i < SEG * D; i += 256) {
+        int t = i / D;
+        sm.x[i] = (t < ntok) ? h2f(src[i], dtype) : 0.0f;
+    }
+    if (rt_g) {
+        const float4 *s4 = (const float4 *)rt_g;
+        float4 *d4 = (float4 *)sm.rt;
+        for (int i = tid; i < D * D / 4; i += 256) d4[i] = s4[i];
+    }
+    __syncthreads();
+    const int t0 = wave * TPW;
+    if (!rt_g) {
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) {
+            y[i][0] = sm.x[(t0 + i) * D + lane];
+            y[i][1] = sm.x[(t0 + i) * D + lane + 64];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) { y[i][0] = 0.0f; y[i][1] = 0.0f; }
+        for (int c = 0; c < D; c += 4) {
+            float rl[4], rh[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) { rl[k] = sm.rt[(c + k) * D + lane]; rh[k] = sm.rt[(c + k) * D + lane + 64]; }
+#pragma unroll
+            for (int i = 0; i < TPW; ++i) {
+                float4 xv = *(const float4 *)&sm.x[(t0 + i) * D + c];
+                float xs[4] = {xv.x, xv.y, xv.z, xv.w};
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    y[i][0] = fmaf(xs[k], rl[k], y[i][0]);
+                    y[i][1] = fmaf(xs[k], rh[k], y[i][1]);
+                }
+            }
+        }
+    }
+    __syncthreads();
+}
+
+// Group scores (L1 of magnitudes, pairwise) and exact ranks by
+// (score desc, group index asc) of the groups holding channels lane, lane+64.
+__device__ __forceinline__ void group_ranks(float ylo, float yhi, int log2g, uint64_t *keys,
+                                            int &rank_lo, int &rank_hi) {
+    const int lane = threadIdx.x & 63;
+    float slo = fabsf(ylo), shi = fabsf(yhi);
+    if (log2g >= 1) { slo = slo + shfl_xor_f(slo, 1); shi = shi + shfl_xor_f(shi, 1); }
+    if (log2g >= 2) { slo = slo + shfl_xor_f(slo, 2); shi = shi + shfl_xor_f(shi, 2); }
+    const int ng = D >> log2g;
+    const int glo = lane >> log2g, ghi = (64 >> log2g) + (lane >> log2g);
+    const uint64_t klo = ((uint64_t)__float_as_uint(slo) << 8) | (uint64_t)(255 - glo);
+    const uint64_t khi = ((uint64_t)__float_as_uint(shi) << 8) | (uint64_t)(255 - ghi);
+    if ((lane & ((1 << log2g) - 1)) == 0) { keys[glo] = klo; keys[ghi] = khi; }
+    __syncthreads();
+    int rl = 0, rh = 0;
+    for (int j = 0; j < ng; j += 2) {
+        uint64_t k0 = keys[j], k1 = keys[j + 1];
+        rl += (k0 > klo) + (k1 > klo);
+        rh += (k0 > khi) + (k1 > khi);
+    }
+    __syncthreads();
+    rank_lo = rl; rank_hi = rh;
+}
+
+// Per-token statistics of one wave's 16 tokens: energy, dropped energy of
+// every (r, g) candidate; for K also the block deviation per B candidate.
+template <int B>
+__device__ __forceinline__ void block_dev(const float (&y)[TPW][2], float *out_tok, int t0, int valid_ntok) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int b0 = 0; b0 < TPW; b0 += B) {
+        float mlo = y[b0][0], mhi = y[b0][1];
+#pragma unroll
+        for (int t = 1; t < B; ++t) { mlo = mlo + y[b0 + t][0]; mhi = mhi + y[b0 + t][1]; }
+        mlo = mlo * (1.0f / (float)B); mhi = mhi * (1.0f / (float)B);
+#pragma unroll
+        for (int t = 0; t < B; ++t) {
+            float dl = y[b0 + t][0] - mlo, dh = y[b0 + t][1] - mhi;
+            float v = tree128(dl * dl, dh * dh);
+            if (lane == 0 && t0 + b0 + t < valid_ntok) out_tok[t0 + b0 + t] = v;
+        }
+    }
+}
+
+__device__ __forceinline__ void token_stats(const Geom &g, const float (&y)[TPW][2], int which, SegSmem &sm, int ntok) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, t0 = wave * TPW;
+    uint64_t *keys = sm.keys[wave];
+    for (int i = 0; i < TPW; ++i) {
+        float ylo = 0.0f, yhi = 0.0f;          // static select (no dynamic register indexing)
+#pragma unroll
+        for (int x = 0; x < TPW; ++x)
+            if (x == i) { ylo = y[x][0]; yhi = y[x][1]; }
+        const float elo = ylo * ylo, ehi = yhi * yhi;
+        const float tot = tree128(elo, ehi);
+        if (lane == 0) sm.tot[which][t0 + i] = tot;
+        for (int gi = 0; gi < 3; ++gi) {
+            const int log2g = ilog2i(g.group_cand[gi]);
+            int rlo, rhi;
+            group_ranks(ylo, yhi, log2g, keys, rlo, rhi);
+            for (int ri = 0; ri < 3; ++ri) {
+                const int n = g.keep_cand[ri] >> log2g;
+                float d = tree128(rlo < n ? 0.0f : elo, rhi < n ? 0.0f : ehi);
+                if (lane == 0) sm.drop[which][ri * 3 + gi][t0 + i] = d;
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void block_stats(const Geom &g, const float (&y)[TPW][2], SegSmem &sm, int ntok) {
+    const int t0 = (threadIdx.x >> 6) * TPW;
+    for (int bi = 0; bi < 3; ++bi) {
+        switch (g.block_cand[bi]) {
+            case 4: block_dev<4>(y, sm.bvar[bi], t0, ntok); break;
+            case 8: block_dev<8>(y, sm.bvar[bi], t0, ntok); break;
+            default: block_dev<16>(y, sm.bvar[bi], t0, ntok); break;
+        }
+    }
+}
+
+// tree over the 64 per-token values (wave 0; adjacent pairwise tree)
+__device__ __forceinline__ float tree64_lds(const float *v) {
+    float x = v[threadIdx.x & 63];
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) x = x + shfl_xor_f(x, m);
+    return x;
+}
+
+// Strategy choice (Sec. 5.5): first (r, g) in candidate order whose dropped
+// energy is below tau_ch * energy for K and for V; first B whose block
+// deviation is below tau_blk * K energy; fallbacks are the last candidates.
+__device__ __forceinline__ void choose_strategy(const Geom &g, SegSmem &sm) {
+    if (threadIdx.x < 64) {
+        const float TK = tree64_lds(sm.tot[0]), TV = tree64_lds(sm.tot[1]);
+        int chosen = NCAND - 1;
+        for (int ci = 0; ci < NCAND; ++ci) {
+            const float DK = tree64_lds(sm.drop[0][ci]), DV = tree64_lds(sm.drop[1][ci]);
+            const float lk = g.tau_ch * TK, lv = g.tau_ch * TV;
+            if (DK < lk && DV < lv) { chosen = ci; break; }
+        }
+        int bsel = g.block_cand[2];
+        for (int bi = 0; bi < 3; ++bi) {
+            const float VB = tree64_lds(sm.bvar[bi]);
+            const float lim = g.tau_blk * TK;
+            if (VB < lim) { bsel = g.block_cand[bi]; break; }
+        }
+        if (threadIdx.x == 0) {
+            sm.strat[0] = g.keep_cand[chosen / 3];
+            sm.strat[1] = ilog2i(g.group_cand[chosen % 3]);
+            sm.strat[2] = ilog2i(bsel);
+        }
+    }
+    __syncthreads();
+}
+
+// Pack one vector held as (lane: channel lane, lane+64): bitmap + values.
+__device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log2g, int dtype, uint64_t *keys,
+                                            uint8_t *bm_out, uint8_t *val_out, bool active) {
+    const int lane = threadIdx.x & 63;
+    int rlo, rhi;
+    group_ranks(ylo, yhi, log2g, keys, rlo, rhi);
+    const int n = r >> log2g;
+    const bool klo = rlo < n, khi = rhi < n;
+    const uint64_t mlo = __ballot(klo), mhi = __ballot(khi);
+    // group flags in bitmap order
+    const int gph = 64 >> log2g;                 // groups per half
+    const int src = (lane % gph) << log2g;
+    const int flo = __shfl((int)klo, src, WAVE), fhi = __shfl((int)khi, src, WAVE);
+    const bool flag = (lane < 2 * gph) && ((lane / gph) ? fhi : flo);
+    const uint64_t bm = __ballot(flag);
+    if (!active) return;
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    if (klo) {
+        int slot = __popcll(mlo & below);
+        *(uint16_t *)(val_out + 2 * slot) = f2h(ylo, dtype);
+    }
+    if (khi) {
+        int slot = __popcll(mlo) + __popcll(mhi & below);
+        *(uint16_t *)(val_out + 2 * slot) = f2h(yhi, dtype);
+    }
+    if (lane == 0) {
+        uint32_t *w = (uint32_t *)bm_out;
+        if (log2g == 0) {
+            w[0] = (uint32_t)mlo; w[1] = (uint32_t)(mlo >> 32); w[2] = (uint32_t)mhi; w[3] = (uint32_t)(mhi >> 32);
+        } else if (log2g == 1) {
+            w[0] = (uint32_t)bm; w[1] = (uint32_t)(bm >> 32);
+        } else {
+            w[0] = (uint32_t)bm;
+        }
+    }
+}
+
+// Encode the workgroup's tokens (K in yk, V in yv) into the token arena at
+// tok and the block keys into the score arena at sc (Sec. 5.2).
+template <int B>
+__device__ __forceinline__ void pack_segment_B(const float (&yk)[TPW][2], const float (&yv)[TPW][2], int r, int log2g, int dtype,
+                               uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys) {
+    const int wave = threadIdx.x >> 6, t0 = wave * TPW;
+    const int bmb = 16 >> log2g, vb = 2 * r, rec = bmb + vb;
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+        const int t = t0 + i, bi = t / B, j = t % B;
+        const bool act = t < ntok;
+        uint8_t *blk = tok + (uint64_t)bi * B * 2 * rec;
+        pack_vector(yk[i][0], yk[i][1], r, log2g, dtype, keys, blk + j * bmb, blk + B * bmb + j * vb, act);
+        pack_vector(yv[i][0], yv[i][1], r, log2g, dtype, keys, blk + B * (bmb + vb) + j * bmb,
+                    blk + B * (2 * bmb + vb) + j * vb, act);
+    }
+#pragma unroll
+    for (int b0 = 0; b0 < TPW; b0 += B) {
+        float mlo = yk[b0][0], mhi = yk[b0][1];
+#pragma unroll
+        for (int t = 1; t < B; ++t) { mlo = mlo + yk[b0 + t][0]; mhi = mhi + yk[b0 + t][1]; }
+        mlo = mlo * (1.0f / (float)B); mhi = mhi * (1.0f / (float)B);
+        const int bi = (t0 + b0) / B;
+        uint8_t *rp = sc + (uint64_t)bi * rec;
+        pack_vector(mlo, mhi, r, log2g, dtype, keys, rp, rp + bmb, t0 + b0 < ntok);
+    }
+}
+
+__device__ __forceinline__ void pack_segment(const float (&yk)[TPW][2], const float (&yv)[TPW][2], int r, int log2g, int log2b,
+                             int dtype, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys) {
+    switch (log2b) {
+        case 2: pack_segment_B<4>(yk, yv, r, log2g, dtype, tok, sc, ntok, keys); break;
+        case 3: pack_segment_B<8>(yk, yv, r, log2g, dtype, tok, sc, ntok, keys); break;
+        default: pack_segment_B<16>(yk, yv, r, log2g, dtype, tok, sc, ntok, keys); break;
+    }
+}
+
+// ------------------------------------------------------------------ kernels
+
+// R^T of K and V and R of V for every window of every pair, into the arena.
+__global__ void k_copy_rot(Geom g, const float *rk, const float *rv) {
+    const int p = blockIdx.y, w = blockIdx.x;
+    const float *Rk = rk + ((uint64_t)p * g.nw + w) * D * D;
+    const float *Rv = rv + ((uint64_t)p * g.nw + w) * D * D;
+    float *dst = g.rot_of(p, w);
+    for (int i = threadIdx.x; i < D * D; i += blockDim.x) {
+        const int j = i / D, c = i % D;        // source R[j][c]
+        dst[c * D + j] = Rk[i];
+        dst[D * D + c * D + j] = Rv[i];
+        dst[2 * D * D + i] = Rv[i];
+    }
+}
+
+__global__ void k_set_meta(Geom g, const int32_t *ctx) {
+    const int p = blockIdx.x * blockDim.x + threadIdx.x;
+    if (p >= g.npairs) return;
+    PairMeta *m = g.meta_of(p);
+    m->L = ctx[p / g.hkv];
+    m->nblk_final = 0; m->tok_tail = 0; m->sc_tail = 0;
+}
+
+// mode 0: strategy selection of full prefill segments; mode 1: packing.
+__global__ void __launch_bounds__(256) k_prefill(Geom g, const uint16_t *k, const uint16_t *v, int64_t seq_stride,
+                                                 int mode) {
+    __shared__ SegSmem sm;
+    const int p = blockIdx.y, seg = blockIdx.x;
+    const PairMeta *meta = g.meta_of(p);
+    const int nfull = meta->L / SEG;
+    if (seg >= nfull) return;
+    const uint64_t base = ((uint64_t)p * seq_stride + (uint64_t)seg * SEG) * D;
+    Desc *desc = g.desc_of(p) + seg;
+    const int win = (seg * SEG) / g.W;
+    const float *rot = g.rotated ? g.rot_of(p, win) : nullptr;
+    float yk[TPW][2], yv[TPW][2];
+    rotate_tile(k + base, SEG, rot, g.dtype, sm, yk);
+    rotate_tile(v + base, SEG, rot ? rot + D * D : nullptr, g.dtype, sm, yv);
+    const int wave = threadIdx.x >> 6;
+    if (mode == 0) {
+        if (g.force) {
+            if (threadIdx.x == 0) {
+                desc->r = (uint8_t)g.def_keep; desc->log2g = (uint8_t)ilog2i(g.def_group);
+                desc->log2b = (uint8_t)ilog2i(g.def_block); desc->flags = 0;
+            }
+            return;
+        }
+        token_stats(g, yk, 0, sm, SEG);
+        token_stats(g, yv, 1, sm, SEG);
+        block_stats(g, yk, sm, SEG);
+        __syncthreads();
+        choose_strategy(g, sm);
+        if (threadIdx.x == 0) {
+            desc->r = (uint8_t)sm.strat[0]; desc->log2g = (uint8_t)sm.strat[1];
+            desc->log2b = (uint8_t)sm.strat[2]; desc->flags = 0;
+        }
+    } else {
+        const Desc d = *desc;
+        pack_segment(yk, yv, d.r, d.log2g, d.log2b, g.dtype, g.tok_of(p) + d.tok_off, g.sc_of(p) + d.sc_off, SEG,
+                     sm.keys[wave]);
+    }
+}
+
+// Exclusive scan of segment sizes per pair -> descriptor offsets and tails.
+__global__ void __launch_bounds__(256) k_scan(Geom g) {
+    __shared__ uint32_t s_tok[256], s_sc[256], s_blk[256];
+    __shared__ uint32_t carry[3];
+    const int p = blockIdx.x, tid = threadIdx.x;
+    PairMeta *meta = g.meta_of(p);
+    const int nfull = meta->L / SEG;
+    Desc *desc = g.desc_of(p);
+    if (tid == 0) { carry[0] = carry[1] = carry[2] = 0; }
+    __syncthreads();
+    for (int base = 0; base < nfull; base += 256) {
+        const int s = base + tid;
+        uint32_t tb = 0, sb = 0, nb = 0;
+        if (s < nfull) {
+            const Desc d = desc[s];
+            const uint32_t rec = (uint32_t)vec_bytes(d.r, d.log2g);
+            tb = SEG * 2 * rec; nb = SEG >> d.log2b; sb = nb * rec;
+        }
+        s_tok[tid] = tb; s_sc[tid] = sb; s_blk[tid] = nb;
+        __syncthreads();
+        for (int off = 1; off < 256; off <<= 1) {      // inclusive Hillis-Steele (integers: exact)
+            uint32_t a = 0, b = 0, c = 0;
+            if (tid >= off) { a = s_tok[tid - off]; b = s_sc[tid - off]; c = s_blk[tid - off]; }
+            __syncthreads();
+            s_tok[tid] += a; s_sc[tid] += b; s_blk[tid] += c;
+            __syncthreads();
+        }
+        if (s < nfull) {
+            desc[s].tok_off = carry[0] + s_tok[tid] - tb;
+            desc[s].sc_off = carry[1] + s_sc[tid] - sb;
+            desc[s].first_block = carry[2] + s_blk[tid] - nb;
+        }
+        __syncthreads();
+        if (tid == 255) { carry[0] += s_tok[255]; carry[1] += s_sc[255]; carry[2] += s_blk[255]; }
+        __syncthreads();
+    }
+    if (tid == 0) { meta->tok_tail = carry[0]; meta->sc_tail = carry[1]; meta->nblk_final = (int32_t)carry[2]; }
+}
+
+// Remainder tokens of a prefill (L mod S) into the staging area and the
+// update buffer, as if appended one by one.
+__global__ void k_stage_tail(Geom g, const uint16_t *k, const uint16_t *v, int64_t seq_stride) {
+    const int p = blockIdx.x;
+    const int L = g.meta_of(p)->L, nf = L / SEG, m = L % SEG;
+    const int prov = m >= UBUF;
+    uint16_t *stg = g.stg_of(p), *buf = g.buf_of(p);
+    const uint64_t base = ((uint64_t)p * seq_stride + (uint64_t)nf * SEG) * D;
+    for (int i = threadIdx.x; i < m * D; i += blockDim.x) {
+        stg[i] = k[base + i];
+        stg[SEG * D + i] = v[base + i];
+        const int t = i / D;
+        if (t >= UBUF * prov) {
+            buf[i - UBUF * prov * D] = k[base + i];
+            buf[UBUF * D + i - UBUF * prov * D] = v[base + i];
+        }
+    }
+}
+
+__global__ void k_append(Geom g, const uint16_t *kn, const uint16_t *vn) {
+    const int p = blockIdx.x;
+    PairMeta *meta = g.meta_of(p);
+    const int L = meta->L, m = L % SEG;
+    const int nb = m - (m >= UBUF ? UBUF : 0);
+    uint16_t *stg = g.stg_of(p), *buf = g.buf_of(p);
+    for (int i = threadIdx.x; i < D; i += blockDim.x) {
+        const uint16_t a = kn[(uint64_t)p * D + i], b = vn[(uint64_t)p * D + i];
+        stg[m * D + i] = a; stg[SEG * D + m * D + i] = b;
+        buf[nb * D + i] = a; buf[UBUF * D + nb * D + i] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) meta->L = L + 1;
+}
+
+// Provisional flush (U tokens, previous strategy) or finalize (S tokens, own
+// strategy, recompressed in place) of a pair's trailing segment.
+__global__ void __launch_bounds__(256) k_maintain(Geom g, int mode) {
+    __shared__ SegSmem sm;
+    const int p = blockIdx.x;
+    PairMeta *meta = g.meta_of(p);
+    const int L = meta->L, m = L % SEG;
+    bool finalize = false, flush = false;
+    if (mode == MAINT_APPEND) {
+        if (L > 0 && (L % UBUF) == 0) { finalize = (m == 0); flush = !finalize; }
+    } else {
+        flush = m >= UBUF;
+    }
+    if (!finalize && !flush) return;
+    const int seg = finalize ? L / SEG - 1 : L / SEG;
+    const int ntok = finalize ? SEG : UBUF;
+    const int win = (seg * SEG) / g.W;
+    const float *rot = g.rotated ? g.rot_of(p, win) : nullptr;
+    const uint16_t *stg = g.stg_of(p);
+    float yk[TPW][2], yv[TPW][2];
+    rotate_tile(stg, ntok, rot, g.dtype, sm, yk);
+    rotate_tile(stg + SEG * D, ntok, rot ? rot + D * D : nullptr, g.dtype, sm, yv);
+    Desc *desc = g.desc_of(p);
+    const int wave = threadIdx.x >> 6;
+    int r, log2g, log2b;
+    if (finalize) {
+        if (g.force) {
+            r = g.def_keep; log2g = ilog2i(g.def_group); log2b = ilog2i(g.def_block);
+        } else {
+            token_stats(g, yk, 0, sm, SEG);
+            token_stats(g, yv, 1, sm, SEG);
+            block_stats(g, yk, sm, SEG);
+            __syncthreads();
+            choose_strategy(g, sm);
+            r = sm.strat[0]; log2g = sm.strat[1]; log2b = sm.strat[2];
+        }
+    } else if (seg > 0) {
+        const Desc pd = desc[seg - 1];
+        r = pd.r; log2g = pd.log2g; log2b = pd.log2b;
+    } else {
+        r = g.def_keep; log2g = ilog2i(g.def_group); log2b = ilog2i(g.def_block);
+    }
+    const uint32_t tok_off = meta->tok_tail, sc_off = meta->sc_tail;
+    const int nblk0 = meta->nblk_final;
+    pack_segment(yk, yv, r, log2g, log2b, g.dtype, g.tok_of(p) + tok_off, g.sc_of(p) + sc_off, ntok, sm.keys[wave]);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        Desc d;
+        d.tok_off = tok_off; d.sc_off = sc_off; d.first_block = (uint32_t)nblk0;
+        d.r = (uint8_t)r; d.log2g = (uint8_t)log2g; d.log2b = (uint8_t)log2b; d.flags = finalize ? 0 : 1;
+        desc[seg] = d;
+        if (finalize) {
+            const uint32_t rec = (uint32_t)vec_bytes(r, log2g);
+            meta->tok_tail = tok_off + SEG * 2 * rec;
+            meta->sc_tail = sc_off + (SEG >> log2b) * rec;
+            meta->nblk_final = nblk0 + (SEG >> log2b);
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, hipStream_t s) {
+    hipLaunchKernelGGL(k_copy_rot, dim3(g.nw, g.npairs), dim3(256), 0, s, g, rk, rv);
+    return hipGetLastError();
+}
+
+hipError_t launch_set_meta(const Geom &g, const int32_t *ctx_dev, hipStream_t s) {
+    hipLaunchKernelGGL(k_set_meta, dim3(ceil_div(g.npairs, 256)), dim3(256), 0, s, g, ctx_dev);
+    return hipGetLastError();
+}
+
+hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, int64_t seq_stride,
+                           const int32_t *ctx_dev, int max_full_segs, int any_tail, hipStream_t s) {
+    hipError_t e = launch_set_meta(g, ctx_dev, s);
+    if (e != hipSuccess) return e;
+    if (max_full_segs > 0) {
+        hipLaunchKernelGGL(k_prefill, dim3(max_full_segs, g.npairs), dim3(256), 0, s, g, k, v, seq_stride, 0);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_scan, dim3(g.npairs), dim3(256), 0, s, g);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (max_full_segs > 0) {
+        hipLaunchKernelGGL(k_prefill, dim3(max_full_segs, g.npairs), dim3(256), 0, s, g, k, v, seq_stride, 1);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (any_tail) {
+        hipLaunchKernelGGL(k_stage_tail, dim3(g.npairs), dim3(256), 0, s, g, k, v, seq_stride);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(k_maintain, dim3(g.npairs), dim3(256), 0, s, g, (int)MAINT_AFTER_PREFILL);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_append(const Geom &g, const uint16_t *k, const uint16_t *v, hipStream_t s) {
+    hipLaunchKernelGGL(k_append, dim3(g.npairs), dim3(128), 0, s, g, k, v);
+    return hipGetLastError();
+}
+
+hipError_t launch_maintain(const Geom &g, int mode, hipStream_t s) {
+    hipLaunchKernelGGL(k_maintain, dim3(g.npairs), dim3(256), 0, s, g, mode);
+    return hipGetLastError();
+}
+
+}  // namespace mosaic

@@ -1,0 +1,138 @@
+// mosaic_internal.h -- shared definitions of the gfx950 MosaicKV library
+// (not part of the C ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mosaic {
+
+constexpr int D = 128;        // head dim
+constexpr int SEG = 64;       // strategy segment (tokens)
+constexpr int UBUF = 32;      // update buffer (tokens)
+constexpr int WAVE = 64;
+constexpr int SPLIT_BLOCKS = 64;   // selected blocks per split-K partition
+constexpr int SCORE_SEGS = 32;     // segments per block-scoring workgroup
+constexpr int LANE_REC_DW = 57;    // per-lane LDS record slot (dwords, odd -> no bank conflicts)
+
+struct Desc {                 // 16-byte segment descriptor (layout is part of the ABI)
+    uint32_t tok_off, sc_off, first_block;
+    uint8_t r, log2g, log2b, flags;
+};
+static_assert(sizeof(Desc) == 16, "descriptor size");
+
+struct PairMeta {             // per (sequence, kv head) device counters, 64 bytes
+    int32_t L;                // tokens in the cache
+    int32_t nblk_final;       // scoreable blocks of finalized segments
+    uint32_t tok_tail;        // token-arena bytes of finalized segments
+    uint32_t sc_tail;         // score-arena bytes of finalized segments
+    int32_t pad[12];
+};
+static_assert(sizeof(PairMeta) == 64, "meta size");
+
+// Everything a kernel needs to find a pair's regions; passed by value.
+struct Geom {
+    int npairs, hkv, G, GP, dtype;
+    int W, nw, cap, max_desc, rotated;
+    uint8_t *meta, *desc, *sc, *tok;
+    uint16_t *buf, *stg;
+    float *rot;
+    uint64_t meta_stride, desc_stride, sc_stride, tok_stride, buf_stride, stg_stride, rot_stride;
+    int keep_cand[3], group_cand[3], block_cand[3];
+    int def_keep, def_group, def_block;
+    float tau_ch, tau_blk;
+    int sel_num, sel_den, force;
+
+    __host__ __device__ PairMeta *meta_of(int p) const { return (PairMeta *)(meta + (uint64_t)p * meta_stride); }
+    __host__ __device__ Desc *desc_of(int p) const { return (Desc *)(desc + (uint64_t)p * desc_stride); }
+    __host__ __device__ uint8_t *sc_of(int p) const { return sc + (uint64_t)p * sc_stride; }
+    __host__ __device__ uint8_t *tok_of(int p) const { return tok + (uint64_t)p * tok_stride; }
+    __host__ __device__ uint16_t *buf_of(int p) const { return (uint16_t *)((uint8_t *)buf + (uint64_t)p * buf_stride); }
+    __host__ __device__ uint16_t *stg_of(int p) const { return (uint16_t *)((uint8_t *)stg + (uint64_t)p * stg_stride); }
+    // rotation window w of pair p: [0] = R_k^T, [1] = R_v^T, [2] = R_v  (each D x D fp32)
+    __host__ __device__ float *rot_of(int p, int w) const {
+        if (w >= nw) w = nw - 1;
+        return (float *)((uint8_t *)rot + (uint64_t)p * rot_stride) + (uint64_t)w * 3 * D * D;
+    }
+};
+
+struct WsGeom {               // decode workspace
+    float *qrot; uint64_t qrot_stride;      // [nw][D][GP]
+    float *score; uint64_t score_stride;    // [max_blocks]
+    int32_t *sel; uint64_t sel_stride;      // [max_blocks]
+    int32_t *wsel; uint64_t wsel_stride;    // [nw + 2]
+    float *part; uint64_t part_stride;      // [max_splits][GP * (D + 2)]
+    int32_t *tag; uint64_t tag_stride;      // [max_splits]
+    int max_blocks, max_splits;
+};
+
+// ---------------------------------------------------------------- elements
+__device__ __forceinline__ float h2f(uint16_t h, int dtype) {
+    if (dtype) return __uint_as_float((uint32_t)h << 16);
+    return (float)__builtin_bit_cast(_Float16, h);
+}
+__device__ __forceinline__ uint16_t f2h(float f, int dtype) {
+    if (dtype) {   // bf16, round to nearest even (inputs are finite)
+        uint32_t u = __float_as_uint(f);
+        u += 0x7fffu + ((u >> 16) & 1u);
+        return (uint16_t)(u >> 16);
+    }
+    return __builtin_bit_cast(uint16_t, (_Float16)f);   // v_cvt_f16_f32, RNE
+}
+
+__device__ __forceinline__ int vec_bytes(int r, int log2g) { return 2 * r + (16 >> log2g); }
+
+// ---------------------------------------------------------------- wave helpers
+__device__ __forceinline__ float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, WAVE); }
+
+// tree sum over the 128 channels held as (lane l: channel l, channel l+64):
+// butterfly inside each half gives the adjacent-pair tree of that half, and
+// the final add joins the two halves -- the pairwise adjacent tree of 128.
+__device__ __forceinline__ float tree128(float lo, float hi) {
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) {
+        lo = lo + shfl_xor_f(lo, m);
+        hi = hi + shfl_xor_f(hi, m);
+    }
+    return lo + hi;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) v = fmaxf(v, shfl_xor_f(v, m));
+    return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) v += shfl_xor_f(v, m);
+    return v;
+}
+
+// orderable key of an fp32 score (larger score -> larger key); -0 is +0
+__device__ __forceinline__ uint32_t score_key(float s) {
+    uint32_t b = __float_as_uint(s);
+    if (b == 0x80000000u) b = 0;
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// ---------------------------------------------------------------- launchers
+// (implemented in the .hip files; all return hipError_t of the launch)
+hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, hipStream_t s);
+hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, int64_t seq_stride,
+                           const int32_t *ctx_dev, int max_full_segs, int any_tail, hipStream_t s);
+hipError_t launch_set_meta(const Geom &g, const int32_t *ctx_dev, hipStream_t s);
+hipError_t launch_append(const Geom &g, const uint16_t *k, const uint16_t *v, hipStream_t s);
+hipError_t launch_maintain(const Geom &g, int mode, hipStream_t s);
+hipError_t launch_decode(const Geom &g, const WsGeom &w, const uint16_t *q, float *out, float scale,
+                         int max_desc_used, int max_windows_used, hipStream_t s);
+hipError_t launch_dense(const uint16_t *q, const uint16_t *k, const uint16_t *v, float *out, int nseq,
+                        int hkv, int G, int dtype, int64_t seq_stride, int max_ctx, const int32_t *ctx,
+                        float scale, float *part, int max_splits, hipStream_t s);
+
+size_t dense_part_bytes(int npairs, int G, int max_ctx);
+
+constexpr int MAINT_APPEND = 0;        // after an append: flush or finalize where a buffer filled
+constexpr int MAINT_AFTER_PREFILL = 1; // after compress: flush a >= U-token remainder
+
+}  // namespace mosaic

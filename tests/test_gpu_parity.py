@@ -1,0 +1,136 @@
+"""GPU parity: the HIP library against the CPU oracle on the same seeded inputs.
+
+Bit-exact: descriptors (strategy choices, offsets), packed score and token
+arenas, update buffer and staging, block scores and the selected block lists.
+Within 2e-3 max-abs and 1e-3 relative L2: the fp32 attention outputs.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from _parity import (D, assert_close, assert_state_equal, bits, gpu_cache, gpu_scores_sel, oracle_decode_all,
+                     oracle_pairs, params_pair, scale_of)
+from oracle import oracle as O
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    # name: (spec, extra params)
+    "c1": (gen.spec("c1"), {}),
+    "ragged_bf16_w128": (gen.spec("c3", ctx=(0, 1, 31, 32, 33, 63, 64, 100, 1000, 2049), hkv=2, kind="gauss",
+                                  rot_window=128), {}),
+    "g7_student": (gen.spec("c5", ctx=(300, 77, 129, 2000), appends=0), {}),
+    "forced_norot_fp16": (gen.spec("c2", ctx=(700, 64, 1500), hkv=2, rotate=False), dict(force_default=True)),
+    "mixed_strategies": (gen.spec("c2", ctx=(4096, 2500), hkv=4), {}),
+    "keep_all_rho1": (gen.spec("c1", ctx=(333, 200), hkv=2), dict(force_default=True, default=(128, 1, 4),
+                                                                  select=(1, 1))),
+}
+
+
+def _case(name):
+    spec, extra = CASES[name]
+    cap = spec.max_ctx + 130
+    lay = gen.make_layer(spec, 0, capacity=cap)
+    lp, op = params_pair(spec, **extra)
+    return spec, lay, lp, op, cap
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_compress_bit_exact(name):
+    spec, lay, lp, op, cap = _case(name)
+    print(f"[compress] {name} ctx={spec.ctx} hkv={spec.hkv} G={spec.group} {spec.dtype}", flush=True)
+    c = gpu_cache(lp, spec, lay, cap)
+    ops = oracle_pairs(op, spec, lay, cap)
+    for p in range(spec.num_seqs * spec.hkv):
+        assert_state_equal(c, p, ops[p], where=name)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_decode_parity(name):
+    spec, lay, lp, op, cap = _case(name)
+    print(f"[decode] {name} ctx={spec.ctx}", flush=True)
+    c = gpu_cache(lp, spec, lay, cap)
+    ops = oracle_pairs(op, spec, lay, cap)
+    q = gen.make_queries(spec, 0)
+    out = c.decode(q.cuda(), scale_of())
+    torch.cuda.synchronize()
+    want, sels, scores = oracle_decode_all(ops, spec, q, scale_of())
+    for p in range(spec.num_seqs * spec.hkv):
+        nb = ops[p].info().nblk
+        gs, gsel, _ = gpu_scores_sel(c, p, nb)
+        assert np.array_equal(gs.view(np.uint32), scores[p].view(np.uint32)), f"{name} pair {p}: block scores"
+        assert np.array_equal(gsel, sels[p]), f"{name} pair {p}: selected blocks"
+    assert_close(out.cpu().numpy(), want, name)
+
+
+@pytest.mark.parametrize("name", ["c1", "ragged_bf16_w128", "g7_student"])
+def test_append_flush_finalize_parity(name):
+    spec, lay, lp, op, cap = _case(name)
+    steps = 100
+    print(f"[append] {name} steps={steps}", flush=True)
+    c = gpu_cache(lp, spec, lay, cap)
+    ops = oracle_pairs(op, spec, lay, cap)
+    sc = scale_of()
+    for t in range(steps):
+        kn, vn = gen.make_appends(spec, t)
+        c.append(kn.cuda(), vn.cuda())
+        kb, vb = bits(kn), bits(vn)
+        for p, pr in enumerate(ops):
+            b, h = divmod(p, spec.hkv)
+            pr.append(kb[b, h], vb[b, h])
+        if t % 33 == 32 or t == steps - 1:
+            torch.cuda.synchronize()
+            for p in range(len(ops)):
+                assert_state_equal(c, p, ops[p], where=f"{name} step {t}")
+            q = gen.make_queries(spec, t + 1)
+            out = c.decode(q.cuda(), sc)
+            want, _, _ = oracle_decode_all(ops, spec, q, sc)
+            assert_close(out.cpu().numpy(), want, f"{name} step {t}")
+
+
+def test_keep_all_equals_dense_on_gpu():
+    """r = D, rho = 1, identity rotation: the method is dense attention."""
+    spec = gen.spec("c1", ctx=(333, 200, 64, 31), hkv=2, rotate=False)
+    cap = spec.max_ctx + 130
+    lay = gen.make_layer(spec, 0, capacity=cap)
+    lp, _ = params_pair(spec, force_default=True, default=(128, 1, 4), select=(1, 1))
+    c = gpu_cache(lp, spec, lay, cap)
+    q = gen.make_queries(spec, 0).cuda()
+    out = c.decode(q, scale_of()).cpu().numpy()
+    kb, vb, qb = bits(lay["k"]), bits(lay["v"]), bits(q)
+    for b in range(spec.num_seqs):
+        L = spec.ctx[b]
+        for h in range(spec.hkv):
+            want = O.dense_attention(qb[b, h * spec.group:(h + 1) * spec.group], kb[b, h, :L], vb[b, h, :L],
+                                     np.float32(scale_of()), spec.dtype)
+            assert_close(out[b, h * spec.group:(h + 1) * spec.group], want, f"seq {b} head {h}")
+
+
+@pytest.mark.parametrize("dtype,G", [("fp16", 4), ("bf16", 7)])
+def test_dense_baseline(dtype, G):
+    import paper_2607_00760_amd as M
+    spec = gen.spec("c1", ctx=(3000, 1025, 1), hkv=2, group=G, dtype=dtype)
+    lay = gen.make_layer(spec, 0)
+    q = gen.make_queries(spec, 0).cuda()
+    ctx = torch.tensor(spec.ctx, dtype=torch.int32, device="cuda")
+    out = M.dense_decode(q, lay["k"].cuda(), lay["v"].cuda(), ctx, scale_of(), spec.max_ctx, G).cpu().numpy()
+    kb, vb, qb = bits(lay["k"]), bits(lay["v"]), bits(q)
+    for b in range(spec.num_seqs):
+        for h in range(spec.hkv):
+            L = spec.ctx[b]
+            want = O.dense_attention(qb[b, h * G:(h + 1) * G], kb[b, h, :L], vb[b, h, :L], np.float32(scale_of()), dtype)
+            assert_close(out[b, h * G:(h + 1) * G], want, f"dense seq {b} head {h}")
+
+
+def test_decode_is_deterministic():
+    spec, lay, lp, op, cap = _case("mixed_strategies")
+    c = gpu_cache(lp, spec, lay, cap)
+    q = gen.make_queries(spec, 3).cuda()
+    a = c.decode(q, scale_of()).clone()
+    b = c.decode(q, scale_of()).clone()
+    c2 = gpu_cache(lp, spec, lay, cap)
+    d = c2.decode(q, scale_of())
+    assert torch.equal(a, b) and torch.equal(a, d)

@@ -224,7 +224,7 @@ def _rotations(x32, L, W, nw, device):
     return R
 
 
-def make_layer(s: WorkloadSpec, layer: int = 0, device="cpu", queries=None):
+def make_layer(s: WorkloadSpec, layer: int = 0, device="cpu", queries=None, capacity=None):
     """Dense prefill cache of one layer.
 
     Returns dict(k, v [num_seqs][Hkv][max_ctx][D] cache dtype, zero past each
@@ -232,7 +232,8 @@ def make_layer(s: WorkloadSpec, layer: int = 0, device="cpu", queries=None):
     fp32 or None; planted: bool mask per (seq, kvh) or None; plant_c).
     """
     Lmax = s.max_ctx
-    nw = max(1, -(-s.capacity // s.rot_window))
+    cap = s.capacity if capacity is None else capacity
+    nw = max(1, -(-cap // s.rot_window))
     k = torch.zeros((s.num_seqs, s.hkv, Lmax, D), dtype=s.torch_dtype, device=device)
     v = torch.zeros_like(k)
     rk = torch.empty((s.num_seqs, s.hkv, nw, D, D), dtype=torch.float32, device=device) if s.rotate else None
