@@ -1,0 +1,296 @@
+#!/usr/bin/env python3
+"""Benchmark of the MosaicKV decode step on one MI355X.
+
+Workload (the metric's configuration): decode attention over a compressed
+KV cache, batch 8 x 131072-token contexts, 32 query / 8 kv heads, head dim
+128, bf16, ~3x compression, 5 % of segments planted to carry 80 % of the
+softmax mass.  A step is one mosaic_decode_attention call (q rotation, block
+scoring, top-k, split-K packed attention, reduce with back-rotation) over the
+resident cache.  A >= 1 GiB buffer is overwritten before every step so that
+the 256 MB MALL holds none of the step's data; only the decode itself sits
+between the step's events.
+
+Prints ONE JSON line: value = microseconds per decode step (lower is better),
+plus the roofline of the dominant kernel, the dense fp16 baseline of the same
+shape, the compression pass and the CPU oracle on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import concurrent.futures as cf
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "compressed decode-attn µs/step + effective HBM GB/s, 128K ctx ×8 seqs vs dense"
+HBM_PEAK_GBPS = 8000.0
+D = 128
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c3")
+    ap.add_argument("--ctx", type=int, default=0, help="override the context length (smoke runs)")
+    ap.add_argument("--flush-mb", type=int, default=1024)
+    ap.add_argument("--dense-steps", type=int, default=5)
+    ap.add_argument("--cpu-sample-pairs", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(cache, spec, nb_list, sel_list, desc_list):
+    """Bytes the method must move per decode step, per kernel (score / attn /
+    qrot / reduce) and in total: block keys and descriptors (score), the
+    selected blocks' packed K and V plus update-buffer tokens (attn), R_k^T
+    per window (qrot), R_v per window with selected blocks (reduce), q and
+    the fp32 output."""
+    G = spec.group
+    W = spec.rot_window
+    tot = dict(score=0, attn=0, qrot=0, reduce=0)
+    nwq = max(1, -(-max(spec.ctx) // W))
+    for p, (nb, sel, descs) in enumerate(zip(nb_list, sel_list, desc_list)):
+        L = spec.ctx[p // spec.hkv]
+        n_desc = len(descs)
+        rec = [2 * d[3] + (16 >> d[4]) for d in descs]
+        blocks_per = [((32 if d[6] & 1 else 64) >> d[5]) for d in descs]
+        tot["score"] += sum(r * n for r, n in zip(rec, blocks_per)) + 16 * n_desc
+        # selected blocks -> descriptor (first_block ascending)
+        fb = [d[2] for d in descs]
+        import bisect
+        wins = set()
+        for b in sel:
+            i = bisect.bisect_right(fb, b) - 1
+            B = 1 << descs[i][5]
+            tot["attn"] += B * 2 * rec[i]
+            wins.add((i * 64) // W)
+        m = L % 64
+        nbuf = m - (32 if m >= 32 else 0)
+        tot["attn"] += nbuf * 2 * D * 2
+        tot["qrot"] += (nwq if cache.rotated else 0) * D * D * 4 + G * D * 2
+        tot["reduce"] += (len(wins) if cache.rotated else 0) * D * D * 4 + G * D * 4
+    tot["total"] = sum(tot.values())
+    return tot
+
+
+def source_hash():
+    h = hashlib.sha256()
+    for f in ("decode.hip", "mosaic_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2607_00760_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        sys.exit("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)")
+    import numpy as np
+    import torch
+
+    import paper_2607_00760_amd as M
+    from workloads import gen
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    spec = gen.spec(args.config)
+    if args.ctx:
+        spec = gen.spec(args.config, ctx=(args.ctx,) * spec.num_seqs)
+    cap = spec.max_ctx
+    log(f"generating {spec.name}: {spec.num_seqs} x {spec.max_ctx} tokens, {spec.hkv} kv heads")
+    t0 = time.time()
+    lay = gen.make_layer(spec, 0, device=dev, capacity=cap)
+    torch.cuda.synchronize()
+    t_gen = time.time() - t0
+    q = lay["queries"] if lay["queries"] is not None else gen.make_queries(spec, 0, device=dev)
+    params = M.Params(num_kv_heads=spec.hkv, group_size=spec.group, dtype=spec.dtype, rot_window=spec.rot_window,
+                      tau_channel=spec.tau_channel, tau_block=spec.tau_block, select=spec.select)
+    cache = M.MosaicCache(params, spec.num_seqs, cap, rotated=spec.rotate, device=dev)
+    # compression pass (timed once, after one untimed pass)
+    cache.compress(lay["k"], lay["v"], lay["ctx_lens"], lay["rot_k"], lay["rot_v"])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    cache.compress(lay["k"], lay["v"], lay["ctx_lens"], lay["rot_k"], lay["rot_v"])
+    e1.record()
+    torch.cuda.synchronize()
+    compress_ms = e0.elapsed_time(e1)
+    stats = cache.stats()
+    log(f"data {t_gen:.1f}s, compress {compress_ms:.2f} ms, ratio {stats['ratio']:.3f}")
+
+    flush = torch.empty(args.flush_mb << 20, dtype=torch.uint8, device=dev)
+    out = torch.empty((spec.num_seqs, spec.hq, D), dtype=torch.float32, device=dev)
+    scale = 1.0 / math.sqrt(D)
+    cache.set_timing(True)
+
+    def step():
+        flush.zero_()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        cache.decode(q, scale, out=out)
+        b.record()
+        return a, b
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    step_ms, kern = [], {k: [] for k in M.MosaicCache.KERNELS}
+    torch.cuda.synchronize()
+    w0 = time.time()
+    for _ in range(args.steps):
+        a, b = step()
+        kt = cache.decode_timing()           # waits for this step's kernels
+        b.synchronize()
+        step_ms.append(a.elapsed_time(b))
+        for k, v in kt.items():
+            kern[k].append(v)
+    torch.cuda.synchronize()
+    wall = time.time() - w0
+    cache.set_timing(False)
+    ms = float(np.mean(step_ms))
+    log(f"decode {1e3 * ms:.1f} us/step over {args.steps} steps")
+    kern_us = {k: 1e3 * float(np.mean(v)) for k, v in kern.items()}
+
+    # algorithmic bytes from the cache's own descriptors and selections
+    lay_c, wsl = cache.layout, cache.ws_layout
+    nb_list, sel_list, desc_list = [], [], []
+    for p in range(cache.num_pairs):
+        L = spec.ctx[p // spec.hkv]
+        nd = L // 64 + (1 if L % 64 >= 32 else 0)
+        raw = cache.region("desc", p, 16 * nd).cpu().numpy()
+        dd = []
+        for j in range(nd):
+            r = raw[16 * j:16 * j + 16]
+            u = r[:12].view(np.uint32)
+            dd.append((int(u[0]), int(u[1]), int(u[2]), int(r[12]), int(r[13]), int(r[14]), int(r[15])))
+        desc_list.append(dd)
+        nw = lay_c.num_windows
+        wsel = cache.ws_region("wsel", p, 4 * (nw + 2)).cpu().numpy().view(np.int32)
+        k = int(wsel[nw])
+        sel_list.append(cache.ws_region("sel", p, 4 * max(k, 1)).cpu().numpy().view(np.int32)[:k].tolist())
+        nb_list.append(int(wsel[nw + 1]))
+    ab = algorithmic_bytes(cache, spec, nb_list, sel_list, desc_list)
+    dom = max(("score", "attn"), key=lambda k: kern_us[k])
+    achieved = ab[dom] / (kern_us[dom] * 1e-6) / 1e9
+    traffic = None
+    tf = os.path.join(ROOT, "profiles", f"traffic_{args.config}.json")
+    if os.path.exists(tf) and not args.ctx:
+        t = json.load(open(tf))
+        if t.get("source_hash") == source_hash() and t.get("kernel") == dom:
+            traffic = t.get("bytes_per_launch")
+
+    # dense fp16 attention of the same shape (own split-K kernel), same flush protocol
+    dense_us = None
+    if not args.no_dense:
+        kd = lay["k"].to(torch.float16)
+        vd = lay["v"].to(torch.float16)
+        qd = q.to(torch.float16)
+        ctx = torch.tensor(lay["ctx_lens"], dtype=torch.int32, device=dev)
+        dout = M.dense_decode(qd, kd, vd, ctx, scale, spec.max_ctx, spec.group)
+        ws = torch.empty(1 << 20, dtype=torch.uint8, device=dev)
+        import ctypes as C
+        n = C.c_size_t()
+        M.load().mosaic_dense_workspace_bytes(spec.num_seqs, spec.hkv, spec.group, spec.max_ctx, C.byref(n))
+        ws = torch.empty(n.value, dtype=torch.uint8, device=dev)
+        dts = []
+        for i in range(args.dense_steps + 1):
+            flush.zero_()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            M.dense_decode(qd, kd, vd, ctx, scale, spec.max_ctx, spec.group, out=dout, ws=ws)
+            b.record()
+            torch.cuda.synchronize()
+            if i:
+                dts.append(a.elapsed_time(b))
+        dense_us = 1e3 * float(np.mean(dts))
+        log(f"dense fp16 {dense_us:.1f} us/step")
+        del kd, vd
+
+    # CPU oracle on a bounded sample (decode of a few pairs, scaled to the workload)
+    cpu = None
+    parity = None
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O
+        ns = min(args.cpu_sample_pairs, cache.num_pairs)
+        op = O.Params(group=spec.group, dtype=spec.dtype, rot_window=spec.rot_window, tau_channel=spec.tau_channel,
+                      tau_block=spec.tau_block, select=spec.select)
+        qb = gen.bits(q)
+
+        def comp(p):
+            b, h = divmod(p, spec.hkv)
+            L = spec.ctx[b]
+            pr = O.Pair(op, cap, lay["rot_k"][b, h].cpu().numpy() if spec.rotate else None,
+                        lay["rot_v"][b, h].cpu().numpy() if spec.rotate else None)
+            t = time.time()
+            pr.compress(gen.bits(lay["k"][b, h, :L]), gen.bits(lay["v"][b, h, :L]))
+            return pr, time.time() - t
+
+        threads = min(ns, os.cpu_count() or 1, 16)
+        log(f"oracle: compressing {ns} pairs on {threads} threads")
+        with cf.ThreadPoolExecutor(threads) as ex:
+            res = list(ex.map(comp, range(ns)))
+        pairs = [r[0] for r in res]
+
+        def dec(p):
+            b, h = divmod(p, spec.hkv)
+            return pairs[p].decode(qb[b, h * spec.group:(h + 1) * spec.group], scale)
+
+        t = time.time()
+        with cf.ThreadPoolExecutor(threads) as ex:
+            outs = list(ex.map(dec, range(ns)))
+        t_dec = time.time() - t
+        cpu = dict(value=t_dec * (cache.num_pairs / ns) * 1e6, unit="us/step", cores=threads, kind="oracle",
+                   sample=f"oracle decode of {ns} of {cache.num_pairs} (sequence, kv head) pairs on {threads} "
+                          f"threads, scaled x{cache.num_pairs / ns:g}; oracle compress of those pairs took "
+                          f"{sum(r[1] for r in res):.1f} thread-s")
+        got = out.cpu().numpy()
+        err, rel, sel_ok = 0.0, 0.0, True
+        for p in range(ns):
+            b, h = divmod(p, spec.hkv)
+            o, s_o = outs[p]
+            g_ = got[b, h * spec.group:(h + 1) * spec.group]
+            err = max(err, float(np.abs(g_ - o).max()))
+            rel = max(rel, float(np.linalg.norm(g_ - o) / max(np.linalg.norm(o), 1e-30)))
+            sel_ok &= list(s_o) == sel_list[p]
+        parity = dict(pairs=ns, max_abs=err, rel_l2=rel, selected_blocks_identical=bool(sel_ok))
+
+    value = ms * 1e3
+    res = {
+        "metric": METRIC, "value": round(value, 3), "unit": "us/step", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": spec.dtype, "data": "synthetic",
+        "config": {"workload": f"{spec.name}: decode attention over a compressed KV cache, batch {spec.num_seqs} x "
+                               f"{spec.max_ctx} tokens, {spec.hq} q / {spec.hkv} kv heads, d=128, {spec.dtype}, "
+                               f"select 1/10 of blocks, planted 5% of segments",
+                   "num_seqs": spec.num_seqs, "ctx": spec.max_ctx, "q_heads": spec.hq, "kv_heads": spec.hkv,
+                   "head_dim": D, "select": f"{spec.select[0]}/{spec.select[1]}", "mall_flush_mb": args.flush_mb},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "algorithmic_bytes_per_launch": ab[dom], "mean_launch_us": round(kern_us[dom], 3)},
+        "effective_gbps": round(ab["total"] / (ms * 1e-3) / 1e9, 1),
+        "algorithmic_bytes_per_step": ab,
+        "kernels_us": {k: round(v, 3) for k, v in kern_us.items()},
+        "dense_us_per_step": None if dense_us is None else round(dense_us, 2),
+        "speedup_vs_dense": None if dense_us is None else round(dense_us / value, 2),
+        "wall_ms_per_step_incl_flush": round(1e3 * wall / args.steps, 3),
+        "compress_ms": round(compress_ms, 3), "memory_ratio": round(stats["ratio"], 4),
+        "strategies": {f"{k[0]}/{k[1]}/{k[2]}": v for k, v in sorted(stats["strategies"].items())},
+        "cpu_baseline": cpu, "parity": parity, "datagen_s": round(t_gen, 1), "source_hash": source_hash(),
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

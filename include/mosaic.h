@@ -205,6 +205,16 @@ typedef struct {
 } mosaic_stats;
 mosaic_status mosaic_cache_stats(const mosaic_cache *cache, mosaic_stats *out, void *stream);
 
+/* Per-kernel timing of mosaic_decode_attention (tracing aid, Sec. 6.3's
+ * Score / TopK / Attn breakdown).  With enable = 1, every later decode records
+ * HIP events on its stream around each of its kernels (no device memory is
+ * allocated).  mosaic_decode_timing waits for the last timed decode and writes
+ * its kernel times in milliseconds to ms[0..4] = q rotation, block scoring,
+ * top-k, split-K attention, reduce.  Errors: STATE (timing off or no decode
+ * yet), HIP. */
+mosaic_status mosaic_set_timing(mosaic_cache *cache, int32_t enable);
+mosaic_status mosaic_decode_timing(mosaic_cache *cache, float *ms);
+
 /* Host view of a sequence's length (no device access). */
 int32_t mosaic_seq_tokens(const mosaic_cache *cache, int32_t seq);
 

@@ -163,6 +163,17 @@ class MosaicCache:
                                                    self.workspace.numel(), _stream(self.device)))
         return out
 
+    KERNELS = ("qrot", "score", "topk", "attn", "reduce")
+
+    def set_timing(self, enable: bool = True):
+        check(self.lib.mosaic_set_timing(self._h, int(enable)))
+
+    def decode_timing(self) -> dict:
+        """Per-kernel ms of the last decode (after set_timing(True))."""
+        ms = (C.c_float * 5)()
+        check(self.lib.mosaic_decode_timing(self._h, ms))
+        return dict(zip(self.KERNELS, list(ms)))
+
     def stats(self) -> dict:
         st = MosaicStats()
         import torch

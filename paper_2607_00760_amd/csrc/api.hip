@@ -51,6 +51,8 @@ struct mosaic_cache {
     uint64_t ctx_off;            // device int32 [num_seqs] (inside the arena)
     uint8_t *arena;
     bool compressed;
+    bool timing = false, timed_once = false;
+    hipEvent_t ev[6] = {};
     std::vector<int32_t> L;      // host mirror of each sequence's length
     Geom geom() const {
         Geom g{};
@@ -221,6 +223,8 @@ mosaic_status mosaic_cache_bind(mosaic_cache *c, void *arena, size_t bytes) {
 }
 
 mosaic_status mosaic_cache_destroy(mosaic_cache *c) {
+    if (c && c->ev[0])
+        for (auto &e : c->ev) hipEventDestroy(e);
     delete c;
     return ok();
 }
@@ -321,8 +325,9 @@ mosaic_status mosaic_decode_attention(mosaic_cache *c, const void *q, float *out
     }
     const int nwu = std::max(1, std::min(c->nw, (maxL + c->P.rot_window - 1) / c->P.rot_window));
     hipError_t e = launch_decode(c->geom(), c->wsgeom(ws), (const uint16_t *)q, out, sm_scale, max_desc, nwu,
-                                 (hipStream_t)stream);
+                                 (hipStream_t)stream, c->timing ? c->ev : nullptr);
     if (e != hipSuccess) return hip_fail(e, "decode launch");
+    if (c->timing) c->timed_once = true;
     return ok();
 }
 
@@ -398,6 +403,31 @@ mosaic_status mosaic_cache_stats(const mosaic_cache *c, mosaic_stats *out, void 
         if (c->rotated) out->rotation_bytes += (int64_t)((L + c->P.rot_window - 1) / c->P.rot_window) * 2 * D * D * 4;
     }
     out->dense_bytes = out->tokens * 2 * D * 2 * hkv;
+    return ok();
+}
+
+mosaic_status mosaic_set_timing(mosaic_cache *c, int32_t enable) {
+    if (!c) return fail(MOSAIC_ERR_INVALID, "NULL cache");
+    if (enable && !c->ev[0]) {
+        for (auto &e : c->ev) {
+            hipError_t r = hipEventCreate(&e);
+            if (r != hipSuccess) return hip_fail(r, "event create");
+        }
+    }
+    c->timing = enable != 0;
+    c->timed_once = false;
+    return ok();
+}
+
+mosaic_status mosaic_decode_timing(mosaic_cache *c, float *ms) {
+    if (!c || !ms) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    if (!c->timing || !c->timed_once) return fail(MOSAIC_ERR_STATE, "no timed decode");
+    hipError_t e = hipEventSynchronize(c->ev[5]);
+    if (e != hipSuccess) return hip_fail(e, "event synchronize");
+    for (int i = 0; i < 5; ++i) {
+        e = hipEventElapsedTime(&ms[i], c->ev[i], c->ev[i + 1]);
+        if (e != hipSuccess) return hip_fail(e, "event elapsed");
+    }
     return ok();
 }
 

@@ -550,8 +550,9 @@ __global__ void __launch_bounds__(128) k_reduce(Geom g, WsGeom ws, float *out) {
 
 template <int GP>
 hipError_t launch_decode_t(const Geom &g, const WsGeom &w, const uint16_t *q, float *out, float scale,
-                           int max_desc_used, int max_windows_used, hipStream_t s) {
+                           int max_desc_used, int max_windows_used, hipStream_t s, hipEvent_t *ev) {
     const int nwq = g.rotated ? max_windows_used : 1;
+    if (ev) hipEventRecord(ev[0], s);
     hipLaunchKernelGGL(k_qrot, dim3(nwq, g.npairs), dim3(128), 0, s, g, w, q);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -569,29 +570,35 @@ hipError_t launch_decode_t(const Geom &g, const WsGeom &w, const uint16_t *q, fl
     spw = min(spw, max(1, g.W / SEG));
     const int stage_bytes = spw * seg_bytes + 16;
     const size_t score_smem = 2 * D * GP * 4 + 32 * sizeof(Desc) + 34 * 4 + stage_bytes;
+    if (ev) hipEventRecord(ev[1], s);
     if (max_desc_used > 0) {
         hipLaunchKernelGGL(k_score<GP>, dim3(ceil_div(max_desc_used, spw), g.npairs), dim3(256), score_smem, s, g, w,
                            spw, stage_bytes);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
+    if (ev) hipEventRecord(ev[2], s);
     hipLaunchKernelGGL(k_topk, dim3(g.npairs), dim3(1024), 0, s, g, w);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     int slot_dw = (maxrec + 3) / 4;
     if ((slot_dw & 1) == 0) slot_dw += 1;
     const size_t attn_smem = D * GP * 4 + SPLIT_BLOCKS * sizeof(BlkInfo) + (SPLIT_BLOCKS + 2) * 4 +
                              4 * 64 * GP * 4 + 4 * GP * (D + 2) * 4 + 256 * 4 + (size_t)256 * slot_dw * 4;
+    if (ev) hipEventRecord(ev[3], s);
     hipLaunchKernelGGL(k_attn<GP>, dim3(w.max_splits, g.npairs), dim3(256), attn_smem, s, g, w, scale, q, slot_dw);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (ev) hipEventRecord(ev[4], s);
     hipLaunchKernelGGL(k_reduce<GP>, dim3(g.npairs), dim3(128), 0, s, g, w, out);
-    return hipGetLastError();
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (ev) hipEventRecord(ev[5], s);
+    return hipSuccess;
 }
 
 }  // namespace
 
 hipError_t launch_decode(const Geom &g, const WsGeom &w, const uint16_t *q, float *out, float scale,
-                         int max_desc_used, int max_windows_used, hipStream_t s) {
-    if (g.GP == 4) return launch_decode_t<4>(g, w, q, out, scale, max_desc_used, max_windows_used, s);
-    return launch_decode_t<8>(g, w, q, out, scale, max_desc_used, max_windows_used, s);
+                         int max_desc_used, int max_windows_used, hipStream_t s, hipEvent_t *ev) {
+    if (g.GP == 4) return launch_decode_t<4>(g, w, q, out, scale, max_desc_used, max_windows_used, s, ev);
+    return launch_decode_t<8>(g, w, q, out, scale, max_desc_used, max_windows_used, s, ev);
 }
 
 }  // namespace mosaic

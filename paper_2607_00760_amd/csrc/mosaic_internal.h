@@ -125,7 +125,7 @@ hipError_t launch_set_meta(const Geom &g, const int32_t *ctx_dev, hipStream_t s)
 hipError_t launch_append(const Geom &g, const uint16_t *k, const uint16_t *v, hipStream_t s);
 hipError_t launch_maintain(const Geom &g, int mode, hipStream_t s);
 hipError_t launch_decode(const Geom &g, const WsGeom &w, const uint16_t *q, float *out, float scale,
-                         int max_desc_used, int max_windows_used, hipStream_t s);
+                         int max_desc_used, int max_windows_used, hipStream_t s, hipEvent_t *ev);
 hipError_t launch_dense(const uint16_t *q, const uint16_t *k, const uint16_t *v, float *out, int nseq,
                         int hkv, int G, int dtype, int64_t seq_stride, int max_ctx, const int32_t *ctx,
                         float scale, float *part, int max_splits, hipStream_t s);
