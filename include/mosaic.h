@@ -133,10 +133,11 @@ mosaic_status mosaic_workspace_bytes(const mosaic_cache *cache, int32_t op, size
  *   score + p * score_stride : fp32 [max_blocks] block scores
  *   sel   + p * sel_stride   : int32 [max_blocks] selected blocks, ascending
  *   wsel  + p * wsel_stride  : int32 [windows + 2]: first selected entry of
- *                              each window, then k, then the block count */
+ *                              each window, then k, then the block count
+ *   bseg  + p * bseg_stride  : uint32 [max_blocks]: segment << 4 | block in segment */
 typedef struct {
     uint64_t qrot_off, qrot_stride, score_off, score_stride, sel_off, sel_stride, wsel_off, wsel_stride;
-    uint64_t part_off, part_stride, tag_off, tag_stride, total;
+    uint64_t part_off, part_stride, tag_off, tag_stride, bseg_off, bseg_stride, total;
     int32_t max_blocks, max_splits, gp, reserved;
 } mosaic_ws_layout;
 mosaic_status mosaic_decode_ws_layout(const mosaic_cache *cache, mosaic_ws_layout *out);

@@ -81,6 +81,7 @@ struct mosaic_cache {
         w.wsel = (int32_t *)(b + wsl.wsel_off); w.wsel_stride = wsl.wsel_stride;
         w.part = (float *)(b + wsl.part_off); w.part_stride = wsl.part_stride;
         w.tag = (int32_t *)(b + wsl.tag_off); w.tag_stride = wsl.tag_stride;
+        w.bseg = (uint32_t *)(b + wsl.bseg_off); w.bseg_stride = wsl.bseg_stride;
         w.max_blocks = max_blocks; w.max_splits = max_splits;
         return w;
     }
@@ -197,6 +198,7 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     wregion(w.wsel_off, w.wsel_stride, (uint64_t)(c->nw + 2) * 4);
     wregion(w.part_off, w.part_stride, (uint64_t)c->max_splits * c->GP * (D + 2) * 4);
     wregion(w.tag_off, w.tag_stride, (uint64_t)c->max_splits * 4);
+    wregion(w.bseg_off, w.bseg_stride, (uint64_t)c->max_blocks * 4);
     w.total = off;
     w.max_blocks = c->max_blocks; w.max_splits = c->max_splits; w.gp = c->GP;
     c->arena = nullptr;

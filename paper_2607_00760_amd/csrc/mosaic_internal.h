@@ -62,6 +62,7 @@ struct WsGeom {               // decode workspace
     int32_t *wsel; uint64_t wsel_stride;    // [nw + 2]
     float *part; uint64_t part_stride;      // [max_splits][GP * (D + 2)]
     int32_t *tag; uint64_t tag_stride;      // [max_splits]
+    uint32_t *bseg; uint64_t bseg_stride;   // [max_blocks]: segment << 4 | block in segment
     int max_blocks, max_splits;
 };
 
