@@ -153,8 +153,10 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     maxrec = std::max(maxrec, 2 * params->default_keep + 16 / params->default_group);
     for (int i = 0; i < 3; ++i) minb = std::min(minb, params->block_cand[i]);
     c->maxrec = maxrec; c->minb = minb;
-    const uint64_t tok_bytes = (uint64_t)c->max_desc * SEG * 2 * maxrec + 64;
-    const uint64_t sc_bytes = (uint64_t)c->max_desc * (SEG / minb) * maxrec + 64;
+    // + 256: the decode kernels read whole 16-byte bitmaps and up to 2 * 128 bytes
+    // of values past a vector (never used), which must stay inside the arena
+    const uint64_t tok_bytes = (uint64_t)c->max_desc * SEG * 2 * maxrec + 256;
+    const uint64_t sc_bytes = (uint64_t)c->max_desc * (SEG / minb) * maxrec + 256;
     if (tok_bytes >= (1ull << 32)) {
         delete c;
         return fail(MOSAIC_ERR_CAPACITY, "max_tokens %d: a pair's token arena would exceed 4 GiB", max_tokens);

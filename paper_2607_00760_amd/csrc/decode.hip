@@ -2,26 +2,28 @@
 // Sec. 5.3; stage-2 dynamic sequence compression, Sec. 4.2).
 //
 //   qrot   : q . R_k^T once per (pair, window) -- the rotation is merged into
-//            the single query vector instead of un-rotating the cache.  R_k^T
-//            is staged in LDS; each output channel is an fp32 fused chain.
-//   score  : every block key of a pair streamed once (a workgroup stages a
-//            contiguous run of segments' records in LDS with 16-byte loads);
-//            lane per block key: a packed vector product walking the bitmap's
-//            set bits in ascending order, fp32 fused chain, max over the GQA
+//            the single query vector instead of un-rotating the cache.  Each
+//            workgroup produces 16 output channels from an LDS slice of R_k^T;
+//            every output is one fp32 fused chain over the input channels.
+//   score  : lane per block key.  The packed record (bitmap + values) is read
+//            straight into registers; a fixed, unrolled slot sequence walks
+//            the bitmap's set bits in ascending order (v_ffbl on the current
+//            word), fp32 fused chain over the kept channels, max over the GQA
 //            group.  These scores decide the selection, so their arithmetic
 //            order is fixed.
 //   topk   : exact radix select (8-bit digits, LDS histograms) of the k-th
 //            largest score key, then an ordered compaction breaking ties by
 //            the lowest block index; scores live in LDS when they fit.
-//   attn   : split-K over the selected list, one rotation window per split.
-//            A wave processes chunks of whole blocks (<= 64 tokens): their
-//            packed records are staged in LDS with coalesced 16-byte loads
-//            (the next chunk is prefetched into registers meanwhile), the
-//            packed K and V are scattered into a dense LDS tile, and both
-//            contractions run on the matrix cores (16x16x32): logits as
-//            K . q^T with q split into two 16-bit halves, online softmax in
-//            fp32 on the accumulator layout, then P . V with P split the same
-//            way.  The update buffer is one more split (dense, unrotated).
+//   attn   : split-K over the selected list (up to 128 blocks of one rotation
+//            window per split).  The split's blocks are ordered by size, so a
+//            64-token chunk never cuts a block and a token finds its block by
+//            a closed form.  Lane per token: the packed K record is expanded
+//            from registers into a zeroed LDS tile with the same bitmap walk,
+//            logits K . q^T on the matrix cores (16x16x32, q split into two
+//            16-bit halves), online softmax in fp32 on the accumulator layout,
+//            then V expanded the same way and P . V on the matrix cores.  The
+//            next chunk's records are loaded while the current one is
+//            processed.  The update buffer is one more split (dense, unrotated).
 //   reduce : log-sum-exp merge of the splits per window, back-rotation of
 //            each window's accumulator by R_v (staged in LDS), merge of the
 //            windows and the buffer.
@@ -34,6 +36,7 @@ namespace {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(8))) _Float16 halfx8;
 typedef __attribute__((ext_vector_type(4))) float floatx4;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 
 template <int DT> struct Mma;
 template <> struct Mma<1> {
@@ -49,7 +52,25 @@ template <> struct Mma<0> {
     }
 };
 
+template <int DT> __device__ __forceinline__ float h2f_t(uint32_t h16) {
+    if (DT) return __uint_as_float(h16 << 16);
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)h16);
+}
+
 __device__ __forceinline__ void wave_sync() { __builtin_amdgcn_wave_barrier(); }
+
+// LDS byte addresses as plain integers (so that address arithmetic folds into
+// single mad/shift-add instructions) and accesses through them
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+__device__ __forceinline__ uint32_t lds_addr(const void *p) { return (uint32_t)(uintptr_t)(const lds_u8 *)p; }
+template <typename T> __device__ __forceinline__ T lds_ld(uint32_t a) {
+    return *(const __attribute__((address_space(3))) T *)(uintptr_t)a;
+}
+template <typename T> __device__ __forceinline__ void lds_st(uint32_t a, T v) {
+    *(__attribute__((address_space(3))) T *)(uintptr_t)a = v;
+}
+// keep the compiler from moving memory operations across this point
+__device__ __forceinline__ void mem_fence_compiler() { asm volatile("" ::: "memory"); }
 
 __device__ __forceinline__ int pair_ndesc(const PairMeta &m, int &n_final, int &prov, int &nbuf) {
     n_final = m.L / SEG;
@@ -86,89 +107,224 @@ __device__ __forceinline__ void stage_copy(uint4 *dst, const uint4 *src, int nby
     }
 }
 
-// packed vector product: acc[h] = chain over kept slots of (q[c][h], value)
-template <int GP>
-__device__ __forceinline__ void packed_dot(const uint32_t *bm, const uint16_t *vals, int log2g, int dtype,
-                                           const float *qs /* [D][GP] */, float (&acc)[GP]) {
+// ------------------------------------------------------------------ qrot
+constexpr int QROT_COLS = 16;
+
+__global__ void __launch_bounds__(64) k_qrot(Geom g, WsGeom ws, const uint16_t *q) {
+    __shared__ __align__(16) float rt[D][QROT_COLS];      // R_k^T[c][j0 + jj] = R_k[j0 + jj][c]
+    __shared__ float qs[8][D];
+    constexpr int NCG = D / QROT_COLS;
+    const int w = blockIdx.x / NCG, j0 = (blockIdx.x % NCG) * QROT_COLS;
+    const int p = blockIdx.y, tid = threadIdx.x, G = g.G;
+    if (g.rotated) {
+        const float *src = g.rot_of(p, w);
+        uint4 t[8];
 #pragma unroll
-    for (int h = 0; h < GP; ++h) acc[h] = 0.0f;
-    const int nwords = 4 >> log2g, gsz = 1 << log2g;
-    int slot = 0;
-    for (int wi = 0; wi < nwords; ++wi) {
-        uint32_t bits = bm[wi];
-        while (bits) {
-            const int bpos = __builtin_ctz(bits);
-            bits &= bits - 1u;
-            const int c0 = (wi * 32 + bpos) << log2g;
-            for (int e = 0; e < gsz; ++e) {
-                const float v = h2f(vals[slot++], dtype);
-                const float *qc = qs + (c0 + e) * GP;
+        for (int k = 0; k < 8; ++k) {
+            const int idx = tid + 64 * k, c = idx >> 2, part = idx & 3;
+            t[k] = *(const uint4 *)(src + c * D + j0 + 4 * part);
+        }
 #pragma unroll
-                for (int h = 0; h < GP; ++h) acc[h] = fmaf(qc[h], v, acc[h]);
+        for (int k = 0; k < 8; ++k) {
+            const int idx = tid + 64 * k, c = idx >> 2, part = idx & 3;
+            *(uint4 *)&rt[c][4 * part] = t[k];
+        }
+    }
+    for (int i = tid; i < G * D; i += 64) qs[i / D][i % D] = h2f(q[(uint64_t)p * G * D + i], g.dtype);
+    __syncthreads();
+    const int jj = tid & 15, h0 = tid >> 4;         // heads h0 and h0 + 4
+    float a0 = 0.0f, a1 = 0.0f;
+    if (g.rotated) {
+        const bool two = h0 + 4 < G;
+#pragma unroll 8
+        for (int c = 0; c < D; ++c) {
+            const float r = rt[c][jj];
+            a0 = fmaf(qs[h0][c], r, a0);
+            if (two) a1 = fmaf(qs[h0 + 4][c], r, a1);
+        }
+    } else {
+        a0 = (h0 < G) ? qs[h0][j0 + jj] : 0.0f;
+        a1 = (h0 + 4 < G) ? qs[h0 + 4][j0 + jj] : 0.0f;
+    }
+    float *dst = ws.qrot + (uint64_t)p * (ws.qrot_stride / 4) + ((uint64_t)w * D + j0 + jj) * g.GP;
+    if (h0 < g.GP) dst[h0] = (h0 < G) ? a0 : 0.0f;
+    if (h0 + 4 < g.GP) dst[h0 + 4] = (h0 + 4 < G) ? a1 : 0.0f;
+}
+
+// ------------------------------------------------------------------ bitmap walk
+// A packed vector keeps r values in ascending channel order; its bitmap marks
+// the kept groups of 1 << log2g channels.  The walk visits the set bits in
+// ascending order, one per step, so that a fixed, unrolled slot sequence can
+// take the values from registers.  The position is v_ffbl of the current
+// bitmap word; the words are walked in order, with empty words in the middle
+// squeezed out first so that a step moves on by at most one word.  Each word
+// carries the caller's address of its first group.
+struct Walk {
+    uint32_t cur, n1, n2, n3;
+    uint32_t a, a1, a2, a3;
+    __device__ __forceinline__ uint32_t pos() const { return (uint32_t)__builtin_ctz(cur); }
+    template <int NWD>
+    __device__ __forceinline__ void step() {
+        cur &= cur - 1u;
+        if (NWD > 1) {
+            const bool z = cur == 0u;
+            cur = z ? n1 : cur;
+            a = z ? a1 : a;
+            if (NWD > 2) {
+                n1 = z ? n2 : n1; a1 = z ? a2 : a1;
+                n2 = z ? n3 : n2; a2 = z ? a3 : a2;
             }
         }
     }
-}
-
-// ------------------------------------------------------------------ qrot
-__global__ void __launch_bounds__(256) k_qrot(Geom g, WsGeom ws, const uint16_t *q) {
-    __shared__ __align__(16) float rt[D * D];
-    __shared__ float qs[8][D];
-    const int w = blockIdx.x, p = blockIdx.y, tid = threadIdx.x;
-    const int G = g.G;
-    for (int i = tid; i < G * D; i += 256) qs[i / D][i % D] = h2f(q[((uint64_t)p * G) * D + i], g.dtype);
-    if (g.rotated) stage_copy<256, 16>((uint4 *)rt, (const uint4 *)g.rot_of(p, w), D * D * 4, tid);
-    __syncthreads();
-    if (tid >= D) return;
-    const int j = tid;
-    float acc[8];
-#pragma unroll
-    for (int h = 0; h < 8; ++h) acc[h] = 0.0f;
-    if (g.rotated) {
-        for (int c = 0; c < D; ++c) {           // R_k^T: rt[c*D + j] = R_k[j][c]
-            const float r = rt[c * D + j];
-#pragma unroll
-            for (int h = 0; h < 8; ++h)
-                if (h < G) acc[h] = fmaf(qs[h][c], r, acc[h]);
-        }
-    } else {
-#pragma unroll
-        for (int h = 0; h < 8; ++h) acc[h] = (h < G) ? qs[h][j] : 0.0f;
-    }
-    float *dst = ws.qrot + (uint64_t)p * (ws.qrot_stride / 4) + ((uint64_t)w * D + j) * g.GP;
-#pragma unroll
-    for (int h = 0; h < 8; ++h)
-        if (h < g.GP) dst[h] = (h < G) ? acc[h] : 0.0f;
-}
-
-// ------------------------------------------------------------------ score
-// Ascending set bits of a packed vector's bitmap (group indices), one at a time.
-struct BitIter {
-    uint32_t cur, w1, w2, w3;
-    int base;
-    __device__ __forceinline__ BitIter(uint32_t a, uint32_t b, uint32_t c, uint32_t d)
-        : cur(a), w1(b), w2(c), w3(d), base(0) {}
-    __device__ __forceinline__ int next() {
-        while (cur == 0u) { cur = w1; w1 = w2; w2 = w3; w3 = 0u; base += 32; }
-        const int b = __builtin_ctz(cur);
-        cur &= cur - 1u;
-        return base + b;
-    }
 };
 
-// element s (static) of r packed 16-bit values held two per dword
+__device__ __forceinline__ void cswap_empty(uint32_t &wa, uint32_t &aa, uint32_t &wb, uint32_t &ab) {
+    const bool z = wa == 0u;
+    wa = z ? wb : wa;
+    aa = z ? ab : aa;
+    wb = z ? 0u : wb;
+}
+
+template <int NWD>
+__device__ __forceinline__ Walk make_walk(const uint32_t (&bw)[4], uint32_t a0, uint32_t astep) {
+    uint32_t w[4], a[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) { w[k] = k < NWD ? bw[k] : 0u; a[k] = a0 + (uint32_t)k * astep; }
+    if (NWD == 2) {
+        const bool hole = w[0] == 0u && w[1] != 0u;
+        if (__ballot(hole)) cswap_empty(w[0], a[0], w[1], a[1]);
+    } else if (NWD == 4) {
+        const bool hole = (w[0] == 0u && (w[1] | w[2] | w[3]) != 0u) || (w[1] == 0u && (w[2] | w[3]) != 0u) ||
+                          (w[2] == 0u && w[3] != 0u);
+        if (__ballot(hole)) {                      // stable: non-empty words to the front
+#pragma unroll
+            for (int round = 0; round < 2; ++round) {
+                cswap_empty(w[0], a[0], w[1], a[1]);
+                cswap_empty(w[2], a[2], w[3], a[3]);
+                cswap_empty(w[1], a[1], w[2], a[2]);
+            }
+        }
+    }
+    Walk wk;
+    wk.cur = w[0]; wk.n1 = w[1]; wk.n2 = w[2]; wk.n3 = w[3];
+    wk.a = a[0]; wk.a1 = a[1]; wk.a2 = a[2]; wk.a3 = a[3];
+    return wk;
+}
+
+// element s (static) of packed 16-bit values held two per dword
 template <int N>
 __device__ __forceinline__ uint32_t half_at(const uint32_t (&v)[N], int s) {
     return (s & 1) ? (v[s >> 1] >> 16) : (v[s >> 1] & 0xffffu);
 }
 
-template <int GP, int RMAX>
-__global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw, int stage_bytes) {
-    extern __shared__ __align__(16) uint8_t smem[];
-    float *qs = (float *)smem;                                   // [2][D][GP]
-    Desc *ds = (Desc *)(smem + 2 * D * GP * 4);                   // [<= 32]
-    int *bpre = (int *)(ds + 32);                                 // [<= 33]
-    uint32_t *arena = (uint32_t *)(smem + 2 * D * GP * 4 + 32 * sizeof(Desc) + 48 * 4);   // 16-aligned
+// A packed vector (bitmap words + values) held in registers.
+template <int RMAX>
+struct PVec {
+    uint32_t bw[4];
+    uint32_t v[RMAX / 2];
+};
+
+// bm and val point at the vector's bitmap and values; rmax is the largest r
+// in the wave (uniform) and a16 (uniform) says both pointers are 16-byte
+// aligned.  The loads take a fixed 16-byte bitmap and rmax values: what lies
+// past a vector's own bitmap or values is read (inside the arena's slack) and
+// never used.
+template <int RMAX>
+__device__ __forceinline__ void load_pvec(PVec<RMAX> &x, const uint8_t *bm, const uint8_t *val, int rmax, bool a16) {
+    if (a16) {
+        const uint4 b = *(const uint4 *)bm;
+        x.bw[0] = b.x; x.bw[1] = b.y; x.bw[2] = b.z; x.bw[3] = b.w;
+        const uint4 *v4 = (const uint4 *)val;
+#pragma unroll
+        for (int k = 0; k < RMAX / 8; ++k) {
+            uint4 t = make_uint4(0u, 0u, 0u, 0u);
+            if (8 * k < rmax) t = v4[k];
+            x.v[4 * k] = t.x; x.v[4 * k + 1] = t.y; x.v[4 * k + 2] = t.z; x.v[4 * k + 3] = t.w;
+        }
+    } else {
+        const uint32_t *b = (const uint32_t *)bm, *v = (const uint32_t *)val;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) x.bw[k] = b[k];
+#pragma unroll
+        for (int k = 0; k < RMAX / 2; ++k) x.v[k] = (2 * k < rmax) ? v[k] : 0u;
+    }
+}
+
+// maximum over the wave (every lane active)
+__device__ __forceinline__ int wave_max_i(int v) {
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) v = max(v, __shfl_xor(v, m, 64));
+    return __builtin_amdgcn_readfirstlane(v);
+}
+
+// ------------------------------------------------------------------ score
+// One walk: acc[h] += q[c][h] * value over the kept channels c, ascending.
+// qs + qoff is the [D][GP] fp32 query of the vector's window.  RV is the
+// number of kept values when it is a compile-time constant, else 0 and r
+// (wave-uniform over the calling lanes) gives it.
+template <int DT, int GP, int RMAX, int L2G, int RV>
+__device__ __forceinline__ void score_walk(const PVec<RMAX> &x, int r, uint32_t qaddr, float (&acc)[GP]) {
+    constexpr int GS = 1 << L2G, NWD = 4 >> L2G;
+    constexpr uint32_t QB = GP * 4;                           // bytes of q per channel
+    Walk wk = make_walk<NWD>(x.bw, qaddr, 32u * GS * QB);      // LDS address of group 0 of word k
+    const int n = RV ? RV : r;
+#pragma unroll
+    for (int k = 0; k < (RV ? RV : RMAX) / GS; ++k) {
+        if (RV || k * GS < n) {                               // wave-uniform
+            const uint32_t qc = wk.a + wk.pos() * (GS * QB);
+#pragma unroll
+            for (int e = 0; e < GS; ++e) {
+                const float xv = h2f_t<DT>(half_at(x.v, k * GS + e));
+#pragma unroll
+                for (int h4 = 0; h4 < GP; h4 += 4) {
+                    const floatx4 q4 = lds_ld<floatx4>(qc + e * QB + h4 * 4);
+                    acc[h4] = fmaf(q4[0], xv, acc[h4]);
+                    acc[h4 + 1] = fmaf(q4[1], xv, acc[h4 + 1]);
+                    acc[h4 + 2] = fmaf(q4[2], xv, acc[h4 + 2]);
+                    acc[h4 + 3] = fmaf(q4[3], xv, acc[h4 + 3]);
+                }
+            }
+            wk.template step<NWD>();
+        }
+    }
+}
+
+template <int DT, int GP, int RMAX, int L2G>
+__device__ __forceinline__ void score_r(const PVec<RMAX> &x, int r, uint32_t qaddr, float (&acc)[GP]) {
+    if (r == 32) score_walk<DT, GP, RMAX, L2G, 32>(x, r, qaddr, acc);
+    else if (r == 16) score_walk<DT, GP, RMAX, L2G, 16>(x, r, qaddr, acc);
+    else if (RMAX >= 48 && r == 48) score_walk<DT, GP, RMAX, L2G, (RMAX >= 48 ? 48 : 0)>(x, r, qaddr, acc);
+    else score_walk<DT, GP, RMAX, L2G, 0>(x, r, qaddr, acc);
+}
+
+// One pass per distinct (r, log2g) among the active lanes, so that every walk
+// runs with a wave-uniform trip count and no per-step predicate.
+template <int DT, int GP, int RMAX>
+__device__ __forceinline__ void score_any(const PVec<RMAX> &x, int r, int l2g, uint32_t qaddr, float (&acc)[GP]) {
+    const int key = (r << 2) | l2g;
+    uint64_t todo = __ballot(1);
+    while (todo) {
+        const int kv = __builtin_amdgcn_readlane(key, (int)__builtin_ctzll(todo));
+        const bool mine = key == kv;
+        todo &= ~__ballot(mine);
+        if (mine) {
+            const int rv = kv >> 2;
+            if ((kv & 3) == 0) score_r<DT, GP, RMAX, 0>(x, rv, qaddr, acc);
+            else if ((kv & 3) == 1) score_r<DT, GP, RMAX, 1>(x, rv, qaddr, acc);
+            else score_r<DT, GP, RMAX, 2>(x, rv, qaddr, acc);
+        }
+    }
+}
+
+// grid (ceil(max segments / spw), pairs): a workgroup scores the block keys of
+// spw <= SCORE_SEGS consecutive segments, one lane per block key; spw is at
+// most a rotation window's segments, so a workgroup sees at most two windows.
+template <int DT, int GP, int RMAX>
+__global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
+    __shared__ __align__(16) float qs[2][D * GP];
+    __shared__ Desc ds[SCORE_SEGS];
+    __shared__ uint8_t b2s[SCORE_SEGS * 16];                 // block (relative) -> segment (relative)
+    __shared__ int s_nblk;
 
     const int p = blockIdx.y, tid = threadIdx.x;
     const PairMeta meta = *g.meta_of(p);
@@ -178,72 +334,56 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw, int s
     if (s0 >= ndesc) return;
     const int ns = min(spw, ndesc - s0);
     const Desc *gd = g.desc_of(p);
-    if (tid < ns) ds[tid] = gd[s0 + tid];
-    __syncthreads();
-    if (tid == 0) {
-        int acc = 0;
-        for (int i = 0; i < ns; ++i) {
-            bpre[i] = acc;
-            const int ntok = (ds[i].flags & 1) ? UBUF : SEG;
-            acc += ntok >> ds[i].log2b;
-        }
-        bpre[ns] = acc;
+    const uint32_t fb0 = gd[s0].first_block;
+    if (tid < ns) {
+        const Desc d = gd[s0 + tid];
+        ds[tid] = d;
+        const int nb = ((d.flags & 1) ? UBUF : SEG) >> d.log2b;
+        const int o = (int)(d.first_block - fb0);
+        for (int j = 0; j < nb; ++j) b2s[o + j] = (uint8_t)tid;
+        if (tid == ns - 1) s_nblk = o + nb;
     }
-    const int w0 = (s0 * SEG) / g.W;
-    const int qw0 = g.rotated ? w0 : 0;
-    const int qw1 = g.rotated ? ((s0 + ns - 1) * SEG) / g.W : 0;
+    const int w0 = g.rotated ? (s0 * SEG) / g.W : 0;
+    const int w1 = g.rotated ? ((s0 + ns - 1) * SEG) / g.W : 0;
     {
-        const float *src = ws.qrot + (uint64_t)p * (ws.qrot_stride / 4);
-        for (int i = tid; i < D * GP; i += 256) {
-            qs[i] = src[(uint64_t)qw0 * D * GP + i];
-            qs[D * GP + i] = src[(uint64_t)qw1 * D * GP + i];
+        const float4 *src = (const float4 *)(ws.qrot + (uint64_t)p * (ws.qrot_stride / 4));
+        float4 *d0 = (float4 *)qs[0], *d1 = (float4 *)qs[1];
+        for (int i = tid; i < D * GP / 4; i += 256) {
+            const float4 x0 = src[(uint64_t)w0 * D * GP / 4 + i], x1 = src[(uint64_t)w1 * D * GP / 4 + i];
+            d0[i] = x0;
+            d1[i] = x1;
         }
     }
-    const Desc dl = ds[ns - 1];
-    const int ntl = (dl.flags & 1) ? UBUF : SEG;
-    const uint32_t lo = ds[0].sc_off;
-    const uint32_t hi = dl.sc_off + (uint32_t)(ntl >> dl.log2b) * (uint32_t)vec_bytes(dl.r, dl.log2g);
-    const int nbytes = (int)((hi - lo + 15u) & ~15u);
-    stage_copy<256, 12>((uint4 *)arena, (const uint4 *)(g.sc_of(p) + lo), min(nbytes, stage_bytes), tid);
     __syncthreads();
-    const int nblk = bpre[ns];
+    const int nblk = s_nblk;
     float *out = ws.score + (uint64_t)p * (ws.score_stride / 4);
     uint32_t *bseg = ws.bseg + (uint64_t)p * (ws.bseg_stride / 4);
-    for (int b = tid; b < nblk; b += 256) {
-        int i = 0;
-        while (i + 1 < ns && bpre[i + 1] <= b) ++i;
+    const uint8_t *sc = g.sc_of(p);
+    for (int b0 = 0; b0 < nblk; b0 += 256) {
+        const int b = b0 + tid;
+        const bool valid = b < nblk;
+        const int i = valid ? b2s[b] : 0;
         const Desc d = ds[i];
-        const int j = b - bpre[i];
-        const int r = d.r, l2g = d.log2g, nwd = 4 >> l2g, gm = (1 << l2g) - 1;
-        const uint32_t *rp = arena + ((d.sc_off - lo + (uint32_t)j * vec_bytes(r, l2g)) >> 2);
-        // the record: bitmap words, then r values (two per dword)
-        BitIter it(rp[0], nwd > 1 ? rp[1] : 0u, nwd > 2 ? rp[2] : 0u, nwd > 3 ? rp[3] : 0u);
-        uint32_t v[RMAX / 2];
-#pragma unroll
-        for (int k = 0; k < RMAX / 2; ++k) v[k] = (2 * k < r) ? rp[nwd + k] : 0u;
-        const int w = ((s0 + i) * SEG) / g.W;
-        const float *q = qs + ((g.rotated && w != w0) ? D * GP : 0);
+        const int j = b - (int)(d.first_block - fb0);
+        const int r = valid ? d.r : 0, l2g = d.log2g;
+        const uint8_t *rec = valid ? sc + d.sc_off + (uint32_t)j * (uint32_t)vec_bytes(r, l2g) : sc;
+        const uint32_t qoff = (g.rotated && ((s0 + i) * SEG) / g.W != w0) ? D * GP * 4 : 0;
+        const bool a16 = __all(!valid || (l2g == 0 && ((uintptr_t)rec & 15u) == 0));
+        PVec<RMAX> x;
+        load_pvec<RMAX>(x, rec, rec + (16 >> l2g), wave_max_i(r), a16);
         float acc[GP];
 #pragma unroll
         for (int h = 0; h < GP; ++h) acc[h] = 0.0f;
-        int cb = 0;
-#pragma unroll
-        for (int sl = 0; sl < RMAX; ++sl) {
-            if (sl < r) {
-                if ((sl & gm) == 0) cb = it.next() << l2g;
-                const float *qc = q + (cb + (sl & gm)) * GP;
-                const float x = h2f((uint16_t)half_at(v, sl), g.dtype);
-#pragma unroll
-                for (int h = 0; h < GP; ++h) acc[h] = fmaf(qc[h], x, acc[h]);
-            }
-        }
+        score_any<DT, GP, RMAX>(x, r, l2g, lds_addr(qs) + qoff, acc);
         float best = acc[0];
 #pragma unroll
         for (int h = 1; h < GP; ++h)
             if (h < g.G) best = fmaxf(best, acc[h]);
         if (__float_as_uint(best) == 0x80000000u) best = 0.0f;
-        out[d.first_block + j] = best;
-        bseg[d.first_block + j] = ((uint32_t)(s0 + i) << 4) | (uint32_t)j;
+        if (valid) {
+            out[d.first_block + j] = best;
+            bseg[d.first_block + j] = ((uint32_t)(s0 + i) << 4) | (uint32_t)j;
+        }
     }
 }
 
@@ -380,8 +520,9 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
 }
 
 // ------------------------------------------------------------------ attention
-struct BlkInfo { uint32_t goff; int16_t r, log2g, log2b, tok0; int32_t pad; };   // 16 bytes
+struct BlkInfo { uint32_t goff; uint8_t r, log2g, log2b, pad; };   // 8 bytes
 
+// split s of a pair: window w, selected-list range [e0, e1); w = -2 past the end
 __device__ __forceinline__ void split_of(const int32_t *wsel, int nw, int s, int &w_out, int &e0, int &e1,
                                          int &total) {
     int acc = 0;
@@ -399,15 +540,13 @@ __device__ __forceinline__ void split_of(const int32_t *wsel, int nw, int s, int
     total = acc;
 }
 
-constexpr int CH_TOK = 64;           // tokens per chunk (one wave)
+constexpr int CH_TOK = 64;           // tokens per chunk (one wave, lane per token)
 constexpr int KT_STRIDE = 136;       // u16 per token row of the K tile (128 + 8 pad)
 constexpr int VT_STRIDE = 68;        // u16 per channel row of the V tile (64 + 4 pad)
 constexpr int TILE_BYTES = 17408;    // max(64 * 272, 128 * 136)
 constexpr int ATTN_NWV = 2;          // waves per attention workgroup
-constexpr int MAX_CHUNKS = SPLIT_BLOCKS * 16 / CH_TOK;
-// block table + chunk tables, rounded up to 16 bytes (pointer arithmetic on
-// LDS stays in the LDS address space)
-constexpr int ATTN_HDR_BYTES = (16 * SPLIT_BLOCKS + 4 * (2 * MAX_CHUNKS + 2) + 16 + 15) / 16 * 16;
+// block table [SPLIT_BLOCKS] + per-wave class counts, 16-byte multiple
+constexpr int ATTN_HDR_BYTES = (8 * SPLIT_BLOCKS + 2 * 4 * 4 + 15) / 16 * 16;
 
 template <int DT>
 __device__ __forceinline__ typename Mma<DT>::v8 pack8(const uint16_t (&h)[8]) {
@@ -417,64 +556,78 @@ __device__ __forceinline__ typename Mma<DT>::v8 pack8(const uint16_t (&h)[8]) {
     return __builtin_bit_cast(typename Mma<DT>::v8, u);
 }
 
-// One token's packed K and V vectors, held in registers.
-template <int RMAX>
-struct TokRec {
-    uint32_t kb[4], vb[4];          // bitmap words
-    uint32_t kv[RMAX / 2], vv[RMAX / 2];   // values, two per dword
-};
-
-template <int RMAX>
-__device__ __forceinline__ void load_tok(TokRec<RMAX> &t, const uint8_t *blkrec, int j, int r, int l2g, int B,
-                                         bool valid) {
-    const int bmb = 16 >> l2g, vb = 2 * r, nwd = 4 >> l2g;
-    const uint32_t *kb = (const uint32_t *)(blkrec + j * bmb);
-    const uint32_t *kv = (const uint32_t *)(blkrec + B * bmb + j * vb);
-    const uint32_t *vbm = (const uint32_t *)(blkrec + B * (bmb + vb) + j * bmb);
-    const uint32_t *vv = (const uint32_t *)(blkrec + B * (2 * bmb + vb) + j * vb);
+// Expand a packed vector into an LDS tile at base + off: COL = false puts
+// channel c at + 2c (a token-major row of the K tile), COL = true at
+// + c * VT_STRIDE * 2 (a column of the channel-major V tile).  RV as in the
+// score walk.
+template <int RMAX, int L2G, int RV, bool COL>
+__device__ __forceinline__ void scatter_walk(const PVec<RMAX> &x, int r, uint32_t addr) {
+    constexpr int GS = 1 << L2G, NWD = 4 >> L2G;
+    constexpr uint32_t CB = COL ? VT_STRIDE * 2 : 2;           // bytes per channel
+    Walk wk = make_walk<NWD>(x.bw, addr, 32u * GS * CB);
+    const int n = RV ? RV : r;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        t.kb[k] = (valid && k < nwd) ? kb[k] : 0u;
-        t.vb[k] = (valid && k < nwd) ? vbm[k] : 0u;
-    }
+    for (int k = 0; k < (RV ? RV : RMAX) / GS; ++k) {
+        if (RV || k * GS < n) {                               // wave-uniform
+            const uint32_t dst = wk.a + wk.pos() * (GS * CB);
+            if (!COL && GS == 1) lds_st<uint16_t>(dst, (uint16_t)half_at(x.v, k));
+            else if (!COL && GS == 2) lds_st<uint32_t>(dst, x.v[k]);
+            else if (!COL) lds_st<u32x2>(dst, u32x2{x.v[2 * k], x.v[2 * k + 1]});
+            else {
 #pragma unroll
-    for (int k = 0; k < RMAX / 2; ++k) {
-        t.kv[k] = (valid && 2 * k < r) ? kv[k] : 0u;
-        t.vv[k] = (valid && 2 * k < r) ? vv[k] : 0u;
-    }
-}
-
-// scatter a packed vector held in registers into a dense 16-bit tile:
-// element c goes to base[c * cstride]; slots are walked in fixed order
-template <int RMAX>
-__device__ __forceinline__ void scatter_regs(const uint32_t (&bw)[4], const uint32_t (&vals)[RMAX / 2], int r,
-                                             int l2g, uint16_t *base, int cstride) {
-    BitIter it(bw[0], bw[1], bw[2], bw[3]);
-    const int gm = (1 << l2g) - 1;
-    int cb = 0;
-#pragma unroll
-    for (int sl = 0; sl < RMAX; ++sl) {
-        if (sl < r) {
-            if ((sl & gm) == 0) cb = it.next() << l2g;
-            base[(cb + (sl & gm)) * cstride] = (uint16_t)half_at(vals, sl);
+                for (int e = 0; e < GS; ++e) lds_st<uint16_t>(dst + e * CB, (uint16_t)half_at(x.v, k * GS + e));
+            }
+            wk.template step<NWD>();
         }
     }
 }
 
-template <int DT, int GP, int RMAX, bool DBUF>
-__global__ void __launch_bounds__(128) k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
+template <int RMAX, int L2G, bool COL>
+__device__ __forceinline__ void scatter_r(const PVec<RMAX> &x, int r, uint32_t addr) {
+    if (r == 32) scatter_walk<RMAX, L2G, 32, COL>(x, r, addr);
+    else if (r == 16) scatter_walk<RMAX, L2G, 16, COL>(x, r, addr);
+    else if (RMAX >= 48 && r == 48) scatter_walk<RMAX, L2G, (RMAX >= 48 ? 48 : 0), COL>(x, r, addr);
+    else scatter_walk<RMAX, L2G, 0, COL>(x, r, addr);
+}
+
+// called by the lanes that hold a token; one pass per distinct (r, log2g)
+template <int RMAX, bool COL>
+__device__ __forceinline__ void scatter_any(const PVec<RMAX> &x, int r, int l2g, uint32_t addr) {
+    const int key = (r << 2) | l2g;
+    uint64_t todo = __ballot(1);
+    while (todo) {
+        const int kv = __builtin_amdgcn_readlane(key, (int)__builtin_ctzll(todo));
+        const bool mine = key == kv;
+        todo &= ~__ballot(mine);
+        if (mine) {
+            const int rv = kv >> 2;
+            if ((kv & 3) == 0) scatter_r<RMAX, 0, COL>(x, rv, addr);
+            else if ((kv & 3) == 1) scatter_r<RMAX, 1, COL>(x, rv, addr);
+            else scatter_r<RMAX, 2, COL>(x, rv, addr);
+        }
+    }
+}
+
+// where this lane's token of a chunk lives
+struct TokLoc {
+    uint32_t kbm, kval, vbm, vval;     // byte offsets in the pair's token arena
+    int r, l2g;
+    bool valid, a16;
+};
+
+template <int DT, int GP, int RMAX>
+__global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
+k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     using M8 = typename Mma<DT>::v8;
     constexpr int NWV = ATTN_NWV;
     extern __shared__ __align__(16) uint8_t smem[];
-    BlkInfo *blk = (BlkInfo *)smem;                         // [SPLIT_BLOCKS], sorted by block size
-    int *ch_first = (int *)(blk + SPLIT_BLOCKS);            // [MAX_CHUNKS + 1]
-    int *ch_ntok = ch_first + MAX_CHUNKS + 1;               // [MAX_CHUNKS]
-    int *s_nch = ch_ntok + MAX_CHUNKS + 1;                  // [1]
+    BlkInfo *blk = (BlkInfo *)smem;                         // [SPLIT_BLOCKS], ordered 16, 8, 4
+    int *wcnt = (int *)(smem + 8 * SPLIT_BLOCKS);           // [NWV][4] blocks per size class
     uint8_t *wbase = smem + ATTN_HDR_BYTES;                 // [NWV] tiles
 
     const int p = blockIdx.y, s = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, q4 = lane >> 4;
-    uint16_t *tile = (uint16_t *)(wbase + wave * TILE_BYTES);
+    uint8_t *tile = wbase + wave * TILE_BYTES;
 
     const PairMeta meta = *g.meta_of(p);
     int nf, prov, nbuf;
@@ -544,38 +697,38 @@ __global__ void __launch_bounds__(128) k_attn(Geom g, WsGeom ws, float scale, co
         return;
     }
 
-    // ---- split setup (wave 0): blocks sorted by size (16, 8, 4; stable), so
-    // every block starts at a multiple of its size and no block straddles a
-    // 64-token chunk; chunk c holds tokens [64c, 64c + 64) of the sorted run
+    // ---- split setup: one thread per selected block; blocks ordered by size
+    // (16, then 8, then 4; ascending index inside a size), so every block
+    // starts at a multiple of its size and none straddles a 64-token chunk
     const int nbk = e1 - e0;
-    if (wave == 0) {
-        const bool on = lane < nbk;
-        uint32_t goff = 0; int r = 0, l2g = 0, l2b = 0;
+    {
+        const bool on = tid < nbk;
+        uint32_t goff = 0; int r = 0, l2g = 0, l2b = 2;
         if (on) {
-            const uint32_t bs = ws.bseg[(uint64_t)p * (ws.bseg_stride / 4) + sel[e0 + lane]];
+            const uint32_t bs = ws.bseg[(uint64_t)p * (ws.bseg_stride / 4) + sel[e0 + tid]];
             const Desc d = g.desc_of(p)[bs >> 4];
             const int jb = (int)(bs & 15u);
             r = d.r; l2g = d.log2g; l2b = d.log2b;
             goff = d.tok_off + (uint32_t)(jb << l2b) * (uint32_t)(2 * vec_bytes(r, l2g));
         }
-        const uint64_t m16 = __ballot(on && l2b == 4), m8 = __ballot(on && l2b == 3), m4 = __ballot(on && l2b == 2);
-        const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-        const int c16 = __popcll(m16), c8 = __popcll(m8), c4 = __popcll(m4);
-        int pos = 0, off = 0;
-        if (l2b == 4) { const int rk = __popcll(m16 & below); pos = rk; off = 16 * rk; }
-        else if (l2b == 3) { const int rk = __popcll(m8 & below); pos = c16 + rk; off = 16 * c16 + 8 * rk; }
-        else { const int rk = __popcll(m4 & below); pos = c16 + c8 + rk; off = 16 * c16 + 8 * c8 + 4 * rk; }
-        if (on) {
-            BlkInfo bi;
-            bi.goff = goff; bi.r = (int16_t)r; bi.log2g = (int16_t)l2g; bi.log2b = (int16_t)l2b;
-            bi.tok0 = (int16_t)(off & (CH_TOK - 1)); bi.pad = 0;
-            blk[pos] = bi;
-            if ((off & (CH_TOK - 1)) == 0) ch_first[off / CH_TOK] = pos;
+        const int cls = on ? 4 - l2b : 3;
+        const uint64_t m0 = __ballot(cls == 0), m1 = __ballot(cls == 1), m2 = __ballot(cls == 2);
+        if (lane == 0) {
+            wcnt[wave * 4 + 0] = __popcll(m0);
+            wcnt[wave * 4 + 1] = __popcll(m1);
+            wcnt[wave * 4 + 2] = __popcll(m2);
         }
-        const int T = 16 * c16 + 8 * c8 + 4 * c4;
-        const int nch = (T + CH_TOK - 1) / CH_TOK;
-        if (lane < nch) ch_ntok[lane] = min(CH_TOK, T - CH_TOK * lane);
-        if (lane == 0) { ch_first[nch] = nbk; s_nch[0] = nch; }
+        __syncthreads();
+        if (on) {
+            const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+            const int c16 = wcnt[0] + wcnt[4], c8 = wcnt[1] + wcnt[5];
+            const int base = cls == 0 ? 0 : (cls == 1 ? c16 : c16 + c8);
+            const uint64_t mc = cls == 0 ? m0 : (cls == 1 ? m1 : m2);
+            const int pos = base + (wave ? wcnt[cls] : 0) + __popcll(mc & below);
+            BlkInfo bi;
+            bi.goff = goff; bi.r = (uint8_t)r; bi.log2g = (uint8_t)l2g; bi.log2b = (uint8_t)l2b; bi.pad = 0;
+            blk[pos] = bi;
+        }
     }
     // q operand: B[k = channel][n = head] of the logits K . q^T, split hi + lo
     M8 qhi[4], qlo[4];
@@ -597,25 +750,52 @@ __global__ void __launch_bounds__(128) k_attn(Geom g, WsGeom ws, float scale, co
         }
     }
     __syncthreads();
-    const int nch = s_nch[0];
+    const int n16 = wcnt[0] + wcnt[4], n8 = wcnt[1] + wcnt[5], n4 = wcnt[2] + wcnt[6];
+    const int T16 = 16 * n16, T8 = T16 + 8 * n8, T = T8 + 4 * n4;
+    const int nch = (T + CH_TOK - 1) / CH_TOK;
     const uint8_t *tokg = g.tok_of(p);
+
+    // token t of the split's ordered run -> its packed records
+    auto locate = [&](int c) {
+        TokLoc L;
+        const int t = c * CH_TOK + lane;
+        L.valid = c < nch && t < T;
+        int bi, j;
+        if (t < T16) { bi = t >> 4; j = t & 15; }
+        else if (t < T8) { bi = n16 + ((t - T16) >> 3); j = (t - T16) & 7; }
+        else { bi = n16 + n8 + ((t - T8) >> 2); j = (t - T8) & 3; }
+        if (!L.valid) { bi = 0; j = 0; }
+        const BlkInfo b = blk[bi];
+        const int r = b.r, l2g = b.log2g, B = 1 << b.log2b, bmb = 16 >> l2g;
+        const uint32_t base = b.goff;
+        L.kbm = base + j * bmb;
+        L.kval = base + B * bmb + j * 2 * r;
+        L.vbm = base + B * (bmb + 2 * r) + j * bmb;
+        L.vval = base + B * (2 * bmb + 2 * r) + j * 2 * r;
+        L.r = L.valid ? r : 0;
+        L.l2g = l2g;
+        L.a16 = __all(!L.valid || (l2g == 0 && (r & 7) == 0 && (base & 15u) == 0));
+        return L;
+    };
 
     float m_run = -INFINITY, l_run = 0.0f;                  // head l16
     floatx4 acc_o[8];                                       // [channel tile][head 4*q4 + r]
 #pragma unroll
     for (int ct = 0; ct < 8; ++ct) acc_o[ct] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
 
-    // this lane's token of chunk c: block info and index inside the block
-    auto locate = [&](int c, BlkInfo &info, int &j, bool &valid) {
-        int bi = ch_first[c];
-        const int b1 = ch_first[c + 1];
-        while (bi + 1 < b1 && blk[bi + 1].tok0 > 0 && blk[bi + 1].tok0 <= lane) ++bi;
-        info = blk[bi];
-        j = lane - info.tok0;
-        valid = lane < ch_ntok[c];
-    };
-    auto process = [&](const TokRec<RMAX> &t, const BlkInfo &info, bool valid, int ntok) {
-        // ---- K: zero the tile, scatter packed keys (token-major rows), logits on MFMA
+    int c = wave;
+    TokLoc cur = locate(c);
+    PVec<RMAX> kx, vx;
+    {
+        const int rm = wave_max_i(cur.r);
+        load_pvec<RMAX>(kx, tokg + cur.kbm, tokg + cur.kval, rm, cur.a16);
+        load_pvec<RMAX>(vx, tokg + cur.vbm, tokg + cur.vval, rm, cur.a16);
+    }
+    for (; c < nch; c += NWV) {
+        const int ntok = min(CH_TOK, T - c * CH_TOK);
+        const TokLoc nxt = locate(c + NWV);
+        const int rmn = wave_max_i(nxt.r);
+        // ---- K: zero the tile, expand packed keys (token-major rows), logits on MFMA
         {
             uint4 *t4 = (uint4 *)tile;
             const uint4 zz = {0u, 0u, 0u, 0u};
@@ -623,15 +803,18 @@ __global__ void __launch_bounds__(128) k_attn(Geom g, WsGeom ws, float scale, co
             for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
         }
         wave_sync();
-        if (valid) scatter_regs<RMAX>(t.kb, t.kv, info.r, info.log2g, tile + lane * KT_STRIDE, 1);
+        if (cur.valid) scatter_any<RMAX, false>(kx, cur.r, cur.l2g, lds_addr(tile) + lane * (KT_STRIDE * 2));
         wave_sync();
+        mem_fence_compiler();
+        load_pvec<RMAX>(kx, tokg + nxt.kbm, tokg + nxt.kval, rmn, nxt.a16);
         float z[4][4];
+        const uint16_t *tk = (const uint16_t *)tile;
 #pragma unroll
         for (int n = 0; n < 4; ++n) {
             floatx4 a4 = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks) {
-                const uint4 kv = *(const uint4 *)(tile + (n * 16 + l16) * KT_STRIDE + ks * 32 + q4 * 8);
+                const uint4 kv = *(const uint4 *)(tk + (n * 16 + l16) * KT_STRIDE + ks * 32 + q4 * 8);
                 const M8 a = __builtin_bit_cast(M8, kv);
                 a4 = Mma<DT>::run(a, qhi[ks], a4);
                 a4 = Mma<DT>::run(a, qlo[ks], a4);
@@ -664,7 +847,7 @@ __global__ void __launch_bounds__(128) k_attn(Geom g, WsGeom ws, float scale, co
         ls += __shfl_xor(ls, 32, 64);
         l_run = l_run * alpha + ls;
         m_run = mn;
-        // ---- V: zero the tile, scatter packed values (channel-major rows)
+        // ---- V: zero the tile, expand packed values (channel-major rows)
         wave_sync();
         {
             uint4 *t4 = (uint4 *)tile;
@@ -673,8 +856,10 @@ __global__ void __launch_bounds__(128) k_attn(Geom g, WsGeom ws, float scale, co
             for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
         }
         wave_sync();
-        if (valid) scatter_regs<RMAX>(t.vb, t.vv, info.r, info.log2g, tile + lane, VT_STRIDE);
+        if (cur.valid) scatter_any<RMAX, true>(vx, cur.r, cur.l2g, lds_addr(tile) + lane * 2);
         wave_sync();
+        mem_fence_compiler();
+        load_pvec<RMAX>(vx, tokg + nxt.vbm, tokg + nxt.vval, rmn, nxt.a16);
         // ---- P . V on MFMA: A = P[head l16][tokens], B = V[tokens][channel tile]
         float ar[4];
 #pragma unroll
@@ -683,6 +868,7 @@ __global__ void __launch_bounds__(128) k_attn(Geom g, WsGeom ws, float scale, co
         for (int ct = 0; ct < 8; ++ct)
 #pragma unroll
             for (int r = 0; r < 4; ++r) acc_o[ct][r] *= ar[r];
+        const uint16_t *tv = (const uint16_t *)tile;
 #pragma unroll
         for (int kv = 0; kv < 2; ++kv) {
             uint16_t hh[8], ll[8];
@@ -695,7 +881,7 @@ __global__ void __launch_bounds__(128) k_attn(Geom g, WsGeom ws, float scale, co
             const M8 ah = pack8<DT>(hh), al = pack8<DT>(ll);
 #pragma unroll
             for (int ct = 0; ct < 8; ++ct) {
-                const uint16_t *row = tile + (ct * 16 + l16) * VT_STRIDE + kv * 32 + q4 * 4;
+                const uint16_t *row = tv + (ct * 16 + l16) * VT_STRIDE + kv * 32 + q4 * 4;
                 const uint2 v0 = *(const uint2 *)row, v1 = *(const uint2 *)(row + 16);
                 const uint4 vv4 = {v0.x, v0.y, v1.x, v1.y};
                 const M8 bv = __builtin_bit_cast(M8, vv4);
@@ -704,44 +890,7 @@ __global__ void __launch_bounds__(128) k_attn(Geom g, WsGeom ws, float scale, co
             }
         }
         wave_sync();
-    };
-
-    if (DBUF) {
-        // two register sets: the next chunk's loads are in flight while one is processed
-        TokRec<RMAX> ta, tb;
-        BlkInfo ia, ib;
-        int ja = 0, jb = 0;
-        bool va = false, vb = false;
-        int c = wave;
-        if (c < nch) {
-            locate(c, ia, ja, va);
-            load_tok<RMAX>(ta, tokg + ia.goff, ja, ia.r, ia.log2g, 1 << ia.log2b, va);
-        }
-        for (; c < nch; c += 2 * NWV) {
-            const int cn = c + NWV;
-            if (cn < nch) {
-                locate(cn, ib, jb, vb);
-                load_tok<RMAX>(tb, tokg + ib.goff, jb, ib.r, ib.log2g, 1 << ib.log2b, vb);
-            }
-            process(ta, ia, va, ch_ntok[c]);
-            if (cn >= nch) break;
-            const int cnn = cn + NWV;
-            if (cnn < nch) {
-                locate(cnn, ia, ja, va);
-                load_tok<RMAX>(ta, tokg + ia.goff, ja, ia.r, ia.log2g, 1 << ia.log2b, va);
-            }
-            process(tb, ib, vb, ch_ntok[cn]);
-        }
-    } else {
-        for (int c = wave; c < nch; c += NWV) {
-            TokRec<RMAX> t;
-            BlkInfo info;
-            int j = 0;
-            bool valid = false;
-            locate(c, info, j, valid);
-            load_tok<RMAX>(t, tokg + info.goff, j, info.r, info.log2g, 1 << info.log2b, valid);
-            process(t, info, valid, ch_ntok[c]);
-        }
+        cur = nxt;
     }
     // ---- merge the waves' (m, l, acc) and write the split's partial
     __syncthreads();
@@ -874,50 +1023,27 @@ __global__ void __launch_bounds__(256) k_reduce(Geom g, WsGeom ws, float *out) {
         if (hb + u < G) o[(hb + u) * D + j] = (Lg[u] > 0.0f) ? Og[u] / Lg[u] : 0.0f;
 }
 
-int max_record_bytes(const Geom &g) {
-    int maxrec = 2 * g.def_keep + (16 >> (31 - __builtin_clz(g.def_group)));
-    for (int i = 0; i < 3; ++i)
-        for (int k = 0; k < 3; ++k)
-            maxrec = max(maxrec, 2 * g.keep_cand[i] + (16 >> (31 - __builtin_clz(g.group_cand[k]))));
-    return maxrec;
+int max_keep(const Geom &g) {
+    int r = g.def_keep;
+    for (int i = 0; i < 3; ++i) r = max(r, g.keep_cand[i]);
+    return r;
 }
 
 template <int DT, int GP>
-hipError_t launch_attn(const Geom &g, const WsGeom &w, const uint16_t *q, float scale, hipStream_t s) {
-    const size_t smem = ATTN_HDR_BYTES + (size_t)ATTN_NWV * TILE_BYTES;
-    const dim3 grid(w.max_splits, g.npairs), block(64 * ATTN_NWV);
-    if (max_record_bytes(g) <= 2 * 48 + 16)
-        hipLaunchKernelGGL((k_attn<DT, GP, 48, true>), grid, block, smem, s, g, w, scale, q);
-    else
-        hipLaunchKernelGGL((k_attn<DT, GP, 128, false>), grid, block, smem, s, g, w, scale, q);
-    return hipGetLastError();
-}
-
-template <int GP>
-hipError_t launch_decode_t(const Geom &g, const WsGeom &w, const uint16_t *q, float *out, float scale,
-                           int max_desc_used, int max_windows_used, hipStream_t s, hipEvent_t *ev) {
+hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, float *out, float scale,
+                            int max_desc_used, int max_windows_used, hipStream_t s, hipEvent_t *ev) {
     const int nwq = g.rotated ? max_windows_used : 1;
+    const bool small = max_keep(g) <= 48;
     if (ev) hipEventRecord(ev[0], s);
-    hipLaunchKernelGGL(k_qrot, dim3(nwq, g.npairs), dim3(256), 0, s, g, w, q);
+    hipLaunchKernelGGL(k_qrot, dim3(nwq * (D / QROT_COLS), g.npairs), dim3(64), 0, s, g, w, q);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    // block scoring: stage at most 48 KiB of score records per workgroup
-    const int maxrec = max_record_bytes(g);
-    int minb = g.def_block;
-    for (int i = 0; i < 3; ++i) minb = min(minb, g.block_cand[i]);
-    const int seg_bytes = (SEG / minb) * maxrec;
-    int spw = min(SCORE_SEGS, max(1, 49152 / seg_bytes));
-    spw = min(spw, max(1, g.W / SEG));
-    const int stage_bytes = ((spw * seg_bytes) + 31) & ~15;
-    const size_t score_smem = 2 * D * GP * 4 + 32 * sizeof(Desc) + 48 * 4 + stage_bytes;
     if (ev) hipEventRecord(ev[1], s);
     if (max_desc_used > 0) {
-        if (maxrec <= 2 * 48 + 16)
-            hipLaunchKernelGGL((k_score<GP, 48>), dim3(ceil_div(max_desc_used, spw), g.npairs), dim3(256), score_smem, s,
-                               g, w, spw, stage_bytes);
-        else
-            hipLaunchKernelGGL((k_score<GP, 128>), dim3(ceil_div(max_desc_used, spw), g.npairs), dim3(256), score_smem,
-                               s, g, w, spw, stage_bytes);
+        const int spw = max(1, min(SCORE_SEGS, g.W / SEG));
+        const dim3 grid(ceil_div(max_desc_used, spw), g.npairs);
+        if (small) hipLaunchKernelGGL((k_score<DT, GP, 48>), grid, dim3(256), 0, s, g, w, spw);
+        else hipLaunchKernelGGL((k_score<DT, GP, 128>), grid, dim3(256), 0, s, g, w, spw);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev) hipEventRecord(ev[2], s);
@@ -925,8 +1051,13 @@ hipError_t launch_decode_t(const Geom &g, const WsGeom &w, const uint16_t *q, fl
     hipLaunchKernelGGL(k_topk, dim3(g.npairs), dim3(1024), topk_smem, s, g, w);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev) hipEventRecord(ev[3], s);
-    e = g.dtype ? launch_attn<1, GP>(g, w, q, scale, s) : launch_attn<0, GP>(g, w, q, scale, s);
-    if (e != hipSuccess) return e;
+    {
+        const size_t smem = ATTN_HDR_BYTES + (size_t)ATTN_NWV * TILE_BYTES;
+        const dim3 grid(w.max_splits, g.npairs), block(64 * ATTN_NWV);
+        if (small) hipLaunchKernelGGL((k_attn<DT, GP, 48>), grid, block, smem, s, g, w, scale, q);
+        else hipLaunchKernelGGL((k_attn<DT, GP, 128>), grid, block, smem, s, g, w, scale, q);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     if (ev) hipEventRecord(ev[4], s);
     const size_t red_smem = (size_t)min(w.max_splits, REDUCE_MAX_SPLITS) * (2 * GP + 1) * 4;
     hipLaunchKernelGGL(k_reduce<GP>, dim3(g.npairs), dim3(256), red_smem, s, g, w, out);
@@ -939,8 +1070,12 @@ hipError_t launch_decode_t(const Geom &g, const WsGeom &w, const uint16_t *q, fl
 
 hipError_t launch_decode(const Geom &g, const WsGeom &w, const uint16_t *q, float *out, float scale,
                          int max_desc_used, int max_windows_used, hipStream_t s, hipEvent_t *ev) {
-    if (g.GP == 4) return launch_decode_t<4>(g, w, q, out, scale, max_desc_used, max_windows_used, s, ev);
-    return launch_decode_t<8>(g, w, q, out, scale, max_desc_used, max_windows_used, s, ev);
+    if (g.dtype) {
+        if (g.GP == 4) return launch_decode_dt<1, 4>(g, w, q, out, scale, max_desc_used, max_windows_used, s, ev);
+        return launch_decode_dt<1, 8>(g, w, q, out, scale, max_desc_used, max_windows_used, s, ev);
+    }
+    if (g.GP == 4) return launch_decode_dt<0, 4>(g, w, q, out, scale, max_desc_used, max_windows_used, s, ev);
+    return launch_decode_dt<0, 8>(g, w, q, out, scale, max_desc_used, max_windows_used, s, ev);
 }
 
 }  // namespace mosaic

@@ -10,9 +10,8 @@ constexpr int D = 128;        // head dim
 constexpr int SEG = 64;       // strategy segment (tokens)
 constexpr int UBUF = 32;      // update buffer (tokens)
 constexpr int WAVE = 64;
-constexpr int SPLIT_BLOCKS = 64;   // selected blocks per split-K partition
+constexpr int SPLIT_BLOCKS = 128;  // selected blocks per split-K partition
 constexpr int SCORE_SEGS = 32;     // segments per block-scoring workgroup
-constexpr int LANE_REC_DW = 57;    // per-lane LDS record slot (dwords, odd -> no bank conflicts)
 
 struct Desc {                 // 16-byte segment descriptor (layout is part of the ABI)
     uint32_t tok_off, sc_off, first_block;
