@@ -578,6 +578,7 @@ __device__ __forceinline__ void scatter_walk(const PVec<RMAX> &x, int r, uint32_
                 for (int e = 0; e < GS; ++e) lds_st<uint16_t>(dst + e * CB, (uint16_t)half_at(x.v, k * GS + e));
             }
             wk.template step<NWD>();
+            __builtin_amdgcn_sched_barrier(0);       // keep the steps in order: short live ranges
         }
     }
 }
@@ -608,12 +609,25 @@ __device__ __forceinline__ void scatter_any(const PVec<RMAX> &x, int r, int l2g,
     }
 }
 
-// where this lane's token of a chunk lives
+// where this lane's token of a chunk lives: its block's byte offset in the
+// pair's token arena and (token in block, r, log2g, log2b) packed in a word
 struct TokLoc {
-    uint32_t kbm, kval, vbm, vval;     // byte offsets in the pair's token arena
-    int r, l2g;
+    uint32_t base, info;
     bool valid, a16;
+    __device__ __forceinline__ int j() const { return info & 0xff; }
+    __device__ __forceinline__ int r() const { return (info >> 8) & 0xff; }
+    __device__ __forceinline__ int l2g() const { return (info >> 16) & 0xf; }
+    __device__ __forceinline__ int l2b() const { return info >> 20; }
 };
+
+// load the packed K (V when V_ is set) vector of a located token
+template <int RMAX>
+__device__ __forceinline__ void load_tok(PVec<RMAX> &x, const uint8_t *tokg, const TokLoc &L, bool V_, int rmax) {
+    const int r = L.r(), l2g = L.l2g(), B = 1 << L.l2b(), bmb = 16 >> l2g, j = L.j();
+    const uint32_t half = V_ ? (uint32_t)(B * (bmb + 2 * r)) : 0u;
+    const uint8_t *b = tokg + L.base + half;
+    load_pvec<RMAX>(x, b + j * bmb, b + B * bmb + j * 2 * r, rmax, L.a16);
+}
 
 template <int DT, int GP, int RMAX>
 __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
@@ -750,7 +764,10 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         }
     }
     __syncthreads();
-    const int n16 = wcnt[0] + wcnt[4], n8 = wcnt[1] + wcnt[5], n4 = wcnt[2] + wcnt[6];
+    // uniform counts (scalar registers)
+    const int n16 = __builtin_amdgcn_readfirstlane(wcnt[0] + wcnt[4]);
+    const int n8 = __builtin_amdgcn_readfirstlane(wcnt[1] + wcnt[5]);
+    const int n4 = __builtin_amdgcn_readfirstlane(wcnt[2] + wcnt[6]);
     const int T16 = 16 * n16, T8 = T16 + 8 * n8, T = T8 + 4 * n4;
     const int nch = (T + CH_TOK - 1) / CH_TOK;
     const uint8_t *tokg = g.tok_of(p);
@@ -766,15 +783,10 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         else { bi = n16 + n8 + ((t - T8) >> 2); j = (t - T8) & 3; }
         if (!L.valid) { bi = 0; j = 0; }
         const BlkInfo b = blk[bi];
-        const int r = b.r, l2g = b.log2g, B = 1 << b.log2b, bmb = 16 >> l2g;
-        const uint32_t base = b.goff;
-        L.kbm = base + j * bmb;
-        L.kval = base + B * bmb + j * 2 * r;
-        L.vbm = base + B * (bmb + 2 * r) + j * bmb;
-        L.vval = base + B * (2 * bmb + 2 * r) + j * 2 * r;
-        L.r = L.valid ? r : 0;
-        L.l2g = l2g;
-        L.a16 = __all(!L.valid || (l2g == 0 && (r & 7) == 0 && (base & 15u) == 0));
+        L.base = b.goff;
+        L.info = (uint32_t)j | ((uint32_t)(L.valid ? b.r : 0) << 8) | ((uint32_t)b.log2g << 16) |
+                 ((uint32_t)b.log2b << 20);
+        L.a16 = __all(!L.valid || (b.log2g == 0 && (b.r & 7) == 0 && (b.goff & 15u) == 0));
         return L;
     };
 
@@ -787,14 +799,14 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     TokLoc cur = locate(c);
     PVec<RMAX> kx, vx;
     {
-        const int rm = wave_max_i(cur.r);
-        load_pvec<RMAX>(kx, tokg + cur.kbm, tokg + cur.kval, rm, cur.a16);
-        load_pvec<RMAX>(vx, tokg + cur.vbm, tokg + cur.vval, rm, cur.a16);
+        const int rm = wave_max_i(cur.r());
+        load_tok<RMAX>(kx, tokg, cur, false, rm);
+        load_tok<RMAX>(vx, tokg, cur, true, rm);
     }
     for (; c < nch; c += NWV) {
         const int ntok = min(CH_TOK, T - c * CH_TOK);
         const TokLoc nxt = locate(c + NWV);
-        const int rmn = wave_max_i(nxt.r);
+        const int rmn = wave_max_i(nxt.r());
         // ---- K: zero the tile, expand packed keys (token-major rows), logits on MFMA
         {
             uint4 *t4 = (uint4 *)tile;
@@ -803,10 +815,10 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
         }
         wave_sync();
-        if (cur.valid) scatter_any<RMAX, false>(kx, cur.r, cur.l2g, lds_addr(tile) + lane * (KT_STRIDE * 2));
+        if (cur.valid) scatter_any<RMAX, false>(kx, cur.r(), cur.l2g(), lds_addr(tile) + lane * (KT_STRIDE * 2));
         wave_sync();
         mem_fence_compiler();
-        load_pvec<RMAX>(kx, tokg + nxt.kbm, tokg + nxt.kval, rmn, nxt.a16);
+        load_tok<RMAX>(kx, tokg, nxt, false, rmn);
         float z[4][4];
         const uint16_t *tk = (const uint16_t *)tile;
 #pragma unroll
@@ -856,10 +868,10 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
         }
         wave_sync();
-        if (cur.valid) scatter_any<RMAX, true>(vx, cur.r, cur.l2g, lds_addr(tile) + lane * 2);
+        if (cur.valid) scatter_any<RMAX, true>(vx, cur.r(), cur.l2g(), lds_addr(tile) + lane * 2);
         wave_sync();
         mem_fence_compiler();
-        load_pvec<RMAX>(vx, tokg + nxt.vbm, tokg + nxt.vval, rmn, nxt.a16);
+        load_tok<RMAX>(vx, tokg, nxt, true, rmn);
         // ---- P . V on MFMA: A = P[head l16][tokens], B = V[tokens][channel tile]
         float ar[4];
 #pragma unroll
