@@ -41,12 +41,14 @@ typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 template <int DT> struct Mma;
 template <> struct Mma<1> {
     using v8 = bf16x8;
+    using el = __bf16;
     static __device__ __forceinline__ floatx4 run(v8 a, v8 b, floatx4 c) {
         return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
     }
 };
 template <> struct Mma<0> {
     using v8 = halfx8;
+    using el = _Float16;
     static __device__ __forceinline__ floatx4 run(v8 a, v8 b, floatx4 c) {
         return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
     }
@@ -548,12 +550,19 @@ constexpr int ATTN_NWV = 2;          // waves per attention workgroup
 // block table [SPLIT_BLOCKS] + per-wave class counts, 16-byte multiple
 constexpr int ATTN_HDR_BYTES = (8 * SPLIT_BLOCKS + 2 * 4 * 4 + 15) / 16 * 16;
 
+// x = hi + lo with hi, lo in the MFMA's 16-bit type (round to nearest even);
+// hi + lo carries x to ~16 (bf16) or ~22 (fp16) significant bits
 template <int DT>
-__device__ __forceinline__ typename Mma<DT>::v8 pack8(const uint16_t (&h)[8]) {
-    uint4 u;
-    u.x = h[0] | ((uint32_t)h[1] << 16); u.y = h[2] | ((uint32_t)h[3] << 16);
-    u.z = h[4] | ((uint32_t)h[5] << 16); u.w = h[6] | ((uint32_t)h[7] << 16);
-    return __builtin_bit_cast(typename Mma<DT>::v8, u);
+__device__ __forceinline__ void split8(const float (&x)[8], typename Mma<DT>::v8 &hi, typename Mma<DT>::v8 &lo) {
+    using M8 = typename Mma<DT>::v8;
+    using E = typename Mma<DT>::el;
+    M8 h, l;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = (E)x[i];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) l[i] = (E)(x[i] - (float)h[i]);
+    hi = h;
+    lo = l;
 }
 
 // Expand a packed vector into an LDS tile at base + off: COL = false puts
@@ -751,16 +760,13 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         const float *src = ws.qrot + (uint64_t)p * (ws.qrot_stride / 4) + (uint64_t)qw * D * GP;
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
-            uint16_t hh[8], ll[8];
+            float xs[8];
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const int c = ks * 32 + q4 * 8 + i;
-                const float x = (l16 < G) ? src[c * GP + (l16 < GP ? l16 : 0)] : 0.0f;
-                hh[i] = f2h(x, DT);
-                ll[i] = f2h(x - h2f(hh[i], DT), DT);
+                xs[i] = (l16 < G) ? src[c * GP + (l16 < GP ? l16 : 0)] : 0.0f;
             }
-            qhi[ks] = pack8<DT>(hh);
-            qlo[ks] = pack8<DT>(ll);
+            split8<DT>(xs, qhi[ks], qlo[ks]);
         }
     }
     __syncthreads();
@@ -832,10 +838,14 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
                 a4 = Mma<DT>::run(a, qlo[ks], a4);
             }
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int tt = n * 16 + q4 * 4 + r;
-                z[n][r] = (tt < ntok) ? a4[r] * scale : -INFINITY;
-            }
+            for (int r = 0; r < 4; ++r) z[n][r] = a4[r] * scale;
+        }
+        if (ntok < CH_TOK) {                                  // the split's last chunk
+#pragma unroll
+            for (int n = 0; n < 4; ++n)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (n * 16 + q4 * 4 + r >= ntok) z[n][r] = -INFINITY;
         }
         // ---- online softmax for head l16 (tokens across r, n and the lane quarters)
         float cm = -INFINITY;
@@ -845,14 +855,16 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             for (int r = 0; r < 4; ++r) cm = fmaxf(cm, z[n][r]);
         cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
         cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
+        // every chunk holds a valid token, so mn is finite: exp(-inf - mn) = 0
+        // covers the masked tokens and the first chunk's alpha
         const float mn = fmaxf(m_run, cm);
-        const float alpha = (m_run == -INFINITY) ? 0.0f : __expf(m_run - mn);
+        const float alpha = __expf(m_run - mn);
         float ls = 0.0f;
 #pragma unroll
         for (int n = 0; n < 4; ++n)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                z[n][r] = (z[n][r] == -INFINITY) ? 0.0f : __expf(z[n][r] - mn);
+                z[n][r] = __expf(z[n][r] - mn);
                 ls += z[n][r];
             }
         ls += __shfl_xor(ls, 16, 64);
@@ -873,24 +885,23 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         mem_fence_compiler();
         load_tok<RMAX>(vx, tokg, nxt, true, rmn);
         // ---- P . V on MFMA: A = P[head l16][tokens], B = V[tokens][channel tile]
-        float ar[4];
+        if (!__all(alpha == 1.0f)) {                      // some head's running max moved
+            float ar[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, q4 * 4 + r, 64);
+            for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, q4 * 4 + r, 64);
 #pragma unroll
-        for (int ct = 0; ct < 8; ++ct)
+            for (int ct = 0; ct < 8; ++ct)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) acc_o[ct][r] *= ar[r];
+                for (int r = 0; r < 4; ++r) acc_o[ct][r] *= ar[r];
+        }
         const uint16_t *tv = (const uint16_t *)tile;
 #pragma unroll
         for (int kv = 0; kv < 2; ++kv) {
-            uint16_t hh[8], ll[8];
+            float xs[8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const float x = z[2 * kv + (i >> 2)][i & 3];
-                hh[i] = f2h(x, DT);
-                ll[i] = f2h(x - h2f(hh[i], DT), DT);
-            }
-            const M8 ah = pack8<DT>(hh), al = pack8<DT>(ll);
+            for (int i = 0; i < 8; ++i) xs[i] = z[2 * kv + (i >> 2)][i & 3];
+            M8 ah, al;
+            split8<DT>(xs, ah, al);
 #pragma unroll
             for (int ct = 0; ct < 8; ++ct) {
                 const uint16_t *row = tv + (ct * 16 + l16) * VT_STRIDE + kv * 32 + q4 * 4;
