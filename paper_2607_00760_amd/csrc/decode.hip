@@ -287,21 +287,29 @@ __device__ __forceinline__ void score_walk(const PVec<RMAX> &x, int r, uint32_t 
                 }
             }
             wk.template step<NWD>();
+            if ((k & 3) == 3) __builtin_amdgcn_sched_barrier(0);   // bound the look-ahead
         }
     }
 }
 
-template <int DT, int GP, int RMAX, int L2G>
+// FR: every kept count is 16, 32 or 48 (checked on the host), each with its
+// own fully unrolled walk; otherwise one walk with a runtime trip count.  The
+// two kinds live in different kernels so that the compiler cannot fold the
+// fixed walks into the general one.
+template <int DT, int GP, int RMAX, int L2G, bool FR>
 __device__ __forceinline__ void score_r(const PVec<RMAX> &x, int r, uint32_t qaddr, float (&acc)[GP]) {
-    if (r == 32) score_walk<DT, GP, RMAX, L2G, 32>(x, r, qaddr, acc);
-    else if (r == 16) score_walk<DT, GP, RMAX, L2G, 16>(x, r, qaddr, acc);
-    else if (RMAX >= 48 && r == 48) score_walk<DT, GP, RMAX, L2G, (RMAX >= 48 ? 48 : 0)>(x, r, qaddr, acc);
-    else score_walk<DT, GP, RMAX, L2G, 0>(x, r, qaddr, acc);
+    if (FR) {
+        if (r == 32) score_walk<DT, GP, RMAX, L2G, 32>(x, r, qaddr, acc);
+        else if (r == 16) score_walk<DT, GP, RMAX, L2G, 16>(x, r, qaddr, acc);
+        else score_walk<DT, GP, RMAX, L2G, (RMAX >= 48 ? 48 : 16)>(x, r, qaddr, acc);
+    } else {
+        score_walk<DT, GP, RMAX, L2G, 0>(x, r, qaddr, acc);
+    }
 }
 
 // One pass per distinct (r, log2g) among the active lanes, so that every walk
 // runs with a wave-uniform trip count and no per-step predicate.
-template <int DT, int GP, int RMAX>
+template <int DT, int GP, int RMAX, bool FR>
 __device__ __forceinline__ void score_any(const PVec<RMAX> &x, int r, int l2g, uint32_t qaddr, float (&acc)[GP]) {
     const int key = (r << 2) | l2g;
     uint64_t todo = __ballot(1);
@@ -311,9 +319,9 @@ __device__ __forceinline__ void score_any(const PVec<RMAX> &x, int r, int l2g, u
         todo &= ~__ballot(mine);
         if (mine) {
             const int rv = kv >> 2;
-            if ((kv & 3) == 0) score_r<DT, GP, RMAX, 0>(x, rv, qaddr, acc);
-            else if ((kv & 3) == 1) score_r<DT, GP, RMAX, 1>(x, rv, qaddr, acc);
-            else score_r<DT, GP, RMAX, 2>(x, rv, qaddr, acc);
+            if ((kv & 3) == 0) score_r<DT, GP, RMAX, 0, FR>(x, rv, qaddr, acc);
+            else if ((kv & 3) == 1) score_r<DT, GP, RMAX, 1, FR>(x, rv, qaddr, acc);
+            else score_r<DT, GP, RMAX, 2, FR>(x, rv, qaddr, acc);
         }
     }
 }
@@ -321,7 +329,7 @@ __device__ __forceinline__ void score_any(const PVec<RMAX> &x, int r, int l2g, u
 // grid (ceil(max segments / spw), pairs): a workgroup scores the block keys of
 // spw <= SCORE_SEGS consecutive segments, one lane per block key; spw is at
 // most a rotation window's segments, so a workgroup sees at most two windows.
-template <int DT, int GP, int RMAX>
+template <int DT, int GP, int RMAX, bool FR>
 __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
     __shared__ __align__(16) float qs[2][D * GP];
     __shared__ Desc ds[SCORE_SEGS];
@@ -376,7 +384,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         float acc[GP];
 #pragma unroll
         for (int h = 0; h < GP; ++h) acc[h] = 0.0f;
-        score_any<DT, GP, RMAX>(x, r, l2g, lds_addr(qs) + qoff, acc);
+        score_any<DT, GP, RMAX, FR>(x, r, l2g, lds_addr(qs) + qoff, acc);
         float best = acc[0];
 #pragma unroll
         for (int h = 1; h < GP; ++h)
@@ -592,16 +600,19 @@ __device__ __forceinline__ void scatter_walk(const PVec<RMAX> &x, int r, uint32_
     }
 }
 
-template <int RMAX, int L2G, bool COL>
+template <int RMAX, int L2G, bool COL, bool FR>
 __device__ __forceinline__ void scatter_r(const PVec<RMAX> &x, int r, uint32_t addr) {
-    if (r == 32) scatter_walk<RMAX, L2G, 32, COL>(x, r, addr);
-    else if (r == 16) scatter_walk<RMAX, L2G, 16, COL>(x, r, addr);
-    else if (RMAX >= 48 && r == 48) scatter_walk<RMAX, L2G, (RMAX >= 48 ? 48 : 0), COL>(x, r, addr);
-    else scatter_walk<RMAX, L2G, 0, COL>(x, r, addr);
+    if (FR) {
+        if (r == 32) scatter_walk<RMAX, L2G, 32, COL>(x, r, addr);
+        else if (r == 16) scatter_walk<RMAX, L2G, 16, COL>(x, r, addr);
+        else scatter_walk<RMAX, L2G, (RMAX >= 48 ? 48 : 16), COL>(x, r, addr);
+    } else {
+        scatter_walk<RMAX, L2G, 0, COL>(x, r, addr);
+    }
 }
 
 // called by the lanes that hold a token; one pass per distinct (r, log2g)
-template <int RMAX, bool COL>
+template <int RMAX, bool COL, bool FR>
 __device__ __forceinline__ void scatter_any(const PVec<RMAX> &x, int r, int l2g, uint32_t addr) {
     const int key = (r << 2) | l2g;
     uint64_t todo = __ballot(1);
@@ -611,9 +622,9 @@ __device__ __forceinline__ void scatter_any(const PVec<RMAX> &x, int r, int l2g,
         todo &= ~__ballot(mine);
         if (mine) {
             const int rv = kv >> 2;
-            if ((kv & 3) == 0) scatter_r<RMAX, 0, COL>(x, rv, addr);
-            else if ((kv & 3) == 1) scatter_r<RMAX, 1, COL>(x, rv, addr);
-            else scatter_r<RMAX, 2, COL>(x, rv, addr);
+            if ((kv & 3) == 0) scatter_r<RMAX, 0, COL, FR>(x, rv, addr);
+            else if ((kv & 3) == 1) scatter_r<RMAX, 1, COL, FR>(x, rv, addr);
+            else scatter_r<RMAX, 2, COL, FR>(x, rv, addr);
         }
     }
 }
@@ -638,7 +649,7 @@ __device__ __forceinline__ void load_tok(PVec<RMAX> &x, const uint8_t *tokg, con
     load_pvec<RMAX>(x, b + j * bmb, b + B * bmb + j * 2 * r, rmax, L.a16);
 }
 
-template <int DT, int GP, int RMAX>
+template <int DT, int GP, int RMAX, bool FR>
 __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
 k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     using M8 = typename Mma<DT>::v8;
@@ -821,7 +832,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
         }
         wave_sync();
-        if (cur.valid) scatter_any<RMAX, false>(kx, cur.r(), cur.l2g(), lds_addr(tile) + lane * (KT_STRIDE * 2));
+        if (cur.valid) scatter_any<RMAX, false, FR>(kx, cur.r(), cur.l2g(), lds_addr(tile) + lane * (KT_STRIDE * 2));
         wave_sync();
         mem_fence_compiler();
         load_tok<RMAX>(kx, tokg, nxt, false, rmn);
@@ -880,7 +891,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
         }
         wave_sync();
-        if (cur.valid) scatter_any<RMAX, true>(vx, cur.r(), cur.l2g(), lds_addr(tile) + lane * 2);
+        if (cur.valid) scatter_any<RMAX, true, FR>(vx, cur.r(), cur.l2g(), lds_addr(tile) + lane * 2);
         wave_sync();
         mem_fence_compiler();
         load_tok<RMAX>(vx, tokg, nxt, true, rmn);
@@ -1057,6 +1068,11 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, f
                             int max_desc_used, int max_windows_used, hipStream_t s, hipEvent_t *ev) {
     const int nwq = g.rotated ? max_windows_used : 1;
     const bool small = max_keep(g) <= 48;
+    bool fixed = true;                         // every possible kept count in {16, 32, 48}
+    for (int i = 0; i < 4; ++i) {
+        const int r = i < 3 ? g.keep_cand[i] : g.def_keep;
+        fixed = fixed && (r == 16 || r == 32 || r == 48);
+    }
     if (ev) hipEventRecord(ev[0], s);
     hipLaunchKernelGGL(k_qrot, dim3(nwq * (D / QROT_COLS), g.npairs), dim3(64), 0, s, g, w, q);
     hipError_t e = hipGetLastError();
@@ -1065,8 +1081,9 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, f
     if (max_desc_used > 0) {
         const int spw = max(1, min(SCORE_SEGS, g.W / SEG));
         const dim3 grid(ceil_div(max_desc_used, spw), g.npairs);
-        if (small) hipLaunchKernelGGL((k_score<DT, GP, 48>), grid, dim3(256), 0, s, g, w, spw);
-        else hipLaunchKernelGGL((k_score<DT, GP, 128>), grid, dim3(256), 0, s, g, w, spw);
+        if (fixed) hipLaunchKernelGGL((k_score<DT, GP, 48, true>), grid, dim3(256), 0, s, g, w, spw);
+        else if (small) hipLaunchKernelGGL((k_score<DT, GP, 48, false>), grid, dim3(256), 0, s, g, w, spw);
+        else hipLaunchKernelGGL((k_score<DT, GP, 128, false>), grid, dim3(256), 0, s, g, w, spw);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev) hipEventRecord(ev[2], s);
@@ -1077,8 +1094,9 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, f
     {
         const size_t smem = ATTN_HDR_BYTES + (size_t)ATTN_NWV * TILE_BYTES;
         const dim3 grid(w.max_splits, g.npairs), block(64 * ATTN_NWV);
-        if (small) hipLaunchKernelGGL((k_attn<DT, GP, 48>), grid, block, smem, s, g, w, scale, q);
-        else hipLaunchKernelGGL((k_attn<DT, GP, 128>), grid, block, smem, s, g, w, scale, q);
+        if (fixed) hipLaunchKernelGGL((k_attn<DT, GP, 48, true>), grid, block, smem, s, g, w, scale, q);
+        else if (small) hipLaunchKernelGGL((k_attn<DT, GP, 48, false>), grid, block, smem, s, g, w, scale, q);
+        else hipLaunchKernelGGL((k_attn<DT, GP, 128, false>), grid, block, smem, s, g, w, scale, q);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev) hipEventRecord(ev[4], s);
