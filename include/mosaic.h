@@ -134,7 +134,13 @@ mosaic_status mosaic_workspace_bytes(const mosaic_cache *cache, int32_t op, size
  *   sel   + p * sel_stride   : int32 [max_blocks] selected blocks, ascending
  *   wsel  + p * wsel_stride  : int32 [windows + 2]: first selected entry of
  *                              each window, then k, then the block count
- *   bseg  + p * bseg_stride  : uint32 [max_blocks]: segment << 4 | block in segment */
+ *   part  + p * part_stride  : fp32 [max_splits + windows + 1][GP * (D + 2)]:
+ *                              split-K partials (max, sum, accumulator per head),
+ *                              then one merged slot per window and one for the buffer
+ *   tag   + p * tag_stride   : int32 [max_splits]: window of each split
+ *   bseg  + p * bseg_stride  : uint32 [max_blocks]: segment << 4 | block in segment
+ * Calls that overlap on one workspace race; separate streams need separate
+ * workspaces. */
 typedef struct {
     uint64_t qrot_off, qrot_stride, score_off, score_stride, sel_off, sel_stride, wsel_off, wsel_stride;
     uint64_t part_off, part_stride, tag_off, tag_stride, bseg_off, bseg_stride, total;

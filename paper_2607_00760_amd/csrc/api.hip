@@ -197,8 +197,10 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     wregion(w.qrot_off, w.qrot_stride, (uint64_t)c->nw * D * c->GP * 4);
     wregion(w.score_off, w.score_stride, (uint64_t)c->max_blocks * 4);
     wregion(w.sel_off, w.sel_stride, (uint64_t)c->max_blocks * 4);
+    // wsel: window starts in the selected list, k, block count
     wregion(w.wsel_off, w.wsel_stride, (uint64_t)(c->nw + 2) * 4);
-    wregion(w.part_off, w.part_stride, (uint64_t)c->max_splits * c->GP * (D + 2) * 4);
+    // part: split partials, then one merged slot per window and one for the buffer
+    wregion(w.part_off, w.part_stride, (uint64_t)(c->max_splits + c->nw + 1) * c->GP * (D + 2) * 4);
     wregion(w.tag_off, w.tag_stride, (uint64_t)c->max_splits * 4);
     wregion(w.bseg_off, w.bseg_stride, (uint64_t)c->max_blocks * 4);
     w.total = off;

@@ -425,12 +425,36 @@ __device__ uint32_t block_excl_scan_1024(uint32_t v, uint32_t *s) {
     return base + x - v;
 }
 
+// Exact k-th largest score key by radix selection over the range of the
+// keys: each pass histograms the candidates (keys inside the current range)
+// into 2048 bins of width 2^s, so that the bins spread over the keys that
+// are actually present instead of over fixed bit fields; at most three passes
+// narrow the range to the single threshold key T.  Then the selected list is
+// written in ascending block order: every key > T, and the keys == T with the
+// lowest block indices.
+constexpr int TOPK_BINS = 2048;
+
+__device__ __forceinline__ uint32_t block_reduce_1024(uint32_t v, uint32_t *s, bool take_max) {
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) {
+        const uint32_t y = __shfl_xor(v, m, 64);
+        v = take_max ? max(v, y) : min(v, y);
+    }
+    if (lane == 0) s[wv] = v;
+    __syncthreads();
+    uint32_t r = s[0];
+    for (int i = 1; i < 16; ++i) r = take_max ? max(r, s[i]) : min(r, s[i]);
+    __syncthreads();
+    return r;
+}
+
 __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
     extern __shared__ __align__(16) uint32_t keys[];            // [min(nb, TOPK_LDS_KEYS)] when staged
-    __shared__ uint32_t hist[256];
+    __shared__ uint32_t hist[TOPK_BINS];
     __shared__ uint32_t scan[64];
-    __shared__ uint32_t s_prefix, s_rem;
-    const int p = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+    __shared__ uint32_t s_bin, s_rem;
+    const int p = blockIdx.x, tid = threadIdx.x;
     const PairMeta meta = *g.meta_of(p);
     const int nb = pair_nblocks(g, p, meta);
     int nf, prov, nbuf;
@@ -444,58 +468,53 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
     int32_t *sel = ws.sel + (uint64_t)p * (ws.sel_stride / 4);
     int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
     const bool in_lds = nb <= TOPK_LDS_KEYS;
-    if (in_lds) {
-        for (int i0 = 0; i0 < nb; i0 += 1024 * 8) {
-            float v[8];
+    uint32_t kmin = 0xffffffffu, kmax = 0u;
+    for (int i0 = 0; i0 < nb; i0 += 1024 * 16) {
+        float v[16];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) { const int i = i0 + u * 1024 + tid; v[u] = i < nb ? sc[i] : 0.0f; }
+        for (int u = 0; u < 16; ++u) { const int i = i0 + u * 1024 + tid; v[u] = i < nb ? sc[i] : 0.0f; }
 #pragma unroll
-            for (int u = 0; u < 8; ++u) { const int i = i0 + u * 1024 + tid; if (i < nb) keys[i] = score_key(v[u]); }
+        for (int u = 0; u < 16; ++u) {
+            const int i = i0 + u * 1024 + tid;
+            if (i < nb) {
+                const uint32_t key = score_key(v[u]);
+                if (in_lds) keys[i] = key;
+                kmin = min(kmin, key);
+                kmax = max(kmax, key);
+            }
         }
     }
-    if (tid == 0) { s_prefix = 0; s_rem = (uint32_t)k; }
-    __syncthreads();
-    uint32_t mask = 0;
-    for (int pass = 0; pass < 4 && k > 0; ++pass) {
-        const int shift = 24 - 8 * pass;
-        if (tid < 256) hist[tid] = 0;
+    uint32_t base = block_reduce_1024(kmin, scan, false);
+    uint32_t span = block_reduce_1024(kmax, scan, true) - base;   // candidates: [base, base + span]
+    uint32_t rem = (uint32_t)k;                                    // how many candidates to take
+    while (k > 0) {
+        const int bits = 32 - (span ? __builtin_clz(span) : 32);
+        const int sh = bits > 11 ? bits - 11 : 0;                 // (span >> sh) < 2048
+        for (int i = tid; i < TOPK_BINS; i += 1024) hist[i] = 0;
         __syncthreads();
-        const uint32_t prefix = s_prefix;
         for (int i = tid; i < nb; i += 1024) {
             const uint32_t key = in_lds ? keys[i] : score_key(sc[i]);
-            if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+            const uint32_t d = key - base;
+            if (key >= base && d <= span) atomicAdd(&hist[d >> sh], 1u);
         }
         __syncthreads();
-        if (tid < 64) {
-            // digit d: largest with count(digit >= d) >= rem; lane owns 4 digits, high to low
-            const uint32_t rem = s_rem;
-            uint32_t c4[4], own = 0;
-#pragma unroll
-            for (int u = 0; u < 4; ++u) { c4[u] = hist[255 - (lane * 4 + u)]; own += c4[u]; }
-            uint32_t incl = own;
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const uint32_t y = __shfl_up(incl, off, 64);
-                if (lane >= off) incl += y;
-            }
-            const uint32_t excl = incl - own;
-            if (excl < rem && incl >= rem) {
-                uint32_t cum = excl;
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    if (cum + c4[u] >= rem) {
-                        s_prefix = prefix | ((uint32_t)(255 - (lane * 4 + u)) << shift);
-                        s_rem = rem - cum;
-                        break;
-                    }
-                    cum += c4[u];
-                }
-            }
+        // bins from the top: thread t owns bins 2047 - 2t and 2046 - 2t
+        const uint32_t h0 = hist[TOPK_BINS - 1 - 2 * tid], h1 = hist[TOPK_BINS - 2 - 2 * tid];
+        const uint32_t above = block_excl_scan_1024(h0 + h1, scan);
+        if (above < rem && above + h0 + h1 >= rem) {
+            if (above + h0 >= rem) { s_bin = TOPK_BINS - 1 - 2 * tid; s_rem = rem - above; }
+            else { s_bin = TOPK_BINS - 2 - 2 * tid; s_rem = rem - above - h0; }
         }
-        mask |= 255u << shift;
         __syncthreads();
+        const uint32_t b = s_bin;
+        rem = s_rem;
+        base += b << sh;
+        const uint32_t width = sh ? ((1u << sh) - 1u) : 0u;
+        span = min(span - (b << sh), width);
+        __syncthreads();
+        if (sh == 0) break;
     }
-    const uint32_t T = s_prefix, take_eq_total = s_rem;
+    const uint32_t T = base, take_eq_total = rem;
     const int chunk = (nb + 1023) / 1024;
     const int i0 = min(nb, tid * chunk), i1 = min(nb, i0 + chunk);
     uint32_t gt = 0, eq = 0;
@@ -507,24 +526,40 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
     const uint32_t eq_before = block_excl_scan_1024(eq, scan);
     uint32_t take = 0;
     if (take_eq_total > eq_before) take = min(eq, take_eq_total - eq_before);
-    const uint32_t pos0 = block_excl_scan_1024(gt + take, scan);
-    if (k > 0) {
-        uint32_t pos = pos0, seen = 0;
-        for (int i = i0; i < i1; ++i) {
+    // first block of each rotation window (windows past the last segment start at nb)
+    int *fbw = (int *)hist;
+    const int segs_per_win = g.W / SEG;
+    const Desc *gd = g.desc_of(p);
+    const int nwl = min(g.nw, TOPK_BINS);                  // windows tracked in LDS
+    for (int w = tid; w < nwl; w += 1024) {
+        const int s0 = w * segs_per_win;
+        fbw[w] = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
+    }
+    const uint32_t pos0 = block_excl_scan_1024(gt + take, scan);   // (its barriers publish fbw)
+    // write the selected list; a window starting inside [i0, i1) records the
+    // list position reached there (windows starting at nb record k)
+    int wn = 0;
+    while (wn < nwl && fbw[wn] < i0) ++wn;
+    uint32_t pos = pos0, seen = 0;
+    for (int i = i0; i < i1; ++i) {
+        while (wn < nwl && fbw[wn] == i) wsel[wn++] = (int)pos;
+        if (k > 0) {
             const uint32_t key = in_lds ? keys[i] : score_key(sc[i]);
             if (key > T) sel[pos++] = i;
             else if (key == T && seen < take) { sel[pos++] = i; ++seen; }
         }
     }
-    __syncthreads();
-    const int segs_per_win = g.W / SEG;
-    const Desc *gd = g.desc_of(p);
-    for (int w = tid; w < g.nw; w += 1024) {
-        const int s = w * segs_per_win;
-        const int fb = (s < ndesc) ? (int)gd[s].first_block : nb;
-        int lo = 0, hi = k;
-        while (lo < hi) { const int mid = (lo + hi) >> 1; if (sel[mid] < fb) lo = mid + 1; else hi = mid; }
-        wsel[w] = lo;
+    if (tid == 1023)
+        for (; wn < nwl; ++wn) wsel[wn] = k;
+    if (g.nw > nwl) {                                      // more windows than LDS slots
+        __syncthreads();
+        for (int w = nwl + tid; w < g.nw; w += 1024) {
+            const int s0 = w * segs_per_win;
+            const int fb = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
+            int lo = 0, hi = k;
+            while (lo < hi) { const int mid = (lo + hi) >> 1; if (sel[mid] < fb) lo = mid + 1; else hi = mid; }
+            wsel[w] = lo;
+        }
     }
     if (tid == 0) { wsel[g.nw] = k; wsel[g.nw + 1] = nb; }
 }
@@ -532,13 +567,15 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
 // ------------------------------------------------------------------ attention
 struct BlkInfo { uint32_t goff; uint8_t r, log2g, log2b, pad; };   // 8 bytes
 
-// split s of a pair: window w, selected-list range [e0, e1); w = -2 past the end
-__device__ __forceinline__ void split_of(const int32_t *wsel, int nw, int s, int &w_out, int &e0, int &e1,
+// split s of a pair: window w, selected-list range [e0, e1); w = -2 past the end.
+// The list bounds are clamped to [0, lim] (the list's capacity), so that no
+// workspace content can send an index outside it.
+__device__ __forceinline__ void split_of(const int32_t *wsel, int nw, int s, int lim, int &w_out, int &e0, int &e1,
                                          int &total) {
     int acc = 0;
     w_out = -2; e0 = e1 = 0;
     for (int w = 0; w < nw; ++w) {
-        const int a = wsel[w], b = wsel[w + 1];
+        const int a = min(max(wsel[w], 0), lim), b = min(max(wsel[w + 1], a), lim);
         const int nsp = (b - a + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS;
         if (w_out == -2 && s < acc + nsp) {
             w_out = w;
@@ -669,7 +706,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     const int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
     const int32_t *sel = ws.sel + (uint64_t)p * (ws.sel_stride / 4);
     int w, e0, e1, total;
-    split_of(wsel, g.nw, s, w, e0, e1, total);
+    split_of(wsel, g.nw, s, ws.max_blocks, w, e0, e1, total);
     int32_t *tag = ws.tag + (uint64_t)p * (ws.tag_stride / 4);
     float *part = ws.part + (uint64_t)p * (ws.part_stride / 4) + (uint64_t)s * GP * (D + 2);
     const bool is_buf = (w == -2) && (s == total) && nbuf > 0;
@@ -738,9 +775,10 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     {
         const bool on = tid < nbk;
         uint32_t goff = 0; int r = 0, l2g = 0, l2b = 2;
-        if (on) {
-            const uint32_t bs = ws.bseg[(uint64_t)p * (ws.bseg_stride / 4) + sel[e0 + tid]];
-            const Desc d = g.desc_of(p)[bs >> 4];
+        if (on) {                                   // (indices checked against their arrays)
+            const uint32_t bi = (uint32_t)sel[e0 + tid];
+            const uint32_t bs = bi < (uint32_t)ws.max_blocks ? ws.bseg[(uint64_t)p * (ws.bseg_stride / 4) + bi] : 0u;
+            const Desc d = g.desc_of(p)[min(bs >> 4, (uint32_t)g.max_desc - 1)];
             const int jb = (int)(bs & 15u);
             r = d.r; l2g = d.log2g; l2b = d.log2b;
             goff = d.tok_off + (uint32_t)(jb << l2b) * (uint32_t)(2 * vec_bytes(r, l2g));
@@ -955,106 +993,176 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
 }
 
 // ------------------------------------------------------------------ reduce
-constexpr int REDUCE_MAX_SPLITS = 1024;
+// grid (windows in use + 1, pairs).  Workgroup x < nwu merges the splits of
+// rotation window x (log-sum-exp) and rotates the merged accumulator back by
+// R_v (staged in LDS while the partials load); x == nwu takes the update
+// buffer's split.  Each writes (max, sum, output) per head to a window slot
+// after the split partials; k_merge then combines a pair's window slots into
+// the output (a kernel boundary, rather than a device-wide fence per
+// workgroup, makes the slots visible).
+constexpr int RED_THREADS = 256;
+constexpr int RED_CHUNK = 128;                             // splits per staged chunk
 
 template <int GP>
-__global__ void __launch_bounds__(256) k_reduce(Geom g, WsGeom ws, float *out) {
+__global__ void __launch_bounds__(RED_THREADS) k_reduce(Geom g, WsGeom ws, int nwu) {
     __shared__ __align__(16) float rv[D * D];
     __shared__ float A[GP][D];
-    extern __shared__ __align__(16) float hdr[];            // [nsplit][2 GP + 1]: m, l, tag
-    const int p = blockIdx.x, tid = threadIdx.x, G = g.G;
+    __shared__ float hm[RED_CHUNK][2 * GP];                 // (max, sum) per head of staged splits
+    __shared__ int wbeg[RED_CHUNK + 1];
+    const int x = blockIdx.x, p = blockIdx.y, tid = threadIdx.x;
+    constexpr int PS = GP * (D + 2);                        // floats per partial
+    constexpr int NPT = GP * D / RED_THREADS;               // outputs per thread: (h, j) = i / D, i % D
     const PairMeta meta = *g.meta_of(p);
-    float *o = out + (uint64_t)p * G * D;
-    const int32_t *tag = ws.tag + (uint64_t)p * (ws.tag_stride / 4);
-    const float *part = ws.part + (uint64_t)p * (ws.part_stride / 4);
-    const int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
     int nf, prov, nbuf;
     pair_ndesc(meta, nf, prov, nbuf);
-    int w_, e0_, e1_, total;
-    split_of(wsel, g.nw, 0, w_, e0_, e1_, total);
-    const int nsplit = min(total + (nbuf > 0 ? 1 : 0), REDUCE_MAX_SPLITS);
-    constexpr int HW = 2 * GP + 1;
-    for (int i = tid; i < nsplit * HW; i += 256) {
-        const int s = i / HW, k = i % HW;
-        hdr[i] = (k < 2 * GP) ? part[(uint64_t)s * GP * (D + 2) + k] : __int_as_float(tag[s]);
-    }
-    __syncthreads();
-    constexpr int HPT = GP / 2;                    // heads per thread; thread (half, j)
-    const int j = tid & 127, hb = (tid >> 7) * HPT;
-    float Mg[HPT], Lg[HPT], Og[HPT];
+    int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
+    const float *part = ws.part + (uint64_t)p * (ws.part_stride / 4);
+    float *slot = ws.part + (uint64_t)p * (ws.part_stride / 4) + (uint64_t)(ws.max_splits + x) * PS;
+    const bool buf = x == nwu;
+    const bool rot = !buf && g.rotated;
+    // this workgroup's split range [S0, S1): splits are ordered by window, the
+    // buffer's last.  R_v of the window is staged to LDS meanwhile.
+    int S0 = 0, S1 = 0;
+    {
+        int acc = 0;
+        const int lim = ws.max_blocks;
+        for (int w0 = 0; w0 < g.nw; w0 += RED_CHUNK) {
+            const int n = min(RED_CHUNK, g.nw - w0);
+            __syncthreads();
+            int wv[2];
 #pragma unroll
-    for (int u = 0; u < HPT; ++u) { Mg[u] = -INFINITY; Lg[u] = 0.0f; Og[u] = 0.0f; }
-    for (int w = -1; w < g.nw; ++w) {              // -1 = update buffer
-        // per head: window max and its weights (every thread computes its own heads)
-        float M[HPT];
-        bool any = false;
+            for (int e = 0; e < 2; ++e) wv[e] = (tid + e * RED_THREADS <= n) ? wsel[w0 + tid + e * RED_THREADS] : 0;
+            if (w0 == 0 && rot)
+                stage_copy<RED_THREADS, 16>((uint4 *)rv, (const uint4 *)(g.rot_of(p, x) + 2 * D * D), D * D * 4, tid);
 #pragma unroll
-        for (int u = 0; u < HPT; ++u) M[u] = -INFINITY;
-        for (int s = 0; s < nsplit; ++s) {
-            if (__float_as_int(hdr[s * HW + 2 * GP]) != w) continue;
-            any = true;
-#pragma unroll
-            for (int u = 0; u < HPT; ++u) M[u] = fmaxf(M[u], hdr[s * HW + hb + u]);
-        }
-        if (!any) continue;                         // uniform: the same for every thread
-        const bool rot = (w >= 0) && g.rotated;
-        __syncthreads();
-        if (rot) stage_copy<256, 16>((uint4 *)rv, (const uint4 *)(g.rot_of(p, w) + 2 * D * D), D * D * 4, tid);
-        float Lw[HPT], Aw[HPT];
-#pragma unroll
-        for (int u = 0; u < HPT; ++u) { Lw[u] = 0.0f; Aw[u] = 0.0f; }
-        for (int s0 = 0; s0 < nsplit; s0 += 8) {
-            float av[8][HPT];
-#pragma unroll
-            for (int x = 0; x < 8; ++x) {            // issue the loads of 8 splits together
-                const int s = s0 + x;
-                const bool use = s < nsplit && __float_as_int(hdr[s * HW + 2 * GP]) == w;
-#pragma unroll
-                for (int u = 0; u < HPT; ++u)
-                    av[x][u] = use ? part[(uint64_t)s * GP * (D + 2) + 2 * GP + (hb + u) * D + j] : 0.0f;
+            for (int e = 0; e < 2; ++e) if (tid + e * RED_THREADS <= n) wbeg[tid + e * RED_THREADS] = wv[e];
+            __syncthreads();
+            for (int i = 0; i < n; ++i) {
+                const int a = min(max(wbeg[i], 0), lim), b = min(max(wbeg[i + 1], a), lim);
+                const int nsp = (b - a + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS;
+                if (w0 + i == x) { S0 = acc; S1 = acc + nsp; }
+                acc += nsp;
             }
+        }
+        if (buf) { S0 = acc; S1 = acc + (nbuf > 0 ? 1 : 0); }
+        S0 = min(S0, ws.max_splits);
+        S1 = min(S1, ws.max_splits);
+    }
+    float M[GP], Lw[GP], Aw[NPT];
 #pragma unroll
-            for (int x = 0; x < 8; ++x) {
-                const int s = s0 + x;
-                if (s >= nsplit || __float_as_int(hdr[s * HW + 2 * GP]) != w) continue;
+    for (int h = 0; h < GP; ++h) { M[h] = -INFINITY; Lw[h] = 0.0f; }
 #pragma unroll
-                for (int u = 0; u < HPT; ++u) {
-                    const float m = hdr[s * HW + hb + u];
-                    const float f = (m == -INFINITY) ? 0.0f : __expf(m - M[u]);
-                    Aw[u] += av[x][u] * f;
-                    Lw[u] += hdr[s * HW + GP + hb + u] * f;
+    for (int u = 0; u < NPT; ++u) Aw[u] = 0.0f;
+    // per-head maximum over the splits
+    for (int c0 = S0; c0 < S1; c0 += RED_CHUNK) {
+        const int n = min(RED_CHUNK, S1 - c0);
+        __syncthreads();
+        for (int i = tid; i < n * 2 * GP; i += RED_THREADS)
+            hm[i / (2 * GP)][i % (2 * GP)] = part[(uint64_t)(c0 + i / (2 * GP)) * PS + i % (2 * GP)];
+        __syncthreads();
+        for (int e = 0; e < n; ++e)
+#pragma unroll
+            for (int h = 0; h < GP; ++h) M[h] = fmaxf(M[h], hm[e][h]);
+    }
+    // weighted sums (exp(m_s - M) computed from the staged headers)
+    for (int c0 = S0; c0 < S1; c0 += RED_CHUNK) {
+        const int n = min(RED_CHUNK, S1 - c0);
+        if (S1 - S0 > RED_CHUNK) {                          // more than one chunk: restage
+            __syncthreads();
+            for (int i = tid; i < n * 2 * GP; i += RED_THREADS)
+                hm[i / (2 * GP)][i % (2 * GP)] = part[(uint64_t)(c0 + i / (2 * GP)) * PS + i % (2 * GP)];
+            __syncthreads();
+        }
+        for (int e0 = 0; e0 < n; e0 += 8) {
+            float av[8][NPT];
+#pragma unroll
+            for (int e = 0; e < 8; ++e)                      // issue the loads of 8 splits together
+#pragma unroll
+                for (int u = 0; u < NPT; ++u)
+                    av[e][u] = (e0 + e < n) ? part[(uint64_t)(c0 + e0 + e) * PS + 2 * GP + tid + u * RED_THREADS] : 0.0f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                if (e0 + e >= n) break;
+#pragma unroll
+                for (int u = 0; u < NPT; ++u) {
+                    const int h = (tid + u * RED_THREADS) / D;
+                    const float m = hm[e0 + e][h];
+                    const float f = (m == -INFINITY) ? 0.0f : __expf(m - M[h]);
+                    Aw[u] = fmaf(av[e][u], f, Aw[u]);
+                }
+#pragma unroll
+                for (int h = 0; h < GP; ++h) {
+                    const float m = hm[e0 + e][h];
+                    Lw[h] += (m == -INFINITY) ? 0.0f : hm[e0 + e][GP + h] * __expf(m - M[h]);
                 }
             }
         }
-        float Ow[HPT];
+    }
+#pragma unroll
+    for (int u = 0; u < NPT; ++u) { const int i = tid + u * RED_THREADS; A[i / D][i % D] = Aw[u]; }
+    __syncthreads();
+    // back-rotation x = y . R_v of the window's accumulator
+#pragma unroll
+    for (int u = 0; u < NPT; ++u) {
+        const int i = tid + u * RED_THREADS, h = i / D, j = i % D;
+        float o = A[h][j];
         if (rot) {
-#pragma unroll
-            for (int u = 0; u < HPT; ++u) A[hb + u][j] = Aw[u];
-            __syncthreads();
-#pragma unroll
-            for (int u = 0; u < HPT; ++u) Ow[u] = 0.0f;
-            for (int c = 0; c < D; ++c) {
-                const float r = rv[c * D + j];              // R_v[c][j]: x = y . R
-#pragma unroll
-                for (int u = 0; u < HPT; ++u) Ow[u] = fmaf(A[hb + u][c], r, Ow[u]);
-            }
-        } else {
-#pragma unroll
-            for (int u = 0; u < HPT; ++u) Ow[u] = Aw[u];
+            o = 0.0f;
+#pragma unroll 8
+            for (int c = 0; c < D; ++c) o = fmaf(A[h][c], rv[c * D + j], o);
         }
+        slot[2 * GP + i] = o;
+    }
+    if (tid < GP) { slot[tid] = M[tid]; slot[GP + tid] = Lw[tid]; }
+}
+
+// grid (pairs): online log-sum-exp merge of the window slots (and the buffer's)
+template <int GP>
+__global__ void __launch_bounds__(RED_THREADS) k_merge(Geom g, WsGeom ws, float *out, int nwu) {
+    __shared__ float hm[RED_CHUNK][2 * GP];
+    constexpr int PS = GP * (D + 2);
+    constexpr int NPT = GP * D / RED_THREADS;
+    const int p = blockIdx.x, tid = threadIdx.x, G = g.G;
+    const float *slots = ws.part + (uint64_t)p * (ws.part_stride / 4) + (uint64_t)ws.max_splits * PS;
+    float *o = out + (uint64_t)p * G * D;
+    float num[NPT], den[NPT], Mx[NPT];
 #pragma unroll
-        for (int u = 0; u < HPT; ++u) {
-            if (M[u] == -INFINITY) continue;
-            const float mn = fmaxf(Mg[u], M[u]);
-            const float a = (Mg[u] == -INFINITY) ? 0.0f : __expf(Mg[u] - mn), b = __expf(M[u] - mn);
-            Og[u] = Og[u] * a + Ow[u] * b;
-            Lg[u] = Lg[u] * a + Lw[u] * b;
-            Mg[u] = mn;
+    for (int u = 0; u < NPT; ++u) { num[u] = 0.0f; den[u] = 0.0f; Mx[u] = -INFINITY; }
+    for (int y0 = 0; y0 <= nwu; y0 += RED_CHUNK) {
+        const int n = min(RED_CHUNK, nwu + 1 - y0);
+        float v[8][NPT];
+        __syncthreads();
+        for (int i = tid; i < n * 2 * GP; i += RED_THREADS)
+            hm[i / (2 * GP)][i % (2 * GP)] = slots[(uint64_t)(y0 + i / (2 * GP)) * PS + i % (2 * GP)];
+        __syncthreads();
+        for (int e0 = 0; e0 < n; e0 += 8) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+#pragma unroll
+                for (int u = 0; u < NPT; ++u)
+                    v[e][u] = (e0 + e < n) ? slots[(uint64_t)(y0 + e0 + e) * PS + 2 * GP + tid + u * RED_THREADS] : 0.0f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                if (e0 + e >= n) break;
+#pragma unroll
+                for (int u = 0; u < NPT; ++u) {
+                    const int h = (tid + u * RED_THREADS) / D;
+                    const float m = hm[e0 + e][h];
+                    if (m == -INFINITY) continue;
+                    const float mn = fmaxf(Mx[u], m);
+                    const float a = __expf(Mx[u] - mn), b = __expf(m - mn);
+                    num[u] = num[u] * a + v[e][u] * b;
+                    den[u] = den[u] * a + hm[e0 + e][GP + h] * b;
+                    Mx[u] = mn;
+                }
+            }
         }
     }
 #pragma unroll
-    for (int u = 0; u < HPT; ++u)
-        if (hb + u < G) o[(hb + u) * D + j] = (Lg[u] > 0.0f) ? Og[u] / Lg[u] : 0.0f;
+    for (int u = 0; u < NPT; ++u) {
+        const int i = tid + u * RED_THREADS;
+        if (i / D < G) o[i] = (den[u] > 0.0f) ? num[u] / den[u] : 0.0f;
+    }
 }
 
 int max_keep(const Geom &g) {
@@ -1100,8 +1208,10 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, f
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev) hipEventRecord(ev[4], s);
-    const size_t red_smem = (size_t)min(w.max_splits, REDUCE_MAX_SPLITS) * (2 * GP + 1) * 4;
-    hipLaunchKernelGGL(k_reduce<GP>, dim3(g.npairs), dim3(256), red_smem, s, g, w, out);
+    hipLaunchKernelGGL(k_reduce<GP>, dim3(max_windows_used + 1, g.npairs), dim3(RED_THREADS), 0, s, g, w,
+                       max_windows_used);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_merge<GP>, dim3(g.npairs), dim3(RED_THREADS), 0, s, g, w, out, max_windows_used);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev) hipEventRecord(ev[5], s);
     return hipSuccess;
