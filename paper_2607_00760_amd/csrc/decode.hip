@@ -252,11 +252,16 @@ __device__ __forceinline__ void load_pvec(PVec<RMAX> &x, const uint8_t *bm, cons
     }
 }
 
-// maximum over the wave (every lane active)
+// maximum over the wave of 0 <= v < 256 (every lane active): eight ballots,
+// no cross-lane data movement
 __device__ __forceinline__ int wave_max_i(int v) {
+    int m = 0;
 #pragma unroll
-    for (int m = 1; m < 64; m <<= 1) v = max(v, __shfl_xor(v, m, 64));
-    return __builtin_amdgcn_readfirstlane(v);
+    for (int b = 7; b >= 0; --b) {
+        const int c = m | (1 << b);
+        if (__ballot(v >= c)) m = c;
+    }
+    return m;
 }
 
 // ------------------------------------------------------------------ score
@@ -399,30 +404,57 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
 
 // ------------------------------------------------------------------ topk
 constexpr int TOPK_LDS_KEYS = 32768;
+constexpr int TOPK_BINS = 2048;
+constexpr int TOPK_KPT = 16;                               // keys per thread held in registers
 
-__device__ uint32_t block_excl_scan_1024(uint32_t v, uint32_t *s) {
+// wave-level inclusive scans on the data-parallel-primitive lane shifts (no
+// LDS round trips): shifts by 1, 2, 4, 8 inside each 16-lane row, then the
+// row broadcasts of lanes 15 and 31
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_u(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, 0xf, false);
+}
+__device__ __forceinline__ uint32_t wave_scan_add(uint32_t x) {
+    x += dpp_u<0x111, 0xf>(x);
+    x += dpp_u<0x112, 0xf>(x);
+    x += dpp_u<0x114, 0xf>(x);
+    x += dpp_u<0x118, 0xf>(x);
+    x += dpp_u<0x142, 0xa>(x);
+    x += dpp_u<0x143, 0xc>(x);
+    return x;
+}
+// maximum over the wave (every lane active); lanes that read out of range get 0
+__device__ __forceinline__ uint32_t wave_max_u(uint32_t x) {
+    x = max(x, dpp_u<0x111, 0xf>(x));
+    x = max(x, dpp_u<0x112, 0xf>(x));
+    x = max(x, dpp_u<0x114, 0xf>(x));
+    x = max(x, dpp_u<0x118, 0xf>(x));
+    x = max(x, dpp_u<0x142, 0xa>(x));
+    x = max(x, dpp_u<0x143, 0xc>(x));
+    return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+
+// exclusive prefix sum over the 1024 threads of the block; s: 16 words of LDS
+__device__ __forceinline__ uint32_t block_excl_scan_1024(uint32_t v, uint32_t *s) {
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    uint32_t x = v;                                      // inclusive wave scan
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t y = __shfl_up(x, off, 64);
-        if (lane >= off) x += y;
-    }
+    const uint32_t x = wave_scan_add(v);
     if (lane == 63) s[wv] = x;
     __syncthreads();
-    if (tid < 16) {
-        uint32_t t = s[tid];
-#pragma unroll
-        for (int off = 1; off < 16; off <<= 1) {
-            const uint32_t y = __shfl_up(t, off, 64);
-            if (tid >= off) t += y;
-        }
-        s[16 + tid] = t;
-    }
-    __syncthreads();
-    const uint32_t base = wv ? s[16 + wv - 1] : 0u;
+    uint32_t base = 0;
+    for (int i = 0; i < wv; ++i) base += s[i];
     __syncthreads();
     return base + x - v;
+}
+
+// block-wide minimum of lo and maximum of hi (1024 threads); s: 32 words
+__device__ __forceinline__ void block_minmax_1024(uint32_t &lo, uint32_t &hi, uint32_t *s) {
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const uint32_t l = ~wave_max_u(~lo), h = wave_max_u(hi);
+    if (lane == 0) { s[wv] = l; s[16 + wv] = h; }
+    __syncthreads();
+    lo = s[0]; hi = s[16];
+    for (int i = 1; i < 16; ++i) { lo = min(lo, s[i]); hi = max(hi, s[16 + i]); }
+    __syncthreads();
 }
 
 // Exact k-th largest score key by radix selection over the range of the
@@ -431,83 +463,77 @@ __device__ uint32_t block_excl_scan_1024(uint32_t v, uint32_t *s) {
 // are actually present instead of over fixed bit fields; at most three passes
 // narrow the range to the single threshold key T.  Then the selected list is
 // written in ascending block order: every key > T, and the keys == T with the
-// lowest block indices.
-constexpr int TOPK_BINS = 2048;
-
-__device__ __forceinline__ uint32_t block_reduce_1024(uint32_t v, uint32_t *s, bool take_max) {
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-#pragma unroll
-    for (int m = 1; m < 64; m <<= 1) {
-        const uint32_t y = __shfl_xor(v, m, 64);
-        v = take_max ? max(v, y) : min(v, y);
-    }
-    if (lane == 0) s[wv] = v;
-    __syncthreads();
-    uint32_t r = s[0];
-    for (int i = 1; i < 16; ++i) r = take_max ? max(r, s[i]) : min(r, s[i]);
-    __syncthreads();
-    return r;
-}
-
-__global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
-    extern __shared__ __align__(16) uint32_t keys[];            // [min(nb, TOPK_LDS_KEYS)] when staged
-    __shared__ uint32_t hist[TOPK_BINS];
-    __shared__ uint32_t scan[64];
-    __shared__ uint32_t s_bin, s_rem;
-    const int p = blockIdx.x, tid = threadIdx.x;
-    const PairMeta meta = *g.meta_of(p);
-    const int nb = pair_nblocks(g, p, meta);
-    int nf, prov, nbuf;
-    const int ndesc = pair_ndesc(meta, nf, prov, nbuf);
-    int k = 0;
-    if (nb > 0) {
-        const long long kk = ((long long)nb * g.sel_num + g.sel_den - 1) / g.sel_den;
-        k = (int)(kk < 1 ? 1 : (kk > nb ? nb : kk));
-    }
+// lowest block indices.  Thread t owns the keys [t * chunk, (t + 1) * chunk);
+// with REG (chunk <= 16) they stay in registers, else they are read from LDS
+// (or from the score array when they do not fit).
+template <bool REG>
+__device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p, int nb, int ndesc, int k,
+                                          uint32_t *keys, uint32_t *hist, uint32_t *sbuf) {
+    const int tid = threadIdx.x;
     const float *sc = ws.score + (uint64_t)p * (ws.score_stride / 4);
     int32_t *sel = ws.sel + (uint64_t)p * (ws.sel_stride / 4);
     int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
+    const int chunk = REG ? TOPK_KPT : (nb + 1023) / 1024;
+    const int i0 = min(nb, tid * chunk), i1 = min(nb, i0 + chunk), n_own = i1 - i0;
     const bool in_lds = nb <= TOPK_LDS_KEYS;
+    uint32_t kr[REG ? TOPK_KPT : 1];
     uint32_t kmin = 0xffffffffu, kmax = 0u;
-    for (int i0 = 0; i0 < nb; i0 += 1024 * 16) {
-        float v[16];
+    if (REG) {
+        const float4 *s4 = (const float4 *)(sc + i0);
 #pragma unroll
-        for (int u = 0; u < 16; ++u) { const int i = i0 + u * 1024 + tid; v[u] = i < nb ? sc[i] : 0.0f; }
+        for (int q = 0; q < TOPK_KPT / 4; ++q) {
+            float4 f = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            if (4 * q < n_own) f = s4[q];
+            const float fv[4] = {f.x, f.y, f.z, f.w};
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-            const int i = i0 + u * 1024 + tid;
-            if (i < nb) {
-                const uint32_t key = score_key(v[u]);
-                if (in_lds) keys[i] = key;
-                kmin = min(kmin, key);
-                kmax = max(kmax, key);
-            }
+            for (int e = 0; e < 4; ++e) kr[4 * q + e] = score_key(fv[e]);
+        }
+#pragma unroll
+        for (int j = 0; j < TOPK_KPT; ++j)
+            if (j < n_own) { kmin = min(kmin, kr[j]); kmax = max(kmax, kr[j]); }
+    } else {
+        for (int i = i0; i < i1; ++i) {
+            const uint32_t key = score_key(sc[i]);
+            if (in_lds) keys[i] = key;
+            kmin = min(kmin, key);
+            kmax = max(kmax, key);
         }
     }
-    uint32_t base = block_reduce_1024(kmin, scan, false);
-    uint32_t span = block_reduce_1024(kmax, scan, true) - base;   // candidates: [base, base + span]
+    auto key_at = [&](int j) -> uint32_t {                 // j-th owned key (j < n_own)
+        if (REG) return kr[j];
+        return in_lds ? keys[i0 + j] : score_key(sc[i0 + j]);
+    };
+    block_minmax_1024(kmin, kmax, sbuf);
+    uint32_t base = kmin, span = kmax - kmin;                     // candidates: [base, base + span]
     uint32_t rem = (uint32_t)k;                                    // how many candidates to take
     while (k > 0) {
         const int bits = 32 - (span ? __builtin_clz(span) : 32);
         const int sh = bits > 11 ? bits - 11 : 0;                 // (span >> sh) < 2048
         for (int i = tid; i < TOPK_BINS; i += 1024) hist[i] = 0;
         __syncthreads();
-        for (int i = tid; i < nb; i += 1024) {
-            const uint32_t key = in_lds ? keys[i] : score_key(sc[i]);
-            const uint32_t d = key - base;
-            if (key >= base && d <= span) atomicAdd(&hist[d >> sh], 1u);
+        if (REG) {
+#pragma unroll
+            for (int j = 0; j < TOPK_KPT; ++j) {
+                const uint32_t d = kr[j] - base;
+                if (j < n_own && kr[j] >= base && d <= span) atomicAdd(&hist[d >> sh], 1u);
+            }
+        } else {
+            for (int j = 0; j < n_own; ++j) {
+                const uint32_t key = key_at(j), d = key - base;
+                if (key >= base && d <= span) atomicAdd(&hist[d >> sh], 1u);
+            }
         }
         __syncthreads();
         // bins from the top: thread t owns bins 2047 - 2t and 2046 - 2t
         const uint32_t h0 = hist[TOPK_BINS - 1 - 2 * tid], h1 = hist[TOPK_BINS - 2 - 2 * tid];
-        const uint32_t above = block_excl_scan_1024(h0 + h1, scan);
+        const uint32_t above = block_excl_scan_1024(h0 + h1, sbuf);
         if (above < rem && above + h0 + h1 >= rem) {
-            if (above + h0 >= rem) { s_bin = TOPK_BINS - 1 - 2 * tid; s_rem = rem - above; }
-            else { s_bin = TOPK_BINS - 2 - 2 * tid; s_rem = rem - above - h0; }
+            if (above + h0 >= rem) { sbuf[32] = TOPK_BINS - 1 - 2 * tid; sbuf[33] = rem - above; }
+            else { sbuf[32] = TOPK_BINS - 2 - 2 * tid; sbuf[33] = rem - above - h0; }
         }
         __syncthreads();
-        const uint32_t b = s_bin;
-        rem = s_rem;
+        const uint32_t b = sbuf[32];
+        rem = sbuf[33];
         base += b << sh;
         const uint32_t width = sh ? ((1u << sh) - 1u) : 0u;
         span = min(span - (b << sh), width);
@@ -515,15 +541,17 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
         if (sh == 0) break;
     }
     const uint32_t T = base, take_eq_total = rem;
-    const int chunk = (nb + 1023) / 1024;
-    const int i0 = min(nb, tid * chunk), i1 = min(nb, i0 + chunk);
     uint32_t gt = 0, eq = 0;
-    if (k > 0)
-        for (int i = i0; i < i1; ++i) {
-            const uint32_t key = in_lds ? keys[i] : score_key(sc[i]);
-            gt += key > T; eq += key == T;
+    if (k > 0) {
+        if (REG) {
+#pragma unroll
+            for (int j = 0; j < TOPK_KPT; ++j)
+                if (j < n_own) { gt += kr[j] > T; eq += kr[j] == T; }
+        } else {
+            for (int j = 0; j < n_own; ++j) { const uint32_t key = key_at(j); gt += key > T; eq += key == T; }
         }
-    const uint32_t eq_before = block_excl_scan_1024(eq, scan);
+    }
+    const uint32_t eq_before = block_excl_scan_1024(eq, sbuf);
     uint32_t take = 0;
     if (take_eq_total > eq_before) take = min(eq, take_eq_total - eq_before);
     // first block of each rotation window (windows past the last segment start at nb)
@@ -535,19 +563,28 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
         const int s0 = w * segs_per_win;
         fbw[w] = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
     }
-    const uint32_t pos0 = block_excl_scan_1024(gt + take, scan);   // (its barriers publish fbw)
+    const uint32_t pos0 = block_excl_scan_1024(gt + take, sbuf);   // (its barriers publish fbw)
     // write the selected list; a window starting inside [i0, i1) records the
     // list position reached there (windows starting at nb record k)
     int wn = 0;
     while (wn < nwl && fbw[wn] < i0) ++wn;
     uint32_t pos = pos0, seen = 0;
-    for (int i = i0; i < i1; ++i) {
+    auto emit = [&](int j, uint32_t key) {
+        const int i = i0 + j;
         while (wn < nwl && fbw[wn] == i) wsel[wn++] = (int)pos;
         if (k > 0) {
-            const uint32_t key = in_lds ? keys[i] : score_key(sc[i]);
-            if (key > T) sel[pos++] = i;
-            else if (key == T && seen < take) { sel[pos++] = i; ++seen; }
+            const bool take_it = key > T || (key == T && seen < take);
+            seen += (key == T && take_it) ? 1u : 0u;
+            if (take_it && pos < (uint32_t)nb) sel[pos] = i;
+            pos += take_it ? 1u : 0u;
         }
+    };
+    if (REG) {
+#pragma unroll
+        for (int j = 0; j < TOPK_KPT; ++j)
+            if (j < n_own) emit(j, kr[j]);
+    } else {
+        for (int j = 0; j < n_own; ++j) emit(j, key_at(j));
     }
     if (tid == 1023)
         for (; wn < nwl; ++wn) wsel[wn] = k;
@@ -564,8 +601,28 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
     if (tid == 0) { wsel[g.nw] = k; wsel[g.nw + 1] = nb; }
 }
 
+__global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
+    extern __shared__ __align__(16) uint32_t keys[];            // [min(nb, TOPK_LDS_KEYS)] when staged
+    __shared__ uint32_t hist[TOPK_BINS];
+    __shared__ uint32_t sbuf[64];
+    const int p = blockIdx.x;
+    const PairMeta meta = *g.meta_of(p);
+    const int nb = pair_nblocks(g, p, meta);
+    int nf, prov, nbuf;
+    const int ndesc = pair_ndesc(meta, nf, prov, nbuf);
+    int k = 0;
+    if (nb > 0) {
+        const long long kk = ((long long)nb * g.sel_num + g.sel_den - 1) / g.sel_den;
+        k = (int)(kk < 1 ? 1 : (kk > nb ? nb : kk));
+    }
+    if (nb <= 1024 * TOPK_KPT) topk_body<true>(g, ws, p, nb, ndesc, k, keys, hist, sbuf);
+    else topk_body<false>(g, ws, p, nb, ndesc, k, keys, hist, sbuf);
+}
+
 // ------------------------------------------------------------------ attention
-struct BlkInfo { uint32_t goff; uint8_t r, log2g, log2b, pad; };   // 8 bytes
+// a selected block in the attention kernel's LDS table: byte offset in the
+// pair's token arena, and r << 8 | log2g << 16 | log2b << 20
+typedef uint2 BlkInfo;
 
 // split s of a pair: window w, selected-list range [e0, e1); w = -2 past the end.
 // The list bounds are clamped to [0, lim] (the list's capacity), so that no
@@ -797,9 +854,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             const int base = cls == 0 ? 0 : (cls == 1 ? c16 : c16 + c8);
             const uint64_t mc = cls == 0 ? m0 : (cls == 1 ? m1 : m2);
             const int pos = base + (wave ? wcnt[cls] : 0) + __popcll(mc & below);
-            BlkInfo bi;
-            bi.goff = goff; bi.r = (uint8_t)r; bi.log2g = (uint8_t)l2g; bi.log2b = (uint8_t)l2b; bi.pad = 0;
-            blk[pos] = bi;
+            blk[pos] = make_uint2(goff, ((uint32_t)r << 8) | ((uint32_t)l2g << 16) | ((uint32_t)l2b << 20));
         }
     }
     // q operand: B[k = channel][n = head] of the logits K . q^T, split hi + lo
@@ -838,10 +893,9 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         else { bi = n16 + n8 + ((t - T8) >> 2); j = (t - T8) & 3; }
         if (!L.valid) { bi = 0; j = 0; }
         const BlkInfo b = blk[bi];
-        L.base = b.goff;
-        L.info = (uint32_t)j | ((uint32_t)(L.valid ? b.r : 0) << 8) | ((uint32_t)b.log2g << 16) |
-                 ((uint32_t)b.log2b << 20);
-        L.a16 = __all(!L.valid || (b.log2g == 0 && (b.r & 7) == 0 && (b.goff & 15u) == 0));
+        L.base = b.x;
+        L.info = (uint32_t)j | (L.valid ? b.y : (b.y & ~0xff00u));
+        L.a16 = __all(!L.valid || ((b.y & 0xf0700u) == 0 && (b.x & 15u) == 0));   // log2g 0, r % 8 == 0
         return L;
     };
 
