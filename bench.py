@@ -45,6 +45,7 @@ def parse():
     ap.add_argument("--cpu-sample-pairs", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-graph", action="store_true")
     return ap.parse_args()
 
 
@@ -154,22 +155,64 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    step_ms, kern = [], {k: [] for k in M.MosaicCache.KERNELS}
+    # the timed steps: plain library calls, no per-kernel events between them
+    cache.set_timing(False)
+    step_ms = []
     torch.cuda.synchronize()
     w0 = time.time()
     for _ in range(args.steps):
         a, b = step()
-        kt = cache.decode_timing()           # waits for this step's kernels
         b.synchronize()
         step_ms.append(a.elapsed_time(b))
+    torch.cuda.synchronize()
+    wall = time.time() - w0
+    ms = float(np.mean(step_ms))
+    log(f"decode {1e3 * ms:.1f} us/step over {args.steps} steps")
+    ref_out = out.clone()
+    # per-kernel durations: the same steps again with events on the launch stream
+    cache.set_timing(True)
+    kern = {k: [] for k in M.MosaicCache.KERNELS}
+    for _ in range(args.steps):
+        a, b = step()
+        kt = cache.decode_timing()           # waits for this step's kernels
         for k, v in kt.items():
             kern[k].append(v)
     torch.cuda.synchronize()
-    wall = time.time() - w0
     cache.set_timing(False)
-    ms = float(np.mean(step_ms))
-    log(f"decode {1e3 * ms:.1f} us/step over {args.steps} steps")
     kern_us = {k: 1e3 * float(np.mean(v)) for k, v in kern.items()}
+    # the same call captured once into a HIP graph and replayed (every replay is
+    # checked against the eager output)
+    graph_us = None
+    if not args.no_graph:
+        gs = torch.cuda.Stream()
+        gs.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(gs):
+            cache.decode(q, scale, out=out)
+        torch.cuda.current_stream().wait_stream(gs)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            cache.decode(q, scale, out=out)
+        torch.cuda.synchronize()
+        gms, same = [], True
+        for i in range(args.steps + 1):
+            evict()
+            out.zero_()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            graph.replay()
+            b.record()
+            b.synchronize()
+            same &= bool(torch.equal(out, ref_out))
+            if i:
+                gms.append(a.elapsed_time(b))
+        if same:
+            graph_us = 1e3 * float(np.mean(gms))
+            log(f"graph replay {graph_us:.1f} us/step")
+        else:
+            log("graph replay output differs from the eager call; not reported")
+        del graph
+        out.copy_(ref_out)
 
     # algorithmic bytes from the cache's own descriptors and selections
     lay_c, wsl = cache.layout, cache.ws_layout
@@ -290,6 +333,7 @@ def main():
         "effective_gbps": round(ab["total"] / (ms * 1e-3) / 1e9, 1),
         "algorithmic_bytes_per_step": ab,
         "kernels_us": {k: round(v, 3) for k, v in kern_us.items()},
+        "graph_replay_us_per_step": None if graph_us is None else round(graph_us, 3),
         "dense_us_per_step": None if dense_us is None else round(dense_us, 2),
         "speedup_vs_dense": None if dense_us is None else round(dense_us / value, 2),
         "wall_ms_per_step_incl_flush": round(1e3 * wall / args.steps, 3),

@@ -228,19 +228,47 @@ struct PVec {
 
 // bm and val point at the vector's bitmap and values; rmax is the largest r
 // in the wave (uniform) and a16 (uniform) says both pointers are 16-byte
-// aligned.  The loads take a fixed 16-byte bitmap and rmax values: what lies
-// past a vector's own bitmap or values is read (inside the arena's slack) and
-// never used.
-template <int RMAX>
+// aligned (A16: always so).  The loads take a fixed 16-byte bitmap and rmax
+// values: what lies past a vector's own bitmap or values is read (inside the
+// arena's slack) and never used.  Value slots at or past rmax keep what they
+// held: a walk reads only its first r slots, and leaving them unwritten keeps
+// the registers of earlier, still outstanding loads free of write-after-write
+// waits.
+//
+// A16: 1 = the pointers are known 16-byte aligned, 0 = dword loads, -1 = chosen
+// by a16 at run time.  ZF zero-fills the slots past rmax.  Without it every
+// slot is loaded, those past rmax from the start of the values again (lines
+// the wave reads anyway): straight-line loads with no branch, so that a
+// prefetch into loop-carried registers leaves no join whose bookkeeping would
+// make the wave wait on loads that are still in flight.
+//
+// RL > 0 (with A16 = 1): exactly the first RL 16-byte granules of values, with
+// no condition (the caller knows r <= 8 RL for every lane of the wave).
+template <int RMAX, int A16, bool ZF, int RL = 0>
 __device__ __forceinline__ void load_pvec(PVec<RMAX> &x, const uint8_t *bm, const uint8_t *val, int rmax, bool a16) {
-    if (a16) {
+    static_assert(RL == 0 || (A16 == 1 && RL <= RMAX / 8), "fixed granule count needs aligned records");
+    if (RL > 0) {
+        const uint4 b = *(const uint4 *)bm;
+        x.bw[0] = b.x; x.bw[1] = b.y; x.bw[2] = b.z; x.bw[3] = b.w;
+        const uint4 *v4 = (const uint4 *)val;
+#pragma unroll
+        for (int k = 0; k < RL; ++k) {
+            const uint4 t = v4[k];
+            x.v[4 * k] = t.x; x.v[4 * k + 1] = t.y; x.v[4 * k + 2] = t.z; x.v[4 * k + 3] = t.w;
+        }
+    } else if (A16 == 1 || (A16 == -1 && a16)) {
         const uint4 b = *(const uint4 *)bm;
         x.bw[0] = b.x; x.bw[1] = b.y; x.bw[2] = b.z; x.bw[3] = b.w;
         const uint4 *v4 = (const uint4 *)val;
 #pragma unroll
         for (int k = 0; k < RMAX / 8; ++k) {
-            uint4 t = make_uint4(0u, 0u, 0u, 0u);
-            if (8 * k < rmax) t = v4[k];
+            uint4 t;
+            if (ZF) {
+                t = make_uint4(0u, 0u, 0u, 0u);
+                if (8 * k < rmax) t = v4[k];
+            } else {
+                t = v4[(8 * k < rmax) ? k : 0];
+            }
             x.v[4 * k] = t.x; x.v[4 * k + 1] = t.y; x.v[4 * k + 2] = t.z; x.v[4 * k + 3] = t.w;
         }
     } else {
@@ -248,7 +276,10 @@ __device__ __forceinline__ void load_pvec(PVec<RMAX> &x, const uint8_t *bm, cons
 #pragma unroll
         for (int k = 0; k < 4; ++k) x.bw[k] = b[k];
 #pragma unroll
-        for (int k = 0; k < RMAX / 2; ++k) x.v[k] = (2 * k < rmax) ? v[k] : 0u;
+        for (int k = 0; k < RMAX / 2; ++k) {
+            if (ZF) x.v[k] = (2 * k < rmax) ? v[k] : 0u;
+            else x.v[k] = v[(2 * k < rmax) ? k : 0];
+        }
     }
 }
 
@@ -263,6 +294,8 @@ __device__ __forceinline__ int wave_max_i(int v) {
     }
     return m;
 }
+
+template <int V> struct IntC { static constexpr int value = V; };
 
 // ------------------------------------------------------------------ score
 // One walk: acc[h] += q[c][h] * value over the kept channels c, ascending.
@@ -385,7 +418,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         const uint32_t qoff = (g.rotated && ((s0 + i) * SEG) / g.W != w0) ? D * GP * 4 : 0;
         const bool a16 = __all(!valid || (l2g == 0 && ((uintptr_t)rec & 15u) == 0));
         PVec<RMAX> x;
-        load_pvec<RMAX>(x, rec, rec + (16 >> l2g), wave_max_i(r), a16);
+        load_pvec<RMAX, -1, true>(x, rec, rec + (16 >> l2g), wave_max_i(r), a16);
         float acc[GP];
 #pragma unroll
         for (int h = 0; h < GP; ++h) acc[h] = 0.0f;
@@ -727,7 +760,7 @@ __device__ __forceinline__ void scatter_any(const PVec<RMAX> &x, int r, int l2g,
 // pair's token arena and (token in block, r, log2g, log2b) packed in a word
 struct TokLoc {
     uint32_t base, info;
-    bool valid, a16;
+    bool valid;
     __device__ __forceinline__ int j() const { return info & 0xff; }
     __device__ __forceinline__ int r() const { return (info >> 8) & 0xff; }
     __device__ __forceinline__ int l2g() const { return (info >> 16) & 0xf; }
@@ -735,12 +768,12 @@ struct TokLoc {
 };
 
 // load the packed K (V when V_ is set) vector of a located token
-template <int RMAX>
+template <int RMAX, int RL>
 __device__ __forceinline__ void load_tok(PVec<RMAX> &x, const uint8_t *tokg, const TokLoc &L, bool V_, int rmax) {
     const int r = L.r(), l2g = L.l2g(), B = 1 << L.l2b(), bmb = 16 >> l2g, j = L.j();
     const uint32_t half = V_ ? (uint32_t)(B * (bmb + 2 * r)) : 0u;
     const uint8_t *b = tokg + L.base + half;
-    load_pvec<RMAX>(x, b + j * bmb, b + B * bmb + j * 2 * r, rmax, L.a16);
+    load_pvec<RMAX, RL ? 1 : 0, false, RL>(x, b + j * bmb, b + B * bmb + j * 2 * r, rmax, false);
 }
 
 template <int DT, int GP, int RMAX, bool FR>
@@ -829,6 +862,8 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     // (16, then 8, then 4; ascending index inside a size), so every block
     // starts at a multiple of its size and none straddles a 64-token chunk
     const int nbk = e1 - e0;
+    bool all16;                                     // every record of the split 16-byte aligned
+    int rsplit;                                     // largest kept count in the split
     {
         const bool on = tid < nbk;
         uint32_t goff = 0; int r = 0, l2g = 0, l2b = 2;
@@ -847,7 +882,11 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             wcnt[wave * 4 + 1] = __popcll(m1);
             wcnt[wave * 4 + 2] = __popcll(m2);
         }
-        __syncthreads();
+        const int rw = wave_max_i(on ? r : 0);
+        if (lane == 0) wcnt[wave * 4 + 3] = rw;
+        // one channel per group, r % 8 == 0 and an aligned block: 16-byte
+        // bitmaps and 2r-byte value runs at 16-byte offsets
+        all16 = __syncthreads_and(!on || (l2g == 0 && (r & 7) == 0 && (goff & 15u) == 0));
         if (on) {
             const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
             const int c16 = wcnt[0] + wcnt[4], c8 = wcnt[1] + wcnt[5];
@@ -878,6 +917,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     const int n16 = __builtin_amdgcn_readfirstlane(wcnt[0] + wcnt[4]);
     const int n8 = __builtin_amdgcn_readfirstlane(wcnt[1] + wcnt[5]);
     const int n4 = __builtin_amdgcn_readfirstlane(wcnt[2] + wcnt[6]);
+    rsplit = __builtin_amdgcn_readfirstlane(max(wcnt[3], wcnt[7]));
     const int T16 = 16 * n16, T8 = T16 + 8 * n8, T = T8 + 4 * n4;
     const int nch = (T + CH_TOK - 1) / CH_TOK;
     const uint8_t *tokg = g.tok_of(p);
@@ -895,7 +935,6 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         const BlkInfo b = blk[bi];
         L.base = b.x;
         L.info = (uint32_t)j | (L.valid ? b.y : (b.y & ~0xff00u));
-        L.a16 = __all(!L.valid || ((b.y & 0xf0700u) == 0 && (b.x & 15u) == 0));   // log2g 0, r % 8 == 0
         return L;
     };
 
@@ -904,120 +943,133 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
 #pragma unroll
     for (int ct = 0; ct < 8; ++ct) acc_o[ct] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
 
-    int c = wave;
-    TokLoc cur = locate(c);
-    PVec<RMAX> kx, vx;
-    {
-        const int rm = wave_max_i(cur.r());
-        load_tok<RMAX>(kx, tokg, cur, false, rm);
-        load_tok<RMAX>(vx, tokg, cur, true, rm);
-    }
-    for (; c < nch; c += NWV) {
-        const int ntok = min(CH_TOK, T - c * CH_TOK);
-        const TokLoc nxt = locate(c + NWV);
-        const int rmn = wave_max_i(nxt.r());
-        // ---- K: zero the tile, expand packed keys (token-major rows), logits on MFMA
+    // the chunk loop, compiled for aligned records (a fixed number RL of 16-byte
+    // value loads per vector: 4 when no kept count of the split exceeds 32) and
+    // for any records (dword loads): one straight-line load form per copy keeps
+    // the prefetched registers free of copies at joins, which would wait on them
+    auto chunks = [&](auto rlc) {
+        constexpr int RL = decltype(rlc)::value;
+        int c = wave;
+        TokLoc cur = locate(c);
+        PVec<RMAX> kx, vx;
         {
-            uint4 *t4 = (uint4 *)tile;
-            const uint4 zz = {0u, 0u, 0u, 0u};
-#pragma unroll
-            for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
+            const int rm = wave_max_i(cur.r());
+            __builtin_amdgcn_sched_barrier(0);
+            load_tok<RMAX, RL>(kx, tokg, cur, false, rm);
+            __builtin_amdgcn_sched_barrier(0);          // K's loads before V's, as in the loop
+            load_tok<RMAX, RL>(vx, tokg, cur, true, rm);
+            __builtin_amdgcn_sched_barrier(0);
         }
-        wave_sync();
-        if (cur.valid) scatter_any<RMAX, false, FR>(kx, cur.r(), cur.l2g(), lds_addr(tile) + lane * (KT_STRIDE * 2));
-        wave_sync();
-        mem_fence_compiler();
-        load_tok<RMAX>(kx, tokg, nxt, false, rmn);
-        float z[4][4];
-        const uint16_t *tk = (const uint16_t *)tile;
-#pragma unroll
-        for (int n = 0; n < 4; ++n) {
-            floatx4 a4 = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                const uint4 kv = *(const uint4 *)(tk + (n * 16 + l16) * KT_STRIDE + ks * 32 + q4 * 8);
-                const M8 a = __builtin_bit_cast(M8, kv);
-                a4 = Mma<DT>::run(a, qhi[ks], a4);
-                a4 = Mma<DT>::run(a, qlo[ks], a4);
+        for (; c < nch; c += NWV) {
+            const int ntok = min(CH_TOK, T - c * CH_TOK);
+            const TokLoc nxt = locate(c + NWV);
+            const int rmn = wave_max_i(nxt.r());
+            // ---- K: zero the tile, expand packed keys (token-major rows), logits on MFMA
+            {
+                uint4 *t4 = (uint4 *)tile;
+                const uint4 zz = {0u, 0u, 0u, 0u};
+    #pragma unroll
+                for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
             }
-#pragma unroll
-            for (int r = 0; r < 4; ++r) z[n][r] = a4[r] * scale;
-        }
-        if (ntok < CH_TOK) {                                  // the split's last chunk
-#pragma unroll
+            wave_sync();
+            if (cur.valid) scatter_any<RMAX, false, FR>(kx, cur.r(), cur.l2g(), lds_addr(tile) + lane * (KT_STRIDE * 2));
+            wave_sync();
+            mem_fence_compiler();
+            load_tok<RMAX, RL>(kx, tokg, nxt, false, rmn);
+            float z[4][4];
+            const uint16_t *tk = (const uint16_t *)tile;
+    #pragma unroll
+            for (int n = 0; n < 4; ++n) {
+                floatx4 a4 = {0.0f, 0.0f, 0.0f, 0.0f};
+    #pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    const uint4 kv = *(const uint4 *)(tk + (n * 16 + l16) * KT_STRIDE + ks * 32 + q4 * 8);
+                    const M8 a = __builtin_bit_cast(M8, kv);
+                    a4 = Mma<DT>::run(a, qhi[ks], a4);
+                    a4 = Mma<DT>::run(a, qlo[ks], a4);
+                }
+    #pragma unroll
+                for (int r = 0; r < 4; ++r) z[n][r] = a4[r] * scale;
+            }
+            if (ntok < CH_TOK) {                                  // the split's last chunk
+    #pragma unroll
+                for (int n = 0; n < 4; ++n)
+    #pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (n * 16 + q4 * 4 + r >= ntok) z[n][r] = -INFINITY;
+            }
+            // ---- online softmax for head l16 (tokens across r, n and the lane quarters)
+            float cm = -INFINITY;
+    #pragma unroll
             for (int n = 0; n < 4; ++n)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    if (n * 16 + q4 * 4 + r >= ntok) z[n][r] = -INFINITY;
-        }
-        // ---- online softmax for head l16 (tokens across r, n and the lane quarters)
-        float cm = -INFINITY;
-#pragma unroll
-        for (int n = 0; n < 4; ++n)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) cm = fmaxf(cm, z[n][r]);
-        cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
-        cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
-        // every chunk holds a valid token, so mn is finite: exp(-inf - mn) = 0
-        // covers the masked tokens and the first chunk's alpha
-        const float mn = fmaxf(m_run, cm);
-        const float alpha = __expf(m_run - mn);
-        float ls = 0.0f;
-#pragma unroll
-        for (int n = 0; n < 4; ++n)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                z[n][r] = __expf(z[n][r] - mn);
-                ls += z[n][r];
+    #pragma unroll
+                for (int r = 0; r < 4; ++r) cm = fmaxf(cm, z[n][r]);
+            cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
+            cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
+            // every chunk holds a valid token, so mn is finite: exp(-inf - mn) = 0
+            // covers the masked tokens and the first chunk's alpha
+            const float mn = fmaxf(m_run, cm);
+            const float alpha = __expf(m_run - mn);
+            float ls = 0.0f;
+    #pragma unroll
+            for (int n = 0; n < 4; ++n)
+    #pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    z[n][r] = __expf(z[n][r] - mn);
+                    ls += z[n][r];
+                }
+            ls += __shfl_xor(ls, 16, 64);
+            ls += __shfl_xor(ls, 32, 64);
+            l_run = l_run * alpha + ls;
+            m_run = mn;
+            // ---- V: zero the tile, expand packed values (channel-major rows)
+            wave_sync();
+            {
+                uint4 *t4 = (uint4 *)tile;
+                const uint4 zz = {0u, 0u, 0u, 0u};
+    #pragma unroll
+                for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
             }
-        ls += __shfl_xor(ls, 16, 64);
-        ls += __shfl_xor(ls, 32, 64);
-        l_run = l_run * alpha + ls;
-        m_run = mn;
-        // ---- V: zero the tile, expand packed values (channel-major rows)
-        wave_sync();
-        {
-            uint4 *t4 = (uint4 *)tile;
-            const uint4 zz = {0u, 0u, 0u, 0u};
-#pragma unroll
-            for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
-        }
-        wave_sync();
-        if (cur.valid) scatter_any<RMAX, true, FR>(vx, cur.r(), cur.l2g(), lds_addr(tile) + lane * 2);
-        wave_sync();
-        mem_fence_compiler();
-        load_tok<RMAX>(vx, tokg, nxt, true, rmn);
-        // ---- P . V on MFMA: A = P[head l16][tokens], B = V[tokens][channel tile]
-        if (!__all(alpha == 1.0f)) {                      // some head's running max moved
-            float ar[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, q4 * 4 + r, 64);
-#pragma unroll
-            for (int ct = 0; ct < 8; ++ct)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) acc_o[ct][r] *= ar[r];
-        }
-        const uint16_t *tv = (const uint16_t *)tile;
-#pragma unroll
-        for (int kv = 0; kv < 2; ++kv) {
-            float xs[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) xs[i] = z[2 * kv + (i >> 2)][i & 3];
-            M8 ah, al;
-            split8<DT>(xs, ah, al);
-#pragma unroll
-            for (int ct = 0; ct < 8; ++ct) {
-                const uint16_t *row = tv + (ct * 16 + l16) * VT_STRIDE + kv * 32 + q4 * 4;
-                const uint2 v0 = *(const uint2 *)row, v1 = *(const uint2 *)(row + 16);
-                const uint4 vv4 = {v0.x, v0.y, v1.x, v1.y};
-                const M8 bv = __builtin_bit_cast(M8, vv4);
-                acc_o[ct] = Mma<DT>::run(ah, bv, acc_o[ct]);
-                acc_o[ct] = Mma<DT>::run(al, bv, acc_o[ct]);
+            wave_sync();
+            if (cur.valid) scatter_any<RMAX, true, FR>(vx, cur.r(), cur.l2g(), lds_addr(tile) + lane * 2);
+            wave_sync();
+            mem_fence_compiler();
+            load_tok<RMAX, RL>(vx, tokg, nxt, true, rmn);
+            // ---- P . V on MFMA: A = P[head l16][tokens], B = V[tokens][channel tile]
+            if (!__all(alpha == 1.0f)) {                      // some head's running max moved
+                float ar[4];
+    #pragma unroll
+                for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, q4 * 4 + r, 64);
+    #pragma unroll
+                for (int ct = 0; ct < 8; ++ct)
+    #pragma unroll
+                    for (int r = 0; r < 4; ++r) acc_o[ct][r] *= ar[r];
             }
+            const uint16_t *tv = (const uint16_t *)tile;
+    #pragma unroll
+            for (int kv = 0; kv < 2; ++kv) {
+                float xs[8];
+    #pragma unroll
+                for (int i = 0; i < 8; ++i) xs[i] = z[2 * kv + (i >> 2)][i & 3];
+                M8 ah, al;
+                split8<DT>(xs, ah, al);
+    #pragma unroll
+                for (int ct = 0; ct < 8; ++ct) {
+                    const uint16_t *row = tv + (ct * 16 + l16) * VT_STRIDE + kv * 32 + q4 * 4;
+                    const uint2 v0 = *(const uint2 *)row, v1 = *(const uint2 *)(row + 16);
+                    const uint4 vv4 = {v0.x, v0.y, v1.x, v1.y};
+                    const M8 bv = __builtin_bit_cast(M8, vv4);
+                    acc_o[ct] = Mma<DT>::run(ah, bv, acc_o[ct]);
+                    acc_o[ct] = Mma<DT>::run(al, bv, acc_o[ct]);
+                }
+            }
+            wave_sync();
+            cur = nxt;
         }
-        wave_sync();
-        cur = nxt;
-    }
+    };
+    if (!all16) chunks(IntC<0>{});
+    else if (RMAX > 32 && rsplit <= 32) chunks(IntC<4>{});
+    else chunks(IntC<RMAX / 8>{});
     // ---- merge the waves' (m, l, acc) and write the split's partial
     __syncthreads();
     float *mrg = (float *)(wbase + wave * TILE_BYTES);      // [16][D + 2]
