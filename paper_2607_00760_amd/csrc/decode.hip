@@ -37,6 +37,7 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(8))) _Float16 halfx8;
 typedef __attribute__((ext_vector_type(4))) float floatx4;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 
 template <int DT> struct Mma;
 template <> struct Mma<1> {
@@ -960,49 +961,64 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             load_tok<RMAX, RL>(vx, tokg, cur, true, rm);
             __builtin_amdgcn_sched_barrier(0);
         }
+        // the tile starts zero; every MFMA operand read below zeroes what it
+        // read, and the reads cover every position a scatter can write, so
+        // each scatter finds the tile zero again
+        {
+            uint4 *t4 = (uint4 *)tile;
+            const uint4 zz = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
+        }
+        wave_sync();
         for (; c < nch; c += NWV) {
             const int ntok = min(CH_TOK, T - c * CH_TOK);
             const TokLoc nxt = locate(c + NWV);
             const int rmn = wave_max_i(nxt.r());
-            // ---- K: zero the tile, expand packed keys (token-major rows), logits on MFMA
-            {
-                uint4 *t4 = (uint4 *)tile;
-                const uint4 zz = {0u, 0u, 0u, 0u};
-    #pragma unroll
-                for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
-            }
-            wave_sync();
+            // ---- K: expand packed keys (token-major rows), logits on MFMA
             if (cur.valid) scatter_any<RMAX, false, FR>(kx, cur.r(), cur.l2g(), lds_addr(tile) + lane * (KT_STRIDE * 2));
             wave_sync();
             mem_fence_compiler();
             load_tok<RMAX, RL>(kx, tokg, nxt, false, rmn);
             float z[4][4];
-            const uint16_t *tk = (const uint16_t *)tile;
-    #pragma unroll
-            for (int n = 0; n < 4; ++n) {
-                floatx4 a4 = {0.0f, 0.0f, 0.0f, 0.0f};
-    #pragma unroll
+            {
+                // four independent accumulators (token groups n), hi and lo
+                // passes apart, so no product waits on the one before it
+                const uint32_t tb = lds_addr(tile);
+                floatx4 a4[4];
+#pragma unroll
+                for (int n = 0; n < 4; ++n) a4[n] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
                 for (int ks = 0; ks < 4; ++ks) {
-                    const uint4 kv = *(const uint4 *)(tk + (n * 16 + l16) * KT_STRIDE + ks * 32 + q4 * 8);
-                    const M8 a = __builtin_bit_cast(M8, kv);
-                    a4 = Mma<DT>::run(a, qhi[ks], a4);
-                    a4 = Mma<DT>::run(a, qlo[ks], a4);
+                    M8 a[4];
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) {
+                        const uint32_t ad = tb + (uint32_t)(((n * 16 + l16) * KT_STRIDE + ks * 32 + q4 * 8) * 2);
+                        a[n] = __builtin_bit_cast(M8, lds_ld<u32x4>(ad));
+                        lds_st<u32x4>(ad, u32x4{0u, 0u, 0u, 0u});
+                    }
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) a4[n] = Mma<DT>::run(a[n], qhi[ks], a4[n]);
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) a4[n] = Mma<DT>::run(a[n], qlo[ks], a4[n]);
                 }
-    #pragma unroll
-                for (int r = 0; r < 4; ++r) z[n][r] = a4[r] * scale;
+#pragma unroll
+                for (int n = 0; n < 4; ++n)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) z[n][r] = a4[n][r] * scale;
             }
             if (ntok < CH_TOK) {                                  // the split's last chunk
-    #pragma unroll
+#pragma unroll
                 for (int n = 0; n < 4; ++n)
-    #pragma unroll
+#pragma unroll
                     for (int r = 0; r < 4; ++r)
                         if (n * 16 + q4 * 4 + r >= ntok) z[n][r] = -INFINITY;
             }
             // ---- online softmax for head l16 (tokens across r, n and the lane quarters)
             float cm = -INFINITY;
-    #pragma unroll
+#pragma unroll
             for (int n = 0; n < 4; ++n)
-    #pragma unroll
+#pragma unroll
                 for (int r = 0; r < 4; ++r) cm = fmaxf(cm, z[n][r]);
             cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
             cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
@@ -1011,9 +1027,9 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             const float mn = fmaxf(m_run, cm);
             const float alpha = __expf(m_run - mn);
             float ls = 0.0f;
-    #pragma unroll
+#pragma unroll
             for (int n = 0; n < 4; ++n)
-    #pragma unroll
+#pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     z[n][r] = __expf(z[n][r] - mn);
                     ls += z[n][r];
@@ -1022,14 +1038,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             ls += __shfl_xor(ls, 32, 64);
             l_run = l_run * alpha + ls;
             m_run = mn;
-            // ---- V: zero the tile, expand packed values (channel-major rows)
-            wave_sync();
-            {
-                uint4 *t4 = (uint4 *)tile;
-                const uint4 zz = {0u, 0u, 0u, 0u};
-    #pragma unroll
-                for (int k = 0; k < TILE_BYTES / 16 / 64; ++k) t4[lane + k * 64] = zz;
-            }
+            // ---- V: expand packed values (channel-major rows)
             wave_sync();
             if (cur.valid) scatter_any<RMAX, true, FR>(vx, cur.r(), cur.l2g(), lds_addr(tile) + lane * 2);
             wave_sync();
@@ -1038,30 +1047,34 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             // ---- P . V on MFMA: A = P[head l16][tokens], B = V[tokens][channel tile]
             if (!__all(alpha == 1.0f)) {                      // some head's running max moved
                 float ar[4];
-    #pragma unroll
+#pragma unroll
                 for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, q4 * 4 + r, 64);
-    #pragma unroll
+#pragma unroll
                 for (int ct = 0; ct < 8; ++ct)
-    #pragma unroll
+#pragma unroll
                     for (int r = 0; r < 4; ++r) acc_o[ct][r] *= ar[r];
             }
-            const uint16_t *tv = (const uint16_t *)tile;
-    #pragma unroll
+            const uint32_t tb = lds_addr(tile);
+#pragma unroll
             for (int kv = 0; kv < 2; ++kv) {
                 float xs[8];
-    #pragma unroll
+#pragma unroll
                 for (int i = 0; i < 8; ++i) xs[i] = z[2 * kv + (i >> 2)][i & 3];
                 M8 ah, al;
                 split8<DT>(xs, ah, al);
-    #pragma unroll
+                M8 bv[8];
+#pragma unroll
                 for (int ct = 0; ct < 8; ++ct) {
-                    const uint16_t *row = tv + (ct * 16 + l16) * VT_STRIDE + kv * 32 + q4 * 4;
-                    const uint2 v0 = *(const uint2 *)row, v1 = *(const uint2 *)(row + 16);
-                    const uint4 vv4 = {v0.x, v0.y, v1.x, v1.y};
-                    const M8 bv = __builtin_bit_cast(M8, vv4);
-                    acc_o[ct] = Mma<DT>::run(ah, bv, acc_o[ct]);
-                    acc_o[ct] = Mma<DT>::run(al, bv, acc_o[ct]);
+                    const uint32_t ad = tb + (uint32_t)(((ct * 16 + l16) * VT_STRIDE + kv * 32 + q4 * 4) * 2);
+                    const u32x2 v0 = lds_ld<u32x2>(ad), v1 = lds_ld<u32x2>(ad + 32);
+                    lds_st<u32x2>(ad, u32x2{0u, 0u});
+                    lds_st<u32x2>(ad + 32, u32x2{0u, 0u});
+                    bv[ct] = __builtin_bit_cast(M8, u32x4{v0.x, v0.y, v1.x, v1.y});
                 }
+#pragma unroll
+                for (int ct = 0; ct < 8; ++ct) acc_o[ct] = Mma<DT>::run(ah, bv[ct], acc_o[ct]);
+#pragma unroll
+                for (int ct = 0; ct < 8; ++ct) acc_o[ct] = Mma<DT>::run(al, bv[ct], acc_o[ct]);
             }
             wave_sync();
             cur = nxt;
