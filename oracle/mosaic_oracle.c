@@ -33,8 +33,7 @@
  *    (provisional), and a completed segment is finalized with its own
  *    strategy and recompressed in place.
  *
- * Where the paper is silent the readings are fixed here and listed in the
- * repository's design notes: loss = relative dropped energy (R-3), group
+ * Where the paper is silent these readings are taken (labels R-n): loss = relative dropped energy (R-3), group
  * score = L1 of the group's magnitudes (R-2), candidate order rate-first
  * (R-4), block variance relative to total energy (R-5), global top-k per
  * (sequence, kv head) with k = ceil(rho * N_blocks) (R-7), GQA block score =

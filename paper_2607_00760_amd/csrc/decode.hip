@@ -11,22 +11,28 @@
 //            word), fp32 fused chain over the kept channels, max over the GQA
 //            group.  These scores decide the selection, so their arithmetic
 //            order is fixed.
-//   topk   : exact radix select (8-bit digits, LDS histograms) of the k-th
-//            largest score key, then an ordered compaction breaking ties by
-//            the lowest block index; scores live in LDS when they fit.
+//   topk   : exact selection of the k-th largest score key: passes over the
+//            range [min, max] of the keys still in play, 2048 bins each, so
+//            the bins follow the keys that are present (at most three passes
+//            reach a single key), then an ordered compaction that breaks ties
+//            by the lowest block index.  Up to 16384 blocks per pair the keys
+//            stay in registers (16 per thread); scans and reductions use lane
+//            shifts inside the wave.
 //   attn   : split-K over the selected list (up to 128 blocks of one rotation
 //            window per split).  The split's blocks are ordered by size, so a
 //            64-token chunk never cuts a block and a token finds its block by
 //            a closed form.  Lane per token: the packed K record is expanded
-//            from registers into a zeroed LDS tile with the same bitmap walk,
+//            from registers into an LDS tile with the same bitmap walk,
 //            logits K . q^T on the matrix cores (16x16x32, q split into two
 //            16-bit halves), online softmax in fp32 on the accumulator layout,
 //            then V expanded the same way and P . V on the matrix cores.  The
+//            matrix-core operand reads zero what they read, so the tile is
+//            zero again for the next expansion without a clearing pass.  The
 //            next chunk's records are loaded while the current one is
 //            processed.  The update buffer is one more split (dense, unrotated).
-//   reduce : log-sum-exp merge of the splits per window, back-rotation of
-//            each window's accumulator by R_v (staged in LDS), merge of the
-//            windows and the buffer.
+//   reduce : log-sum-exp merge of the splits per window and back-rotation of
+//            each window's accumulator by R_v (staged in LDS); merge then
+//            combines the windows and the buffer into the output.
 #include "mosaic_internal.h"
 
 namespace mosaic {
