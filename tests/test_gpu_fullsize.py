@@ -1,0 +1,210 @@
+"""GPU parity at the workloads' full sizes, in the launch configuration the
+benchmark times (one library call per step over every sequence and kv head).
+
+The GPU runs the whole workload; the oracle recomputes a seeded sample of
+(sequence, kv head) pairs one by one and must agree with it exactly on the
+packed bytes, descriptors, block scores and selections of those pairs, and
+within 2e-3 max-abs / 1e-3 rel-L2 on their outputs.  The 1M-token case (one
+layer of the 32) is too large for the oracle to compress whole in a test: it
+checks a prefix of the cache byte for byte, the scores of that prefix, that
+the selection is the top-k of the GPU's own scores, and the attention output
+against an independent fp64 evaluation over the GPU's selection (packed
+records decoded here, rotation merged back by R_v).
+"""
+import concurrent.futures as cf
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from _parity import (D, assert_close, assert_state_equal, bits, gpu_cache, gpu_scores_sel, params_pair,
+                     scale_of)
+from oracle import oracle as O
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+
+def _sample(n_pairs, k, seed):
+    rng = np.random.default_rng(seed)
+    return sorted(int(x) for x in rng.choice(n_pairs, size=min(k, n_pairs), replace=False))
+
+
+def _oracle_pair(op, spec, lay, cap, pi, L=None):
+    b, h = divmod(pi, spec.hkv)
+    L = lay["ctx_lens"][b] if L is None else L
+    rk = lay["rot_k"][b, h].cpu().numpy() if lay["rot_k"] is not None else None
+    rv = lay["rot_v"][b, h].cpu().numpy() if lay["rot_v"] is not None else None
+    pr = O.Pair(op, cap, rk, rv)
+    pr.compress(bits(lay["k"][b, h, :L]), bits(lay["v"][b, h, :L]))
+    return pr
+
+
+def _oracle_pairs(op, spec, lay, cap, pairs):
+    with cf.ThreadPoolExecutor(len(pairs)) as ex:
+        return dict(zip(pairs, ex.map(lambda pi: _oracle_pair(op, spec, lay, cap, pi), pairs)))
+
+
+def _check_decode(c, spec, ops, q, out, where):
+    G, sc = spec.group, scale_of()
+    qb = bits(q)
+    got = out.cpu().numpy()
+    for pi, pr in ops.items():
+        b, h = divmod(pi, spec.hkv)
+        qq = qb[b, h * G:(h + 1) * G]
+        want, sel = pr.decode(qq, sc)
+        nb = pr.info().nblk
+        gs, gsel, _ = gpu_scores_sel(c, pi, nb)
+        assert np.array_equal(gs.view(np.uint32), pr.scores(qq).view(np.uint32)), f"{where} pair {pi}: block scores"
+        assert np.array_equal(gsel, sel), f"{where} pair {pi}: selected blocks"
+        assert_close(got[b, h * G:(h + 1) * G], want, f"{where} pair {pi}")
+
+
+def test_c3_full_size_sampled():
+    """8 x 131072 tokens, 32 q / 8 kv heads, bf16, planted segments: the bench workload."""
+    spec = gen.spec("c3")
+    print(f"[fullsize] c3 {spec.num_seqs}x{spec.max_ctx}", flush=True)
+    cap = spec.capacity
+    lay = gen.make_layer(spec, 0, device="cuda", capacity=cap)
+    lp, op = params_pair(spec)
+    c = gpu_cache(lp, spec, lay, cap)
+    q = lay["queries"]
+    out = c.decode(q, scale_of())
+    torch.cuda.synchronize()
+    pairs = _sample(spec.num_seqs * spec.hkv, 2, 3)
+    ops = _oracle_pairs(op, spec, lay, cap, pairs)
+    for pi, pr in ops.items():
+        assert_state_equal(c, pi, pr, where="c3")
+    _check_decode(c, spec, ops, q, out, "c3")
+
+
+@pytest.mark.parametrize("name, n_sample, check_every", [("c2", 2, 4), ("c5", 2, 16)])
+def test_append_decode_full_size_sampled(name, n_sample, check_every):
+    """c2: 4 x 32768 fp16 with 16 x (append + decode); c5: 16 ragged sequences
+    (16K..98K) of G = 7 Student-t bf16 with 64 x (append + decode), which
+    crosses provisional flushes and segment finalizations."""
+    spec = gen.spec(name)
+    print(f"[fullsize] {name} ctx={spec.ctx[:4]}... steps={spec.appends}", flush=True)
+    cap = spec.capacity
+    lay = gen.make_layer(spec, 0, device="cuda", capacity=cap)
+    lp, op = params_pair(spec)
+    c = gpu_cache(lp, spec, lay, cap)
+    pairs = _sample(spec.num_seqs * spec.hkv, n_sample, 7)
+    ops = _oracle_pairs(op, spec, lay, cap, pairs)
+    for pi, pr in ops.items():
+        assert_state_equal(c, pi, pr, where=f"{name} prefill")
+    for t in range(spec.appends):
+        kn, vn = gen.make_appends(spec, t)
+        c.append(kn.cuda(), vn.cuda())
+        kb, vb = bits(kn), bits(vn)
+        for pi, pr in ops.items():
+            b, h = divmod(pi, spec.hkv)
+            pr.append(kb[b, h], vb[b, h])
+        q = gen.make_queries(spec, t + 1)
+        out = c.decode(q.cuda(), scale_of())
+        if t % check_every == check_every - 1 or t == spec.appends - 1:
+            torch.cuda.synchronize()
+            for pi, pr in ops.items():
+                assert_state_equal(c, pi, pr, where=f"{name} step {t}")
+            _check_decode(c, spec, ops, q, out, f"{name} step {t}")
+
+
+def _unpack_blocks(c, pi, descs, blocks, dtype):
+    """Independent decoder of the selected blocks' packed K/V records of one
+    pair -> (K, V) [tokens][D] fp64 in the rotated space (zeros on dropped
+    channels), token counts per block."""
+    npdt = np.float16 if dtype == "fp16" else None
+    tok = c.region("token", pi).cpu().numpy()
+    fb = np.array([d[2] for d in descs])
+    Ks, Vs = [], []
+    for blk in blocks:
+        i = int(np.searchsorted(fb, blk, side="right") - 1)
+        off, _, first, r, l2g, l2b, _ = descs[i]
+        g, B = 1 << l2g, 1 << l2b
+        bmb, vb = D // (8 * g), 2 * r
+        base = off + (blk - first) * B * 2 * (bmb + vb)
+        for half, dst in ((0, Ks), (1, Vs)):
+            h0 = base + half * B * (bmb + vb)
+            for j in range(B):
+                bm = np.unpackbits(tok[h0 + j * bmb: h0 + (j + 1) * bmb], bitorder="little")[:D // g]
+                raw = tok[h0 + B * bmb + j * vb: h0 + B * bmb + (j + 1) * vb].view(np.uint16)
+                if npdt is not None:
+                    vals = raw.view(np.float16).astype(np.float64)
+                else:
+                    vals = (raw.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+                x = np.zeros(D)
+                ch = np.nonzero(np.repeat(bm, g))[0]
+                x[ch] = vals
+                dst.append(x)
+    return np.array(Ks), np.array(Vs)
+
+
+def test_c4_one_layer_full_size_properties():
+    """One layer of the 1M-token workload (1 x 1,048,576 tokens, 8 kv heads, fp16)."""
+    spec = gen.spec("c4", layers=1)
+    print(f"[fullsize] c4 one layer {spec.max_ctx}", flush=True)
+    cap = spec.capacity
+    lay = gen.make_layer(spec, 0, device="cuda", capacity=cap)
+    lp, op = params_pair(spec)
+    c = gpu_cache(lp, spec, lay, cap)
+    q = gen.make_queries(spec, 0)
+    out = c.decode(q.cuda(), scale_of())
+    torch.cuda.synchronize()
+    pi = _sample(spec.hkv, 1, 11)[0]
+    b, h = divmod(pi, spec.hkv)
+    G, sc = spec.group, scale_of()
+    # (1) a 2-window prefix, compressed by the oracle, equals the GPU's first bytes
+    Lp = 2 * spec.rot_window
+    pr = _oracle_pair(op, spec, lay, cap, pi, L=Lp)
+    nd = pr.info().n_desc
+    gd = c.region("desc", pi, 16 * nd).cpu().numpy()
+    assert np.array_equal(gd, pr.descriptor_bytes()), "c4 prefix descriptors"
+    ot, osc = pr.token_arena(), pr.score_arena()
+    assert np.array_equal(c.region("token", pi, ot.size).cpu().numpy(), ot), "c4 prefix token arena"
+    assert np.array_equal(c.region("score", pi, osc.size).cpu().numpy(), osc), "c4 prefix score arena"
+    # (2) the prefix blocks' scores equal the oracle's
+    qq = bits(q)[b, h * G:(h + 1) * G]
+    nbp = pr.info().nblk
+    nb = int(c.ws_region("wsel", pi, 4 * (c.layout.num_windows + 2)).cpu().numpy().view(np.int32)[-1])
+    gs, gsel, _ = gpu_scores_sel(c, pi, nb)
+    assert np.array_equal(gs[:nbp].view(np.uint32), pr.scores(qq).view(np.uint32)), "c4 prefix scores"
+    # (3) the selection is the top-k of the GPU's scores by (score desc, index asc)
+    k = -(-nb * spec.select[0] // spec.select[1])
+    key = np.where(gs == 0, 0.0, gs)
+    order = np.lexsort((np.arange(nb), -key.astype(np.float64)))
+    assert np.array_equal(gsel, np.sort(order[:k])), "c4 selection is not the top-k of the scores"
+    # (4) attention over that selection, evaluated here in fp64
+    L = spec.ctx[b]
+    nd_all = L // 64 + (1 if L % 64 >= 32 else 0)
+    raw = c.region("desc", pi, 16 * nd_all).cpu().numpy()
+    descs = []
+    for j in range(nd_all):
+        rr = raw[16 * j:16 * j + 16]
+        u = rr[:12].view(np.uint32)
+        descs.append((int(u[0]), int(u[1]), int(u[2]), int(rr[12]), int(rr[13]), int(rr[14]), int(rr[15])))
+    K, V = _unpack_blocks(c, pi, descs, gsel, spec.dtype)
+    fb = np.array([d[2] for d in descs])
+    win = []
+    for blk in gsel:
+        i = int(np.searchsorted(fb, blk, side="right") - 1)
+        win += [(i * 64) // spec.rot_window] * (1 << descs[i][5])
+    win = np.array(win)
+    rk = lay["rot_k"][b, h].double().cpu().numpy()
+    rv = lay["rot_v"][b, h].double().cpu().numpy()
+    qf = q[b, h * G:(h + 1) * G].double().numpy()
+    logits = np.empty((G, len(K)))
+    for w in np.unique(win):
+        m = win == w
+        logits[:, m] = (qf @ rk[w].T) @ K[m].T
+    logits *= sc
+    nbuf = L % 64 - (32 if L % 64 >= 32 else 0)
+    assert nbuf == 0
+    mx = logits.max(1, keepdims=True)
+    p = np.exp(logits - mx)
+    acc = np.zeros((G, D))
+    for w in np.unique(win):
+        m = win == w
+        acc += (p[:, m] @ V[m]) @ rv[w]
+    want = acc / p.sum(1, keepdims=True)
+    assert_close(out.cpu().numpy()[b, h * G:(h + 1) * G], want, "c4 attention over the GPU selection")
