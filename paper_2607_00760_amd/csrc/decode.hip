@@ -117,9 +117,14 @@ __device__ __forceinline__ void stage_copy(uint4 *dst, const uint4 *src, int nby
 }
 
 // ------------------------------------------------------------------ qrot
-constexpr int QROT_COLS = 16;
+// grid (windows * 2, pairs), 256 threads: a workgroup produces 64 output
+// channels j0..j0+63 of every query head of one (pair, window).  It stages the
+// matching 256-byte half of every row of R_k^T (32 KB, each 128-byte line read
+// by one workgroup only) and the pair's queries in LDS; thread (j, h) then runs
+// the fp32 fused chain over the input channels c for head h (and h + 4).
+constexpr int QROT_COLS = 64;
 
-__global__ void __launch_bounds__(64) k_qrot(Geom g, WsGeom ws, const uint16_t *q) {
+__global__ void __launch_bounds__(256) k_qrot(Geom g, WsGeom ws, const uint16_t *q) {
     __shared__ __align__(16) float rt[D][QROT_COLS];      // R_k^T[c][j0 + jj] = R_k[j0 + jj][c]
     __shared__ float qs[8][D];
     constexpr int NCG = D / QROT_COLS;
@@ -127,29 +132,34 @@ __global__ void __launch_bounds__(64) k_qrot(Geom g, WsGeom ws, const uint16_t *
     const int p = blockIdx.y, tid = threadIdx.x, G = g.G;
     if (g.rotated) {
         const float *src = g.rot_of(p, w);
-        uint4 t[8];
+        constexpr int PER = D * QROT_COLS / 4 / 256;       // 16-byte pieces per thread
+        uint4 t[PER];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int idx = tid + 64 * k, c = idx >> 2, part = idx & 3;
+        for (int k = 0; k < PER; ++k) {
+            const int idx = tid + 256 * k, c = idx / (QROT_COLS / 4), part = idx % (QROT_COLS / 4);
             t[k] = *(const uint4 *)(src + c * D + j0 + 4 * part);
         }
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int idx = tid + 64 * k, c = idx >> 2, part = idx & 3;
+        for (int k = 0; k < PER; ++k) {
+            const int idx = tid + 256 * k, c = idx / (QROT_COLS / 4), part = idx % (QROT_COLS / 4);
             *(uint4 *)&rt[c][4 * part] = t[k];
         }
     }
-    for (int i = tid; i < G * D; i += 64) qs[i / D][i % D] = h2f(q[(uint64_t)p * G * D + i], g.dtype);
+    for (int i = tid; i < G * D; i += 256) qs[i / D][i % D] = h2f(q[(uint64_t)p * G * D + i], g.dtype);
     __syncthreads();
-    const int jj = tid & 15, h0 = tid >> 4;         // heads h0 and h0 + 4
+    const int jj = tid & (QROT_COLS - 1), h0 = tid / QROT_COLS;   // heads h0 and h0 + 4
     float a0 = 0.0f, a1 = 0.0f;
     if (g.rotated) {
-        const bool two = h0 + 4 < G;
+        if (h0 + 4 < G) {
 #pragma unroll 8
-        for (int c = 0; c < D; ++c) {
-            const float r = rt[c][jj];
-            a0 = fmaf(qs[h0][c], r, a0);
-            if (two) a1 = fmaf(qs[h0 + 4][c], r, a1);
+            for (int c = 0; c < D; ++c) {
+                const float r = rt[c][jj];
+                a0 = fmaf(qs[h0][c], r, a0);
+                a1 = fmaf(qs[h0 + 4][c], r, a1);
+            }
+        } else if (h0 < G) {
+#pragma unroll 8
+            for (int c = 0; c < D; ++c) a0 = fmaf(qs[h0][c], rt[c][jj], a0);
         }
     } else {
         a0 = (h0 < G) ? qs[h0][j0 + jj] : 0.0f;
@@ -308,30 +318,47 @@ template <int V> struct IntC { static constexpr int value = V; };
 // One walk: acc[h] += q[c][h] * value over the kept channels c, ascending.
 // qs + qoff is the [D][GP] fp32 query of the vector's window.  RV is the
 // number of kept values when it is a compile-time constant, else 0 and r
-// (wave-uniform over the calling lanes) gives it.
+// (wave-uniform over the calling lanes) gives it.  The LDS reads of q run SA
+// steps ahead of their products (the positions do not depend on q), so a
+// step does not wait for its own read.
 template <int DT, int GP, int RMAX, int L2G, int RV>
 __device__ __forceinline__ void score_walk(const PVec<RMAX> &x, int r, uint32_t qaddr, float (&acc)[GP]) {
     constexpr int GS = 1 << L2G, NWD = 4 >> L2G;
     constexpr uint32_t QB = GP * 4;                           // bytes of q per channel
+    constexpr int NS = (RV ? RV : RMAX) / GS;                 // most steps
+    constexpr int SA = GS == 1 ? 2 : 0;                       // reads in flight ahead of use
+    constexpr int NQ = GS * (GP / 4);                         // 16-byte reads per step
     Walk wk = make_walk<NWD>(x.bw, qaddr, 32u * GS * QB);      // LDS address of group 0 of word k
     const int n = RV ? RV : r;
+    floatx4 ring[SA + 1][NQ];
+    auto issue = [&](int j) {                                 // j static in the unrolled code
+        const uint32_t qc = wk.a + wk.pos() * (GS * QB);
 #pragma unroll
-    for (int k = 0; k < (RV ? RV : RMAX) / GS; ++k) {
+        for (int e = 0; e < GS; ++e)
+#pragma unroll
+            for (int h4 = 0; h4 < GP; h4 += 4)
+                ring[j % (SA + 1)][e * (GP / 4) + h4 / 4] = lds_ld<floatx4>(qc + e * QB + h4 * 4);
+        wk.template step<NWD>();
+    };
+#pragma unroll
+    for (int j = 0; j < SA; ++j)
+        if (j < NS && (RV || j * GS < n)) issue(j);
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
         if (RV || k * GS < n) {                               // wave-uniform
-            const uint32_t qc = wk.a + wk.pos() * (GS * QB);
+            if (k + SA < NS && (RV || (k + SA) * GS < n)) issue(k + SA);
 #pragma unroll
             for (int e = 0; e < GS; ++e) {
                 const float xv = h2f_t<DT>(half_at(x.v, k * GS + e));
 #pragma unroll
                 for (int h4 = 0; h4 < GP; h4 += 4) {
-                    const floatx4 q4 = lds_ld<floatx4>(qc + e * QB + h4 * 4);
+                    const floatx4 q4 = ring[k % (SA + 1)][e * (GP / 4) + h4 / 4];
                     acc[h4] = fmaf(q4[0], xv, acc[h4]);
                     acc[h4 + 1] = fmaf(q4[1], xv, acc[h4 + 1]);
                     acc[h4 + 2] = fmaf(q4[2], xv, acc[h4 + 2]);
                     acc[h4 + 3] = fmaf(q4[3], xv, acc[h4 + 3]);
                 }
             }
-            wk.template step<NWD>();
             if ((k & 3) == 3) __builtin_amdgcn_sched_barrier(0);   // bound the look-ahead
         }
     }
@@ -1307,7 +1334,7 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, f
         fixed = fixed && (r == 16 || r == 32 || r == 48);
     }
     if (ev) hipEventRecord(ev[0], s);
-    hipLaunchKernelGGL(k_qrot, dim3(nwq * (D / QROT_COLS), g.npairs), dim3(64), 0, s, g, w, q);
+    hipLaunchKernelGGL(k_qrot, dim3(nwq * (D / QROT_COLS), g.npairs), dim3(256), 0, s, g, w, q);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (ev) hipEventRecord(ev[1], s);
