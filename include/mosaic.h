@@ -134,9 +134,9 @@ mosaic_status mosaic_workspace_bytes(const mosaic_cache *cache, int32_t op, size
  *   sel   + p * sel_stride   : int32 [max_blocks] selected blocks, ascending
  *   wsel  + p * wsel_stride  : int32 [windows + 2]: first selected entry of
  *                              each window, then k, then the block count
- *   part  + p * part_stride  : fp32 [max_splits + windows + 1][GP * (D + 2)]:
- *                              split-K partials (max, sum, accumulator per head),
- *                              then one merged slot per window and one for the buffer
+ *   part  + p * part_stride  : fp32 [max_splits][GP * (D + 2)]: split-K
+ *                              partials (max, sum, accumulator rotated back
+ *                              by R_v, per head)
  *   tag   + p * tag_stride   : int32 [max_splits]: window of each split
  *   bseg  + p * bseg_stride  : uint32 [max_blocks]: segment << 4 | block in segment
  * Calls that overlap on one workspace race; separate streams need separate

@@ -199,8 +199,8 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     wregion(w.sel_off, w.sel_stride, (uint64_t)c->max_blocks * 4);
     // wsel: window starts in the selected list, k, block count
     wregion(w.wsel_off, w.wsel_stride, (uint64_t)(c->nw + 2) * 4);
-    // part: split partials, then one merged slot per window and one for the buffer
-    wregion(w.part_off, w.part_stride, (uint64_t)(c->max_splits + c->nw + 1) * c->GP * (D + 2) * 4);
+    // part: split partials (max, sum, unrotated accumulator per head)
+    wregion(w.part_off, w.part_stride, (uint64_t)c->max_splits * c->GP * (D + 2) * 4);
     wregion(w.tag_off, w.tag_stride, (uint64_t)c->max_splits * 4);
     wregion(w.bseg_off, w.bseg_stride, (uint64_t)c->max_blocks * 4);
     w.total = off;

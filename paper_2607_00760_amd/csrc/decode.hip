@@ -30,9 +30,9 @@
 //            zero again for the next expansion without a clearing pass.  The
 //            next chunk's records are loaded while the current one is
 //            processed.  The update buffer is one more split (dense, unrotated).
-//   reduce : log-sum-exp merge of the splits per window and back-rotation of
-//            each window's accumulator by R_v (staged in LDS); merge then
-//            combines the windows and the buffer into the output.
+//            Each window split rotates its accumulator back by R_v before
+//            writing it (the rotation stays merged into one vector per split).
+//   combine: log-sum-exp merge of every split of a pair into the output.
 #include "mosaic_internal.h"
 
 namespace mosaic {
@@ -716,8 +716,10 @@ constexpr int KT_STRIDE = 136;       // u16 per token row of the K tile (128 + 8
 constexpr int VT_STRIDE = 68;        // u16 per channel row of the V tile (64 + 4 pad)
 constexpr int TILE_BYTES = 17408;    // max(64 * 272, 128 * 136)
 constexpr int ATTN_NWV = 2;          // waves per attention workgroup
-// block table [SPLIT_BLOCKS] + per-wave class counts, 16-byte multiple
-constexpr int ATTN_HDR_BYTES = (8 * SPLIT_BLOCKS + 2 * 4 * 4 + 15) / 16 * 16;
+// block table [SPLIT_BLOCKS] + per-wave class counts (16-byte multiple), then
+// the merged accumulator [D][8] for the back-rotation
+constexpr int ATTN_ACM_OFF = (8 * SPLIT_BLOCKS + 2 * 4 * 4 + 15) / 16 * 16;
+constexpr int ATTN_HDR_BYTES = ATTN_ACM_OFF + D * 8 * 4;
 
 // x = hi + lo with hi, lo in the MFMA's 16-bit type (round to nearest even);
 // hi + lo carries x to ~16 (bf16) or ~22 (fp16) significant bits
@@ -1125,6 +1127,8 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) mrg[(q4 * 4 + r) * (D + 2) + 2 + ct * 16 + l16] = acc_o[ct][r];
     __syncthreads();
+    // merged accumulator, channel-major [D][GP]
+    float *acm = (float *)(smem + ATTN_ACM_OFF);
     for (int i = tid; i < GP * D; i += NWV * 64) {
         const int h = i / D, cc = i % D;
         float Mx = -INFINITY;
@@ -1138,183 +1142,93 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             A += mw[h * (D + 2) + 2 + cc] * f;
             Ls += mw[h * (D + 2) + 1] * f;
         }
-        part[2 * GP + h * D + cc] = A;
+        if (g.rotated) acm[cc * GP + h] = A;
+        else part[2 * GP + h * D + cc] = A;
         if (cc == 0) { part[h] = Mx; part[GP + h] = Ls; }
+    }
+    if (g.rotated) {
+        // back-rotation of the split's accumulator by its window's R_v (the
+        // rotation stays merged into the single output vector): thread j
+        // produces output channel j of every head, x_j = sum_c a_c R_v[c][j]
+        // R_v is staged through the tiles in two halves of 64 rows (32 KB)
+        static_assert(NWV * 64 == D, "one thread per output channel");
+        static_assert(NWV * TILE_BYTES >= 64 * D * 4, "half of R_v fits the tiles");
+        const float *rvg = g.rot_of(p, w) + 2 * D * D;
+        const int j = tid;
+        float o[GP];
+#pragma unroll
+        for (int h = 0; h < GP; ++h) o[h] = 0.0f;
+        const uint32_t aa = lds_addr(acm), ra = lds_addr(wbase);
+        constexpr int PER = 64 * D / 4 / (NWV * 64);        // 16-byte pieces per thread per half
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+            u32x4 t[PER];
+#pragma unroll
+            for (int k = 0; k < PER; ++k) t[k] = ((const u32x4 *)(rvg + hf * 64 * D))[tid + NWV * 64 * k];
+            __syncthreads();                                // merge rows / previous half read
+#pragma unroll
+            for (int k = 0; k < PER; ++k) lds_st<u32x4>(ra + (uint32_t)(tid + NWV * 64 * k) * 16, t[k]);
+            __syncthreads();
+#pragma unroll 8
+            for (int c = 0; c < 64; ++c) {
+                const float r = lds_ld<float>(ra + (uint32_t)(c * D + j) * 4);
+#pragma unroll
+                for (int h4 = 0; h4 < GP; h4 += 4) {
+                    const floatx4 a4 = lds_ld<floatx4>(aa + (uint32_t)((hf * 64 + c) * GP + h4) * 4);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) o[h4 + e] = fmaf(a4[e], r, o[h4 + e]);
+                }
+            }
+        }
+#pragma unroll
+        for (int h = 0; h < GP; ++h) part[2 * GP + h * D + j] = o[h];
     }
     if (tid == 0) tag[s] = w;
 }
 
-// ------------------------------------------------------------------ reduce
-// grid (windows in use + 1, pairs).  Workgroup x < nwu merges the splits of
-// rotation window x (log-sum-exp) and rotates the merged accumulator back by
-// R_v (staged in LDS while the partials load); x == nwu takes the update
-// buffer's split.  Each writes (max, sum, output) per head to a window slot
-// after the split partials; k_merge then combines a pair's window slots into
-// the output (a kernel boundary, rather than a device-wide fence per
-// workgroup, makes the slots visible).
+// ------------------------------------------------------------------ combine
+// grid (pairs, GP * D / 256), one output per thread: online log-sum-exp merge of a pair's split partials (already
+// in the unrotated space: the window splits were rotated back by R_v, the
+// update buffer's split never was rotated) into the output.  Splits tagged -2
+// hold nothing.  A kernel boundary, rather than a device-wide fence per
+// workgroup, makes the partials visible.
 constexpr int RED_THREADS = 256;
-constexpr int RED_CHUNK = 128;                             // splits per staged chunk
 
 template <int GP>
-__global__ void __launch_bounds__(RED_THREADS) k_reduce(Geom g, WsGeom ws, int nwu) {
-    __shared__ __align__(16) float rv[D * D];
-    __shared__ float A[GP][D];
-    __shared__ float hm[RED_CHUNK][2 * GP];                 // (max, sum) per head of staged splits
-    __shared__ int wbeg[RED_CHUNK + 1];
-    const int x = blockIdx.x, p = blockIdx.y, tid = threadIdx.x;
-    constexpr int PS = GP * (D + 2);                        // floats per partial
-    constexpr int NPT = GP * D / RED_THREADS;               // outputs per thread: (h, j) = i / D, i % D
-    const PairMeta meta = *g.meta_of(p);
-    int nf, prov, nbuf;
-    pair_ndesc(meta, nf, prov, nbuf);
-    int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
-    const float *part = ws.part + (uint64_t)p * (ws.part_stride / 4);
-    float *slot = ws.part + (uint64_t)p * (ws.part_stride / 4) + (uint64_t)(ws.max_splits + x) * PS;
-    const bool buf = x == nwu;
-    const bool rot = !buf && g.rotated;
-    // this workgroup's split range [S0, S1): splits are ordered by window, the
-    // buffer's last.  R_v of the window is staged to LDS meanwhile.
-    int S0 = 0, S1 = 0;
-    {
-        int acc = 0;
-        const int lim = ws.max_blocks;
-        for (int w0 = 0; w0 < g.nw; w0 += RED_CHUNK) {
-            const int n = min(RED_CHUNK, g.nw - w0);
-            __syncthreads();
-            int wv[2];
-#pragma unroll
-            for (int e = 0; e < 2; ++e) wv[e] = (tid + e * RED_THREADS <= n) ? wsel[w0 + tid + e * RED_THREADS] : 0;
-            if (w0 == 0 && rot)
-                stage_copy<RED_THREADS, 16>((uint4 *)rv, (const uint4 *)(g.rot_of(p, x) + 2 * D * D), D * D * 4, tid);
-#pragma unroll
-            for (int e = 0; e < 2; ++e) if (tid + e * RED_THREADS <= n) wbeg[tid + e * RED_THREADS] = wv[e];
-            __syncthreads();
-            for (int i = 0; i < n; ++i) {
-                const int a = min(max(wbeg[i], 0), lim), b = min(max(wbeg[i + 1], a), lim);
-                const int nsp = (b - a + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS;
-                if (w0 + i == x) { S0 = acc; S1 = acc + nsp; }
-                acc += nsp;
-            }
-        }
-        if (buf) { S0 = acc; S1 = acc + (nbuf > 0 ? 1 : 0); }
-        S0 = min(S0, ws.max_splits);
-        S1 = min(S1, ws.max_splits);
-    }
-    float M[GP], Lw[GP], Aw[NPT];
-#pragma unroll
-    for (int h = 0; h < GP; ++h) { M[h] = -INFINITY; Lw[h] = 0.0f; }
-#pragma unroll
-    for (int u = 0; u < NPT; ++u) Aw[u] = 0.0f;
-    // per-head maximum over the splits
-    for (int c0 = S0; c0 < S1; c0 += RED_CHUNK) {
-        const int n = min(RED_CHUNK, S1 - c0);
-        __syncthreads();
-        for (int i = tid; i < n * 2 * GP; i += RED_THREADS)
-            hm[i / (2 * GP)][i % (2 * GP)] = part[(uint64_t)(c0 + i / (2 * GP)) * PS + i % (2 * GP)];
-        __syncthreads();
-        for (int e = 0; e < n; ++e)
-#pragma unroll
-            for (int h = 0; h < GP; ++h) M[h] = fmaxf(M[h], hm[e][h]);
-    }
-    // weighted sums (exp(m_s - M) computed from the staged headers)
-    for (int c0 = S0; c0 < S1; c0 += RED_CHUNK) {
-        const int n = min(RED_CHUNK, S1 - c0);
-        if (S1 - S0 > RED_CHUNK) {                          // more than one chunk: restage
-            __syncthreads();
-            for (int i = tid; i < n * 2 * GP; i += RED_THREADS)
-                hm[i / (2 * GP)][i % (2 * GP)] = part[(uint64_t)(c0 + i / (2 * GP)) * PS + i % (2 * GP)];
-            __syncthreads();
-        }
-        for (int e0 = 0; e0 < n; e0 += 8) {
-            float av[8][NPT];
-#pragma unroll
-            for (int e = 0; e < 8; ++e)                      // issue the loads of 8 splits together
-#pragma unroll
-                for (int u = 0; u < NPT; ++u)
-                    av[e][u] = (e0 + e < n) ? part[(uint64_t)(c0 + e0 + e) * PS + 2 * GP + tid + u * RED_THREADS] : 0.0f;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                if (e0 + e >= n) break;
-#pragma unroll
-                for (int u = 0; u < NPT; ++u) {
-                    const int h = (tid + u * RED_THREADS) / D;
-                    const float m = hm[e0 + e][h];
-                    const float f = (m == -INFINITY) ? 0.0f : __expf(m - M[h]);
-                    Aw[u] = fmaf(av[e][u], f, Aw[u]);
-                }
-#pragma unroll
-                for (int h = 0; h < GP; ++h) {
-                    const float m = hm[e0 + e][h];
-                    Lw[h] += (m == -INFINITY) ? 0.0f : hm[e0 + e][GP + h] * __expf(m - M[h]);
-                }
-            }
-        }
-    }
-#pragma unroll
-    for (int u = 0; u < NPT; ++u) { const int i = tid + u * RED_THREADS; A[i / D][i % D] = Aw[u]; }
-    __syncthreads();
-    // back-rotation x = y . R_v of the window's accumulator
-#pragma unroll
-    for (int u = 0; u < NPT; ++u) {
-        const int i = tid + u * RED_THREADS, h = i / D, j = i % D;
-        float o = A[h][j];
-        if (rot) {
-            o = 0.0f;
-#pragma unroll 8
-            for (int c = 0; c < D; ++c) o = fmaf(A[h][c], rv[c * D + j], o);
-        }
-        slot[2 * GP + i] = o;
-    }
-    if (tid < GP) { slot[tid] = M[tid]; slot[GP + tid] = Lw[tid]; }
-}
-
-// grid (pairs): online log-sum-exp merge of the window slots (and the buffer's)
-template <int GP>
-__global__ void __launch_bounds__(RED_THREADS) k_merge(Geom g, WsGeom ws, float *out, int nwu) {
-    __shared__ float hm[RED_CHUNK][2 * GP];
+__global__ void __launch_bounds__(RED_THREADS) k_combine(Geom g, WsGeom ws, float *out) {
     constexpr int PS = GP * (D + 2);
-    constexpr int NPT = GP * D / RED_THREADS;
+    constexpr int CB = 32;                                  // splits whose loads are issued together
     const int p = blockIdx.x, tid = threadIdx.x, G = g.G;
-    const float *slots = ws.part + (uint64_t)p * (ws.part_stride / 4) + (uint64_t)ws.max_splits * PS;
-    float *o = out + (uint64_t)p * G * D;
-    float num[NPT], den[NPT], Mx[NPT];
+    const int i = blockIdx.y * RED_THREADS + tid, h = i / D;   // output (head, channel)
+    const float *part = ws.part + (uint64_t)p * (ws.part_stride / 4);
+    const int32_t *tag = ws.tag + (uint64_t)p * (ws.tag_stride / 4);
+    float num = 0.0f, den = 0.0f, Mx = -INFINITY;
+    for (int y0 = 0; y0 < ws.max_splits; y0 += CB) {
+        const int n = min(CB, ws.max_splits - y0);
+        int t[CB];
+        float m[CB], l[CB], v[CB];
 #pragma unroll
-    for (int u = 0; u < NPT; ++u) { num[u] = 0.0f; den[u] = 0.0f; Mx[u] = -INFINITY; }
-    for (int y0 = 0; y0 <= nwu; y0 += RED_CHUNK) {
-        const int n = min(RED_CHUNK, nwu + 1 - y0);
-        float v[8][NPT];
-        __syncthreads();
-        for (int i = tid; i < n * 2 * GP; i += RED_THREADS)
-            hm[i / (2 * GP)][i % (2 * GP)] = slots[(uint64_t)(y0 + i / (2 * GP)) * PS + i % (2 * GP)];
-        __syncthreads();
-        for (int e0 = 0; e0 < n; e0 += 8) {
+        for (int e = 0; e < CB; ++e) {
+            if (e < n) {
+                const float *ps = part + (uint64_t)(y0 + e) * PS;
+                t[e] = tag[y0 + e];
+                m[e] = ps[h];
+                l[e] = ps[GP + h];
+                v[e] = ps[2 * GP + i];
+            }
+        }
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-#pragma unroll
-                for (int u = 0; u < NPT; ++u)
-                    v[e][u] = (e0 + e < n) ? slots[(uint64_t)(y0 + e0 + e) * PS + 2 * GP + tid + u * RED_THREADS] : 0.0f;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                if (e0 + e >= n) break;
-#pragma unroll
-                for (int u = 0; u < NPT; ++u) {
-                    const int h = (tid + u * RED_THREADS) / D;
-                    const float m = hm[e0 + e][h];
-                    if (m == -INFINITY) continue;
-                    const float mn = fmaxf(Mx[u], m);
-                    const float a = __expf(Mx[u] - mn), b = __expf(m - mn);
-                    num[u] = num[u] * a + v[e][u] * b;
-                    den[u] = den[u] * a + hm[e0 + e][GP + h] * b;
-                    Mx[u] = mn;
-                }
+        for (int e = 0; e < CB; ++e) {
+            if (e < n && t[e] != -2 && m[e] != -INFINITY) {
+                const float mn = fmaxf(Mx, m[e]);
+                const float a = __expf(Mx - mn), b = __expf(m[e] - mn);
+                num = num * a + v[e] * b;
+                den = den * a + l[e] * b;
+                Mx = mn;
             }
         }
     }
-#pragma unroll
-    for (int u = 0; u < NPT; ++u) {
-        const int i = tid + u * RED_THREADS;
-        if (i / D < G) o[i] = (den[u] > 0.0f) ? num[u] / den[u] : 0.0f;
-    }
+    if (h < G) out[(uint64_t)p * G * D + i] = (den > 0.0f) ? num / den : 0.0f;
 }
 
 int max_keep(const Geom &g) {
@@ -1360,10 +1274,7 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, f
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev) hipEventRecord(ev[4], s);
-    hipLaunchKernelGGL(k_reduce<GP>, dim3(max_windows_used + 1, g.npairs), dim3(RED_THREADS), 0, s, g, w,
-                       max_windows_used);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_merge<GP>, dim3(g.npairs), dim3(RED_THREADS), 0, s, g, w, out, max_windows_used);
+    hipLaunchKernelGGL(k_combine<GP>, dim3(g.npairs, GP * D / RED_THREADS), dim3(RED_THREADS), 0, s, g, w, out);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev) hipEventRecord(ev[5], s);
     return hipSuccess;
