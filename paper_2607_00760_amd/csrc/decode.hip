@@ -481,6 +481,10 @@ template <int CTRL, int ROWS>
 __device__ __forceinline__ uint32_t dpp_u(uint32_t x) {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, 0xf, false);
 }
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
 __device__ __forceinline__ uint32_t wave_scan_add(uint32_t x) {
     x += dpp_u<0x111, 0xf>(x);
     x += dpp_u<0x112, 0xf>(x);
@@ -932,20 +936,28 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             blk[pos] = make_uint2(goff, ((uint32_t)r << 8) | ((uint32_t)l2g << 16) | ((uint32_t)l2b << 20));
         }
     }
-    // q operand: B[k = channel][n = head] of the logits K . q^T, split hi + lo
-    M8 qhi[4], qlo[4];
+    // q operand: B[k = channel][n] of the logits K . q^T.  Column n < GP holds
+    // the 16-bit high part of head n's query, column GP + n its residual, so
+    // one product gives both halves of every head's logit (added across the
+    // lanes afterwards): the matrix-core columns past the group are not idle.
+    static_assert(2 * GP <= 16, "high and low query parts share the 16 columns");
+    M8 qhl[4];
     {
         const int qw = g.rotated ? w : 0;
         const float *src = ws.qrot + (uint64_t)p * (ws.qrot_stride / 4) + (uint64_t)qw * D * GP;
+        const int hq = l16 < GP ? l16 : l16 - GP;           // head of this column
+        const bool live = l16 < 2 * GP && hq < G;
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
             float xs[8];
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const int c = ks * 32 + q4 * 8 + i;
-                xs[i] = (l16 < G) ? src[c * GP + (l16 < GP ? l16 : 0)] : 0.0f;
+                xs[i] = live ? src[c * GP + hq] : 0.0f;
             }
-            split8<DT>(xs, qhi[ks], qlo[ks]);
+            M8 hi, lo;
+            split8<DT>(xs, hi, lo);
+            qhl[ks] = (l16 < GP) ? hi : lo;
         }
     }
     __syncthreads();
@@ -1017,8 +1029,8 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             load_tok<RMAX, RL>(kx, tokg, nxt, false, rmn);
             float z[4][4];
             {
-                // four independent accumulators (token groups n), hi and lo
-                // passes apart, so no product waits on the one before it
+                // four independent accumulators (token groups n), so no
+                // product waits on the one before it
                 const uint32_t tb = lds_addr(tile);
                 floatx4 a4[4];
 #pragma unroll
@@ -1033,14 +1045,13 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
                         lds_st<u32x4>(ad, u32x4{0u, 0u, 0u, 0u});
                     }
 #pragma unroll
-                    for (int n = 0; n < 4; ++n) a4[n] = Mma<DT>::run(a[n], qhi[ks], a4[n]);
-#pragma unroll
-                    for (int n = 0; n < 4; ++n) a4[n] = Mma<DT>::run(a[n], qlo[ks], a4[n]);
+                    for (int n = 0; n < 4; ++n) a4[n] = Mma<DT>::run(a[n], qhl[ks], a4[n]);
                 }
+                // head l16 < GP: high-part logit + residual logit of column l16 + GP
 #pragma unroll
                 for (int n = 0; n < 4; ++n)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) z[n][r] = a4[n][r] * scale;
+                    for (int r = 0; r < 4; ++r) z[n][r] = (a4[n][r] + dpp_f<0x100 + GP>(a4[n][r])) * scale;
             }
             if (ntok < CH_TOK) {                                  // the split's last chunk
 #pragma unroll
@@ -1083,7 +1094,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             if (!__all(alpha == 1.0f)) {                      // some head's running max moved
                 float ar[4];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, q4 * 4 + r, 64);
+                for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, (q4 * 4 + r) % GP, 64);
 #pragma unroll
                 for (int ct = 0; ct < 8; ++ct)
 #pragma unroll
@@ -1095,8 +1106,17 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
                 float xs[8];
 #pragma unroll
                 for (int i = 0; i < 8; ++i) xs[i] = z[2 * kv + (i >> 2)][i & 3];
+                // A rows n < GP: P's 16-bit high part for head n; rows GP + n:
+                // its residual, moved over from lane n (one product for both)
                 M8 ah, al;
                 split8<DT>(xs, ah, al);
+                u32x4 alw = __builtin_bit_cast(u32x4, al), ahw = __builtin_bit_cast(u32x4, ah);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t sh = dpp_u<0x110 + GP, 0xf>(alw[e]);
+                    ahw[e] = (l16 < GP) ? ahw[e] : sh;
+                }
+                const M8 apl = __builtin_bit_cast(M8, ahw);
                 M8 bv[8];
 #pragma unroll
                 for (int ct = 0; ct < 8; ++ct) {
@@ -1107,9 +1127,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
                     bv[ct] = __builtin_bit_cast(M8, u32x4{v0.x, v0.y, v1.x, v1.y});
                 }
 #pragma unroll
-                for (int ct = 0; ct < 8; ++ct) acc_o[ct] = Mma<DT>::run(ah, bv[ct], acc_o[ct]);
-#pragma unroll
-                for (int ct = 0; ct < 8; ++ct) acc_o[ct] = Mma<DT>::run(al, bv[ct], acc_o[ct]);
+                for (int ct = 0; ct < 8; ++ct) acc_o[ct] = Mma<DT>::run(apl, bv[ct], acc_o[ct]);
             }
             wave_sync();
             cur = nxt;
@@ -1139,7 +1157,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         for (int x = 0; x < NWV; ++x) {
             const float *mw = (const float *)(wbase + x * TILE_BYTES);
             const float f = (mw[h * (D + 2)] == -INFINITY) ? 0.0f : __expf(mw[h * (D + 2)] - Mx);
-            A += mw[h * (D + 2) + 2 + cc] * f;
+            A += (mw[h * (D + 2) + 2 + cc] + mw[(h + GP) * (D + 2) + 2 + cc]) * f;   // high + residual rows
             Ls += mw[h * (D + 2) + 1] * f;
         }
         if (g.rotated) acm[cc * GP + h] = A;
