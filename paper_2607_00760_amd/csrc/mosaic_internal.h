@@ -11,7 +11,7 @@ constexpr int SEG = 64;       // strategy segment (tokens)
 constexpr int UBUF = 32;      // update buffer (tokens)
 constexpr int WAVE = 64;
 constexpr int SPLIT_BLOCKS = 128;  // selected blocks per split-K partition
-constexpr int SCORE_SEGS = 32;     // segments per block-scoring workgroup
+constexpr int SCORE_SEGS = 128;    // segments per block-scoring workgroup (one launch round)
 
 struct Desc {                 // 16-byte segment descriptor (layout is part of the ABI)
     uint32_t tok_off, sc_off, first_block;
