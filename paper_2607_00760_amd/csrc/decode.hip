@@ -574,30 +574,38 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
         if (REG) return kr[j];
         return in_lds ? keys[i0 + j] : score_key(sc[i0 + j]);
     };
-    block_minmax_1024(kmin, kmax, sbuf);
+    // two histograms in turn: a pass zeroes the next one while it reads its own
+    for (int i = tid; i < TOPK_BINS; i += 1024) hist[i] = 0;
+    block_minmax_1024(kmin, kmax, sbuf);                          // (its barriers publish the zeros)
     uint32_t base = kmin, span = kmax - kmin;                     // candidates: [base, base + span]
     uint32_t rem = (uint32_t)k;                                    // how many candidates to take
-    while (k > 0) {
+    const int lane = tid & 63, wv = tid >> 6;
+    for (int pass = 0; k > 0; ++pass) {
+        uint32_t *hc = hist + (pass & 1) * TOPK_BINS, *hn = hist + ((pass + 1) & 1) * TOPK_BINS;
         const int bits = 32 - (span ? __builtin_clz(span) : 32);
         const int sh = bits > 11 ? bits - 11 : 0;                 // (span >> sh) < 2048
-        for (int i = tid; i < TOPK_BINS; i += 1024) hist[i] = 0;
-        __syncthreads();
         if (REG) {
 #pragma unroll
             for (int j = 0; j < TOPK_KPT; ++j) {
                 const uint32_t d = kr[j] - base;
-                if (j < n_own && kr[j] >= base && d <= span) atomicAdd(&hist[d >> sh], 1u);
+                if (j < n_own && kr[j] >= base && d <= span) atomicAdd(&hc[d >> sh], 1u);
             }
         } else {
             for (int j = 0; j < n_own; ++j) {
                 const uint32_t key = key_at(j), d = key - base;
-                if (key >= base && d <= span) atomicAdd(&hist[d >> sh], 1u);
+                if (key >= base && d <= span) atomicAdd(&hc[d >> sh], 1u);
             }
         }
         __syncthreads();
         // bins from the top: thread t owns bins 2047 - 2t and 2046 - 2t
-        const uint32_t h0 = hist[TOPK_BINS - 1 - 2 * tid], h1 = hist[TOPK_BINS - 2 - 2 * tid];
-        const uint32_t above = block_excl_scan_1024(h0 + h1, sbuf);
+        const uint32_t h0 = hc[TOPK_BINS - 1 - 2 * tid], h1 = hc[TOPK_BINS - 2 - 2 * tid];
+        hn[2 * tid] = 0;
+        hn[2 * tid + 1] = 0;
+        const uint32_t x = wave_scan_add(h0 + h1);
+        if (lane == 63) sbuf[wv] = x;
+        __syncthreads();
+        uint32_t above = x - (h0 + h1);
+        for (int i = 0; i < wv; ++i) above += sbuf[i];
         if (above < rem && above + h0 + h1 >= rem) {
             if (above + h0 >= rem) { sbuf[32] = TOPK_BINS - 1 - 2 * tid; sbuf[33] = rem - above; }
             else { sbuf[32] = TOPK_BINS - 2 - 2 * tid; sbuf[33] = rem - above - h0; }
@@ -608,7 +616,6 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
         base += b << sh;
         const uint32_t width = sh ? ((1u << sh) - 1u) : 0u;
         span = min(span - (b << sh), width);
-        __syncthreads();
         if (sh == 0) break;
     }
     const uint32_t T = base, take_eq_total = rem;
@@ -622,9 +629,6 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
             for (int j = 0; j < n_own; ++j) { const uint32_t key = key_at(j); gt += key > T; eq += key == T; }
         }
     }
-    const uint32_t eq_before = block_excl_scan_1024(eq, sbuf);
-    uint32_t take = 0;
-    if (take_eq_total > eq_before) take = min(eq, take_eq_total - eq_before);
     // first block of each rotation window (windows past the last segment start at nb)
     int *fbw = (int *)hist;
     const int segs_per_win = g.W / SEG;
@@ -634,7 +638,21 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
         const int s0 = w * segs_per_win;
         fbw[w] = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
     }
-    const uint32_t pos0 = block_excl_scan_1024(gt + take, sbuf);   // (its barriers publish fbw)
+    // equal keys are taken in block order until take_eq_total, so a thread's
+    // list position is (greater keys before it) + min(equal keys before it,
+    // take_eq_total): one scan of both counts (packed while they fit 16 bits)
+    uint32_t gt_before, eq_before;
+    if (nb < 65536) {
+        const uint32_t both = block_excl_scan_1024((gt << 16) | eq, sbuf);   // (its barriers publish fbw)
+        gt_before = both >> 16;
+        eq_before = both & 0xffffu;
+    } else {
+        eq_before = block_excl_scan_1024(eq, sbuf);
+        gt_before = block_excl_scan_1024(gt, sbuf);
+    }
+    uint32_t take = 0;
+    if (take_eq_total > eq_before) take = min(eq, take_eq_total - eq_before);
+    const uint32_t pos0 = gt_before + min(eq_before, take_eq_total);
     // write the selected list; a window starting inside [i0, i1) records the
     // list position reached there (windows starting at nb record k)
     int wn = 0;
@@ -674,7 +692,7 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
 
 __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
     extern __shared__ __align__(16) uint32_t keys[];            // [min(nb, TOPK_LDS_KEYS)] when staged
-    __shared__ uint32_t hist[TOPK_BINS];
+    __shared__ uint32_t hist[2 * TOPK_BINS];
     __shared__ uint32_t sbuf[64];
     const int p = blockIdx.x;
     const PairMeta meta = *g.meta_of(p);
