@@ -481,6 +481,19 @@ template <int CTRL, int ROWS>
 __device__ __forceinline__ uint32_t dpp_u(uint32_t x) {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, 0xf, false);
 }
+// x combined with its value in lane ^ 16 or lane ^ 32, on the cross-row
+// swap instructions (no LDS round trip): the swap leaves each lane holding
+// its own value and its partner's
+template <int X>
+__device__ __forceinline__ void xor_pair(float x, float &a, float &b) {
+    static_assert(X == 16 || X == 32, "row pairs or wave halves");
+    const uint32_t u = __float_as_uint(x);
+    if (X == 16) { const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false); a = __uint_as_float(r[0]); b = __uint_as_float(r[1]); }
+    else { const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false); a = __uint_as_float(r[0]); b = __uint_as_float(r[1]); }
+}
+template <int X> __device__ __forceinline__ float xor_max(float x) { float a, b; xor_pair<X>(x, a, b); return fmaxf(a, b); }
+template <int X> __device__ __forceinline__ float xor_sum(float x) { float a, b; xor_pair<X>(x, a, b); return a + b; }
+
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float x) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
@@ -1084,8 +1097,8 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             for (int n = 0; n < 4; ++n)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) cm = fmaxf(cm, z[n][r]);
-            cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
-            cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
+            cm = xor_max<16>(cm);
+            cm = xor_max<32>(cm);
             // every chunk holds a valid token, so mn is finite: exp(-inf - mn) = 0
             // covers the masked tokens and the first chunk's alpha
             const float mn = fmaxf(m_run, cm);
@@ -1098,8 +1111,8 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
                     z[n][r] = __expf(z[n][r] - mn);
                     ls += z[n][r];
                 }
-            ls += __shfl_xor(ls, 16, 64);
-            ls += __shfl_xor(ls, 32, 64);
+            ls = xor_sum<16>(ls);
+            ls = xor_sum<32>(ls);
             l_run = l_run * alpha + ls;
             m_run = mn;
             // ---- V: expand packed values (channel-major rows)
@@ -1112,7 +1125,16 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             if (!__all(alpha == 1.0f)) {                      // some head's running max moved
                 float ar[4];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, (q4 * 4 + r) % GP, 64);
+                for (int r = 0; r < 4; ++r) {                  // alpha of head (q4 * 4 + r) % GP
+                    const float a0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), r));
+                    if (GP == 4) {
+                        ar[r] = a0;
+                    } else {
+                        const float a1 =
+                            __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), 4 + r));
+                        ar[r] = (q4 & 1) ? a1 : a0;
+                    }
+                }
 #pragma unroll
                 for (int ct = 0; ct < 8; ++ct)
 #pragma unroll
