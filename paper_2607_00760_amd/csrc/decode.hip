@@ -857,7 +857,13 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     int *wcnt = (int *)(smem + 8 * SPLIT_BLOCKS);           // [NWV][4] blocks per size class
     uint8_t *wbase = smem + ATTN_HDR_BYTES;                 // [NWV] tiles
 
-    const int p = blockIdx.y, s = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // XCD-aware order: workgroups are dealt to the eight XCDs in turn, so
+    // block b runs on XCD b % 8.  Every split of a pair gets the same residue,
+    // which keeps the pair's R_v, rotated queries and selection in one L2.
+    const int bid = blockIdx.x, xcd = bid & 7, idx = bid >> 3;
+    const int p = xcd + 8 * (idx / ws.max_splits), s = idx % ws.max_splits;
+    if (p >= g.npairs) return;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, q4 = lane >> 4;
     uint8_t *tile = wbase + wave * TILE_BYTES;
 
@@ -1325,7 +1331,7 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, f
     if (ev) hipEventRecord(ev[3], s);
     {
         const size_t smem = ATTN_HDR_BYTES + (size_t)ATTN_NWV * TILE_BYTES;
-        const dim3 grid(w.max_splits, g.npairs), block(64 * ATTN_NWV);
+        const dim3 grid(w.max_splits * ((g.npairs + 7) / 8 * 8)), block(64 * ATTN_NWV);
         if (fixed) hipLaunchKernelGGL((k_attn<DT, GP, 48, true>), grid, block, smem, s, g, w, scale, q);
         else if (small) hipLaunchKernelGGL((k_attn<DT, GP, 48, false>), grid, block, smem, s, g, w, scale, q);
         else hipLaunchKernelGGL((k_attn<DT, GP, 128, false>), grid, block, smem, s, g, w, scale, q);
