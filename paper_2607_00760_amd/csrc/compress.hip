@@ -84,21 +84,27 @@ __device__ __forceinline__ void group_ranks(float ylo, float yhi, int log2g, uin
                                             int &rank_lo, int &rank_hi) {
     const int lane = threadIdx.x & 63;
     float slo = fabsf(ylo), shi = fabsf(yhi);
-    if (log2g >= 1) { slo = slo + shfl_xor_f(slo, 1); shi = shi + shfl_xor_f(shi, 1); }
-    if (log2g >= 2) { slo = slo + shfl_xor_f(slo, 2); shi = shi + shfl_xor_f(shi, 2); }
+    // group sums of adjacent lanes (lane ^ 1, then lane ^ 2: quad permutes)
+    if (log2g >= 1) { slo = slo + dpp_read<0xb1, 0xf>(slo); shi = shi + dpp_read<0xb1, 0xf>(shi); }
+    if (log2g >= 2) { slo = slo + dpp_read<0x4e, 0xf>(slo); shi = shi + dpp_read<0x4e, 0xf>(shi); }
     const int ng = D >> log2g;
     const int glo = lane >> log2g, ghi = (64 >> log2g) + (lane >> log2g);
     const uint64_t klo = ((uint64_t)__float_as_uint(slo) << 8) | (uint64_t)(255 - glo);
     const uint64_t khi = ((uint64_t)__float_as_uint(shi) << 8) | (uint64_t)(255 - ghi);
+    // keys is this wave's own array and a wave's LDS operations complete in
+    // order, so keeping the compiler from moving memory operations across
+    // these points is all the ordering the exchange needs (no barrier)
     if ((lane & ((1 << log2g) - 1)) == 0) { keys[glo] = klo; keys[ghi] = khi; }
-    __syncthreads();
+    __builtin_amdgcn_wave_barrier();
+    asm volatile("" ::: "memory");
     int rl = 0, rh = 0;
     for (int j = 0; j < ng; j += 2) {
         uint64_t k0 = keys[j], k1 = keys[j + 1];
         rl += (k0 > klo) + (k1 > klo);
         rh += (k0 > khi) + (k1 > khi);
     }
-    __syncthreads();
+    __builtin_amdgcn_wave_barrier();
+    asm volatile("" ::: "memory");
     rank_lo = rl; rank_hi = rh;
 }
 
@@ -158,12 +164,7 @@ __device__ __forceinline__ void block_stats(const Geom &g, const float (&y)[TPW]
 }
 
 // tree over the 64 per-token values (wave 0; adjacent pairwise tree)
-__device__ __forceinline__ float tree64_lds(const float *v) {
-    float x = v[threadIdx.x & 63];
-#pragma unroll
-    for (int m = 1; m < 64; m <<= 1) x = x + shfl_xor_f(x, m);
-    return x;
-}
+__device__ __forceinline__ float tree64_lds(const float *v) { return tree64(v[threadIdx.x & 63]); }
 
 // Strategy choice (Sec. 5.5): first (r, g) in candidate order whose dropped
 // energy is below tau_ch * energy for K and for V; first B whose block

@@ -84,17 +84,34 @@ __device__ __forceinline__ int vec_bytes(int r, int log2g) { return 2 * r + (16 
 // ---------------------------------------------------------------- wave helpers
 __device__ __forceinline__ float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, WAVE); }
 
-// tree sum over the 128 channels held as (lane l: channel l, channel l+64):
-// butterfly inside each half gives the adjacent-pair tree of that half, and
-// the final add joins the two halves -- the pairwise adjacent tree of 128.
-__device__ __forceinline__ float tree128(float lo, float hi) {
-#pragma unroll
-    for (int m = 1; m < 64; m <<= 1) {
-        lo = lo + shfl_xor_f(lo, m);
-        hi = hi + shfl_xor_f(hi, m);
-    }
-    return lo + hi;
+// data-parallel-primitive lane move: lane i reads lane i - shift (row shifts),
+// or a row reads the last lane of the row before it (row broadcasts); lanes
+// outside ROWS, or without a source, read 0
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_read(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROWS, 0xf, false));
 }
+
+// pairwise adjacent tree over the 64 lanes: (x0+x1), (x2+x3), ... level by
+// level.  Level L adds, in lane 2^L k + 2^L - 1, the partial sum 2^(L-1)
+// lanes below (row shifts by 1, 2, 4, 8, then the broadcasts of lanes 15 and
+// 31), so lane 63 ends with the tree's sum; it is returned to every lane.
+// The operands of every addition are those of the butterfly form of the
+// same tree.
+__device__ __forceinline__ float tree64(float x) {
+    x = x + dpp_read<0x111, 0xf>(x);
+    x = x + dpp_read<0x112, 0xf>(x);
+    x = x + dpp_read<0x114, 0xf>(x);
+    x = x + dpp_read<0x118, 0xf>(x);
+    x = x + dpp_read<0x142, 0xa>(x);
+    x = x + dpp_read<0x143, 0xc>(x);
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
+// tree sum over the 128 channels held as (lane l: channel l, channel l+64):
+// the adjacent tree of each half, then the two halves joined -- the pairwise
+// adjacent tree of 128.
+__device__ __forceinline__ float tree128(float lo, float hi) { return tree64(lo) + tree64(hi); }
 
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
