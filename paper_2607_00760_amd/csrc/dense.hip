@@ -44,6 +44,7 @@ __global__ void __launch_bounds__(256) k_dense_split(const uint16_t *q, const ui
         for (int h = 0; h < GP; ++h) z[h] = 0.0f;
         if (valid) {
             const uint4 *row = (const uint4 *)(kp + (uint64_t)t * D);
+#pragma unroll 4
             for (int x = 0; x < D / 8; ++x) {
                 const uint4 u = row[x];
                 const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
@@ -73,6 +74,7 @@ __global__ void __launch_bounds__(256) k_dense_split(const uint16_t *q, const ui
         }
         __syncthreads();
         const int tmax = any ? min(64, t1 - cb) : 0;
+#pragma unroll 8
         for (int tt = 0; tt < tmax; ++tt) {
             const uint32_t w2 = *(const uint32_t *)(vp + (uint64_t)(cb + tt) * D + 2 * lane);
             const float v0 = h2f((uint16_t)(w2 & 0xffffu), dtype), v1 = h2f((uint16_t)(w2 >> 16), dtype);
@@ -108,32 +110,39 @@ __global__ void __launch_bounds__(256) k_dense_split(const uint16_t *q, const ui
     }
 }
 
+// grid (pairs, GP * D / 256): one output per thread; the loads of 32 chunks
+// are issued together, then merged by online log-sum-exp
 template <int GP>
-__global__ void __launch_bounds__(128) k_dense_reduce(int hkv, int G, const int32_t *ctx, const float *part,
+__global__ void __launch_bounds__(256) k_dense_reduce(int hkv, int G, const int32_t *ctx, const float *part,
                                                       int max_splits, float *outp) {
-    const int p = blockIdx.x, j = threadIdx.x;
+    constexpr int CB = 32;
+    const int p = blockIdx.x, i = blockIdx.y * 256 + threadIdx.x, h = i / D;
     const int L = ctx[p / hkv];
     const int ns = (L + DCHUNK - 1) / DCHUNK;
-    float M[GP], Ls[GP], A[GP];
+    float M = -INFINITY, Ls = 0.0f, A = 0.0f;
+    for (int s0 = 0; s0 < ns; s0 += CB) {
+        float m[CB], l[CB], a[CB];
 #pragma unroll
-    for (int h = 0; h < GP; ++h) { M[h] = -INFINITY; Ls[h] = 0.0f; A[h] = 0.0f; }
-    for (int s = 0; s < ns; ++s) {
-        const float *ps = part + ((uint64_t)p * max_splits + s) * GP * (D + 2);
+        for (int e = 0; e < CB; ++e) {
+            if (s0 + e < ns) {
+                const float *ps = part + ((uint64_t)p * max_splits + s0 + e) * GP * (D + 2);
+                m[e] = ps[h];
+                l[e] = ps[GP + h];
+                a[e] = ps[2 * GP + i];
+            }
+        }
 #pragma unroll
-        for (int h = 0; h < GP; ++h) {
-            const float m = ps[h];
-            if (m == -INFINITY) continue;
-            const float mn = fmaxf(M[h], m);
-            const float a = (M[h] == -INFINITY) ? 0.0f : __expf(M[h] - mn), b = __expf(m - mn);
-            A[h] = A[h] * a + ps[2 * GP + h * D + j] * b;
-            Ls[h] = Ls[h] * a + ps[GP + h] * b;
-            M[h] = mn;
+        for (int e = 0; e < CB; ++e) {
+            if (s0 + e < ns && m[e] != -INFINITY) {
+                const float mn = fmaxf(M, m[e]);
+                const float x = (M == -INFINITY) ? 0.0f : __expf(M - mn), y = __expf(m[e] - mn);
+                A = A * x + a[e] * y;
+                Ls = Ls * x + l[e] * y;
+                M = mn;
+            }
         }
     }
-    float *o = outp + (uint64_t)p * G * D;
-#pragma unroll
-    for (int h = 0; h < GP; ++h)
-        if (h < G) o[h * D + j] = (Ls[h] > 0.0f) ? A[h] / Ls[h] : 0.0f;
+    if (h < G) outp[(uint64_t)p * G * D + i] = (Ls > 0.0f) ? A / Ls : 0.0f;
 }
 
 }  // namespace
@@ -155,13 +164,13 @@ hipError_t launch_dense(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                            scale, part, ms);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(k_dense_reduce<4>, dim3(npairs), dim3(128), 0, s, hkv, G, ctx, part, ms, out);
+        hipLaunchKernelGGL(k_dense_reduce<4>, dim3(npairs, 4 * D / 256), dim3(256), 0, s, hkv, G, ctx, part, ms, out);
     } else {
         hipLaunchKernelGGL(k_dense_split<8>, dim3(ms, npairs), dim3(256), 0, s, q, k, v, hkv, G, dtype, seq_stride, ctx,
                            scale, part, ms);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(k_dense_reduce<8>, dim3(npairs), dim3(128), 0, s, hkv, G, ctx, part, ms, out);
+        hipLaunchKernelGGL(k_dense_reduce<8>, dim3(npairs, 8 * D / 256), dim3(256), 0, s, hkv, G, ctx, part, ms, out);
     }
     return hipGetLastError();
 }
