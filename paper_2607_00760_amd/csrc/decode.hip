@@ -417,6 +417,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
     const int ns = min(spw, ndesc - s0);
     const Desc *gd = g.desc_of(p);
     const uint32_t fb0 = gd[s0].first_block;
+    bool plain = true;                      // one channel per group, r a multiple of 8 up to 32, aligned records
     if (tid < ns) {
         const Desc d = gd[s0 + tid];
         ds[tid] = d;
@@ -424,6 +425,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         const int o = (int)(d.first_block - fb0);
         for (int j = 0; j < nb; ++j) b2s[o + j] = (uint8_t)tid;
         if (tid == ns - 1) s_nblk = o + nb;
+        plain = d.log2g == 0 && (d.r & 7) == 0 && d.r <= 32 && (d.sc_off & 15u) == 0;
     }
     const int w0 = g.rotated ? (s0 * SEG) / g.W : 0;
     const int w1 = g.rotated ? ((s0 + ns - 1) * SEG) / g.W : 0;
@@ -436,11 +438,53 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
             d1[i] = x1;
         }
     }
-    __syncthreads();
+    plain = __syncthreads_and(plain);
     const int nblk = s_nblk;
     float *out = ws.score + (uint64_t)p * (ws.score_stride / 4);
     uint32_t *bseg = ws.bseg + (uint64_t)p * (ws.bseg_stride / 4);
     const uint8_t *sc = g.sc_of(p);
+    if (plain) {
+        // every record is 16-byte aligned with at most 32 values: four fixed
+        // 16-byte value loads, and the next key's record is loaded while the
+        // current one is scored (one load form, so no join waits on it)
+        auto where = [&](int b, int &i, int &j, int &r) {
+            const bool valid = b < nblk;
+            i = valid ? b2s[b] : 0;
+            const Desc d = ds[i];
+            j = b - (int)(d.first_block - fb0);
+            r = valid ? d.r : 0;
+            return valid ? sc + d.sc_off + (uint32_t)j * (uint32_t)vec_bytes(d.r, 0) : sc;
+        };
+        int i, j, r;
+        const uint8_t *rec = where(tid, i, j, r);
+        PVec<RMAX> x;
+        load_pvec<RMAX, 1, false, 4>(x, rec, rec + 16, 32, true);
+        for (int b0 = 0; b0 < nblk; b0 += 256) {
+            int in, jn, rn;
+            const uint8_t *recn = where(b0 + 256 + tid, in, jn, rn);
+            PVec<RMAX> xn;
+            __builtin_amdgcn_sched_barrier(0);
+            load_pvec<RMAX, 1, false, 4>(xn, recn, recn + 16, 32, true);
+            __builtin_amdgcn_sched_barrier(0);
+            const uint32_t qoff = (g.rotated && ((s0 + i) * SEG) / g.W != w0) ? D * GP * 4 : 0;
+            float acc[GP];
+#pragma unroll
+            for (int h = 0; h < GP; ++h) acc[h] = 0.0f;
+            score_any<DT, GP, RMAX, FR>(x, r, 0, lds_addr(qs) + qoff, acc);
+            float best = acc[0];
+#pragma unroll
+            for (int h = 1; h < GP; ++h)
+                if (h < g.G) best = fmaxf(best, acc[h]);
+            if (__float_as_uint(best) == 0x80000000u) best = 0.0f;
+            if (b0 + tid < nblk) {
+                const uint32_t fb = ds[i].first_block;
+                out[fb + j] = best;
+                bseg[fb + j] = ((uint32_t)(s0 + i) << 4) | (uint32_t)j;
+            }
+            x = xn; i = in; j = jn; r = rn;
+        }
+        return;
+    }
     for (int b0 = 0; b0 < nblk; b0 += 256) {
         const int b = b0 + tid;
         const bool valid = b < nblk;
