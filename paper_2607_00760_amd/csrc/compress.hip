@@ -23,7 +23,6 @@ constexpr int TPW = 16;            // tokens per wave
 constexpr int NCAND = 9;
 
 struct SegSmem {
-    float rt[D * D];               // R^T of the matrix being applied (rt[c*D + j] = R[j][c])
     float x[SEG * D];              // the segment's input tokens, fp32
     float tot[2][SEG];             // per-token energy (K, V)
     float drop[2][NCAND][SEG];     // per-token dropped energy per (r, g) candidate
@@ -34,19 +33,17 @@ struct SegSmem {
 
 __device__ __forceinline__ int ilog2i(int v) { return 31 - __clz(v); }
 
-// Stage the tokens and (optionally) R^T, then y[i][0..1] = rotated channels
-// (l, l+64) of token 16w+i.  y = x . R^T as fp32 fmaf chains over ascending c.
+// Stage the tokens, then y[i][0..1] = rotated channels (l, l+64) of token
+// 16w+i.  y = x . R^T as fp32 fmaf chains over ascending c; the rows of R^T
+// (rt_g[c*D + j] = R[j][c]) are read from the arena (cached: a window's R is
+// shared by all of its segments), the next four rows while the current four
+// are applied, so the workgroup keeps no copy of R in LDS.
 __device__ __forceinline__ void rotate_tile(const uint16_t *src, int ntok, const float *rt_g, int dtype,
                             SegSmem &sm, float (&y)[TPW][2]) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int i = tid; i < SEG * D; i += 256) {
         int t = i / D;
         sm.x[i] = (t < ntok) ? h2f(src[i], dtype) : 0.0f;
-    }
-    if (rt_g) {
-        const float4 *s4 = (const float4 *)rt_g;
-        float4 *d4 = (float4 *)sm.rt;
-        for (int i = tid; i < D * D / 4; i += 256) d4[i] = s4[i];
     }
     __syncthreads();
     const int t0 = wave * TPW;
@@ -59,10 +56,15 @@ __device__ __forceinline__ void rotate_tile(const uint16_t *src, int ntok, const
     } else {
 #pragma unroll
         for (int i = 0; i < TPW; ++i) { y[i][0] = 0.0f; y[i][1] = 0.0f; }
-        for (int c = 0; c < D; c += 4) {
-            float rl[4], rh[4];
+        const float *r0 = rt_g + lane, *r1 = rt_g + lane + 64;
+        float rl[4], rh[4];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) { rl[k] = sm.rt[(c + k) * D + lane]; rh[k] = sm.rt[(c + k) * D + lane + 64]; }
+        for (int k = 0; k < 4; ++k) { rl[k] = r0[k * D]; rh[k] = r1[k * D]; }
+        for (int c = 0; c < D; c += 4) {
+            const int cn = (c + 4 < D) ? c + 4 : c;          // the last block reloads itself
+            float nl[4], nh[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) { nl[k] = r0[(cn + k) * D]; nh[k] = r1[(cn + k) * D]; }
 #pragma unroll
             for (int i = 0; i < TPW; ++i) {
                 float4 xv = *(const float4 *)&sm.x[(t0 + i) * D + c];
@@ -73,6 +75,8 @@ __device__ __forceinline__ void rotate_tile(const uint16_t *src, int ntok, const
                     y[i][1] = fmaf(xs[k], rh[k], y[i][1]);
                 }
             }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) { rl[k] = nl[k]; rh[k] = nh[k]; }
         }
     }
     __syncthreads();
