@@ -102,7 +102,8 @@ __device__ __forceinline__ void group_ranks(float ylo, float yhi, int log2g, uin
     __builtin_amdgcn_wave_barrier();
     asm volatile("" ::: "memory");
     int rl = 0, rh = 0;
-    for (int j = 0; j < ng; j += 2) {
+#pragma unroll 8
+    for (int j = 0; j < ng; j += 2) {                      // ng is a multiple of 16: reads issued 8 at a time
         uint64_t k0 = keys[j], k1 = keys[j + 1];
         rl += (k0 > klo) + (k1 > klo);
         rh += (k0 > khi) + (k1 > khi);
