@@ -562,14 +562,21 @@ __device__ __forceinline__ uint32_t wave_max_u(uint32_t x) {
     return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
 }
 
+// sum of s[0 .. n) for n <= 64 (wave-uniform): one read per lane, then the
+// lane shifts and the last lane's total (no chain of dependent LDS reads)
+__device__ __forceinline__ uint32_t sum_below(const uint32_t *s, int n) {
+    const int lane = threadIdx.x & 63;
+    const uint32_t x = lane < n ? s[lane] : 0u;
+    return (uint32_t)__builtin_amdgcn_readlane((int)wave_scan_add(x), 63);
+}
+
 // exclusive prefix sum over the 1024 threads of the block; s: 16 words of LDS
 __device__ __forceinline__ uint32_t block_excl_scan_1024(uint32_t v, uint32_t *s) {
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const uint32_t x = wave_scan_add(v);
     if (lane == 63) s[wv] = x;
     __syncthreads();
-    uint32_t base = 0;
-    for (int i = 0; i < wv; ++i) base += s[i];
+    const uint32_t base = sum_below(s, wv);
     __syncthreads();
     return base + x - v;
 }
@@ -662,7 +669,7 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
         if (lane == 63) sbuf[wv] = x;
         __syncthreads();
         uint32_t above = x - (h0 + h1);
-        for (int i = 0; i < wv; ++i) above += sbuf[i];
+        above += sum_below(sbuf, wv);
         if (above < rem && above + h0 + h1 >= rem) {
             if (above + h0 >= rem) { sbuf[32] = TOPK_BINS - 1 - 2 * tid; sbuf[33] = rem - above; }
             else { sbuf[32] = TOPK_BINS - 2 - 2 * tid; sbuf[33] = rem - above - h0; }
@@ -714,10 +721,14 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
     // list position reached there (windows starting at nb record k)
     int wn = 0;
     while (wn < nwl && fbw[wn] < i0) ++wn;
+    int nextfb = wn < nwl ? fbw[wn] : 0x7fffffff;          // next window start, kept in a register
     uint32_t pos = pos0, seen = 0;
     auto emit = [&](int j, uint32_t key) {
         const int i = i0 + j;
-        while (wn < nwl && fbw[wn] == i) wsel[wn++] = (int)pos;
+        while (nextfb == i) {
+            wsel[wn++] = (int)pos;
+            nextfb = wn < nwl ? fbw[wn] : 0x7fffffff;
+        }
         if (k > 0) {
             const bool take_it = key > T || (key == T && seen < take);
             seen += (key == T && take_it) ? 1u : 0u;
