@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="c3")
+    ap.add_argument("--mode", choices=("mosaic", "quest"), default="mosaic",
+                    help="quest: every channel kept, 16-token blocks, no rotation (sequence-only "
+                         "compression on the same kernels)")
     ap.add_argument("--ctx", type=int, default=0, help="override the context length (smoke runs)")
     ap.add_argument("--flush-mb", type=int, default=1024)
     ap.add_argument("--dense-steps", type=int, default=5)
@@ -122,6 +125,13 @@ def main():
     spec = gen.spec(args.config)
     if args.ctx:
         spec = gen.spec(args.config, ctx=(args.ctx,) * spec.num_seqs)
+    # method parameters beyond the workload's: the quest mode keeps all D
+    # channels of every vector in 16-token blocks, unrotated (the sequence-only
+    # baseline of the paper's evaluation, run on this library's own kernels)
+    extra = {}
+    if args.mode == "quest":
+        spec = gen.spec(args.config, ctx=spec.ctx, rotate=False)
+        extra = dict(default=(D, 1, 16), force_default=True)
     cap = spec.max_ctx
     log(f"generating {spec.name}: {spec.num_seqs} x {spec.max_ctx} tokens, {spec.hkv} kv heads")
     t0 = time.time()
@@ -130,7 +140,7 @@ def main():
     t_gen = time.time() - t0
     q = lay["queries"] if lay["queries"] is not None else gen.make_queries(spec, 0, device=dev)
     params = M.Params(num_kv_heads=spec.hkv, group_size=spec.group, dtype=spec.dtype, rot_window=spec.rot_window,
-                      tau_channel=spec.tau_channel, tau_block=spec.tau_block, select=spec.select)
+                      tau_channel=spec.tau_channel, tau_block=spec.tau_block, select=spec.select, **extra)
     cache = M.MosaicCache(params, spec.num_seqs, cap, rotated=spec.rotate, device=dev)
     # compression pass (timed once, after one untimed pass)
     cache.compress(lay["k"], lay["v"], lay["ctx_lens"], lay["rot_k"], lay["rot_v"])
@@ -260,7 +270,7 @@ def main():
     achieved = ab[dom] / (kern_us[dom] * 1e-6) / 1e9
     traffic = None
     tf = os.path.join(ROOT, "profiles", f"traffic_{args.config}.json")
-    if os.path.exists(tf) and not args.ctx:
+    if os.path.exists(tf) and not args.ctx and args.mode == "mosaic":
         t = json.load(open(tf))
         if t.get("source_hash") == source_hash() and t.get("kernel") == dom:
             traffic = t.get("bytes_per_launch")
@@ -299,7 +309,7 @@ def main():
         from oracle import oracle as O
         ns = min(args.cpu_sample_pairs, cache.num_pairs)
         op = O.Params(group=spec.group, dtype=spec.dtype, rot_window=spec.rot_window, tau_channel=spec.tau_channel,
-                      tau_block=spec.tau_block, select=spec.select)
+                      tau_block=spec.tau_block, select=spec.select, **extra)
         qb = gen.bits(q)
 
         def comp(p):
@@ -347,7 +357,10 @@ def main():
         "vs_baseline": None, "dtype": spec.dtype, "data": "synthetic",
         "config": {"workload": f"{spec.name}: decode attention over a compressed KV cache, batch {spec.num_seqs} x "
                                f"{spec.max_ctx} tokens, {spec.hq} q / {spec.hkv} kv heads, d=128, {spec.dtype}, "
-                               f"select 1/10 of blocks, planted 5% of segments",
+                               f"select 1/10 of blocks, planted 5% of segments"
+                               + ("; quest mode: all channels kept, 16-token blocks, no rotation"
+                                  if args.mode == "quest" else ""),
+                   "mode": args.mode,
                    "num_seqs": spec.num_seqs, "ctx": spec.max_ctx, "q_heads": spec.hq, "kv_heads": spec.hkv,
                    "head_dim": D, "select": f"{spec.select[0]}/{spec.select[1]}", "mall_flush_mb": args.flush_mb},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,

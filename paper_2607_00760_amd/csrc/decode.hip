@@ -418,6 +418,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
     const Desc *gd = g.desc_of(p);
     const uint32_t fb0 = gd[s0].first_block;
     bool plain = true;                      // one channel per group, r a multiple of 8 up to 32, aligned records
+    bool dense = true;                      // every channel kept (r = D), aligned records
     if (tid < ns) {
         const Desc d = gd[s0 + tid];
         ds[tid] = d;
@@ -426,6 +427,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         for (int j = 0; j < nb; ++j) b2s[o + j] = (uint8_t)tid;
         if (tid == ns - 1) s_nblk = o + nb;
         plain = d.log2g == 0 && (d.r & 7) == 0 && d.r <= 32 && (d.sc_off & 15u) == 0;
+        dense = d.log2g == 0 && d.r == D && (d.sc_off & 15u) == 0;
     }
     const int w0 = g.rotated ? (s0 * SEG) / g.W : 0;
     const int w1 = g.rotated ? ((s0 + ns - 1) * SEG) / g.W : 0;
@@ -439,10 +441,60 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         }
     }
     plain = __syncthreads_and(plain);
+    if (RMAX >= D) dense = __syncthreads_and(dense);
     const int nblk = s_nblk;
     float *out = ws.score + (uint64_t)p * (ws.score_stride / 4);
     uint32_t *bseg = ws.bseg + (uint64_t)p * (ws.bseg_stride / 4);
     const uint8_t *sc = g.sc_of(p);
+    if constexpr (RMAX >= D) {
+        if (dense) {
+            // every channel kept: the values are the dense key in channel
+            // order; the same ascending fp32 chain reads q row by row (one
+            // address for the whole wave)
+            for (int b0 = 0; b0 < nblk; b0 += 256) {
+                const int b = b0 + tid;
+                const bool valid = b < nblk;
+                const int i = valid ? b2s[b] : 0;
+                const Desc d = ds[i];
+                const int j = b - (int)(d.first_block - fb0);
+                const uint8_t *rec = valid ? sc + d.sc_off + (uint32_t)j * (uint32_t)vec_bytes(D, 0) : sc;
+                const uint4 *v4 = (const uint4 *)(rec + 16);
+                uint4 t[D / 8];
+#pragma unroll
+                for (int k = 0; k < D / 8; ++k) t[k] = v4[k];
+                const uint32_t qa = lds_addr(qs) + ((g.rotated && ((s0 + i) * SEG) / g.W != w0) ? D * GP * 4 : 0);
+                float acc[GP];
+#pragma unroll
+                for (int h = 0; h < GP; ++h) acc[h] = 0.0f;
+#pragma unroll
+                for (int k = 0; k < D / 8; ++k) {
+                    const uint32_t w4[4] = {t[k].x, t[k].y, t[k].z, t[k].w};
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const float xv = h2f_t<DT>((e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xffffu));
+#pragma unroll
+                        for (int h4 = 0; h4 < GP; h4 += 4) {
+                            const floatx4 q4v = lds_ld<floatx4>(qa + (uint32_t)(((8 * k + e) * GP + h4) * 4));
+                            acc[h4] = fmaf(q4v[0], xv, acc[h4]);
+                            acc[h4 + 1] = fmaf(q4v[1], xv, acc[h4 + 1]);
+                            acc[h4 + 2] = fmaf(q4v[2], xv, acc[h4 + 2]);
+                            acc[h4 + 3] = fmaf(q4v[3], xv, acc[h4 + 3]);
+                        }
+                    }
+                }
+                float best = acc[0];
+#pragma unroll
+                for (int h = 1; h < GP; ++h)
+                    if (h < g.G) best = fmaxf(best, acc[h]);
+                if (__float_as_uint(best) == 0x80000000u) best = 0.0f;
+                if (valid) {
+                    out[d.first_block + j] = best;
+                    bseg[d.first_block + j] = ((uint32_t)(s0 + i) << 4) | (uint32_t)j;
+                }
+            }
+            return;
+        }
+    }
     if (plain) {
         // every record is 16-byte aligned with at most 32 values: four fixed
         // 16-byte value loads, and the next key's record is loaded while the
@@ -902,6 +954,31 @@ __device__ __forceinline__ void load_tok(PVec<RMAX> &x, const uint8_t *tokg, con
     load_pvec<RMAX, RL ? 1 : 0, false, RL>(x, b + j * bmb, b + B * bmb + j * 2 * r, rmax, false);
 }
 
+// A vector that keeps every channel (r = D, one channel per group): its
+// values are the dense row in channel order, so no walk is needed.  K goes to
+// the token-major row at addr with 16-byte stores, V to the channel-major
+// column at addr with one 16-bit store per channel (the wave's lanes write
+// consecutive columns of one row per store).  vals is 16-byte aligned.
+template <bool COL>
+__device__ __forceinline__ void dense_put(const uint8_t *vals, uint32_t addr) {
+    const uint4 *v4 = (const uint4 *)vals;
+    uint4 t[D / 8];
+#pragma unroll
+    for (int k = 0; k < D / 8; ++k) t[k] = v4[k];
+#pragma unroll
+    for (int k = 0; k < D / 8; ++k) {
+        if (!COL) {
+            lds_st<u32x4>(addr + (uint32_t)(16 * k), u32x4{t[k].x, t[k].y, t[k].z, t[k].w});
+        } else {
+            const uint32_t w[4] = {t[k].x, t[k].y, t[k].z, t[k].w};
+#pragma unroll
+            for (int h = 0; h < 8; ++h)
+                lds_st<uint16_t>(addr + (uint32_t)((8 * k + h) * VT_STRIDE * 2),
+                                 (uint16_t)((h & 1) ? (w[h >> 1] >> 16) : w[h >> 1]));
+        }
+    }
+}
+
 template <int DT, int GP, int RMAX, bool FR>
 __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
 k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
@@ -995,6 +1072,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     // starts at a multiple of its size and none straddles a 64-token chunk
     const int nbk = e1 - e0;
     bool all16;                                     // every record of the split 16-byte aligned
+    bool dense = false;                             // every block keeps all D channels (RMAX = D kernels)
     int rsplit;                                     // largest kept count in the split
     {
         const bool on = tid < nbk;
@@ -1019,6 +1097,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         // one channel per group, r % 8 == 0 and an aligned block: 16-byte
         // bitmaps and 2r-byte value runs at 16-byte offsets
         all16 = __syncthreads_and(!on || (l2g == 0 && (r & 7) == 0 && (goff & 15u) == 0));
+        if (RMAX >= D) dense = __syncthreads_and(!on || (l2g == 0 && r == D));
         if (on) {
             const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
             const int c16 = wcnt[0] + wcnt[4], c8 = wcnt[1] + wcnt[5];
@@ -1088,11 +1167,11 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     // for any records (dword loads): one straight-line load form per copy keeps
     // the prefetched registers free of copies at joins, which would wait on them
     auto chunks = [&](auto rlc) {
-        constexpr int RL = decltype(rlc)::value;
+        constexpr int RL = decltype(rlc)::value;            // < 0: dense blocks, no walk, no prefetch
         int c = wave;
         TokLoc cur = locate(c);
         PVec<RMAX> kx, vx;
-        {
+        if constexpr (RL >= 0) {
             const int rm = wave_max_i(cur.r());
             __builtin_amdgcn_sched_barrier(0);
             load_tok<RMAX, RL>(kx, tokg, cur, false, rm);
@@ -1102,7 +1181,9 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         }
         // the tile starts zero; every MFMA operand read below zeroes what it
         // read, and the reads cover every position a scatter can write, so
-        // each scatter finds the tile zero again
+        // each scatter finds the tile zero again (dense blocks overwrite the
+        // rows and columns of their tokens instead; a last chunk's unused rows
+        // hold finite values of earlier tokens, whose weights are zero)
         {
             uint4 *t4 = (uint4 *)tile;
             const uint4 zz = {0u, 0u, 0u, 0u};
@@ -1113,12 +1194,18 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         for (; c < nch; c += NWV) {
             const int ntok = min(CH_TOK, T - c * CH_TOK);
             const TokLoc nxt = locate(c + NWV);
-            const int rmn = wave_max_i(nxt.r());
+            const int rmn = RL >= 0 ? wave_max_i(nxt.r()) : 0;
             // ---- K: expand packed keys (token-major rows), logits on MFMA
-            if (cur.valid) scatter_any<RMAX, false, FR>(kx, cur.r(), cur.l2g(), lds_addr(tile) + lane * (KT_STRIDE * 2));
+            if constexpr (RL < 0) {
+                if (cur.valid)
+                    dense_put<false>(tokg + cur.base + (16 << cur.l2b()) + cur.j() * 2 * D,
+                                     lds_addr(tile) + lane * (KT_STRIDE * 2));
+            } else if (cur.valid) {
+                scatter_any<RMAX, false, FR>(kx, cur.r(), cur.l2g(), lds_addr(tile) + lane * (KT_STRIDE * 2));
+            }
             wave_sync();
             mem_fence_compiler();
-            load_tok<RMAX, RL>(kx, tokg, nxt, false, rmn);
+            if constexpr (RL >= 0) load_tok<RMAX, RL>(kx, tokg, nxt, false, rmn);
             float z[4][4];
             {
                 // four independent accumulators (token groups n), so no
@@ -1134,7 +1221,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
                     for (int n = 0; n < 4; ++n) {
                         const uint32_t ad = tb + (uint32_t)(((n * 16 + l16) * KT_STRIDE + ks * 32 + q4 * 8) * 2);
                         a[n] = __builtin_bit_cast(M8, lds_ld<u32x4>(ad));
-                        lds_st<u32x4>(ad, u32x4{0u, 0u, 0u, 0u});
+                        if (RL >= 0) lds_st<u32x4>(ad, u32x4{0u, 0u, 0u, 0u});
                     }
 #pragma unroll
                     for (int n = 0; n < 4; ++n) a4[n] = Mma<DT>::run(a[n], qhl[ks], a4[n]);
@@ -1178,10 +1265,17 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             m_run = mn;
             // ---- V: expand packed values (channel-major rows)
             wave_sync();
-            if (cur.valid) scatter_any<RMAX, true, FR>(vx, cur.r(), cur.l2g(), lds_addr(tile) + lane * 2);
+            if constexpr (RL < 0) {
+                if (cur.valid) {
+                    const int B = 1 << cur.l2b();
+                    dense_put<true>(tokg + cur.base + B * (16 + 2 * D) + 16 * B + cur.j() * 2 * D, lds_addr(tile) + lane * 2);
+                }
+            } else if (cur.valid) {
+                scatter_any<RMAX, true, FR>(vx, cur.r(), cur.l2g(), lds_addr(tile) + lane * 2);
+            }
             wave_sync();
             mem_fence_compiler();
-            load_tok<RMAX, RL>(vx, tokg, nxt, true, rmn);
+            if constexpr (RL >= 0) load_tok<RMAX, RL>(vx, tokg, nxt, true, rmn);
             // ---- P . V on MFMA: A = P[head l16][tokens], B = V[tokens][channel tile]
             if (!__all(alpha == 1.0f)) {                      // some head's running max moved
                 float ar[4];
@@ -1223,8 +1317,10 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
                 for (int ct = 0; ct < 8; ++ct) {
                     const uint32_t ad = tb + (uint32_t)(((ct * 16 + l16) * VT_STRIDE + kv * 32 + q4 * 4) * 2);
                     const u32x2 v0 = lds_ld<u32x2>(ad), v1 = lds_ld<u32x2>(ad + 32);
-                    lds_st<u32x2>(ad, u32x2{0u, 0u});
-                    lds_st<u32x2>(ad + 32, u32x2{0u, 0u});
+                    if (RL >= 0) {
+                        lds_st<u32x2>(ad, u32x2{0u, 0u});
+                        lds_st<u32x2>(ad + 32, u32x2{0u, 0u});
+                    }
                     bv[ct] = __builtin_bit_cast(M8, u32x4{v0.x, v0.y, v1.x, v1.y});
                 }
 #pragma unroll
@@ -1234,9 +1330,15 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             cur = nxt;
         }
     };
-    if (!all16) chunks(IntC<0>{});
-    else if (RMAX > 32 && rsplit <= 32) chunks(IntC<4>{});
-    else chunks(IntC<RMAX / 8>{});
+    bool done = false;
+    if constexpr (RMAX >= D) {
+        if (all16 && dense) { chunks(IntC<-1>{}); done = true; }
+    }
+    if (!done) {
+        if (!all16) chunks(IntC<0>{});
+        else if (RMAX > 32 && rsplit <= 32) chunks(IntC<4>{});
+        else chunks(IntC<RMAX / 8>{});
+    }
     // ---- merge the waves' (m, l, acc) and write the split's partial
     __syncthreads();
     float *mrg = (float *)(wbase + wave * TILE_BYTES);      // [16][D + 2]

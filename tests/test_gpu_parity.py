@@ -27,6 +27,9 @@ CASES = {
     "mixed_strategies": (gen.spec("c2", ctx=(4096, 2500), hkv=4), {}),
     "keep_all_rho1": (gen.spec("c1", ctx=(333, 200), hkv=2), dict(force_default=True, default=(128, 1, 4),
                                                                   select=(1, 1))),
+    # the sequence-only (quest) mode: every channel kept, 16-token blocks, no rotation
+    "quest_mode": (gen.spec("c3", ctx=(2500, 700), hkv=2, rotate=False), dict(force_default=True,
+                                                                              default=(128, 1, 16))),
     # kept counts outside 16/32/48: the general (runtime trip count) walks
     "odd_keeps": (gen.spec("c2", ctx=(1500, 900), hkv=2), dict(keep_cand=(8, 24, 40), default=(24, 2, 8),
                                                             tau_channel=0.2)),
