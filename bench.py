@@ -17,6 +17,7 @@ shape, the compression pass and the CPU oracle on a bounded sample.
 from __future__ import annotations
 
 import argparse
+import ctypes as C
 import concurrent.futures as cf
 import hashlib
 import json
@@ -49,6 +50,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--no-rotations", action="store_true", help="skip timing the GPU rotation computation")
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="only run 5 device-to-device copies of MIB MiB (the reference kernel that scales the "
                          "FETCH_SIZE / WRITE_SIZE counters to bytes) and exit")
@@ -153,6 +155,23 @@ def main():
     compress_ms = e0.elapsed_time(e1)
     stats = cache.stats()
     log(f"data {t_gen:.1f}s, compress {compress_ms:.2f} ms, ratio {stats['ratio']:.3f}")
+    # the rotation matrices computed on the GPU from the same K/V (covariance
+    # and Jacobi eigensolver; the cache above used the host's rotations)
+    rotations_ms = None
+    if spec.rotate and not args.no_rotations:
+        rws = torch.empty(0, dtype=torch.uint8, device=dev)
+        rk_g, rv_g = M.compute_rotations(params, lay["k"], lay["v"], lay["ctx_lens"], cap)
+        n = C.c_size_t()
+        M.load().mosaic_rotation_workspace_bytes(C.byref(params.to_c()), spec.num_seqs, cap, C.byref(n))
+        rws = torch.empty(n.value, dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        e0.record()
+        M.compute_rotations(params, lay["k"], lay["v"], lay["ctx_lens"], cap, ws=rws)
+        e1.record()
+        torch.cuda.synchronize()
+        rotations_ms = e0.elapsed_time(e1)
+        del rk_g, rv_g, rws
+        log(f"rotations on the GPU {rotations_ms:.2f} ms")
 
     flush = torch.empty(args.flush_mb << 20, dtype=torch.uint8, device=dev)
     out = torch.empty((spec.num_seqs, spec.hq, D), dtype=torch.float32, device=dev)
@@ -284,7 +303,6 @@ def main():
         ctx = torch.tensor(lay["ctx_lens"], dtype=torch.int32, device=dev)
         dout = M.dense_decode(qd, kd, vd, ctx, scale, spec.max_ctx, spec.group)
         ws = torch.empty(1 << 20, dtype=torch.uint8, device=dev)
-        import ctypes as C
         n = C.c_size_t()
         M.load().mosaic_dense_workspace_bytes(spec.num_seqs, spec.hkv, spec.group, spec.max_ctx, C.byref(n))
         ws = torch.empty(n.value, dtype=torch.uint8, device=dev)
@@ -374,6 +392,7 @@ def main():
         "speedup_vs_dense": None if dense_us is None else round(dense_us / value, 2),
         "wall_ms_per_step_incl_flush": round(1e3 * wall / args.steps, 3),
         "compress_ms": round(compress_ms, 3), "memory_ratio": round(stats["ratio"], 4),
+        "rotations_ms": None if rotations_ms is None else round(rotations_ms, 3),
         "strategies": {f"{k[0]}/{k[1]}/{k[2]}": v for k, v in sorted(stats["strategies"].items())},
         "cpu_baseline": cpu, "parity": parity, "datagen_s": round(t_gen, 1), "source_hash": source_hash(),
     }

@@ -188,6 +188,34 @@ mosaic_status mosaic_append(mosaic_cache *cache, const void *k_new, const void *
 mosaic_status mosaic_decode_attention(mosaic_cache *cache, const void *q, float *out, float sm_scale,
                                       void *ws, size_t ws_bytes, void *stream);
 
+/* Rotation matrices computed from the cache on the GPU (Sec. 2.3; Sec. 5.2:
+ * once the KV cache exists, the SVD rotation of each window's K matrix and of
+ * its V matrix is computed; the paper does this on the host).  For every
+ * (sequence, kv head) and window w, R's rows are the eigenvectors of the
+ * uncentered covariance X^T X of the window's vectors X (tokens
+ * [w W, min((w + 1) W, ctx_len))), by descending eigenvalue, each signed so
+ * that its largest-magnitude component is positive.  A window past the last
+ * token repeats the last window that has tokens; a sequence with no token
+ * gets the identity.  The output is what mosaic_compress takes as rot_k/v.
+ *   params        : num_kv_heads, dtype, rot_window W (a multiple of 64)
+ *   k, v          : as for mosaic_compress ([num_seqs][num_kv_heads][seq_stride][128])
+ *   ctx_lens_host : [num_seqs], each <= max_tokens
+ *   rot_k, rot_v  : outputs [num_seqs][num_kv_heads][ceil(max_tokens / W)][128][128] fp32
+ *   evals_k/v     : optional outputs (both or neither) [...][ceil(max_tokens / W)][128]
+ *                   fp32, the eigenvalues in row order (descending)
+ *   ws            : at least mosaic_rotation_workspace_bytes bytes, 16-byte aligned
+ * Arithmetic: fp32 covariance (exact 16-bit products, one chain per element
+ * in token order per 4096-token slice, slices summed in order), cyclic Jacobi
+ * in fp32 until the off-diagonal energy is below 1e-14 of the diagonal's.
+ * Errors: INVALID (NULL, misaligned, bad shape, small workspace), CAPACITY
+ * (a context longer than max_tokens), UNSUPPORTED (head_dim != 128). */
+mosaic_status mosaic_rotation_workspace_bytes(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
+                                              size_t *bytes);
+mosaic_status mosaic_compute_rotations(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
+                                       const void *k, const void *v, int64_t seq_stride,
+                                       const int32_t *ctx_lens_host, float *rot_k, float *rot_v, float *evals_k,
+                                       float *evals_v, void *ws, size_t ws_bytes, void *stream);
+
 /* Uncompressed baseline: dense split-K decode attention over K/V laid out as
  * for mosaic_compress (the "Full" baseline of Sec. 6.1).
  *   ctx_lens: DEVICE int32 [num_seqs].  ws: mosaic_dense_workspace_bytes. */

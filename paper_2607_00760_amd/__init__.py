@@ -227,3 +227,35 @@ def dense_decode(q, k, v, ctx_lens_dev, sm_scale: float, max_ctx: int, group_siz
                                                 max_ctx, _ptr(ctx_lens_dev), float(sm_scale), _ptr(ws), ws.numel(),
                                                 _stream(k.device)))
     return out
+
+
+def compute_rotations(params: Params, k, v, ctx_lens, max_tokens: int, evals: bool = False, ws=None):
+    """Rotation matrices of every window from the cache itself (GPU covariance
+    and Jacobi eigensolver): k, v [S][Hkv][seq_stride][128] on the GPU,
+    ctx_lens a list of ints.  Returns (rot_k, rot_v) [S][Hkv][nw][128][128]
+    fp32, plus (evals_k, evals_v) [S][Hkv][nw][128] when evals is set."""
+    import torch
+    lib = load()
+    S, Hkv, stride, _ = k.shape
+    _check_tensor(k, "k", None, None)
+    _check_tensor(v, "v", k.dtype, k.device)
+    p = params.to_c()
+    p.num_kv_heads = Hkv
+    p.dtype = 1 if k.dtype == torch.bfloat16 else 0
+    n = C.c_size_t()
+    check(lib.mosaic_rotation_workspace_bytes(C.byref(p), S, max_tokens, C.byref(n)))
+    if ws is None or ws.numel() < n.value:
+        ws = torch.empty(n.value, dtype=torch.uint8, device=k.device)
+    nw = -(-max_tokens // params.rot_window)
+    rk = torch.empty((S, Hkv, nw, D, D), dtype=torch.float32, device=k.device)
+    rv = torch.empty_like(rk)
+    ek = ev = None
+    if evals:
+        ek = torch.empty((S, Hkv, nw, D), dtype=torch.float32, device=k.device)
+        ev = torch.empty_like(ek)
+    lens = (C.c_int32 * S)(*[int(x) for x in ctx_lens])
+    with torch.cuda.device(k.device):
+        check(lib.mosaic_compute_rotations(C.byref(p), S, max_tokens, _ptr(k), _ptr(v), stride, lens, _ptr(rk),
+                                           _ptr(rv), _ptr(ek) if evals else None, _ptr(ev) if evals else None,
+                                           _ptr(ws), ws.numel(), _stream(k.device)))
+    return (rk, rv, ek, ev) if evals else (rk, rv)

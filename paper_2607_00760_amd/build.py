@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmosaic.so")
 ARCH = os.environ.get("MOSAIC_OFFLOAD_ARCH", "gfx950")
-SOURCES = ["api.hip", "compress.hip", "decode.hip", "dense.hip"]
+SOURCES = ["api.hip", "compress.hip", "decode.hip", "dense.hip", "rotation.hip"]
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -366,6 +366,62 @@ mosaic_status mosaic_dense_decode_attention(const void *q, const void *k, const 
     return ok();
 }
 
+static mosaic_status rotation_shape(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens, int &nw) {
+    if (!params) return fail(MOSAIC_ERR_INVALID, "NULL params");
+    if (params->head_dim != 128) return fail(MOSAIC_ERR_UNSUPPORTED, "head_dim %d", params->head_dim);
+    if (params->num_kv_heads < 1 || num_seqs < 1 || max_tokens < 1)
+        return fail(MOSAIC_ERR_INVALID, "num_seqs %d, num_kv_heads %d, max_tokens %d", num_seqs, params->num_kv_heads,
+                    max_tokens);
+    if (params->rot_window < SEG || params->rot_window % SEG)
+        return fail(MOSAIC_ERR_INVALID, "rot_window %d: a positive multiple of %d", params->rot_window, SEG);
+    nw = (max_tokens + params->rot_window - 1) / params->rot_window;
+    return MOSAIC_OK;
+}
+
+mosaic_status mosaic_rotation_workspace_bytes(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
+                                              size_t *bytes) {
+    int nw = 0;
+    if (!bytes) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    const mosaic_status st = rotation_shape(params, num_seqs, max_tokens, nw);
+    if (st != MOSAIC_OK) return st;
+    *bytes = rotation_ws_bytes(num_seqs, params->num_kv_heads, nw, params->rot_window);
+    return ok();
+}
+
+mosaic_status mosaic_compute_rotations(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
+                                       const void *k, const void *v, int64_t seq_stride,
+                                       const int32_t *ctx_lens_host, float *rot_k, float *rot_v, float *evals_k,
+                                       float *evals_v, void *ws, size_t ws_bytes, void *stream) {
+    int nw = 0;
+    const mosaic_status st = rotation_shape(params, num_seqs, max_tokens, nw);
+    if (st != MOSAIC_OK) return st;
+    if (!k || !v || !ctx_lens_host || !rot_k || !rot_v || !ws) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    if (params->dtype != MOSAIC_FP16 && params->dtype != MOSAIC_BF16) return fail(MOSAIC_ERR_INVALID, "dtype %d", params->dtype);
+    if (((uintptr_t)k | (uintptr_t)v | (uintptr_t)rot_k | (uintptr_t)rot_v | (uintptr_t)ws) % 16)
+        return fail(MOSAIC_ERR_INVALID, "k, v, rot_k, rot_v and ws must be 16-byte aligned");
+    if ((evals_k == nullptr) != (evals_v == nullptr)) return fail(MOSAIC_ERR_INVALID, "evals_k and evals_v: both or neither");
+    int maxL = 0;
+    for (int s = 0; s < num_seqs; ++s) {
+        const int L = ctx_lens_host[s];
+        if (L < 0) return fail(MOSAIC_ERR_INVALID, "ctx_lens[%d] = %d < 0", s, L);
+        if (L > max_tokens) return fail(MOSAIC_ERR_CAPACITY, "ctx_lens[%d] = %d > max_tokens %d", s, L, max_tokens);
+        maxL = std::max(maxL, L);
+    }
+    if (seq_stride < maxL || seq_stride < 1) return fail(MOSAIC_ERR_INVALID, "seq_stride %lld < longest context %d",
+                                                         (long long)seq_stride, maxL);
+    const size_t need = rotation_ws_bytes(num_seqs, params->num_kv_heads, nw, params->rot_window);
+    if (ws_bytes < need) return fail(MOSAIC_ERR_INVALID, "workspace %zu < %zu", ws_bytes, need);
+    hipStream_t s = (hipStream_t)stream;
+    int32_t *ctx_dev = (int32_t *)ws;
+    hipError_t e = hipMemcpyAsync(ctx_dev, ctx_lens_host, sizeof(int32_t) * num_seqs, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "copy of context lengths");
+    e = launch_rotations((const uint16_t *)k, (const uint16_t *)v, seq_stride, num_seqs, params->num_kv_heads,
+                         params->dtype, ctx_dev, params->rot_window, nw, rot_k, rot_v, evals_k, evals_v,
+                         (float *)((uint8_t *)ws + rotation_ctx_bytes(num_seqs)), s);
+    if (e != hipSuccess) return hip_fail(e, "rotation launch");
+    return ok();
+}
+
 mosaic_status mosaic_cache_stats(const mosaic_cache *c, mosaic_stats *out, void *stream) {
     if (!c || !out) return fail(MOSAIC_ERR_INVALID, "NULL argument");
     if (!c->arena || !c->compressed) return fail(MOSAIC_ERR_STATE, "stats before compress");

@@ -148,6 +148,11 @@ hipError_t launch_dense(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                         float scale, float *part, int max_splits, hipStream_t s);
 
 size_t dense_part_bytes(int npairs, int G, int max_ctx);
+size_t rotation_ctx_bytes(int num_seqs);
+size_t rotation_ws_bytes(int num_seqs, int hkv, int nw, int W);
+hipError_t launch_rotations(const uint16_t *k, const uint16_t *v, int64_t seq_stride, int num_seqs, int hkv,
+                            int dtype, const int32_t *ctx_dev, int W, int nw, float *rot_k, float *rot_v, float *ev_k,
+                            float *ev_v, float *part, hipStream_t s);
 
 constexpr int MAINT_APPEND = 0;        // after an append: flush or finalize where a buffer filled
 constexpr int MAINT_AFTER_PREFILL = 1; // after compress: flush a >= U-token remainder

@@ -1,0 +1,113 @@
+"""GPU rotation matrices (fp32 covariance and cyclic Jacobi on the GPU,
+mosaic_compute_rotations) against the rotation oracle (fp64 covariance,
+numpy eigh).  Eigenvectors of close eigenvalues are not unique, so the checks
+are the properties that define the result: orthonormal rows, the rotated
+covariance R C R^T diagonal (off-diagonal energy) with the oracle's
+eigenvalues on its diagonal in descending order, the sign rule, the
+eigenvectors themselves where a wide eigenvalue gap isolates them, window
+repetition past the last token and the identity for an empty sequence.
+
+Tolerances (relative to the largest eigenvalue): the covariance is summed in
+fp32 over up to 4096 tokens per chain (exact 16-bit products), then the
+Jacobi rotations accumulate fp32 rounding over a few thousand steps; 5e-5 of
+the largest eigenvalue bounds both with margin, and an eigenvector whose gap
+to its neighbours is g (relative) moves by about that error over g.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_00760_amd as M
+from oracle import rotation as RO
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+D = 128
+TOL = 5e-5
+
+CASES = {
+    "outliers_fp16": gen.spec("c1", ctx=(2500, 700, 0), hkv=2, rot_window=1024),
+    "gauss_bf16": gen.spec("c3", ctx=(1500, 64), hkv=2, kind="gauss", rot_window=1024),
+    "student_bf16": gen.spec("c5", ctx=(3000, 100), hkv=2, rot_window=2048, appends=0),
+    # one window of 65536 tokens (16 covariance slices) and a short second one
+    "long_window": gen.spec("c3", ctx=(70000,), hkv=1, kind="gauss"),
+}
+
+
+def _check_window(Rg, eg, Ro, eo, X, where):
+    lam = max(float(eo[0]), 1e-30)
+    assert np.abs(Rg @ Rg.T - np.eye(D)).max() <= 3e-5, f"{where}: rows not orthonormal"
+    Cm = X.T @ X
+    Mr = Rg @ Cm @ Rg.T
+    dg = np.diag(Mr)
+    assert np.abs(dg - eo).max() <= TOL * lam, f"{where}: Rayleigh quotients vs oracle eigenvalues"
+    assert np.abs(Mr - np.diag(dg)).max() <= TOL * lam, f"{where}: rotated covariance not diagonal"
+    assert np.abs(eg - eo).max() <= TOL * lam, f"{where}: eigenvalues"
+    assert np.all(np.diff(eg) <= 0), f"{where}: eigenvalues not descending"
+    top = np.argmax(np.abs(Rg), axis=1)
+    assert np.all(Rg[np.arange(D), top] > 0), f"{where}: sign rule"
+    gaps = np.abs(np.diff(eo))
+    gap = np.minimum(np.concatenate([[np.inf], gaps]), np.concatenate([gaps, [np.inf]])) / lam
+    srt = np.sort(np.abs(Ro), axis=1)
+    clear_sign = (srt[:, -1] - srt[:, -2]) > 1e-3                  # largest component not nearly tied
+    iso = np.nonzero((gap > 1e-2) & clear_sign)[0]
+    for i in iso:
+        err = np.abs(Rg[i] - Ro[i]).max()
+        assert err <= 2 * TOL / gap[i] + 1e-5, f"{where}: eigenvector {i} (gap {gap[i]:.3g}) off by {err:.3g}"
+    return len(iso)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_rotations_match_oracle(name):
+    spec = CASES[name]
+    print(f"[rotation] {name} ctx={spec.ctx} W={spec.rot_window} {spec.dtype}", flush=True)
+    cap = spec.max_ctx
+    lay = gen.make_layer(spec, 0, capacity=cap)
+    params = M.Params(num_kv_heads=spec.hkv, group_size=spec.group, dtype=spec.dtype, rot_window=spec.rot_window)
+    k, v = lay["k"].cuda(), lay["v"].cuda()
+    rk, rv, ek, ev = M.compute_rotations(params, k, v, spec.ctx, cap, evals=True)
+    torch.cuda.synchronize()
+    out = {"k": (rk.double().cpu().numpy(), ek.double().cpu().numpy()),
+           "v": (rv.double().cpu().numpy(), ev.double().cpu().numpy())}
+    nw = -(-cap // spec.rot_window)
+    n_iso = 0
+    for b in range(spec.num_seqs):
+        L = spec.ctx[b]
+        for h in range(spec.hkv):
+            for which in ("k", "v"):
+                x = lay[which][b, h].double().numpy()          # 16-bit inputs, exact in fp64
+                Ro, eo = RO.rotations(x, L, spec.rot_window, nw)
+                Rg, eg = out[which][0][b, h], out[which][1][b, h]
+                nwt = -(-L // spec.rot_window)
+                if nwt == 0:
+                    for w in range(nw):
+                        assert np.array_equal(Rg[w], np.eye(D)) and not eg[w].any(), f"{name}: empty sequence"
+                    continue
+                for w in range(nw):
+                    if w >= nwt:
+                        assert np.array_equal(Rg[w], Rg[nwt - 1]), f"{name}: window {w} repeats {nwt - 1}"
+                        continue
+                    a, e = w * spec.rot_window, min((w + 1) * spec.rot_window, L)
+                    n_iso += _check_window(Rg[w], eg[w], Ro[w], eo[w], x[a:e], f"{name} seq {b} head {h} {which} w{w}")
+    print(f"[rotation] {name}: {n_iso} isolated eigenvectors compared", flush=True)
+
+
+def test_rotations_feed_compress():
+    """The GPU rotations, given to mosaic_compress, compress exactly as the
+    oracle does with the same matrices."""
+    from _parity import assert_state_equal, bits, gpu_cache, params_pair
+    from oracle import oracle as O
+    spec = gen.spec("c2", ctx=(1500, 700), hkv=2, rot_window=1024)
+    cap = spec.max_ctx
+    lay = gen.make_layer(spec, 0, capacity=cap)
+    lp, op = params_pair(spec)
+    rk, rv = M.compute_rotations(lp, lay["k"].cuda(), lay["v"].cuda(), spec.ctx, cap)
+    lay = dict(lay, rot_k=rk.cpu(), rot_v=rv.cpu())
+    c = gpu_cache(lp, spec, lay, cap)
+    for pi in range(spec.num_seqs * spec.hkv):
+        b, h = divmod(pi, spec.hkv)
+        L = spec.ctx[b]
+        pr = O.Pair(op, cap, lay["rot_k"][b, h].numpy(), lay["rot_v"][b, h].numpy())
+        pr.compress(bits(lay["k"][b, h, :L]), bits(lay["v"][b, h, :L]))
+        assert_state_equal(c, pi, pr, where=f"gpu rotations pair {pi}")
