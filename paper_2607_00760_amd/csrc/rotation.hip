@@ -4,13 +4,10 @@
 // rotated by it).  The rows of R are the right singular vectors of the
 // window's matrix X, i.e. the eigenvectors of X^T X by descending eigenvalue.
 //
-//   k_cov    : uncentered covariance X^T X in fp32.  The 16-bit inputs make
-//              every product exact in fp32; each element is one fused chain in
-//              token order over a 4096-token slice, and the slices are summed
-//              in slice order by the solver, so the result does not depend on
-//              scheduling.  A workgroup stages 64 tokens at a time in LDS and
-//              thread (ti, tj) owns the 8 x 8 tile of rows 8 ti.. and columns
-//              8 tj.. (64 FMAs per four 16-byte LDS reads).
+//   k_cov    : uncentered covariance X^T X on the matrix cores (16x16x32,
+//              16-bit operands: every product is exact, fp32 accumulation)
+//              over 4096-token slices; the solver sums the slices in slice
+//              order, so the result does not depend on scheduling.
 //   k_jacobi : one workgroup per matrix: A and the accumulated rotations V in
 //              LDS (rows padded to 129 floats), cyclic Jacobi with the
 //              round-robin ordering that pairs all 128 indices into 64
@@ -36,47 +33,92 @@ constexpr int COV_TILE = 64;      // tokens staged per round
 constexpr int JP = D + 1;         // padded LDS row of the solver
 constexpr int JACOBI_MAX_SWEEPS = 40;
 
-// grid (slices, windows, pairs * 2); z = 2 * pair + (0: K, 1: V)
+typedef float cov_f4 __attribute__((ext_vector_type(4)));
+
+template <int DT> struct CovMma;
+template <> struct CovMma<1> {
+    typedef __bf16 v8 __attribute__((ext_vector_type(8)));
+    static __device__ __forceinline__ cov_f4 run(v8 a, v8 b, cov_f4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+};
+template <> struct CovMma<0> {
+    typedef _Float16 v8 __attribute__((ext_vector_type(8)));
+    static __device__ __forceinline__ cov_f4 run(v8 a, v8 b, cov_f4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+    }
+};
+
+// grid (slices, windows, pairs * 2); z = 2 * pair + (0: K, 1: V).  C = X^T X
+// on the matrix cores: both operands are "8 consecutive tokens of one
+// channel", so each 64-token tile is staged channel-major in LDS (the lanes
+// of a store write 64 consecutive tokens of one channel; rows padded to 72
+// elements so that the 16 lanes of an operand read spread over the banks).
+// Wave w owns output rows 32 w .. 32 w + 31 (2 x 8 tiles of 16 x 16).
+template <int DT>
 __global__ void __launch_bounds__(256) k_cov(const uint16_t *k, const uint16_t *v, int64_t seq_stride, int hkv,
-                                             int dtype, const int32_t *ctx, int W, int nslices, float *part) {
-    __shared__ __align__(16) float xs[COV_TILE][D];
+                                             const int32_t *ctx, int W, int nslices, float *part) {
+    using M8 = typename CovMma<DT>::v8;
+    constexpr int XS = COV_TILE + 8;                       // elements per staged channel row
+    __shared__ __align__(16) uint16_t xt[D * XS];
     const int sl = blockIdx.x, w = blockIdx.y, z = blockIdx.z, p = z >> 1, kv = z & 1;
-    const int tid = threadIdx.x, ti = tid >> 4, tj = tid & 15;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, q4 = lane >> 4;
     const int L = ctx[p / hkv];
     const int64_t a = (int64_t)w * W + (int64_t)sl * COV_SLICE;
     const int64_t b = min(min((int64_t)(w + 1) * W, (int64_t)L), a + COV_SLICE);
     const uint16_t *src = (kv ? v : k) + (uint64_t)p * (uint64_t)seq_stride * D;
-    float acc[8][8];
+    cov_f4 acc[2][8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int r = 0; r < 2; ++r)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] = 0.0f;
+        for (int c = 0; c < 8; ++c) acc[r][c] = cov_f4{0.0f, 0.0f, 0.0f, 0.0f};
+    const uint32_t xa = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t *)xt;
     for (int64_t t0 = a; t0 < b; t0 += COV_TILE) {
         const int n = (int)min((int64_t)COV_TILE, b - t0);
         __syncthreads();                                   // previous tile consumed
-        for (int i = tid; i < COV_TILE * D; i += 256) {
-            const int t = i / D, c = i % D;
-            xs[t][c] = (t < n) ? h2f(src[(uint64_t)(t0 + t) * D + c], dtype) : 0.0f;
+        {
+            const int t = lane;                            // token of this lane; octets wave, wave + 4, ...
+            uint4 val[4];
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const int o = wave + 4 * kk;
+                val[kk] = (t < n) ? *(const uint4 *)(src + (uint64_t)(t0 + t) * D + 8 * o) : make_uint4(0u, 0u, 0u, 0u);
+            }
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const int o = wave + 4 * kk;
+                const uint32_t wv[4] = {val[kk].x, val[kk].y, val[kk].z, val[kk].w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    xt[(8 * o + e) * XS + t] = (uint16_t)((e & 1) ? (wv[e >> 1] >> 16) : wv[e >> 1]);
+            }
         }
         __syncthreads();
-        for (int t = 0; t < n; ++t) {
-            const float4 r0 = *(const float4 *)&xs[t][8 * ti], r1 = *(const float4 *)&xs[t][8 * ti + 4];
-            const float4 c0 = *(const float4 *)&xs[t][8 * tj], c1 = *(const float4 *)&xs[t][8 * tj + 4];
-            const float r[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
-            const float c[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
+        for (int ks = 0; ks < COV_TILE / 32; ++ks) {
+            M8 bo[8];
 #pragma unroll
-                for (int j = 0; j < 8; ++j) acc[i][j] = fmaf(r[i], c[j], acc[i][j]);
+            for (int c = 0; c < 8; ++c)
+                bo[c] = __builtin_bit_cast(M8, *(const __attribute__((address_space(3))) uint4 *)(uintptr_t)(
+                                                   xa + (uint32_t)(((16 * c + l16) * XS + 32 * ks + 8 * q4) * 2)));
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const M8 ao = __builtin_bit_cast(M8, *(const __attribute__((address_space(3))) uint4 *)(uintptr_t)(
+                                                         xa + (uint32_t)(((16 * (2 * wave + r) + l16) * XS + 32 * ks + 8 * q4) * 2)));
+#pragma unroll
+                for (int c = 0; c < 8; ++c) acc[r][c] = CovMma<DT>::run(ao, bo[c], acc[r][c]);
+            }
         }
     }
+    // accumulator layout: element e of tile (r, c) is row 4 q4 + e, column l16
     float *out = part + ((((uint64_t)z * gridDim.y + w) * nslices + sl) * D * D);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        float4 *o = (float4 *)(out + (uint64_t)(8 * ti + i) * D + 8 * tj);
-        o[0] = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
-        o[1] = make_float4(acc[i][4], acc[i][5], acc[i][6], acc[i][7]);
-    }
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                out[(uint64_t)(16 * (2 * wave + r) + 4 * q4 + e) * D + 16 * c + l16] = acc[r][c][e];
 }
 
 // position i of step s of the round-robin tournament over 128 indices
@@ -116,9 +158,12 @@ __global__ void __launch_bounds__(256) k_jacobi(const int32_t *ctx, int hkv, int
     const int ws = min(w, nwt - 1);                        // the window solved here
     const float *src = part + (((uint64_t)z * nw + ws) * nslices) * D * D;
     for (int i = tid; i < D * D; i += 256) {
+        // the matrix-core products round C[i][j] and C[j][i] separately: both
+        // halves take the upper triangle's value, so A is exactly symmetric
+        const int r = i / D, c = i % D, u = min(r, c) * D + max(r, c);
         float x = 0.0f;
-        for (int sl = 0; sl < nslices; ++sl) x += src[(uint64_t)sl * D * D + i];
-        A[(i / D) * JP + i % D] = x;
+        for (int sl = 0; sl < nslices; ++sl) x += src[(uint64_t)sl * D * D + u];
+        A[r * JP + c] = x;
         V[(i / D) * JP + i % D] = (i / D == i % D) ? 1.0f : 0.0f;
     }
     __syncthreads();
@@ -226,8 +271,12 @@ hipError_t launch_rotations(const uint16_t *k, const uint16_t *v, int64_t seq_st
                             float *ev_v, float *part, hipStream_t s) {
     const int npairs = num_seqs * hkv;
     const int nslices = (W + COV_SLICE - 1) / COV_SLICE;
-    hipLaunchKernelGGL(k_cov, dim3(nslices, nw, npairs * 2), dim3(256), 0, s, k, v, seq_stride, hkv, dtype, ctx_dev,
-                       W, nslices, part);
+    if (dtype == 1)
+        hipLaunchKernelGGL(k_cov<1>, dim3(nslices, nw, npairs * 2), dim3(256), 0, s, k, v, seq_stride, hkv, ctx_dev, W,
+                           nslices, part);
+    else
+        hipLaunchKernelGGL(k_cov<0>, dim3(nslices, nw, npairs * 2), dim3(256), 0, s, k, v, seq_stride, hkv, ctx_dev, W,
+                           nslices, part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const size_t smem = (size_t)2 * D * JP * sizeof(float);

@@ -7,8 +7,8 @@ eigenvalues on its diagonal in descending order, the sign rule, the
 eigenvectors themselves where a wide eigenvalue gap isolates them, window
 repetition past the last token and the identity for an empty sequence.
 
-Tolerances (relative to the largest eigenvalue): the covariance is summed in
-fp32 over up to 4096 tokens per chain (exact 16-bit products), then the
+Tolerances (relative to the largest eigenvalue): the covariance accumulates
+exact 16-bit products in fp32 over 4096-token slices, then the
 Jacobi rotations accumulate fp32 rounding over a few thousand steps; 5e-5 of
 the largest eigenvalue bounds both with margin, and an eigenvector whose gap
 to its neighbours is g (relative) moves by about that error over g.
