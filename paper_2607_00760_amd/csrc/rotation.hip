@@ -8,12 +8,14 @@
 //              16-bit operands: every product is exact, fp32 accumulation)
 //              over 4096-token slices; the solver sums the slices in slice
 //              order, so the result does not depend on scheduling.
-//   k_jacobi : one workgroup per matrix: A and the accumulated rotations V in
+//   k_jacobi : one 1024-thread workgroup per matrix: A and the accumulated rotations V in
 //              LDS (rows padded to 129 floats), cyclic Jacobi with the
 //              round-robin ordering that pairs all 128 indices into 64
-//              disjoint rotations per step (127 steps per sweep), rows of A,
-//              then columns of A and V, sweeps until the off-diagonal energy
-//              is below 1e-14 of the diagonal's (at most 40).  Then the
+//              disjoint rotations per step (127 steps per sweep), A updated
+//              one 2 x 2 block (rows of one pair, columns of another) per
+//              thread and V by columns in the same pass, sweeps until the
+//              off-diagonal energy is below 1e-12 of the diagonal's (at most
+//              30).  Then the
 //              eigenvalues are ranked (descending, index ascending on ties)
 //              and each eigenvector is written as row rank of R, normalized
 //              and signed so that its largest-magnitude component is
@@ -31,7 +33,7 @@ namespace {
 constexpr int COV_SLICE = 4096;   // tokens per covariance workgroup
 constexpr int COV_TILE = 64;      // tokens staged per round
 constexpr int JP = D + 1;         // padded LDS row of the solver
-constexpr int JACOBI_MAX_SWEEPS = 40;
+constexpr int JACOBI_MAX_SWEEPS = 30;
 
 typedef float cov_f4 __attribute__((ext_vector_type(4)));
 
@@ -124,23 +126,28 @@ __global__ void __launch_bounds__(256) k_cov(const uint16_t *k, const uint16_t *
 // position i of step s of the round-robin tournament over 128 indices
 __device__ __forceinline__ int rr_index(int i, int s) { return i == 0 ? 0 : 1 + (i - 1 + s) % (D - 1); }
 
-// sum over the 256 threads of the block; red: 4 floats of LDS
-__device__ __forceinline__ float block_sum_256(float x, float *red) {
-    x = tree64(x);                                         // lane 63's tree over the wave (broadcast)
+constexpr int JT = 1024;          // threads of a solver workgroup
+
+// sum over the JT threads of the block (fixed order); red: JT / 64 floats of LDS
+__device__ __forceinline__ float block_sum_jt(float x, float *red) {
+    x = tree64(x);                                         // the wave's tree (every lane holds it)
     const int tid = threadIdx.x;
     __syncthreads();
     if ((tid & 63) == 0) red[tid >> 6] = x;
     __syncthreads();
-    return (red[0] + red[1]) + (red[2] + red[3]);
+    float t = 0.0f;
+#pragma unroll
+    for (int i = 0; i < JT / 64; ++i) t += red[i];
+    return t;
 }
 
 // grid (windows, pairs * 2); dynamic LDS: A and V [D][JP] floats
-__global__ void __launch_bounds__(256) k_jacobi(const int32_t *ctx, int hkv, int W, int nw, int nslices,
+__global__ void __launch_bounds__(JT) k_jacobi(const int32_t *ctx, int hkv, int W, int nw, int nslices,
                                                 const float *part, float *rot_k, float *rot_v, float *ev_k,
                                                 float *ev_v) {
     extern __shared__ __align__(16) float jsm[];
     float *A = jsm, *V = jsm + D * JP;
-    __shared__ float rc[64], rs[64], red[4];
+    __shared__ float rc[64], rs[64], red[JT / 64];
     __shared__ int rp[64], rq[64];
     __shared__ int s_done;
     const int w = blockIdx.x, z = blockIdx.y, p = z >> 1, kv = z & 1, tid = threadIdx.x;
@@ -150,14 +157,14 @@ __global__ void __launch_bounds__(256) k_jacobi(const int32_t *ctx, int hkv, int
     float *ev = (kv ? ev_v : ev_k);
     if (ev) ev += ((uint64_t)p * nw + w) * D;
     if (nwt == 0) {                                        // no token: the identity
-        for (int i = tid; i < D * D; i += 256) R[i] = (i / D == i % D) ? 1.0f : 0.0f;
+        for (int i = tid; i < D * D; i += JT) R[i] = (i / D == i % D) ? 1.0f : 0.0f;
         if (ev)
-            for (int i = tid; i < D; i += 256) ev[i] = 0.0f;
+            for (int i = tid; i < D; i += JT) ev[i] = 0.0f;
         return;
     }
     const int ws = min(w, nwt - 1);                        // the window solved here
     const float *src = part + (((uint64_t)z * nw + ws) * nslices) * D * D;
-    for (int i = tid; i < D * D; i += 256) {
+    for (int i = tid; i < D * D; i += JT) {
         // the matrix-core products round C[i][j] and C[j][i] separately: both
         // halves take the upper triangle's value, so A is exactly symmetric
         const int r = i / D, c = i % D, u = min(r, c) * D + max(r, c);
@@ -170,15 +177,15 @@ __global__ void __launch_bounds__(256) k_jacobi(const int32_t *ctx, int hkv, int
     for (int sweep = 0; sweep < JACOBI_MAX_SWEEPS; ++sweep) {
         // convergence: off-diagonal energy against the diagonal's
         float off = 0.0f, dia = 0.0f;
-        for (int i = tid; i < D * D; i += 256) {
+        for (int i = tid; i < D * D; i += JT) {
             const int r = i / D, c = i % D;
             const float x = A[r * JP + c];
             if (r == c) dia = fmaf(x, x, dia);
             else off = fmaf(x, x, off);
         }
-        off = block_sum_256(off, red);
-        dia = block_sum_256(dia, red);
-        if (tid == 0) s_done = !(off > 1e-14f * dia);
+        off = block_sum_jt(off, red);
+        dia = block_sum_jt(dia, red);
+        if (tid == 0) s_done = !(off > 1e-12f * dia);
         __syncthreads();
         if (s_done) break;
         for (int st = 0; st < D - 1; ++st) {
@@ -197,33 +204,34 @@ __global__ void __launch_bounds__(256) k_jacobi(const int32_t *ctx, int hkv, int
                 rp[tid] = pp; rq[tid] = qq; rc[tid] = c; rs[tid] = s;
             }
             __syncthreads();
-            // rows: A <- J^T A
-            for (int u = tid; u < 64 * D; u += 256) {
-                const int kk = u / D, j = u % D;
-                const float c = rc[kk], s = rs[kk];
-                float *ap = A + rp[kk] * JP, *aq = A + rq[kk] * JP;
-                const float x = ap[j], y = aq[j];
-                ap[j] = c * x - s * y;
-                aq[j] = s * x + c * y;
+            // A <- J^T A J one 2 x 2 block (rows of pair kk, columns of pair mm)
+            // at a time: the block's new value depends on the block only, so
+            // one pass suffices (rows first, then columns, per element)
+            for (int u = tid; u < 64 * 64; u += JT) {
+                const int kk = u >> 6, mm = u & 63;
+                const float ck = rc[kk], sk = rs[kk], cm = rc[mm], sm = rs[mm];
+                const int pk = rp[kk], qk = rq[kk], pm = rp[mm], qm = rq[mm];
+                const float bpp = A[pk * JP + pm], bpq = A[pk * JP + qm], bqp = A[qk * JP + pm], bqq = A[qk * JP + qm];
+                const float tpp = ck * bpp - sk * bqp, tpq = ck * bpq - sk * bqq;
+                const float tqp = sk * bpp + ck * bqp, tqq = sk * bpq + ck * bqq;
+                A[pk * JP + pm] = cm * tpp - sm * tpq;
+                A[qk * JP + qm] = sm * tqp + cm * tqq;
+                if (kk == mm) {                            // the rotated pair is zero by construction
+                    A[pk * JP + qm] = 0.0f;
+                    A[qk * JP + pm] = 0.0f;
+                } else {
+                    A[pk * JP + qm] = sm * tpp + cm * tpq;
+                    A[qk * JP + pm] = cm * tqp - sm * tqq;
+                }
             }
-            __syncthreads();
-            // columns: A <- A J, V <- V J
-            for (int u = tid; u < 64 * D; u += 256) {
-                const int kk = u % 64, i = u / 64;
-                const float c = rc[kk], s = rs[kk];
-                const int pp = rp[kk], qq = rq[kk];
-                float *ar = A + i * JP, *vr = V + i * JP;
-                const float x = ar[pp], y = ar[qq];
-                ar[pp] = c * x - s * y;
-                ar[qq] = s * x + c * y;
-                const float vx = vr[pp], vy = vr[qq];
-                vr[pp] = c * vx - s * vy;
-                vr[qq] = s * vx + c * vy;
-            }
-            __syncthreads();
-            if (tid < 64) {                                // the rotated pair is zero by construction
-                A[rp[tid] * JP + rq[tid]] = 0.0f;
-                A[rq[tid] * JP + rp[tid]] = 0.0f;
+            // V <- V J
+            for (int u = tid; u < 64 * D; u += JT) {
+                const int mm = u & 63, i = u >> 6;
+                const float cm = rc[mm], sm = rs[mm];
+                float *vr = V + i * JP;
+                const float x = vr[rp[mm]], y = vr[rq[mm]];
+                vr[rp[mm]] = cm * x - sm * y;
+                vr[rq[mm]] = sm * x + cm * y;
             }
             __syncthreads();
         }
@@ -280,7 +288,7 @@ hipError_t launch_rotations(const uint16_t *k, const uint16_t *v, int64_t seq_st
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const size_t smem = (size_t)2 * D * JP * sizeof(float);
-    hipLaunchKernelGGL(k_jacobi, dim3(nw, npairs * 2), dim3(256), smem, s, ctx_dev, hkv, W, nw, nslices, part, rot_k,
+    hipLaunchKernelGGL(k_jacobi, dim3(nw, npairs * 2), dim3(JT), smem, s, ctx_dev, hkv, W, nw, nslices, part, rot_k,
                        rot_v, ev_k, ev_v);
     return hipGetLastError();
 }
