@@ -51,6 +51,7 @@ def parse():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-rotations", action="store_true", help="skip timing the GPU rotation computation")
+    ap.add_argument("--no-extras", action="store_true", help="skip the append-path and encoding-overlap timings")
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="only run 5 device-to-device copies of MIB MiB (the reference kernel that scales the "
                          "FETCH_SIZE / WRITE_SIZE counters to bytes) and exit")
@@ -101,6 +102,79 @@ def source_hash():
 
 def log(msg):
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def update_path_us(M, gen, spec, params, dev):
+    """Append calls of the c3 batch shape (every (sequence, kv head) pair at
+    once) on a short cache: the call whose 32nd token fills the update buffer
+    (provisional flush, Sec. 5.4) and the call that completes a 64-token
+    segment (finalize with its own strategy), against a plain append."""
+    import torch
+    small = gen.spec(spec.name, ctx=(4096,) * spec.num_seqs, appends=64)
+    lay = gen.make_layer(small, 0, device=dev, capacity=small.capacity)
+    cache = M.MosaicCache(params, small.num_seqs, small.capacity, rotated=small.rotate, device=dev)
+    cache.compress(lay["k"], lay["v"], lay["ctx_lens"], lay["rot_k"], lay["rot_v"])
+    apps = [tuple(x.to(dev) for x in gen.make_appends(small, t)) for t in range(64)]
+    torch.cuda.synchronize()
+    times = []
+    for t in range(64):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        cache.append(*apps[t])
+        b.record()
+        torch.cuda.synchronize()
+        times.append(1e3 * a.elapsed_time(b))
+    plain = [x for i, x in enumerate(times) if i not in (31, 63)]
+    return {"pairs": small.num_seqs * small.hkv, "append_us": round(float(sorted(plain)[len(plain) // 2]), 1),
+            "append_with_flush_us": round(times[31], 1), "append_with_finalize_us": round(times[63], 1)}
+
+
+def encoding_overlap(cache, lay, dev, compress_ms):
+    """Compression of one layer on a second stream while a stand-in of the
+    next layer's prefill compute runs on the first (Sec. 5.5 asynchronous
+    encoding): bf16 GEMMs sized to take about as long as the compression."""
+    import torch
+    a = torch.randn(8192, 8192, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(8192, 8192, device=dev, dtype=torch.bfloat16)
+    c = torch.empty(8192, 8192, device=dev, dtype=torch.bfloat16)
+
+    def compute(n):
+        for _ in range(n):
+            torch.matmul(a, b, out=c)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    compute(2)
+    torch.cuda.synchronize()
+    e0.record()
+    compute(10)
+    e1.record()
+    torch.cuda.synchronize()
+    per = e0.elapsed_time(e1) / 10
+    n = max(1, int(round(compress_ms / per)))
+
+    def run(side):
+        torch.cuda.synchronize()
+        e0.record()
+        if side is None:
+            compute(n)
+            cache.compress(lay["k"], lay["v"], lay["ctx_lens"], lay["rot_k"], lay["rot_v"])
+        else:
+            side.wait_event(e0)
+            with torch.cuda.stream(side):
+                cache.compress(lay["k"], lay["v"], lay["ctx_lens"], lay["rot_k"], lay["rot_v"])
+            compute(n)
+            done = torch.cuda.Event()
+            done.record(side)
+            torch.cuda.current_stream().wait_event(done)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+    side = torch.cuda.Stream(device=dev)                   # default priority
+    serial = min(run(None) for _ in range(2))
+    overlapped = min(run(side) for _ in range(2))
+    compute_ms = n * per
+    return {"compute_ms": round(compute_ms, 2), "compress_ms": round(compress_ms, 2),
+            "serial_ms": round(serial, 2), "overlapped_ms": round(overlapped, 2),
+            "hidden_fraction": round((serial - overlapped) / compress_ms, 3)}
 
 
 def main():
@@ -172,6 +246,14 @@ def main():
         rotations_ms = e0.elapsed_time(e1)
         del rk_g, rv_g, rws
         log(f"rotations on the GPU {rotations_ms:.2f} ms")
+
+    update_path = None
+    overlap = None
+    if not args.no_extras:
+        update_path = update_path_us(M, gen, spec, params, dev)
+        log(f"append {update_path}")
+        overlap = encoding_overlap(cache, lay, dev, compress_ms)
+        log(f"encoding overlap {overlap}")
 
     flush = torch.empty(args.flush_mb << 20, dtype=torch.uint8, device=dev)
     out = torch.empty((spec.num_seqs, spec.hq, D), dtype=torch.float32, device=dev)
@@ -393,6 +475,7 @@ def main():
         "wall_ms_per_step_incl_flush": round(1e3 * wall / args.steps, 3),
         "compress_ms": round(compress_ms, 3), "memory_ratio": round(stats["ratio"], 4),
         "rotations_ms": None if rotations_ms is None else round(rotations_ms, 3),
+        "update_path": update_path, "encoding_overlap": overlap,
         "strategies": {f"{k[0]}/{k[1]}/{k[2]}": v for k, v in sorted(stats["strategies"].items())},
         "cpu_baseline": cpu, "parity": parity, "datagen_s": round(t_gen, 1), "source_hash": source_hash(),
     }
