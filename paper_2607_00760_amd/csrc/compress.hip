@@ -207,11 +207,11 @@ __device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log
     const int n = r >> log2g;
     const bool klo = rlo < n, khi = rhi < n;
     const uint64_t mlo = __ballot(klo), mhi = __ballot(khi);
-    // group flags in bitmap order
+    // group flags in bitmap order: group i's first channel is src = i * g of
+    // its half, whose kept flag is bit src of that half's ballot
     const int gph = 64 >> log2g;                 // groups per half
     const int src = (lane % gph) << log2g;
-    const int flo = __shfl((int)klo, src, WAVE), fhi = __shfl((int)khi, src, WAVE);
-    const bool flag = (lane < 2 * gph) && ((lane / gph) ? fhi : flo);
+    const bool flag = (lane < 2 * gph) && ((((lane / gph) ? mhi : mlo) >> src) & 1ull);
     const uint64_t bm = __ballot(flag);
     if (!active) return;
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
