@@ -208,3 +208,54 @@ def test_c4_one_layer_full_size_properties():
         acc += (p[:, m] @ V[m]) @ rv[w]
     want = acc / p.sum(1, keepdims=True)
     assert_close(out.cpu().numpy()[b, h * G:(h + 1) * G], want, "c4 attention over the GPU selection")
+
+
+def test_c3_quest_mode_full_size_sampled():
+    """The quest mode (every channel kept, 16-token blocks, no rotation) on the
+    full 8 x 131072 bf16 workload: sampled pairs against the oracle."""
+    spec = gen.spec("c3", rotate=False)
+    print(f"[fullsize] c3 quest mode {spec.num_seqs}x{spec.max_ctx}", flush=True)
+    cap = spec.capacity
+    lay = gen.make_layer(spec, 0, device="cuda", capacity=cap)
+    lp, op = params_pair(spec, force_default=True, default=(D, 1, 16))
+    c = gpu_cache(lp, spec, lay, cap)
+    q = lay["queries"]
+    out = c.decode(q, scale_of())
+    torch.cuda.synchronize()
+    pairs = _sample(spec.num_seqs * spec.hkv, 2, 5)
+    ops = _oracle_pairs(op, spec, lay, cap, pairs)
+    for pi, pr in ops.items():
+        assert_state_equal(c, pi, pr, where="c3 quest")
+    _check_decode(c, spec, ops, q, out, "c3 quest")
+
+
+def test_c3_gpu_rotations_full_size_sampled():
+    """GPU rotation matrices of the full c3 cache (256 matrices of 65536
+    tokens): sampled windows against the fp64 oracle (orthonormal rows,
+    diagonalized covariance, eigenvalues, sign rule)."""
+    import paper_2607_00760_amd as M
+    from oracle import rotation as RO
+    spec = gen.spec("c3")
+    print(f"[fullsize] c3 rotations {spec.num_seqs}x{spec.max_ctx}", flush=True)
+    cap = spec.capacity
+    lay = gen.make_layer(spec, 0, device="cuda", capacity=cap)
+    lp, _ = params_pair(spec)
+    rk, rv, ek, ev = M.compute_rotations(lp, lay["k"], lay["v"], spec.ctx, cap, evals=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(9)
+    for _ in range(3):
+        b, h, w = int(rng.integers(spec.num_seqs)), int(rng.integers(spec.hkv)), int(rng.integers(2))
+        for which, R, E in (("k", rk, ek), ("v", rv, ev)):
+            a, e = w * spec.rot_window, (w + 1) * spec.rot_window
+            x = lay[which][b, h, a:e].double().cpu().numpy()
+            Ro, eo = RO.window_rotation(x)
+            Rg = R[b, h, w].double().cpu().numpy()
+            eg = E[b, h, w].double().cpu().numpy()
+            lam = float(eo[0])
+            assert np.abs(Rg @ Rg.T - np.eye(D)).max() <= 3e-5, f"{which} {b} {h} {w}: orthonormal"
+            Mr = Rg @ (x.T @ x) @ Rg.T
+            assert np.abs(np.diag(Mr) - eo).max() <= 5e-5 * lam, f"{which} {b} {h} {w}: Rayleigh quotients"
+            assert np.abs(Mr - np.diag(np.diag(Mr))).max() <= 5e-5 * lam, f"{which} {b} {h} {w}: diagonal"
+            assert np.abs(eg - eo).max() <= 5e-5 * lam, f"{which} {b} {h} {w}: eigenvalues"
+            top = np.argmax(np.abs(Rg), axis=1)
+            assert np.all(Rg[np.arange(D), top] > 0), f"{which} {b} {h} {w}: sign rule"
