@@ -78,6 +78,9 @@ typedef struct {
     float tau_channel, tau_block;
     int32_t select_num, select_den;  /* rho = num / den */
     int32_t force_default;           /* 1: every segment uses the default */
+    int32_t trunc;                   /* channels represented (Sec. 5.2 channel truncation):
+                                        channels >= trunc are never kept and have no bitmap
+                                        bit; a multiple of 32 up to D (0 means D) */
 } orc_params;
 
 typedef struct {
@@ -222,11 +225,13 @@ int orc_topk_mask(const float *s, int n, int k, uint8_t *keep) {
     return 0;
 }
 
-/* kept-channel mask of one rotated vector for strategy (r, g) */
-static void keep_channels(const float *y, int r, int g, uint8_t *kch) {
+/* kept-channel mask of one rotated vector for strategy (r, g): the top r / g
+   groups among the first T / g (channels >= T are truncated, never kept) */
+static void keep_channels(const float *y, int r, int g, int T, uint8_t *kch) {
     float s[D]; uint8_t kg[D];
     orc_group_scores(y, g, s);
-    orc_topk_mask(s, D / g, r / g, kg);
+    for (int i = 0; i < D / g; ++i) kg[i] = 0;
+    orc_topk_mask(s, T / g, r / g, kg);
     for (int c = 0; c < D; ++c) kch[c] = kg[c / g];
 }
 
@@ -236,19 +241,21 @@ static void keep_channels(const float *y, int r, int g, uint8_t *kch) {
 /* i = group i kept][values: the r kept elements in ascending channel  */
 /* order, fp32 -> dtype RNE].                                          */
 /* ------------------------------------------------------------------ */
-int orc_bitmap_bytes(int g) { return D / (8 * g); }
-int orc_vec_bytes(int r, int g, int elem_bytes) { return r * elem_bytes + D / (8 * g); }
+static int trunc_of(const orc_params *P) { return (P->trunc > 0 && P->trunc < D) ? P->trunc : D; }
+int orc_bitmap_bytes_t(int g, int T) { return T / (8 * g); }
+int orc_vec_bytes_t(int r, int g, int elem_bytes, int T) { return r * elem_bytes + T / (8 * g); }
+int orc_bitmap_bytes(int g) { return orc_bitmap_bytes_t(g, D); }
+int orc_vec_bytes(int r, int g, int elem_bytes) { return orc_vec_bytes_t(r, g, elem_bytes, D); }
 
-static void pack_bitmap(const uint8_t *kch, int g, uint8_t *out) {
-    int nbits = D / g, nwords = nbits / 32;
-    for (int w = 0; w < nwords; ++w) {
-        uint32_t word = 0;
-        for (int b = 0; b < 32; ++b)
-            if (kch[(w * 32 + b) * g]) word |= 1u << b;
-        out[4 * w + 0] = (uint8_t)(word & 0xff);
-        out[4 * w + 1] = (uint8_t)((word >> 8) & 0xff);
-        out[4 * w + 2] = (uint8_t)((word >> 16) & 0xff);
-        out[4 * w + 3] = (uint8_t)((word >> 24) & 0xff);
+/* T / g bits, bit i = group i kept, least significant bit first in each
+   byte (for whole 32-bit words this is the little-endian word layout) */
+static void pack_bitmap(const uint8_t *kch, int g, int T, uint8_t *out) {
+    int nbytes = T / (8 * g);
+    for (int i = 0; i < nbytes; ++i) {
+        uint8_t byte = 0;
+        for (int b = 0; b < 8; ++b)
+            if (kch[(i * 8 + b) * g]) byte |= (uint8_t)(1u << b);
+        out[i] = byte;
     }
 }
 
@@ -266,8 +273,8 @@ static void pack_values(const float *y, const uint8_t *kch, int dtype, uint8_t *
 /* Public: pack one rotated vector (for layout tests). */
 void orc_pack_vector(const float *y, int r, int g, int dtype, uint8_t *out) {
     uint8_t kch[D];
-    keep_channels(y, r, g, kch);
-    pack_bitmap(kch, g, out);
+    keep_channels(y, r, g, D, kch);
+    pack_bitmap(kch, g, D, out);
     pack_values(y, kch, dtype, out + orc_bitmap_bytes(g));
 }
 
@@ -280,6 +287,7 @@ static int ilog2(int v) { int l = 0; while ((1 << l) < v) ++l; return l; }
 void orc_choose_strategy(const orc_params *P, const float *yk, const float *yv, int n,
                          int *r_out, int *g_out, int *b_out) {
     if (P->force_default) { *r_out = P->def_keep; *g_out = P->def_group; *b_out = P->def_block; return; }
+    const int T = trunc_of(P);
     float totk[64], totv[64], dk[9][64], dv[9][64];
     for (int t = 0; t < n; ++t) {
         float ek[D], ev[D];
@@ -288,7 +296,7 @@ void orc_choose_strategy(const orc_params *P, const float *yk, const float *yv, 
         for (int ci = 0; ci < 9; ++ci) {
             int r = P->keep_cand[ci / 3], g = P->group_cand[ci % 3];
             uint8_t kk[D], kv[D]; float mk[D], mv[D];
-            keep_channels(yk + t * D, r, g, kk); keep_channels(yv + t * D, r, g, kv);
+            keep_channels(yk + t * D, r, g, T, kk); keep_channels(yv + t * D, r, g, T, kv);
             for (int c = 0; c < D; ++c) { mk[c] = kk[c] ? 0.0f : ek[c]; mv[c] = kv[c] ? 0.0f : ev[c]; }
             dk[ci][t] = orc_tree_sum(mk, D); dv[ci][t] = orc_tree_sum(mv, D);
         }
@@ -335,22 +343,22 @@ static void block_mean(const float *yk, int b0, int B, float *mu) {
 
 /* Encode n tokens (n = S or U) with strategy (r, g, B) into a token-arena
    record and a score-arena record (Sec. 5.2 compressed KV encoding). */
-static void encode_segment(const float *yk, const float *yv, int n, int r, int g, int B, int dtype,
+static void encode_segment(const float *yk, const float *yv, int n, int r, int g, int B, int dtype, int T,
                            uint8_t *tok, uint8_t *sc) {
-    int bmb = orc_bitmap_bytes(g), vb = r * 2, rec = bmb + vb;
+    int bmb = orc_bitmap_bytes_t(g, T), vb = r * 2, rec = bmb + vb;
     uint8_t kch[D];
     for (int b0 = 0, bi = 0; b0 < n; b0 += B, ++bi) {
         uint8_t *blk = tok + (size_t)bi * B * 2 * rec;
         uint8_t *kbm = blk, *kval = blk + B * bmb, *vbm = kval + B * vb, *vval = vbm + B * bmb;
         for (int j = 0; j < B; ++j) {
             const float *k = yk + (size_t)(b0 + j) * D, *v = yv + (size_t)(b0 + j) * D;
-            keep_channels(k, r, g, kch); pack_bitmap(kch, g, kbm + j * bmb); pack_values(k, kch, dtype, kval + j * vb);
-            keep_channels(v, r, g, kch); pack_bitmap(kch, g, vbm + j * bmb); pack_values(v, kch, dtype, vval + j * vb);
+            keep_channels(k, r, g, T, kch); pack_bitmap(kch, g, T, kbm + j * bmb); pack_values(k, kch, dtype, kval + j * vb);
+            keep_channels(v, r, g, T, kch); pack_bitmap(kch, g, T, vbm + j * bmb); pack_values(v, kch, dtype, vval + j * vb);
         }
         float mu[D];
         block_mean(yk, b0, B, mu);
-        keep_channels(mu, r, g, kch);
-        pack_bitmap(kch, g, sc + (size_t)bi * rec);
+        keep_channels(mu, r, g, T, kch);
+        pack_bitmap(kch, g, T, sc + (size_t)bi * rec);
         pack_values(mu, kch, dtype, sc + (size_t)bi * rec + bmb);
     }
 }
@@ -359,9 +367,10 @@ static void encode_segment(const float *yk, const float *yv, int n, int r, int g
 /* Per-(sequence, kv head) cache state.                                */
 /* ------------------------------------------------------------------ */
 static int max_vec_bytes(const orc_params *P) {
-    int m = orc_vec_bytes(P->def_keep, P->def_group, 2);
+    const int T = trunc_of(P);
+    int m = orc_vec_bytes_t(P->def_keep, P->def_group, 2, T);
     for (int i = 0; i < 3; ++i) for (int j = 0; j < 3; ++j) {
-        int v = orc_vec_bytes(P->keep_cand[i], P->group_cand[j], 2);
+        int v = orc_vec_bytes_t(P->keep_cand[i], P->group_cand[j], 2, T);
         if (v > m) m = v;
     }
     return m;
@@ -427,8 +436,8 @@ static void finalize_segment(orc_pair *p) {
     rotate_tokens(p, p->stgv, S, nf * S, p->rv, yv);
     int r, g, B;
     orc_choose_strategy(P, yk, yv, S, &r, &g, &B);
-    int rec = orc_vec_bytes(r, g, 2);
-    encode_segment(yk, yv, S, r, g, B, P->dtype, p->tok + p->tok_tail, p->sc + p->sc_tail);
+    int rec = orc_vec_bytes_t(r, g, 2, trunc_of(P));
+    encode_segment(yk, yv, S, r, g, B, P->dtype, trunc_of(P), p->tok + p->tok_tail, p->sc + p->sc_tail);
     orc_desc *d = &p->desc[nf];
     d->tok_off = p->tok_tail; d->sc_off = p->sc_tail; d->first_block = (uint32_t)p->nblk_final;
     d->r = (uint8_t)r; d->log2g = (uint8_t)ilog2(g); d->log2b = (uint8_t)ilog2(B); d->flags = 0;
@@ -448,7 +457,7 @@ static void flush_provisional(orc_pair *p) {
     float *yk = (float *)malloc((size_t)U * D * sizeof(float)), *yv = (float *)malloc((size_t)U * D * sizeof(float));
     rotate_tokens(p, p->stgk, U, nf * S, p->rk, yk);
     rotate_tokens(p, p->stgv, U, nf * S, p->rv, yv);
-    encode_segment(yk, yv, U, r, g, B, P->dtype, p->tok + p->tok_tail, p->sc + p->sc_tail);
+    encode_segment(yk, yv, U, r, g, B, P->dtype, trunc_of(P), p->tok + p->tok_tail, p->sc + p->sc_tail);
     orc_desc *d = &p->desc[nf];
     d->tok_off = p->tok_tail; d->sc_off = p->sc_tail; d->first_block = (uint32_t)p->nblk_final;
     d->r = (uint8_t)r; d->log2g = (uint8_t)ilog2(g); d->log2b = (uint8_t)ilog2(B); d->flags = 1;
@@ -500,7 +509,7 @@ void orc_pair_info(const orc_pair *p, orc_info *o) {
                   + (uint64_t)o->n_buf * 2 * D * 2;
     if (o->prov) {
         const orc_desc *d = &p->desc[o->n_final];
-        int B = 1 << d->log2b, rec = orc_vec_bytes(d->r, 1 << d->log2g, 2);
+        int B = 1 << d->log2b, rec = orc_vec_bytes_t(d->r, 1 << d->log2g, 2, trunc_of(&p->P));
         o->nblk += P->update_buf / B;
         used += (uint64_t)P->update_buf * 2 * rec + (uint64_t)(P->update_buf / B) * rec;
     }
@@ -542,14 +551,15 @@ int orc_pair_scores(const orc_pair *p, const uint16_t *q, float *scores, int cap
         const orc_desc *d = &p->desc[di];
         int pos = di * P->seg_len, w = pos / P->rot_window;
         if (w != cur_w) { for (int h = 0; h < G; ++h) qrot32(p, q + (size_t)h * D, pos, qr[h]); cur_w = w; }
-        int g = 1 << d->log2g, B = 1 << d->log2b, r = d->r, rec = orc_vec_bytes(r, g, 2), bmb = orc_bitmap_bytes(g);
+        const int T = trunc_of(P);
+        int g = 1 << d->log2g, B = 1 << d->log2b, r = d->r, rec = orc_vec_bytes_t(r, g, 2, T), bmb = orc_bitmap_bytes_t(g, T);
         int nblk = desc_ntok(p, d) / B;
         for (int j = 0; j < nblk; ++j) {
             const uint8_t *rp = p->sc + d->sc_off + (size_t)j * rec;
             float best = 0.0f;
             for (int h = 0; h < G; ++h) {
                 float acc = 0.0f; int slot = 0;
-                for (int gi = 0; gi < D / g; ++gi) {
+                for (int gi = 0; gi < T / g; ++gi) {
                     if (!((rp[gi >> 3] >> (gi & 7)) & 1)) continue;
                     for (int e = 0; e < g; ++e) {
                         int c = gi * g + e;
@@ -577,10 +587,10 @@ int orc_select_count(int nblk, int num, int den) {
 }
 
 /* unpack one packed vector into dense fp64 (0 at dropped channels) */
-static void unpack64(const uint8_t *bm, const uint8_t *vals, int g, int dtype, double *out) {
+static void unpack64(const uint8_t *bm, const uint8_t *vals, int g, int T, int dtype, double *out) {
     int slot = 0;
     for (int gi = 0; gi < D / g; ++gi) {
-        int kept = (bm[gi >> 3] >> (gi & 7)) & 1;
+        int kept = gi < T / g ? (bm[gi >> 3] >> (gi & 7)) & 1 : 0;
         for (int e = 0; e < g; ++e) {
             int c = gi * g + e;
             if (kept) {
@@ -630,7 +640,7 @@ int orc_pair_decode(const orc_pair *p, const uint16_t *q, float scale, double *o
             }
             cur_w = w;
         }
-        int g = 1 << d->log2g, B = 1 << d->log2b, r = d->r, bmb = orc_bitmap_bytes(g), vb = 2 * r, rec = bmb + vb;
+        int g = 1 << d->log2g, B = 1 << d->log2b, r = d->r, bmb = orc_bitmap_bytes_t(g, trunc_of(P)), vb = 2 * r, rec = bmb + vb;
         int nblk = desc_ntok(p, d) / B;
         for (int j = 0; j < nblk; ++j, ++bglob) {
             if (!keep[bglob]) continue;
@@ -638,8 +648,8 @@ int orc_pair_decode(const orc_pair *p, const uint16_t *q, float scale, double *o
             const uint8_t *kbm = blk, *kval = blk + B * bmb, *vbm = kval + B * vb, *vval = vbm + B * bmb;
             for (int t = 0; t < B; ++t) {
                 double kd[D];
-                unpack64(kbm + t * bmb, kval + t * vb, g, P->dtype, kd);
-                unpack64(vbm + t * bmb, vval + t * vb, g, P->dtype, vv + (size_t)nt * D);
+                unpack64(kbm + t * bmb, kval + t * vb, g, trunc_of(P), P->dtype, kd);
+                unpack64(vbm + t * bmb, vval + t * vb, g, trunc_of(P), P->dtype, vv + (size_t)nt * D);
                 for (int h = 0; h < G; ++h) {
                     double a = 0.0;
                     for (int c = 0; c < D; ++c) a += qr[h][c] * kd[c];
@@ -718,7 +728,8 @@ void orc_dense_attention(const uint16_t *q, const uint16_t *k, const uint16_t *v
 
 /* Byte accounting per token of a full segment (for the ratio closed form):
    2 packed vectors per token plus one block key per B tokens. */
-double orc_bytes_per_token(int r, int g, int B, int elem_bytes) {
-    double v = (double)orc_vec_bytes(r, g, elem_bytes);
+double orc_bytes_per_token_t(int r, int g, int B, int elem_bytes, int T) {
+    double v = (double)orc_vec_bytes_t(r, g, elem_bytes, T);
     return 2.0 * v + v / (double)B;
 }
+double orc_bytes_per_token(int r, int g, int B, int elem_bytes) { return orc_bytes_per_token_t(r, g, B, elem_bytes, D); }

@@ -42,6 +42,7 @@ class OrcParams(C.Structure):
         ("def_keep", C.c_int32), ("def_group", C.c_int32), ("def_block", C.c_int32),
         ("tau_channel", C.c_float), ("tau_block", C.c_float),
         ("select_num", C.c_int32), ("select_den", C.c_int32), ("force_default", C.c_int32),
+        ("trunc", C.c_int32),
     ]
 
 
@@ -72,6 +73,7 @@ class Params:
     tau_block: float = 0.90
     select: tuple = (1, 10)
     force_default: bool = False
+    trunc: int = 128                # channels represented in the bitmap (Sec. 5.2 channel truncation)
 
     def to_c(self) -> OrcParams:
         p = OrcParams()
@@ -86,6 +88,7 @@ class Params:
         p.tau_channel, p.tau_block = self.tau_channel, self.tau_block
         p.select_num, p.select_den = self.select
         p.force_default = 1 if self.force_default else 0
+        p.trunc = self.trunc
         return p
 
 
@@ -111,6 +114,7 @@ def lib():
         L.orc_pack_vector.argtypes = [fp, C.c_int, C.c_int, C.c_int, u8p]; L.orc_pack_vector.restype = None
         L.orc_bitmap_bytes.argtypes = [C.c_int]; L.orc_bitmap_bytes.restype = C.c_int
         L.orc_vec_bytes.argtypes = [C.c_int, C.c_int, C.c_int]; L.orc_vec_bytes.restype = C.c_int
+        L.orc_vec_bytes_t.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int]; L.orc_vec_bytes_t.restype = C.c_int
         L.orc_choose_strategy.argtypes = [C.POINTER(OrcParams), fp, fp, C.c_int, i32p, i32p, i32p]
         L.orc_choose_strategy.restype = None
         L.orc_pair_new.argtypes = [C.POINTER(OrcParams), C.c_int, fp, fp, C.c_int]
@@ -131,6 +135,8 @@ def lib():
         L.orc_dense_attention.restype = None
         L.orc_bytes_per_token.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int]
         L.orc_bytes_per_token.restype = C.c_double
+        L.orc_bytes_per_token_t.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, C.c_int]
+        L.orc_bytes_per_token_t.restype = C.c_double
         _lib = L
     return _lib
 
@@ -200,8 +206,8 @@ def topk_mask(s, k):
     return keep.astype(bool)
 
 
-def vec_bytes(r, g, elem_bytes=2):
-    return lib().orc_vec_bytes(r, g, elem_bytes)
+def vec_bytes(r, g, elem_bytes=2, trunc=D):
+    return lib().orc_vec_bytes_t(r, g, elem_bytes, trunc)
 
 
 def bitmap_bytes(g):
@@ -228,8 +234,10 @@ def select_count(nblk, num, den):
     return lib().orc_select_count(nblk, num, den)
 
 
-def bytes_per_token(r, g, B, elem_bytes=2):
-    return lib().orc_bytes_per_token(r, g, B, elem_bytes)
+def bytes_per_token(r, g, B, elem_bytes=2, trunc=D):
+    """Bytes per token of a full segment: two packed vectors (K, V) and 1/B of
+    a block key; the bitmap represents the first trunc channels."""
+    return lib().orc_bytes_per_token_t(r, g, B, elem_bytes, trunc)
 
 
 def dense_attention(q, k, v, scale, dtype="fp16"):
@@ -294,7 +302,7 @@ class Pair:
         n = i.tok_tail
         if i.prov:
             d = self.descriptors()[-1]
-            n = d["tok_off"] + self.params.update_buf * 2 * vec_bytes(d["r"], 1 << d["log2g"])
+            n = d["tok_off"] + self.params.update_buf * 2 * vec_bytes(d["r"], 1 << d["log2g"], 2, self.params.trunc)
         return self._bytes("orc_pair_tok", n)
 
     def score_arena(self):
@@ -302,7 +310,8 @@ class Pair:
         n = i.sc_tail
         if i.prov:
             d = self.descriptors()[-1]
-            n = d["sc_off"] + (self.params.update_buf >> d["log2b"]) * vec_bytes(d["r"], 1 << d["log2g"])
+            n = d["sc_off"] + (self.params.update_buf >> d["log2b"]) * vec_bytes(d["r"], 1 << d["log2g"], 2,
+                                                                                self.params.trunc)
         return self._bytes("orc_pair_sc", n)
 
     def descriptors(self):

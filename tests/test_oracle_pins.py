@@ -459,3 +459,67 @@ def test_first_provisional_uses_default():
     d = pr.descriptors()
     assert len(d) == 1 and d[0]["flags"] == 1 and (d[0]["r"], d[0]["log2g"], d[0]["log2b"]) == (48, 1, 4)
     assert pr.info().n_buf == 8
+
+
+# ---------------------------------------------------------------- channel truncation (Sec. 5.2)
+def test_truncation_ratio_closed_form():
+    # 96-bit bitmaps at the default strategy: 2 (64 + 12) + (64 + 12) / 8 bytes per token
+    assert O.bitmap_bytes(1) == 16 and O.vec_bytes(32, 1, 2, 96) == 64 + 12
+    for g, T, bm in ((1, 96, 12), (2, 96, 6), (4, 96, 3), (1, 64, 8), (4, 128, 4)):
+        assert O.vec_bytes(32, g, 2, T) == 64 + bm
+    assert abs(512 / O.bytes_per_token(32, 1, 8, 2, 96) - 512 / 161.5) < 1e-12
+    P = O.Params(force_default=True, dtype="bf16", trunc=96)
+    pr = O.Pair(P, 640)
+    x = to_bits(rng(21).standard_normal((640, D)), "bf16")
+    pr.compress(x, x)
+    per_seg = 64 * 2 * (32 * 2 + 12) + 8 * (32 * 2 + 12) + 16
+    assert pr.info().used_bytes == 10 * per_seg
+
+
+@pytest.mark.parametrize("g", [1, 2, 4])
+def test_truncated_bitmap_is_brute_force_topk_of_leading_channels(g):
+    """Identity rotation, forced (32, g, 4): every packed K vector keeps the
+    top 32 / g groups among the first 96 / g by L1 score (lowest index on ties),
+    its bitmap is 96 / g bits LSB first, its values in ascending channel order."""
+    T, r, B = 96, 32, 4
+    P = O.Params(force_default=True, default=(r, g, B), dtype="fp16", trunc=T)
+    x = rng(22 + g).standard_normal((64, D)) * np.linspace(0.2, 3.0, D)[None, :]   # tail channels largest
+    kb = to_bits(x, "fp16")
+    pr = O.Pair(P, 64)
+    pr.compress(kb, kb)
+    tok = pr.token_arena()
+    y = from_bits(kb, "fp16")
+    bmb, vb = T // (8 * g), 2 * r
+    for t in range(64):
+        s = np.abs(y[t]).reshape(D // g, g).sum(axis=1)          # group L1 (g <= 4 adds in a pairwise order)
+        order = sorted(range(T // g), key=lambda i: (-s[i], i))[: r // g]
+        want_bits = np.zeros(T // g, np.uint8)
+        want_bits[order] = 1
+        blk = tok[(t // B) * B * 2 * (bmb + vb):]
+        bm = np.unpackbits(blk[(t % B) * bmb:(t % B + 1) * bmb], bitorder="little")
+        assert np.array_equal(bm, want_bits), t
+        ch = np.nonzero(np.repeat(want_bits, g))[0]
+        vals = blk[B * bmb + (t % B) * vb: B * bmb + (t % B + 1) * vb].view(np.uint16)
+        assert np.array_equal(vals, kb[t][ch]), t
+
+
+def test_truncated_keep_everything_equals_dense_over_leading_channels():
+    """r = T = 96, rho = 1, identity rotation: attention over the first 96
+    channels of K and V (the truncated ones read as zero); update-buffer
+    tokens stay dense, so they keep all channels."""
+    r_ = rng(23)
+    G, L, T = 4, 200, 96
+    P = O.Params(group=G, dtype="bf16", force_default=True, default=(T, 1, 8), select=(1, 1), rot_window=128,
+                 trunc=T)
+    k = to_bits(r_.standard_normal((L, D)), "bf16")
+    v = to_bits(r_.standard_normal((L, D)), "bf16")
+    q = to_bits(r_.standard_normal((G, D)), "bf16")
+    pr = O.Pair(P, L)
+    pr.compress(k, v)
+    out, _ = pr.decode(q, 1 / math.sqrt(D))
+    kz, vz = k.copy(), v.copy()
+    nc = (L // 64) * 64                        # compressed tokens; the rest is the update buffer
+    kz[:nc, T:] = 0
+    vz[:nc, T:] = 0
+    ref = _numpy_attention(q, kz, vz, 1 / math.sqrt(D), "bf16")
+    assert np.max(np.abs(out - ref)) < 1e-12
