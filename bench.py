@@ -40,6 +40,10 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="c3")
+    ap.add_argument("--trunc", type=int, default=128,
+                    help="channels represented in the bitmaps (channel truncation; 128 = none)")
+    ap.add_argument("--force-default", action="store_true",
+                    help="every segment takes the default strategy (32, 1, 8) instead of the search")
     ap.add_argument("--mode", choices=("mosaic", "quest"), default="mosaic",
                     help="quest: every channel kept, 16-token blocks, no rotation (sequence-only "
                          "compression on the same kernels)")
@@ -71,7 +75,7 @@ def algorithmic_bytes(cache, spec, nb_list, sel_list, desc_list):
     for p, (nb, sel, descs) in enumerate(zip(nb_list, sel_list, desc_list)):
         L = spec.ctx[p // spec.hkv]
         n_desc = len(descs)
-        rec = [2 * d[3] + (16 >> d[4]) for d in descs]
+        rec = [2 * d[3] + (((cache.params.trunc >> d[4]) + 31) // 32) * 4 for d in descs]
         blocks_per = [((32 if d[6] & 1 else 64) >> d[5]) for d in descs]
         tot["score"] += sum(r * n for r, n in zip(rec, blocks_per)) + 16 * n_desc
         # selected blocks -> descriptor (first_block ascending)
@@ -204,7 +208,9 @@ def main():
     # method parameters beyond the workload's: the quest mode keeps all D
     # channels of every vector in 16-token blocks, unrotated (the sequence-only
     # baseline of the paper's evaluation, run on this library's own kernels)
-    extra = {}
+    extra = {} if args.trunc == D else dict(trunc=args.trunc)
+    if args.force_default:
+        extra["force_default"] = True
     if args.mode == "quest":
         spec = gen.spec(args.config, ctx=spec.ctx, rotate=False)
         extra = dict(default=(D, 1, 16), force_default=True)
@@ -371,7 +377,7 @@ def main():
     achieved = ab[dom] / (kern_us[dom] * 1e-6) / 1e9
     traffic = None
     tf = os.path.join(ROOT, "profiles", f"traffic_{args.config}.json")
-    if os.path.exists(tf) and not args.ctx and args.mode == "mosaic":
+    if os.path.exists(tf) and not args.ctx and args.mode == "mosaic" and args.trunc == D and not args.force_default:
         t = json.load(open(tf))
         if t.get("source_hash") == source_hash() and t.get("kernel") == dom:
             traffic = t.get("bytes_per_launch")
@@ -459,7 +465,9 @@ def main():
                                f"{spec.max_ctx} tokens, {spec.hq} q / {spec.hkv} kv heads, d=128, {spec.dtype}, "
                                f"select 1/10 of blocks, planted 5% of segments"
                                + ("; quest mode: all channels kept, 16-token blocks, no rotation"
-                                  if args.mode == "quest" else ""),
+                                  if args.mode == "quest" else "")
+                               + (f"; bitmaps of the first {args.trunc} channels" if args.trunc != D else "")
+                               + ("; default strategy forced" if args.force_default else ""),
                    "mode": args.mode,
                    "num_seqs": spec.num_seqs, "ctx": spec.max_ctx, "q_heads": spec.hq, "kv_heads": spec.hkv,
                    "head_dim": D, "select": f"{spec.select[0]}/{spec.select[1]}", "mall_flush_mb": args.flush_mb},

@@ -71,11 +71,16 @@ typedef struct {
     int32_t select_num;        /* rho = select_num / select_den: blocks kept per */
     int32_t select_den;        /*   (sequence, kv head) = ceil(rho * blocks) */
     int32_t force_default_strategy; /* 1: skip the search, use the default */
+    int32_t trunc_channels;    /* T: channels represented in the bitmaps (Sec. 5.2 channel
+                                  truncation: after the rotation the last D - T channels are
+                                  never kept and get no bitmap bit); 32, 64, 96 or 128, at
+                                  least every kept count.  128 = no truncation */
 } mosaic_params;
 
 /* Fills *p with the paper's defaults (Sec. 5.5, Sec. 6.1): r in {16, 32, 48},
  * g in {4, 2, 1}, B in {16, 8, 4}, default (32, 1, 8), S = 64, U = 32,
- * W = 65536, tau = (0.30, 0.90), rho = 1/10, fp16, 8 kv heads, G = 4. */
+ * W = 65536, tau = (0.30, 0.90), rho = 1/10, fp16, 8 kv heads, G = 4,
+ * T = 128 (no truncation). */
 void mosaic_params_default(mosaic_params *p);
 
 typedef struct mosaic_cache mosaic_cache;  /* host bookkeeping + bound arena */

@@ -40,7 +40,8 @@
  * max over the group's query heads (R-8), buffer tokens always attended
  * dense and unrotated (R-9), provisional strategy = previous finalized
  * segment or the default (R-10), prefill remainder handled as appends
- * (R-11), y = x . R^T with row j of R the j-th rotated channel (R-12).
+ * (R-11), y = x . R^T with row j of R the j-th rotated channel (R-12), a
+ * truncated bitmap stored in whole 32-bit words (R-19).
  *
  * Exactly-defined orders (so that integer and byte results are unique):
  *  chain(a, b)  : acc = 0; for i ascending: acc = fmaf(a_i, b_i, acc)
@@ -80,7 +81,8 @@ typedef struct {
     int32_t force_default;           /* 1: every segment uses the default */
     int32_t trunc;                   /* channels represented (Sec. 5.2 channel truncation):
                                         channels >= trunc are never kept and have no bitmap
-                                        bit; a multiple of 32 up to D (0 means D) */
+                                        bit; a multiple of 32 up to D (0 means D); the
+                                        bitmap is rounded up to whole 32-bit words */
 } orc_params;
 
 typedef struct {
@@ -242,15 +244,17 @@ static void keep_channels(const float *y, int r, int g, int T, uint8_t *kch) {
 /* order, fp32 -> dtype RNE].                                          */
 /* ------------------------------------------------------------------ */
 static int trunc_of(const orc_params *P) { return (P->trunc > 0 && P->trunc < D) ? P->trunc : D; }
-int orc_bitmap_bytes_t(int g, int T) { return T / (8 * g); }
-int orc_vec_bytes_t(int r, int g, int elem_bytes, int T) { return r * elem_bytes + T / (8 * g); }
+/* a bitmap of T / g bits is stored in whole little-endian 32-bit words (reading R-19) */
+int orc_bitmap_bytes_t(int g, int T) { return ((T / g + 31) / 32) * 4; }
+int orc_vec_bytes_t(int r, int g, int elem_bytes, int T) { return r * elem_bytes + orc_bitmap_bytes_t(g, T); }
 int orc_bitmap_bytes(int g) { return orc_bitmap_bytes_t(g, D); }
 int orc_vec_bytes(int r, int g, int elem_bytes) { return orc_vec_bytes_t(r, g, elem_bytes, D); }
 
 /* T / g bits, bit i = group i kept, least significant bit first in each
-   byte (for whole 32-bit words this is the little-endian word layout) */
+   byte (the little-endian word layout), padded with zero bits to whole
+   32-bit words */
 static void pack_bitmap(const uint8_t *kch, int g, int T, uint8_t *out) {
-    int nbytes = T / (8 * g);
+    int nbytes = orc_bitmap_bytes_t(g, T);
     for (int i = 0; i < nbytes; ++i) {
         uint8_t byte = 0;
         for (int b = 0; b < 8; ++b)

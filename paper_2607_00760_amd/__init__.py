@@ -34,6 +34,7 @@ class Params:
     tau_block: float = 0.90
     select: tuple = (1, 10)
     force_default: bool = False
+    trunc: int = 128                 # channels represented in the bitmaps (Sec. 5.2 channel truncation)
 
     def to_c(self) -> MosaicParams:
         p = MosaicParams()
@@ -47,6 +48,7 @@ class Params:
         p.tau_channel, p.tau_block = self.tau_channel, self.tau_block
         p.select_num, p.select_den = self.select
         p.force_default_strategy = 1 if self.force_default else 0
+        p.trunc_channels = self.trunc
         return p
 
 

@@ -70,6 +70,7 @@ struct mosaic_cache {
         g.def_keep = P.default_keep; g.def_group = P.default_group; g.def_block = P.default_block;
         g.tau_ch = P.tau_channel; g.tau_blk = P.tau_block;
         g.sel_num = P.select_num; g.sel_den = P.select_den; g.force = P.force_default_strategy;
+        g.trunc = P.trunc_channels;
         return g;
     }
     WsGeom wsgeom(void *ws) const {
@@ -101,6 +102,7 @@ void mosaic_params_default(mosaic_params *p) {
     p->tau_channel = 0.30f; p->tau_block = 0.90f;
     p->select_num = 1; p->select_den = 10;
     p->force_default_strategy = 0;
+    p->trunc_channels = 128;
 }
 
 static mosaic_status check_params(const mosaic_params *p) {
@@ -129,6 +131,11 @@ static mosaic_status check_params(const mosaic_params *p) {
     if (std::isnan(p->tau_channel) || std::isnan(p->tau_block) || p->tau_channel < 0 || p->tau_block < 0)
         return fail(MOSAIC_ERR_INVALID, "thresholds must be >= 0");
     if (p->select_num < 1 || p->select_den < 1) return fail(MOSAIC_ERR_INVALID, "select ratio %d/%d", p->select_num, p->select_den);
+    const int T = p->trunc_channels;
+    if (T < 32 || T > 128 || T % 32) return fail(MOSAIC_ERR_INVALID, "trunc_channels %d: 32, 64, 96 or 128", T);
+    for (int i = 0; i < 3; ++i)
+        if (p->keep_cand[i] > T) return fail(MOSAIC_ERR_INVALID, "keep_cand[%d] = %d > trunc_channels %d", i, p->keep_cand[i], T);
+    if (p->default_keep > T) return fail(MOSAIC_ERR_INVALID, "default_keep %d > trunc_channels %d", p->default_keep, T);
     return MOSAIC_OK;
 }
 
@@ -447,7 +454,7 @@ mosaic_status mosaic_cache_stats(const mosaic_cache *c, mosaic_stats *out, void 
         int64_t used = (int64_t)meta[p].tok_tail + meta[p].sc_tail + 16ll * nd + (int64_t)nbuf * 2 * D * 2;
         if (prov) {
             const Desc &d = desc[nf];
-            const int rec = 2 * d.r + (16 >> d.log2g);
+            const int rec = vec_bytes(d.r, d.log2g, c->P.trunc_channels);
             used += (int64_t)UBUF * 2 * rec + (int64_t)(UBUF >> d.log2b) * rec;
         }
         out->used_bytes += used;

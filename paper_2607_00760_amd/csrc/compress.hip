@@ -84,7 +84,9 @@ __device__ __forceinline__ void rotate_tile(const uint16_t *src, int ntok, const
 
 // Group scores (L1 of magnitudes, pairwise) and exact ranks by
 // (score desc, group index asc) of the groups holding channels lane, lane+64.
-__device__ __forceinline__ void group_ranks(float ylo, float yhi, int log2g, uint64_t *keys,
+// Groups at or past ngt (truncated channels, Sec. 5.2) take key 0, below
+// every represented group, so they never rank among the kept ones.
+__device__ __forceinline__ void group_ranks(float ylo, float yhi, int log2g, int ngt, uint64_t *keys,
                                             int &rank_lo, int &rank_hi) {
     const int lane = threadIdx.x & 63;
     float slo = fabsf(ylo), shi = fabsf(yhi);
@@ -93,8 +95,8 @@ __device__ __forceinline__ void group_ranks(float ylo, float yhi, int log2g, uin
     if (log2g >= 2) { slo = slo + dpp_read<0x4e, 0xf>(slo); shi = shi + dpp_read<0x4e, 0xf>(shi); }
     const int ng = D >> log2g;
     const int glo = lane >> log2g, ghi = (64 >> log2g) + (lane >> log2g);
-    const uint64_t klo = ((uint64_t)__float_as_uint(slo) << 8) | (uint64_t)(255 - glo);
-    const uint64_t khi = ((uint64_t)__float_as_uint(shi) << 8) | (uint64_t)(255 - ghi);
+    const uint64_t klo = glo < ngt ? ((uint64_t)__float_as_uint(slo) << 8) | (uint64_t)(255 - glo) : 0ull;
+    const uint64_t khi = ghi < ngt ? ((uint64_t)__float_as_uint(shi) << 8) | (uint64_t)(255 - ghi) : 0ull;
     // keys is this wave's own array and a wave's LDS operations complete in
     // order, so keeping the compiler from moving memory operations across
     // these points is all the ordering the exchange needs (no barrier)
@@ -147,7 +149,7 @@ __device__ __forceinline__ void token_stats(const Geom &g, const float (&y)[TPW]
         for (int gi = 0; gi < 3; ++gi) {
             const int log2g = ilog2i(g.group_cand[gi]);
             int rlo, rhi;
-            group_ranks(ylo, yhi, log2g, keys, rlo, rhi);
+            group_ranks(ylo, yhi, log2g, g.trunc >> log2g, keys, rlo, rhi);
             for (int ri = 0; ri < 3; ++ri) {
                 const int n = g.keep_cand[ri] >> log2g;
                 float d = tree128(rlo < n ? 0.0f : elo, rhi < n ? 0.0f : ehi);
@@ -199,11 +201,11 @@ __device__ __forceinline__ void choose_strategy(const Geom &g, SegSmem &sm) {
 }
 
 // Pack one vector held as (lane: channel lane, lane+64): bitmap + values.
-__device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log2g, int dtype, uint64_t *keys,
+__device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log2g, int T, int dtype, uint64_t *keys,
                                             uint8_t *bm_out, uint8_t *val_out, bool active) {
     const int lane = threadIdx.x & 63;
     int rlo, rhi;
-    group_ranks(ylo, yhi, log2g, keys, rlo, rhi);
+    group_ranks(ylo, yhi, log2g, T >> log2g, keys, rlo, rhi);
     const int n = r >> log2g;
     const bool klo = rlo < n, khi = rhi < n;
     const uint64_t mlo = __ballot(klo), mhi = __ballot(khi);
@@ -223,7 +225,12 @@ __device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log
         int slot = __popcll(mlo) + __popcll(mhi & below);
         *(uint16_t *)(val_out + 2 * slot) = f2h(yhi, dtype);
     }
-    if (lane == 0) {
+    if (T < D) {
+        // a truncated bitmap (T / g bits in whole 32-bit words): lane i stores byte i
+        const uint64_t lo64 = log2g == 0 ? mlo : bm, hi64 = log2g == 0 ? mhi : 0ull;
+        const int nbytes = bm_bytes(log2g, T);
+        if (lane < nbytes) bm_out[lane] = (uint8_t)((lane < 8 ? lo64 >> (8 * lane) : hi64 >> (8 * (lane - 8))) & 0xffu);
+    } else if (lane == 0) {
         uint32_t *w = (uint32_t *)bm_out;
         if (log2g == 0) {
             w[0] = (uint32_t)mlo; w[1] = (uint32_t)(mlo >> 32); w[2] = (uint32_t)mhi; w[3] = (uint32_t)(mhi >> 32);
@@ -238,17 +245,17 @@ __device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log
 // Encode the workgroup's tokens (K in yk, V in yv) into the token arena at
 // tok and the block keys into the score arena at sc (Sec. 5.2).
 template <int B>
-__device__ __forceinline__ void pack_segment_B(const float (&yk)[TPW][2], const float (&yv)[TPW][2], int r, int log2g, int dtype,
-                               uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys) {
+__device__ __forceinline__ void pack_segment_B(const float (&yk)[TPW][2], const float (&yv)[TPW][2], int r, int log2g, int T,
+                               int dtype, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys) {
     const int wave = threadIdx.x >> 6, t0 = wave * TPW;
-    const int bmb = 16 >> log2g, vb = 2 * r, rec = bmb + vb;
+    const int bmb = bm_bytes(log2g, T), vb = 2 * r, rec = bmb + vb;
 #pragma unroll
     for (int i = 0; i < TPW; ++i) {
         const int t = t0 + i, bi = t / B, j = t % B;
         const bool act = t < ntok;
         uint8_t *blk = tok + (uint64_t)bi * B * 2 * rec;
-        pack_vector(yk[i][0], yk[i][1], r, log2g, dtype, keys, blk + j * bmb, blk + B * bmb + j * vb, act);
-        pack_vector(yv[i][0], yv[i][1], r, log2g, dtype, keys, blk + B * (bmb + vb) + j * bmb,
+        pack_vector(yk[i][0], yk[i][1], r, log2g, T, dtype, keys, blk + j * bmb, blk + B * bmb + j * vb, act);
+        pack_vector(yv[i][0], yv[i][1], r, log2g, T, dtype, keys, blk + B * (bmb + vb) + j * bmb,
                     blk + B * (2 * bmb + vb) + j * vb, act);
     }
 #pragma unroll
@@ -259,16 +266,16 @@ __device__ __forceinline__ void pack_segment_B(const float (&yk)[TPW][2], const 
         mlo = mlo * (1.0f / (float)B); mhi = mhi * (1.0f / (float)B);
         const int bi = (t0 + b0) / B;
         uint8_t *rp = sc + (uint64_t)bi * rec;
-        pack_vector(mlo, mhi, r, log2g, dtype, keys, rp, rp + bmb, t0 + b0 < ntok);
+        pack_vector(mlo, mhi, r, log2g, T, dtype, keys, rp, rp + bmb, t0 + b0 < ntok);
     }
 }
 
 __device__ __forceinline__ void pack_segment(const float (&yk)[TPW][2], const float (&yv)[TPW][2], int r, int log2g, int log2b,
-                             int dtype, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys) {
+                             int T, int dtype, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys) {
     switch (log2b) {
-        case 2: pack_segment_B<4>(yk, yv, r, log2g, dtype, tok, sc, ntok, keys); break;
-        case 3: pack_segment_B<8>(yk, yv, r, log2g, dtype, tok, sc, ntok, keys); break;
-        default: pack_segment_B<16>(yk, yv, r, log2g, dtype, tok, sc, ntok, keys); break;
+        case 2: pack_segment_B<4>(yk, yv, r, log2g, T, dtype, tok, sc, ntok, keys); break;
+        case 3: pack_segment_B<8>(yk, yv, r, log2g, T, dtype, tok, sc, ntok, keys); break;
+        default: pack_segment_B<16>(yk, yv, r, log2g, T, dtype, tok, sc, ntok, keys); break;
     }
 }
 
@@ -331,8 +338,8 @@ __global__ void __launch_bounds__(256) k_prefill(Geom g, const uint16_t *k, cons
         }
     } else {
         const Desc d = *desc;
-        pack_segment(yk, yv, d.r, d.log2g, d.log2b, g.dtype, g.tok_of(p) + d.tok_off, g.sc_of(p) + d.sc_off, SEG,
-                     sm.keys[wave]);
+        pack_segment(yk, yv, d.r, d.log2g, d.log2b, g.trunc, g.dtype, g.tok_of(p) + d.tok_off, g.sc_of(p) + d.sc_off,
+                     SEG, sm.keys[wave]);
     }
 }
 
@@ -351,7 +358,7 @@ __global__ void __launch_bounds__(256) k_scan(Geom g) {
         uint32_t tb = 0, sb = 0, nb = 0;
         if (s < nfull) {
             const Desc d = desc[s];
-            const uint32_t rec = (uint32_t)vec_bytes(d.r, d.log2g);
+            const uint32_t rec = (uint32_t)vec_bytes(d.r, d.log2g, g.trunc);
             tb = SEG * 2 * rec; nb = SEG >> d.log2b; sb = nb * rec;
         }
         s_tok[tid] = tb; s_sc[tid] = sb; s_blk[tid] = nb;
@@ -453,7 +460,8 @@ __global__ void __launch_bounds__(256) k_maintain(Geom g, int mode) {
     }
     const uint32_t tok_off = meta->tok_tail, sc_off = meta->sc_tail;
     const int nblk0 = meta->nblk_final;
-    pack_segment(yk, yv, r, log2g, log2b, g.dtype, g.tok_of(p) + tok_off, g.sc_of(p) + sc_off, ntok, sm.keys[wave]);
+    pack_segment(yk, yv, r, log2g, log2b, g.trunc, g.dtype, g.tok_of(p) + tok_off, g.sc_of(p) + sc_off, ntok,
+                 sm.keys[wave]);
     __syncthreads();
     if (threadIdx.x == 0) {
         Desc d;
@@ -461,7 +469,7 @@ __global__ void __launch_bounds__(256) k_maintain(Geom g, int mode) {
         d.r = (uint8_t)r; d.log2g = (uint8_t)log2g; d.log2b = (uint8_t)log2b; d.flags = finalize ? 0 : 1;
         desc[seg] = d;
         if (finalize) {
-            const uint32_t rec = (uint32_t)vec_bytes(r, log2g);
+            const uint32_t rec = (uint32_t)vec_bytes(r, log2g, g.trunc);
             meta->tok_tail = tok_off + SEG * 2 * rec;
             meta->sc_tail = sc_off + (SEG >> log2b) * rec;
             meta->nblk_final = nblk0 + (SEG >> log2b);

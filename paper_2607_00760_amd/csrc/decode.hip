@@ -230,6 +230,17 @@ __device__ __forceinline__ Walk make_walk(const uint32_t (&bw)[4], uint32_t a0, 
     return wk;
 }
 
+// A truncated bitmap (Sec. 5.2: only the first T channels are represented)
+// has T / g bits; the whole 16-byte bitmap loads read the values after it
+// as well, so the words are cut to the first nbits bits before a walk.
+__device__ __forceinline__ void mask_words(uint32_t (&bw)[4], int nbits) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int lo = 32 * k;
+        bw[k] = nbits >= lo + 32 ? bw[k] : (nbits <= lo ? 0u : bw[k] & ((1u << (nbits - lo)) - 1u));
+    }
+}
+
 // element s (static) of packed 16-bit values held two per dword
 template <int N>
 __device__ __forceinline__ uint32_t half_at(const uint32_t (&v)[N], int s) {
@@ -426,7 +437,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         const int o = (int)(d.first_block - fb0);
         for (int j = 0; j < nb; ++j) b2s[o + j] = (uint8_t)tid;
         if (tid == ns - 1) s_nblk = o + nb;
-        plain = d.log2g == 0 && (d.r & 7) == 0 && d.r <= 32 && (d.sc_off & 15u) == 0;
+        plain = d.log2g == 0 && (d.r & 7) == 0 && d.r <= 32 && (d.sc_off & 15u) == 0 && g.trunc == D;
         dense = d.log2g == 0 && d.r == D && (d.sc_off & 15u) == 0;
     }
     const int w0 = g.rotated ? (s0 * SEG) / g.W : 0;
@@ -457,7 +468,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
                 const int i = valid ? b2s[b] : 0;
                 const Desc d = ds[i];
                 const int j = b - (int)(d.first_block - fb0);
-                const uint8_t *rec = valid ? sc + d.sc_off + (uint32_t)j * (uint32_t)vec_bytes(D, 0) : sc;
+                const uint8_t *rec = valid ? sc + d.sc_off + (uint32_t)j * (uint32_t)vec_bytes(D, 0, g.trunc) : sc;
                 const uint4 *v4 = (const uint4 *)(rec + 16);
                 uint4 t[D / 8];
 #pragma unroll
@@ -505,7 +516,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
             const Desc d = ds[i];
             j = b - (int)(d.first_block - fb0);
             r = valid ? d.r : 0;
-            return valid ? sc + d.sc_off + (uint32_t)j * (uint32_t)vec_bytes(d.r, 0) : sc;
+            return valid ? sc + d.sc_off + (uint32_t)j * (uint32_t)vec_bytes(d.r, 0, D) : sc;
         };
         int i, j, r;
         const uint8_t *rec = where(tid, i, j, r);
@@ -544,11 +555,12 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         const Desc d = ds[i];
         const int j = b - (int)(d.first_block - fb0);
         const int r = valid ? d.r : 0, l2g = d.log2g;
-        const uint8_t *rec = valid ? sc + d.sc_off + (uint32_t)j * (uint32_t)vec_bytes(r, l2g) : sc;
+        const uint8_t *rec = valid ? sc + d.sc_off + (uint32_t)j * (uint32_t)vec_bytes(r, l2g, g.trunc) : sc;
         const uint32_t qoff = (g.rotated && ((s0 + i) * SEG) / g.W != w0) ? D * GP * 4 : 0;
-        const bool a16 = __all(!valid || (l2g == 0 && ((uintptr_t)rec & 15u) == 0));
+        const bool a16 = __all(!valid || (l2g == 0 && ((uintptr_t)rec & 15u) == 0 && g.trunc == D));
         PVec<RMAX> x;
-        load_pvec<RMAX, -1, true>(x, rec, rec + (16 >> l2g), wave_max_i(r), a16);
+        load_pvec<RMAX, -1, true>(x, rec, rec + bm_bytes(l2g, g.trunc), wave_max_i(r), a16);
+        if (g.trunc < D) mask_words(x.bw, g.trunc >> l2g);
         float acc[GP];
 #pragma unroll
         for (int h = 0; h < GP; ++h) acc[h] = 0.0f;
@@ -947,8 +959,8 @@ struct TokLoc {
 
 // load the packed K (V when V_ is set) vector of a located token
 template <int RMAX, int RL>
-__device__ __forceinline__ void load_tok(PVec<RMAX> &x, const uint8_t *tokg, const TokLoc &L, bool V_, int rmax) {
-    const int r = L.r(), l2g = L.l2g(), B = 1 << L.l2b(), bmb = 16 >> l2g, j = L.j();
+__device__ __forceinline__ void load_tok(PVec<RMAX> &x, const uint8_t *tokg, const TokLoc &L, bool V_, int rmax, int T) {
+    const int r = L.r(), l2g = L.l2g(), B = 1 << L.l2b(), bmb = bm_bytes(l2g, T), j = L.j();
     const uint32_t half = V_ ? (uint32_t)(B * (bmb + 2 * r)) : 0u;
     const uint8_t *b = tokg + L.base + half;
     load_pvec<RMAX, RL ? 1 : 0, false, RL>(x, b + j * bmb, b + B * bmb + j * 2 * r, rmax, false);
@@ -1083,7 +1095,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             const Desc d = g.desc_of(p)[min(bs >> 4, (uint32_t)g.max_desc - 1)];
             const int jb = (int)(bs & 15u);
             r = d.r; l2g = d.log2g; l2b = d.log2b;
-            goff = d.tok_off + (uint32_t)(jb << l2b) * (uint32_t)(2 * vec_bytes(r, l2g));
+            goff = d.tok_off + (uint32_t)(jb << l2b) * (uint32_t)(2 * vec_bytes(r, l2g, g.trunc));
         }
         const int cls = on ? 4 - l2b : 3;
         const uint64_t m0 = __ballot(cls == 0), m1 = __ballot(cls == 1), m2 = __ballot(cls == 2);
@@ -1096,7 +1108,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         if (lane == 0) wcnt[wave * 4 + 3] = rw;
         // one channel per group, r % 8 == 0 and an aligned block: 16-byte
         // bitmaps and 2r-byte value runs at 16-byte offsets
-        all16 = __syncthreads_and(!on || (l2g == 0 && (r & 7) == 0 && (goff & 15u) == 0));
+        all16 = __syncthreads_and(!on || (l2g == 0 && (r & 7) == 0 && (goff & 15u) == 0 && g.trunc == D));
         if (RMAX >= D) dense = __syncthreads_and(!on || (l2g == 0 && r == D));
         if (on) {
             const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -1174,9 +1186,9 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         if constexpr (RL >= 0) {
             const int rm = wave_max_i(cur.r());
             __builtin_amdgcn_sched_barrier(0);
-            load_tok<RMAX, RL>(kx, tokg, cur, false, rm);
+            load_tok<RMAX, RL>(kx, tokg, cur, false, rm, g.trunc);
             __builtin_amdgcn_sched_barrier(0);          // K's loads before V's, as in the loop
-            load_tok<RMAX, RL>(vx, tokg, cur, true, rm);
+            load_tok<RMAX, RL>(vx, tokg, cur, true, rm, g.trunc);
             __builtin_amdgcn_sched_barrier(0);
         }
         // the tile starts zero; every MFMA operand read below zeroes what it
@@ -1201,11 +1213,12 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
                     dense_put<false>(tokg + cur.base + (16 << cur.l2b()) + cur.j() * 2 * D,
                                      lds_addr(tile) + lane * (KT_STRIDE * 2));
             } else if (cur.valid) {
+                if (g.trunc < D) mask_words(kx.bw, g.trunc >> cur.l2g());
                 scatter_any<RMAX, false, FR>(kx, cur.r(), cur.l2g(), lds_addr(tile) + lane * (KT_STRIDE * 2));
             }
             wave_sync();
             mem_fence_compiler();
-            if constexpr (RL >= 0) load_tok<RMAX, RL>(kx, tokg, nxt, false, rmn);
+            if constexpr (RL >= 0) load_tok<RMAX, RL>(kx, tokg, nxt, false, rmn, g.trunc);
             float z[4][4];
             {
                 // four independent accumulators (token groups n), so no
@@ -1271,11 +1284,12 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
                     dense_put<true>(tokg + cur.base + B * (16 + 2 * D) + 16 * B + cur.j() * 2 * D, lds_addr(tile) + lane * 2);
                 }
             } else if (cur.valid) {
+                if (g.trunc < D) mask_words(vx.bw, g.trunc >> cur.l2g());
                 scatter_any<RMAX, true, FR>(vx, cur.r(), cur.l2g(), lds_addr(tile) + lane * 2);
             }
             wave_sync();
             mem_fence_compiler();
-            if constexpr (RL >= 0) load_tok<RMAX, RL>(vx, tokg, nxt, true, rmn);
+            if constexpr (RL >= 0) load_tok<RMAX, RL>(vx, tokg, nxt, true, rmn, g.trunc);
             // ---- P . V on MFMA: A = P[head l16][tokens], B = V[tokens][channel tile]
             if (!__all(alpha == 1.0f)) {                      // some head's running max moved
                 float ar[4];

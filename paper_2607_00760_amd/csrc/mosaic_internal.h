@@ -40,6 +40,7 @@ struct Geom {
     int def_keep, def_group, def_block;
     float tau_ch, tau_blk;
     int sel_num, sel_den, force;
+    int trunc;                        // channels represented in the bitmaps (T)
 
     __host__ __device__ PairMeta *meta_of(int p) const { return (PairMeta *)(meta + (uint64_t)p * meta_stride); }
     __host__ __device__ Desc *desc_of(int p) const { return (Desc *)(desc + (uint64_t)p * desc_stride); }
@@ -79,7 +80,11 @@ __device__ __forceinline__ uint16_t f2h(float f, int dtype) {
     return __builtin_bit_cast(uint16_t, (_Float16)f);   // v_cvt_f16_f32, RNE
 }
 
-__device__ __forceinline__ int vec_bytes(int r, int log2g) { return 2 * r + (16 >> log2g); }
+// bitmap bytes of a vector whose first T channels are represented (T / g
+// bits in whole 32-bit words, so every record stays 4-byte aligned), and its
+// record size
+__host__ __device__ __forceinline__ int bm_bytes(int log2g, int T) { return (((T >> log2g) + 31) >> 5) << 2; }
+__host__ __device__ __forceinline__ int vec_bytes(int r, int log2g, int T) { return 2 * r + bm_bytes(log2g, T); }
 
 // ---------------------------------------------------------------- wave helpers
 __device__ __forceinline__ float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, WAVE); }

@@ -30,6 +30,10 @@ CASES = {
     # the sequence-only (quest) mode: every channel kept, 16-token blocks, no rotation
     "quest_mode": (gen.spec("c3", ctx=(2500, 700), hkv=2, rotate=False), dict(force_default=True,
                                                                               default=(128, 1, 16))),
+    # channel truncation: bitmaps of the first 96 (64) channels, 12 / 6 / 3-byte bitmaps
+    "truncated_96": (gen.spec("c1", ctx=(3000, 1200), hkv=2), dict(trunc=96)),
+    "truncated_64_g2": (gen.spec("c2", ctx=(1500, 700), hkv=2), dict(trunc=64, force_default=True,
+                                                                    default=(32, 2, 8))),
     # kept counts outside 16/32/48: the general (runtime trip count) walks
     "odd_keeps": (gen.spec("c2", ctx=(1500, 900), hkv=2), dict(keep_cand=(8, 24, 40), default=(24, 2, 8),
                                                             tau_channel=0.2)),
