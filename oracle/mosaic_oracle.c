@@ -41,7 +41,8 @@
  * dense and unrotated (R-9), provisional strategy = previous finalized
  * segment or the default (R-10), prefill remainder handled as appends
  * (R-11), y = x . R^T with row j of R the j-th rotated channel (R-12), a
- * truncated bitmap stored in whole 32-bit words (R-19).
+ * truncated bitmap stored in whole 32-bit words (R-19), FP8 values as OCP
+ * E4M3 without a scale factor, block keys kept 16-bit (R-20).
  *
  * Exactly-defined orders (so that integer and byte results are unique):
  *  chain(a, b)  : acc = 0; for i ascending: acc = fmaf(a_i, b_i, acc)
@@ -83,6 +84,9 @@ typedef struct {
                                         channels >= trunc are never kept and have no bitmap
                                         bit; a multiple of 32 up to D (0 means D); the
                                         bitmap is rounded up to whole 32-bit words */
+    int32_t fp8;                     /* 1: K and V token values stored as OCP FP8 E4M3
+                                        (Sec. 7, quantizing the compressed elements);
+                                        block keys keep the 16-bit dtype (reading R-20) */
 } orc_params;
 
 typedef struct {
@@ -165,6 +169,37 @@ uint16_t orc_f32_to_bf16(float f) {
     return (uint16_t)(u >> 16);
 }
 
+/* OCP 8-bit floating point E4M3 (sign, 4 exponent bits with bias 7, 3
+   mantissa bits, no infinities, only S.1111.111 is NaN): the value of a code
+   and the nearest code of a finite fp32 value (ties to the even code),
+   saturated to +-448, the largest finite magnitude.  Written from the format's
+   definition with exact double arithmetic. */
+float orc_e4m3_to_f32(uint8_t c) {
+    int s = c >> 7, e = (c >> 3) & 15, m = c & 7;
+    if (e == 15 && m == 7) return NAN;
+    double v = e == 0 ? ldexp((double)m / 8.0, -6) : ldexp(1.0 + (double)m / 8.0, e - 7);
+    return (float)(s ? -v : v);
+}
+
+uint8_t orc_f32_to_e4m3(float f) {
+    uint8_t sign = signbit(f) ? 0x80 : 0x00;
+    double a = fabs((double)f);
+    if (a >= 448.0) return (uint8_t)(sign | 0x7e);
+    int e;
+    if (a < ldexp(1.0, -6)) e = -6;                  /* subnormal spacing 2^-9 */
+    else { (void)frexp(a, &e); e -= 1; }             /* a in [2^e, 2^(e+1)) */
+    double step = ldexp(1.0, e - 3);                 /* spacing of the codes at a */
+    double q = a / step, n = floor(q), fr = q - n;   /* exact: step is a power of two */
+    if (fr > 0.5 || (fr == 0.5 && fmod(n, 2.0) == 1.0)) n += 1.0;
+    /* n * step is the rounded magnitude: n < 8 only below 2^-6 (subnormal
+       codes 0..7), else 8 <= n <= 16 with n = 16 the next binade */
+    int code;
+    if (n < 8.0) code = (int)n;
+    else code = ((e + 7) << 3) + (int)n - 8;
+    if (code > 0x7e) code = 0x7e;
+    return (uint8_t)(sign | code);
+}
+
 static float to_f32(uint16_t v, int dtype) { return dtype ? orc_bf16_to_f32(v) : orc_f16_to_f32(v); }
 static uint16_t from_f32(float v, int dtype) { return dtype ? orc_f32_to_bf16(v) : orc_f32_to_f16(v); }
 
@@ -241,9 +276,12 @@ static void keep_channels(const float *y, int r, int g, int T, uint8_t *kch) {
 /* Packed KV format (Sec. 5.1).                                        */
 /* A packed vector = [bitmap: D/g bits as little-endian u32 words, bit */
 /* i = group i kept][values: the r kept elements in ascending channel  */
-/* order, fp32 -> dtype RNE].                                          */
+/* order, fp32 -> dtype RNE, or -> E4M3 when fp8 is set (token records */
+/* only)].                                                             */
 /* ------------------------------------------------------------------ */
 static int trunc_of(const orc_params *P) { return (P->trunc > 0 && P->trunc < D) ? P->trunc : D; }
+/* bytes per kept value of the K and V token records */
+static int tok_eb(const orc_params *P) { return P->fp8 ? 1 : 2; }
 /* a bitmap of T / g bits is stored in whole little-endian 32-bit words (reading R-19) */
 int orc_bitmap_bytes_t(int g, int T) { return ((T / g + 31) / 32) * 4; }
 int orc_vec_bytes_t(int r, int g, int elem_bytes, int T) { return r * elem_bytes + orc_bitmap_bytes_t(g, T); }
@@ -263,13 +301,19 @@ static void pack_bitmap(const uint8_t *kch, int g, int T, uint8_t *out) {
     }
 }
 
-static void pack_values(const float *y, const uint8_t *kch, int dtype, uint8_t *out) {
+/* the kept values in ascending channel order: eb = 2 -> the 16-bit dtype
+   (little-endian), eb = 1 -> E4M3 codes; one rounding from fp32 either way */
+static void pack_values(const float *y, const uint8_t *kch, int dtype, int eb, uint8_t *out) {
     int slot = 0;
     for (int c = 0; c < D; ++c) {
         if (!kch[c]) continue;
-        uint16_t h = from_f32(y[c], dtype);
-        out[2 * slot] = (uint8_t)(h & 0xff);
-        out[2 * slot + 1] = (uint8_t)(h >> 8);
+        if (eb == 1) {
+            out[slot] = orc_f32_to_e4m3(y[c]);
+        } else {
+            uint16_t h = from_f32(y[c], dtype);
+            out[2 * slot] = (uint8_t)(h & 0xff);
+            out[2 * slot + 1] = (uint8_t)(h >> 8);
+        }
         slot++;
     }
 }
@@ -279,7 +323,7 @@ void orc_pack_vector(const float *y, int r, int g, int dtype, uint8_t *out) {
     uint8_t kch[D];
     keep_channels(y, r, g, D, kch);
     pack_bitmap(kch, g, D, out);
-    pack_values(y, kch, dtype, out + orc_bitmap_bytes(g));
+    pack_values(y, kch, dtype, 2, out + orc_bitmap_bytes(g));
 }
 
 static int ilog2(int v) { int l = 0; while ((1 << l) < v) ++l; return l; }
@@ -348,22 +392,23 @@ static void block_mean(const float *yk, int b0, int B, float *mu) {
 /* Encode n tokens (n = S or U) with strategy (r, g, B) into a token-arena
    record and a score-arena record (Sec. 5.2 compressed KV encoding). */
 static void encode_segment(const float *yk, const float *yv, int n, int r, int g, int B, int dtype, int T,
-                           uint8_t *tok, uint8_t *sc) {
-    int bmb = orc_bitmap_bytes_t(g, T), vb = r * 2, rec = bmb + vb;
+                           int eb, uint8_t *tok, uint8_t *sc) {
+    /* token records hold eb-byte values, block keys 16-bit ones */
+    int bmb = orc_bitmap_bytes_t(g, T), vb = r * eb, rec = bmb + vb, srec = bmb + 2 * r;
     uint8_t kch[D];
     for (int b0 = 0, bi = 0; b0 < n; b0 += B, ++bi) {
         uint8_t *blk = tok + (size_t)bi * B * 2 * rec;
         uint8_t *kbm = blk, *kval = blk + B * bmb, *vbm = kval + B * vb, *vval = vbm + B * bmb;
         for (int j = 0; j < B; ++j) {
             const float *k = yk + (size_t)(b0 + j) * D, *v = yv + (size_t)(b0 + j) * D;
-            keep_channels(k, r, g, T, kch); pack_bitmap(kch, g, T, kbm + j * bmb); pack_values(k, kch, dtype, kval + j * vb);
-            keep_channels(v, r, g, T, kch); pack_bitmap(kch, g, T, vbm + j * bmb); pack_values(v, kch, dtype, vval + j * vb);
+            keep_channels(k, r, g, T, kch); pack_bitmap(kch, g, T, kbm + j * bmb); pack_values(k, kch, dtype, eb, kval + j * vb);
+            keep_channels(v, r, g, T, kch); pack_bitmap(kch, g, T, vbm + j * bmb); pack_values(v, kch, dtype, eb, vval + j * vb);
         }
         float mu[D];
         block_mean(yk, b0, B, mu);
         keep_channels(mu, r, g, T, kch);
-        pack_bitmap(kch, g, T, sc + (size_t)bi * rec);
-        pack_values(mu, kch, dtype, sc + (size_t)bi * rec + bmb);
+        pack_bitmap(kch, g, T, sc + (size_t)bi * srec);
+        pack_values(mu, kch, dtype, 2, sc + (size_t)bi * srec + bmb);
     }
 }
 
@@ -440,13 +485,13 @@ static void finalize_segment(orc_pair *p) {
     rotate_tokens(p, p->stgv, S, nf * S, p->rv, yv);
     int r, g, B;
     orc_choose_strategy(P, yk, yv, S, &r, &g, &B);
-    int rec = orc_vec_bytes_t(r, g, 2, trunc_of(P));
-    encode_segment(yk, yv, S, r, g, B, P->dtype, trunc_of(P), p->tok + p->tok_tail, p->sc + p->sc_tail);
+    int rec = orc_vec_bytes_t(r, g, tok_eb(P), trunc_of(P)), srec = orc_vec_bytes_t(r, g, 2, trunc_of(P));
+    encode_segment(yk, yv, S, r, g, B, P->dtype, trunc_of(P), tok_eb(P), p->tok + p->tok_tail, p->sc + p->sc_tail);
     orc_desc *d = &p->desc[nf];
     d->tok_off = p->tok_tail; d->sc_off = p->sc_tail; d->first_block = (uint32_t)p->nblk_final;
     d->r = (uint8_t)r; d->log2g = (uint8_t)ilog2(g); d->log2b = (uint8_t)ilog2(B); d->flags = 0;
     p->tok_tail += (uint32_t)(S * 2 * rec);
-    p->sc_tail += (uint32_t)((S / B) * rec);
+    p->sc_tail += (uint32_t)((S / B) * srec);
     p->nblk_final += S / B;
     free(yk); free(yv);
 }
@@ -461,7 +506,7 @@ static void flush_provisional(orc_pair *p) {
     float *yk = (float *)malloc((size_t)U * D * sizeof(float)), *yv = (float *)malloc((size_t)U * D * sizeof(float));
     rotate_tokens(p, p->stgk, U, nf * S, p->rk, yk);
     rotate_tokens(p, p->stgv, U, nf * S, p->rv, yv);
-    encode_segment(yk, yv, U, r, g, B, P->dtype, trunc_of(P), p->tok + p->tok_tail, p->sc + p->sc_tail);
+    encode_segment(yk, yv, U, r, g, B, P->dtype, trunc_of(P), tok_eb(P), p->tok + p->tok_tail, p->sc + p->sc_tail);
     orc_desc *d = &p->desc[nf];
     d->tok_off = p->tok_tail; d->sc_off = p->sc_tail; d->first_block = (uint32_t)p->nblk_final;
     d->r = (uint8_t)r; d->log2g = (uint8_t)ilog2(g); d->log2b = (uint8_t)ilog2(B); d->flags = 1;
@@ -513,9 +558,10 @@ void orc_pair_info(const orc_pair *p, orc_info *o) {
                   + (uint64_t)o->n_buf * 2 * D * 2;
     if (o->prov) {
         const orc_desc *d = &p->desc[o->n_final];
-        int B = 1 << d->log2b, rec = orc_vec_bytes_t(d->r, 1 << d->log2g, 2, trunc_of(&p->P));
+        int B = 1 << d->log2b, rec = orc_vec_bytes_t(d->r, 1 << d->log2g, tok_eb(P), trunc_of(P)),
+            srec = orc_vec_bytes_t(d->r, 1 << d->log2g, 2, trunc_of(P));
         o->nblk += P->update_buf / B;
-        used += (uint64_t)P->update_buf * 2 * rec + (uint64_t)(P->update_buf / B) * rec;
+        used += (uint64_t)P->update_buf * 2 * rec + (uint64_t)(P->update_buf / B) * srec;
     }
     o->tok_tail = p->tok_tail; o->sc_tail = p->sc_tail; o->used_bytes = used;
 }
@@ -591,15 +637,16 @@ int orc_select_count(int nblk, int num, int den) {
 }
 
 /* unpack one packed vector into dense fp64 (0 at dropped channels) */
-static void unpack64(const uint8_t *bm, const uint8_t *vals, int g, int T, int dtype, double *out) {
+static void unpack64(const uint8_t *bm, const uint8_t *vals, int g, int T, int dtype, int eb, double *out) {
     int slot = 0;
     for (int gi = 0; gi < D / g; ++gi) {
         int kept = gi < T / g ? (bm[gi >> 3] >> (gi & 7)) & 1 : 0;
         for (int e = 0; e < g; ++e) {
             int c = gi * g + e;
             if (kept) {
-                uint16_t hv = (uint16_t)(vals[2 * slot] | (vals[2 * slot + 1] << 8));
-                out[c] = (double)to_f32(hv, dtype); slot++;
+                if (eb == 1) out[c] = (double)orc_e4m3_to_f32(vals[slot]);
+                else out[c] = (double)to_f32((uint16_t)(vals[2 * slot] | (vals[2 * slot + 1] << 8)), dtype);
+                slot++;
             } else out[c] = 0.0;
         }
     }
@@ -644,7 +691,8 @@ int orc_pair_decode(const orc_pair *p, const uint16_t *q, float scale, double *o
             }
             cur_w = w;
         }
-        int g = 1 << d->log2g, B = 1 << d->log2b, r = d->r, bmb = orc_bitmap_bytes_t(g, trunc_of(P)), vb = 2 * r, rec = bmb + vb;
+        int g = 1 << d->log2g, B = 1 << d->log2b, r = d->r, bmb = orc_bitmap_bytes_t(g, trunc_of(P)), eb = tok_eb(P),
+            vb = eb * r, rec = bmb + vb;
         int nblk = desc_ntok(p, d) / B;
         for (int j = 0; j < nblk; ++j, ++bglob) {
             if (!keep[bglob]) continue;
@@ -652,8 +700,8 @@ int orc_pair_decode(const orc_pair *p, const uint16_t *q, float scale, double *o
             const uint8_t *kbm = blk, *kval = blk + B * bmb, *vbm = kval + B * vb, *vval = vbm + B * bmb;
             for (int t = 0; t < B; ++t) {
                 double kd[D];
-                unpack64(kbm + t * bmb, kval + t * vb, g, trunc_of(P), P->dtype, kd);
-                unpack64(vbm + t * bmb, vval + t * vb, g, trunc_of(P), P->dtype, vv + (size_t)nt * D);
+                unpack64(kbm + t * bmb, kval + t * vb, g, trunc_of(P), P->dtype, eb, kd);
+                unpack64(vbm + t * bmb, vval + t * vb, g, trunc_of(P), P->dtype, eb, vv + (size_t)nt * D);
                 for (int h = 0; h < G; ++h) {
                     double a = 0.0;
                     for (int c = 0; c < D; ++c) a += qr[h][c] * kd[c];
@@ -731,9 +779,9 @@ void orc_dense_attention(const uint16_t *q, const uint16_t *k, const uint16_t *v
 }
 
 /* Byte accounting per token of a full segment (for the ratio closed form):
-   2 packed vectors per token plus one block key per B tokens. */
+   2 packed vectors per token with elem_bytes-byte values, plus one block key
+   (16-bit values) per B tokens. */
 double orc_bytes_per_token_t(int r, int g, int B, int elem_bytes, int T) {
-    double v = (double)orc_vec_bytes_t(r, g, elem_bytes, T);
-    return 2.0 * v + v / (double)B;
+    return 2.0 * (double)orc_vec_bytes_t(r, g, elem_bytes, T) + (double)orc_vec_bytes_t(r, g, 2, T) / (double)B;
 }
 double orc_bytes_per_token(int r, int g, int B, int elem_bytes) { return orc_bytes_per_token_t(r, g, B, elem_bytes, D); }

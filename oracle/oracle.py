@@ -42,7 +42,7 @@ class OrcParams(C.Structure):
         ("def_keep", C.c_int32), ("def_group", C.c_int32), ("def_block", C.c_int32),
         ("tau_channel", C.c_float), ("tau_block", C.c_float),
         ("select_num", C.c_int32), ("select_den", C.c_int32), ("force_default", C.c_int32),
-        ("trunc", C.c_int32),
+        ("trunc", C.c_int32), ("fp8", C.c_int32),
     ]
 
 
@@ -74,6 +74,7 @@ class Params:
     select: tuple = (1, 10)
     force_default: bool = False
     trunc: int = 128                # channels represented in the bitmap (Sec. 5.2 channel truncation)
+    fp8: bool = False               # K/V token values as E4M3 (Sec. 7, combining with quantization)
 
     def to_c(self) -> OrcParams:
         p = OrcParams()
@@ -89,6 +90,7 @@ class Params:
         p.select_num, p.select_den = self.select
         p.force_default = 1 if self.force_default else 0
         p.trunc = self.trunc
+        p.fp8 = 1 if self.fp8 else 0
         return p
 
 
@@ -106,6 +108,8 @@ def lib():
         L.orc_f16_to_f32.argtypes = [C.c_uint16]; L.orc_f16_to_f32.restype = C.c_float
         L.orc_f32_to_f16.argtypes = [C.c_float]; L.orc_f32_to_f16.restype = C.c_uint16
         L.orc_bf16_to_f32.argtypes = [C.c_uint16]; L.orc_bf16_to_f32.restype = C.c_float
+        L.orc_e4m3_to_f32.argtypes = [C.c_uint8]; L.orc_e4m3_to_f32.restype = C.c_float
+        L.orc_f32_to_e4m3.argtypes = [C.c_float]; L.orc_f32_to_e4m3.restype = C.c_uint8
         L.orc_f32_to_bf16.argtypes = [C.c_float]; L.orc_f32_to_bf16.restype = C.c_uint16
         L.orc_tree_sum.argtypes = [fp, C.c_int]; L.orc_tree_sum.restype = C.c_float
         L.orc_rotate.argtypes = [fp, fp, fp]; L.orc_rotate.restype = None
@@ -172,6 +176,16 @@ def f16_bits_to_f32(b):
 def bf16_bits_to_f32(b):
     L = lib()
     return np.array([L.orc_bf16_to_f32(int(v)) for v in np.asarray(b, np.uint16).ravel()], np.float32)
+
+
+def f32_to_e4m3(x):
+    L = lib()
+    return np.array([L.orc_f32_to_e4m3(float(v)) for v in np.asarray(x, np.float32).ravel()], np.uint8)
+
+
+def e4m3_to_f32(b):
+    L = lib()
+    return np.array([L.orc_e4m3_to_f32(int(v)) for v in np.asarray(b, np.uint8).ravel()], np.float32)
 
 
 # ---- vector primitives -----------------------------------------------------
@@ -276,6 +290,11 @@ class Pair:
                 pass
             self._h = None
 
+    @property
+    def elem_bytes(self):
+        """Bytes per kept value in the K and V token records."""
+        return 1 if self.params.fp8 else 2
+
     def compress(self, k, v):
         k, v = _u16(k).reshape(-1, D), _u16(v).reshape(-1, D)
         rc = lib().orc_pair_compress(self._h, _p(k, C.c_uint16), _p(v, C.c_uint16), k.shape[0])
@@ -302,7 +321,8 @@ class Pair:
         n = i.tok_tail
         if i.prov:
             d = self.descriptors()[-1]
-            n = d["tok_off"] + self.params.update_buf * 2 * vec_bytes(d["r"], 1 << d["log2g"], 2, self.params.trunc)
+            n = d["tok_off"] + self.params.update_buf * 2 * vec_bytes(d["r"], 1 << d["log2g"], self.elem_bytes,
+                                                                     self.params.trunc)
         return self._bytes("orc_pair_tok", n)
 
     def score_arena(self):

@@ -525,3 +525,107 @@ def test_truncated_keep_everything_equals_dense_over_leading_channels():
     vz[:nc, T:] = 0
     ref = _numpy_attention(q, kz, vz, 1 / math.sqrt(D), "bf16")
     assert np.max(np.abs(out - ref)) < 1e-12
+
+
+# ---------------------------------------------------------------- FP8 values (Sec. 7, reading R-20)
+def _torch_e4m3(x):
+    return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+
+
+def test_e4m3_decode_matches_torch():
+    codes = np.arange(256, dtype=np.uint8)
+    want = torch.from_numpy(codes).view(torch.float8_e4m3fn).float().numpy()
+    got = O.e4m3_to_f32(codes)
+    fin = np.isfinite(want)
+    assert np.array_equal(np.isnan(got), ~fin) and fin.sum() == 254
+    assert np.array_equal(got[fin], want[fin])
+    assert np.signbit(got[0x80]) and not np.signbit(got[0x00])
+    # the format's landmarks: largest finite, smallest normal and subnormal, one
+    assert (got[0x7e], got[0x08], got[0x01], got[0x38]) == (448.0, 2.0**-6, 2.0**-9, 1.0)
+
+
+def test_e4m3_rne_matches_torch_and_saturates():
+    r = rng(30)
+    scaled = (r.standard_normal(60000) * r.choice([2.0**-12, 2.0**-8, 2.0**-5, 1.0, 30.0, 300.0], 60000))
+    scaled = scaled.astype(np.float32)
+    vals = O.e4m3_to_f32(np.arange(0, 0x7f, dtype=np.uint8)).astype(np.float64)
+    mids = (vals[:-1] + vals[1:]) / 2                      # ties: 4 significant bits, exact in fp32
+    edge = np.concatenate([vals, mids, np.nextafter(mids.astype(np.float32), np.float32(0)),
+                           np.nextafter(mids.astype(np.float32), np.float32(1e9)),
+                           [0.0, 1e-30, 2.0**-10, 463.99, 448.0 + 8.0]]).astype(np.float32)
+    for xs in (scaled[np.abs(scaled) < 464], edge, -edge):
+        assert np.array_equal(O.f32_to_e4m3(xs), _torch_e4m3(xs))
+    # past the largest finite value's rounding range torch gives NaN; the reading saturates
+    big = np.array([464.0, 500.0, 1e6, 3e38], np.float32)
+    assert np.all(O.f32_to_e4m3(big) == 0x7E) and np.all(O.f32_to_e4m3(-big) == 0xFE)
+
+
+def test_fp8_record_sizes_closed_form():
+    # default strategy with E4M3 token values: 2 (32 + 16) + (64 + 16) / 8 = 106 bytes per token
+    assert O.vec_bytes(32, 1, 1) == 48 and O.bytes_per_token(32, 1, 8, 1) == 106.0
+    assert abs(512 / O.bytes_per_token(32, 1, 8, 1) - 4.830188679245283) < 1e-12
+    P = O.Params(force_default=True, dtype="bf16", fp8=True)
+    pr = O.Pair(P, 640)
+    x = to_bits(rng(31).standard_normal((640, D)), "bf16")
+    pr.compress(x, x)
+    per_seg = 64 * 2 * (32 + 16) + 8 * (32 * 2 + 16) + 16
+    assert pr.info().used_bytes == 10 * per_seg
+
+
+@pytest.mark.parametrize("dtype", ["fp16", "bf16"])
+def test_fp8_records_hold_e4m3_of_the_kept_values(dtype):
+    """Identity rotation, forced (32, 1, 8): each K and V token record is the
+    16-byte bitmap of the 32 largest |x| followed by their E4M3 codes in
+    ascending channel order; block keys keep 16-bit values."""
+    r, B = 32, 8
+    P = O.Params(force_default=True, default=(r, 1, B), dtype=dtype, fp8=True)
+    x = rng(32).standard_normal((64, D)) * np.exp(rng(33).uniform(-6, 4, (64, D)))   # subnormal to saturated
+    kb = to_bits(x, dtype)
+    vb_bits = to_bits(-x[::-1], dtype)
+    pr = O.Pair(P, 64)
+    pr.compress(kb, vb_bits)
+    tok, sc = pr.token_arena(), pr.score_arena()
+    rec = 16 + r
+    assert tok.size == 64 * 2 * rec and sc.size == (64 // B) * (16 + 2 * r)
+    for which, bits_ in ((0, kb), (1, vb_bits)):
+        y = from_bits(bits_, dtype)
+        for t in range(64):
+            ch = np.sort(sorted(range(D), key=lambda c: (-abs(y[t, c]), c))[:r])
+            blk = tok[(t // B) * B * 2 * rec + which * B * rec:]
+            bm = np.unpackbits(blk[(t % B) * 16:(t % B + 1) * 16], bitorder="little")
+            assert np.array_equal(np.nonzero(bm)[0], ch), (which, t)
+            codes = blk[B * 16 + (t % B) * r: B * 16 + (t % B + 1) * r]
+            assert np.array_equal(codes, _torch_e4m3(np.clip(y[t, ch], -448, 448))), (which, t)
+    # the first block key: the fp32 mean of its 8 keys (ascending adds, times 1/8),
+    # the 16-byte bitmap of its 32 largest |mu|, then their 16-bit values
+    yk = from_bits(kb, dtype).astype(np.float32)
+    acc = yk[0].copy()
+    for t in range(1, B):
+        acc = (acc + yk[t]).astype(np.float32)
+    mu = (acc * np.float32(1.0 / B)).astype(np.float32)
+    ch = np.sort(sorted(range(D), key=lambda c: (-abs(float(mu[c])), c))[:r])
+    assert np.array_equal(np.nonzero(np.unpackbits(sc[:16], bitorder="little"))[0], ch)
+    assert np.array_equal(sc[16:16 + 2 * r].view(np.uint16), to_bits(mu[ch], dtype))
+
+
+def test_fp8_keep_everything_equals_dense_over_e4m3_values():
+    """r = D, rho = 1, identity rotation, E4M3 values: attention over K and V
+    rounded to E4M3 for the compressed tokens; update-buffer tokens stay 16-bit."""
+    r_ = rng(34)
+    G, L = 4, 200
+    P = O.Params(group=G, dtype="bf16", force_default=True, default=(D, 1, 8), select=(1, 1), rot_window=128,
+                 fp8=True)
+    k = to_bits(r_.standard_normal((L, D)), "bf16")
+    v = to_bits(r_.standard_normal((L, D)), "bf16")
+    q = to_bits(r_.standard_normal((G, D)), "bf16")
+    pr = O.Pair(P, L)
+    pr.compress(k, v)
+    out, _ = pr.decode(q, 1 / math.sqrt(D))
+    nc = (L // 64) * 64
+    e4 = lambda b: torch.from_numpy(_torch_e4m3(from_bits(b, "bf16"))).view(torch.float8_e4m3fn).float().numpy()
+    kq, vq = k.copy(), v.copy()
+    kq[:nc] = to_bits(e4(k[:nc]), "bf16")                  # E4M3 values are exact in bf16
+    vq[:nc] = to_bits(e4(v[:nc]), "bf16")
+    assert not np.array_equal(kq, k)
+    ref = _numpy_attention(q, kq, vq, 1 / math.sqrt(D), "bf16")
+    assert np.max(np.abs(out - ref)) < 1e-12
