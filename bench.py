@@ -44,6 +44,8 @@ def parse():
                     help="channels represented in the bitmaps (channel truncation; 128 = none)")
     ap.add_argument("--force-default", action="store_true",
                     help="every segment takes the default strategy (32, 1, 8) instead of the search")
+    ap.add_argument("--fp8", action="store_true",
+                    help="K and V token values stored as E4M3 codes (block keys stay 16-bit)")
     ap.add_argument("--mode", choices=("mosaic", "quest"), default="mosaic",
                     help="quest: every channel kept, 16-token blocks, no rotation (sequence-only "
                          "compression on the same kernels)")
@@ -75,9 +77,11 @@ def algorithmic_bytes(cache, spec, nb_list, sel_list, desc_list):
     for p, (nb, sel, descs) in enumerate(zip(nb_list, sel_list, desc_list)):
         L = spec.ctx[p // spec.hkv]
         n_desc = len(descs)
-        rec = [2 * d[3] + (((cache.params.trunc >> d[4]) + 31) // 32) * 4 for d in descs]
+        bmb = [(((cache.params.trunc >> d[4]) + 31) // 32) * 4 for d in descs]
+        srec = [2 * d[3] + b for d, b in zip(descs, bmb)]                  # block keys: 16-bit values
+        rec = [(1 if cache.params.fp8 else 2) * d[3] + b for d, b in zip(descs, bmb)]   # K / V tokens
         blocks_per = [((32 if d[6] & 1 else 64) >> d[5]) for d in descs]
-        tot["score"] += sum(r * n for r, n in zip(rec, blocks_per)) + 16 * n_desc
+        tot["score"] += sum(r * n for r, n in zip(srec, blocks_per)) + 16 * n_desc
         # selected blocks -> descriptor (first_block ascending)
         fb = [d[2] for d in descs]
         import bisect
@@ -214,6 +218,8 @@ def main():
     if args.mode == "quest":
         spec = gen.spec(args.config, ctx=spec.ctx, rotate=False)
         extra = dict(default=(D, 1, 16), force_default=True)
+    if args.fp8:
+        extra["fp8"] = True
     cap = spec.max_ctx
     log(f"generating {spec.name}: {spec.num_seqs} x {spec.max_ctx} tokens, {spec.hkv} kv heads")
     t0 = time.time()
@@ -377,7 +383,8 @@ def main():
     achieved = ab[dom] / (kern_us[dom] * 1e-6) / 1e9
     traffic = None
     tf = os.path.join(ROOT, "profiles", f"traffic_{args.config}.json")
-    if os.path.exists(tf) and not args.ctx and args.mode == "mosaic" and args.trunc == D and not args.force_default:
+    if os.path.exists(tf) and not args.ctx and args.mode == "mosaic" and args.trunc == D and not args.force_default \
+            and not args.fp8:
         t = json.load(open(tf))
         if t.get("source_hash") == source_hash() and t.get("kernel") == dom:
             traffic = t.get("bytes_per_launch")
@@ -467,7 +474,8 @@ def main():
                                + ("; quest mode: all channels kept, 16-token blocks, no rotation"
                                   if args.mode == "quest" else "")
                                + (f"; bitmaps of the first {args.trunc} channels" if args.trunc != D else "")
-                               + ("; default strategy forced" if args.force_default else ""),
+                               + ("; default strategy forced" if args.force_default else "")
+                               + ("; E4M3 token values" if args.fp8 else ""),
                    "mode": args.mode,
                    "num_seqs": spec.num_seqs, "ctx": spec.max_ctx, "q_heads": spec.hq, "kv_heads": spec.hkv,
                    "head_dim": D, "select": f"{spec.select[0]}/{spec.select[1]}", "mall_flush_mb": args.flush_mb},

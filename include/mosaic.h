@@ -75,12 +75,19 @@ typedef struct {
                                   truncation: after the rotation the last D - T channels are
                                   never kept and get no bitmap bit); 32, 64, 96 or 128, at
                                   least every kept count.  128 = no truncation */
+    int32_t value_fp8;         /* 1: the kept values of the K and V token records are stored as
+                                  OCP FP8 E4M3 codes (Sec. 7: the compressed elements can be
+                                  quantized further), one byte each, each the nearest code to
+                                  the fp32 rotated value (ties to the even code, saturating at
+                                  +-448, no scale factor); every kept count must then be a
+                                  multiple of 4.  Block keys, the update buffer and the staging
+                                  area keep the 16-bit dtype.  0 = 16-bit values */
 } mosaic_params;
 
 /* Fills *p with the paper's defaults (Sec. 5.5, Sec. 6.1): r in {16, 32, 48},
  * g in {4, 2, 1}, B in {16, 8, 4}, default (32, 1, 8), S = 64, U = 32,
  * W = 65536, tau = (0.30, 0.90), rho = 1/10, fp16, 8 kv heads, G = 4,
- * T = 128 (no truncation). */
+ * T = 128 (no truncation), 16-bit values. */
 void mosaic_params_default(mosaic_params *p);
 
 typedef struct mosaic_cache mosaic_cache;  /* host bookkeeping + bound arena */

@@ -35,6 +35,7 @@ class Params:
     select: tuple = (1, 10)
     force_default: bool = False
     trunc: int = 128                 # channels represented in the bitmaps (Sec. 5.2 channel truncation)
+    fp8: bool = False                # K/V token values as E4M3 codes (Sec. 7, combining with quantization)
 
     def to_c(self) -> MosaicParams:
         p = MosaicParams()
@@ -49,6 +50,7 @@ class Params:
         p.select_num, p.select_den = self.select
         p.force_default_strategy = 1 if self.force_default else 0
         p.trunc_channels = self.trunc
+        p.value_fp8 = 1 if self.fp8 else 0
         return p
 
 

@@ -28,7 +28,7 @@ class MosaicParams(C.Structure):
         ("default_keep", C.c_int32), ("default_group", C.c_int32), ("default_block", C.c_int32),
         ("tau_channel", C.c_float), ("tau_block", C.c_float),
         ("select_num", C.c_int32), ("select_den", C.c_int32), ("force_default_strategy", C.c_int32),
-        ("trunc_channels", C.c_int32),
+        ("trunc_channels", C.c_int32), ("value_fp8", C.c_int32),
     ]
 
 

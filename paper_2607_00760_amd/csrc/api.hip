@@ -71,6 +71,7 @@ struct mosaic_cache {
         g.tau_ch = P.tau_channel; g.tau_blk = P.tau_block;
         g.sel_num = P.select_num; g.sel_den = P.select_den; g.force = P.force_default_strategy;
         g.trunc = P.trunc_channels;
+        g.fp8 = P.value_fp8;
         return g;
     }
     WsGeom wsgeom(void *ws) const {
@@ -103,6 +104,7 @@ void mosaic_params_default(mosaic_params *p) {
     p->select_num = 1; p->select_den = 10;
     p->force_default_strategy = 0;
     p->trunc_channels = 128;
+    p->value_fp8 = 0;
 }
 
 static mosaic_status check_params(const mosaic_params *p) {
@@ -136,6 +138,13 @@ static mosaic_status check_params(const mosaic_params *p) {
     for (int i = 0; i < 3; ++i)
         if (p->keep_cand[i] > T) return fail(MOSAIC_ERR_INVALID, "keep_cand[%d] = %d > trunc_channels %d", i, p->keep_cand[i], T);
     if (p->default_keep > T) return fail(MOSAIC_ERR_INVALID, "default_keep %d > trunc_channels %d", p->default_keep, T);
+    if (p->value_fp8 != 0 && p->value_fp8 != 1) return fail(MOSAIC_ERR_INVALID, "value_fp8 %d: 0 or 1", p->value_fp8);
+    if (p->value_fp8) {                     // one-byte values: records stay 4-byte aligned
+        for (int i = 0; i < 3; ++i)
+            if (p->keep_cand[i] % 4)
+                return fail(MOSAIC_ERR_INVALID, "keep_cand[%d] = %d: a multiple of 4 with value_fp8", i, p->keep_cand[i]);
+        if (p->default_keep % 4) return fail(MOSAIC_ERR_INVALID, "default_keep %d: a multiple of 4 with value_fp8", p->default_keep);
+    }
     return MOSAIC_OK;
 }
 
@@ -153,16 +162,20 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     c->GP = params->group_size <= 4 ? 4 : 8;
     c->nw = (max_tokens + params->rot_window - 1) / params->rot_window;
     c->max_desc = max_tokens / SEG + 2;
-    int maxrec = 0, minb = params->default_block;
+    int maxrec = 0, maxtok = 0, minb = params->default_block;
+    const int eb = params->value_fp8 ? 1 : 2;          // bytes per value of a token record
     for (int i = 0; i < 3; ++i)
-        for (int j = 0; j < 3; ++j)
+        for (int j = 0; j < 3; ++j) {
             maxrec = std::max(maxrec, 2 * params->keep_cand[i] + 16 / params->group_cand[j]);
+            maxtok = std::max(maxtok, eb * params->keep_cand[i] + 16 / params->group_cand[j]);
+        }
     maxrec = std::max(maxrec, 2 * params->default_keep + 16 / params->default_group);
+    maxtok = std::max(maxtok, eb * params->default_keep + 16 / params->default_group);
     for (int i = 0; i < 3; ++i) minb = std::min(minb, params->block_cand[i]);
     c->maxrec = maxrec; c->minb = minb;
     // + 256: the decode kernels read whole 16-byte bitmaps and up to 2 * 128 bytes
     // of values past a vector (never used), which must stay inside the arena
-    const uint64_t tok_bytes = (uint64_t)c->max_desc * SEG * 2 * maxrec + 256;
+    const uint64_t tok_bytes = (uint64_t)c->max_desc * SEG * 2 * maxtok + 256;
     const uint64_t sc_bytes = (uint64_t)c->max_desc * (SEG / minb) * maxrec + 256;
     if (tok_bytes >= (1ull << 32)) {
         delete c;
@@ -454,8 +467,9 @@ mosaic_status mosaic_cache_stats(const mosaic_cache *c, mosaic_stats *out, void 
         int64_t used = (int64_t)meta[p].tok_tail + meta[p].sc_tail + 16ll * nd + (int64_t)nbuf * 2 * D * 2;
         if (prov) {
             const Desc &d = desc[nf];
-            const int rec = vec_bytes(d.r, d.log2g, c->P.trunc_channels);
-            used += (int64_t)UBUF * 2 * rec + (int64_t)(UBUF >> d.log2b) * rec;
+            const int rec = tok_vec_bytes(d.r, d.log2g, c->P.trunc_channels, c->P.value_fp8);
+            const int srec = vec_bytes(d.r, d.log2g, c->P.trunc_channels);
+            used += (int64_t)UBUF * 2 * rec + (int64_t)(UBUF >> d.log2b) * srec;
         }
         out->used_bytes += used;
         out->tokens += (p % hkv == 0) ? L : 0;

@@ -200,9 +200,10 @@ __device__ __forceinline__ void choose_strategy(const Geom &g, SegSmem &sm) {
     __syncthreads();
 }
 
-// Pack one vector held as (lane: channel lane, lane+64): bitmap + values.
-__device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log2g, int T, int dtype, uint64_t *keys,
-                                            uint8_t *bm_out, uint8_t *val_out, bool active) {
+// Pack one vector held as (lane: channel lane, lane+64): bitmap + values,
+// the values as E4M3 codes (one byte each) when e4m3 is set, else 16-bit.
+__device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log2g, int T, int dtype, bool e4m3,
+                                            uint64_t *keys, uint8_t *bm_out, uint8_t *val_out, bool active) {
     const int lane = threadIdx.x & 63;
     int rlo, rhi;
     group_ranks(ylo, yhi, log2g, T >> log2g, keys, rlo, rhi);
@@ -219,11 +220,13 @@ __device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     if (klo) {
         int slot = __popcll(mlo & below);
-        *(uint16_t *)(val_out + 2 * slot) = f2h(ylo, dtype);
+        if (e4m3) val_out[slot] = (uint8_t)f2e4m3(ylo);
+        else *(uint16_t *)(val_out + 2 * slot) = f2h(ylo, dtype);
     }
     if (khi) {
         int slot = __popcll(mlo) + __popcll(mhi & below);
-        *(uint16_t *)(val_out + 2 * slot) = f2h(yhi, dtype);
+        if (e4m3) val_out[slot] = (uint8_t)f2e4m3(yhi);
+        else *(uint16_t *)(val_out + 2 * slot) = f2h(yhi, dtype);
     }
     if (T < D) {
         // a truncated bitmap (T / g bits in whole 32-bit words): lane i stores byte i
@@ -243,19 +246,20 @@ __device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log
 }
 
 // Encode the workgroup's tokens (K in yk, V in yv) into the token arena at
-// tok and the block keys into the score arena at sc (Sec. 5.2).
+// tok and the block keys into the score arena at sc (Sec. 5.2).  Token
+// values are E4M3 codes when fp8 is set; block keys keep 16-bit values.
 template <int B>
 __device__ __forceinline__ void pack_segment_B(const float (&yk)[TPW][2], const float (&yv)[TPW][2], int r, int log2g, int T,
-                               int dtype, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys) {
+                               int dtype, bool fp8, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys) {
     const int wave = threadIdx.x >> 6, t0 = wave * TPW;
-    const int bmb = bm_bytes(log2g, T), vb = 2 * r, rec = bmb + vb;
+    const int bmb = bm_bytes(log2g, T), vb = fp8 ? r : 2 * r, rec = bmb + vb, srec = vec_bytes(r, log2g, T);
 #pragma unroll
     for (int i = 0; i < TPW; ++i) {
         const int t = t0 + i, bi = t / B, j = t % B;
         const bool act = t < ntok;
         uint8_t *blk = tok + (uint64_t)bi * B * 2 * rec;
-        pack_vector(yk[i][0], yk[i][1], r, log2g, T, dtype, keys, blk + j * bmb, blk + B * bmb + j * vb, act);
-        pack_vector(yv[i][0], yv[i][1], r, log2g, T, dtype, keys, blk + B * (bmb + vb) + j * bmb,
+        pack_vector(yk[i][0], yk[i][1], r, log2g, T, dtype, fp8, keys, blk + j * bmb, blk + B * bmb + j * vb, act);
+        pack_vector(yv[i][0], yv[i][1], r, log2g, T, dtype, fp8, keys, blk + B * (bmb + vb) + j * bmb,
                     blk + B * (2 * bmb + vb) + j * vb, act);
     }
 #pragma unroll
@@ -265,17 +269,17 @@ __device__ __forceinline__ void pack_segment_B(const float (&yk)[TPW][2], const 
         for (int t = 1; t < B; ++t) { mlo = mlo + yk[b0 + t][0]; mhi = mhi + yk[b0 + t][1]; }
         mlo = mlo * (1.0f / (float)B); mhi = mhi * (1.0f / (float)B);
         const int bi = (t0 + b0) / B;
-        uint8_t *rp = sc + (uint64_t)bi * rec;
-        pack_vector(mlo, mhi, r, log2g, T, dtype, keys, rp, rp + bmb, t0 + b0 < ntok);
+        uint8_t *rp = sc + (uint64_t)bi * srec;
+        pack_vector(mlo, mhi, r, log2g, T, dtype, false, keys, rp, rp + bmb, t0 + b0 < ntok);
     }
 }
 
 __device__ __forceinline__ void pack_segment(const float (&yk)[TPW][2], const float (&yv)[TPW][2], int r, int log2g, int log2b,
-                             int T, int dtype, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys) {
+                             int T, int dtype, bool fp8, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys) {
     switch (log2b) {
-        case 2: pack_segment_B<4>(yk, yv, r, log2g, T, dtype, tok, sc, ntok, keys); break;
-        case 3: pack_segment_B<8>(yk, yv, r, log2g, T, dtype, tok, sc, ntok, keys); break;
-        default: pack_segment_B<16>(yk, yv, r, log2g, T, dtype, tok, sc, ntok, keys); break;
+        case 2: pack_segment_B<4>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys); break;
+        case 3: pack_segment_B<8>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys); break;
+        default: pack_segment_B<16>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys); break;
     }
 }
 
@@ -338,7 +342,7 @@ __global__ void __launch_bounds__(256) k_prefill(Geom g, const uint16_t *k, cons
         }
     } else {
         const Desc d = *desc;
-        pack_segment(yk, yv, d.r, d.log2g, d.log2b, g.trunc, g.dtype, g.tok_of(p) + d.tok_off, g.sc_of(p) + d.sc_off,
+        pack_segment(yk, yv, d.r, d.log2g, d.log2b, g.trunc, g.dtype, g.fp8 != 0, g.tok_of(p) + d.tok_off, g.sc_of(p) + d.sc_off,
                      SEG, sm.keys[wave]);
     }
 }
@@ -358,8 +362,8 @@ __global__ void __launch_bounds__(256) k_scan(Geom g) {
         uint32_t tb = 0, sb = 0, nb = 0;
         if (s < nfull) {
             const Desc d = desc[s];
-            const uint32_t rec = (uint32_t)vec_bytes(d.r, d.log2g, g.trunc);
-            tb = SEG * 2 * rec; nb = SEG >> d.log2b; sb = nb * rec;
+            tb = SEG * 2 * (uint32_t)tok_vec_bytes(d.r, d.log2g, g.trunc, g.fp8);
+            nb = SEG >> d.log2b; sb = nb * (uint32_t)vec_bytes(d.r, d.log2g, g.trunc);
         }
         s_tok[tid] = tb; s_sc[tid] = sb; s_blk[tid] = nb;
         __syncthreads();
@@ -460,7 +464,7 @@ __global__ void __launch_bounds__(256) k_maintain(Geom g, int mode) {
     }
     const uint32_t tok_off = meta->tok_tail, sc_off = meta->sc_tail;
     const int nblk0 = meta->nblk_final;
-    pack_segment(yk, yv, r, log2g, log2b, g.trunc, g.dtype, g.tok_of(p) + tok_off, g.sc_of(p) + sc_off, ntok,
+    pack_segment(yk, yv, r, log2g, log2b, g.trunc, g.dtype, g.fp8 != 0, g.tok_of(p) + tok_off, g.sc_of(p) + sc_off, ntok,
                  sm.keys[wave]);
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -469,9 +473,8 @@ __global__ void __launch_bounds__(256) k_maintain(Geom g, int mode) {
         d.r = (uint8_t)r; d.log2g = (uint8_t)log2g; d.log2b = (uint8_t)log2b; d.flags = finalize ? 0 : 1;
         desc[seg] = d;
         if (finalize) {
-            const uint32_t rec = (uint32_t)vec_bytes(r, log2g, g.trunc);
-            meta->tok_tail = tok_off + SEG * 2 * rec;
-            meta->sc_tail = sc_off + (SEG >> log2b) * rec;
+            meta->tok_tail = tok_off + SEG * 2 * (uint32_t)tok_vec_bytes(r, log2g, g.trunc, g.fp8);
+            meta->sc_tail = sc_off + (SEG >> log2b) * (uint32_t)vec_bytes(r, log2g, g.trunc);
             meta->nblk_final = nblk0 + (SEG >> log2b);
         }
     }

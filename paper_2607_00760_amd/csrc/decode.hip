@@ -254,6 +254,36 @@ struct PVec {
     uint32_t v[RMAX / 2];
 };
 
+// A token record with one-byte E4M3 values, as loaded (four codes per word,
+// slot order from the low byte); widened to the dtype just before its walk,
+// so that the loads of a prefetch are not waited on where they are issued.
+template <int RMAX>
+struct PVec8 {
+    uint32_t bw[4];
+    uint32_t v[RMAX / 4];
+};
+
+// codes 2 HI and 2 HI + 1 of w -> the two 16-bit values of the dtype (exact:
+// every E4M3 value is a bf16 and an fp16 value), the first in the low half
+template <int DT, bool HI>
+__device__ __forceinline__ uint32_t e4m3x2(uint32_t w) {
+    if constexpr (DT) return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI));
+    else return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, HI));
+}
+
+// the first NW words of codes (4 NW values) widened into a 16-bit vector
+template <int DT, int RMAX, int NW>
+__device__ __forceinline__ void widen(const PVec8<RMAX> &c, PVec<RMAX> &x) {
+    static_assert(NW <= RMAX / 4, "code words");
+#pragma unroll
+    for (int k = 0; k < 4; ++k) x.bw[k] = c.bw[k];
+#pragma unroll
+    for (int k = 0; k < NW; ++k) {
+        x.v[2 * k] = e4m3x2<DT, false>(c.v[k]);
+        x.v[2 * k + 1] = e4m3x2<DT, true>(c.v[k]);
+    }
+}
+
 // bm and val point at the vector's bitmap and values; rmax is the largest r
 // in the wave (uniform) and a16 (uniform) says both pointers are 16-byte
 // aligned (A16: always so).  The loads take a fixed 16-byte bitmap and rmax
@@ -966,6 +996,46 @@ __device__ __forceinline__ void load_tok(PVec<RMAX> &x, const uint8_t *tokg, con
     load_pvec<RMAX, RL ? 1 : 0, false, RL>(x, b + j * bmb, b + B * bmb + j * 2 * r, rmax, false);
 }
 
+// the same for a record with E4M3 values: r bytes of values.  RL > 0: the
+// first RL / 2 16-byte granules (8 RL codes, as many values as RL granules
+// of 16-bit values), the records being 16-byte aligned; else dword loads of
+// every word below rmax, the others from the start of the values again.
+template <int RMAX, int RL>
+__device__ __forceinline__ void load_tok(PVec8<RMAX> &x, const uint8_t *tokg, const TokLoc &L, bool V_, int rmax, int T) {
+    static_assert(RL % 2 == 0 && RL <= RMAX / 8, "whole 16-byte granules of codes");
+    const int r = L.r(), l2g = L.l2g(), B = 1 << L.l2b(), bmb = bm_bytes(l2g, T), j = L.j();
+    const uint8_t *b = tokg + L.base + (V_ ? (uint32_t)(B * (bmb + r)) : 0u);
+    const uint8_t *bm = b + j * bmb, *val = b + B * bmb + j * r;
+    if constexpr (RL > 0) {
+        const uint4 bb = *(const uint4 *)bm;
+        x.bw[0] = bb.x; x.bw[1] = bb.y; x.bw[2] = bb.z; x.bw[3] = bb.w;
+        const uint4 *v4 = (const uint4 *)val;
+#pragma unroll
+        for (int k = 0; k < RL / 2; ++k) {
+            const uint4 t = v4[k];
+            x.v[4 * k] = t.x; x.v[4 * k + 1] = t.y; x.v[4 * k + 2] = t.z; x.v[4 * k + 3] = t.w;
+        }
+    } else {
+        const uint32_t *bq = (const uint32_t *)bm, *v = (const uint32_t *)val;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) x.bw[k] = bq[k];
+#pragma unroll
+        for (int k = 0; k < RMAX / 4; ++k) x.v[k] = v[(4 * k < rmax) ? k : 0];
+    }
+}
+
+// walk a loaded record into the tile (widening E4M3 codes first)
+template <int DT, int RMAX, int RL, bool COL, bool FR>
+__device__ __forceinline__ void scatter_rec(const PVec<RMAX> &x, int r, int l2g, uint32_t addr) {
+    scatter_any<RMAX, COL, FR>(x, r, l2g, addr);
+}
+template <int DT, int RMAX, int RL, bool COL, bool FR>
+__device__ __forceinline__ void scatter_rec(const PVec8<RMAX> &c, int r, int l2g, uint32_t addr) {
+    PVec<RMAX> x;
+    widen<DT, RMAX, (RL > 0 ? 2 * RL : RMAX / 4)>(c, x);
+    scatter_any<RMAX, COL, FR>(x, r, l2g, addr);
+}
+
 // A vector that keeps every channel (r = D, one channel per group): its
 // values are the dense row in channel order, so no walk is needed.  K goes to
 // the token-major row at addr with 16-byte stores, V to the channel-major
@@ -991,7 +1061,7 @@ __device__ __forceinline__ void dense_put(const uint8_t *vals, uint32_t addr) {
     }
 }
 
-template <int DT, int GP, int RMAX, bool FR>
+template <int DT, int GP, int RMAX, bool FR, bool F8>
 __global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
 k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     using M8 = typename Mma<DT>::v8;
@@ -1095,7 +1165,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             const Desc d = g.desc_of(p)[min(bs >> 4, (uint32_t)g.max_desc - 1)];
             const int jb = (int)(bs & 15u);
             r = d.r; l2g = d.log2g; l2b = d.log2b;
-            goff = d.tok_off + (uint32_t)(jb << l2b) * (uint32_t)(2 * vec_bytes(r, l2g, g.trunc));
+            goff = d.tok_off + (uint32_t)(jb << l2b) * (uint32_t)(2 * tok_vec_bytes(r, l2g, g.trunc, F8));
         }
         const int cls = on ? 4 - l2b : 3;
         const uint64_t m0 = __ballot(cls == 0), m1 = __ballot(cls == 1), m2 = __ballot(cls == 2);
@@ -1106,10 +1176,10 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         }
         const int rw = wave_max_i(on ? r : 0);
         if (lane == 0) wcnt[wave * 4 + 3] = rw;
-        // one channel per group, r % 8 == 0 and an aligned block: 16-byte
-        // bitmaps and 2r-byte value runs at 16-byte offsets
-        all16 = __syncthreads_and(!on || (l2g == 0 && (r & 7) == 0 && (goff & 15u) == 0 && g.trunc == D));
-        if (RMAX >= D) dense = __syncthreads_and(!on || (l2g == 0 && r == D));
+        // one channel per group, r % 8 == 0 (r % 16 == 0 with E4M3 values) and
+        // an aligned block: 16-byte bitmaps and value runs at 16-byte offsets
+        all16 = __syncthreads_and(!on || (l2g == 0 && (r & (F8 ? 15 : 7)) == 0 && (goff & 15u) == 0 && g.trunc == D));
+        if (RMAX >= D && !F8) dense = __syncthreads_and(!on || (l2g == 0 && r == D));
         if (on) {
             const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
             const int c16 = wcnt[0] + wcnt[4], c8 = wcnt[1] + wcnt[5];
@@ -1182,7 +1252,8 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         constexpr int RL = decltype(rlc)::value;            // < 0: dense blocks, no walk, no prefetch
         int c = wave;
         TokLoc cur = locate(c);
-        PVec<RMAX> kx, vx;
+        using PV = std::conditional_t<F8, PVec8<RMAX>, PVec<RMAX>>;
+        PV kx, vx;
         if constexpr (RL >= 0) {
             const int rm = wave_max_i(cur.r());
             __builtin_amdgcn_sched_barrier(0);
@@ -1214,7 +1285,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
                                      lds_addr(tile) + lane * (KT_STRIDE * 2));
             } else if (cur.valid) {
                 if (g.trunc < D) mask_words(kx.bw, g.trunc >> cur.l2g());
-                scatter_any<RMAX, false, FR>(kx, cur.r(), cur.l2g(), lds_addr(tile) + lane * (KT_STRIDE * 2));
+                scatter_rec<DT, RMAX, RL, false, FR>(kx, cur.r(), cur.l2g(), lds_addr(tile) + lane * (KT_STRIDE * 2));
             }
             wave_sync();
             mem_fence_compiler();
@@ -1285,7 +1356,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
                 }
             } else if (cur.valid) {
                 if (g.trunc < D) mask_words(vx.bw, g.trunc >> cur.l2g());
-                scatter_any<RMAX, true, FR>(vx, cur.r(), cur.l2g(), lds_addr(tile) + lane * 2);
+                scatter_rec<DT, RMAX, RL, true, FR>(vx, cur.r(), cur.l2g(), lds_addr(tile) + lane * 2);
             }
             wave_sync();
             mem_fence_compiler();
@@ -1345,7 +1416,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         }
     };
     bool done = false;
-    if constexpr (RMAX >= D) {
+    if constexpr (RMAX >= D && !F8) {
         if (all16 && dense) { chunks(IntC<-1>{}); done = true; }
     }
     if (!done) {
@@ -1503,9 +1574,15 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, f
     {
         const size_t smem = ATTN_HDR_BYTES + (size_t)ATTN_NWV * TILE_BYTES;
         const dim3 grid(w.max_splits * ((g.npairs + 7) / 8 * 8)), block(64 * ATTN_NWV);
-        if (fixed) hipLaunchKernelGGL((k_attn<DT, GP, 48, true>), grid, block, smem, s, g, w, scale, q);
-        else if (small) hipLaunchKernelGGL((k_attn<DT, GP, 48, false>), grid, block, smem, s, g, w, scale, q);
-        else hipLaunchKernelGGL((k_attn<DT, GP, 128, false>), grid, block, smem, s, g, w, scale, q);
+        if (g.fp8) {
+            if (fixed) hipLaunchKernelGGL((k_attn<DT, GP, 48, true, true>), grid, block, smem, s, g, w, scale, q);
+            else if (small) hipLaunchKernelGGL((k_attn<DT, GP, 48, false, true>), grid, block, smem, s, g, w, scale, q);
+            else hipLaunchKernelGGL((k_attn<DT, GP, 128, false, true>), grid, block, smem, s, g, w, scale, q);
+        } else {
+            if (fixed) hipLaunchKernelGGL((k_attn<DT, GP, 48, true, false>), grid, block, smem, s, g, w, scale, q);
+            else if (small) hipLaunchKernelGGL((k_attn<DT, GP, 48, false, false>), grid, block, smem, s, g, w, scale, q);
+            else hipLaunchKernelGGL((k_attn<DT, GP, 128, false, false>), grid, block, smem, s, g, w, scale, q);
+        }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev) hipEventRecord(ev[4], s);

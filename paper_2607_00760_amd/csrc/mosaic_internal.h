@@ -41,6 +41,7 @@ struct Geom {
     float tau_ch, tau_blk;
     int sel_num, sel_den, force;
     int trunc;                        // channels represented in the bitmaps (T)
+    int fp8;                          // K and V token values stored as E4M3 codes
 
     __host__ __device__ PairMeta *meta_of(int p) const { return (PairMeta *)(meta + (uint64_t)p * meta_stride); }
     __host__ __device__ Desc *desc_of(int p) const { return (Desc *)(desc + (uint64_t)p * desc_stride); }
@@ -85,6 +86,33 @@ __device__ __forceinline__ uint16_t f2h(float f, int dtype) {
 // record size
 __host__ __device__ __forceinline__ int bm_bytes(int log2g, int T) { return (((T >> log2g) + 31) >> 5) << 2; }
 __host__ __device__ __forceinline__ int vec_bytes(int r, int log2g, int T) { return 2 * r + bm_bytes(log2g, T); }
+// a K or V token record: one byte per kept value with E4M3 values, else two
+// (block keys always hold 16-bit values: vec_bytes)
+__host__ __device__ __forceinline__ int tok_vec_bytes(int r, int log2g, int T, int fp8) {
+    return (fp8 ? r : 2 * r) + bm_bytes(log2g, T);
+}
+
+// OCP FP8 E4M3 code (bias 7, largest finite 448, no infinities) of a finite
+// fp32 value: the nearest code, ties to the even code; magnitudes of 448 and
+// more saturate to 448.  Below 2^-6 the codes are the multiples of 2^-9
+// (x 512 is exact, then one round-to-nearest-even to an integer); above, the
+// fp32 exponent is rebiased and the mantissa rounded to 3 bits, a carry
+// moving into the exponent field.
+__device__ __forceinline__ uint32_t f2e4m3(float f) {
+    const uint32_t u = __float_as_uint(f), s = (u >> 24) & 0x80u, a = u & 0x7fffffffu;
+    uint32_t c;
+    if (a >= 0x43e00000u) {
+        c = 0x7eu;
+    } else if (a < 0x3c800000u) {
+        c = (uint32_t)__builtin_rintf(__uint_as_float(a) * 512.0f);
+    } else {
+        const uint32_t m = a & 0x7fffffu, rem = m & 0xfffffu;
+        c = (((a >> 23) - 120u) << 3) | (m >> 20);
+        c += (rem > 0x80000u || (rem == 0x80000u && (c & 1u))) ? 1u : 0u;
+        c = c > 0x7eu ? 0x7eu : c;
+    }
+    return s | c;
+}
 
 // ---------------------------------------------------------------- wave helpers
 __device__ __forceinline__ float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, WAVE); }

@@ -52,6 +52,7 @@ def test_defaults_match_paper():
     assert list(p.keep_cand) == [16, 32, 48] and list(p.group_cand) == [4, 2, 1] and list(p.block_cand) == [16, 8, 4]
     assert (p.default_keep, p.default_group, p.default_block) == (32, 1, 8)
     assert (p.select_num, p.select_den) == (1, 10)
+    assert (p.trunc_channels, p.value_fp8) == (128, 0)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -60,7 +61,10 @@ def test_defaults_match_paper():
     (dict(rot_window=100), -1), (dict(keep_cand=(16, 30, 48)), -1), (dict(group_cand=(3, 2, 1)), -1),
     (dict(block_cand=(16, 8, 2)), -1), (dict(default=(33, 1, 8)), -1), (dict(tau_channel=float("nan")), -1),
     (dict(select=(0, 10)), -1), (dict(max_tokens=0), -1), (dict(num_seqs=0), -1),
-    (dict(max_tokens=40_000_000), -3),
+    (dict(max_tokens=40_000_000), -3), (dict(trunc=100), -1), (dict(trunc=96, default=(128, 1, 8)), -1),
+    # one-byte values keep records 4-byte aligned only with kept counts that are multiples of 4
+    (dict(fp8=True, keep_cand=(18, 32, 48), group_cand=(2, 2, 1)), -1),
+    (dict(fp8=True, default=(18, 2, 8), group_cand=(2, 2, 1)), -1),
 ])
 def test_create_rejects(kw, status):
     st, h = _create(**kw)

@@ -37,6 +37,17 @@ CASES = {
     # kept counts outside 16/32/48: the general (runtime trip count) walks
     "odd_keeps": (gen.spec("c2", ctx=(1500, 900), hkv=2), dict(keep_cand=(8, 24, 40), default=(24, 2, 8),
                                                             tau_channel=0.2)),
+    # E4M3 token values: strategy search (16-byte granule and dword loads), the
+    # default strategy (fixed-count walks), kept counts that are multiples of 4
+    # but not of 16 (dword loads), every channel kept (the general walk), and
+    # with truncated bitmaps
+    "fp8_search_bf16": (gen.spec("c3", ctx=(3000, 1200), hkv=2), dict(fp8=True)),
+    "fp8_default_fp16": (gen.spec("c1", ctx=(1500, 700, 64, 5), hkv=2), dict(fp8=True, force_default=True)),
+    "fp8_keeps_by_4": (gen.spec("c2", ctx=(1500, 900), hkv=2), dict(fp8=True, keep_cand=(12, 20, 44),
+                                                                 default=(20, 2, 8), tau_channel=0.2)),
+    "fp8_keep_all": (gen.spec("c1", ctx=(333, 200), hkv=2), dict(fp8=True, force_default=True,
+                                                              default=(128, 1, 4), select=(1, 1))),
+    "fp8_truncated_96": (gen.spec("c1", ctx=(2000, 900), hkv=2), dict(fp8=True, trunc=96)),
 }
 
 
@@ -76,7 +87,7 @@ def test_decode_parity(name):
     assert_close(out.cpu().numpy(), want, name)
 
 
-@pytest.mark.parametrize("name", ["c1", "ragged_bf16_w128", "g7_student"])
+@pytest.mark.parametrize("name", ["c1", "ragged_bf16_w128", "g7_student", "fp8_search_bf16"])
 def test_append_flush_finalize_parity(name):
     spec, lay, lp, op, cap = _case(name)
     steps = 100
