@@ -19,15 +19,18 @@ namespace mosaic {
 
 namespace {
 
-constexpr int TPW = 16;            // tokens per wave
 constexpr int NCAND = 9;
 
+// NWV waves of SEG / NWV tokens each: 4 x 16 for the prefill (throughput),
+// 16 x 4 for the flush and finalize of the append path (latency: a quarter of
+// the serial work per wave and four waves per SIMD to hide it)
+template <int NWV>
 struct SegSmem {
-    float x[SEG * D];              // the segment's input tokens, fp32
+    float x[SEG * D];              // the segment's input tokens, fp32; then the rotated keys
     float tot[2][SEG];             // per-token energy (K, V)
     float drop[2][NCAND][SEG];     // per-token dropped energy per (r, g) candidate
     float bvar[3][SEG];            // per-token deviation from its block mean, per B candidate
-    uint64_t keys[4][D];           // per-wave group keys of the vector being ranked
+    uint64_t keys[NWV][D];         // per-wave group keys of the vector being ranked
     int strat[4];                  // chosen r, log2 g, log2 B
 };
 
@@ -38,10 +41,11 @@ __device__ __forceinline__ int ilog2i(int v) { return 31 - __clz(v); }
 // (rt_g[c*D + j] = R[j][c]) are read from the arena (cached: a window's R is
 // shared by all of its segments), the next four rows while the current four
 // are applied, so the workgroup keeps no copy of R in LDS.
+template <int TPW, int NWV>
 __device__ __forceinline__ void rotate_tile(const uint16_t *src, int ntok, const float *rt_g, int dtype,
-                            SegSmem &sm, float (&y)[TPW][2]) {
+                            SegSmem<NWV> &sm, float (&y)[TPW][2]) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    for (int i = tid; i < SEG * D; i += 256) {
+    for (int i = tid; i < SEG * D; i += 64 * NWV) {
         int t = i / D;
         sm.x[i] = (t < ntok) ? h2f(src[i], dtype) : 0.0f;
     }
@@ -115,11 +119,35 @@ __device__ __forceinline__ void group_ranks(float ylo, float yhi, int log2g, int
     rank_lo = rl; rank_hi = rh;
 }
 
-// Per-token statistics of one wave's 16 tokens: energy, dropped energy of
-// every (r, g) candidate; for K also the block deviation per B candidate.
+// fp32 mean of the B rotated keys of the block starting at token b0, read
+// from the staged keys ys (ascending adds, then times 1 / B)
 template <int B>
-__device__ __forceinline__ void block_dev(const float (&y)[TPW][2], float *out_tok, int t0, int valid_ntok) {
+__device__ __forceinline__ void block_mean_lds(const float *ys, int b0, float &mlo, float &mhi) {
     const int lane = threadIdx.x & 63;
+    mlo = ys[b0 * D + lane]; mhi = ys[b0 * D + lane + 64];
+#pragma unroll
+    for (int t = 1; t < B; ++t) { mlo = mlo + ys[(b0 + t) * D + lane]; mhi = mhi + ys[(b0 + t) * D + lane + 64]; }
+    mlo = mlo * (1.0f / (float)B); mhi = mhi * (1.0f / (float)B);
+}
+
+// Per-token statistics of one wave's TPW tokens: energy, dropped energy of
+// every (r, g) candidate; for K also the block deviation per B candidate
+// (blocks longer than a wave's run take their mean from the staged keys ys).
+template <int B, int TPW>
+__device__ __forceinline__ void block_dev(const float (&y)[TPW][2], float *out_tok, int t0, int valid_ntok,
+                                          const float *ys) {
+    const int lane = threadIdx.x & 63;
+    if constexpr (B > TPW) {
+        float mlo, mhi;
+        block_mean_lds<B>(ys, t0 / B * B, mlo, mhi);
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) {
+            float dl = y[t][0] - mlo, dh = y[t][1] - mhi;
+            float v = tree128(dl * dl, dh * dh);
+            if (lane == 0 && t0 + t < valid_ntok) out_tok[t0 + t] = v;
+        }
+        return;
+    }
 #pragma unroll
     for (int b0 = 0; b0 < TPW; b0 += B) {
         float mlo = y[b0][0], mhi = y[b0][1];
@@ -135,7 +163,8 @@ __device__ __forceinline__ void block_dev(const float (&y)[TPW][2], float *out_t
     }
 }
 
-__device__ __forceinline__ void token_stats(const Geom &g, const float (&y)[TPW][2], int which, SegSmem &sm, int ntok) {
+template <int TPW, int NWV>
+__device__ __forceinline__ void token_stats(const Geom &g, const float (&y)[TPW][2], int which, SegSmem<NWV> &sm, int ntok) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, t0 = wave * TPW;
     uint64_t *keys = sm.keys[wave];
     for (int i = 0; i < TPW; ++i) {
@@ -159,13 +188,14 @@ __device__ __forceinline__ void token_stats(const Geom &g, const float (&y)[TPW]
     }
 }
 
-__device__ __forceinline__ void block_stats(const Geom &g, const float (&y)[TPW][2], SegSmem &sm, int ntok) {
+template <int TPW, int NWV>
+__device__ __forceinline__ void block_stats(const Geom &g, const float (&y)[TPW][2], SegSmem<NWV> &sm, int ntok) {
     const int t0 = (threadIdx.x >> 6) * TPW;
     for (int bi = 0; bi < 3; ++bi) {
         switch (g.block_cand[bi]) {
-            case 4: block_dev<4>(y, sm.bvar[bi], t0, ntok); break;
-            case 8: block_dev<8>(y, sm.bvar[bi], t0, ntok); break;
-            default: block_dev<16>(y, sm.bvar[bi], t0, ntok); break;
+            case 4: block_dev<4, TPW>(y, sm.bvar[bi], t0, ntok, sm.x); break;
+            case 8: block_dev<8, TPW>(y, sm.bvar[bi], t0, ntok, sm.x); break;
+            default: block_dev<16, TPW>(y, sm.bvar[bi], t0, ntok, sm.x); break;
         }
     }
 }
@@ -176,7 +206,8 @@ __device__ __forceinline__ float tree64_lds(const float *v) { return tree64(v[th
 // Strategy choice (Sec. 5.5): first (r, g) in candidate order whose dropped
 // energy is below tau_ch * energy for K and for V; first B whose block
 // deviation is below tau_blk * K energy; fallbacks are the last candidates.
-__device__ __forceinline__ void choose_strategy(const Geom &g, SegSmem &sm) {
+template <int NWV>
+__device__ __forceinline__ void choose_strategy(const Geom &g, SegSmem<NWV> &sm) {
     if (threadIdx.x < 64) {
         const float TK = tree64_lds(sm.tot[0]), TV = tree64_lds(sm.tot[1]);
         int chosen = NCAND - 1;
@@ -247,10 +278,13 @@ __device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log
 
 // Encode the workgroup's tokens (K in yk, V in yv) into the token arena at
 // tok and the block keys into the score arena at sc (Sec. 5.2).  Token
-// values are E4M3 codes when fp8 is set; block keys keep 16-bit values.
-template <int B>
+// values are E4M3 codes when fp8 is set; block keys keep 16-bit values.  A
+// block longer than a wave's run gets its key from the wave holding its first
+// token, which reads the block's keys from the staged ys.
+template <int B, int TPW>
 __device__ __forceinline__ void pack_segment_B(const float (&yk)[TPW][2], const float (&yv)[TPW][2], int r, int log2g, int T,
-                               int dtype, bool fp8, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys) {
+                               int dtype, bool fp8, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys,
+                               const float *ys) {
     const int wave = threadIdx.x >> 6, t0 = wave * TPW;
     const int bmb = bm_bytes(log2g, T), vb = fp8 ? r : 2 * r, rec = bmb + vb, srec = vec_bytes(r, log2g, T);
 #pragma unroll
@@ -261,6 +295,15 @@ __device__ __forceinline__ void pack_segment_B(const float (&yk)[TPW][2], const 
         pack_vector(yk[i][0], yk[i][1], r, log2g, T, dtype, fp8, keys, blk + j * bmb, blk + B * bmb + j * vb, act);
         pack_vector(yv[i][0], yv[i][1], r, log2g, T, dtype, fp8, keys, blk + B * (bmb + vb) + j * bmb,
                     blk + B * (2 * bmb + vb) + j * vb, act);
+    }
+    if constexpr (B > TPW) {
+        if (t0 % B == 0) {                       // wave-uniform
+            float mlo, mhi;
+            block_mean_lds<B>(ys, t0, mlo, mhi);
+            uint8_t *rp = sc + (uint64_t)(t0 / B) * srec;
+            pack_vector(mlo, mhi, r, log2g, T, dtype, false, keys, rp, rp + bmb, t0 < ntok);
+        }
+        return;
     }
 #pragma unroll
     for (int b0 = 0; b0 < TPW; b0 += B) {
@@ -274,13 +317,28 @@ __device__ __forceinline__ void pack_segment_B(const float (&yk)[TPW][2], const 
     }
 }
 
+template <int TPW>
 __device__ __forceinline__ void pack_segment(const float (&yk)[TPW][2], const float (&yv)[TPW][2], int r, int log2g, int log2b,
-                             int T, int dtype, bool fp8, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys) {
+                             int T, int dtype, bool fp8, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys,
+                             const float *ys) {
     switch (log2b) {
-        case 2: pack_segment_B<4>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys); break;
-        case 3: pack_segment_B<8>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys); break;
-        default: pack_segment_B<16>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys); break;
+        case 2: pack_segment_B<4, TPW>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys, ys); break;
+        case 3: pack_segment_B<8, TPW>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys, ys); break;
+        default: pack_segment_B<16, TPW>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys, ys); break;
     }
+}
+
+// the rotated keys of the wave's tokens into sm.x (after both rotations, when
+// the input tokens are no longer needed), for blocks spanning several waves
+template <int TPW, int NWV>
+__device__ __forceinline__ void stage_keys(const float (&yk)[TPW][2], SegSmem<NWV> &sm) {
+    const int lane = threadIdx.x & 63, t0 = (threadIdx.x >> 6) * TPW;
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+        sm.x[(t0 + i) * D + lane] = yk[i][0];
+        sm.x[(t0 + i) * D + lane + 64] = yk[i][1];
+    }
+    __syncthreads();
 }
 
 // ------------------------------------------------------------------ kernels
@@ -310,7 +368,8 @@ __global__ void k_set_meta(Geom g, const int32_t *ctx) {
 // mode 0: strategy selection of full prefill segments; mode 1: packing.
 __global__ void __launch_bounds__(256) k_prefill(Geom g, const uint16_t *k, const uint16_t *v, int64_t seq_stride,
                                                  int mode) {
-    __shared__ SegSmem sm;
+    constexpr int TPW = 16, NWV = 4;
+    __shared__ SegSmem<NWV> sm;
     const int p = blockIdx.y, seg = blockIdx.x;
     const PairMeta *meta = g.meta_of(p);
     const int nfull = meta->L / SEG;
@@ -343,7 +402,7 @@ __global__ void __launch_bounds__(256) k_prefill(Geom g, const uint16_t *k, cons
     } else {
         const Desc d = *desc;
         pack_segment(yk, yv, d.r, d.log2g, d.log2b, g.trunc, g.dtype, g.fp8 != 0, g.tok_of(p) + d.tok_off, g.sc_of(p) + d.sc_off,
-                     SEG, sm.keys[wave]);
+                     SEG, sm.keys[wave], sm.x);
     }
 }
 
@@ -422,8 +481,9 @@ __global__ void k_append(Geom g, const uint16_t *kn, const uint16_t *vn) {
 
 // Provisional flush (U tokens, previous strategy) or finalize (S tokens, own
 // strategy, recompressed in place) of a pair's trailing segment.
-__global__ void __launch_bounds__(256) k_maintain(Geom g, int mode) {
-    __shared__ SegSmem sm;
+__global__ void __launch_bounds__(1024) k_maintain(Geom g, int mode) {
+    constexpr int TPW = 4, NWV = 16;
+    __shared__ SegSmem<NWV> sm;
     const int p = blockIdx.x;
     PairMeta *meta = g.meta_of(p);
     const int L = meta->L, m = L % SEG;
@@ -442,6 +502,7 @@ __global__ void __launch_bounds__(256) k_maintain(Geom g, int mode) {
     float yk[TPW][2], yv[TPW][2];
     rotate_tile(stg, ntok, rot, g.dtype, sm, yk);
     rotate_tile(stg + SEG * D, ntok, rot ? rot + D * D : nullptr, g.dtype, sm, yv);
+    stage_keys(yk, sm);
     Desc *desc = g.desc_of(p);
     const int wave = threadIdx.x >> 6;
     int r, log2g, log2b;
@@ -465,7 +526,7 @@ __global__ void __launch_bounds__(256) k_maintain(Geom g, int mode) {
     const uint32_t tok_off = meta->tok_tail, sc_off = meta->sc_tail;
     const int nblk0 = meta->nblk_final;
     pack_segment(yk, yv, r, log2g, log2b, g.trunc, g.dtype, g.fp8 != 0, g.tok_of(p) + tok_off, g.sc_of(p) + sc_off, ntok,
-                 sm.keys[wave]);
+                 sm.keys[wave], sm.x);
     __syncthreads();
     if (threadIdx.x == 0) {
         Desc d;
@@ -509,7 +570,7 @@ hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, 
     if (any_tail) {
         hipLaunchKernelGGL(k_stage_tail, dim3(g.npairs), dim3(256), 0, s, g, k, v, seq_stride);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL(k_maintain, dim3(g.npairs), dim3(256), 0, s, g, (int)MAINT_AFTER_PREFILL);
+        hipLaunchKernelGGL(k_maintain, dim3(g.npairs), dim3(1024), 0, s, g, (int)MAINT_AFTER_PREFILL);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;
@@ -521,7 +582,7 @@ hipError_t launch_append(const Geom &g, const uint16_t *k, const uint16_t *v, hi
 }
 
 hipError_t launch_maintain(const Geom &g, int mode, hipStream_t s) {
-    hipLaunchKernelGGL(k_maintain, dim3(g.npairs), dim3(256), 0, s, g, mode);
+    hipLaunchKernelGGL(k_maintain, dim3(g.npairs), dim3(1024), 0, s, g, mode);
     return hipGetLastError();
 }
 
