@@ -114,27 +114,31 @@ def log(msg):
 
 def update_path_us(M, gen, spec, params, dev):
     """Append calls of the c3 batch shape (every (sequence, kv head) pair at
-    once) on a short cache: the call whose 32nd token fills the update buffer
-    (provisional flush, Sec. 5.4) and the call that completes a 64-token
-    segment (finalize with its own strategy), against a plain append."""
+    once) on a short cache: the calls whose 32nd token fills the update buffer
+    (provisional flush, Sec. 5.4) and the calls that complete a 64-token
+    segment (finalize with its own strategy), against plain appends; medians
+    over 256 appends (4 of each kind)."""
     import torch
-    small = gen.spec(spec.name, ctx=(4096,) * spec.num_seqs, appends=64)
+    n = 256
+    small = gen.spec(spec.name, ctx=(4096,) * spec.num_seqs, appends=n)
     lay = gen.make_layer(small, 0, device=dev, capacity=small.capacity)
     cache = M.MosaicCache(params, small.num_seqs, small.capacity, rotated=small.rotate, device=dev)
     cache.compress(lay["k"], lay["v"], lay["ctx_lens"], lay["rot_k"], lay["rot_v"])
-    apps = [tuple(x.to(dev) for x in gen.make_appends(small, t)) for t in range(64)]
+    apps = [tuple(x.to(dev) for x in gen.make_appends(small, t)) for t in range(n)]
     torch.cuda.synchronize()
     times = []
-    for t in range(64):
+    for t in range(n):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
         cache.append(*apps[t])
         b.record()
         torch.cuda.synchronize()
         times.append(1e3 * a.elapsed_time(b))
-    plain = [x for i, x in enumerate(times) if i not in (31, 63)]
-    return {"pairs": small.num_seqs * small.hkv, "append_us": round(float(sorted(plain)[len(plain) // 2]), 1),
-            "append_with_flush_us": round(times[31], 1), "append_with_finalize_us": round(times[63], 1)}
+    med = lambda xs: round(float(sorted(xs)[len(xs) // 2]), 1)
+    kind = lambda t: (t + 1) % 64 == 0 and 2 or ((t + 1) % 32 == 0 and 1) or 0   # 4096 + t + 1 tokens after call t
+    return {"pairs": small.num_seqs * small.hkv, "append_us": med([x for t, x in enumerate(times) if kind(t) == 0]),
+            "append_with_flush_us": med([x for t, x in enumerate(times) if kind(t) == 1]),
+            "append_with_finalize_us": med([x for t, x in enumerate(times) if kind(t) == 2]), "samples": n}
 
 
 def encoding_overlap(cache, lay, dev, compress_ms):

@@ -319,16 +319,16 @@ mosaic_status mosaic_append(mosaic_cache *c, const void *k_new, const void *v_ne
     if (!c->arena || !c->compressed) return fail(MOSAIC_ERR_STATE, "append before compress");
     if (!k_new || !v_new) return fail(MOSAIC_ERR_INVALID, "NULL k_new or v_new");
     if (((uintptr_t)k_new | (uintptr_t)v_new) % 4) return fail(MOSAIC_ERR_INVALID, "k_new/v_new must be 4-byte aligned");
-    bool due = false;
+    int due = 0;                            // MAINT_FLUSH / MAINT_FINALIZE of some sequence
     for (int q = 0; q < c->num_seqs; ++q) {
         if (c->L[q] + 1 > c->max_tokens) return fail(MOSAIC_ERR_CAPACITY, "sequence %d is full (%d tokens)", q, c->L[q]);
-        due |= ((c->L[q] + 1) % UBUF) == 0;
+        if ((c->L[q] + 1) % UBUF == 0) due |= ((c->L[q] + 1) % SEG == 0) ? MAINT_FINALIZE : MAINT_FLUSH;
     }
     hipStream_t s = (hipStream_t)stream;
     const Geom g = c->geom();
     hipError_t e = launch_append(g, (const uint16_t *)k_new, (const uint16_t *)v_new, s);
     if (e != hipSuccess) return hip_fail(e, "append launch");
-    if (due && (e = launch_maintain(g, MAINT_APPEND, s)) != hipSuccess) return hip_fail(e, "flush/finalize launch");
+    if (due && (e = launch_maintain(g, MAINT_APPEND, due, s)) != hipSuccess) return hip_fail(e, "flush/finalize launch");
     for (int q = 0; q < c->num_seqs; ++q) c->L[q] += 1;
     return ok();
 }

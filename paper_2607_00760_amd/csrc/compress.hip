@@ -45,7 +45,7 @@ template <int TPW, int NWV>
 __device__ __forceinline__ void rotate_tile(const uint16_t *src, int ntok, const float *rt_g, int dtype,
                             SegSmem<NWV> &sm, float (&y)[TPW][2]) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    for (int i = tid; i < SEG * D; i += 64 * NWV) {
+    for (int i = tid; i < NWV * TPW * D; i += 64 * NWV) {
         int t = i / D;
         sm.x[i] = (t < ntok) ? h2f(src[i], dtype) : 0.0f;
     }
@@ -280,12 +280,16 @@ __device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log
 // tok and the block keys into the score arena at sc (Sec. 5.2).  Token
 // values are E4M3 codes when fp8 is set; block keys keep 16-bit values.  A
 // block longer than a wave's run gets its key from the wave holding its first
-// token, which reads the block's keys from the staged ys.
+// token, which reads the block's keys from the staged ys.  The workgroup holds
+// tokens tb.. of the ntok being encoded (tb a multiple of every block size).
 template <int B, int TPW>
 __device__ __forceinline__ void pack_segment_B(const float (&yk)[TPW][2], const float (&yv)[TPW][2], int r, int log2g, int T,
                                int dtype, bool fp8, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys,
-                               const float *ys) {
+                               const float *ys, int tb) {
     const int wave = threadIdx.x >> 6, t0 = wave * TPW;
+    tok += (uint64_t)(tb / B) * B * 2 * (bm_bytes(log2g, T) + (fp8 ? r : 2 * r));
+    sc += (uint64_t)(tb / B) * vec_bytes(r, log2g, T);
+    ntok -= tb;
     const int bmb = bm_bytes(log2g, T), vb = fp8 ? r : 2 * r, rec = bmb + vb, srec = vec_bytes(r, log2g, T);
 #pragma unroll
     for (int i = 0; i < TPW; ++i) {
@@ -320,11 +324,11 @@ __device__ __forceinline__ void pack_segment_B(const float (&yk)[TPW][2], const 
 template <int TPW>
 __device__ __forceinline__ void pack_segment(const float (&yk)[TPW][2], const float (&yv)[TPW][2], int r, int log2g, int log2b,
                              int T, int dtype, bool fp8, uint8_t *tok, uint8_t *sc, int ntok, uint64_t *keys,
-                             const float *ys) {
+                             const float *ys, int tb) {
     switch (log2b) {
-        case 2: pack_segment_B<4, TPW>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys, ys); break;
-        case 3: pack_segment_B<8, TPW>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys, ys); break;
-        default: pack_segment_B<16, TPW>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys, ys); break;
+        case 2: pack_segment_B<4, TPW>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys, ys, tb); break;
+        case 3: pack_segment_B<8, TPW>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys, ys, tb); break;
+        default: pack_segment_B<16, TPW>(yk, yv, r, log2g, T, dtype, fp8, tok, sc, ntok, keys, ys, tb); break;
     }
 }
 
@@ -402,7 +406,7 @@ __global__ void __launch_bounds__(256) k_prefill(Geom g, const uint16_t *k, cons
     } else {
         const Desc d = *desc;
         pack_segment(yk, yv, d.r, d.log2g, d.log2b, g.trunc, g.dtype, g.fp8 != 0, g.tok_of(p) + d.tok_off, g.sc_of(p) + d.sc_off,
-                     SEG, sm.keys[wave], sm.x);
+                     SEG, sm.keys[wave], sm.x, 0);
     }
 }
 
@@ -479,66 +483,138 @@ __global__ void k_append(Geom g, const uint16_t *kn, const uint16_t *vn) {
     if (threadIdx.x == 0) meta->L = L + 1;
 }
 
-// Provisional flush (U tokens, previous strategy) or finalize (S tokens, own
-// strategy, recompressed in place) of a pair's trailing segment.
-__global__ void __launch_bounds__(1024) k_maintain(Geom g, int mode) {
-    constexpr int TPW = 4, NWV = 16;
-    __shared__ SegSmem<NWV> sm;
-    const int p = blockIdx.x;
-    PairMeta *meta = g.meta_of(p);
-    const int L = meta->L, m = L % SEG;
-    bool finalize = false, flush = false;
+// Provisional flush (U tokens, previous strategy) and finalize (S tokens, own
+// strategy, recompressed in place) of a pair's trailing segment.  Both are
+// latency-bound (a few dozen pairs at a time), so a pair's work is spread over
+// workgroups of 4 waves x 4 tokens (blockIdx.y: tokens 16 y .. 16 y + 15): two
+// for the flush, four for each of the finalize's two kernels.  The finalize's
+// strategy needs every token's statistics, so its first kernel writes them to
+// the pair's update buffer, which is empty when a segment completes (every
+// buffered token belongs to it) and is next written by the following append.
+constexpr int MT_TPW = 4, MT_NWV = 4, MT_TOK = MT_TPW * MT_NWV;
+constexpr int FST_N = 2 + 2 * NCAND + 3;           // per-token statistics: tot K/V, drop K/V x 9, bvar x 3
+static_assert(FST_N * SEG * 4 + 16 <= 2 * UBUF * D * 2, "finalize statistics and offsets fit the update buffer");
+
+__device__ __forceinline__ bool maint_due(const Geom &g, int mode, int L, bool fin) {
+    const int m = L % SEG;
     if (mode == MAINT_APPEND) {
-        if (L > 0 && (L % UBUF) == 0) { finalize = (m == 0); flush = !finalize; }
-    } else {
-        flush = m >= UBUF;
+        if (L <= 0 || (L % UBUF) != 0) return false;
+        return fin ? m == 0 : m != 0;
     }
-    if (!finalize && !flush) return;
-    const int seg = finalize ? L / SEG - 1 : L / SEG;
-    const int ntok = finalize ? SEG : UBUF;
+    return !fin && m >= UBUF;
+}
+
+// rotate this workgroup's tokens of the trailing segment (K into yk, V into
+// yv) and stage the rotated keys for blocks spanning several waves
+__device__ __forceinline__ void maint_rotate(const Geom &g, int p, int seg, int tb, int ntok, SegSmem<MT_NWV> &sm,
+                                             float (&yk)[MT_TPW][2], float (&yv)[MT_TPW][2]) {
     const int win = (seg * SEG) / g.W;
     const float *rot = g.rotated ? g.rot_of(p, win) : nullptr;
-    const uint16_t *stg = g.stg_of(p);
-    float yk[TPW][2], yv[TPW][2];
-    rotate_tile(stg, ntok, rot, g.dtype, sm, yk);
-    rotate_tile(stg + SEG * D, ntok, rot ? rot + D * D : nullptr, g.dtype, sm, yv);
+    const uint16_t *stg = g.stg_of(p) + (uint64_t)tb * D;
+    rotate_tile(stg, ntok - tb, rot, g.dtype, sm, yk);
+    rotate_tile(stg + SEG * D, ntok - tb, rot ? rot + D * D : nullptr, g.dtype, sm, yv);
     stage_keys(yk, sm);
-    Desc *desc = g.desc_of(p);
+}
+
+__device__ __forceinline__ void maint_pack(const Geom &g, int p, int seg, int tb, int ntok, bool fin, int r, int log2g,
+                                           int log2b, uint32_t tok_off, uint32_t sc_off, int nblk0,
+                                           SegSmem<MT_NWV> &sm, const float (&yk)[MT_TPW][2],
+                                           const float (&yv)[MT_TPW][2]) {
     const int wave = threadIdx.x >> 6;
-    int r, log2g, log2b;
-    if (finalize) {
-        if (g.force) {
-            r = g.def_keep; log2g = ilog2i(g.def_group); log2b = ilog2i(g.def_block);
-        } else {
-            token_stats(g, yk, 0, sm, SEG);
-            token_stats(g, yv, 1, sm, SEG);
-            block_stats(g, yk, sm, SEG);
-            __syncthreads();
-            choose_strategy(g, sm);
-            r = sm.strat[0]; log2g = sm.strat[1]; log2b = sm.strat[2];
-        }
-    } else if (seg > 0) {
-        const Desc pd = desc[seg - 1];
-        r = pd.r; log2g = pd.log2g; log2b = pd.log2b;
-    } else {
-        r = g.def_keep; log2g = ilog2i(g.def_group); log2b = ilog2i(g.def_block);
-    }
-    const uint32_t tok_off = meta->tok_tail, sc_off = meta->sc_tail;
-    const int nblk0 = meta->nblk_final;
     pack_segment(yk, yv, r, log2g, log2b, g.trunc, g.dtype, g.fp8 != 0, g.tok_of(p) + tok_off, g.sc_of(p) + sc_off, ntok,
-                 sm.keys[wave], sm.x);
-    __syncthreads();
-    if (threadIdx.x == 0) {
+                 sm.keys[wave], sm.x, tb);
+    if (threadIdx.x == 0 && blockIdx.y == 0) {
         Desc d;
         d.tok_off = tok_off; d.sc_off = sc_off; d.first_block = (uint32_t)nblk0;
-        d.r = (uint8_t)r; d.log2g = (uint8_t)log2g; d.log2b = (uint8_t)log2b; d.flags = finalize ? 0 : 1;
-        desc[seg] = d;
-        if (finalize) {
+        d.r = (uint8_t)r; d.log2g = (uint8_t)log2g; d.log2b = (uint8_t)log2b; d.flags = fin ? 0 : 1;
+        g.desc_of(p)[seg] = d;
+        if (fin) {
+            PairMeta *meta = g.meta_of(p);
             meta->tok_tail = tok_off + SEG * 2 * (uint32_t)tok_vec_bytes(r, log2g, g.trunc, g.fp8);
             meta->sc_tail = sc_off + (SEG >> log2b) * (uint32_t)vec_bytes(r, log2g, g.trunc);
             meta->nblk_final = nblk0 + (SEG >> log2b);
         }
     }
+}
+
+__global__ void __launch_bounds__(256) k_flush(Geom g, int mode) {
+    __shared__ SegSmem<MT_NWV> sm;
+    const int p = blockIdx.x;
+    const PairMeta *meta = g.meta_of(p);
+    const int L = meta->L;
+    if (!maint_due(g, mode, L, false)) return;
+    const int seg = L / SEG, tb = (int)blockIdx.y * MT_TOK;
+    float yk[MT_TPW][2], yv[MT_TPW][2];
+    maint_rotate(g, p, seg, tb, UBUF, sm, yk, yv);
+    int r, log2g, log2b;
+    if (seg > 0) {
+        const Desc pd = g.desc_of(p)[seg - 1];
+        r = pd.r; log2g = pd.log2g; log2b = pd.log2b;
+    } else {
+        r = g.def_keep; log2g = ilog2i(g.def_group); log2b = ilog2i(g.def_block);
+    }
+    // a flush leaves the tails alone: every workgroup reads the same offsets
+    maint_pack(g, p, seg, tb, UBUF, false, r, log2g, log2b, meta->tok_tail, meta->sc_tail, meta->nblk_final, sm, yk, yv);
+}
+
+// finalize, first kernel: statistics of this workgroup's 16 tokens into the
+// scratch st[FST_N][SEG] (fp32) and, from workgroup 0, the segment's starting
+// offsets after it (the second kernel changes the tails)
+__global__ void __launch_bounds__(256) k_fin_stats(Geom g) {
+    __shared__ SegSmem<MT_NWV> sm;
+    const int p = blockIdx.x;
+    const PairMeta *meta = g.meta_of(p);
+    const int L = meta->L;
+    if (!maint_due(g, MAINT_APPEND, L, true)) return;
+    const int seg = L / SEG - 1, tb = (int)blockIdx.y * MT_TOK;
+    float *st = (float *)g.buf_of(p);
+    if (blockIdx.y == 0 && threadIdx.x == 0) {
+        uint32_t *off = (uint32_t *)(st + FST_N * SEG);
+        off[0] = meta->tok_tail; off[1] = meta->sc_tail; off[2] = (uint32_t)meta->nblk_final;
+    }
+    if (g.force) return;
+    float yk[MT_TPW][2], yv[MT_TPW][2];
+    maint_rotate(g, p, seg, tb, SEG, sm, yk, yv);
+    token_stats(g, yk, 0, sm, MT_TOK);
+    token_stats(g, yv, 1, sm, MT_TOK);
+    block_stats(g, yk, sm, MT_TOK);
+    __syncthreads();
+    for (int i = threadIdx.x; i < FST_N * MT_TOK; i += 256) {
+        const int k = i / MT_TOK, t = i % MT_TOK;
+        const float v = k < 2 ? sm.tot[k][t] : (k < 2 + 2 * NCAND ? sm.drop[(k - 2) / NCAND][(k - 2) % NCAND][t]
+                                                                  : sm.bvar[k - 2 - 2 * NCAND][t]);
+        st[k * SEG + tb + t] = v;
+    }
+}
+
+// finalize, second kernel: every workgroup takes the same strategy from the
+// 64 tokens' statistics, then packs its 16 tokens
+__global__ void __launch_bounds__(256) k_fin_pack(Geom g) {
+    __shared__ SegSmem<MT_NWV> sm;
+    const int p = blockIdx.x;
+    const int L = g.meta_of(p)->L;
+    if (!maint_due(g, MAINT_APPEND, L, true)) return;
+    const int seg = L / SEG - 1, tb = (int)blockIdx.y * MT_TOK;
+    const float *st = (const float *)g.buf_of(p);
+    const uint32_t *off = (const uint32_t *)(st + FST_N * SEG);
+    float yk[MT_TPW][2], yv[MT_TPW][2];
+    maint_rotate(g, p, seg, tb, SEG, sm, yk, yv);
+    int r, log2g, log2b;
+    if (g.force) {
+        r = g.def_keep; log2g = ilog2i(g.def_group); log2b = ilog2i(g.def_block);
+    } else {
+        for (int i = threadIdx.x; i < FST_N * SEG; i += 256) {
+            const int k = i / SEG, t = i % SEG;
+            const float v = st[i];
+            if (k < 2) sm.tot[k][t] = v;
+            else if (k < 2 + 2 * NCAND) sm.drop[(k - 2) / NCAND][(k - 2) % NCAND][t] = v;
+            else sm.bvar[k - 2 - 2 * NCAND][t] = v;
+        }
+        __syncthreads();
+        choose_strategy(g, sm);
+        r = sm.strat[0]; log2g = sm.strat[1]; log2b = sm.strat[2];
+    }
+    maint_pack(g, p, seg, tb, SEG, true, r, log2g, log2b, off[0], off[1], (int)off[2], sm, yk, yv);
 }
 
 }  // namespace
@@ -570,8 +646,7 @@ hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, 
     if (any_tail) {
         hipLaunchKernelGGL(k_stage_tail, dim3(g.npairs), dim3(256), 0, s, g, k, v, seq_stride);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL(k_maintain, dim3(g.npairs), dim3(1024), 0, s, g, (int)MAINT_AFTER_PREFILL);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = launch_maintain(g, MAINT_AFTER_PREFILL, MAINT_FLUSH, s)) != hipSuccess) return e;
     }
     return hipSuccess;
 }
@@ -581,9 +656,19 @@ hipError_t launch_append(const Geom &g, const uint16_t *k, const uint16_t *v, hi
     return hipGetLastError();
 }
 
-hipError_t launch_maintain(const Geom &g, int mode, hipStream_t s) {
-    hipLaunchKernelGGL(k_maintain, dim3(g.npairs), dim3(1024), 0, s, g, mode);
-    return hipGetLastError();
+hipError_t launch_maintain(const Geom &g, int mode, int what, hipStream_t s) {
+    hipError_t e;
+    if (what & MAINT_FLUSH) {
+        hipLaunchKernelGGL(k_flush, dim3(g.npairs, UBUF / MT_TOK), dim3(256), 0, s, g, mode);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if ((what & MAINT_FINALIZE) && mode == MAINT_APPEND) {
+        hipLaunchKernelGGL(k_fin_stats, dim3(g.npairs, SEG / MT_TOK), dim3(256), 0, s, g);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(k_fin_pack, dim3(g.npairs, SEG / MT_TOK), dim3(256), 0, s, g);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace mosaic

@@ -173,7 +173,9 @@ hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, 
                            const int32_t *ctx_dev, int max_full_segs, int any_tail, hipStream_t s);
 hipError_t launch_set_meta(const Geom &g, const int32_t *ctx_dev, hipStream_t s);
 hipError_t launch_append(const Geom &g, const uint16_t *k, const uint16_t *v, hipStream_t s);
-hipError_t launch_maintain(const Geom &g, int mode, hipStream_t s);
+// what: MAINT_FLUSH and / or MAINT_FINALIZE, the kernels to launch (each
+// acts only on the pairs whose state calls for it)
+hipError_t launch_maintain(const Geom &g, int mode, int what, hipStream_t s);
 hipError_t launch_decode(const Geom &g, const WsGeom &w, const uint16_t *q, float *out, float scale,
                          int max_desc_used, int max_windows_used, hipStream_t s, hipEvent_t *ev);
 hipError_t launch_dense(const uint16_t *q, const uint16_t *k, const uint16_t *v, float *out, int nseq,
@@ -189,5 +191,7 @@ hipError_t launch_rotations(const uint16_t *k, const uint16_t *v, int64_t seq_st
 
 constexpr int MAINT_APPEND = 0;        // after an append: flush or finalize where a buffer filled
 constexpr int MAINT_AFTER_PREFILL = 1; // after compress: flush a >= U-token remainder
+constexpr int MAINT_FLUSH = 1;
+constexpr int MAINT_FINALIZE = 2;
 
 }  // namespace mosaic
