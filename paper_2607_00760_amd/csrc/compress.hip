@@ -486,12 +486,12 @@ __global__ void k_append(Geom g, const uint16_t *kn, const uint16_t *vn) {
 // Provisional flush (U tokens, previous strategy) and finalize (S tokens, own
 // strategy, recompressed in place) of a pair's trailing segment.  Both are
 // latency-bound (a few dozen pairs at a time), so a pair's work is spread over
-// workgroups of 4 waves x 4 tokens (blockIdx.y: tokens 16 y .. 16 y + 15): two
+// workgroups of 8 waves x 2 tokens (blockIdx.y: tokens 16 y .. 16 y + 15): two
 // for the flush, four for each of the finalize's two kernels.  The finalize's
 // strategy needs every token's statistics, so its first kernel writes them to
 // the pair's update buffer, which is empty when a segment completes (every
 // buffered token belongs to it) and is next written by the following append.
-constexpr int MT_TPW = 4, MT_NWV = 4, MT_TOK = MT_TPW * MT_NWV;
+constexpr int MT_TPW = 2, MT_NWV = 8, MT_TOK = MT_TPW * MT_NWV, MT_THREADS = 64 * MT_NWV;
 constexpr int FST_N = 2 + 2 * NCAND + 3;           // per-token statistics: tot K/V, drop K/V x 9, bvar x 3
 static_assert(FST_N * SEG * 4 + 16 <= 2 * UBUF * D * 2, "finalize statistics and offsets fit the update buffer");
 
@@ -537,7 +537,7 @@ __device__ __forceinline__ void maint_pack(const Geom &g, int p, int seg, int tb
     }
 }
 
-__global__ void __launch_bounds__(256) k_flush(Geom g, int mode) {
+__global__ void __launch_bounds__(MT_THREADS) k_flush(Geom g, int mode) {
     __shared__ SegSmem<MT_NWV> sm;
     const int p = blockIdx.x;
     const PairMeta *meta = g.meta_of(p);
@@ -560,7 +560,7 @@ __global__ void __launch_bounds__(256) k_flush(Geom g, int mode) {
 // finalize, first kernel: statistics of this workgroup's 16 tokens into the
 // scratch st[FST_N][SEG] (fp32) and, from workgroup 0, the segment's starting
 // offsets after it (the second kernel changes the tails)
-__global__ void __launch_bounds__(256) k_fin_stats(Geom g) {
+__global__ void __launch_bounds__(MT_THREADS) k_fin_stats(Geom g) {
     __shared__ SegSmem<MT_NWV> sm;
     const int p = blockIdx.x;
     const PairMeta *meta = g.meta_of(p);
@@ -579,7 +579,7 @@ __global__ void __launch_bounds__(256) k_fin_stats(Geom g) {
     token_stats(g, yv, 1, sm, MT_TOK);
     block_stats(g, yk, sm, MT_TOK);
     __syncthreads();
-    for (int i = threadIdx.x; i < FST_N * MT_TOK; i += 256) {
+    for (int i = threadIdx.x; i < FST_N * MT_TOK; i += MT_THREADS) {
         const int k = i / MT_TOK, t = i % MT_TOK;
         const float v = k < 2 ? sm.tot[k][t] : (k < 2 + 2 * NCAND ? sm.drop[(k - 2) / NCAND][(k - 2) % NCAND][t]
                                                                   : sm.bvar[k - 2 - 2 * NCAND][t]);
@@ -589,7 +589,7 @@ __global__ void __launch_bounds__(256) k_fin_stats(Geom g) {
 
 // finalize, second kernel: every workgroup takes the same strategy from the
 // 64 tokens' statistics, then packs its 16 tokens
-__global__ void __launch_bounds__(256) k_fin_pack(Geom g) {
+__global__ void __launch_bounds__(MT_THREADS) k_fin_pack(Geom g) {
     __shared__ SegSmem<MT_NWV> sm;
     const int p = blockIdx.x;
     const int L = g.meta_of(p)->L;
@@ -603,7 +603,7 @@ __global__ void __launch_bounds__(256) k_fin_pack(Geom g) {
     if (g.force) {
         r = g.def_keep; log2g = ilog2i(g.def_group); log2b = ilog2i(g.def_block);
     } else {
-        for (int i = threadIdx.x; i < FST_N * SEG; i += 256) {
+        for (int i = threadIdx.x; i < FST_N * SEG; i += MT_THREADS) {
             const int k = i / SEG, t = i % SEG;
             const float v = st[i];
             if (k < 2) sm.tot[k][t] = v;
@@ -659,13 +659,13 @@ hipError_t launch_append(const Geom &g, const uint16_t *k, const uint16_t *v, hi
 hipError_t launch_maintain(const Geom &g, int mode, int what, hipStream_t s) {
     hipError_t e;
     if (what & MAINT_FLUSH) {
-        hipLaunchKernelGGL(k_flush, dim3(g.npairs, UBUF / MT_TOK), dim3(256), 0, s, g, mode);
+        hipLaunchKernelGGL(k_flush, dim3(g.npairs, UBUF / MT_TOK), dim3(MT_THREADS), 0, s, g, mode);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if ((what & MAINT_FINALIZE) && mode == MAINT_APPEND) {
-        hipLaunchKernelGGL(k_fin_stats, dim3(g.npairs, SEG / MT_TOK), dim3(256), 0, s, g);
+        hipLaunchKernelGGL(k_fin_stats, dim3(g.npairs, SEG / MT_TOK), dim3(MT_THREADS), 0, s, g);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL(k_fin_pack, dim3(g.npairs, SEG / MT_TOK), dim3(256), 0, s, g);
+        hipLaunchKernelGGL(k_fin_pack, dim3(g.npairs, SEG / MT_TOK), dim3(MT_THREADS), 0, s, g);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;
