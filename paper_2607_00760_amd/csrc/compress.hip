@@ -6,13 +6,15 @@
 //   Sec. 5.5), the update buffer (Sec. 5.3) and heterogeneous double
 //   compression buffering (Sec. 5.4).
 //
-// Work decomposition: one 256-thread workgroup per 64-token segment.  Wave w
-// owns tokens [16w, 16w+16); lane l owns channels l and l+64, so a vector's
-// 128 channels live in one wave and channel trees, ranks, bitmaps and slot
-// numbers are wave-local (butterflies, ballots, mbcnt).  The rotation is an
-// fp32 fused-multiply-add chain over ascending input channels per output
-// channel (R^T staged in LDS, x broadcast from LDS), so every rotated value,
-// kept index and packed byte is reproducible bit for bit.
+// Work decomposition: the prefill runs one 256-thread workgroup per 64-token
+// segment, wave w owning tokens [16w, 16w+16); the append path's flush and
+// finalize run 16-token workgroups of 8 waves x 2 tokens.  Lane l owns
+// channels l and l+64, so a vector's 128 channels live in one wave and
+// channel trees, ranks, bitmaps and slot numbers are wave-local (butterflies,
+// ballots, mbcnt).  The rotation is an fp32 fused-multiply-add chain over
+// ascending input channels per output channel (rows of R^T read from the
+// arena, x broadcast from LDS), so every rotated value, kept index and packed
+// byte is reproducible bit for bit.
 #include "mosaic_internal.h"
 
 namespace mosaic {
