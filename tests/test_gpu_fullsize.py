@@ -229,6 +229,26 @@ def test_c3_quest_mode_full_size_sampled():
     _check_decode(c, spec, ops, q, out, "c3 quest")
 
 
+def test_c3_fp8_full_size_sampled():
+    """E4M3 token values on the full 8 x 131072 bf16 workload with the
+    strategy search: sampled pairs against the oracle (bytes, scores,
+    selections, outputs)."""
+    spec = gen.spec("c3")
+    print(f"[fullsize] c3 fp8 {spec.num_seqs}x{spec.max_ctx}", flush=True)
+    cap = spec.capacity
+    lay = gen.make_layer(spec, 0, device="cuda", capacity=cap)
+    lp, op = params_pair(spec, fp8=True)
+    c = gpu_cache(lp, spec, lay, cap)
+    q = lay["queries"]
+    out = c.decode(q, scale_of())
+    torch.cuda.synchronize()
+    pairs = _sample(spec.num_seqs * spec.hkv, 2, 6)
+    ops = _oracle_pairs(op, spec, lay, cap, pairs)
+    for pi, pr in ops.items():
+        assert_state_equal(c, pi, pr, where="c3 fp8")
+    _check_decode(c, spec, ops, q, out, "c3 fp8")
+
+
 def test_c3_gpu_rotations_full_size_sampled():
     """GPU rotation matrices of the full c3 cache (256 matrices of 65536
     tokens): sampled windows against the fp64 oracle (orthonormal rows,
