@@ -247,6 +247,11 @@ __device__ __forceinline__ uint32_t half_at(const uint32_t (&v)[N], int s) {
     return (s & 1) ? (v[s >> 1] >> 16) : (v[s >> 1] & 0xffffu);
 }
 
+// 16 bytes at a 4-byte aligned address: every record is 4-byte aligned, and
+// the target runs vector memory loads in unaligned mode, so one dwordx4 load
+// serves any record (the compiler merges plain dword runs the same way)
+typedef uint32_t u32x4a4 __attribute__((ext_vector_type(4), aligned(4)));
+
 // A packed vector (bitmap words + values) held in registers.
 template <int RMAX>
 struct PVec {
@@ -300,18 +305,19 @@ __device__ __forceinline__ void widen(const PVec8<RMAX> &c, PVec<RMAX> &x) {
 // prefetch into loop-carried registers leaves no join whose bookkeeping would
 // make the wave wait on loads that are still in flight.
 //
-// RL > 0 (with A16 = 1): exactly the first RL 16-byte granules of values, with
-// no condition (the caller knows r <= 8 RL for every lane of the wave).
+// RL > 0: exactly the first RL 16-byte granules of values and a 16-byte
+// bitmap, with no condition (the caller knows r <= 8 RL for every lane of the
+// wave), at any 4-byte aligned record.
 template <int RMAX, int A16, bool ZF, int RL = 0>
 __device__ __forceinline__ void load_pvec(PVec<RMAX> &x, const uint8_t *bm, const uint8_t *val, int rmax, bool a16) {
-    static_assert(RL == 0 || (A16 == 1 && RL <= RMAX / 8), "fixed granule count needs aligned records");
+    static_assert(RL == 0 || (A16 == 1 && RL <= RMAX / 8), "fixed granule count");
     if (RL > 0) {
-        const uint4 b = *(const uint4 *)bm;
+        const u32x4a4 b = *(const u32x4a4 *)bm;
         x.bw[0] = b.x; x.bw[1] = b.y; x.bw[2] = b.z; x.bw[3] = b.w;
-        const uint4 *v4 = (const uint4 *)val;
+        const u32x4a4 *v4 = (const u32x4a4 *)val;
 #pragma unroll
         for (int k = 0; k < RL; ++k) {
-            const uint4 t = v4[k];
+            const u32x4a4 t = v4[k];
             x.v[4 * k] = t.x; x.v[4 * k + 1] = t.y; x.v[4 * k + 2] = t.z; x.v[4 * k + 3] = t.w;
         }
     } else if (A16 == 1 || (A16 == -1 && a16)) {
@@ -467,7 +473,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         const int o = (int)(d.first_block - fb0);
         for (int j = 0; j < nb; ++j) b2s[o + j] = (uint8_t)tid;
         if (tid == ns - 1) s_nblk = o + nb;
-        plain = d.log2g == 0 && (d.r & 7) == 0 && d.r <= 32 && (d.sc_off & 15u) == 0 && g.trunc == D;
+        plain = d.log2g == 0 && d.r <= 32 && (d.sc_off & 3u) == 0;
         dense = d.log2g == 0 && d.r == D && (d.sc_off & 15u) == 0;
     }
     const int w0 = g.rotated ? (s0 * SEG) / g.W : 0;
@@ -537,28 +543,31 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         }
     }
     if (plain) {
-        // every record is 16-byte aligned with at most 32 values: four fixed
-        // 16-byte value loads, and the next key's record is loaded while the
-        // current one is scored (one load form, so no join waits on it)
+        // one channel per group and at most 32 values: a 16-byte bitmap and
+        // four fixed 16-byte value loads at any 4-byte aligned record, and the
+        // next key's record is loaded while the current one is scored (one
+        // load form, so no join waits on it)
         auto where = [&](int b, int &i, int &j, int &r) {
             const bool valid = b < nblk;
             i = valid ? b2s[b] : 0;
             const Desc d = ds[i];
             j = b - (int)(d.first_block - fb0);
             r = valid ? d.r : 0;
-            return valid ? sc + d.sc_off + (uint32_t)j * (uint32_t)vec_bytes(d.r, 0, D) : sc;
+            return valid ? sc + d.sc_off + (uint32_t)j * (uint32_t)vec_bytes(d.r, 0, g.trunc) : sc;
         };
+        const int bmb = bm_bytes(0, g.trunc);
         int i, j, r;
         const uint8_t *rec = where(tid, i, j, r);
         PVec<RMAX> x;
-        load_pvec<RMAX, 1, false, 4>(x, rec, rec + 16, 32, true);
+        load_pvec<RMAX, 1, false, 4>(x, rec, rec + bmb, 32, true);
         for (int b0 = 0; b0 < nblk; b0 += 256) {
             int in, jn, rn;
             const uint8_t *recn = where(b0 + 256 + tid, in, jn, rn);
             PVec<RMAX> xn;
             __builtin_amdgcn_sched_barrier(0);
-            load_pvec<RMAX, 1, false, 4>(xn, recn, recn + 16, 32, true);
+            load_pvec<RMAX, 1, false, 4>(xn, recn, recn + bmb, 32, true);
             __builtin_amdgcn_sched_barrier(0);
+            if (g.trunc < D) mask_words(x.bw, g.trunc);       // a truncated bitmap's bytes past T bits are values
             const uint32_t qoff = (g.rotated && ((s0 + i) * SEG) / g.W != w0) ? D * GP * 4 : 0;
             float acc[GP];
 #pragma unroll
@@ -998,8 +1007,8 @@ __device__ __forceinline__ void load_tok(PVec<RMAX> &x, const uint8_t *tokg, con
 
 // the same for a record with E4M3 values: r bytes of values.  RL > 0: the
 // first RL / 2 16-byte granules (8 RL codes, as many values as RL granules
-// of 16-bit values), the records being 16-byte aligned; else dword loads of
-// every word below rmax, the others from the start of the values again.
+// of 16-bit values), at any 4-byte aligned record; else dword loads of every
+// word below rmax, the others from the start of the values again.
 template <int RMAX, int RL>
 __device__ __forceinline__ void load_tok(PVec8<RMAX> &x, const uint8_t *tokg, const TokLoc &L, bool V_, int rmax, int T) {
     static_assert(RL % 2 == 0 && RL <= RMAX / 8, "whole 16-byte granules of codes");
@@ -1007,12 +1016,12 @@ __device__ __forceinline__ void load_tok(PVec8<RMAX> &x, const uint8_t *tokg, co
     const uint8_t *b = tokg + L.base + (V_ ? (uint32_t)(B * (bmb + r)) : 0u);
     const uint8_t *bm = b + j * bmb, *val = b + B * bmb + j * r;
     if constexpr (RL > 0) {
-        const uint4 bb = *(const uint4 *)bm;
+        const u32x4a4 bb = *(const u32x4a4 *)bm;
         x.bw[0] = bb.x; x.bw[1] = bb.y; x.bw[2] = bb.z; x.bw[3] = bb.w;
-        const uint4 *v4 = (const uint4 *)val;
+        const u32x4a4 *v4 = (const u32x4a4 *)val;
 #pragma unroll
         for (int k = 0; k < RL / 2; ++k) {
-            const uint4 t = v4[k];
+            const u32x4a4 t = v4[k];
             x.v[4 * k] = t.x; x.v[4 * k + 1] = t.y; x.v[4 * k + 2] = t.z; x.v[4 * k + 3] = t.w;
         }
     } else {
@@ -1153,7 +1162,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     // (16, then 8, then 4; ascending index inside a size), so every block
     // starts at a multiple of its size and none straddles a 64-token chunk
     const int nbk = e1 - e0;
-    bool all16;                                     // every record of the split 16-byte aligned
+    bool all16;                                     // every record of the split 4-byte aligned (granule loads)
     bool dense = false;                             // every block keeps all D channels (RMAX = D kernels)
     int rsplit;                                     // largest kept count in the split
     {
@@ -1176,10 +1185,11 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         }
         const int rw = wave_max_i(on ? r : 0);
         if (lane == 0) wcnt[wave * 4 + 3] = rw;
-        // one channel per group, r % 8 == 0 (r % 16 == 0 with E4M3 values) and
-        // an aligned block: 16-byte bitmaps and value runs at 16-byte offsets
-        all16 = __syncthreads_and(!on || (l2g == 0 && (r & (F8 ? 15 : 7)) == 0 && (goff & 15u) == 0 && g.trunc == D));
-        if (RMAX >= D && !F8) dense = __syncthreads_and(!on || (l2g == 0 && r == D));
+        // granule loads take a fixed 16-byte bitmap and whole 16-byte runs of
+        // values at any 4-byte aligned record (what lies past a record is read
+        // inside the arena's slack and never used; a walk reads D / g bits)
+        all16 = __syncthreads_and(!on || (goff & 3u) == 0);
+        if (RMAX >= D && !F8) dense = __syncthreads_and(!on || (l2g == 0 && r == D && (goff & 15u) == 0));
         if (on) {
             const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
             const int c16 = wcnt[0] + wcnt[4], c8 = wcnt[1] + wcnt[5];
