@@ -55,3 +55,47 @@ def rotations(x: np.ndarray, L: int, W: int, nw: int):
         else:
             R[w], ev[w] = last
     return R, ev
+
+
+# ---- selection-pattern channel reorder (Sec. 5.5) --------------------------
+# Reading R-21 (the paper names the goal, not the procedure): channels are
+# ordered by how often each is selected, i.e. among the r largest |y| of a
+# token's rotated vector (lowest channel first on ties), over the window's
+# tokens, most often first, lower current row first on equal counts; rows of R
+# follow.  Channels selected alike become neighbours and the least selected
+# come last, where a truncation of the bitmap drops them.  y is the
+# compressor's fp32 chain (oracle.rotate); x holds the 16-bit inputs as fp32.
+def selection_counts(x, R, r):
+    """x [n][D] fp32 (exact 16-bit values), R [D][D] fp32 -> counts [D] int64."""
+    from oracle import oracle as O
+    x = np.asarray(x, dtype=np.float32).reshape(-1, D)
+    counts = np.zeros(D, dtype=np.int64)
+    if x.shape[0] == 0:
+        return counts
+    y = O.rotate(x, np.asarray(R, dtype=np.float32))
+    order = np.argsort(-np.abs(y), axis=1, kind="stable")   # equal magnitudes keep ascending channels
+    np.add.at(counts, order[:, :r].ravel(), 1)
+    return counts
+
+
+def reorder_order(counts):
+    """New row order: descending count, ascending row on ties."""
+    return np.argsort(-np.asarray(counts), kind="stable")
+
+
+def reorder_rotations(x, L, W, R, r):
+    """Rotations of one (sequence, kv head) reordered window by window: x [>= L][D]
+    fp32, R [nw][D][D] fp32 -> (R' [nw][D][D], orders [nw][D]).  A window without
+    tokens takes the order of the last window with tokens (identity before any)."""
+    R = np.asarray(R, dtype=np.float32)
+    nw = R.shape[0]
+    out = np.empty_like(R)
+    orders = np.empty((nw, D), dtype=np.int64)
+    last = np.arange(D)
+    for w in range(nw):
+        a, b = w * W, min((w + 1) * W, L)
+        if a < b:
+            last = reorder_order(selection_counts(x[a:b], R[w], r))
+        orders[w] = last
+        out[w] = R[w][last]
+    return out, orders
