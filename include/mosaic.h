@@ -228,6 +228,30 @@ mosaic_status mosaic_compute_rotations(const mosaic_params *params, int32_t num_
                                        const int32_t *ctx_lens_host, float *rot_k, float *rot_v, float *evals_k,
                                        float *evals_v, void *ws, size_t ws_bytes, void *stream);
 
+/* Selection-pattern channel reorder (Sec. 5.5: the rotated channels are reordered
+ * so that channels with similar selection patterns become neighbours; reading R-21
+ * of the library's design notes gives the procedure).  For every rotation window of
+ * every (sequence, kv head), K and V apart, counts how many of the window's tokens
+ * keep each rotated channel among their default_keep largest magnitudes (y = x . R^T
+ * by the compressor's own fp32 chain, lowest channel first on ties), then permutes
+ * the rows of that window's R in place: most selected first, lower row first on
+ * equal counts.  A window without tokens takes the order of the last window with
+ * tokens; the windows of a sequence without tokens are left alone.  Eigenvalues
+ * returned by mosaic_compute_rotations keep the old row order.
+ *   k, v, seq_stride, ctx_lens_host, rot_k, rot_v: as mosaic_compute_rotations
+ *                   (rot_k / rot_v are read and rewritten in place)
+ *   ws            : at least mosaic_reorder_workspace_bytes bytes, 256-byte aligned
+ *                   (context lengths, counts, transposed copies of R)
+ * Errors: INVALID (NULL, misaligned, bad shape, small workspace, default_keep out
+ * of 1..128), CAPACITY (a context longer than max_tokens), UNSUPPORTED
+ * (head_dim != 128). */
+mosaic_status mosaic_reorder_workspace_bytes(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
+                                             size_t *bytes);
+mosaic_status mosaic_reorder_rotations(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
+                                       const void *k, const void *v, int64_t seq_stride,
+                                       const int32_t *ctx_lens_host, float *rot_k, float *rot_v, void *ws,
+                                       size_t ws_bytes, void *stream);
+
 /* Uncompressed baseline: dense split-K decode attention over K/V laid out as
  * for mosaic_compress (the "Full" baseline of Sec. 6.1).
  *   ctx_lens: DEVICE int32 [num_seqs].  ws: mosaic_dense_workspace_bytes. */

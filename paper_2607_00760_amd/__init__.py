@@ -263,3 +263,31 @@ def compute_rotations(params: Params, k, v, ctx_lens, max_tokens: int, evals: bo
                                            _ptr(rv), _ptr(ek) if evals else None, _ptr(ev) if evals else None,
                                            _ptr(ws), ws.numel(), _stream(k.device)))
     return (rk, rv, ek, ev) if evals else (rk, rv)
+
+
+def reorder_rotations(params: Params, k, v, ctx_lens, max_tokens: int, rot_k, rot_v, ws=None):
+    """Selection-pattern reorder of the rows of rot_k / rot_v in place (the
+    layout compute_rotations returns), counted over the tokens of k, v
+    [S][Hkv][seq_stride][128] on the GPU with params.default[0] kept channels."""
+    import torch
+    lib = load()
+    S, Hkv, stride, _ = k.shape
+    _check_tensor(k, "k", None, None)
+    _check_tensor(v, "v", k.dtype, k.device)
+    nw = -(-max_tokens // params.rot_window)
+    for t, name in ((rot_k, "rot_k"), (rot_v, "rot_v")):
+        _check_tensor(t, name, torch.float32, k.device)
+        if tuple(t.shape) != (S, Hkv, nw, D, D):
+            raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {(S, Hkv, nw, D, D)}")
+    p = params.to_c()
+    p.num_kv_heads = Hkv
+    p.dtype = 1 if k.dtype == torch.bfloat16 else 0
+    n = C.c_size_t()
+    check(lib.mosaic_reorder_workspace_bytes(C.byref(p), S, max_tokens, C.byref(n)))
+    if ws is None or ws.numel() < n.value:
+        ws = torch.empty(n.value, dtype=torch.uint8, device=k.device)
+    lens = (C.c_int32 * S)(*[int(x) for x in ctx_lens])
+    with torch.cuda.device(k.device):
+        check(lib.mosaic_reorder_rotations(C.byref(p), S, max_tokens, _ptr(k), _ptr(v), stride, lens, _ptr(rot_k),
+                                           _ptr(rot_v), _ptr(ws), ws.numel(), _stream(k.device)))
+    return rot_k, rot_v

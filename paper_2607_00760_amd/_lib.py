@@ -17,6 +17,7 @@ EXPORTED = [
     "mosaic_compress", "mosaic_append", "mosaic_decode_attention", "mosaic_dense_workspace_bytes",
     "mosaic_dense_decode_attention", "mosaic_cache_stats", "mosaic_seq_tokens", "mosaic_last_error",
     "mosaic_set_timing", "mosaic_decode_timing", "mosaic_rotation_workspace_bytes", "mosaic_compute_rotations",
+    "mosaic_reorder_workspace_bytes", "mosaic_reorder_rotations",
 ]
 
 
@@ -88,6 +89,9 @@ def load() -> C.CDLL:
         L.mosaic_rotation_workspace_bytes.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, C.POINTER(sz)]
         L.mosaic_compute_rotations.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, vp, vp, C.c_int64,
                                                C.POINTER(C.c_int32), vp, vp, vp, vp, vp, sz, vp]
+        L.mosaic_reorder_workspace_bytes.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, C.POINTER(sz)]
+        L.mosaic_reorder_rotations.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, vp, vp, C.c_int64,
+                                               C.POINTER(C.c_int32), vp, vp, vp, sz, vp]
         L.mosaic_set_timing.argtypes = [vp, C.c_int32]
         L.mosaic_decode_timing.argtypes = [vp, C.POINTER(C.c_float)]
         L.mosaic_seq_tokens.argtypes = [vp, C.c_int32]

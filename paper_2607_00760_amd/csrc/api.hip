@@ -442,6 +442,50 @@ mosaic_status mosaic_compute_rotations(const mosaic_params *params, int32_t num_
     return ok();
 }
 
+mosaic_status mosaic_reorder_workspace_bytes(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
+                                             size_t *bytes) {
+    int nw = 0;
+    if (!bytes) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    const mosaic_status st = rotation_shape(params, num_seqs, max_tokens, nw);
+    if (st != MOSAIC_OK) return st;
+    *bytes = reorder_ws_bytes(num_seqs, params->num_kv_heads, nw);
+    return ok();
+}
+
+mosaic_status mosaic_reorder_rotations(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
+                                       const void *k, const void *v, int64_t seq_stride,
+                                       const int32_t *ctx_lens_host, float *rot_k, float *rot_v, void *ws,
+                                       size_t ws_bytes, void *stream) {
+    int nw = 0;
+    const mosaic_status st = rotation_shape(params, num_seqs, max_tokens, nw);
+    if (st != MOSAIC_OK) return st;
+    if (!k || !v || !ctx_lens_host || !rot_k || !rot_v || !ws) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    if (params->dtype != MOSAIC_FP16 && params->dtype != MOSAIC_BF16) return fail(MOSAIC_ERR_INVALID, "dtype %d", params->dtype);
+    if (params->default_keep < 1 || params->default_keep > D)
+        return fail(MOSAIC_ERR_INVALID, "default_keep %d: 1..128", params->default_keep);
+    if (((uintptr_t)k | (uintptr_t)v | (uintptr_t)rot_k | (uintptr_t)rot_v) % 16 || (uintptr_t)ws % 256)
+        return fail(MOSAIC_ERR_INVALID, "k, v, rot_k and rot_v must be 16-byte aligned, ws 256-byte aligned");
+    int maxL = 0;
+    for (int s = 0; s < num_seqs; ++s) {
+        const int L = ctx_lens_host[s];
+        if (L < 0) return fail(MOSAIC_ERR_INVALID, "ctx_lens[%d] = %d < 0", s, L);
+        if (L > max_tokens) return fail(MOSAIC_ERR_CAPACITY, "ctx_lens[%d] = %d > max_tokens %d", s, L, max_tokens);
+        maxL = std::max(maxL, L);
+    }
+    if (seq_stride < maxL || seq_stride < 1) return fail(MOSAIC_ERR_INVALID, "seq_stride %lld < longest context %d",
+                                                         (long long)seq_stride, maxL);
+    const size_t need = reorder_ws_bytes(num_seqs, params->num_kv_heads, nw);
+    if (ws_bytes < need) return fail(MOSAIC_ERR_INVALID, "workspace %zu < %zu", ws_bytes, need);
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = hipMemcpyAsync(ws, ctx_lens_host, sizeof(int32_t) * num_seqs, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "copy of context lengths");
+    e = launch_reorder((const uint16_t *)k, (const uint16_t *)v, seq_stride, num_seqs, params->num_kv_heads,
+                       params->dtype, (const int32_t *)ws, params->rot_window, nw, params->default_keep, rot_k, rot_v,
+                       (uint8_t *)ws, s);
+    if (e != hipSuccess) return hip_fail(e, "reorder launch");
+    return ok();
+}
+
 mosaic_status mosaic_cache_stats(const mosaic_cache *c, mosaic_stats *out, void *stream) {
     if (!c || !out) return fail(MOSAIC_ERR_INVALID, "NULL argument");
     if (!c->arena || !c->compressed) return fail(MOSAIC_ERR_STATE, "stats before compress");

@@ -619,6 +619,95 @@ __global__ void __launch_bounds__(MT_THREADS) k_fin_pack(Geom g) {
     maint_pack(g, p, seg, tb, SEG, true, r, log2g, log2b, off[0], off[1], (int)off[2], sm, yk, yv);
 }
 
+// ------------------------------------------------------------------ channel reorder
+// Selection-pattern reorder of the rotation rows (Sec. 5.5, reading R-21).
+constexpr int SEL_SLICE = 4096;    // tokens per counting workgroup
+
+// R^T of every window of every pair, K and V (matrix (2 pair + which) nw + w),
+// for the compressor's rotation loop
+__global__ void k_sel_transpose(const float *rk, const float *rv, int npairs, int nw, float *rt) {
+    const int m = blockIdx.x, pw = m >> 1, which = m & 1;      // m = 2 pair + which
+    const int w = blockIdx.y;
+    const float *R = (which ? rv : rk) + ((uint64_t)pw * nw + w) * D * D;
+    float *dst = rt + ((uint64_t)m * nw + w) * D * D;
+    for (int i = threadIdx.x; i < D * D; i += blockDim.x) {
+        const int j = i / D, c = i % D;
+        dst[c * D + j] = R[i];
+    }
+}
+
+__global__ void k_sel_zero(uint32_t *counts, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) counts[i] = 0u;
+}
+
+// grid (slices, windows, 2 pairs): every token of the slice rotated with the
+// window's R (the compressor's chain) and ranked; each channel counts the
+// tokens whose r largest magnitudes hold it (integer adds: exact in any order)
+__global__ void __launch_bounds__(256) k_sel_count(const uint16_t *k, const uint16_t *v, int64_t seq_stride, int hkv,
+                                                   int dtype, const int32_t *ctx, int W, int nw, int r,
+                                                   const float *rt, uint32_t *counts) {
+    constexpr int TPW = 16, NWV = 4;
+    __shared__ SegSmem<NWV> sm;
+    const int sl = blockIdx.x, w = blockIdx.y, m = blockIdx.z, pair = m >> 1, which = m & 1;
+    const int L = ctx[pair / hkv];
+    const int64_t a = (int64_t)w * W + (int64_t)sl * SEL_SLICE;
+    const int64_t e = min(min((int64_t)(w + 1) * W, (int64_t)L), a + SEL_SLICE);
+    if (a >= e) return;
+    const uint16_t *src = (which ? v : k) + ((uint64_t)pair * seq_stride + (uint64_t)a) * D;
+    const float *rtw = rt + ((uint64_t)m * nw + w) * D * D;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t clo = 0, chi = 0;
+    for (int64_t t0 = 0; t0 < e - a; t0 += SEG) {
+        const int ntok = (int)min((int64_t)SEG, e - a - t0);
+        float y[TPW][2];
+        rotate_tile(src + (uint64_t)t0 * D, ntok, rtw, dtype, sm, y);
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) {
+            if (wave * TPW + i < ntok) {                     // wave-uniform
+                int rlo, rhi;
+                group_ranks(y[i][0], y[i][1], 0, D, sm.keys[wave], rlo, rhi);
+                clo += rlo < r ? 1u : 0u;
+                chi += rhi < r ? 1u : 0u;
+            }
+        }
+    }
+    uint32_t *cnt = counts + ((uint64_t)m * nw + w) * D;
+    atomicAdd(&cnt[lane], clo);
+    atomicAdd(&cnt[lane + 64], chi);
+}
+
+// grid (windows, 2 pairs), 1024 threads: rows of R by descending count
+// (lower row first on ties), in place; a window without tokens takes the
+// order of the last window with tokens, and a pair with no tokens keeps R
+__global__ void __launch_bounds__(1024) k_sel_permute(float *rk, float *rv, int hkv, const int32_t *ctx, int W, int nw,
+                                                      const uint32_t *counts) {
+    __shared__ uint32_t cnt[D];
+    __shared__ int pos[D];
+    const int w = blockIdx.x, m = blockIdx.y, pair = m >> 1, which = m & 1, tid = threadIdx.x;
+    const int L = ctx[pair / hkv];
+    const int nwt = min(nw, (L + W - 1) / W);                 // windows with tokens
+    if (nwt == 0) return;
+    const int ws = min(w, nwt - 1);
+    if (tid < D) cnt[tid] = counts[((uint64_t)m * nw + ws) * D + tid];
+    __syncthreads();
+    if (tid < D) {
+        const uint32_t mine = cnt[tid];
+        int rank = 0;
+        for (int c = 0; c < D; ++c) rank += (cnt[c] > mine || (cnt[c] == mine && c < tid)) ? 1 : 0;
+        pos[tid] = rank;
+    }
+    __syncthreads();
+    float *R = (which ? rv : rk) + ((uint64_t)pair * nw + w) * D * D;
+    const int row = tid >> 3, part = (tid & 7) * 16;        // 128 rows x 8 parts of 16 values
+    float4 t[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) t[i] = *(const float4 *)(R + row * D + part + 4 * i);
+    __syncthreads();                                         // every row read before any is written
+#pragma unroll
+    for (int i = 0; i < 4; ++i) *(float4 *)(R + pos[row] * D + part + 4 * i) = t[i];
+}
+
 }  // namespace
 
 hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, hipStream_t s) {
@@ -651,6 +740,31 @@ hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, 
         if ((e = launch_maintain(g, MAINT_AFTER_PREFILL, MAINT_FLUSH, s)) != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+size_t reorder_ws_bytes(int num_seqs, int hkv, int nw) {
+    const size_t m = (size_t)num_seqs * hkv * 2 * nw;
+    return ((size_t)num_seqs * sizeof(int32_t) + 255) / 256 * 256 + (m * D * sizeof(uint32_t) + 255) / 256 * 256
+           + m * D * D * sizeof(float);
+}
+
+hipError_t launch_reorder(const uint16_t *k, const uint16_t *v, int64_t seq_stride, int num_seqs, int hkv, int dtype,
+                          const int32_t *ctx_dev, int W, int nw, int r, float *rot_k, float *rot_v, uint8_t *ws,
+                          hipStream_t s) {
+    const int npairs = num_seqs * hkv, m = npairs * 2;
+    uint32_t *counts = (uint32_t *)(ws + ((size_t)num_seqs * sizeof(int32_t) + 255) / 256 * 256);
+    float *rt = (float *)((uint8_t *)counts + ((size_t)m * nw * D * sizeof(uint32_t) + 255) / 256 * 256);
+    const int ncnt = m * nw * D;
+    hipLaunchKernelGGL(k_sel_zero, dim3(ceil_div(ncnt, 256)), dim3(256), 0, s, counts, ncnt);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_sel_transpose, dim3(m, nw), dim3(256), 0, s, rot_k, rot_v, npairs, nw, rt);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_sel_count, dim3(ceil_div(W, SEL_SLICE), nw, m), dim3(256), 0, s, k, v, seq_stride, hkv, dtype,
+                       ctx_dev, W, nw, r, rt, counts);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_sel_permute, dim3(nw, m), dim3(1024), 0, s, rot_k, rot_v, hkv, ctx_dev, W, nw, counts);
+    return hipGetLastError();
 }
 
 hipError_t launch_append(const Geom &g, const uint16_t *k, const uint16_t *v, hipStream_t s) {

@@ -140,3 +140,41 @@ def test_rotations_feed_compress():
             tol = 1e-5 * ay.max()
             assert np.all(ay[ch] >= thr - tol) and np.all(ay[~bm] <= thr + tol), \
                 f"pair {pi} token {t}: kept channels are not the r largest"
+
+
+@pytest.mark.parametrize("name,keep", [("c2_fp16", 32), ("c3_bf16_r16", 16)])
+def test_reorder_matches_oracle(name, keep):
+    """mosaic_reorder_rotations against the oracle's selection-pattern reorder
+    on the same fp32 matrices (the oracle's eigenbases): the reordered
+    matrices are identical bit for bit (the counts are integers over the
+    compressor's exact fp32 chain), including windows without tokens and an
+    empty sequence."""
+    spec = (gen.spec("c2", ctx=(1500, 700, 0), hkv=2, rot_window=1024) if name == "c2_fp16"
+            else gen.spec("c3", ctx=(2100, 64), hkv=2, kind="gauss", rot_window=1024))
+    print(f"[reorder] {name} ctx={spec.ctx} r={keep}", flush=True)
+    cap = spec.max_ctx + 1024                                 # one window past the longest context
+    lay = gen.make_layer(spec, 0, capacity=cap)
+    W, nw = spec.rot_window, -(-cap // spec.rot_window)
+    R = {}
+    for which in ("k", "v"):
+        R[which] = np.zeros((spec.num_seqs, spec.hkv, nw, D, D), np.float32)
+        for b in range(spec.num_seqs):
+            for h in range(spec.hkv):
+                R[which][b, h] = RO.rotations(lay[which][b, h].double().numpy(), spec.ctx[b], W, nw)[0]
+    params = M.Params(num_kv_heads=spec.hkv, group_size=spec.group, dtype=spec.dtype, rot_window=W,
+                      default=(keep, 1, 8))
+    rk, rv = torch.from_numpy(R["k"]).cuda(), torch.from_numpy(R["v"]).cuda()
+    M.reorder_rotations(params, lay["k"].cuda(), lay["v"].cuda(), spec.ctx, cap, rk, rv)
+    torch.cuda.synchronize()
+    got = {"k": rk.cpu().numpy(), "v": rv.cpu().numpy()}
+    moved = 0
+    for b in range(spec.num_seqs):
+        L = spec.ctx[b]
+        for h in range(spec.hkv):
+            for which in ("k", "v"):
+                x = lay[which][b, h].float().numpy()
+                want, orders = RO.reorder_rotations(x, L, W, R[which][b, h], keep)
+                assert np.array_equal(got[which][b, h], want), f"{name} seq {b} head {h} {which}"
+                moved += int((orders != np.arange(D)).any(axis=1).sum())
+    print(f"[reorder] {name}: {moved} windows reordered", flush=True)
+    assert moved > 0
