@@ -248,6 +248,7 @@ def main():
     # the rotation matrices computed on the GPU from the same K/V (covariance
     # and Jacobi eigensolver; the cache above used the host's rotations)
     rotations_ms = None
+    reorder = None
     if spec.rotate and not args.no_rotations:
         rws = torch.empty(0, dtype=torch.uint8, device=dev)
         rk_g, rv_g = M.compute_rotations(params, lay["k"], lay["v"], lay["ctx_lens"], cap)
@@ -260,8 +261,28 @@ def main():
         e1.record()
         torch.cuda.synchronize()
         rotations_ms = e0.elapsed_time(e1)
-        del rk_g, rv_g, rws
         log(f"rotations on the GPU {rotations_ms:.2f} ms")
+        # the selection-pattern reorder of those matrices, and the memory ratio of
+        # the cache compressed with them before and after it
+        def ratio_with(rk_, rv_):
+            c2 = M.MosaicCache(params, spec.num_seqs, cap, rotated=True, device=dev)
+            c2.compress(lay["k"], lay["v"], lay["ctx_lens"], rk_, rv_)
+            r_ = c2.stats()["ratio"]
+            del c2
+            return r_
+        ratio_gpu_rot = ratio_with(rk_g, rv_g)
+        M.load().mosaic_reorder_workspace_bytes(C.byref(params.to_c()), spec.num_seqs, cap, C.byref(n))
+        ows = torch.empty(n.value, dtype=torch.uint8, device=dev)
+        M.reorder_rotations(params, lay["k"], lay["v"], lay["ctx_lens"], cap, rk_g, rv_g, ws=ows)
+        torch.cuda.synchronize()
+        e0.record()
+        M.reorder_rotations(params, lay["k"], lay["v"], lay["ctx_lens"], cap, rk_g, rv_g, ws=ows)   # same work again
+        e1.record()
+        torch.cuda.synchronize()
+        reorder = {"reorder_ms": round(e0.elapsed_time(e1), 3), "ratio_gpu_rotations": round(ratio_gpu_rot, 4),
+                   "ratio_gpu_rotations_reordered": round(ratio_with(rk_g, rv_g), 4)}
+        del rk_g, rv_g, rws, ows
+        log(f"reorder {reorder}")
 
     update_path = None
     overlap = None
@@ -495,6 +516,7 @@ def main():
         "wall_ms_per_step_incl_flush": round(1e3 * wall / args.steps, 3),
         "compress_ms": round(compress_ms, 3), "memory_ratio": round(stats["ratio"], 4),
         "rotations_ms": None if rotations_ms is None else round(rotations_ms, 3),
+        "channel_reorder": reorder,
         "update_path": update_path, "encoding_overlap": overlap,
         "strategies": {f"{k[0]}/{k[1]}/{k[2]}": v for k, v in sorted(stats["strategies"].items())},
         "cpu_baseline": cpu, "parity": parity, "datagen_s": round(t_gen, 1), "source_hash": source_hash(),

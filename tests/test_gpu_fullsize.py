@@ -279,3 +279,29 @@ def test_c3_gpu_rotations_full_size_sampled():
             assert np.abs(eg - eo).max() <= 5e-5 * lam, f"{which} {b} {h} {w}: eigenvalues"
             top = np.argmax(np.abs(Rg), axis=1)
             assert np.all(Rg[np.arange(D), top] > 0), f"{which} {b} {h} {w}: sign rule"
+
+
+def test_c3_reorder_full_size_sampled():
+    """Selection-pattern reorder of the c3 workload's own rotation matrices
+    (64 pairs x 2 windows of 65536 tokens, K and V) in one library call:
+    sampled windows identical to the oracle's reorder of the same matrices."""
+    import paper_2607_00760_amd as M
+    from oracle import rotation as RO
+    spec = gen.spec("c3")
+    print(f"[fullsize] c3 reorder {spec.num_seqs}x{spec.max_ctx}", flush=True)
+    cap = spec.capacity
+    lay = gen.make_layer(spec, 0, device="cuda", capacity=cap)
+    lp, _ = params_pair(spec)
+    rk, rv = lay["rot_k"].clone().contiguous(), lay["rot_v"].clone().contiguous()
+    M.reorder_rotations(lp, lay["k"], lay["v"], spec.ctx, cap, rk, rv)
+    torch.cuda.synchronize()
+    nw = rk.shape[2]
+    rng = np.random.default_rng(10)
+    for _ in range(2):
+        b, h, w = int(rng.integers(spec.num_seqs)), int(rng.integers(spec.hkv)), int(rng.integers(nw))
+        for which, R in (("k", rk), ("v", rv)):
+            a, e = w * spec.rot_window, min((w + 1) * spec.rot_window, spec.ctx[b])
+            R0 = lay["rot_" + which][b, h, w].cpu().numpy()
+            x = lay[which][b, h, a:e].float().cpu().numpy()
+            order = RO.reorder_order(RO.selection_counts(x, R0, lp.default[0]))
+            assert np.array_equal(R[b, h, w].cpu().numpy(), R0[order]), f"{which} seq {b} head {h} window {w}"
