@@ -228,9 +228,9 @@ mosaic_status mosaic_compute_rotations(const mosaic_params *params, int32_t num_
                                        const int32_t *ctx_lens_host, float *rot_k, float *rot_v, float *evals_k,
                                        float *evals_v, void *ws, size_t ws_bytes, void *stream);
 
-/* Selection-pattern channel reorder (Sec. 5.5: the rotated channels are reordered
- * so that channels with similar selection patterns become neighbours; reading R-21
- * of the library's design notes gives the procedure).  For every rotation window of
+/* Selection-pattern channel reorder (Sec. 5.5 asks for the rotated channels to be
+ * reordered so that channels selected alike become neighbours, without fixing a
+ * procedure; this is the one taken here).  For every rotation window of
  * every (sequence, kv head), K and V apart, counts how many of the window's tokens
  * keep each rotated channel among their default_keep largest magnitudes (y = x . R^T
  * by the compressor's own fp32 chain, lowest channel first on ties), then permutes

@@ -620,7 +620,10 @@ __global__ void __launch_bounds__(MT_THREADS) k_fin_pack(Geom g) {
 }
 
 // ------------------------------------------------------------------ channel reorder
-// Selection-pattern reorder of the rotation rows (Sec. 5.5, reading R-21).
+// Selection-pattern reorder of the rotation rows (Sec. 5.5 asks for channels
+// selected alike to become neighbours): the rows of a window's R run by
+// descending count of the window's tokens that keep the channel among their
+// default_keep largest magnitudes, lower row first on equal counts.
 constexpr int SEL_SLICE = 4096;    // tokens per counting workgroup
 
 // R^T of every window of every pair, K and V (matrix (2 pair + which) nw + w),
