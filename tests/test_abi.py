@@ -145,3 +145,31 @@ def test_package_has_no_fallback(monkeypatch, tmp_path):
     monkeypatch.setattr(_lib, "_lib", None)
     with pytest.raises(ImportError):
         _lib.load()
+
+
+def test_rotation_and_reorder_argument_checks():
+    """The rotation and reorder entry points validate everything before any
+    HIP call (workspace sizes, NULL and misaligned pointers, lengths)."""
+    L = _lib.load()
+    p = M.Params(num_kv_heads=2, rot_window=1024).to_c()
+    n_rot, n_reo = C.c_size_t(), C.c_size_t()
+    assert L.mosaic_rotation_workspace_bytes(C.byref(p), 3, 2500, C.byref(n_rot)) == 0
+    assert L.mosaic_reorder_workspace_bytes(C.byref(p), 3, 2500, C.byref(n_reo)) == 0
+    nw = 3                                                    # ceil(2500 / 1024)
+    assert n_reo.value >= 3 * 2 * 2 * nw * 128 * 4 + 3 * 2 * 2 * nw * 128 * 128 * 4
+    assert L.mosaic_reorder_workspace_bytes(C.byref(p), 0, 2500, C.byref(n_reo)) == -1
+    lens = (C.c_int32 * 3)(2500, 10, 0)
+    fake, ws = C.c_void_p(0x100000), C.c_void_p(0x200000)
+    big_ws = 1 << 40
+    args = lambda **kw: [C.byref(p), 3, 2500, kw.get("k", fake), fake, kw.get("stride", 2500), kw.get("lens", lens),
+                         kw.get("rk", fake), fake, kw.get("ws", ws), kw.get("ws_bytes", big_ws), None]
+    assert L.mosaic_reorder_rotations(*args(k=None)) == -1
+    assert L.mosaic_reorder_rotations(*args(rk=C.c_void_p(0x100004))) == -1                 # misaligned R
+    assert L.mosaic_reorder_rotations(*args(ws=C.c_void_p(0x200010))) == -1                 # ws not 256-aligned
+    assert L.mosaic_reorder_rotations(*args(ws_bytes=16)) == -1                              # small workspace
+    assert L.mosaic_reorder_rotations(*args(stride=100)) == -1                               # stride < length
+    assert L.mosaic_reorder_rotations(*args(lens=(C.c_int32 * 3)(2501, 0, 0))) == -3         # past max_tokens
+    assert L.mosaic_reorder_rotations(*args(lens=(C.c_int32 * 3)(-1, 0, 0))) == -1
+    p.default_keep = 0
+    assert L.mosaic_reorder_rotations(*args()) == -1
+    assert "default_keep" in L.mosaic_last_error().decode()
