@@ -48,6 +48,9 @@ CASES = {
     "fp8_keep_all": (gen.spec("c1", ctx=(333, 200), hkv=2), dict(fp8=True, force_default=True,
                                                               default=(128, 1, 4), select=(1, 1))),
     "fp8_truncated_96": (gen.spec("c1", ctx=(2000, 900), hkv=2), dict(fp8=True, trunc=96)),
+    # rotations reordered by selection pattern (the oracle's reorder of the
+    # workload's matrices), with 96-channel bitmaps: the use the reorder serves
+    "reordered_truncated_96": (gen.spec("c2", ctx=(2500, 900), hkv=2, rot_window=1024), dict(trunc=96)),
 }
 
 
@@ -56,6 +59,16 @@ def _case(name):
     cap = spec.max_ctx + 130
     lay = gen.make_layer(spec, 0, capacity=cap)
     lp, op = params_pair(spec, **extra)
+    if name.startswith("reordered"):
+        from oracle import rotation as RO
+        for which in ("k", "v"):
+            R = lay["rot_" + which].clone()
+            for b in range(spec.num_seqs):
+                for h in range(spec.hkv):
+                    x = lay[which][b, h].float().numpy()
+                    R[b, h] = torch.from_numpy(RO.reorder_rotations(x, spec.ctx[b], spec.rot_window,
+                                                                    R[b, h].numpy(), lp.default[0])[0])
+            lay["rot_" + which] = R
     return spec, lay, lp, op, cap
 
 
