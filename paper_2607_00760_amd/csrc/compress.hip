@@ -23,9 +23,10 @@ namespace {
 
 constexpr int NCAND = 9;
 
-// NWV waves of SEG / NWV tokens each: 4 x 16 for the prefill (throughput),
-// 16 x 4 for the flush and finalize of the append path (latency: a quarter of
-// the serial work per wave and four waves per SIMD to hide it)
+// shared memory of a workgroup of NWV waves: 4 waves x 16 tokens for the
+// prefill and the reorder's counting (throughput), 8 waves x 2 tokens for the
+// flush and finalize of the append path (latency: short serial work per wave,
+// several waves per SIMD to hide it)
 template <int NWV>
 struct SegSmem {
     float x[SEG * D];              // the segment's input tokens, fp32; then the rotated keys
