@@ -51,6 +51,9 @@ CASES = {
     # rotations reordered by selection pattern (the oracle's reorder of the
     # workload's matrices), with 96-channel bitmaps: the use the reorder serves
     "reordered_truncated_96": (gen.spec("c2", ctx=(2500, 900), hkv=2, rot_window=1024), dict(trunc=96)),
+    # E4M3 values over a wide range: tokens scaled by 2^-14 .. 2^9, so kept
+    # values fall below 2^-6 (subnormal codes, zeros) and above 448 (saturation)
+    "fp8_wide_range": (gen.spec("c3", ctx=(1500, 700), hkv=2, kind="gauss"), dict(fp8=True)),
 }
 
 
@@ -59,6 +62,11 @@ def _case(name):
     cap = spec.max_ctx + 130
     lay = gen.make_layer(spec, 0, capacity=cap)
     lp, op = params_pair(spec, **extra)
+    if name == "fp8_wide_range":
+        n = lay["k"].shape[2]
+        scale = torch.pow(2.0, (torch.arange(n) % 24 - 14).float())[None, None, :, None]
+        for which in ("k", "v"):
+            lay[which] = (lay[which].float() * scale).to(lay[which].dtype)     # exact: powers of two
     if name.startswith("reordered"):
         from oracle import rotation as RO
         for which in ("k", "v"):
@@ -97,7 +105,8 @@ def test_decode_parity(name):
         gs, gsel, _ = gpu_scores_sel(c, p, nb)
         assert np.array_equal(gs.view(np.uint32), scores[p].view(np.uint32)), f"{name} pair {p}: block scores"
         assert np.array_equal(gsel, sels[p]), f"{name} pair {p}: selected blocks"
-    assert_close(out.cpu().numpy(), want, name)
+    # inputs scaled up to 2^9: the outputs' rounding scales with them
+    assert_close(out.cpu().numpy(), want, name, magnitude=2.0 ** 9 if name == "fp8_wide_range" else 1.0)
 
 
 @pytest.mark.parametrize("name", ["c1", "ragged_bf16_w128", "g7_student", "fp8_search_bf16"])
