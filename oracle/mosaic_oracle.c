@@ -35,14 +35,18 @@
  *
  * Where the paper is silent these readings are taken (labels R-n): loss = relative dropped energy (R-3), group
  * score = L1 of the group's magnitudes (R-2), candidate order rate-first
- * (R-4), block variance relative to total energy (R-5), global top-k per
- * (sequence, kv head) with k = ceil(rho * N_blocks) (R-7), GQA block score =
+ * (R-4), block variance relative to total energy (R-5), a global token
+ * budget per (sequence, kv head): blocks taken in (score desc, index asc)
+ * order while fewer than ceil(rho * scoreable tokens) tokens are taken
+ * (R-7; Sec. 6.1 selects 10 % of tokens), GQA block score =
  * max over the group's query heads (R-8), buffer tokens always attended
  * dense and unrotated (R-9), provisional strategy = previous finalized
  * segment or the default (R-10), prefill remainder handled as appends
  * (R-11), y = x . R^T with row j of R the j-th rotated channel (R-12), a
- * truncated bitmap stored in whole 32-bit words (R-19), FP8 values as OCP
- * E4M3 without a scale factor, block keys kept 16-bit (R-20).
+ * truncated bitmap of exactly T / g bits (R-19), FP8 values as OCP
+ * E4M3 without a scale factor, block keys kept 16-bit (R-20), per-vector and
+ * per-segment energies as pairwise trees over the 128 channels and the 64
+ * tokens (R-22).
  *
  * Exactly-defined orders (so that integer and byte results are unique):
  *  chain(a, b)  : acc = 0; for i ascending: acc = fmaf(a_i, b_i, acc)
@@ -83,7 +87,7 @@ typedef struct {
     int32_t trunc;                   /* channels represented (Sec. 5.2 channel truncation):
                                         channels >= trunc are never kept and have no bitmap
                                         bit; a multiple of 32 up to D (0 means D); the
-                                        bitmap is rounded up to whole 32-bit words */
+                                        bitmap holds exactly trunc / g bits */
     int32_t fp8;                     /* 1: K and V token values stored as OCP FP8 E4M3
                                         (Sec. 7, quantizing the compressed elements);
                                         block keys keep the 16-bit dtype (reading R-20) */
@@ -282,15 +286,16 @@ static void keep_channels(const float *y, int r, int g, int T, uint8_t *kch) {
 static int trunc_of(const orc_params *P) { return (P->trunc > 0 && P->trunc < D) ? P->trunc : D; }
 /* bytes per kept value of the K and V token records */
 static int tok_eb(const orc_params *P) { return P->fp8 ? 1 : 2; }
-/* a bitmap of T / g bits is stored in whole little-endian 32-bit words (reading R-19) */
-int orc_bitmap_bytes_t(int g, int T) { return ((T / g + 31) / 32) * 4; }
+/* a bitmap of exactly T / g bits (reading R-19): T is a multiple of 32 and g
+   divides 4, so T / g is a whole number of bytes */
+int orc_bitmap_bytes_t(int g, int T) { return T / g / 8; }
 int orc_vec_bytes_t(int r, int g, int elem_bytes, int T) { return r * elem_bytes + orc_bitmap_bytes_t(g, T); }
 int orc_bitmap_bytes(int g) { return orc_bitmap_bytes_t(g, D); }
 int orc_vec_bytes(int r, int g, int elem_bytes) { return orc_vec_bytes_t(r, g, elem_bytes, D); }
 
 /* T / g bits, bit i = group i kept, least significant bit first in each
-   byte (the little-endian word layout), padded with zero bits to whole
-   32-bit words */
+   byte (bit i is bit i % 32 of little-endian 32-bit word i / 32 wherever
+   whole words exist) */
 static void pack_bitmap(const uint8_t *kch, int g, int T, uint8_t *out) {
     int nbytes = orc_bitmap_bytes_t(g, T);
     for (int i = 0; i < nbytes; ++i) {
@@ -331,7 +336,12 @@ static int ilog2(int v) { int l = 0; while ((1 << l) < v) ++l; return l; }
 /* ------------------------------------------------------------------ */
 /* Strategy selection (Sec. 4.3, Sec. 5.5; readings R-3..R-6).         */
 /* ------------------------------------------------------------------ */
-/* yk, yv: [n][D] rotated vectors of one segment (n == S == 64). */
+/* yk, yv: [n][D] rotated vectors of one segment (n == S == 64).
+   Energies (reading R-22): a vector's energy and its dropped energy are the
+   pairwise tree over its 128 channels of y_c^2 (dropped channels only for
+   the latter), and a segment's are the pairwise tree over its 64 tokens;
+   the candidate (r, g) must pass for K and for V (R-3, R-4), the block size
+   looks at the rotated keys only (R-5). */
 void orc_choose_strategy(const orc_params *P, const float *yk, const float *yv, int n,
                          int *r_out, int *g_out, int *b_out) {
     if (P->force_default) { *r_out = P->def_keep; *g_out = P->def_group; *b_out = P->def_block; return; }
@@ -636,6 +646,35 @@ int orc_select_count(int nblk, int num, int den) {
     return (int)k;
 }
 
+/* Token budget of the selection (reading R-7 of Sec. 4.2 stage 2 and Sec.
+   6.1, which selects 10 % of tokens): ceil(rho * ntok) tokens, rho = num /
+   den, in integers; at least one token when any is scoreable. */
+int orc_select_budget(int ntok, int num, int den) { return orc_select_count(ntok, num, den); }
+
+/* Blocks by (score desc, index asc), taken while the tokens of the blocks
+   already taken are fewer than the budget: the shortest prefix of that order
+   whose tokens reach the budget (the last block may pass it).  sizes[b] is
+   block b's token count.  A library sort is the ordering step.  Returns the
+   number of blocks taken, or -1 on a non-finite score. */
+int orc_select_blocks(const float *s, const int32_t *sizes, int n, int budget, uint8_t *keep) {
+    vi_t *a = (vi_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(vi_t));
+    if (!a) return -2;
+    for (int i = 0; i < n; ++i) {
+        if (!isfinite(s[i])) { free(a); return -1; }
+        a[i].v = s[i]; a[i].i = i; keep[i] = 0;
+    }
+    qsort(a, (size_t)n, sizeof(vi_t), cmp_desc);
+    long long taken = 0;
+    int nsel = 0;
+    for (int j = 0; j < n && taken < budget; ++j) {
+        keep[a[j].i] = 1;
+        taken += sizes[a[j].i];
+        nsel++;
+    }
+    free(a);
+    return nsel;
+}
+
 /* unpack one packed vector into dense fp64 (0 at dropped channels) */
 static void unpack64(const uint8_t *bm, const uint8_t *vals, int g, int T, int dtype, int eb, double *out) {
     int slot = 0;
@@ -662,9 +701,19 @@ int orc_pair_decode(const orc_pair *p, const uint16_t *q, float scale, double *o
     int G = P->group, nb = inf.nblk;
     float *scores = (float *)malloc((size_t)(nb > 0 ? nb : 1) * sizeof(float));
     uint8_t *keep = (uint8_t *)malloc((size_t)(nb > 0 ? nb : 1));
+    int32_t *bsz = (int32_t *)malloc((size_t)(nb > 0 ? nb : 1) * sizeof(int32_t));
     orc_pair_scores(p, q, scores, nb);
-    int k = orc_select_count(nb, P->select_num, P->select_den);
-    if (nb > 0 && orc_topk_mask(scores, nb, k, keep) != 0) { free(scores); free(keep); return -1; }
+    int ntok = 0;                             /* tokens of the scoreable blocks */
+    for (int di = 0, b = 0; di < inf.n_desc; ++di) {
+        const orc_desc *d = &p->desc[di];
+        for (int j = 0; j < desc_ntok(p, d) >> d->log2b; ++j) bsz[b++] = 1 << d->log2b;
+        ntok += desc_ntok(p, d);
+    }
+    int budget = orc_select_budget(ntok, P->select_num, P->select_den);
+    if (nb > 0 && orc_select_blocks(scores, bsz, nb, budget, keep) < 0) {
+        free(scores); free(keep); free(bsz); return -1;
+    }
+    free(bsz);
     int ns = 0;
     for (int b = 0; b < nb; ++b) if (keep[b]) { if (sel && ns < cap) sel[ns] = b; ns++; }
 

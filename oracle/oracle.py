@@ -133,6 +133,8 @@ def lib():
             getattr(L, nm).argtypes = [C.c_void_p]; getattr(L, nm).restype = rt
         L.orc_pair_scores.argtypes = [C.c_void_p, u16p, fp, C.c_int]; L.orc_pair_scores.restype = C.c_int
         L.orc_select_count.argtypes = [C.c_int, C.c_int, C.c_int]; L.orc_select_count.restype = C.c_int
+        L.orc_select_budget.argtypes = [C.c_int, C.c_int, C.c_int]; L.orc_select_budget.restype = C.c_int
+        L.orc_select_blocks.argtypes = [fp, i32p, C.c_int, C.c_int, u8p]; L.orc_select_blocks.restype = C.c_int
         L.orc_pair_decode.argtypes = [C.c_void_p, u16p, C.c_float, f64p, i32p, C.c_int]
         L.orc_pair_decode.restype = C.c_int
         L.orc_dense_attention.argtypes = [u16p, u16p, u16p, C.c_int, C.c_int, C.c_int, C.c_float, f64p]
@@ -246,6 +248,23 @@ def choose_strategy(params: Params, yk, yv):
 
 def select_count(nblk, num, den):
     return lib().orc_select_count(nblk, num, den)
+
+
+def select_budget(ntok, num, den):
+    """Tokens to select: ceil(rho * ntok) in integers, at least 1 (R-7)."""
+    return lib().orc_select_budget(ntok, num, den)
+
+
+def select_blocks(scores, sizes, budget):
+    """Blocks taken in (score desc, index asc) order while fewer than budget
+    tokens are taken (R-7) -> boolean mask."""
+    s = _f32(scores)
+    z = np.ascontiguousarray(sizes, dtype=np.int32)
+    keep = np.zeros(s.size, np.uint8)
+    rc = lib().orc_select_blocks(_p(s, C.c_float), _p(z, C.c_int32), s.size, budget, _p(keep, C.c_uint8))
+    if rc < 0:
+        raise ValueError("non-finite input")
+    return keep.astype(bool)
 
 
 def bytes_per_token(r, g, B, elem_bytes=2, trunc=D):

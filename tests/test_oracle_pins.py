@@ -240,6 +240,39 @@ def test_strategy_limits():
     assert O.choose_strategy(O.Params(tau_channel=0.0, tau_block=0.0), y, y) == (48, 1, 4)
 
 
+def test_strategy_needs_both_k_and_v():
+    """Reading R-4: one (r, g) for the segment, accepted only if K and V both
+    pass.  All-ones vectors drop (128 - r) / 128 of their energy at any group
+    size; one-hot vectors drop nothing."""
+    ones = np.ones((64, D), np.float32)
+    hot = np.zeros((64, D), np.float32)
+    hot[np.arange(64), (np.arange(64) * 5) % D] = 2.0
+    P = O.Params(tau_channel=0.8, tau_block=0.5)
+    assert O.choose_strategy(P, hot, ones)[:2] == (32, 4)     # a K-only rule gives (16, 4)
+    assert O.choose_strategy(P, ones, hot)[:2] == (32, 4)     # a V-only rule gives (16, 4)
+    assert O.choose_strategy(P, hot, hot)[:2] == (16, 4)
+    assert O.choose_strategy(P, ones, ones)[:2] == (32, 4)
+
+
+def test_strategy_rate_first_order():
+    """Reading R-4: the rate first (r = 16 -> 32 -> 48), then g = 4 -> 2 -> 1.
+    Sixteen dominant channels spaced 4 apart fit r = 16 only one per group:
+    (16, 1); a group-size-first order would take (32, 2)."""
+    y = np.full((64, D), 0.01, np.float32)
+    y[:, 0:64:4] = 1.0
+    assert O.choose_strategy(O.Params(tau_channel=0.05, tau_block=0.5), y, y)[:2] == (16, 1)
+
+
+def test_block_size_looks_at_keys_only():
+    """Reading R-5: the block size follows the intra-block variance of the
+    rotated keys; the values do not enter."""
+    ones = np.ones((64, D), np.float32)
+    alt = np.stack([np.ones(D) * (1 if t % 2 == 0 else -1) for t in range(64)]).astype(np.float32)
+    P = O.Params(tau_channel=0.9, tau_block=0.5)
+    assert O.choose_strategy(P, ones, alt)[2] == 16           # constant keys: no variance
+    assert O.choose_strategy(P, alt, ones)[2] == 4            # every block mean 0: ratio 1, fallback
+
+
 def test_block_size_closed_forms():
     base = np.ones(D, np.float32)
     # constant inside each 8-token group, sign flips between groups: B=16 mean is 0
@@ -361,23 +394,74 @@ def test_orthogonal_rotation_close_to_dense():
     assert np.max(np.abs(out - ref)) < 3e-3        # only the fp16 rounding of rotated values
 
 
-def test_selection_is_topk_of_scores():
+def _ahead_tokens(s, sizes, b):
+    """Tokens of the blocks ranked ahead of block b: higher score, or the same
+    score and a lower index."""
+    return sum(int(sizes[j]) for j in range(len(s)) if s[j] > s[b] or (s[j] == s[b] and j < b))
+
+
+def test_select_budget_closed_forms():
+    # Sec. 6.1: 10 % of tokens, ceil in integers, at least one when any is scoreable
+    assert [O.select_budget(n, 1, 10) for n in (0, 1, 10, 11, 64, 131072)] == [0, 1, 1, 2, 7, 13108]
+    assert O.select_budget(100, 1, 16) == 7 and O.select_budget(100, 1, 8) == 13 and O.select_budget(9, 1, 1) == 9
+
+
+def test_select_blocks_pairwise_definition():
+    """Brute force: a block is taken iff the blocks ranked ahead of it hold
+    fewer tokens than the budget (mixed block sizes, tie storms)."""
+    r = rng(42)
+    for n in range(1, 11):
+        for _ in range(12):
+            s = r.integers(0, 4, n).astype(np.float32)
+            sizes = r.choice([4, 8, 16], n)
+            for budget in range(1, int(sizes.sum()) + 2):
+                m = O.select_blocks(s, sizes, budget)
+                assert m.tolist() == [_ahead_tokens(s, sizes, b) < budget for b in range(n)], (s, sizes, budget)
+
+
+def test_select_blocks_uniform_size_is_block_topk():
+    """One block size B: ceil(ceil(rho B n) / B) = ceil(rho n), so the token
+    budget takes the top ceil(rho n) blocks."""
+    r = rng(43)
+    for B in (4, 8, 16):
+        for nb in (1, 5, 10, 11, 64, 1000):
+            s = r.standard_normal(nb).astype(np.float32)
+            s[r.integers(0, nb, nb // 3)] = 0.5
+            m = O.select_blocks(s, np.full(nb, B), O.select_budget(nb * B, 1, 10))
+            assert np.array_equal(m, O.topk_mask(s, O.select_count(nb, 1, 10))), (B, nb)
+
+
+def test_selection_is_token_budget_of_scores():
+    """Decode selects by the token budget over its own block scores: a block is
+    selected iff the blocks ranked ahead of it hold fewer than ceil(rho *
+    scoreable tokens) tokens; here segments of identical tokens take 16-token
+    blocks, the others 8 or 4, so the sizes are mixed."""
     r = rng(14)
     G, L = 4, 64 * 40 + 45
-    P = O.Params(group=G, dtype="bf16", tau_channel=0.3)
+    P = O.Params(group=G, dtype="bf16", tau_channel=0.3, tau_block=0.9)
     Q, _ = np.linalg.qr(r.standard_normal((D, D)))
     R = Q.astype(np.float32)[None]
-    k = to_bits(r.standard_normal((L, D)), "bf16")
+    x = r.standard_normal((L, D))
+    for seg in range(0, 40, 3):
+        x[64 * seg:64 * seg + 64] = x[64 * seg] * 3.0        # zero block variance -> B = 16
+    k = to_bits(x, "bf16")
     v = to_bits(r.standard_normal((L, D)), "bf16")
     q = to_bits(r.standard_normal((G, D)), "bf16")
     pr = O.Pair(P, L, R, R)
     pr.compress(k, v)
     s = pr.scores(q)
     assert s.size == pr.info().nblk
-    kk = O.select_count(s.size, 1, 10)
-    order = np.lexsort((np.arange(s.size), -s.astype(np.float64)))
+    sizes = []
+    for d in pr.descriptors():
+        n = 32 if d["flags"] & 1 else 64
+        sizes += [1 << d["log2b"]] * (n >> d["log2b"])
+    sizes = np.array(sizes)
+    assert len(set(sizes.tolist())) >= 2 and sizes.sum() == L - pr.info().n_buf
+    budget = -(-int(sizes.sum()) // 10)
     _, sel = pr.decode(q, 0.1)
-    assert np.array_equal(sel, np.sort(order[:kk]))
+    want = [b for b in range(s.size) if _ahead_tokens(s, sizes, b) < budget]
+    assert np.array_equal(sel, want)
+    assert budget <= sizes[sel].sum() < budget + 16
 
 
 def test_block_score_closed_form():
@@ -394,6 +478,42 @@ def test_block_score_closed_form():
     means = k.reshape(16, 4, D).mean(axis=1)           # exact (sums of small ints / 4)
     want = (q.astype(np.float64) @ means.T.astype(np.float64)).max(axis=0)
     assert np.array_equal(s.astype(np.float64), want)
+
+
+def test_block_scores_multi_window_closed_form():
+    """Three rotation windows, each its own signed permutation, integer data,
+    every channel kept: q . R_w^T and the block means rotated by R_w cancel
+    exactly, so every block score is max_h q_h . mean(block) whatever the
+    window; a q rotated with another window's R would not cancel."""
+    r = rng(40)
+    G, W, nw = 4, 128, 3
+    L = W * nw
+    Rk = np.zeros((nw, D, D), np.float32)
+    for w in range(nw):
+        Rk[w][np.arange(D), r.permutation(D)] = r.choice([-1.0, 1.0], D)
+    assert not np.array_equal(Rk[0], Rk[1])
+    P = O.Params(group=G, force_default=True, default=(128, 1, 4), select=(1, 1), rot_window=W)
+    k = r.integers(-3, 4, (L, D)).astype(np.float32)
+    q = r.integers(-3, 4, (G, D)).astype(np.float32)
+    pr = O.Pair(P, L, Rk, Rk)
+    pr.compress(to_bits(k, "fp16"), to_bits(k, "fp16"))
+    s = pr.scores(to_bits(q, "fp16"))
+    means = k.reshape(-1, 4, D).mean(axis=1)
+    want = (q.astype(np.float64) @ means.T.astype(np.float64)).max(axis=0)
+    assert s.size == L // 4 and np.array_equal(s.astype(np.float64), want)
+
+
+@pytest.mark.parametrize("dtype", ["fp16", "bf16"])
+def test_dense_attention_matches_numpy(dtype):
+    """The oracle's dense reference against numpy's softmax attention."""
+    r = rng(41)
+    for L, G in ((0, 4), (1, 4), (77, 7), (300, 4), (1000, 8)):
+        q = to_bits(r.standard_normal((G, D)) * 2, dtype)
+        k = to_bits(r.standard_normal((L, D)), dtype)
+        v = to_bits(r.standard_normal((L, D)), dtype)
+        out = O.dense_attention(q, k, v, 0.125, dtype)
+        ref = _numpy_attention(q, k, v, 0.125, dtype)
+        assert np.max(np.abs(out - ref)) < 1e-12, (L, G)
 
 
 # ---------------------------------------------------------------- update buffer / double buffering
@@ -465,10 +585,17 @@ def test_first_provisional_uses_default():
 def test_truncation_ratio_closed_form():
     # 96-bit bitmaps at the default strategy: 2 (64 + 12) + (64 + 12) / 8 bytes per token
     assert O.bitmap_bytes(1) == 16 and O.vec_bytes(32, 1, 2, 96) == 64 + 12
-    # bitmaps in whole 32-bit words: 96 / g bits -> 12, 8, 4 bytes
-    for g, T, bm in ((1, 96, 12), (2, 96, 8), (4, 96, 4), (1, 64, 8), (2, 64, 4), (4, 64, 4), (4, 128, 4)):
+    # exactly T / g bits: 96 / g bits -> 12, 6, 3 bytes (Sec. 5.2: truncated channels
+    # need no bitmap bit, so every group size saves a quarter of its bitmap)
+    for g, T, bm in ((1, 96, 12), (2, 96, 6), (4, 96, 3), (1, 64, 8), (2, 64, 4), (4, 64, 2), (4, 128, 4),
+                     (4, 32, 1), (2, 32, 2)):
         assert O.vec_bytes(32, g, 2, T) == 64 + bm
     assert abs(512 / O.bytes_per_token(32, 1, 8, 2, 96) - 512 / 161.5) < 1e-12
+    # every group size gains from the truncation: (32, 2, 8) 512 / 153 -> 512 / 148.75
+    assert O.bytes_per_token(32, 2, 8, 2, 128) == 2 * 72 + 72 / 8
+    assert O.bytes_per_token(32, 2, 8, 2, 96) == 2 * 70 + 70 / 8
+    for g in (1, 2, 4):
+        assert O.bytes_per_token(32, g, 8, 2, 96) < O.bytes_per_token(32, g, 8, 2, 128)
     P = O.Params(force_default=True, dtype="bf16", trunc=96)
     pr = O.Pair(P, 640)
     x = to_bits(rng(21).standard_normal((640, D)), "bf16")
@@ -481,8 +608,8 @@ def test_truncation_ratio_closed_form():
 def test_truncated_bitmap_is_brute_force_topk_of_leading_channels(g):
     """Identity rotation, forced (32, g, 4): every packed K vector keeps the
     top 32 / g groups among the first 96 / g by L1 score (lowest index on ties),
-    its bitmap is 96 / g bits LSB first in whole 32-bit words, its values in
-    ascending channel order."""
+    its bitmap is exactly 96 / g bits LSB first, its values in ascending
+    channel order."""
     T, r, B = 96, 32, 4
     P = O.Params(force_default=True, default=(r, g, B), dtype="fp16", trunc=T)
     x = rng(22 + g).standard_normal((64, D)) * np.linspace(0.2, 3.0, D)[None, :]   # tail channels largest
@@ -491,7 +618,7 @@ def test_truncated_bitmap_is_brute_force_topk_of_leading_channels(g):
     pr.compress(kb, kb)
     tok = pr.token_arena()
     y = from_bits(kb, "fp16")
-    bmb, vb = -(-(T // g) // 32) * 4, 2 * r
+    bmb, vb = T // g // 8, 2 * r
     for t in range(64):
         s = np.abs(y[t]).reshape(D // g, g).sum(axis=1)          # group L1 (g <= 4 adds in a pairwise order)
         order = sorted(range(T // g), key=lambda i: (-s[i], i))[: r // g]
@@ -499,7 +626,7 @@ def test_truncated_bitmap_is_brute_force_topk_of_leading_channels(g):
         want_bits[order] = 1
         blk = tok[(t // B) * B * 2 * (bmb + vb):]
         bm = np.unpackbits(blk[(t % B) * bmb:(t % B + 1) * bmb], bitorder="little")
-        assert np.array_equal(bm[:T // g], want_bits) and not bm[T // g:].any(), t
+        assert bm.size == T // g and np.array_equal(bm, want_bits), t
         ch = np.nonzero(np.repeat(want_bits, g))[0]
         vals = blk[B * bmb + (t % B) * vb: B * bmb + (t % B + 1) * vb].view(np.uint16)
         assert np.array_equal(vals, kb[t][ch]), t
