@@ -73,11 +73,12 @@ def algorithmic_bytes(cache, spec, nb_list, sel_list, desc_list):
     G = spec.group
     W = spec.rot_window
     tot = dict(score=0, attn=0, qrot=0, reduce=0)
+    sel_tok = scoreable_tok = 0
     nwq = max(1, -(-max(spec.ctx) // W))
     for p, (nb, sel, descs) in enumerate(zip(nb_list, sel_list, desc_list)):
         L = spec.ctx[p // spec.hkv]
         n_desc = len(descs)
-        bmb = [(((cache.params.trunc >> d[4]) + 31) // 32) * 4 for d in descs]
+        bmb = [(cache.params.trunc >> d[4]) >> 3 for d in descs]          # exactly T / g bits
         srec = [2 * d[3] + b for d, b in zip(descs, bmb)]                  # block keys: 16-bit values
         rec = [(1 if cache.params.fp8 else 2) * d[3] + b for d, b in zip(descs, bmb)]   # K / V tokens
         blocks_per = [((32 if d[6] & 1 else 64) >> d[5]) for d in descs]
@@ -90,7 +91,9 @@ def algorithmic_bytes(cache, spec, nb_list, sel_list, desc_list):
             i = bisect.bisect_right(fb, b) - 1
             B = 1 << descs[i][5]
             tot["attn"] += B * 2 * rec[i]
+            sel_tok += B
             wins.add((i * 64) // W)
+        scoreable_tok += sum(32 if d[6] & 1 else 64 for d in descs)
         m = L % 64
         nbuf = m - (32 if m >= 32 else 0)
         tot["attn"] += nbuf * 2 * D * 2
@@ -98,7 +101,8 @@ def algorithmic_bytes(cache, spec, nb_list, sel_list, desc_list):
         tot["attn"] += (len(wins) if cache.rotated else 0) * D * D * 4
         tot["reduce"] += G * D * 4
     tot["total"] = sum(tot.values())
-    return tot
+    return tot, dict(selected_tokens=sel_tok, scoreable_tokens=scoreable_tok,
+                     fraction=round(sel_tok / max(scoreable_tok, 1), 5))
 
 
 def source_hash():
@@ -403,7 +407,7 @@ def main():
         k = int(wsel[nw])
         sel_list.append(cache.ws_region("sel", p, 4 * max(k, 1)).cpu().numpy().view(np.int32)[:k].tolist())
         nb_list.append(int(wsel[nw + 1]))
-    ab = algorithmic_bytes(cache, spec, nb_list, sel_list, desc_list)
+    ab, selected = algorithmic_bytes(cache, spec, nb_list, sel_list, desc_list)
     dom = max(("score", "attn"), key=lambda k: kern_us[k])
     achieved = ab[dom] / (kern_us[dom] * 1e-6) / 1e9
     traffic = None
@@ -495,7 +499,7 @@ def main():
         "vs_baseline": None, "dtype": spec.dtype, "data": "synthetic",
         "config": {"workload": f"{spec.name}: decode attention over a compressed KV cache, batch {spec.num_seqs} x "
                                f"{spec.max_ctx} tokens, {spec.hq} q / {spec.hkv} kv heads, d=128, {spec.dtype}, "
-                               f"select 1/10 of blocks, planted 5% of segments"
+                               f"select 1/10 of tokens, planted 5% of segments"
                                + ("; quest mode: all channels kept, 16-token blocks, no rotation"
                                   if args.mode == "quest" else "")
                                + (f"; bitmaps of the first {args.trunc} channels" if args.trunc != D else "")
@@ -509,6 +513,7 @@ def main():
                      "algorithmic_bytes_per_launch": ab[dom], "mean_launch_us": round(kern_us[dom], 3)},
         "effective_gbps": round(ab["total"] / (ms * 1e-3) / 1e9, 1),
         "algorithmic_bytes_per_step": ab,
+        "selected": selected,
         "kernels_us": {k: round(v, 3) for k, v in kern_us.items()},
         "graph_replay_us_per_step": None if graph_us is None else round(graph_us, 3),
         "dense_us_per_step": None if dense_us is None else round(dense_us, 2),

@@ -68,13 +68,14 @@ typedef struct {
     int32_t default_block;     /*   force_default_strategy is set */
     float tau_channel;         /* accept (r, g) if dropped energy < tau * energy, K and V */
     float tau_block;           /* accept B if intra-block key variance < tau * energy */
-    int32_t select_num;        /* rho = select_num / select_den: blocks kept per */
-    int32_t select_den;        /*   (sequence, kv head) = ceil(rho * blocks) */
+    int32_t select_num;        /* rho = select_num / select_den: tokens selected per */
+    int32_t select_den;        /*   (sequence, kv head) >= ceil(rho * scoreable tokens) */
     int32_t force_default_strategy; /* 1: skip the search, use the default */
     int32_t trunc_channels;    /* T: channels represented in the bitmaps (Sec. 5.2 channel
                                   truncation: after the rotation the last D - T channels are
-                                  never kept and get no bitmap bit); 32, 64, 96 or 128, at
-                                  least every kept count.  128 = no truncation */
+                                  never kept and get no bitmap bit: a bitmap is T / g bits);
+                                  32, 64, 96 or 128, at least every kept count.  128 = no
+                                  truncation */
     int32_t value_fp8;         /* 1: the kept values of the K and V token records are stored as
                                   OCP FP8 E4M3 codes (Sec. 7: the compressed elements can be
                                   quantized further), one byte each, each the nearest code to
@@ -116,7 +117,7 @@ mosaic_status mosaic_cache_destroy(mosaic_cache *cache);
  *   desc     : 16-byte segment descriptors {uint32 token-arena offset,
  *              uint32 score-arena offset, uint32 first block, uint8 r,
  *              uint8 log2 g, uint8 log2 B, uint8 flags (bit 0 provisional)}
- *   score    : block-key records [bitmap D/(8g) B][r values], block order
+ *   score    : block-key records [bitmap T/(8g) B][r values], block order
  *   token    : per block [K bitmaps][K values][V bitmaps][V values]
  *   buffer   : update buffer [2 (K, V)][U][D] raw elements (Sec. 5.3)
  *   stage    : raw tokens of the trailing segment [2][S][D] (Sec. 5.4)
@@ -147,15 +148,21 @@ mosaic_status mosaic_workspace_bytes(const mosaic_cache *cache, int32_t op, size
  *   wsel  + p * wsel_stride  : int32 [windows + 2]: first selected entry of
  *                              each window, then k, then the block count
  *   part  + p * part_stride  : fp32 [max_splits][GP * (D + 2)]: split-K
- *                              partials (max, sum, accumulator rotated back
- *                              by R_v, per head)
+ *                              partials (max, sum, accumulator per head; a
+ *                              window's splits hold it in the window's
+ *                              rotated space, the buffer's split unrotated)
  *   tag   + p * tag_stride   : int32 [max_splits]: window of each split
- *   bseg  + p * bseg_stride  : uint32 [max_blocks]: segment << 4 | block in segment
+ *                              (-1 the update buffer, -2 none)
+ *   bseg  + p * bseg_stride  : uint32 [max_blocks]: block map, segment << 6 |
+ *                              (log2 B - 2) << 4 | block in segment
+ *   selinfo + p * selinfo_stride : uint32 [max_blocks][2]: per selected entry,
+ *                              the block's token-arena offset and
+ *                              r << 8 | log2 g << 16 | log2 B << 20
  * Calls that overlap on one workspace race; separate streams need separate
  * workspaces. */
 typedef struct {
     uint64_t qrot_off, qrot_stride, score_off, score_stride, sel_off, sel_stride, wsel_off, wsel_stride;
-    uint64_t part_off, part_stride, tag_off, tag_stride, bseg_off, bseg_stride, total;
+    uint64_t part_off, part_stride, tag_off, tag_stride, bseg_off, bseg_stride, selinfo_off, selinfo_stride, total;
     int32_t max_blocks, max_splits, gp, reserved;
 } mosaic_ws_layout;
 mosaic_status mosaic_decode_ws_layout(const mosaic_cache *cache, mosaic_ws_layout *out);
@@ -187,10 +194,12 @@ mosaic_status mosaic_append(mosaic_cache *cache, const void *k_new, const void *
 
 /* One decode step of PackedAttention (Sec. 5.3) for every sequence.  Steps:
  * rotate q into each window (rotation merged into the query), score every
- * block key (max over the GQA group's heads), keep the top ceil(rho * blocks)
- * per (sequence, kv head) by (score desc, block index asc), attend the kept
- * blocks' packed K/V plus the uncompressed update-buffer tokens, and rotate
- * the output back with R_v.
+ * block key (max over the GQA group's heads), select per (sequence, kv head)
+ * blocks in (score desc, block index asc) order while fewer than
+ * ceil(rho * scoreable tokens) tokens are taken (Sec. 4.2 stage 2; Sec. 6.1
+ * selects 10 % of tokens), attend the selected blocks' packed K/V plus the
+ * uncompressed update-buffer tokens, and rotate each window's output back
+ * with its R_v.
  *   q   : [num_seqs][num_kv_heads * group_size][128] (cache dtype)
  *   out : [num_seqs][num_kv_heads * group_size][128] fp32
  *   sm_scale: softmax scale (e.g. 1/sqrt(128)).

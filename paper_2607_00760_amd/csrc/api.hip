@@ -84,6 +84,7 @@ struct mosaic_cache {
         w.part = (float *)(b + wsl.part_off); w.part_stride = wsl.part_stride;
         w.tag = (int32_t *)(b + wsl.tag_off); w.tag_stride = wsl.tag_stride;
         w.bseg = (uint32_t *)(b + wsl.bseg_off); w.bseg_stride = wsl.bseg_stride;
+        w.selinfo = (uint2 *)(b + wsl.selinfo_off); w.selinfo_stride = wsl.selinfo_stride;
         w.max_blocks = max_blocks; w.max_splits = max_splits;
         return w;
     }
@@ -182,8 +183,11 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
         return fail(MOSAIC_ERR_CAPACITY, "max_tokens %d: a pair's token arena would exceed 4 GiB", max_tokens);
     }
     c->max_blocks = c->max_desc * (SEG / minb);
-    c->max_sel = (int)std::min<int64_t>(c->max_blocks, ((int64_t)c->max_blocks * params->select_num +
-                                                        params->select_den - 1) / params->select_den);
+    // the selection takes blocks until ceil(rho * scoreable tokens) tokens: at
+    // most ceil(budget / smallest block) of them
+    const int64_t max_budget = ((int64_t)c->max_desc * SEG * params->select_num + params->select_den - 1) /
+                               params->select_den;
+    c->max_sel = (int)std::min<int64_t>(c->max_blocks, (max_budget + minb - 1) / minb + 1);
     c->max_splits = (c->max_sel + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS + c->nw + 1;
     // arena layout
     mosaic_layout &l = c->lay;
@@ -223,7 +227,8 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     wregion(w.part_off, w.part_stride, (uint64_t)c->max_splits * c->GP * (D + 2) * 4);
     wregion(w.tag_off, w.tag_stride, (uint64_t)c->max_splits * 4);
     wregion(w.bseg_off, w.bseg_stride, (uint64_t)c->max_blocks * 4);
-    w.total = off;
+    wregion(w.selinfo_off, w.selinfo_stride, (uint64_t)c->max_blocks * 8);
+    w.total = off + 256;                     // whole 16-byte loads of the last pair's arrays stay inside
     w.max_blocks = c->max_blocks; w.max_splits = c->max_splits; w.gp = c->GP;
     c->arena = nullptr;
     c->compressed = false;

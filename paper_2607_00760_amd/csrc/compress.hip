@@ -252,18 +252,24 @@ __device__ __forceinline__ void pack_vector(float ylo, float yhi, int r, int log
     const uint64_t bm = __ballot(flag);
     if (!active) return;
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    // with truncated bitmaps of 3 or 6 bytes a block-key record can start at
+    // an odd byte: its 16-bit values are then stored a byte at a time
+    auto put16 = [&](int slot, uint16_t h) {
+        if (T < D) { val_out[2 * slot] = (uint8_t)h; val_out[2 * slot + 1] = (uint8_t)(h >> 8); }
+        else *(uint16_t *)(val_out + 2 * slot) = h;
+    };
     if (klo) {
         int slot = __popcll(mlo & below);
         if (e4m3) val_out[slot] = (uint8_t)f2e4m3(ylo);
-        else *(uint16_t *)(val_out + 2 * slot) = f2h(ylo, dtype);
+        else put16(slot, f2h(ylo, dtype));
     }
     if (khi) {
         int slot = __popcll(mlo) + __popcll(mhi & below);
         if (e4m3) val_out[slot] = (uint8_t)f2e4m3(yhi);
-        else *(uint16_t *)(val_out + 2 * slot) = f2h(yhi, dtype);
+        else put16(slot, f2h(yhi, dtype));
     }
     if (T < D) {
-        // a truncated bitmap (T / g bits in whole 32-bit words): lane i stores byte i
+        // a truncated bitmap (exactly T / g bits, whole bytes): lane i stores byte i
         const uint64_t lo64 = log2g == 0 ? mlo : bm, hi64 = log2g == 0 ? mhi : 0ull;
         const int nbytes = bm_bytes(log2g, T);
         if (lane < nbytes) bm_out[lane] = (uint8_t)((lane < 8 ? lo64 >> (8 * lane) : hi64 >> (8 * (lane - 8))) & 0xffu);

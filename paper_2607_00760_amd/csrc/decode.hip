@@ -252,6 +252,22 @@ __device__ __forceinline__ uint32_t half_at(const uint32_t (&v)[N], int s) {
 // serves any record (the compiler merges plain dword runs the same way)
 typedef uint32_t u32x4a4 __attribute__((ext_vector_type(4), aligned(4)));
 
+// N dwords starting at any byte p: the N + 1 aligned dwords that cover them,
+// joined pairwise by byte shifts (v_alignbyte).  Truncated bitmaps of 3 or 6
+// bytes put token bitmaps and block-key records at any byte; the one dword
+// read past the end stays inside the arena's slack.
+template <int N>
+__device__ __forceinline__ void load_dwords_any(const uint8_t *p, uint32_t (&out)[N]) {
+    const uintptr_t a = (uintptr_t)p;
+    const uint32_t *b = (const uint32_t *)(a & ~(uintptr_t)3);
+    const uint32_t sh = (uint32_t)(a & 3u);
+    uint32_t w[N + 1];
+#pragma unroll
+    for (int k = 0; k <= N; ++k) w[k] = b[k];
+#pragma unroll
+    for (int k = 0; k < N; ++k) out[k] = __builtin_amdgcn_alignbyte(w[k + 1], w[k], sh);
+}
+
 // A packed vector (bitmap words + values) held in registers.
 template <int RMAX>
 struct PVec {
@@ -336,13 +352,19 @@ __device__ __forceinline__ void load_pvec(PVec<RMAX> &x, const uint8_t *bm, cons
             x.v[4 * k] = t.x; x.v[4 * k + 1] = t.y; x.v[4 * k + 2] = t.z; x.v[4 * k + 3] = t.w;
         }
     } else {
-        const uint32_t *b = (const uint32_t *)bm, *v = (const uint32_t *)val;
+        // dword loads at any byte: the bitmap, then the values below rmax
+        // (those past it from the start of the values again, or zero with ZF)
+        load_dwords_any<4>(bm, x.bw);
+        const uintptr_t va = (uintptr_t)val;
+        const uint32_t *v = (const uint32_t *)(va & ~(uintptr_t)3);
+        const uint32_t sh = (uint32_t)(va & 3u);
+        uint32_t u[RMAX / 2 + 1];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) x.bw[k] = b[k];
+        for (int k = 0; k <= RMAX / 2; ++k) u[k] = v[(2 * k < rmax + 2) ? k : 0];
 #pragma unroll
         for (int k = 0; k < RMAX / 2; ++k) {
-            if (ZF) x.v[k] = (2 * k < rmax) ? v[k] : 0u;
-            else x.v[k] = v[(2 * k < rmax) ? k : 0];
+            const uint32_t t = __builtin_amdgcn_alignbyte(u[k + 1], u[k], sh);
+            x.v[k] = (ZF && 2 * k >= rmax) ? 0u : t;
         }
     }
 }
@@ -536,7 +558,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
                 if (__float_as_uint(best) == 0x80000000u) best = 0.0f;
                 if (valid) {
                     out[d.first_block + j] = best;
-                    bseg[d.first_block + j] = ((uint32_t)(s0 + i) << 4) | (uint32_t)j;
+                    bseg[d.first_block + j] = bseg_pack((uint32_t)(s0 + i), d.log2b, j);
                 }
             }
             return;
@@ -581,7 +603,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
             if (b0 + tid < nblk) {
                 const uint32_t fb = ds[i].first_block;
                 out[fb + j] = best;
-                bseg[fb + j] = ((uint32_t)(s0 + i) << 4) | (uint32_t)j;
+                bseg[fb + j] = bseg_pack((uint32_t)(s0 + i), ds[i].log2b, j);
             }
             x = xn; i = in; j = jn; r = rn;
         }
@@ -611,7 +633,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         if (__float_as_uint(best) == 0x80000000u) best = 0.0f;
         if (valid) {
             out[d.first_block + j] = best;
-            bseg[d.first_block + j] = ((uint32_t)(s0 + i) << 4) | (uint32_t)j;
+            bseg[d.first_block + j] = bseg_pack((uint32_t)(s0 + i), d.log2b, j);
         }
     }
 }
@@ -673,15 +695,26 @@ __device__ __forceinline__ uint32_t sum_below(const uint32_t *s, int n) {
     return (uint32_t)__builtin_amdgcn_readlane((int)wave_scan_add(x), 63);
 }
 
-// exclusive prefix sum over the 1024 threads of the block; s: 16 words of LDS
-__device__ __forceinline__ uint32_t block_excl_scan_1024(uint32_t v, uint32_t *s) {
+// exclusive prefix sums over the 1024 threads of the block of N values per
+// thread, and their block totals; s: 16 N words of LDS
+template <int N>
+__device__ __forceinline__ void block_excl_scan_1024(uint32_t (&v)[N], uint32_t (&tot)[N], uint32_t *s) {
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const uint32_t x = wave_scan_add(v);
-    if (lane == 63) s[wv] = x;
+    uint32_t x[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        x[i] = wave_scan_add(v[i]);
+        if (lane == 63) s[16 * i + wv] = x[i];
+    }
     __syncthreads();
-    const uint32_t base = sum_below(s, wv);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const uint32_t y = wave_scan_add(lane < 16 ? s[16 * i + lane] : 0u);   // inclusive over the waves
+        const uint32_t base = wv ? (uint32_t)__builtin_amdgcn_readlane((int)y, wv - 1) : 0u;
+        tot[i] = (uint32_t)__builtin_amdgcn_readlane((int)y, 15);
+        v[i] = base + x[i] - v[i];
+    }
     __syncthreads();
-    return base + x - v;
 }
 
 // block-wide minimum of lo and maximum of hi (1024 threads); s: 32 words
@@ -695,36 +728,45 @@ __device__ __forceinline__ void block_minmax_1024(uint32_t &lo, uint32_t &hi, ui
     __syncthreads();
 }
 
-// Exact k-th largest score key by radix selection over the range of the
-// keys: each pass histograms the candidates (keys inside the current range)
-// into 2048 bins of width 2^s, so that the bins spread over the keys that
-// are actually present instead of over fixed bit fields; at most three passes
-// narrow the range to the single threshold key T.  Then the selected list is
-// written in ascending block order: every key > T, and the keys == T with the
-// lowest block indices.  Thread t owns the keys [t * chunk, (t + 1) * chunk);
-// with REG (chunk <= 16) they stay in registers, else they are read from LDS
-// (or from the score array when they do not fit).
+// Token-budget selection (Sec. 4.2 stage 2; Sec. 6.1 selects 10 % of tokens):
+// blocks are taken in (score desc, block index asc) order while the tokens
+// already taken are fewer than the budget.  The last block taken has the
+// threshold key T: a radix selection over the range of the keys finds it,
+// each pass histogramming the candidates' TOKENS (block sizes, from the block
+// map) into 2048 bins of width 2^s over the keys still in play, so at most
+// three passes narrow the range to T.  Every block above T is taken; the
+// blocks equal to T are taken in block order while the tokens taken among
+// them are fewer than what the budget still needs.  The selected list is
+// written in ascending block order together with each entry's record offset
+// and strategy (for the attention's split setup).  Thread t owns the blocks
+// [t * chunk, (t + 1) * chunk); with REG (chunk <= 16) their keys and map
+// entries stay in registers, else they are read from LDS / the workspace.
 template <bool REG>
-__device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p, int nb, int ndesc, int k,
+__device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p, int nb, int ndesc, int budget,
                                           uint32_t *keys, uint32_t *hist, uint32_t *sbuf) {
     const int tid = threadIdx.x;
     const float *sc = ws.score + (uint64_t)p * (ws.score_stride / 4);
+    const uint32_t *bsg = ws.bseg + (uint64_t)p * (ws.bseg_stride / 4);
     int32_t *sel = ws.sel + (uint64_t)p * (ws.sel_stride / 4);
     int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
+    uint2 *sinfo = ws.selinfo + (uint64_t)p * (ws.selinfo_stride / 8);
     const int chunk = REG ? TOPK_KPT : (nb + 1023) / 1024;
     const int i0 = min(nb, tid * chunk), i1 = min(nb, i0 + chunk), n_own = i1 - i0;
     const bool in_lds = nb <= TOPK_LDS_KEYS;
-    uint32_t kr[REG ? TOPK_KPT : 1];
+    uint32_t kr[REG ? TOPK_KPT : 1], mr[REG ? TOPK_KPT : 1];
     uint32_t kmin = 0xffffffffu, kmax = 0u;
     if (REG) {
         const float4 *s4 = (const float4 *)(sc + i0);
+        const uint4 *m4 = (const uint4 *)(bsg + i0);
 #pragma unroll
         for (int q = 0; q < TOPK_KPT / 4; ++q) {
             float4 f = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            if (4 * q < n_own) f = s4[q];
+            uint4 m = make_uint4(0u, 0u, 0u, 0u);
+            if (4 * q < n_own) { f = s4[q]; m = m4[q]; }
             const float fv[4] = {f.x, f.y, f.z, f.w};
+            const uint32_t mv[4] = {m.x, m.y, m.z, m.w};
 #pragma unroll
-            for (int e = 0; e < 4; ++e) kr[4 * q + e] = score_key(fv[e]);
+            for (int e = 0; e < 4; ++e) { kr[4 * q + e] = score_key(fv[e]); mr[4 * q + e] = mv[e]; }
         }
 #pragma unroll
         for (int j = 0; j < TOPK_KPT; ++j)
@@ -741,13 +783,15 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
         if (REG) return kr[j];
         return in_lds ? keys[i0 + j] : score_key(sc[i0 + j]);
     };
+    auto map_at = [&](int j) -> uint32_t { return REG ? mr[j] : bsg[i0 + j]; };
+    auto tokens = [](uint32_t m) -> uint32_t { return 1u << bseg_log2b(m); };
     // two histograms in turn: a pass zeroes the next one while it reads its own
     for (int i = tid; i < TOPK_BINS; i += 1024) hist[i] = 0;
     block_minmax_1024(kmin, kmax, sbuf);                          // (its barriers publish the zeros)
     uint32_t base = kmin, span = kmax - kmin;                     // candidates: [base, base + span]
-    uint32_t rem = (uint32_t)k;                                    // how many candidates to take
+    uint32_t rem = (uint32_t)budget;                               // tokens still to take
     const int lane = tid & 63, wv = tid >> 6;
-    for (int pass = 0; k > 0; ++pass) {
+    for (int pass = 0; budget > 0; ++pass) {
         uint32_t *hc = hist + (pass & 1) * TOPK_BINS, *hn = hist + ((pass + 1) & 1) * TOPK_BINS;
         const int bits = 32 - (span ? __builtin_clz(span) : 32);
         const int sh = bits > 11 ? bits - 11 : 0;                 // (span >> sh) < 2048
@@ -755,12 +799,12 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
 #pragma unroll
             for (int j = 0; j < TOPK_KPT; ++j) {
                 const uint32_t d = kr[j] - base;
-                if (j < n_own && kr[j] >= base && d <= span) atomicAdd(&hc[d >> sh], 1u);
+                if (j < n_own && kr[j] >= base && d <= span) atomicAdd(&hc[d >> sh], tokens(mr[j]));
             }
         } else {
             for (int j = 0; j < n_own; ++j) {
                 const uint32_t key = key_at(j), d = key - base;
-                if (key >= base && d <= span) atomicAdd(&hc[d >> sh], 1u);
+                if (key >= base && d <= span) atomicAdd(&hc[d >> sh], tokens(map_at(j)));
             }
         }
         __syncthreads();
@@ -785,15 +829,23 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
         span = min(span - (b << sh), width);
         if (sh == 0) break;
     }
-    const uint32_t T = base, take_eq_total = rem;
-    uint32_t gt = 0, eq = 0;
-    if (k > 0) {
+    // T = base; rem = tokens the budget still needs among the blocks equal to T
+    const uint32_t T = base, need_eq = rem;
+    uint32_t cnt[3] = {0u, 0u, 0u};                        // greater blocks, equal blocks, equal tokens
+    if (budget > 0) {
         if (REG) {
 #pragma unroll
             for (int j = 0; j < TOPK_KPT; ++j)
-                if (j < n_own) { gt += kr[j] > T; eq += kr[j] == T; }
+                if (j < n_own) {
+                    cnt[0] += kr[j] > T;
+                    if (kr[j] == T) { cnt[1] += 1u; cnt[2] += tokens(mr[j]); }
+                }
         } else {
-            for (int j = 0; j < n_own; ++j) { const uint32_t key = key_at(j); gt += key > T; eq += key == T; }
+            for (int j = 0; j < n_own; ++j) {
+                const uint32_t key = key_at(j);
+                cnt[0] += key > T;
+                if (key == T) { cnt[1] += 1u; cnt[2] += tokens(map_at(j)); }
+            }
         }
     }
     // first block of each rotation window (windows past the last segment start at nb)
@@ -805,46 +857,54 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
         const int s0 = w * segs_per_win;
         fbw[w] = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
     }
-    // equal keys are taken in block order until take_eq_total, so a thread's
-    // list position is (greater keys before it) + min(equal keys before it,
-    // take_eq_total): one scan of both counts (packed while they fit 16 bits)
-    uint32_t gt_before, eq_before;
-    if (nb < 65536) {
-        const uint32_t both = block_excl_scan_1024((gt << 16) | eq, sbuf);   // (its barriers publish fbw)
-        gt_before = both >> 16;
-        eq_before = both & 0xffffu;
-    } else {
-        eq_before = block_excl_scan_1024(eq, sbuf);
-        gt_before = block_excl_scan_1024(gt, sbuf);
+    const uint32_t own_eq_tok = cnt[2];
+    uint32_t tot[3];
+    block_excl_scan_1024<3>(cnt, tot, sbuf);               // (its barriers publish fbw)
+    // the equal blocks taken are the first E of them in block order: the
+    // thread whose equal tokens cross need_eq counts its own taken ones
+    if (budget > 0 && cnt[2] < need_eq && cnt[2] + own_eq_tok >= need_eq) {
+        uint32_t acc = cnt[2], taken = 0;
+        for (int j = 0; j < n_own; ++j)
+            if (key_at(j) == T) { taken += acc < need_eq; acc += tokens(map_at(j)); }
+        sbuf[40] = cnt[1] + taken;
     }
-    uint32_t take = 0;
-    if (take_eq_total > eq_before) take = min(eq, take_eq_total - eq_before);
-    const uint32_t pos0 = gt_before + min(eq_before, take_eq_total);
+    __syncthreads();
+    const uint32_t E = budget > 0 ? sbuf[40] : 0u;
+    const int k = budget > 0 ? (int)(tot[0] + E) : 0;      // blocks selected
+    const uint32_t pos0 = cnt[0] + min(cnt[1], E);
     // write the selected list; a window starting inside [i0, i1) records the
     // list position reached there (windows starting at nb record k)
     int wn = 0;
     while (wn < nwl && fbw[wn] < i0) ++wn;
     int nextfb = wn < nwl ? fbw[wn] : 0x7fffffff;          // next window start, kept in a register
-    uint32_t pos = pos0, seen = 0;
-    auto emit = [&](int j, uint32_t key) {
+    uint32_t pos = pos0, acc = cnt[2];
+    const int maxd = g.max_desc;
+    auto emit = [&](int j, uint32_t key, uint32_t m) {
         const int i = i0 + j;
         while (nextfb == i) {
             wsel[wn++] = (int)pos;
             nextfb = wn < nwl ? fbw[wn] : 0x7fffffff;
         }
-        if (k > 0) {
-            const bool take_it = key > T || (key == T && seen < take);
-            seen += (key == T && take_it) ? 1u : 0u;
-            if (take_it && pos < (uint32_t)nb) sel[pos] = i;
+        if (budget > 0) {
+            bool take_it = key > T;
+            if (key == T) { take_it = acc < need_eq; acc += tokens(m); }
+            if (take_it && pos < (uint32_t)nb) {
+                sel[pos] = i;
+                const Desc d = gd[min(bseg_seg(m), (uint32_t)maxd - 1)];
+                const uint32_t goff = d.tok_off + (uint32_t)(bseg_j(m) << d.log2b) *
+                                                      (uint32_t)(2 * tok_vec_bytes(d.r, d.log2g, g.trunc, g.fp8));
+                sinfo[pos] = make_uint2(goff, ((uint32_t)d.r << 8) | ((uint32_t)d.log2g << 16) |
+                                                  ((uint32_t)d.log2b << 20));
+            }
             pos += take_it ? 1u : 0u;
         }
     };
     if (REG) {
 #pragma unroll
         for (int j = 0; j < TOPK_KPT; ++j)
-            if (j < n_own) emit(j, kr[j]);
+            if (j < n_own) emit(j, kr[j], mr[j]);
     } else {
-        for (int j = 0; j < n_own; ++j) emit(j, key_at(j));
+        for (int j = 0; j < n_own; ++j) emit(j, key_at(j), map_at(j));
     }
     if (tid == 1023)
         for (; wn < nwl; ++wn) wsel[wn] = k;
@@ -870,13 +930,15 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
     const int nb = pair_nblocks(g, p, meta);
     int nf, prov, nbuf;
     const int ndesc = pair_ndesc(meta, nf, prov, nbuf);
-    int k = 0;
-    if (nb > 0) {
-        const long long kk = ((long long)nb * g.sel_num + g.sel_den - 1) / g.sel_den;
-        k = (int)(kk < 1 ? 1 : (kk > nb ? nb : kk));
+    // the token budget: ceil(rho * scoreable tokens), at least one token
+    const int ntok = nf * SEG + prov * UBUF;
+    int budget = 0;
+    if (nb > 0 && ntok > 0) {
+        const long long bb = ((long long)ntok * g.sel_num + g.sel_den - 1) / g.sel_den;
+        budget = (int)(bb < 1 ? 1 : (bb > ntok ? ntok : bb));
     }
-    if (nb <= 1024 * TOPK_KPT) topk_body<true>(g, ws, p, nb, ndesc, k, keys, hist, sbuf);
-    else topk_body<false>(g, ws, p, nb, ndesc, k, keys, hist, sbuf);
+    if (nb <= 1024 * TOPK_KPT) topk_body<true>(g, ws, p, nb, ndesc, budget, keys, hist, sbuf);
+    else topk_body<false>(g, ws, p, nb, ndesc, budget, keys, hist, sbuf);
 }
 
 // ------------------------------------------------------------------ attention
@@ -909,10 +971,8 @@ constexpr int KT_STRIDE = 136;       // u16 per token row of the K tile (128 + 8
 constexpr int VT_STRIDE = 68;        // u16 per channel row of the V tile (64 + 4 pad)
 constexpr int TILE_BYTES = 17408;    // max(64 * 272, 128 * 136)
 constexpr int ATTN_NWV = 2;          // waves per attention workgroup
-// block table [SPLIT_BLOCKS] + per-wave class counts (16-byte multiple), then
-// the merged accumulator [D][8] for the back-rotation
-constexpr int ATTN_ACM_OFF = (8 * SPLIT_BLOCKS + 2 * 4 * 4 + 15) / 16 * 16;
-constexpr int ATTN_HDR_BYTES = ATTN_ACM_OFF + D * 8 * 4;
+// block table [SPLIT_BLOCKS] + per-wave class counts (16-byte multiple)
+constexpr int ATTN_HDR_BYTES = (8 * SPLIT_BLOCKS + 2 * 4 * 4 + 15) / 16 * 16;
 
 // x = hi + lo with hi, lo in the MFMA's 16-bit type (round to nearest even);
 // hi + lo carries x to ~16 (bf16) or ~22 (fp16) significant bits
@@ -1025,9 +1085,8 @@ __device__ __forceinline__ void load_tok(PVec8<RMAX> &x, const uint8_t *tokg, co
             x.v[4 * k] = t.x; x.v[4 * k + 1] = t.y; x.v[4 * k + 2] = t.z; x.v[4 * k + 3] = t.w;
         }
     } else {
-        const uint32_t *bq = (const uint32_t *)bm, *v = (const uint32_t *)val;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) x.bw[k] = bq[k];
+        load_dwords_any<4>(bm, x.bw);                    // a truncated bitmap can sit at any byte
+        const uint32_t *v = (const uint32_t *)val;       // token values stay 4-byte aligned
 #pragma unroll
         for (int k = 0; k < RMAX / 4; ++k) x.v[k] = v[(4 * k < rmax) ? k : 0];
     }
@@ -1094,7 +1153,6 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     int nf, prov, nbuf;
     pair_ndesc(meta, nf, prov, nbuf);
     const int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
-    const int32_t *sel = ws.sel + (uint64_t)p * (ws.sel_stride / 4);
     int w, e0, e1, total;
     split_of(wsel, g.nw, s, ws.max_blocks, w, e0, e1, total);
     int32_t *tag = ws.tag + (uint64_t)p * (ws.tag_stride / 4);
@@ -1168,13 +1226,10 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     {
         const bool on = tid < nbk;
         uint32_t goff = 0; int r = 0, l2g = 0, l2b = 2;
-        if (on) {                                   // (indices checked against their arrays)
-            const uint32_t bi = (uint32_t)sel[e0 + tid];
-            const uint32_t bs = bi < (uint32_t)ws.max_blocks ? ws.bseg[(uint64_t)p * (ws.bseg_stride / 4) + bi] : 0u;
-            const Desc d = g.desc_of(p)[min(bs >> 4, (uint32_t)g.max_desc - 1)];
-            const int jb = (int)(bs & 15u);
-            r = d.r; l2g = d.log2g; l2b = d.log2b;
-            goff = d.tok_off + (uint32_t)(jb << l2b) * (uint32_t)(2 * tok_vec_bytes(r, l2g, g.trunc, F8));
+        if (on) {                                   // the entry's record offset and strategy (top-k wrote them)
+            const uint2 si = ws.selinfo[(uint64_t)p * (ws.selinfo_stride / 8) + e0 + tid];
+            r = (int)((si.y >> 8) & 0xffu); l2g = (int)((si.y >> 16) & 3u); l2b = (int)min(max((si.y >> 20) & 7u, 2u), 4u);
+            goff = min(si.x, (uint32_t)g.tok_stride);      // keeps every read inside the arena
         }
         const int cls = on ? 4 - l2b : 3;
         const uint64_t m0 = __ballot(cls == 0), m1 = __ballot(cls == 1), m2 = __ballot(cls == 2);
@@ -1188,7 +1243,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         // granule loads take a fixed 16-byte bitmap and whole 16-byte runs of
         // values at any 4-byte aligned record (what lies past a record is read
         // inside the arena's slack and never used; a walk reads D / g bits)
-        all16 = __syncthreads_and(!on || (goff & 3u) == 0);
+        all16 = __syncthreads_and(!on || ((goff & 3u) == 0 && (bm_bytes(l2g, g.trunc) & 3) == 0));
         if (RMAX >= D && !F8) dense = __syncthreads_and(!on || (l2g == 0 && r == D && (goff & 15u) == 0));
         if (on) {
             const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -1443,8 +1498,8 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) mrg[(q4 * 4 + r) * (D + 2) + 2 + ct * 16 + l16] = acc_o[ct][r];
     __syncthreads();
-    // merged accumulator, channel-major [D][GP]
-    float *acm = (float *)(smem + ATTN_ACM_OFF);
+    // the merged (max, sum, accumulator) of the split, in the window's rotated
+    // space (the combine rotates each window's sum back once)
     for (int i = tid; i < GP * D; i += NWV * 64) {
         const int h = i / D, cc = i % D;
         float Mx = -INFINITY;
@@ -1458,93 +1513,100 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
             A += (mw[h * (D + 2) + 2 + cc] + mw[(h + GP) * (D + 2) + 2 + cc]) * f;   // high + residual rows
             Ls += mw[h * (D + 2) + 1] * f;
         }
-        if (g.rotated) acm[cc * GP + h] = A;
-        else part[2 * GP + h * D + cc] = A;
+        part[2 * GP + h * D + cc] = A;
         if (cc == 0) { part[h] = Mx; part[GP + h] = Ls; }
-    }
-    if (g.rotated) {
-        // back-rotation of the split's accumulator by its window's R_v (the
-        // rotation stays merged into the single output vector): thread j
-        // produces output channel j of every head, x_j = sum_c a_c R_v[c][j]
-        // R_v is staged through the tiles in two halves of 64 rows (32 KB)
-        static_assert(NWV * 64 == D, "one thread per output channel");
-        static_assert(NWV * TILE_BYTES >= 64 * D * 4, "half of R_v fits the tiles");
-        const float *rvg = g.rot_of(p, w) + 2 * D * D;
-        const int j = tid;
-        float o[GP];
-#pragma unroll
-        for (int h = 0; h < GP; ++h) o[h] = 0.0f;
-        const uint32_t aa = lds_addr(acm), ra = lds_addr(wbase);
-        constexpr int PER = 64 * D / 4 / (NWV * 64);        // 16-byte pieces per thread per half
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-            u32x4 t[PER];
-#pragma unroll
-            for (int k = 0; k < PER; ++k) t[k] = ((const u32x4 *)(rvg + hf * 64 * D))[tid + NWV * 64 * k];
-            __syncthreads();                                // merge rows / previous half read
-#pragma unroll
-            for (int k = 0; k < PER; ++k) lds_st<u32x4>(ra + (uint32_t)(tid + NWV * 64 * k) * 16, t[k]);
-            __syncthreads();
-#pragma unroll 8
-            for (int c = 0; c < 64; ++c) {
-                const float r = lds_ld<float>(ra + (uint32_t)(c * D + j) * 4);
-#pragma unroll
-                for (int h4 = 0; h4 < GP; h4 += 4) {
-                    const floatx4 a4 = lds_ld<floatx4>(aa + (uint32_t)((hf * 64 + c) * GP + h4) * 4);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) o[h4 + e] = fmaf(a4[e], r, o[h4 + e]);
-                }
-            }
-        }
-#pragma unroll
-        for (int h = 0; h < GP; ++h) part[2 * GP + h * D + j] = o[h];
     }
     if (tid == 0) tag[s] = w;
 }
 
 // ------------------------------------------------------------------ combine
-// grid (pairs, GP * D / 256), one output per thread: online log-sum-exp merge of a pair's split partials (already
-// in the unrotated space: the window splits were rotated back by R_v, the
-// update buffer's split never was rotated) into the output.  Splits tagged -2
-// hold nothing.  A kernel boundary, rather than a device-wide fence per
-// workgroup, makes the partials visible.
-constexpr int RED_THREADS = 256;
+// grid (pairs, D / CMB_COLS), 256 threads: a workgroup produces output channels
+// j0 .. j0 + 15 of every head of a pair.  The splits of a rotation window are
+// consecutive (the attention numbers them window by window, then the update
+// buffer's split): for each window the workgroup merges its splits' (max,
+// sum, accumulator) by log-sum-exp, rotates the merged accumulator back once
+// with the window's R_v (x_j = sum_c a_c R_v[c][j]: rows j0.. of the stored
+// R_v^T, 8 KB per window; the rotation stays merged into one vector per
+// window, Sec. 5.3), and folds the result into a running log-sum-exp merge
+// with the other windows and the buffer's unrotated split.  A kernel boundary
+// makes the attention's partials visible.
+constexpr int CMB_COLS = 16, CMB_THREADS = 256;
 
 template <int GP>
-__global__ void __launch_bounds__(RED_THREADS) k_combine(Geom g, WsGeom ws, float *out) {
+__global__ void __launch_bounds__(CMB_THREADS) k_combine(Geom g, WsGeom ws, float *out) {
     constexpr int PS = GP * (D + 2);
-    constexpr int CB = 32;                                  // splits whose loads are issued together
-    const int p = blockIdx.x, tid = threadIdx.x, G = g.G;
-    const int i = blockIdx.y * RED_THREADS + tid, h = i / D;   // output (head, channel)
+    constexpr int NPART = CMB_THREADS / (GP * CMB_COLS);     // threads per output in the rotation
+    constexpr int CPP = D / NPART;                            // channels per thread
+    __shared__ float am[GP][D];                               // merged accumulator of the current window
+    __shared__ float rv[CMB_COLS][D + 4];                     // R_v[c][j0 + jj] as rows jj
+    __shared__ float wml[2][GP];                              // the window's merged max and sum
+    const int p = blockIdx.x, j0 = blockIdx.y * CMB_COLS, tid = threadIdx.x;
+    const int oi = tid / NPART, part_i = tid % NPART;         // output (head, column) and channel part
+    const int oh = oi / CMB_COLS, oj = oi % CMB_COLS;
+    const PairMeta meta = *g.meta_of(p);
+    int nf, prov, nbuf;
+    pair_ndesc(meta, nf, prov, nbuf);
+    const int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
     const float *part = ws.part + (uint64_t)p * (ws.part_stride / 4);
-    const int32_t *tag = ws.tag + (uint64_t)p * (ws.tag_stride / 4);
-    float num = 0.0f, den = 0.0f, Mx = -INFINITY;
-    for (int y0 = 0; y0 < ws.max_splits; y0 += CB) {
-        const int n = min(CB, ws.max_splits - y0);
-        int t[CB];
-        float m[CB], l[CB], v[CB];
-#pragma unroll
-        for (int e = 0; e < CB; ++e) {
-            if (e < n) {
-                const float *ps = part + (uint64_t)(y0 + e) * PS;
-                t[e] = tag[y0 + e];
-                m[e] = ps[h];
-                l[e] = ps[GP + h];
-                v[e] = ps[2 * GP + i];
+    const int lim = ws.max_blocks;
+    float M = -INFINITY, Lsum = 0.0f, o = 0.0f;               // running merge of output (oh, j0 + oj)
+    int s0 = 0;
+    // windows in order, then the buffer's split (w == nw)
+    for (int w = 0; w <= g.nw; ++w) {
+        int nsp;
+        if (w < g.nw) {
+            const int a = min(max(wsel[w], 0), lim), b = min(max(wsel[w + 1], a), lim);
+            nsp = (b - a + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS;
+        } else {
+            nsp = nbuf > 0 ? 1 : 0;
+        }
+        if (nsp == 0) continue;
+        if (s0 + nsp > ws.max_splits) break;                  // (cannot happen: the grid had this many)
+        const bool rot = w < g.nw && g.rotated;
+        if (rot) {                                            // stage R_v[c][j0 .. j0 + 15] (rows of R_v^T)
+            const float *rvt = g.rot_of(p, w) + D * D + (uint64_t)j0 * D;
+            for (int i = tid; i < CMB_COLS * D / 4; i += CMB_THREADS) {
+                const int jj = i / (D / 4), c4 = i % (D / 4);
+                *(float4 *)&rv[jj][4 * c4] = *(const float4 *)(rvt + (uint64_t)jj * D + 4 * c4);
             }
         }
-#pragma unroll
-        for (int e = 0; e < CB; ++e) {
-            if (e < n && t[e] != -2 && m[e] != -INFINITY) {
-                const float mn = fmaxf(Mx, m[e]);
-                const float a = __expf(Mx - mn), b = __expf(m[e] - mn);
-                num = num * a + v[e] * b;
-                den = den * a + l[e] * b;
-                Mx = mn;
+        // merge the window's splits: element (h, c) per thread
+        for (int i = tid; i < GP * D; i += CMB_THREADS) {
+            const int h = i / D, c = i % D;
+            float Mx = -INFINITY;
+            for (int t = 0; t < nsp; ++t) Mx = fmaxf(Mx, part[(uint64_t)(s0 + t) * PS + h]);
+            float A = 0.0f, Ls = 0.0f;
+            for (int t = 0; t < nsp; ++t) {
+                const float *ps = part + (uint64_t)(s0 + t) * PS;
+                const float f = ps[h] == -INFINITY ? 0.0f : __expf(ps[h] - Mx);
+                A += ps[2 * GP + h * D + c] * f;
+                Ls += ps[GP + h] * f;
             }
+            am[h][c] = A;
+            if (c == 0) { wml[0][h] = Mx; wml[1][h] = Ls; }
         }
+        __syncthreads();
+        float y = 0.0f;
+        if (rot) {
+#pragma unroll 8
+            for (int c = part_i * CPP; c < (part_i + 1) * CPP; ++c) y = fmaf(am[oh][c], rv[oj][c], y);
+#pragma unroll
+            for (int m = 1; m < NPART; m <<= 1) y += __shfl_xor(y, m, WAVE);
+        } else {
+            y = am[oh][j0 + oj];
+        }
+        const float wm = wml[0][oh], wl = wml[1][oh];
+        if (wm != -INFINITY) {
+            const float mn = fmaxf(M, wm);
+            const float a = __expf(M - mn), b = __expf(wm - mn);
+            o = o * a + y * b;
+            Lsum = Lsum * a + wl * b;
+            M = mn;
+        }
+        __syncthreads();                                      // am, rv and wml are rewritten next
+        s0 += nsp;
     }
-    if (h < G) out[(uint64_t)p * G * D + i] = (den > 0.0f) ? num / den : 0.0f;
+    if (part_i == 0 && oh < g.G) out[((uint64_t)p * g.G + oh) * D + j0 + oj] = (Lsum > 0.0f) ? o / Lsum : 0.0f;
 }
 
 int max_keep(const Geom &g) {
@@ -1596,7 +1658,7 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, f
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev) hipEventRecord(ev[4], s);
-    hipLaunchKernelGGL(k_combine<GP>, dim3(g.npairs, GP * D / RED_THREADS), dim3(RED_THREADS), 0, s, g, w, out);
+    hipLaunchKernelGGL(k_combine<GP>, dim3(g.npairs, D / CMB_COLS), dim3(CMB_THREADS), 0, s, g, w, out);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev) hipEventRecord(ev[5], s);
     return hipSuccess;

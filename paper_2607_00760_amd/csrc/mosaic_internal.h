@@ -63,9 +63,20 @@ struct WsGeom {               // decode workspace
     int32_t *wsel; uint64_t wsel_stride;    // [nw + 2]
     float *part; uint64_t part_stride;      // [max_splits][GP * (D + 2)]
     int32_t *tag; uint64_t tag_stride;      // [max_splits]
-    uint32_t *bseg; uint64_t bseg_stride;   // [max_blocks]: segment << 4 | block in segment
+    uint32_t *bseg; uint64_t bseg_stride;   // [max_blocks]: block map, bseg_pack
+    uint2 *selinfo; uint64_t selinfo_stride; // [max_blocks]: per selected entry {token-arena
+                                             //   byte offset, r << 8 | log2g << 16 | log2b << 20}
     int max_blocks, max_splits;
 };
+
+// block map entry of block b of a pair: its segment, log2 of its size (2..4)
+// and its index inside the segment
+__host__ __device__ __forceinline__ uint32_t bseg_pack(uint32_t seg, int log2b, int j) {
+    return (seg << 6) | ((uint32_t)(log2b - 2) << 4) | (uint32_t)j;
+}
+__host__ __device__ __forceinline__ uint32_t bseg_seg(uint32_t e) { return e >> 6; }
+__host__ __device__ __forceinline__ int bseg_log2b(uint32_t e) { return (int)((e >> 4) & 3u) + 2; }
+__host__ __device__ __forceinline__ int bseg_j(uint32_t e) { return (int)(e & 15u); }
 
 // ---------------------------------------------------------------- elements
 __device__ __forceinline__ float h2f(uint16_t h, int dtype) {
@@ -81,10 +92,12 @@ __device__ __forceinline__ uint16_t f2h(float f, int dtype) {
     return __builtin_bit_cast(uint16_t, (_Float16)f);   // v_cvt_f16_f32, RNE
 }
 
-// bitmap bytes of a vector whose first T channels are represented (T / g
-// bits in whole 32-bit words, so every record stays 4-byte aligned), and its
-// record size
-__host__ __device__ __forceinline__ int bm_bytes(int log2g, int T) { return (((T >> log2g) + 31) >> 5) << 2; }
+// bitmap bytes of a vector whose first T channels are represented: exactly
+// T / g bits (T a multiple of 32, g <= 4: whole bytes).  A truncated bitmap of
+// g = 2 or 4 is 6, 3, 4, 2 or 1 bytes, so such token bitmaps and block-key
+// records can sit at any byte; a token record's values (and every run of B >=
+// 4 bitmaps) stay 4-byte aligned.  And the record size:
+__host__ __device__ __forceinline__ int bm_bytes(int log2g, int T) { return (T >> log2g) >> 3; }
 __host__ __device__ __forceinline__ int vec_bytes(int r, int log2g, int T) { return 2 * r + bm_bytes(log2g, T); }
 // a K or V token record: one byte per kept value with E4M3 values, else two
 // (block keys always hold 16-bit values: vec_bytes)

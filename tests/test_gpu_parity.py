@@ -30,7 +30,8 @@ CASES = {
     # the sequence-only (quest) mode: every channel kept, 16-token blocks, no rotation
     "quest_mode": (gen.spec("c3", ctx=(2500, 700), hkv=2, rotate=False), dict(force_default=True,
                                                                               default=(128, 1, 16))),
-    # channel truncation: bitmaps of the first 96 (64) channels, 12 / 6 / 3-byte bitmaps
+    # channel truncation: bitmaps of the first 96 (64) channels: 12 / 6 / 3-byte bitmaps
+    # at g = 1 / 2 / 4 (4 / 2 bytes at T = 64, g = 2 / 4), so g >= 2 records sit at any byte
     "truncated_96": (gen.spec("c1", ctx=(3000, 1200), hkv=2), dict(trunc=96)),
     "truncated_64_g2": (gen.spec("c2", ctx=(1500, 700), hkv=2), dict(trunc=64, force_default=True,
                                                                     default=(32, 2, 8))),
@@ -52,12 +53,14 @@ CASES = {
     # workload's matrices), with 96-channel bitmaps: the use the reorder serves
     "reordered_truncated_96": (gen.spec("c2", ctx=(2500, 900), hkv=2, rot_window=1024), dict(trunc=96)),
     # E4M3 values over a wide range: tokens scaled by 2^-14 .. 2^9, so kept
-    # values fall below 2^-6 (subnormal codes, zeros) and above 448 (saturation)
+    # values fall below 2^-6 (subnormal codes, zeros) and above 448 (saturation);
+    # K and V for the byte-exact compression, K only for the decode (unit-scale
+    # values keep the outputs O(1) under the same absolute bound)
     "fp8_wide_range": (gen.spec("c3", ctx=(1500, 700), hkv=2, kind="gauss"), dict(fp8=True)),
 }
 
 
-def _case(name):
+def _case(name, decode=False):
     spec, extra = CASES[name]
     cap = spec.max_ctx + 130
     lay = gen.make_layer(spec, 0, capacity=cap)
@@ -65,7 +68,7 @@ def _case(name):
     if name == "fp8_wide_range":
         n = lay["k"].shape[2]
         scale = torch.pow(2.0, (torch.arange(n) % 24 - 14).float())[None, None, :, None]
-        for which in ("k", "v"):
+        for which in (("k",) if decode else ("k", "v")):
             lay[which] = (lay[which].float() * scale).to(lay[which].dtype)     # exact: powers of two
     if name.startswith("reordered"):
         from oracle import rotation as RO
@@ -92,7 +95,7 @@ def test_compress_bit_exact(name):
 
 @pytest.mark.parametrize("name", list(CASES))
 def test_decode_parity(name):
-    spec, lay, lp, op, cap = _case(name)
+    spec, lay, lp, op, cap = _case(name, decode=True)
     print(f"[decode] {name} ctx={spec.ctx}", flush=True)
     c = gpu_cache(lp, spec, lay, cap)
     ops = oracle_pairs(op, spec, lay, cap)
@@ -105,8 +108,8 @@ def test_decode_parity(name):
         gs, gsel, _ = gpu_scores_sel(c, p, nb)
         assert np.array_equal(gs.view(np.uint32), scores[p].view(np.uint32)), f"{name} pair {p}: block scores"
         assert np.array_equal(gsel, sels[p]), f"{name} pair {p}: selected blocks"
-    # inputs scaled up to 2^9: the outputs' rounding scales with them
-    assert_close(out.cpu().numpy(), want, name, magnitude=2.0 ** 9 if name == "fp8_wide_range" else 1.0)
+    err, rel = assert_close(out.cpu().numpy(), want, name)
+    print(f"[decode] {name}: max-abs {err:.3e} rel-L2 {rel:.3e}", flush=True)
 
 
 @pytest.mark.parametrize("name", ["c1", "ragged_bf16_w128", "g7_student", "fp8_search_bf16"])
