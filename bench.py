@@ -67,9 +67,9 @@ def parse():
 def algorithmic_bytes(cache, spec, nb_list, sel_list, desc_list):
     """Bytes the method must move per decode step, per kernel (score / attn /
     qrot / reduce) and in total: block keys and descriptors (score), the
-    selected blocks' packed K and V, update-buffer tokens and R_v per window
-    with selected blocks (attn, which rotates each split back), R_k^T per
-    window and q (qrot), the fp32 output (reduce)."""
+    selected blocks' packed K and V and the update-buffer tokens (attn), R_k^T
+    per window and q (qrot), R_v per window with selected blocks and the fp32
+    output (reduce, which rotates each window's merged sum back)."""
     G = spec.group
     W = spec.rot_window
     tot = dict(score=0, attn=0, qrot=0, reduce=0)
@@ -98,7 +98,7 @@ def algorithmic_bytes(cache, spec, nb_list, sel_list, desc_list):
         nbuf = m - (32 if m >= 32 else 0)
         tot["attn"] += nbuf * 2 * D * 2
         tot["qrot"] += (nwq if cache.rotated else 0) * D * D * 4 + G * D * 2
-        tot["attn"] += (len(wins) if cache.rotated else 0) * D * D * 4
+        tot["reduce"] += (len(wins) if cache.rotated else 0) * D * D * 4    # R_v of each window, in the combine
         tot["reduce"] += G * D * 4
     tot["total"] = sum(tot.values())
     return tot, dict(selected_tokens=sel_tok, scoreable_tokens=scoreable_tok,

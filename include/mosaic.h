@@ -153,16 +153,18 @@ mosaic_status mosaic_workspace_bytes(const mosaic_cache *cache, int32_t op, size
  *                              rotated space, the buffer's split unrotated)
  *   tag   + p * tag_stride   : int32 [max_splits]: window of each split
  *                              (-1 the update buffer, -2 none)
- *   bseg  + p * bseg_stride  : uint32 [max_blocks]: block map, segment << 6 |
- *                              (log2 B - 2) << 4 | block in segment
- *   selinfo + p * selinfo_stride : uint32 [max_blocks][2]: per selected entry,
- *                              the block's token-arena offset and
- *                              r << 8 | log2 g << 16 | log2 B << 20
+ *   binfo + p * binfo_stride : uint32 [max_blocks][2]: per block, its
+ *                              token-arena offset and r << 8 | log2 g << 16 |
+ *                              log2 B << 20
+ *   bsize + p * bsize_stride : uint8 [max_blocks]: per block, log2 B
+ *   selinfo + p * selinfo_stride : uint32 [max_blocks][2]: binfo of each
+ *                              entry of the selected list
  * Calls that overlap on one workspace race; separate streams need separate
  * workspaces. */
 typedef struct {
     uint64_t qrot_off, qrot_stride, score_off, score_stride, sel_off, sel_stride, wsel_off, wsel_stride;
-    uint64_t part_off, part_stride, tag_off, tag_stride, bseg_off, bseg_stride, selinfo_off, selinfo_stride, total;
+    uint64_t part_off, part_stride, tag_off, tag_stride, binfo_off, binfo_stride, bsize_off, bsize_stride,
+             selinfo_off, selinfo_stride, total;
     int32_t max_blocks, max_splits, gp, reserved;
 } mosaic_ws_layout;
 mosaic_status mosaic_decode_ws_layout(const mosaic_cache *cache, mosaic_ws_layout *out);

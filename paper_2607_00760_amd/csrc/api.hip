@@ -83,7 +83,8 @@ struct mosaic_cache {
         w.wsel = (int32_t *)(b + wsl.wsel_off); w.wsel_stride = wsl.wsel_stride;
         w.part = (float *)(b + wsl.part_off); w.part_stride = wsl.part_stride;
         w.tag = (int32_t *)(b + wsl.tag_off); w.tag_stride = wsl.tag_stride;
-        w.bseg = (uint32_t *)(b + wsl.bseg_off); w.bseg_stride = wsl.bseg_stride;
+        w.binfo = (uint2 *)(b + wsl.binfo_off); w.binfo_stride = wsl.binfo_stride;
+        w.bsize = b + wsl.bsize_off; w.bsize_stride = wsl.bsize_stride;
         w.selinfo = (uint2 *)(b + wsl.selinfo_off); w.selinfo_stride = wsl.selinfo_stride;
         w.max_blocks = max_blocks; w.max_splits = max_splits;
         return w;
@@ -226,7 +227,8 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     // part: split partials (max, sum, unrotated accumulator per head)
     wregion(w.part_off, w.part_stride, (uint64_t)c->max_splits * c->GP * (D + 2) * 4);
     wregion(w.tag_off, w.tag_stride, (uint64_t)c->max_splits * 4);
-    wregion(w.bseg_off, w.bseg_stride, (uint64_t)c->max_blocks * 4);
+    wregion(w.binfo_off, w.binfo_stride, (uint64_t)c->max_blocks * 8);
+    wregion(w.bsize_off, w.bsize_stride, (uint64_t)c->max_blocks);
     wregion(w.selinfo_off, w.selinfo_stride, (uint64_t)c->max_blocks * 8);
     w.total = off + 256;                     // whole 16-byte loads of the last pair's arrays stay inside
     w.max_blocks = c->max_blocks; w.max_splits = c->max_splits; w.gp = c->GP;

@@ -513,7 +513,13 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
     if (RMAX >= D) dense = __syncthreads_and(dense);
     const int nblk = s_nblk;
     float *out = ws.score + (uint64_t)p * (ws.score_stride / 4);
-    uint32_t *bseg = ws.bseg + (uint64_t)p * (ws.bseg_stride / 4);
+    uint2 *binfo = ws.binfo + (uint64_t)p * (ws.binfo_stride / 8);
+    uint8_t *bsize = ws.bsize + (uint64_t)p * ws.bsize_stride;
+    // a block's token-record offset and strategy (what the selection hands to the attention)
+    auto info_of = [&](const Desc &d, int j) {
+        return blk_info(d.tok_off + (uint32_t)(j << d.log2b) * (uint32_t)(2 * tok_vec_bytes(d.r, d.log2g, g.trunc, g.fp8)),
+                        d.r, d.log2g, d.log2b);
+    };
     const uint8_t *sc = g.sc_of(p);
     if constexpr (RMAX >= D) {
         if (dense) {
@@ -558,7 +564,9 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
                 if (__float_as_uint(best) == 0x80000000u) best = 0.0f;
                 if (valid) {
                     out[d.first_block + j] = best;
-                    bseg[d.first_block + j] = bseg_pack((uint32_t)(s0 + i), d.log2b, j);
+                    binfo[d.first_block + j] = info_of(d, j);
+            bsize[d.first_block + j] = d.log2b;
+                    bsize[d.first_block + j] = d.log2b;
                 }
             }
             return;
@@ -603,7 +611,8 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
             if (b0 + tid < nblk) {
                 const uint32_t fb = ds[i].first_block;
                 out[fb + j] = best;
-                bseg[fb + j] = bseg_pack((uint32_t)(s0 + i), ds[i].log2b, j);
+                binfo[fb + j] = info_of(ds[i], j);
+                bsize[fb + j] = ds[i].log2b;
             }
             x = xn; i = in; j = jn; r = rn;
         }
@@ -633,7 +642,8 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         if (__float_as_uint(best) == 0x80000000u) best = 0.0f;
         if (valid) {
             out[d.first_block + j] = best;
-            bseg[d.first_block + j] = bseg_pack((uint32_t)(s0 + i), d.log2b, j);
+            binfo[d.first_block + j] = info_of(d, j);
+            bsize[d.first_block + j] = d.log2b;
         }
     }
 }
@@ -706,7 +716,7 @@ __device__ __forceinline__ void block_excl_scan_1024(uint32_t (&v)[N], uint32_t 
         x[i] = wave_scan_add(v[i]);
         if (lane == 63) s[16 * i + wv] = x[i];
     }
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int i = 0; i < N; ++i) {
         const uint32_t y = wave_scan_add(lane < 16 ? s[16 * i + lane] : 0u);   // inclusive over the waves
@@ -714,7 +724,7 @@ __device__ __forceinline__ void block_excl_scan_1024(uint32_t (&v)[N], uint32_t 
         tot[i] = (uint32_t)__builtin_amdgcn_readlane((int)y, 15);
         v[i] = base + x[i] - v[i];
     }
-    __syncthreads();
+    lds_barrier();
 }
 
 // block-wide minimum of lo and maximum of hi (1024 threads); s: 32 words
@@ -722,51 +732,63 @@ __device__ __forceinline__ void block_minmax_1024(uint32_t &lo, uint32_t &hi, ui
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const uint32_t l = ~wave_max_u(~lo), h = wave_max_u(hi);
     if (lane == 0) { s[wv] = l; s[16 + wv] = h; }
-    __syncthreads();
+    lds_barrier();
     lo = s[0]; hi = s[16];
     for (int i = 1; i < 16; ++i) { lo = min(lo, s[i]); hi = max(hi, s[16 + i]); }
-    __syncthreads();
+    lds_barrier();
 }
 
 // Token-budget selection (Sec. 4.2 stage 2; Sec. 6.1 selects 10 % of tokens):
 // blocks are taken in (score desc, block index asc) order while the tokens
 // already taken are fewer than the budget.  The last block taken has the
 // threshold key T: a radix selection over the range of the keys finds it,
-// each pass histogramming the candidates' TOKENS (block sizes, from the block
-// map) into 2048 bins of width 2^s over the keys still in play, so at most
-// three passes narrow the range to T.  Every block above T is taken; the
-// blocks equal to T are taken in block order while the tokens taken among
-// them are fewer than what the budget still needs.  The selected list is
-// written in ascending block order together with each entry's record offset
-// and strategy (for the attention's split setup).  Thread t owns the blocks
-// [t * chunk, (t + 1) * chunk); with REG (chunk <= 16) their keys and map
-// entries stay in registers, else they are read from LDS / the workspace.
+// each pass histogramming the candidates' TOKENS (block sizes) into 2048 bins
+// of width 2^s over the keys still in play, so at most three passes narrow
+// the range to T.  Every block above T is taken; the blocks equal to T are
+// taken in block order while the tokens taken among them are fewer than what
+// the budget still needs (one scan of their tokens).  The selected list is
+// written in ascending block order (one scan of the taken counts) together
+// with each entry's record info, and the list position where each rotation
+// window starts.  Thread t owns the blocks [t * chunk, (t + 1) * chunk); with
+// REG (chunk = 16) their keys and record info stay in registers and the
+// taken ones are a 16-bit mask, else they are read from LDS / the workspace.
+constexpr int TOPK_MAXW = 1024;                            // rotation windows tracked in LDS
+
 template <bool REG>
 __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p, int nb, int ndesc, int budget,
-                                          uint32_t *keys, uint32_t *hist, uint32_t *sbuf) {
+                                          uint32_t *keys, uint32_t *hist, uint32_t *sbuf, int *fbw) {
     const int tid = threadIdx.x;
     const float *sc = ws.score + (uint64_t)p * (ws.score_stride / 4);
-    const uint32_t *bsg = ws.bseg + (uint64_t)p * (ws.bseg_stride / 4);
+    const uint2 *bi = ws.binfo + (uint64_t)p * (ws.binfo_stride / 8);
     int32_t *sel = ws.sel + (uint64_t)p * (ws.sel_stride / 4);
     int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
     uint2 *sinfo = ws.selinfo + (uint64_t)p * (ws.selinfo_stride / 8);
     const int chunk = REG ? TOPK_KPT : (nb + 1023) / 1024;
     const int i0 = min(nb, tid * chunk), i1 = min(nb, i0 + chunk), n_own = i1 - i0;
     const bool in_lds = nb <= TOPK_LDS_KEYS;
-    uint32_t kr[REG ? TOPK_KPT : 1], mr[REG ? TOPK_KPT : 1];
+    // first block of each rotation window (windows past the last segment start
+    // at nb), loaded now, published by the first barrier
+    const int segs_per_win = g.W / SEG;
+    const Desc *gd = g.desc_of(p);
+    const int nwl = min(g.nw, TOPK_MAXW);
+    for (int w = tid; w < nwl; w += 1024) {
+        const int s0 = w * segs_per_win;
+        fbw[w] = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
+    }
+    const uint8_t *bz = ws.bsize + (uint64_t)p * ws.bsize_stride;
+    uint32_t kr[REG ? TOPK_KPT : 1];
+    uint32_t zr[REG ? TOPK_KPT / 4 : 1];                  // log2 block sizes, four per word
     uint32_t kmin = 0xffffffffu, kmax = 0u;
     if (REG) {
         const float4 *s4 = (const float4 *)(sc + i0);
-        const uint4 *m4 = (const uint4 *)(bsg + i0);
+        const uint4 z4 = n_own > 0 ? *(const uint4 *)(bz + i0) : make_uint4(0u, 0u, 0u, 0u);
+        zr[0] = z4.x; zr[1] = z4.y; zr[2] = z4.z; zr[3] = z4.w;
 #pragma unroll
         for (int q = 0; q < TOPK_KPT / 4; ++q) {
             float4 f = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            uint4 m = make_uint4(0u, 0u, 0u, 0u);
-            if (4 * q < n_own) { f = s4[q]; m = m4[q]; }
-            const float fv[4] = {f.x, f.y, f.z, f.w};
-            const uint32_t mv[4] = {m.x, m.y, m.z, m.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) { kr[4 * q + e] = score_key(fv[e]); mr[4 * q + e] = mv[e]; }
+            if (4 * q < n_own) f = s4[q];
+            kr[4 * q] = score_key(f.x); kr[4 * q + 1] = score_key(f.y);
+            kr[4 * q + 2] = score_key(f.z); kr[4 * q + 3] = score_key(f.w);
         }
 #pragma unroll
         for (int j = 0; j < TOPK_KPT; ++j)
@@ -779,15 +801,13 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
             kmax = max(kmax, key);
         }
     }
-    auto key_at = [&](int j) -> uint32_t {                 // j-th owned key (j < n_own)
-        if (REG) return kr[j];
-        return in_lds ? keys[i0 + j] : score_key(sc[i0 + j]);
-    };
-    auto map_at = [&](int j) -> uint32_t { return REG ? mr[j] : bsg[i0 + j]; };
-    auto tokens = [](uint32_t m) -> uint32_t { return 1u << bseg_log2b(m); };
+    auto key_at = [&](int j) -> uint32_t { return in_lds ? keys[i0 + j] : score_key(sc[i0 + j]); };   // !REG
+    // tokens of owned block j: 2^(log2 size), from the registers (REG) or the array
+    auto tok_reg = [&](int j) -> uint32_t { return 1u << ((zr[j >> 2] >> (8 * (j & 3))) & 7u); };
+    auto tok_mem = [&](int j) -> uint32_t { return 1u << (bz[i0 + j] & 7u); };
     // two histograms in turn: a pass zeroes the next one while it reads its own
     for (int i = tid; i < TOPK_BINS; i += 1024) hist[i] = 0;
-    block_minmax_1024(kmin, kmax, sbuf);                          // (its barriers publish the zeros)
+    block_minmax_1024(kmin, kmax, sbuf);                          // (its barriers publish the zeros and fbw)
     uint32_t base = kmin, span = kmax - kmin;                     // candidates: [base, base + span]
     uint32_t rem = (uint32_t)budget;                               // tokens still to take
     const int lane = tid & 63, wv = tid >> 6;
@@ -799,29 +819,29 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
 #pragma unroll
             for (int j = 0; j < TOPK_KPT; ++j) {
                 const uint32_t d = kr[j] - base;
-                if (j < n_own && kr[j] >= base && d <= span) atomicAdd(&hc[d >> sh], tokens(mr[j]));
+                if (j < n_own && kr[j] >= base && d <= span) atomicAdd(&hc[d >> sh], tok_reg(j));
             }
         } else {
             for (int j = 0; j < n_own; ++j) {
                 const uint32_t key = key_at(j), d = key - base;
-                if (key >= base && d <= span) atomicAdd(&hc[d >> sh], tokens(map_at(j)));
+                if (key >= base && d <= span) atomicAdd(&hc[d >> sh], tok_mem(j));
             }
         }
-        __syncthreads();
+        lds_barrier();
         // bins from the top: thread t owns bins 2047 - 2t and 2046 - 2t
         const uint32_t h0 = hc[TOPK_BINS - 1 - 2 * tid], h1 = hc[TOPK_BINS - 2 - 2 * tid];
         hn[2 * tid] = 0;
         hn[2 * tid + 1] = 0;
         const uint32_t x = wave_scan_add(h0 + h1);
         if (lane == 63) sbuf[wv] = x;
-        __syncthreads();
+        lds_barrier();
         uint32_t above = x - (h0 + h1);
         above += sum_below(sbuf, wv);
         if (above < rem && above + h0 + h1 >= rem) {
             if (above + h0 >= rem) { sbuf[32] = TOPK_BINS - 1 - 2 * tid; sbuf[33] = rem - above; }
             else { sbuf[32] = TOPK_BINS - 2 - 2 * tid; sbuf[33] = rem - above - h0; }
         }
-        __syncthreads();
+        lds_barrier();
         const uint32_t b = sbuf[32];
         rem = sbuf[33];
         base += b << sh;
@@ -829,87 +849,93 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
         span = min(span - (b << sh), width);
         if (sh == 0) break;
     }
-    // T = base; rem = tokens the budget still needs among the blocks equal to T
-    const uint32_t T = base, need_eq = rem;
-    uint32_t cnt[3] = {0u, 0u, 0u};                        // greater blocks, equal blocks, equal tokens
-    if (budget > 0) {
+    // T = base; need = tokens the budget still needs among the blocks equal to T
+    const uint32_t T = base, need = rem;
+    uint32_t v[1] = {0u}, tot[1];
+    if (budget > 0) {                                      // this thread's tokens equal to T
         if (REG) {
 #pragma unroll
-            for (int j = 0; j < TOPK_KPT; ++j)
-                if (j < n_own) {
-                    cnt[0] += kr[j] > T;
-                    if (kr[j] == T) { cnt[1] += 1u; cnt[2] += tokens(mr[j]); }
-                }
+            for (int j = 0; j < TOPK_KPT; ++j) v[0] += (j < n_own && kr[j] == T) ? tok_reg(j) : 0u;
+        } else {
+            for (int j = 0; j < n_own; ++j) v[0] += key_at(j) == T ? tok_mem(j) : 0u;
+        }
+    }
+    block_excl_scan_1024<1>(v, tot, sbuf);                 // -> equal tokens before this thread
+    // taken blocks: above T, or equal to T while the equal tokens before are below need
+    uint32_t tmask = 0, tcnt = 0;
+    if (budget > 0) {
+        uint32_t acc = v[0];
+        if (REG) {
+#pragma unroll
+            for (int j = 0; j < TOPK_KPT; ++j) {
+                const bool eq = j < n_own && kr[j] == T;
+                const bool t = j < n_own && (kr[j] > T || (eq && acc < need));
+                acc += eq ? tok_reg(j) : 0u;
+                tmask |= t ? (1u << j) : 0u;
+            }
+            tcnt = (uint32_t)__popc(tmask);
         } else {
             for (int j = 0; j < n_own; ++j) {
                 const uint32_t key = key_at(j);
-                cnt[0] += key > T;
-                if (key == T) { cnt[1] += 1u; cnt[2] += tokens(map_at(j)); }
+                tcnt += (key > T || (key == T && acc < need)) ? 1u : 0u;
+                acc += key == T ? tok_mem(j) : 0u;
             }
         }
     }
-    // first block of each rotation window (windows past the last segment start at nb)
-    int *fbw = (int *)hist;
-    const int segs_per_win = g.W / SEG;
-    const Desc *gd = g.desc_of(p);
-    const int nwl = min(g.nw, TOPK_BINS);                  // windows tracked in LDS
-    for (int w = tid; w < nwl; w += 1024) {
-        const int s0 = w * segs_per_win;
-        fbw[w] = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
-    }
-    const uint32_t own_eq_tok = cnt[2];
-    uint32_t tot[3];
-    block_excl_scan_1024<3>(cnt, tot, sbuf);               // (its barriers publish fbw)
-    // the equal blocks taken are the first E of them in block order: the
-    // thread whose equal tokens cross need_eq counts its own taken ones
-    if (budget > 0 && cnt[2] < need_eq && cnt[2] + own_eq_tok >= need_eq) {
-        uint32_t acc = cnt[2], taken = 0;
-        for (int j = 0; j < n_own; ++j)
-            if (key_at(j) == T) { taken += acc < need_eq; acc += tokens(map_at(j)); }
-        sbuf[40] = cnt[1] + taken;
-    }
-    __syncthreads();
-    const uint32_t E = budget > 0 ? sbuf[40] : 0u;
-    const int k = budget > 0 ? (int)(tot[0] + E) : 0;      // blocks selected
-    const uint32_t pos0 = cnt[0] + min(cnt[1], E);
-    // write the selected list; a window starting inside [i0, i1) records the
-    // list position reached there (windows starting at nb record k)
-    int wn = 0;
-    while (wn < nwl && fbw[wn] < i0) ++wn;
-    int nextfb = wn < nwl ? fbw[wn] : 0x7fffffff;          // next window start, kept in a register
-    uint32_t pos = pos0, acc = cnt[2];
-    const int maxd = g.max_desc;
-    auto emit = [&](int j, uint32_t key, uint32_t m) {
-        const int i = i0 + j;
-        while (nextfb == i) {
-            wsel[wn++] = (int)pos;
-            nextfb = wn < nwl ? fbw[wn] : 0x7fffffff;
-        }
-        if (budget > 0) {
-            bool take_it = key > T;
-            if (key == T) { take_it = acc < need_eq; acc += tokens(m); }
-            if (take_it && pos < (uint32_t)nb) {
-                sel[pos] = i;
-                const Desc d = gd[min(bseg_seg(m), (uint32_t)maxd - 1)];
-                const uint32_t goff = d.tok_off + (uint32_t)(bseg_j(m) << d.log2b) *
-                                                      (uint32_t)(2 * tok_vec_bytes(d.r, d.log2g, g.trunc, g.fp8));
-                sinfo[pos] = make_uint2(goff, ((uint32_t)d.r << 8) | ((uint32_t)d.log2g << 16) |
-                                                  ((uint32_t)d.log2b << 20));
-            }
-            pos += take_it ? 1u : 0u;
-        }
-    };
+    const uint32_t eq_before = v[0];
+    v[0] = tcnt;
+    block_excl_scan_1024<1>(v, tot, sbuf);                 // -> list position of this thread's first
+    const uint32_t pos0 = v[0];
+    const int k = budget > 0 ? (int)tot[0] : 0;            // blocks selected
     if (REG) {
+        // the record info of the taken blocks only: all loads issued, then the stores
+        uint2 br[TOPK_KPT];
 #pragma unroll
-        for (int j = 0; j < TOPK_KPT; ++j)
-            if (j < n_own) emit(j, kr[j], mr[j]);
+        for (int j = 0; j < TOPK_KPT; ++j) br[j] = ((tmask >> j) & 1u) ? bi[i0 + j] : make_uint2(0u, 0u);
+        uint32_t pos = pos0;
+#pragma unroll
+        for (int j = 0; j < TOPK_KPT; ++j) {
+            if ((tmask >> j) & 1u) { sel[pos] = i0 + j; sinfo[pos] = br[j]; }
+            pos += (tmask >> j) & 1u;
+        }
+        // window starts: the position of the first block at or after each
+        // start, from the owning thread's first position and taken mask
+        uint32_t *tpos = hist, *tmk = hist + 1024;          // (the histograms are no longer needed)
+        tpos[tid] = pos0;
+        tmk[tid] = tmask;
+        lds_barrier();
+        for (int w = tid; w < nwl; w += 1024) {
+            const int f = fbw[w];
+            if (f >= nb) { wsel[w] = k; continue; }
+            const int t = f / TOPK_KPT, off = f % TOPK_KPT;
+            wsel[w] = (int)(tpos[t] + (uint32_t)__popc(tmk[t] & ((1u << off) - 1u)));
+        }
     } else {
-        for (int j = 0; j < n_own; ++j) emit(j, key_at(j), map_at(j));
+        // the keys again, in order, with the window starts met on the way
+        int wn = 0;
+        while (wn < nwl && fbw[wn] < i0) ++wn;
+        int nextfb = wn < nwl ? fbw[wn] : 0x7fffffff;
+        uint32_t pos = pos0, acc = eq_before;
+        for (int j = 0; j < n_own; ++j) {
+            const int i = i0 + j;
+            while (nextfb == i) {
+                wsel[wn++] = (int)pos;
+                nextfb = wn < nwl ? fbw[wn] : 0x7fffffff;
+            }
+            if (budget > 0) {
+                const uint32_t key = key_at(j);
+                const bool t = key > T || (key == T && acc < need);
+                acc += key == T ? tok_mem(j) : 0u;
+                if (t && pos < (uint32_t)nb) { sel[pos] = i; sinfo[pos] = bi[i]; }
+                pos += t ? 1u : 0u;
+            }
+        }
+        lds_barrier();
+        for (int w = tid; w < nwl; w += 1024)              // windows starting at nb
+            if (fbw[w] >= nb) wsel[w] = k;
     }
-    if (tid == 1023)
-        for (; wn < nwl; ++wn) wsel[wn] = k;
     if (g.nw > nwl) {                                      // more windows than LDS slots
-        __syncthreads();
+        __syncthreads();                                   // (sel from every thread)
         for (int w = nwl + tid; w < g.nw; w += 1024) {
             const int s0 = w * segs_per_win;
             const int fb = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
@@ -925,6 +951,7 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
     extern __shared__ __align__(16) uint32_t keys[];            // [min(nb, TOPK_LDS_KEYS)] when staged
     __shared__ uint32_t hist[2 * TOPK_BINS];
     __shared__ uint32_t sbuf[64];
+    __shared__ int fbw[TOPK_MAXW];
     const int p = blockIdx.x;
     const PairMeta meta = *g.meta_of(p);
     const int nb = pair_nblocks(g, p, meta);
@@ -937,8 +964,8 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
         const long long bb = ((long long)ntok * g.sel_num + g.sel_den - 1) / g.sel_den;
         budget = (int)(bb < 1 ? 1 : (bb > ntok ? ntok : bb));
     }
-    if (nb <= 1024 * TOPK_KPT) topk_body<true>(g, ws, p, nb, ndesc, budget, keys, hist, sbuf);
-    else topk_body<false>(g, ws, p, nb, ndesc, budget, keys, hist, sbuf);
+    if (nb <= 1024 * TOPK_KPT) topk_body<true>(g, ws, p, nb, ndesc, budget, keys, hist, sbuf, fbw);
+    else topk_body<false>(g, ws, p, nb, ndesc, budget, keys, hist, sbuf, fbw);
 }
 
 // ------------------------------------------------------------------ attention
@@ -946,20 +973,26 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
 // pair's token arena, and r << 8 | log2g << 16 | log2b << 20
 typedef uint2 BlkInfo;
 
-// split s of a pair: window w, selected-list range [e0, e1); w = -2 past the end.
-// The list bounds are clamped to [0, lim] (the list's capacity), so that no
-// workspace content can send an index outside it.
-__device__ __forceinline__ void split_of(const int32_t *wsel, int nw, int s, int lim, int &w_out, int &e0, int &e1,
-                                         int &total) {
+// split s of a pair: window w and its entries e0, e0 + stride, e0 + 2 stride,
+// ... (cnt of them); w = -2 past the end.  A window's n selected entries go
+// to ceil(n / SPLIT_BLOCKS) splits dealt round-robin, so every split of a
+// window holds the same mix of 16-, 8- and 4-token blocks (the list is in
+// block order, where blocks of one size cluster), which balances the
+// splits' tokens.  The list bounds are clamped to [0, lim] (the list's
+// capacity), so that no workspace content can send an index outside it.
+__device__ __forceinline__ void split_of(const int32_t *wsel, int nw, int s, int lim, int &w_out, int &e0,
+                                         int &stride, int &cnt, int &total) {
     int acc = 0;
-    w_out = -2; e0 = e1 = 0;
+    w_out = -2; e0 = 0; stride = 1; cnt = 0;
     for (int w = 0; w < nw; ++w) {
         const int a = min(max(wsel[w], 0), lim), b = min(max(wsel[w + 1], a), lim);
         const int nsp = (b - a + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS;
         if (w_out == -2 && s < acc + nsp) {
+            const int k = s - acc;
             w_out = w;
-            e0 = a + (s - acc) * SPLIT_BLOCKS;
-            e1 = min(b, e0 + SPLIT_BLOCKS);
+            e0 = a + k;
+            stride = nsp;
+            cnt = (b - a - k + nsp - 1) / nsp;
         }
         acc += nsp;
     }
@@ -970,9 +1003,17 @@ constexpr int CH_TOK = 64;           // tokens per chunk (one wave, lane per tok
 constexpr int KT_STRIDE = 136;       // u16 per token row of the K tile (128 + 8 pad)
 constexpr int VT_STRIDE = 68;        // u16 per channel row of the V tile (64 + 4 pad)
 constexpr int TILE_BYTES = 17408;    // max(64 * 272, 128 * 136)
-constexpr int ATTN_NWV = 2;          // waves per attention workgroup
+#ifndef MOSAIC_ATTN_WAVES
+#define MOSAIC_ATTN_WAVES 2
+#endif
+constexpr int ATTN_NWV = MOSAIC_ATTN_WAVES;  // waves per attention workgroup
+#ifndef MOSAIC_ATTN_WPE
+#define MOSAIC_ATTN_WPE 2
+#endif
+#define ATTN_WPE MOSAIC_ATTN_WPE             // waves per SIMD the attention's registers allow
 // block table [SPLIT_BLOCKS] + per-wave class counts (16-byte multiple)
-constexpr int ATTN_HDR_BYTES = (8 * SPLIT_BLOCKS + 2 * 4 * 4 + 15) / 16 * 16;
+constexpr int ATTN_HDR_BYTES = (8 * SPLIT_BLOCKS + ATTN_NWV * 4 * 4 + 15) / 16 * 16;
+static_assert(SPLIT_BLOCKS <= 64 * ATTN_NWV, "one setup thread per block of a split");
 
 // x = hi + lo with hi, lo in the MFMA's 16-bit type (round to nearest even);
 // hi + lo carries x to ~16 (bf16) or ~22 (fp16) significant bits
@@ -1130,7 +1171,7 @@ __device__ __forceinline__ void dense_put(const uint8_t *vals, uint32_t addr) {
 }
 
 template <int DT, int GP, int RMAX, bool FR, bool F8>
-__global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(64 * ATTN_NWV) __attribute__((amdgpu_waves_per_eu(ATTN_WPE)))
 k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     using M8 = typename Mma<DT>::v8;
     constexpr int NWV = ATTN_NWV;
@@ -1153,8 +1194,8 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     int nf, prov, nbuf;
     pair_ndesc(meta, nf, prov, nbuf);
     const int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
-    int w, e0, e1, total;
-    split_of(wsel, g.nw, s, ws.max_blocks, w, e0, e1, total);
+    int w, e0, estride, nbk, total;
+    split_of(wsel, g.nw, s, ws.max_blocks, w, e0, estride, nbk, total);
     int32_t *tag = ws.tag + (uint64_t)p * (ws.tag_stride / 4);
     float *part = ws.part + (uint64_t)p * (ws.part_stride / 4) + (uint64_t)s * GP * (D + 2);
     const bool is_buf = (w == -2) && (s == total) && nbuf > 0;
@@ -1219,7 +1260,6 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     // ---- split setup: one thread per selected block; blocks ordered by size
     // (16, then 8, then 4; ascending index inside a size), so every block
     // starts at a multiple of its size and none straddles a 64-token chunk
-    const int nbk = e1 - e0;
     bool all16;                                     // every record of the split 4-byte aligned (granule loads)
     bool dense = false;                             // every block keeps all D channels (RMAX = D kernels)
     int rsplit;                                     // largest kept count in the split
@@ -1227,7 +1267,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         const bool on = tid < nbk;
         uint32_t goff = 0; int r = 0, l2g = 0, l2b = 2;
         if (on) {                                   // the entry's record offset and strategy (top-k wrote them)
-            const uint2 si = ws.selinfo[(uint64_t)p * (ws.selinfo_stride / 8) + e0 + tid];
+            const uint2 si = ws.selinfo[(uint64_t)p * (ws.selinfo_stride / 8) + e0 + tid * estride];
             r = (int)((si.y >> 8) & 0xffu); l2g = (int)((si.y >> 16) & 3u); l2b = (int)min(max((si.y >> 20) & 7u, 2u), 4u);
             goff = min(si.x, (uint32_t)g.tok_stride);      // keeps every read inside the arena
         }
@@ -1247,10 +1287,16 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         if (RMAX >= D && !F8) dense = __syncthreads_and(!on || (l2g == 0 && r == D && (goff & 15u) == 0));
         if (on) {
             const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-            const int c16 = wcnt[0] + wcnt[4], c8 = wcnt[1] + wcnt[5];
+            int c16 = 0, c8 = 0, before = 0;
+#pragma unroll
+            for (int x = 0; x < NWV; ++x) {
+                c16 += wcnt[x * 4];
+                c8 += wcnt[x * 4 + 1];
+                before += x < wave ? wcnt[x * 4 + cls] : 0;
+            }
             const int base = cls == 0 ? 0 : (cls == 1 ? c16 : c16 + c8);
             const uint64_t mc = cls == 0 ? m0 : (cls == 1 ? m1 : m2);
-            const int pos = base + (wave ? wcnt[cls] : 0) + __popcll(mc & below);
+            const int pos = base + before + __popcll(mc & below);
             blk[pos] = make_uint2(goff, ((uint32_t)r << 8) | ((uint32_t)l2g << 16) | ((uint32_t)l2b << 20));
         }
     }
@@ -1280,10 +1326,16 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     }
     __syncthreads();
     // uniform counts (scalar registers)
-    const int n16 = __builtin_amdgcn_readfirstlane(wcnt[0] + wcnt[4]);
-    const int n8 = __builtin_amdgcn_readfirstlane(wcnt[1] + wcnt[5]);
-    const int n4 = __builtin_amdgcn_readfirstlane(wcnt[2] + wcnt[6]);
-    rsplit = __builtin_amdgcn_readfirstlane(max(wcnt[3], wcnt[7]));
+    int n16 = 0, n8 = 0, n4 = 0;
+    rsplit = 0;
+#pragma unroll
+    for (int x = 0; x < NWV; ++x) {
+        n16 += wcnt[x * 4]; n8 += wcnt[x * 4 + 1]; n4 += wcnt[x * 4 + 2]; rsplit = max(rsplit, wcnt[x * 4 + 3]);
+    }
+    n16 = __builtin_amdgcn_readfirstlane(n16);
+    n8 = __builtin_amdgcn_readfirstlane(n8);
+    n4 = __builtin_amdgcn_readfirstlane(n4);
+    rsplit = __builtin_amdgcn_readfirstlane(rsplit);
     const int T16 = 16 * n16, T8 = T16 + 8 * n8, T = T8 + 4 * n4;
     const int nch = (T + CH_TOK - 1) / CH_TOK;
     const uint8_t *tokg = g.tok_of(p);
@@ -1490,14 +1542,14 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         else chunks(IntC<RMAX / 8>{});
     }
     // ---- merge the waves' (m, l, acc) and write the split's partial
-    __syncthreads();
+    lds_barrier();
     float *mrg = (float *)(wbase + wave * TILE_BYTES);      // [16][D + 2]
     if (q4 == 0) { mrg[l16 * (D + 2)] = m_run; mrg[l16 * (D + 2) + 1] = l_run; }
 #pragma unroll
     for (int ct = 0; ct < 8; ++ct)
 #pragma unroll
         for (int r = 0; r < 4; ++r) mrg[(q4 * 4 + r) * (D + 2) + 2 + ct * 16 + l16] = acc_o[ct][r];
-    __syncthreads();
+    lds_barrier();
     // the merged (max, sum, accumulator) of the split, in the window's rotated
     // space (the combine rotates each window's sum back once)
     for (int i = tid; i < GP * D; i += NWV * 64) {
@@ -1537,9 +1589,15 @@ __global__ void __launch_bounds__(CMB_THREADS) k_combine(Geom g, WsGeom ws, floa
     constexpr int PS = GP * (D + 2);
     constexpr int NPART = CMB_THREADS / (GP * CMB_COLS);     // threads per output in the rotation
     constexpr int CPP = D / NPART;                            // channels per thread
+    constexpr int NE = GP * D / CMB_THREADS;                  // merged elements per thread
+    constexpr int CH = 16;                                    // splits merged per round trip
+    constexpr int MAXW = 1024;                                // window bounds staged in LDS
+    static_assert(CMB_COLS * D / 4 == 2 * CMB_THREADS, "two 16-byte pieces of R_v^T rows per thread");
     __shared__ float am[GP][D];                               // merged accumulator of the current window
     __shared__ float rv[CMB_COLS][D + 4];                     // R_v[c][j0 + jj] as rows jj
-    __shared__ float wml[2][GP];                              // the window's merged max and sum
+    __shared__ float sm[CH][GP], sl[CH][GP];                  // staged split maxima and sums
+    __shared__ float wml[2][GP], wsc[GP];                     // the window's running max, sum, rescale
+    __shared__ int wb[MAXW + 1];                              // first list entry of each window
     const int p = blockIdx.x, j0 = blockIdx.y * CMB_COLS, tid = threadIdx.x;
     const int oi = tid / NPART, part_i = tid % NPART;         // output (head, column) and channel part
     const int oh = oi / CMB_COLS, oj = oi % CMB_COLS;
@@ -1549,13 +1607,17 @@ __global__ void __launch_bounds__(CMB_THREADS) k_combine(Geom g, WsGeom ws, floa
     const int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
     const float *part = ws.part + (uint64_t)p * (ws.part_stride / 4);
     const int lim = ws.max_blocks;
+    const int nwl = min(g.nw, MAXW);
+    for (int w = tid; w <= nwl; w += CMB_THREADS) wb[w] = min(max(wsel[w], 0), lim);
+    lds_barrier();
     float M = -INFINITY, Lsum = 0.0f, o = 0.0f;               // running merge of output (oh, j0 + oj)
     int s0 = 0;
     // windows in order, then the buffer's split (w == nw)
     for (int w = 0; w <= g.nw; ++w) {
         int nsp;
         if (w < g.nw) {
-            const int a = min(max(wsel[w], 0), lim), b = min(max(wsel[w + 1], a), lim);
+            const int a = w < nwl ? wb[w] : min(max(wsel[w], 0), lim);
+            const int b = w + 1 <= nwl ? max(wb[w + 1], a) : min(max(wsel[w + 1], a), lim);
             nsp = (b - a + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS;
         } else {
             nsp = nbuf > 0 ? 1 : 0;
@@ -1563,29 +1625,66 @@ __global__ void __launch_bounds__(CMB_THREADS) k_combine(Geom g, WsGeom ws, floa
         if (nsp == 0) continue;
         if (s0 + nsp > ws.max_splits) break;                  // (cannot happen: the grid had this many)
         const bool rot = w < g.nw && g.rotated;
-        if (rot) {                                            // stage R_v[c][j0 .. j0 + 15] (rows of R_v^T)
-            const float *rvt = g.rot_of(p, w) + D * D + (uint64_t)j0 * D;
-            for (int i = tid; i < CMB_COLS * D / 4; i += CMB_THREADS) {
-                const int jj = i / (D / 4), c4 = i % (D / 4);
-                *(float4 *)&rv[jj][4 * c4] = *(const float4 *)(rvt + (uint64_t)jj * D + 4 * c4);
-            }
+        float4 rq0 = make_float4(0.0f, 0.0f, 0.0f, 0.0f), rq1 = rq0;   // R_v[c][j0 .. j0 + 15], loaded now
+        if (rot) {
+            const float4 *rvt = (const float4 *)(g.rot_of(p, w) + D * D + (uint64_t)j0 * D);
+            rq0 = rvt[tid];
+            rq1 = rvt[tid + CMB_THREADS];
         }
-        // merge the window's splits: element (h, c) per thread
-        for (int i = tid; i < GP * D; i += CMB_THREADS) {
-            const int h = i / D, c = i % D;
-            float Mx = -INFINITY;
-            for (int t = 0; t < nsp; ++t) Mx = fmaxf(Mx, part[(uint64_t)(s0 + t) * PS + h]);
-            float A = 0.0f, Ls = 0.0f;
-            for (int t = 0; t < nsp; ++t) {
-                const float *ps = part + (uint64_t)(s0 + t) * PS;
-                const float f = ps[h] == -INFINITY ? 0.0f : __expf(ps[h] - Mx);
-                A += ps[2 * GP + h * D + c] * f;
-                Ls += ps[GP + h] * f;
+        float A[NE];
+#pragma unroll
+        for (int e = 0; e < NE; ++e) A[e] = 0.0f;
+        for (int c0 = 0; c0 < nsp; c0 += CH) {
+            const int n = min(CH, nsp - c0);
+            // one round trip: this thread's accumulator elements of the n
+            // splits, and the splits' maxima and sums into LDS
+            float av[CH][NE];
+#pragma unroll
+            for (int j = 0; j < CH; ++j)
+#pragma unroll
+                for (int e = 0; e < NE; ++e) {
+                    const int i = tid + e * CMB_THREADS;
+                    av[j][e] = j < n ? part[(uint64_t)(s0 + c0 + j) * PS + 2 * GP + i] : 0.0f;
+                }
+            if (tid < n * GP) {
+                const float *ps = part + (uint64_t)(s0 + c0 + tid / GP) * PS;
+                sm[tid / GP][tid % GP] = ps[tid % GP];
+                sl[tid / GP][tid % GP] = ps[GP + tid % GP];
             }
-            am[h][c] = A;
-            if (c == 0) { wml[0][h] = Mx; wml[1][h] = Ls; }
+            if (c0 == 0 && tid < GP) { wml[0][tid] = -INFINITY; wml[1][tid] = 0.0f; }
+            lds_barrier();
+            if (tid < GP) {                                   // new running max, rescale, sum
+                const float Mo = wml[0][tid];
+                float Mc = Mo;
+                for (int j = 0; j < n; ++j) Mc = fmaxf(Mc, sm[j][tid]);
+                const float sc = (Mo == -INFINITY || Mc == -INFINITY) ? 0.0f : __expf(Mo - Mc);
+                float Ls = wml[1][tid] * sc;
+                for (int j = 0; j < n; ++j) Ls += sm[j][tid] == -INFINITY ? 0.0f : sl[j][tid] * __expf(sm[j][tid] - Mc);
+                wml[0][tid] = Mc; wml[1][tid] = Ls; wsc[tid] = sc;
+            }
+            lds_barrier();
+#pragma unroll
+            for (int e = 0; e < NE; ++e) {
+                const int h = (tid + e * CMB_THREADS) / D;
+                const float Mc = wml[0][h];
+                float a = A[e] * wsc[h];
+#pragma unroll
+                for (int j = 0; j < CH; ++j)
+                    if (j < n && sm[j][h] != -INFINITY) a = fmaf(av[j][e], __expf(sm[j][h] - Mc), a);
+                A[e] = a;
+            }
+            lds_barrier();                                    // sm / sl / wml are rewritten next
         }
-        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+            const int i = tid + e * CMB_THREADS;
+            am[i / D][i % D] = A[e];
+        }
+        if (rot) {                                            // (rows of R_v^T: 16 x 32 pieces)
+            *(float4 *)&rv[tid / (D / 4)][4 * (tid % (D / 4))] = rq0;
+            *(float4 *)&rv[(tid + CMB_THREADS) / (D / 4)][4 * ((tid + CMB_THREADS) % (D / 4))] = rq1;
+        }
+        lds_barrier();
         float y = 0.0f;
         if (rot) {
 #pragma unroll 8
@@ -1603,7 +1702,7 @@ __global__ void __launch_bounds__(CMB_THREADS) k_combine(Geom g, WsGeom ws, floa
             Lsum = Lsum * a + wl * b;
             M = mn;
         }
-        __syncthreads();                                      // am, rv and wml are rewritten next
+        lds_barrier();                                        // am, rv and wml are rewritten next
         s0 += nsp;
     }
     if (part_i == 0 && oh < g.G) out[((uint64_t)p * g.G + oh) * D + j0 + oj] = (Lsum > 0.0f) ? o / Lsum : 0.0f;

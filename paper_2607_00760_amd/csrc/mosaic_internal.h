@@ -10,7 +10,10 @@ constexpr int D = 128;        // head dim
 constexpr int SEG = 64;       // strategy segment (tokens)
 constexpr int UBUF = 32;      // update buffer (tokens)
 constexpr int WAVE = 64;
-constexpr int SPLIT_BLOCKS = 128;  // selected blocks per split-K partition
+#ifndef MOSAIC_SPLIT_BLOCKS
+#define MOSAIC_SPLIT_BLOCKS 64
+#endif
+constexpr int SPLIT_BLOCKS = MOSAIC_SPLIT_BLOCKS;  // selected blocks per split-K partition
 constexpr int SCORE_SEGS = 128;    // segments per block-scoring workgroup (one launch round)
 
 struct Desc {                 // 16-byte segment descriptor (layout is part of the ABI)
@@ -63,20 +66,18 @@ struct WsGeom {               // decode workspace
     int32_t *wsel; uint64_t wsel_stride;    // [nw + 2]
     float *part; uint64_t part_stride;      // [max_splits][GP * (D + 2)]
     int32_t *tag; uint64_t tag_stride;      // [max_splits]
-    uint32_t *bseg; uint64_t bseg_stride;   // [max_blocks]: block map, bseg_pack
-    uint2 *selinfo; uint64_t selinfo_stride; // [max_blocks]: per selected entry {token-arena
-                                             //   byte offset, r << 8 | log2g << 16 | log2b << 20}
+    uint2 *binfo; uint64_t binfo_stride;    // [max_blocks]: per block, blk_info
+    uint8_t *bsize; uint64_t bsize_stride;  // [max_blocks]: per block, log2 of its token count
+    uint2 *selinfo; uint64_t selinfo_stride; // [max_blocks]: blk_info of each selected entry
     int max_blocks, max_splits;
 };
 
-// block map entry of block b of a pair: its segment, log2 of its size (2..4)
-// and its index inside the segment
-__host__ __device__ __forceinline__ uint32_t bseg_pack(uint32_t seg, int log2b, int j) {
-    return (seg << 6) | ((uint32_t)(log2b - 2) << 4) | (uint32_t)j;
+// a block's record: its byte offset in the pair's token arena, and
+// r << 8 | log2 g << 16 | log2 B << 20
+__host__ __device__ __forceinline__ uint2 blk_info(uint32_t tok_off, int r, int log2g, int log2b) {
+    return make_uint2(tok_off, ((uint32_t)r << 8) | ((uint32_t)log2g << 16) | ((uint32_t)log2b << 20));
 }
-__host__ __device__ __forceinline__ uint32_t bseg_seg(uint32_t e) { return e >> 6; }
-__host__ __device__ __forceinline__ int bseg_log2b(uint32_t e) { return (int)((e >> 4) & 3u) + 2; }
-__host__ __device__ __forceinline__ int bseg_j(uint32_t e) { return (int)(e & 15u); }
+__host__ __device__ __forceinline__ uint32_t blk_tokens(uint32_t info) { return 1u << ((info >> 20) & 7u); }
 
 // ---------------------------------------------------------------- elements
 __device__ __forceinline__ float h2f(uint16_t h, int dtype) {
@@ -128,6 +129,14 @@ __device__ __forceinline__ uint32_t f2e4m3(float f) {
 }
 
 // ---------------------------------------------------------------- wave helpers
+// Workgroup barrier for data exchanged through LDS only: it waits for the
+// wave's own LDS (and scalar memory) operations, not for its outstanding
+// global loads and stores, so loads issued before it stay in flight across
+// it (__syncthreads also waits for those, as its fence orders global memory).
+// Only for uniform control flow.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+
 __device__ __forceinline__ float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, WAVE); }
 
 // data-parallel-primitive lane move: lane i reads lane i - shift (row shifts),
