@@ -211,6 +211,22 @@ mosaic_status mosaic_append(mosaic_cache *cache, const void *k_new, const void *
 mosaic_status mosaic_decode_attention(mosaic_cache *cache, const void *q, float *out, float sm_scale,
                                       void *ws, size_t ws_bytes, void *stream);
 
+/* mosaic_decode_attention for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same step and output, with the decode workspace taken
+ * from a fixed library-owned device buffer of MOSAIC_NOALLOC_SCRATCH_BYTES
+ * per GPU instead of a caller's.  The buffer is reserved when the library's
+ * code is loaded on a GPU and held until the process ends; the call itself
+ * allocates nothing.  Every call on one GPU shares that GPU's buffer: calls
+ * that overlap on a GPU (other streams or threads) race and must be ordered
+ * by the caller.  The cache must be bound to memory of the current device.
+ * Errors: as mosaic_decode_attention; UNSUPPORTED when the cache's decode
+ * workspace (mosaic_workspace_bytes, MOSAIC_OP_DECODE) exceeds the buffer;
+ * HIP if the buffer's address cannot be obtained. */
+#define MOSAIC_NOALLOC_SCRATCH_BYTES (64u << 20)
+mosaic_status mosaic_decode_attention_noalloc(mosaic_cache *cache, const void *q, float *out, float sm_scale,
+                                              void *stream);
+
 /* Rotation matrices computed from the cache on the GPU (Sec. 2.3; Sec. 5.2:
  * once the KV cache exists, the SVD rotation of each window's K matrix and of
  * its V matrix is computed; the paper does this on the host).  For every

@@ -17,7 +17,7 @@ EXPORTED = [
     "mosaic_compress", "mosaic_append", "mosaic_decode_attention", "mosaic_dense_workspace_bytes",
     "mosaic_dense_decode_attention", "mosaic_cache_stats", "mosaic_seq_tokens", "mosaic_last_error",
     "mosaic_set_timing", "mosaic_decode_timing", "mosaic_rotation_workspace_bytes", "mosaic_compute_rotations",
-    "mosaic_reorder_workspace_bytes", "mosaic_reorder_rotations",
+    "mosaic_reorder_workspace_bytes", "mosaic_reorder_rotations", "mosaic_decode_attention_noalloc",
 ]
 
 
@@ -83,6 +83,7 @@ def load() -> C.CDLL:
         L.mosaic_compress.argtypes = [vp, vp, vp, C.c_int64, C.POINTER(C.c_int32), vp, vp, vp, sz, vp]
         L.mosaic_append.argtypes = [vp, vp, vp, vp]
         L.mosaic_decode_attention.argtypes = [vp, vp, vp, C.c_float, vp, sz, vp]
+        L.mosaic_decode_attention_noalloc.argtypes = [vp, vp, vp, C.c_float, vp]
         L.mosaic_dense_workspace_bytes.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(sz)]
         L.mosaic_dense_decode_attention.argtypes = [vp, vp, vp, vp, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                                     C.c_int32, C.c_int64, C.c_int32, vp, C.c_float, vp, sz, vp]

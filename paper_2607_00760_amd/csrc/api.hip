@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -90,6 +91,38 @@ struct mosaic_cache {
         return w;
     }
 };
+
+// Fixed decode workspace of mosaic_decode_attention_noalloc: one copy per GPU,
+// reserved when the library's code object is loaded on that GPU and held
+// until the process ends.  Host code uses only the device address that
+// hipGetSymbolAddress returns for the current GPU (the array's name is a
+// host-side stand-in); nothing in it needs to start at zero, because every
+// region of the decode workspace is written before it is read within a call.
+static __device__ __align__(256) uint8_t scratch[MOSAIC_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[MAX_DEVICES] = {};
+
+// the address of this GPU's scratch array (resolved once per device, with
+// that device current)
+mosaic_status scratch_of_current_device(void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= MAX_DEVICES) return fail(MOSAIC_ERR_UNSUPPORTED, "device %d beyond %d devices", dev, MAX_DEVICES);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr) return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "scratch address");
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return MOSAIC_OK;
+}
+}  // namespace
 
 extern "C" {
 
@@ -362,6 +395,17 @@ mosaic_status mosaic_decode_attention(mosaic_cache *c, const void *q, float *out
     if (e != hipSuccess) return hip_fail(e, "decode launch");
     if (c->timing) c->timed_once = true;
     return ok();
+}
+
+mosaic_status mosaic_decode_attention_noalloc(mosaic_cache *c, const void *q, float *out, float sm_scale, void *stream) {
+    if (!c) return fail(MOSAIC_ERR_INVALID, "NULL cache");
+    if (c->wsl.total > (uint64_t)MOSAIC_NOALLOC_SCRATCH_BYTES)
+        return fail(MOSAIC_ERR_UNSUPPORTED, "decode workspace of %llu bytes exceeds the %llu-byte fixed buffer",
+                    (unsigned long long)c->wsl.total, (unsigned long long)MOSAIC_NOALLOC_SCRATCH_BYTES);
+    void *ws = nullptr;
+    const mosaic_status st = scratch_of_current_device(&ws);
+    if (st != MOSAIC_OK) return st;
+    return mosaic_decode_attention(c, q, out, sm_scale, ws, (size_t)MOSAIC_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 mosaic_status mosaic_dense_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t group_size,
