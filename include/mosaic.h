@@ -159,12 +159,17 @@ mosaic_status mosaic_workspace_bytes(const mosaic_cache *cache, int32_t op, size
  *   bsize + p * bsize_stride : uint8 [max_blocks]: per block, log2 B
  *   selinfo + p * selinfo_stride : uint32 [max_blocks][2]: binfo of each
  *                              entry of the selected list
+ *   wres  + p * wres_stride  : fp32 [D / 16][windows + 1][GP][18]: for each
+ *                              block of 16 output columns and each window
+ *                              (the last slot: the update buffer), the
+ *                              window's merged max and sum per head and its
+ *                              back-rotated output columns
  * Calls that overlap on one workspace race; separate streams need separate
  * workspaces. */
 typedef struct {
     uint64_t qrot_off, qrot_stride, score_off, score_stride, sel_off, sel_stride, wsel_off, wsel_stride;
     uint64_t part_off, part_stride, tag_off, tag_stride, binfo_off, binfo_stride, bsize_off, bsize_stride,
-             selinfo_off, selinfo_stride, total;
+             selinfo_off, selinfo_stride, wres_off, wres_stride, total;
     int32_t max_blocks, max_splits, gp, reserved;
 } mosaic_ws_layout;
 mosaic_status mosaic_decode_ws_layout(const mosaic_cache *cache, mosaic_ws_layout *out);

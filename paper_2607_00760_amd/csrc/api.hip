@@ -87,6 +87,7 @@ struct mosaic_cache {
         w.binfo = (uint2 *)(b + wsl.binfo_off); w.binfo_stride = wsl.binfo_stride;
         w.bsize = b + wsl.bsize_off; w.bsize_stride = wsl.bsize_stride;
         w.selinfo = (uint2 *)(b + wsl.selinfo_off); w.selinfo_stride = wsl.selinfo_stride;
+        w.wres = (float *)(b + wsl.wres_off); w.wres_stride = wsl.wres_stride;
         w.max_blocks = max_blocks; w.max_splits = max_splits;
         return w;
     }
@@ -263,6 +264,8 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     wregion(w.binfo_off, w.binfo_stride, (uint64_t)c->max_blocks * 8);
     wregion(w.bsize_off, w.bsize_stride, (uint64_t)c->max_blocks);
     wregion(w.selinfo_off, w.selinfo_stride, (uint64_t)c->max_blocks * 8);
+    // wres: each window's merged, back-rotated result per column block
+    wregion(w.wres_off, w.wres_stride, (uint64_t)CMB_NCC * (c->nw + 1) * c->GP * CMB_RES * 4);
     w.total = off + 256;                     // whole 16-byte loads of the last pair's arrays stay inside
     w.max_blocks = c->max_blocks; w.max_splits = c->max_splits; w.gp = c->GP;
     c->arena = nullptr;

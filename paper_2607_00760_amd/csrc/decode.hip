@@ -649,7 +649,6 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
 }
 
 // ------------------------------------------------------------------ topk
-constexpr int TOPK_LDS_KEYS = 32768;
 constexpr int TOPK_BINS = 2048;
 constexpr int TOPK_KPT = 16;                               // keys per thread held in registers
 
@@ -738,6 +737,35 @@ __device__ __forceinline__ void block_minmax_1024(uint32_t &lo, uint32_t &hi, ui
     lds_barrier();
 }
 
+// The bin holding the rem-th token from the top of a filled histogram hc
+// (2048 bins of width 2^sh over [base, base + span]); zeroes hn for the next
+// pass, narrows base / span to that bin and rem to the tokens still needed
+// inside it.  True when the bins were single keys (the threshold is base).
+__device__ __forceinline__ bool radix_pick(const uint32_t *hc, uint32_t *hn, uint32_t *sbuf, int sh, uint32_t &base,
+                                           uint32_t &span, uint32_t &rem) {
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    // bins from the top: thread t owns bins 2047 - 2t and 2046 - 2t
+    const uint32_t h0 = hc[TOPK_BINS - 1 - 2 * tid], h1 = hc[TOPK_BINS - 2 - 2 * tid];
+    hn[2 * tid] = 0;
+    hn[2 * tid + 1] = 0;
+    const uint32_t x = wave_scan_add(h0 + h1);
+    if (lane == 63) sbuf[wv] = x;
+    lds_barrier();
+    uint32_t above = x - (h0 + h1);
+    above += sum_below(sbuf, wv);
+    if (above < rem && above + h0 + h1 >= rem) {
+        if (above + h0 >= rem) { sbuf[32] = TOPK_BINS - 1 - 2 * tid; sbuf[33] = rem - above; }
+        else { sbuf[32] = TOPK_BINS - 2 - 2 * tid; sbuf[33] = rem - above - h0; }
+    }
+    lds_barrier();
+    const uint32_t b = sbuf[32];
+    rem = sbuf[33];
+    base += b << sh;
+    const uint32_t width = sh ? ((1u << sh) - 1u) : 0u;
+    span = min(span - (b << sh), width);
+    return sh == 0;
+}
+
 // Token-budget selection (Sec. 4.2 stage 2; Sec. 6.1 selects 10 % of tokens):
 // blocks are taken in (score desc, block index asc) order while the tokens
 // already taken are fewer than the budget.  The last block taken has the
@@ -749,37 +777,58 @@ __device__ __forceinline__ void block_minmax_1024(uint32_t &lo, uint32_t &hi, ui
 // the budget still needs (one scan of their tokens).  The selected list is
 // written in ascending block order (one scan of the taken counts) together
 // with each entry's record info, and the list position where each rotation
-// window starts.  Thread t owns the blocks [t * chunk, (t + 1) * chunk); with
-// REG (chunk = 16) their keys and record info stay in registers and the
-// taken ones are a 16-bit mask, else they are read from LDS / the workspace.
+// window starts.
 constexpr int TOPK_MAXW = 1024;                            // rotation windows tracked in LDS
 
-template <bool REG>
-__device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p, int nb, int ndesc, int budget,
-                                          uint32_t *keys, uint32_t *hist, uint32_t *sbuf, int *fbw) {
+// first block of each of the first nwl rotation windows (windows past the
+// last segment start at nb)
+__device__ __forceinline__ void window_firsts(const Geom &g, int p, int nb, int ndesc, int nwl, int *fbw) {
+    const int segs_per_win = g.W / SEG;
+    const Desc *gd = g.desc_of(p);
+    for (int w = threadIdx.x; w < nwl; w += 1024) {
+        const int s0 = w * segs_per_win;
+        fbw[w] = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
+    }
+}
+
+// list positions of the windows past the LDS slots (binary search of the
+// finished list), then k and the block count
+__device__ __forceinline__ void window_tail(const Geom &g, int p, int nb, int ndesc, int nwl, int k,
+                                            const int32_t *sel, int32_t *wsel) {
+    const int tid = threadIdx.x;
+    if (g.nw > nwl) {
+        __syncthreads();                                   // (sel from every thread)
+        const int segs_per_win = g.W / SEG;
+        const Desc *gd = g.desc_of(p);
+        for (int w = nwl + tid; w < g.nw; w += 1024) {
+            const int s0 = w * segs_per_win;
+            const int fb = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
+            int lo = 0, hi = k;
+            while (lo < hi) { const int mid = (lo + hi) >> 1; if (sel[mid] < fb) lo = mid + 1; else hi = mid; }
+            wsel[w] = lo;
+        }
+    }
+    if (tid == 0) { wsel[g.nw] = k; wsel[g.nw + 1] = nb; }
+}
+
+// Up to 16 K keys: thread t owns the blocks [16 t, 16 t + 16); their keys
+// and sizes stay in registers and the taken ones are a 16-bit mask.
+__device__ __forceinline__ void topk_reg(const Geom &g, const WsGeom &ws, int p, int nb, int ndesc, int budget,
+                                         uint32_t *hist, uint32_t *sbuf, int *fbw) {
     const int tid = threadIdx.x;
     const float *sc = ws.score + (uint64_t)p * (ws.score_stride / 4);
     const uint2 *bi = ws.binfo + (uint64_t)p * (ws.binfo_stride / 8);
     int32_t *sel = ws.sel + (uint64_t)p * (ws.sel_stride / 4);
     int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
     uint2 *sinfo = ws.selinfo + (uint64_t)p * (ws.selinfo_stride / 8);
-    const int chunk = REG ? TOPK_KPT : (nb + 1023) / 1024;
-    const int i0 = min(nb, tid * chunk), i1 = min(nb, i0 + chunk), n_own = i1 - i0;
-    const bool in_lds = nb <= TOPK_LDS_KEYS;
-    // first block of each rotation window (windows past the last segment start
-    // at nb), loaded now, published by the first barrier
-    const int segs_per_win = g.W / SEG;
-    const Desc *gd = g.desc_of(p);
+    const int i0 = min(nb, tid * TOPK_KPT), i1 = min(nb, i0 + TOPK_KPT), n_own = i1 - i0;
     const int nwl = min(g.nw, TOPK_MAXW);
-    for (int w = tid; w < nwl; w += 1024) {
-        const int s0 = w * segs_per_win;
-        fbw[w] = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
-    }
+    window_firsts(g, p, nb, ndesc, nwl, fbw);              // published by the first barrier
     const uint8_t *bz = ws.bsize + (uint64_t)p * ws.bsize_stride;
-    uint32_t kr[REG ? TOPK_KPT : 1];
-    uint32_t zr[REG ? TOPK_KPT / 4 : 1];                  // log2 block sizes, four per word
+    uint32_t kr[TOPK_KPT];
+    uint32_t zr[TOPK_KPT / 4];                             // log2 block sizes, four per word
     uint32_t kmin = 0xffffffffu, kmax = 0u;
-    if (REG) {
+    {
         const float4 *s4 = (const float4 *)(sc + i0);
         const uint4 z4 = n_own > 0 ? *(const uint4 *)(bz + i0) : make_uint4(0u, 0u, 0u, 0u);
         zr[0] = z4.x; zr[1] = z4.y; zr[2] = z4.z; zr[3] = z4.w;
@@ -793,162 +842,282 @@ __device__ __forceinline__ void topk_body(const Geom &g, const WsGeom &ws, int p
 #pragma unroll
         for (int j = 0; j < TOPK_KPT; ++j)
             if (j < n_own) { kmin = min(kmin, kr[j]); kmax = max(kmax, kr[j]); }
-    } else {
-        for (int i = i0; i < i1; ++i) {
-            const uint32_t key = score_key(sc[i]);
-            if (in_lds) keys[i] = key;
-            kmin = min(kmin, key);
-            kmax = max(kmax, key);
-        }
     }
-    auto key_at = [&](int j) -> uint32_t { return in_lds ? keys[i0 + j] : score_key(sc[i0 + j]); };   // !REG
-    // tokens of owned block j: 2^(log2 size), from the registers (REG) or the array
+    // tokens of owned block j: 2^(log2 size)
     auto tok_reg = [&](int j) -> uint32_t { return 1u << ((zr[j >> 2] >> (8 * (j & 3))) & 7u); };
-    auto tok_mem = [&](int j) -> uint32_t { return 1u << (bz[i0 + j] & 7u); };
     // two histograms in turn: a pass zeroes the next one while it reads its own
     for (int i = tid; i < TOPK_BINS; i += 1024) hist[i] = 0;
     block_minmax_1024(kmin, kmax, sbuf);                          // (its barriers publish the zeros and fbw)
     uint32_t base = kmin, span = kmax - kmin;                     // candidates: [base, base + span]
     uint32_t rem = (uint32_t)budget;                               // tokens still to take
-    const int lane = tid & 63, wv = tid >> 6;
     for (int pass = 0; budget > 0; ++pass) {
         uint32_t *hc = hist + (pass & 1) * TOPK_BINS, *hn = hist + ((pass + 1) & 1) * TOPK_BINS;
         const int bits = 32 - (span ? __builtin_clz(span) : 32);
         const int sh = bits > 11 ? bits - 11 : 0;                 // (span >> sh) < 2048
-        if (REG) {
 #pragma unroll
-            for (int j = 0; j < TOPK_KPT; ++j) {
-                const uint32_t d = kr[j] - base;
-                if (j < n_own && kr[j] >= base && d <= span) atomicAdd(&hc[d >> sh], tok_reg(j));
-            }
-        } else {
-            for (int j = 0; j < n_own; ++j) {
-                const uint32_t key = key_at(j), d = key - base;
-                if (key >= base && d <= span) atomicAdd(&hc[d >> sh], tok_mem(j));
-            }
+        for (int j = 0; j < TOPK_KPT; ++j) {
+            const uint32_t d = kr[j] - base;
+            if (j < n_own && kr[j] >= base && d <= span) atomicAdd(&hc[d >> sh], tok_reg(j));
         }
         lds_barrier();
-        // bins from the top: thread t owns bins 2047 - 2t and 2046 - 2t
-        const uint32_t h0 = hc[TOPK_BINS - 1 - 2 * tid], h1 = hc[TOPK_BINS - 2 - 2 * tid];
-        hn[2 * tid] = 0;
-        hn[2 * tid + 1] = 0;
-        const uint32_t x = wave_scan_add(h0 + h1);
-        if (lane == 63) sbuf[wv] = x;
-        lds_barrier();
-        uint32_t above = x - (h0 + h1);
-        above += sum_below(sbuf, wv);
-        if (above < rem && above + h0 + h1 >= rem) {
-            if (above + h0 >= rem) { sbuf[32] = TOPK_BINS - 1 - 2 * tid; sbuf[33] = rem - above; }
-            else { sbuf[32] = TOPK_BINS - 2 - 2 * tid; sbuf[33] = rem - above - h0; }
-        }
-        lds_barrier();
-        const uint32_t b = sbuf[32];
-        rem = sbuf[33];
-        base += b << sh;
-        const uint32_t width = sh ? ((1u << sh) - 1u) : 0u;
-        span = min(span - (b << sh), width);
-        if (sh == 0) break;
+        if (radix_pick(hc, hn, sbuf, sh, base, span, rem)) break;
     }
     // T = base; need = tokens the budget still needs among the blocks equal to T
     const uint32_t T = base, need = rem;
     uint32_t v[1] = {0u}, tot[1];
     if (budget > 0) {                                      // this thread's tokens equal to T
-        if (REG) {
 #pragma unroll
-            for (int j = 0; j < TOPK_KPT; ++j) v[0] += (j < n_own && kr[j] == T) ? tok_reg(j) : 0u;
-        } else {
-            for (int j = 0; j < n_own; ++j) v[0] += key_at(j) == T ? tok_mem(j) : 0u;
-        }
+        for (int j = 0; j < TOPK_KPT; ++j) v[0] += (j < n_own && kr[j] == T) ? tok_reg(j) : 0u;
     }
     block_excl_scan_1024<1>(v, tot, sbuf);                 // -> equal tokens before this thread
     // taken blocks: above T, or equal to T while the equal tokens before are below need
-    uint32_t tmask = 0, tcnt = 0;
+    uint32_t tmask = 0;
     if (budget > 0) {
         uint32_t acc = v[0];
-        if (REG) {
 #pragma unroll
-            for (int j = 0; j < TOPK_KPT; ++j) {
-                const bool eq = j < n_own && kr[j] == T;
-                const bool t = j < n_own && (kr[j] > T || (eq && acc < need));
-                acc += eq ? tok_reg(j) : 0u;
-                tmask |= t ? (1u << j) : 0u;
-            }
-            tcnt = (uint32_t)__popc(tmask);
-        } else {
-            for (int j = 0; j < n_own; ++j) {
-                const uint32_t key = key_at(j);
-                tcnt += (key > T || (key == T && acc < need)) ? 1u : 0u;
-                acc += key == T ? tok_mem(j) : 0u;
-            }
+        for (int j = 0; j < TOPK_KPT; ++j) {
+            const bool eq = j < n_own && kr[j] == T;
+            const bool t = j < n_own && (kr[j] > T || (eq && acc < need));
+            acc += eq ? tok_reg(j) : 0u;
+            tmask |= t ? (1u << j) : 0u;
         }
     }
-    const uint32_t eq_before = v[0];
-    v[0] = tcnt;
+    v[0] = (uint32_t)__popc(tmask);
     block_excl_scan_1024<1>(v, tot, sbuf);                 // -> list position of this thread's first
     const uint32_t pos0 = v[0];
     const int k = budget > 0 ? (int)tot[0] : 0;            // blocks selected
-    if (REG) {
-        // the record info of the taken blocks only: all loads issued, then the stores
-        uint2 br[TOPK_KPT];
+    // the record info of the taken blocks only: all loads issued, then the stores
+    uint2 br[TOPK_KPT];
 #pragma unroll
-        for (int j = 0; j < TOPK_KPT; ++j) br[j] = ((tmask >> j) & 1u) ? bi[i0 + j] : make_uint2(0u, 0u);
-        uint32_t pos = pos0;
+    for (int j = 0; j < TOPK_KPT; ++j) br[j] = ((tmask >> j) & 1u) ? bi[i0 + j] : make_uint2(0u, 0u);
+    uint32_t pos = pos0;
 #pragma unroll
-        for (int j = 0; j < TOPK_KPT; ++j) {
-            if ((tmask >> j) & 1u) { sel[pos] = i0 + j; sinfo[pos] = br[j]; }
-            pos += (tmask >> j) & 1u;
+    for (int j = 0; j < TOPK_KPT; ++j) {
+        if ((tmask >> j) & 1u) { sel[pos] = i0 + j; sinfo[pos] = br[j]; }
+        pos += (tmask >> j) & 1u;
+    }
+    // window starts: the position of the first block at or after each
+    // start, from the owning thread's first position and taken mask
+    uint32_t *tpos = hist, *tmk = hist + 1024;              // (the histograms are no longer needed)
+    tpos[tid] = pos0;
+    tmk[tid] = tmask;
+    lds_barrier();
+    for (int w = tid; w < nwl; w += 1024) {
+        const int f = fbw[w];
+        if (f >= nb) { wsel[w] = k; continue; }
+        const int t = f / TOPK_KPT, off = f % TOPK_KPT;
+        wsel[w] = (int)(tpos[t] + (uint32_t)__popc(tmk[t] & ((1u << off) - 1u)));
+    }
+    window_tail(g, p, nb, ndesc, nwl, k, sel, wsel);
+}
+
+// More keys (long contexts): each lane reads four consecutive keys (one
+// 16-byte score load, one 4-byte size load), a wave 256 consecutive keys, and
+// TB_UNROLL such groups are in flight per wave, so that a pass over the keys
+// is a few memory round trips.  The block order that the tie rule and the
+// list need is carried by 256-key segments, one wave's keys of one step: a
+// round of up to TB_SEGS segments scans their equal-key tokens, then their
+// taken counts, each with the carry of the rounds before; a segment's taken
+// blocks are four 64-bit masks (bit l of mask e: key 4 l + e).
+constexpr int TB_SEGS = 512;
+constexpr int TB_SEG_KEYS = 256;
+constexpr int TB_UNROLL = 8;
+constexpr size_t TB_SMEM = (size_t)TB_SEGS * (4 + 32);     // u32 prefixes + four u64 masks per segment
+
+// exclusive prefix sums (plus carry) of a[0 .. n) in place, n <= 4096, four
+// consecutive entries per thread; returns the total of the n entries
+__device__ __forceinline__ uint32_t seg_scan(uint32_t *a, int n, uint32_t carry, uint32_t *sbuf) {
+    const int tid = threadIdx.x;
+    uint32_t x[4], v[1], tot[1];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = (4 * tid + e < n) ? a[4 * tid + e] : 0u;
+    v[0] = x[0] + x[1] + x[2] + x[3];
+    block_excl_scan_1024<1>(v, tot, sbuf);
+    uint32_t run = carry + v[0];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        if (4 * tid + e < n) a[4 * tid + e] = run;
+        run += x[e];
+    }
+    lds_barrier();
+    return tot[0];
+}
+
+// four consecutive keys and their log2 block sizes from index i (a multiple
+// of 4 below nb; the lanes past nb read the rest of the arrays' slack)
+struct Key4 {
+    uint32_t k[4];
+    uint32_t z;                                             // four log2 sizes, one per byte
+    __device__ __forceinline__ uint32_t tok(int e) const { return 1u << ((z >> (8 * e)) & 7u); }
+};
+__device__ __forceinline__ Key4 load_key4(const float *sc, const uint8_t *bz, int i) {
+    const float4 f = *(const float4 *)(sc + i);
+    Key4 r;
+    r.k[0] = score_key(f.x); r.k[1] = score_key(f.y); r.k[2] = score_key(f.z); r.k[3] = score_key(f.w);
+    r.z = *(const uint32_t *)(bz + i);
+    return r;
+}
+
+__device__ __forceinline__ void topk_big(const Geom &g, const WsGeom &ws, int p, int nb, int ndesc, int budget,
+                                         uint32_t *segw, uint32_t *hist, uint32_t *sbuf, int *fbw) {
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const float *sc = ws.score + (uint64_t)p * (ws.score_stride / 4);
+    const uint8_t *bz = ws.bsize + (uint64_t)p * ws.bsize_stride;
+    const uint2 *bi = ws.binfo + (uint64_t)p * (ws.binfo_stride / 8);
+    int32_t *sel = ws.sel + (uint64_t)p * (ws.sel_stride / 4);
+    int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
+    uint2 *sinfo = ws.selinfo + (uint64_t)p * (ws.selinfo_stride / 8);
+    uint64_t *segm = (uint64_t *)(segw + TB_SEGS);          // [TB_SEGS][4]
+    const int nwl = min(g.nw, TOPK_MAXW);
+    window_firsts(g, p, nb, ndesc, nwl, fbw);
+    for (int i = tid; i < TOPK_BINS; i += 1024) hist[i] = 0;
+    const int ng = (nb + 3) / 4;                            // groups of four keys
+    // the range of the keys (thread t: groups t, t + 1024, ...)
+    uint32_t kmin = 0xffffffffu, kmax = 0u;
+    for (int q0 = tid; q0 < ng; q0 += 1024 * TB_UNROLL) {
+        Key4 x[TB_UNROLL];
+#pragma unroll
+        for (int u = 0; u < TB_UNROLL; ++u) x[u] = load_key4(sc, bz, 4 * min(q0 + u * 1024, ng - 1));
+#pragma unroll
+        for (int u = 0; u < TB_UNROLL; ++u)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const bool in = 4 * min(q0 + u * 1024, ng - 1) + e < nb;   // (a clamped group repeats the last)
+                kmin = in ? min(kmin, x[u].k[e]) : kmin;
+                kmax = in ? max(kmax, x[u].k[e]) : kmax;
+            }
+    }
+    block_minmax_1024(kmin, kmax, sbuf);
+    uint32_t base = kmin, span = kmax - kmin, rem = (uint32_t)budget;
+    for (int pass = 0; budget > 0; ++pass) {
+        uint32_t *hc = hist + (pass & 1) * TOPK_BINS, *hn = hist + ((pass + 1) & 1) * TOPK_BINS;
+        const int bits = 32 - (span ? __builtin_clz(span) : 32);
+        const int sh = bits > 11 ? bits - 11 : 0;
+        for (int q0 = tid; q0 < ng; q0 += 1024 * TB_UNROLL) {
+            Key4 x[TB_UNROLL];
+#pragma unroll
+            for (int u = 0; u < TB_UNROLL; ++u) x[u] = load_key4(sc, bz, 4 * min(q0 + u * 1024, ng - 1));
+#pragma unroll
+            for (int u = 0; u < TB_UNROLL; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t key = x[u].k[e], d = key - base;
+                    if (4 * (q0 + u * 1024) + e < nb && key >= base && d <= span) atomicAdd(&hc[d >> sh], x[u].tok(e));
+                }
         }
-        // window starts: the position of the first block at or after each
-        // start, from the owning thread's first position and taken mask
-        uint32_t *tpos = hist, *tmk = hist + 1024;          // (the histograms are no longer needed)
-        tpos[tid] = pos0;
-        tmk[tid] = tmask;
         lds_barrier();
+        if (radix_pick(hc, hn, sbuf, sh, base, span, rem)) break;
+    }
+    const uint32_t T = base, need = rem;
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    uint32_t eqc = 0, posc = 0;                             // carries: equal tokens, list positions
+    for (int r0 = 0; budget > 0 && r0 < nb; r0 += TB_SEGS * TB_SEG_KEYS) {
+        const int nk = min(nb - r0, TB_SEGS * TB_SEG_KEYS), ns = (nk + TB_SEG_KEYS - 1) / TB_SEG_KEYS;
+        // the lane's four keys of segment sg of this round (clamped to the
+        // round's last group); in(e): key e is one of the round's keys
+        auto fetch = [&](int sg) {
+            const int o = min(sg * TB_SEG_KEYS + 4 * lane, (nk - 1) & ~3);
+            return load_key4(sc, bz, r0 + o);
+        };
+        auto in = [&](int sg, int e) { return sg * TB_SEG_KEYS + 4 * lane + e < nk; };
+        // (a) tokens equal to T per segment -> their prefixes in block order
+        for (int s0 = wv; s0 < ns; s0 += 16 * TB_UNROLL) {
+            Key4 x[TB_UNROLL];
+#pragma unroll
+            for (int u = 0; u < TB_UNROLL; ++u) x[u] = fetch(s0 + 16 * u);
+#pragma unroll
+            for (int u = 0; u < TB_UNROLL; ++u) {
+                const int sg = s0 + 16 * u;
+                uint32_t e4 = 0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) e4 += (in(sg, e) && x[u].k[e] == T) ? x[u].tok(e) : 0u;
+                const uint32_t tot = wave_scan_add(e4);
+                if (lane == 63 && sg < ns) segw[sg] = tot;
+            }
+        }
+        lds_barrier();
+        const uint32_t eq_round = seg_scan(segw, ns, eqc, sbuf);
+        eqc += eq_round;
+        // (b) taken blocks: four masks per segment and their count
+        for (int s0 = wv; s0 < ns; s0 += 16 * TB_UNROLL) {
+            Key4 x[TB_UNROLL];
+#pragma unroll
+            for (int u = 0; u < TB_UNROLL; ++u) x[u] = fetch(s0 + 16 * u);
+#pragma unroll
+            for (int u = 0; u < TB_UNROLL; ++u) {
+                const int sg = s0 + 16 * u;
+                uint32_t xe[4], e4 = 0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    xe[e] = (in(sg, e) && x[u].k[e] == T) ? x[u].tok(e) : 0u;
+                    e4 += xe[e];
+                }
+                uint32_t pre = (sg < ns ? segw[sg] : 0u) + wave_scan_add(e4) - e4;
+                uint32_t cnt = 0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t key = x[u].k[e];
+                    const bool t = in(sg, e) && (key > T || (key == T && pre < need));
+                    pre += xe[e];
+                    const uint64_t m = __ballot(t);
+                    cnt += (uint32_t)__popcll(m);
+                    if (lane == 0 && sg < ns) segm[4 * sg + e] = m;
+                }
+                if (lane == 0 && sg < ns) segw[sg] = cnt;
+            }
+        }
+        lds_barrier();
+        const uint32_t taken_round = seg_scan(segw, ns, posc, sbuf);
+        posc += taken_round;
+        // (c) the list entries of the round, and the windows that start in it
+        for (int s0 = wv; s0 < ns; s0 += 16 * TB_UNROLL) {
+#pragma unroll
+            for (int u = 0; u < TB_UNROLL; ++u) {
+                const int sg = s0 + 16 * u;
+                if (sg < ns) {
+                    uint32_t pos = segw[sg];
+                    uint64_t m[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        m[e] = segm[4 * sg + e];
+                        pos += (uint32_t)__popcll(m[e] & below);    // taken keys of the lanes before
+                    }
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        if ((m[e] >> lane) & 1ull) {
+                            const int i = r0 + sg * TB_SEG_KEYS + 4 * lane + e;
+                            sel[pos] = i;
+                            sinfo[pos] = bi[i];
+                            ++pos;
+                        }
+                    }
+                }
+            }
+        }
         for (int w = tid; w < nwl; w += 1024) {
             const int f = fbw[w];
-            if (f >= nb) { wsel[w] = k; continue; }
-            const int t = f / TOPK_KPT, off = f % TOPK_KPT;
-            wsel[w] = (int)(tpos[t] + (uint32_t)__popc(tmk[t] & ((1u << off) - 1u)));
-        }
-    } else {
-        // the keys again, in order, with the window starts met on the way
-        int wn = 0;
-        while (wn < nwl && fbw[wn] < i0) ++wn;
-        int nextfb = wn < nwl ? fbw[wn] : 0x7fffffff;
-        uint32_t pos = pos0, acc = eq_before;
-        for (int j = 0; j < n_own; ++j) {
-            const int i = i0 + j;
-            while (nextfb == i) {
-                wsel[wn++] = (int)pos;
-                nextfb = wn < nwl ? fbw[wn] : 0x7fffffff;
-            }
-            if (budget > 0) {
-                const uint32_t key = key_at(j);
-                const bool t = key > T || (key == T && acc < need);
-                acc += key == T ? tok_mem(j) : 0u;
-                if (t && pos < (uint32_t)nb) { sel[pos] = i; sinfo[pos] = bi[i]; }
-                pos += t ? 1u : 0u;
+            if (f >= r0 && f < r0 + nk) {
+                const int sg = (f - r0) / TB_SEG_KEYS, o = (f - r0) % TB_SEG_KEYS, l = o >> 2, e0 = o & 3;
+                const uint64_t bl = (l == 0) ? 0ull : (~0ull >> (64 - l));
+                uint32_t pos = segw[sg];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint64_t m = segm[4 * sg + e];
+                    pos += (uint32_t)__popcll(m & bl) + ((e < e0) ? (uint32_t)((m >> l) & 1ull) : 0u);
+                }
+                wsel[w] = (int)pos;
             }
         }
-        lds_barrier();
-        for (int w = tid; w < nwl; w += 1024)              // windows starting at nb
-            if (fbw[w] >= nb) wsel[w] = k;
+        lds_barrier();                                     // the next round rewrites segw / segm
     }
-    if (g.nw > nwl) {                                      // more windows than LDS slots
-        __syncthreads();                                   // (sel from every thread)
-        for (int w = nwl + tid; w < g.nw; w += 1024) {
-            const int s0 = w * segs_per_win;
-            const int fb = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
-            int lo = 0, hi = k;
-            while (lo < hi) { const int mid = (lo + hi) >> 1; if (sel[mid] < fb) lo = mid + 1; else hi = mid; }
-            wsel[w] = lo;
-        }
-    }
-    if (tid == 0) { wsel[g.nw] = k; wsel[g.nw + 1] = nb; }
+    const int k = budget > 0 ? (int)posc : 0;
+    for (int w = tid; w < nwl; w += 1024)
+        if (budget <= 0 || fbw[w] >= nb) wsel[w] = k;
+    window_tail(g, p, nb, ndesc, nwl, k, sel, wsel);
 }
 
 __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
-    extern __shared__ __align__(16) uint32_t keys[];            // [min(nb, TOPK_LDS_KEYS)] when staged
+    extern __shared__ __align__(16) uint32_t segw[];            // [TB_SMEM / 4] on the long-context path
     __shared__ uint32_t hist[2 * TOPK_BINS];
     __shared__ uint32_t sbuf[64];
     __shared__ int fbw[TOPK_MAXW];
@@ -964,8 +1133,8 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
         const long long bb = ((long long)ntok * g.sel_num + g.sel_den - 1) / g.sel_den;
         budget = (int)(bb < 1 ? 1 : (bb > ntok ? ntok : bb));
     }
-    if (nb <= 1024 * TOPK_KPT) topk_body<true>(g, ws, p, nb, ndesc, budget, keys, hist, sbuf, fbw);
-    else topk_body<false>(g, ws, p, nb, ndesc, budget, keys, hist, sbuf, fbw);
+    if (nb <= 1024 * TOPK_KPT) topk_reg(g, ws, p, nb, ndesc, budget, hist, sbuf, fbw);
+    else topk_big(g, ws, p, nb, ndesc, budget, segw, hist, sbuf, fbw);
 }
 
 // ------------------------------------------------------------------ attention
@@ -1572,17 +1741,17 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
 }
 
 // ------------------------------------------------------------------ combine
-// grid (pairs, D / CMB_COLS), 256 threads: a workgroup produces output channels
-// j0 .. j0 + 15 of every head of a pair.  The splits of a rotation window are
-// consecutive (the attention numbers them window by window, then the update
-// buffer's split): for each window the workgroup merges its splits' (max,
-// sum, accumulator) by log-sum-exp, rotates the merged accumulator back once
-// with the window's R_v (x_j = sum_c a_c R_v[c][j]: rows j0.. of the stored
-// R_v^T, 8 KB per window; the rotation stays merged into one vector per
-// window, Sec. 5.3), and folds the result into a running log-sum-exp merge
-// with the other windows and the buffer's unrotated split.  A kernel boundary
-// makes the attention's partials visible.
-constexpr int CMB_COLS = 16, CMB_THREADS = 256;
+// Two kernels.  k_combine: one workgroup per (pair p, block of 16 output
+// columns j0.., window slot w), 256 threads; slot w = windows is the update
+// buffer's split.  It merges the window's splits' (max, sum, accumulator) by
+// log-sum-exp, rotates the merged accumulator back once with the window's R_v
+// for its columns (x_j = sum_c a_c R_v[c][j]: rows j0.. of the stored R_v^T,
+// 8 KB; the rotation stays merged into one vector per window, Sec. 5.3) and
+// stores the window's (max, sum, columns) per head.  k_merge then merges the
+// windows' results of each output by log-sum-exp.  Kernel boundaries make the
+// attention's partials and the window results visible.  Blocks are ordered
+// so that b % 8, the XCD a block runs on, is p % 8, as in the attention.
+constexpr int CMB_THREADS = 256;
 
 template <int GP>
 __global__ void __launch_bounds__(CMB_THREADS) k_combine(Geom g, WsGeom ws, float *out) {
@@ -1591,14 +1760,15 @@ __global__ void __launch_bounds__(CMB_THREADS) k_combine(Geom g, WsGeom ws, floa
     constexpr int CPP = D / NPART;                            // channels per thread
     constexpr int NE = GP * D / CMB_THREADS;                  // merged elements per thread
     constexpr int CH = 16;                                    // splits merged per round trip
-    constexpr int MAXW = 1024;                                // window bounds staged in LDS
     static_assert(CMB_COLS * D / 4 == 2 * CMB_THREADS, "two 16-byte pieces of R_v^T rows per thread");
-    __shared__ float am[GP][D];                               // merged accumulator of the current window
+    __shared__ float am[GP][D];                               // merged accumulator of the window
     __shared__ float rv[CMB_COLS][D + 4];                     // R_v[c][j0 + jj] as rows jj
     __shared__ float sm[CH][GP], sl[CH][GP];                  // staged split maxima and sums
     __shared__ float wml[2][GP], wsc[GP];                     // the window's running max, sum, rescale
-    __shared__ int wb[MAXW + 1];                              // first list entry of each window
-    const int p = blockIdx.x, j0 = blockIdx.y * CMB_COLS, tid = threadIdx.x;
+    const int np8 = (g.npairs + 7) / 8 * 8;
+    const int bid = blockIdx.x, p = bid % np8, cc = (bid / np8) % CMB_NCC, w = bid / (np8 * CMB_NCC);
+    if (p >= g.npairs) return;
+    const int j0 = cc * CMB_COLS, tid = threadIdx.x;
     const int oi = tid / NPART, part_i = tid % NPART;         // output (head, column) and channel part
     const int oh = oi / CMB_COLS, oj = oi % CMB_COLS;
     const PairMeta meta = *g.meta_of(p);
@@ -1607,30 +1777,25 @@ __global__ void __launch_bounds__(CMB_THREADS) k_combine(Geom g, WsGeom ws, floa
     const int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
     const float *part = ws.part + (uint64_t)p * (ws.part_stride / 4);
     const int lim = ws.max_blocks;
-    const int nwl = min(g.nw, MAXW);
-    for (int w = tid; w <= nwl; w += CMB_THREADS) wb[w] = min(max(wsel[w], 0), lim);
-    lds_barrier();
-    float M = -INFINITY, Lsum = 0.0f, o = 0.0f;               // running merge of output (oh, j0 + oj)
-    int s0 = 0;
-    // windows in order, then the buffer's split (w == nw)
-    for (int w = 0; w <= g.nw; ++w) {
-        int nsp;
-        if (w < g.nw) {
-            const int a = w < nwl ? wb[w] : min(max(wsel[w], 0), lim);
-            const int b = w + 1 <= nwl ? max(wb[w + 1], a) : min(max(wsel[w + 1], a), lim);
-            nsp = (b - a + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS;
-        } else {
-            nsp = nbuf > 0 ? 1 : 0;
-        }
-        if (nsp == 0) continue;
-        if (s0 + nsp > ws.max_splits) break;                  // (cannot happen: the grid had this many)
-        const bool rot = w < g.nw && g.rotated;
-        float4 rq0 = make_float4(0.0f, 0.0f, 0.0f, 0.0f), rq1 = rq0;   // R_v[c][j0 .. j0 + 15], loaded now
-        if (rot) {
-            const float4 *rvt = (const float4 *)(g.rot_of(p, w) + D * D + (uint64_t)j0 * D);
-            rq0 = rvt[tid];
-            rq1 = rvt[tid + CMB_THREADS];
-        }
+    // this slot's splits: the windows' splits are numbered window by window,
+    // then the buffer's (the attention's numbering), s0 = those before it
+    int s0 = 0, nsp = 0;
+    for (int x = 0; x <= min(w, g.nw - 1); ++x) {
+        const int a = min(max(wsel[x], 0), lim), b = min(max(wsel[x + 1], a), lim);
+        const int n = (b - a + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS;
+        if (x < w) s0 += n; else nsp = n;
+    }
+    if (w == g.nw) nsp = nbuf > 0 ? 1 : 0;
+    if (s0 + nsp > ws.max_splits) nsp = 0;                    // (cannot happen: the attention had this many)
+    const bool rot = w < g.nw && g.rotated && nsp > 0;
+    float4 rq0 = make_float4(0.0f, 0.0f, 0.0f, 0.0f), rq1 = rq0;   // R_v[c][j0 .. j0 + 15], loaded now
+    if (rot) {
+        const float4 *rvt = (const float4 *)(g.rot_of(p, w) + D * D + (uint64_t)j0 * D);
+        rq0 = rvt[tid];
+        rq1 = rvt[tid + CMB_THREADS];
+    }
+    float *res = ws.wres + (uint64_t)p * (ws.wres_stride / 4) + ((uint64_t)cc * (g.nw + 1) + w) * (GP * CMB_RES);
+    if (nsp > 0) {
         float A[NE];
 #pragma unroll
         for (int e = 0; e < NE; ++e) A[e] = 0.0f;
@@ -1694,18 +1859,36 @@ __global__ void __launch_bounds__(CMB_THREADS) k_combine(Geom g, WsGeom ws, floa
         } else {
             y = am[oh][j0 + oj];
         }
-        const float wm = wml[0][oh], wl = wml[1][oh];
-        if (wm != -INFINITY) {
-            const float mn = fmaxf(M, wm);
-            const float a = __expf(M - mn), b = __expf(wm - mn);
-            o = o * a + y * b;
-            Lsum = Lsum * a + wl * b;
-            M = mn;
-        }
-        lds_barrier();                                        // am, rv and wml are rewritten next
-        s0 += nsp;
+        if (part_i == 0) res[oh * CMB_RES + 2 + oj] = y;
+        if (tid < GP) { res[tid * CMB_RES] = wml[0][tid]; res[tid * CMB_RES + 1] = wml[1][tid]; }
+    } else if (tid < GP) {                                    // an empty slot
+        res[tid * CMB_RES] = -INFINITY;
+        res[tid * CMB_RES + 1] = 0.0f;
     }
-    if (part_i == 0 && oh < g.G) out[((uint64_t)p * g.G + oh) * D + j0 + oj] = (Lsum > 0.0f) ? o / Lsum : 0.0f;
+}
+
+// one thread per output (pair, head, column): the log-sum-exp merge of its
+// window slots' results, in slot order
+template <int GP>
+__global__ void __launch_bounds__(256) k_merge(Geom g, WsGeom ws, float *out) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    const int p = i / (GP * D), h = (i / D) % GP, j = i % D;
+    if (p >= g.npairs || h >= g.G) return;
+    const int cc = j / CMB_COLS, jj = j % CMB_COLS;
+    const float *r = ws.wres + (uint64_t)p * (ws.wres_stride / 4) + (uint64_t)cc * (g.nw + 1) * (GP * CMB_RES)
+                     + h * CMB_RES;
+    float M = -INFINITY, Lsum = 0.0f, o = 0.0f;
+    for (int x = 0; x <= g.nw; ++x, r += GP * CMB_RES) {
+        const float wm = r[0];
+        if (wm == -INFINITY) continue;
+        const float wl = r[1], y = r[2 + jj];
+        const float mn = fmaxf(M, wm);
+        const float a = __expf(M - mn), b = __expf(wm - mn);    // M = -inf: a = 0
+        o = o * a + y * b;
+        Lsum = Lsum * a + wl * b;
+        M = mn;
+    }
+    out[((uint64_t)p * g.G + h) * D + j] = (Lsum > 0.0f) ? o / Lsum : 0.0f;
 }
 
 int max_keep(const Geom &g) {
@@ -1738,7 +1921,7 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, f
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev) hipEventRecord(ev[2], s);
-    const size_t topk_smem = (size_t)min(w.max_blocks, TOPK_LDS_KEYS) * 4;
+    const size_t topk_smem = w.max_blocks > 1024 * TOPK_KPT ? TB_SMEM : 0;
     hipLaunchKernelGGL(k_topk, dim3(g.npairs), dim3(1024), topk_smem, s, g, w);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev) hipEventRecord(ev[3], s);
@@ -1757,7 +1940,10 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, f
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev) hipEventRecord(ev[4], s);
-    hipLaunchKernelGGL(k_combine<GP>, dim3(g.npairs, D / CMB_COLS), dim3(CMB_THREADS), 0, s, g, w, out);
+    hipLaunchKernelGGL(k_combine<GP>, dim3((g.npairs + 7) / 8 * 8 * CMB_NCC * (g.nw + 1)), dim3(CMB_THREADS), 0, s,
+                       g, w, out);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_merge<GP>, dim3(ceil_div(g.npairs * GP * D, 256)), dim3(256), 0, s, g, w, out);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev) hipEventRecord(ev[5], s);
     return hipSuccess;

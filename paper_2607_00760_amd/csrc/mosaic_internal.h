@@ -15,6 +15,9 @@ constexpr int WAVE = 64;
 #endif
 constexpr int SPLIT_BLOCKS = MOSAIC_SPLIT_BLOCKS;  // selected blocks per split-K partition
 constexpr int SCORE_SEGS = 128;    // segments per block-scoring workgroup (one launch round)
+constexpr int CMB_COLS = 16;                  // output columns per combine workgroup
+constexpr int CMB_NCC = D / CMB_COLS;         // column blocks of an output row
+constexpr int CMB_RES = 2 + CMB_COLS;         // floats per head of a window result: max, sum, columns
 
 struct Desc {                 // 16-byte segment descriptor (layout is part of the ABI)
     uint32_t tok_off, sc_off, first_block;
@@ -69,6 +72,7 @@ struct WsGeom {               // decode workspace
     uint2 *binfo; uint64_t binfo_stride;    // [max_blocks]: per block, blk_info
     uint8_t *bsize; uint64_t bsize_stride;  // [max_blocks]: per block, log2 of its token count
     uint2 *selinfo; uint64_t selinfo_stride; // [max_blocks]: blk_info of each selected entry
+    float *wres; uint64_t wres_stride;      // [CMB_NCC][nw + 1][GP][CMB_RES]: per-window merged results
     int max_blocks, max_splits;
 };
 

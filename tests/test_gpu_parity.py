@@ -57,6 +57,10 @@ CASES = {
     # K and V for the byte-exact compression, K only for the decode (unit-scale
     # values keep the outputs O(1) under the same absolute bound)
     "fp8_wide_range": (gen.spec("c3", ctx=(1500, 700), hkv=2, kind="gauss"), dict(fp8=True)),
+    # more than 16 K blocks in a pair: the top-k's long-context path (strided
+    # passes, 64-key segments), over two rounds of segments for the first pair
+    "long_topk_b4": (gen.spec("c1", ctx=(290000, 70000), hkv=1, rotate=False), dict(force_default=True,
+                                                                                   default=(32, 1, 4))),
 }
 
 
@@ -135,6 +139,30 @@ def test_append_flush_finalize_parity(name):
             out = c.decode(q.cuda(), sc)
             want, _, _ = oracle_decode_all(ops, spec, q, sc)
             assert_close(out.cpu().numpy(), want, f"{name} step {t}")
+
+
+def test_long_topk_all_ties():
+    """A zero query scores every block 0: the selection is the first blocks in
+    block order up to the token budget, on the long-context top-k path, where
+    the equal-token prefix carries from one round of segments to the next."""
+    spec, lay, lp, op, cap = _case("long_topk_b4")
+    c = gpu_cache(lp, spec, lay, cap)
+    ops = oracle_pairs(op, spec, lay, cap)
+    q = torch.zeros((spec.num_seqs, spec.hq, D), dtype=spec.torch_dtype)
+    out = c.decode(q.cuda(), scale_of())
+    torch.cuda.synchronize()
+    want, sels, scores = oracle_decode_all(ops, spec, q, scale_of())
+    for p in range(spec.num_seqs * spec.hkv):
+        nb = ops[p].info().nblk
+        gs, gsel, _ = gpu_scores_sel(c, p, nb)
+        assert not np.any(scores[p]), "a zero query scores every block 0"
+        assert np.array_equal(gs.view(np.uint32), scores[p].view(np.uint32))
+        L = spec.ctx[p // spec.hkv]
+        scoreable = L // 64 * 64 + (32 if L % 64 >= 32 else 0)     # final segments + a provisional half
+        budget = -(-scoreable * spec.select[0] // spec.select[1])
+        assert np.array_equal(sels[p], np.arange(-(-budget // 4))), "oracle: the first blocks in order"
+        assert np.array_equal(gsel, sels[p]), f"pair {p}: selected blocks"
+    assert_close(out.cpu().numpy(), want, "long_topk_all_ties")
 
 
 def test_keep_all_equals_dense_on_gpu():
