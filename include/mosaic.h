@@ -145,8 +145,10 @@ mosaic_status mosaic_workspace_bytes(const mosaic_cache *cache, int32_t op, size
  *   qrot  + p * qrot_stride  : fp32 [windows][D][GP] rotated queries
  *   score + p * score_stride : fp32 [max_blocks] block scores
  *   sel   + p * sel_stride   : int32 [max_blocks] selected blocks, ascending
- *   wsel  + p * wsel_stride  : int32 [windows + 2]: first selected entry of
- *                              each window, then k, then the block count
+ *   wsel  + p * wsel_stride  : int32 [windows + 3]: first selected entry of
+ *                              each window, then k, then the block count;
+ *                              for pair 0 then the call's selected blocks
+ *                              per split-K partition
  *   part  + p * part_stride  : fp32 [max_splits][GP * (D + 2)]: split-K
  *                              partials (max, sum, accumulator per head; a
  *                              window's splits hold it in the window's

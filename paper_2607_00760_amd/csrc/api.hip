@@ -88,7 +88,7 @@ struct mosaic_cache {
         w.bsize = b + wsl.bsize_off; w.bsize_stride = wsl.bsize_stride;
         w.selinfo = (uint2 *)(b + wsl.selinfo_off); w.selinfo_stride = wsl.selinfo_stride;
         w.wres = (float *)(b + wsl.wres_off); w.wres_stride = wsl.wres_stride;
-        w.max_blocks = max_blocks; w.max_splits = max_splits;
+        w.max_blocks = max_blocks; w.max_splits = max_splits; w.max_sel = max_sel;
         return w;
     }
 };
@@ -197,6 +197,10 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     c->npairs = num_seqs * params->num_kv_heads;
     c->GP = params->group_size <= 4 ? 4 : 8;
     c->nw = (max_tokens + params->rot_window - 1) / params->rot_window;
+    if (c->nw > MAX_WINDOWS) {
+        delete c;
+        return fail(MOSAIC_ERR_UNSUPPORTED, "%d rotation windows per sequence (at most %d)", (max_tokens + params->rot_window - 1) / params->rot_window, MAX_WINDOWS);
+    }
     c->max_desc = max_tokens / SEG + 2;
     int maxrec = 0, maxtok = 0, minb = params->default_block;
     const int eb = params->value_fp8 ? 1 : 2;          // bytes per value of a token record
@@ -223,7 +227,7 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     const int64_t max_budget = ((int64_t)c->max_desc * SEG * params->select_num + params->select_den - 1) /
                                params->select_den;
     c->max_sel = (int)std::min<int64_t>(c->max_blocks, (max_budget + minb - 1) / minb + 1);
-    c->max_splits = (c->max_sel + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS + c->nw + 1;
+    c->max_splits = (c->max_sel + SPLIT_MIN - 1) / SPLIT_MIN + c->nw + 1;
     // arena layout
     mosaic_layout &l = c->lay;
     std::memset(&l, 0, sizeof(l));
@@ -256,8 +260,9 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     wregion(w.qrot_off, w.qrot_stride, (uint64_t)c->nw * D * c->GP * 4);
     wregion(w.score_off, w.score_stride, (uint64_t)c->max_blocks * 4);
     wregion(w.sel_off, w.sel_stride, (uint64_t)c->max_blocks * 4);
-    // wsel: window starts in the selected list, k, block count
-    wregion(w.wsel_off, w.wsel_stride, (uint64_t)(c->nw + 2) * 4);
+    // wsel: window starts in the selected list, k, block count (pair 0: and
+    // the call's blocks per split)
+    wregion(w.wsel_off, w.wsel_stride, (uint64_t)(c->nw + 3) * 4);
     // part: split partials (max, sum, unrotated accumulator per head)
     wregion(w.part_off, w.part_stride, (uint64_t)c->max_splits * c->GP * (D + 2) * 4);
     wregion(w.tag_off, w.tag_stride, (uint64_t)c->max_splits * 4);

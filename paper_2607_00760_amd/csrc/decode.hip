@@ -778,7 +778,7 @@ __device__ __forceinline__ bool radix_pick(const uint32_t *hc, uint32_t *hn, uin
 // written in ascending block order (one scan of the taken counts) together
 // with each entry's record info, and the list position where each rotation
 // window starts.
-constexpr int TOPK_MAXW = 1024;                            // rotation windows tracked in LDS
+constexpr int TOPK_MAXW = MAX_WINDOWS;                     // rotation windows tracked in LDS
 
 // first block of each of the first nwl rotation windows (windows past the
 // last segment start at nb)
@@ -791,24 +791,9 @@ __device__ __forceinline__ void window_firsts(const Geom &g, int p, int nb, int 
     }
 }
 
-// list positions of the windows past the LDS slots (binary search of the
-// finished list), then k and the block count
-__device__ __forceinline__ void window_tail(const Geom &g, int p, int nb, int ndesc, int nwl, int k,
-                                            const int32_t *sel, int32_t *wsel) {
-    const int tid = threadIdx.x;
-    if (g.nw > nwl) {
-        __syncthreads();                                   // (sel from every thread)
-        const int segs_per_win = g.W / SEG;
-        const Desc *gd = g.desc_of(p);
-        for (int w = nwl + tid; w < g.nw; w += 1024) {
-            const int s0 = w * segs_per_win;
-            const int fb = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
-            int lo = 0, hi = k;
-            while (lo < hi) { const int mid = (lo + hi) >> 1; if (sel[mid] < fb) lo = mid + 1; else hi = mid; }
-            wsel[w] = lo;
-        }
-    }
-    if (tid == 0) { wsel[g.nw] = k; wsel[g.nw + 1] = nb; }
+// k and the block count after the window starts
+__device__ __forceinline__ void window_tail(const Geom &g, int nb, int k, int32_t *wsel) {
+    if (threadIdx.x == 0) { wsel[g.nw] = k; wsel[g.nw + 1] = nb; }
 }
 
 // Up to 16 K keys: thread t owns the blocks [16 t, 16 t + 16); their keys
@@ -908,7 +893,7 @@ __device__ __forceinline__ void topk_reg(const Geom &g, const WsGeom &ws, int p,
         const int t = f / TOPK_KPT, off = f % TOPK_KPT;
         wsel[w] = (int)(tpos[t] + (uint32_t)__popc(tmk[t] & ((1u << off) - 1u)));
     }
-    window_tail(g, p, nb, ndesc, nwl, k, sel, wsel);
+    window_tail(g, nb, k, wsel);
 }
 
 // More keys (long contexts): each lane reads four consecutive keys (one
@@ -1113,7 +1098,7 @@ __device__ __forceinline__ void topk_big(const Geom &g, const WsGeom &ws, int p,
     const int k = budget > 0 ? (int)posc : 0;
     for (int w = tid; w < nwl; w += 1024)
         if (budget <= 0 || fbw[w] >= nb) wsel[w] = k;
-    window_tail(g, p, nb, ndesc, nwl, k, sel, wsel);
+    window_tail(g, nb, k, wsel);
 }
 
 __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
@@ -1142,20 +1127,112 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
 // pair's token arena, and r << 8 | log2g << 16 | log2b << 20
 typedef uint2 BlkInfo;
 
-// split s of a pair: window w and its entries e0, e0 + stride, e0 + 2 stride,
-// ... (cnt of them); w = -2 past the end.  A window's n selected entries go
-// to ceil(n / SPLIT_BLOCKS) splits dealt round-robin, so every split of a
-// window holds the same mix of 16-, 8- and 4-token blocks (the list is in
-// block order, where blocks of one size cluster), which balances the
-// splits' tokens.  The list bounds are clamped to [0, lim] (the list's
+// Split-K plan of a call.  The selected blocks of all pairs are spread over
+// the attention workgroups that the device runs at once (split_slots), so
+// that the attention runs as one round of workgroups: bps blocks per split,
+// bps = ceil(selected blocks / slots left once every non-empty window and
+// every update buffer has its rounding split), within [SPLIT_MIN,
+// SPLIT_MAX].  Window w of a pair with n selected entries gets ceil(n / bps)
+// splits dealt round-robin, so every split of a window holds the same mix of
+// 16-, 8- and 4-token blocks (the list is in block order, where blocks of one
+// size cluster); a pair's splits are its windows' in order, then one for its
+// update buffer.  Every kernel that numbers splits derives the same plan from
+// the top-k's window bounds.  List bounds are clamped to [0, lim] (the list's
 // capacity), so that no workspace content can send an index outside it.
-__device__ __forceinline__ void split_of(const int32_t *wsel, int nw, int s, int lim, int &w_out, int &e0,
+
+// f(n) for the selected entries n of each window of a pair, in window order
+// (eight windows' bounds per round trip)
+template <typename F>
+__device__ __forceinline__ void for_windows(const int32_t *wsel, int nw, int lim, F f) {
+    for (int w0 = 0; w0 < nw; w0 += 8) {
+        int v[9];
+#pragma unroll
+        for (int i = 0; i <= 8; ++i) v[i] = wsel[min(w0 + i, nw)];
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            if (w0 + i < nw) {
+                const int a = min(max(v[i], 0), lim), b = min(max(v[i + 1], a), lim);
+                f(b - a);
+            }
+    }
+}
+
+// block-wide sum over blockDim.x threads (a multiple of 64); red: 16 words of LDS
+__device__ __forceinline__ int block_sum(int v, int *red) {
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nwv = blockDim.x >> 6;
+    const int x = (int)__builtin_amdgcn_readlane((int)wave_scan_add((uint32_t)v), 63);
+    if (lane == 0) red[wv] = x;
+    __syncthreads();
+    int t = 0;
+    for (int i = 0; i < nwv; ++i) t += red[i];
+    __syncthreads();
+    return t;
+}
+
+__device__ __forceinline__ bool pair_has_buf(const Geom &g, int p) {
+    int nf, prov, nbuf;
+    pair_ndesc(*g.meta_of(p), nf, prov, nbuf);
+    return nbuf > 0;
+}
+
+__device__ __forceinline__ const int32_t *wsel_of(const WsGeom &ws, int p) { return ws.wsel + (uint64_t)p * (ws.wsel_stride / 4); }
+
+// blocks per split of this call (every thread of the block gets it)
+__device__ __forceinline__ int split_blocks(const Geom &g, const WsGeom &ws, int *red) {
+    int ksum = 0, extra = 0;
+    for (int p = threadIdx.x; p < g.npairs; p += blockDim.x) {
+        const bool buf = pair_has_buf(g, p);
+        for_windows(wsel_of(ws, p), g.nw, ws.max_blocks, [&](int n) { ksum += n; extra += n > 0 ? 1 : 0; });
+        extra += buf ? 1 : 0;
+    }
+    ksum = block_sum(ksum, red);
+    extra = block_sum(extra, red);
+    const int avail = max(ws.split_slots - extra, max(ws.split_slots / 4, 1));
+    return min(max((ksum + avail - 1) / avail, SPLIT_MIN), SPLIT_MAX);
+}
+
+// splits of pair p's windows (nbuf > 0 adds the buffer's)
+__device__ __forceinline__ int pair_splits(const Geom &g, const WsGeom &ws, int p, int bps) {
+    const bool buf = pair_has_buf(g, p);
+    int t = 0;
+    for_windows(wsel_of(ws, p), g.nw, ws.max_blocks, [&](int n) { t += (n + bps - 1) / bps; });
+    return t + (buf ? 1 : 0);
+}
+
+// workgroup gidx of the flattened plan -> its pair and the split's index in
+// the pair, or p = -1 past the last split; scan: 16 words of LDS
+__device__ __forceinline__ void plan_locate(const Geom &g, const WsGeom &ws, int bps, int gidx, int *scan,
+                                            int &p_out, int &s_out) {
+    __shared__ int loc[2];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, nwv = blockDim.x >> 6;
+    if (tid == 0) { loc[0] = -1; loc[1] = 0; }
+    int carry = 0;
+    for (int p0 = 0; p0 < g.npairs; p0 += blockDim.x) {     // block order: uniform trip count
+        const int p = p0 + tid;
+        const int n = p < g.npairs ? pair_splits(g, ws, p, bps) : 0;
+        const uint32_t x = wave_scan_add((uint32_t)n);
+        if (lane == 63) scan[wv] = (int)x;
+        __syncthreads();
+        int before = carry, tot = 0;
+        for (int i = 0; i < nwv; ++i) { before += i < wv ? scan[i] : 0; tot += scan[i]; }
+        const int first = before + (int)x - n;                 // this pair's first workgroup
+        if (n > 0 && gidx >= first && gidx < first + n) { loc[0] = p; loc[1] = gidx - first; }
+        carry += tot;
+        __syncthreads();
+    }
+    p_out = loc[0];
+    s_out = loc[1];
+}
+
+// split s of pair p: window w and its entries e0, e0 + stride, e0 + 2 stride,
+// ... (cnt of them); w = -2 past the windows' splits (total of them)
+__device__ __forceinline__ void split_of(const int32_t *wsel, int nw, int s, int lim, int bps, int &w_out, int &e0,
                                          int &stride, int &cnt, int &total) {
     int acc = 0;
     w_out = -2; e0 = 0; stride = 1; cnt = 0;
     for (int w = 0; w < nw; ++w) {
         const int a = min(max(wsel[w], 0), lim), b = min(max(wsel[w + 1], a), lim);
-        const int nsp = (b - a + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS;
+        const int nsp = (b - a + bps - 1) / bps;
         if (w_out == -2 && s < acc + nsp) {
             const int k = s - acc;
             w_out = w;
@@ -1180,9 +1257,9 @@ constexpr int ATTN_NWV = MOSAIC_ATTN_WAVES;  // waves per attention workgroup
 #define MOSAIC_ATTN_WPE 2
 #endif
 #define ATTN_WPE MOSAIC_ATTN_WPE             // waves per SIMD the attention's registers allow
-// block table [SPLIT_BLOCKS] + per-wave class counts (16-byte multiple)
-constexpr int ATTN_HDR_BYTES = (8 * SPLIT_BLOCKS + ATTN_NWV * 4 * 4 + 15) / 16 * 16;
-static_assert(SPLIT_BLOCKS <= 64 * ATTN_NWV, "one setup thread per block of a split");
+// block table [SPLIT_MAX] + per-wave class counts (16-byte multiple)
+constexpr int ATTN_HDR_BYTES = (8 * SPLIT_MAX + ATTN_NWV * 4 * 4 + 15) / 16 * 16;
+static_assert(SPLIT_MAX <= 64 * ATTN_NWV, "one setup thread per block of a split");
 
 // x = hi + lo with hi, lo in the MFMA's 16-bit type (round to nearest even);
 // hi + lo carries x to ~16 (bf16) or ~22 (fp16) significant bits
@@ -1345,26 +1422,27 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
     using M8 = typename Mma<DT>::v8;
     constexpr int NWV = ATTN_NWV;
     extern __shared__ __align__(16) uint8_t smem[];
-    BlkInfo *blk = (BlkInfo *)smem;                         // [SPLIT_BLOCKS], ordered 16, 8, 4
-    int *wcnt = (int *)(smem + 8 * SPLIT_BLOCKS);           // [NWV][4] blocks per size class
+    BlkInfo *blk = (BlkInfo *)smem;                         // [SPLIT_MAX], ordered 16, 8, 4
+    int *wcnt = (int *)(smem + 8 * SPLIT_MAX);              // [NWV][4] blocks per size class
     uint8_t *wbase = smem + ATTN_HDR_BYTES;                 // [NWV] tiles
-
-    // XCD-aware order: workgroups are dealt to the eight XCDs in turn, so
-    // block b runs on XCD b % 8.  Every split of a pair gets the same residue,
-    // which keeps the pair's R_v, rotated queries and selection in one L2.
-    const int bid = blockIdx.x, xcd = bid & 7, idx = bid >> 3;
-    const int p = xcd + 8 * (idx / ws.max_splits), s = idx % ws.max_splits;
-    if (p >= g.npairs) return;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, q4 = lane >> 4;
     uint8_t *tile = wbase + wave * TILE_BYTES;
+
+    // the call's plan: workgroup b takes the b-th split of the flattened list
+    // (pairs in order, each pair's splits in order); the grid covers every plan
+    const int bps = split_blocks(g, ws, wcnt);
+    if (blockIdx.x == 0 && tid == 0) ws.wsel[g.nw + 2] = bps;    // for the combine (pair 0's list header)
+    int p, s;
+    plan_locate(g, ws, bps, blockIdx.x, wcnt, p, s);
+    if (p < 0 || s >= ws.max_splits) return;
 
     const PairMeta meta = *g.meta_of(p);
     int nf, prov, nbuf;
     pair_ndesc(meta, nf, prov, nbuf);
     const int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
     int w, e0, estride, nbk, total;
-    split_of(wsel, g.nw, s, ws.max_blocks, w, e0, estride, nbk, total);
+    split_of(wsel, g.nw, s, ws.max_blocks, bps, w, e0, estride, nbk, total);
     int32_t *tag = ws.tag + (uint64_t)p * (ws.tag_stride / 4);
     float *part = ws.part + (uint64_t)p * (ws.part_stride / 4) + (uint64_t)s * GP * (D + 2);
     const bool is_buf = (w == -2) && (s == total) && nbuf > 0;
@@ -1780,9 +1858,10 @@ __global__ void __launch_bounds__(CMB_THREADS) k_combine(Geom g, WsGeom ws, floa
     // this slot's splits: the windows' splits are numbered window by window,
     // then the buffer's (the attention's numbering), s0 = those before it
     int s0 = 0, nsp = 0;
+    const int bps = min(max(ws.wsel[g.nw + 2], SPLIT_MIN), SPLIT_MAX);   // the attention's plan
     for (int x = 0; x <= min(w, g.nw - 1); ++x) {
         const int a = min(max(wsel[x], 0), lim), b = min(max(wsel[x + 1], a), lim);
-        const int n = (b - a + SPLIT_BLOCKS - 1) / SPLIT_BLOCKS;
+        const int n = (b - a + bps - 1) / bps;
         if (x < w) s0 += n; else nsp = n;
     }
     if (w == g.nw) nsp = nbuf > 0 ? 1 : 0;
@@ -1897,9 +1976,26 @@ int max_keep(const Geom &g) {
     return r;
 }
 
+// attention workgroups the device holds at once: ATTN_WPE waves per SIMD,
+// four SIMDs per compute unit, ATTN_NWV waves per workgroup
+int attn_slots() {
+    static int cached[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+    const int d = dev & 63;
+    if (cached[d] == 0) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
+        cached[d] = cus * 4 * ATTN_WPE / ATTN_NWV;
+    }
+    return cached[d];
+}
+
 template <int DT, int GP>
-hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, float *out, float scale,
+hipError_t launch_decode_dt(const Geom &g, const WsGeom &w_in, const uint16_t *q, float *out, float scale,
                             int max_desc_used, int max_windows_used, hipStream_t s, hipEvent_t *ev) {
+    WsGeom w = w_in;
+    w.split_slots = attn_slots();
     const int nwq = g.rotated ? max_windows_used : 1;
     const bool small = max_keep(g) <= 48;
     bool fixed = true;                         // every possible kept count in {16, 32, 48}
@@ -1926,8 +2022,14 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w, const uint16_t *q, f
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev) hipEventRecord(ev[3], s);
     {
+        // the plan has at most max(slots, selected blocks / SPLIT_MAX) splits
+        // of whole blocks plus one rounding split per window and per buffer,
+        // and never more than every pair's whole partial array
         const size_t smem = ATTN_HDR_BYTES + (size_t)ATTN_NWV * TILE_BYTES;
-        const dim3 grid(w.max_splits * ((g.npairs + 7) / 8 * 8)), block(64 * ATTN_NWV);
+        const long long extra = (long long)g.npairs * (g.nw + 1);
+        const long long whole = std::max<long long>(w.split_slots, (long long)g.npairs * ceil_div(w.max_sel, SPLIT_MAX));
+        const long long nwg = std::min<long long>(whole + extra, (long long)g.npairs * w.max_splits);
+        const dim3 grid((unsigned)nwg), block(64 * ATTN_NWV);
         if (g.fp8) {
             if (fixed) hipLaunchKernelGGL((k_attn<DT, GP, 48, true, true>), grid, block, smem, s, g, w, scale, q);
             else if (small) hipLaunchKernelGGL((k_attn<DT, GP, 48, false, true>), grid, block, smem, s, g, w, scale, q);

@@ -10,10 +10,12 @@ constexpr int D = 128;        // head dim
 constexpr int SEG = 64;       // strategy segment (tokens)
 constexpr int UBUF = 32;      // update buffer (tokens)
 constexpr int WAVE = 64;
-#ifndef MOSAIC_SPLIT_BLOCKS
-#define MOSAIC_SPLIT_BLOCKS 64
-#endif
-constexpr int SPLIT_BLOCKS = MOSAIC_SPLIT_BLOCKS;  // selected blocks per split-K partition
+// selected blocks per split-K partition: chosen per call between these bounds
+// (the fewest sizes the per-pair partial arrays, the most the attention's
+// block table)
+constexpr int SPLIT_MIN = 48;
+constexpr int SPLIT_MAX = 128;
+constexpr int MAX_WINDOWS = 1024;  // rotation windows per sequence (the selection tracks them in LDS)
 constexpr int SCORE_SEGS = 128;    // segments per block-scoring workgroup (one launch round)
 constexpr int CMB_COLS = 16;                  // output columns per combine workgroup
 constexpr int CMB_NCC = D / CMB_COLS;         // column blocks of an output row
@@ -73,7 +75,8 @@ struct WsGeom {               // decode workspace
     uint8_t *bsize; uint64_t bsize_stride;  // [max_blocks]: per block, log2 of its token count
     uint2 *selinfo; uint64_t selinfo_stride; // [max_blocks]: blk_info of each selected entry
     float *wres; uint64_t wres_stride;      // [CMB_NCC][nw + 1][GP][CMB_RES]: per-window merged results
-    int max_blocks, max_splits;
+    int max_blocks, max_splits, max_sel;
+    int split_slots;                        // attention workgroups resident at once on the device
 };
 
 // a block's record: its byte offset in the pair's token arena, and
