@@ -631,7 +631,7 @@ def main():
                    host_cores=cores, cpu_model=model, single_thread_us_per_pair=round(per_pair * 1e6, 1),
                    sample=(f"oracle decode of {ns} of {npairs} (sequence, kv head) pairs, one per thread on {ns} "
                            f"threads ({t_dec:.2f} s wall); a step of {npairs} pairs x {nlayers} layer(s) is "
-                           f"{rounds} rounds of {cores} pairs at the mean per-pair time"
+                           f"{rounds} rounds of {min(npairs, cores)} pairs at the mean per-pair time"
                            + (f"; pairs compressed on the first 1/{frac} of their tokens, x{frac}" if frac > 1 else "")
                            + f"; oracle compress of the sample took {sum(r[1] for r in res):.1f} thread-s"))
         if frac == 1:
