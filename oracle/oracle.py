@@ -20,6 +20,9 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "mosaic_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
+# a separately built copy of the same source to load instead (the sanitizer
+# test builds one with AddressSanitizer and UndefinedBehaviorSanitizer)
+_LIB_OVERRIDE = os.environ.get("MOSAIC_ORACLE_LIB")
 D = 128
 
 CFLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
@@ -100,9 +103,12 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-            build(force=True)
-        L = C.CDLL(_LIB)
+        if _LIB_OVERRIDE:
+            L = C.CDLL(_LIB_OVERRIDE)
+        else:
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build(force=True)
+            L = C.CDLL(_LIB)
         fp, u16p, u8p, i32p, f64p = (C.POINTER(C.c_float), C.POINTER(C.c_uint16), C.POINTER(C.c_uint8),
                                      C.POINTER(C.c_int32), C.POINTER(C.c_double))
         L.orc_f16_to_f32.argtypes = [C.c_uint16]; L.orc_f16_to_f32.restype = C.c_float

@@ -69,43 +69,47 @@ def load() -> C.CDLL:
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_00760_amd.build.build() "
                               "(there is no fallback path)")
-        L = C.CDLL(LIB_PATH)
-        vp, sz = C.c_void_p, C.c_size_t
-        L.mosaic_params_default.argtypes = [C.POINTER(MosaicParams)]
-        L.mosaic_params_default.restype = None
-        L.mosaic_cache_create.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, C.c_int32, C.POINTER(vp)]
-        L.mosaic_cache_arena_bytes.argtypes = [vp, C.POINTER(sz)]
-        L.mosaic_cache_bind.argtypes = [vp, vp, sz]
-        L.mosaic_cache_destroy.argtypes = [vp]
-        L.mosaic_cache_layout.argtypes = [vp, C.POINTER(MosaicLayout)]
-        L.mosaic_workspace_bytes.argtypes = [vp, C.c_int32, C.POINTER(sz)]
-        L.mosaic_decode_ws_layout.argtypes = [vp, C.POINTER(MosaicWsLayout)]
-        L.mosaic_compress.argtypes = [vp, vp, vp, C.c_int64, C.POINTER(C.c_int32), vp, vp, vp, sz, vp]
-        L.mosaic_append.argtypes = [vp, vp, vp, vp]
-        L.mosaic_decode_attention.argtypes = [vp, vp, vp, C.c_float, vp, sz, vp]
-        L.mosaic_decode_attention_noalloc.argtypes = [vp, vp, vp, C.c_float, vp]
-        L.mosaic_dense_workspace_bytes.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(sz)]
-        L.mosaic_dense_decode_attention.argtypes = [vp, vp, vp, vp, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
-                                                    C.c_int32, C.c_int64, C.c_int32, vp, C.c_float, vp, sz, vp]
-        L.mosaic_cache_stats.argtypes = [vp, C.POINTER(MosaicStats), vp]
-        L.mosaic_rotation_workspace_bytes.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, C.POINTER(sz)]
-        L.mosaic_compute_rotations.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, vp, vp, C.c_int64,
-                                               C.POINTER(C.c_int32), vp, vp, vp, vp, vp, sz, vp]
-        L.mosaic_reorder_workspace_bytes.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, C.POINTER(sz)]
-        L.mosaic_reorder_rotations.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, vp, vp, C.c_int64,
-                                               C.POINTER(C.c_int32), vp, vp, vp, sz, vp]
-        L.mosaic_set_timing.argtypes = [vp, C.c_int32]
-        L.mosaic_decode_timing.argtypes = [vp, C.POINTER(C.c_float)]
-        L.mosaic_seq_tokens.argtypes = [vp, C.c_int32]
-        L.mosaic_seq_tokens.restype = C.c_int32
-        L.mosaic_last_error.argtypes = []
-        L.mosaic_last_error.restype = C.c_char_p
-        for n in EXPORTED:
-            f = getattr(L, n)
-            if f.restype is C.c_int:   # default restype -> mosaic_status
-                f.restype = C.c_int32
-        _lib = L
+        _lib = bind_signatures(C.CDLL(LIB_PATH))
     return _lib
+
+
+def bind_signatures(L: C.CDLL) -> C.CDLL:
+    """Set the argument and result types of every exported entry point of L."""
+    vp, sz = C.c_void_p, C.c_size_t
+    L.mosaic_params_default.argtypes = [C.POINTER(MosaicParams)]
+    L.mosaic_params_default.restype = None
+    L.mosaic_cache_create.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, C.c_int32, C.POINTER(vp)]
+    L.mosaic_cache_arena_bytes.argtypes = [vp, C.POINTER(sz)]
+    L.mosaic_cache_bind.argtypes = [vp, vp, sz]
+    L.mosaic_cache_destroy.argtypes = [vp]
+    L.mosaic_cache_layout.argtypes = [vp, C.POINTER(MosaicLayout)]
+    L.mosaic_workspace_bytes.argtypes = [vp, C.c_int32, C.POINTER(sz)]
+    L.mosaic_decode_ws_layout.argtypes = [vp, C.POINTER(MosaicWsLayout)]
+    L.mosaic_compress.argtypes = [vp, vp, vp, C.c_int64, C.POINTER(C.c_int32), vp, vp, vp, sz, vp]
+    L.mosaic_append.argtypes = [vp, vp, vp, vp]
+    L.mosaic_decode_attention.argtypes = [vp, vp, vp, C.c_float, vp, sz, vp]
+    L.mosaic_decode_attention_noalloc.argtypes = [vp, vp, vp, C.c_float, vp]
+    L.mosaic_dense_workspace_bytes.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(sz)]
+    L.mosaic_dense_decode_attention.argtypes = [vp, vp, vp, vp, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                                C.c_int32, C.c_int64, C.c_int32, vp, C.c_float, vp, sz, vp]
+    L.mosaic_cache_stats.argtypes = [vp, C.POINTER(MosaicStats), vp]
+    L.mosaic_rotation_workspace_bytes.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, C.POINTER(sz)]
+    L.mosaic_compute_rotations.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, vp, vp, C.c_int64,
+                                           C.POINTER(C.c_int32), vp, vp, vp, vp, vp, sz, vp]
+    L.mosaic_reorder_workspace_bytes.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, C.POINTER(sz)]
+    L.mosaic_reorder_rotations.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, vp, vp, C.c_int64,
+                                           C.POINTER(C.c_int32), vp, vp, vp, sz, vp]
+    L.mosaic_set_timing.argtypes = [vp, C.c_int32]
+    L.mosaic_decode_timing.argtypes = [vp, C.POINTER(C.c_float)]
+    L.mosaic_seq_tokens.argtypes = [vp, C.c_int32]
+    L.mosaic_seq_tokens.restype = C.c_int32
+    L.mosaic_last_error.argtypes = []
+    L.mosaic_last_error.restype = C.c_char_p
+    for n in EXPORTED:
+        f = getattr(L, n)
+        if f.restype is C.c_int:   # default restype -> mosaic_status
+            f.restype = C.c_int32
+    return L
 
 
 def check(status: int):

@@ -352,7 +352,7 @@ mosaic_status mosaic_compress(mosaic_cache *c, const void *k, const void *v, int
     hipStream_t s = (hipStream_t)stream;
     const Geom g = c->geom();
     int32_t *ctx_dev = (int32_t *)(c->arena + c->ctx_off);
-    hipError_t e = hipMemcpyAsync(ctx_dev, ctx_lens_host, sizeof(int32_t) * c->num_seqs, hipMemcpyHostToDevice, s);
+    hipError_t e = launch_ctx_copy(ctx_dev, ctx_lens_host, c->num_seqs, s);
     if (e != hipSuccess) return hip_fail(e, "copy of context lengths");
     if (c->rotated && (e = launch_copy_rot(g, rot_k, rot_v, s)) != hipSuccess) return hip_fail(e, "rotation copy");
     e = launch_compress(g, (const uint16_t *)k, (const uint16_t *)v, seq_stride, ctx_dev, maxL / SEG, any_tail, s);

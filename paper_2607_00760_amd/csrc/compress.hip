@@ -720,6 +720,11 @@ __global__ void __launch_bounds__(1024) k_sel_permute(float *rk, float *rv, int 
 
 }  // namespace
 
+// the context lengths of a compress call, from the caller's host array into the arena
+hipError_t launch_ctx_copy(int32_t *dst_dev, const int32_t *src_host, int n, hipStream_t s) {
+    return hipMemcpyAsync(dst_dev, src_host, sizeof(int32_t) * (size_t)n, hipMemcpyHostToDevice, s);
+}
+
 hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, hipStream_t s) {
     hipLaunchKernelGGL(k_copy_rot, dim3(g.nw, g.npairs), dim3(256), 0, s, g, rk, rv);
     return hipGetLastError();

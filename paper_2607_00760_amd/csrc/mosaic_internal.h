@@ -197,6 +197,7 @@ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // ---------------------------------------------------------------- launchers
 // (implemented in the .hip files; all return hipError_t of the launch)
+hipError_t launch_ctx_copy(int32_t *dst_dev, const int32_t *src_host, int n, hipStream_t s);
 hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, hipStream_t s);
 hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, int64_t seq_stride,
                            const int32_t *ctx_dev, int max_full_segs, int any_tail, hipStream_t s);
