@@ -137,8 +137,10 @@ typedef struct {
 mosaic_status mosaic_cache_layout(const mosaic_cache *cache, mosaic_layout *out);
 
 enum { MOSAIC_OP_COMPRESS = 0, MOSAIC_OP_APPEND = 1, MOSAIC_OP_DECODE = 2 };
-/* Workspace bytes an operation needs (0 if none).  Depends only on the
- * cache's shape and capacity, so one allocation serves every call. */
+/* Workspace bytes an operation can use (0 if none).  Depends only on the
+ * cache's shape and capacity, so one allocation serves every call.  DECODE
+ * requires its workspace; COMPRESS's is optional (see mosaic_compress): a
+ * worst-case slot of packed records per (pair, segment). */
 mosaic_status mosaic_workspace_bytes(const mosaic_cache *cache, int32_t op, size_t *bytes);
 
 /* Layout of the decode workspace (inspection): per pair p,
@@ -185,9 +187,17 @@ mosaic_status mosaic_decode_ws_layout(const mosaic_cache *cache, mosaic_ws_layou
  *               / W).  NULL (both) iff the cache was created with rotated = 0.
  *   Full segments get their own strategy.  The remaining ctx_len mod S tokens
  *   take the update path (buffer, provisional flush), as if appended.
- * Replaces any previous contents.  ws may be NULL when the workspace size is 0.
+ * Replaces any previous contents.
+ *   ws        : NULL, or 16-byte aligned and at least
+ *               mosaic_workspace_bytes(MOSAIC_OP_COMPRESS) bytes.  With it each
+ *               token is rotated once: a segment is packed right after its
+ *               strategy is chosen, into its slot of ws, and the records move
+ *               to their offsets once all sizes are known.  With NULL the
+ *               tokens are rotated twice (strategy pass, then packing pass)
+ *               and nothing extra is needed.  Both give the same bytes.
  * Errors: STATE (not bound), CAPACITY (ctx_len > max_tokens),
- * INVALID (NULL, negative length, misaligned pointer, seq_stride < max ctx). */
+ * INVALID (NULL, negative length, misaligned pointer, seq_stride < max ctx,
+ * workspace too small). */
 mosaic_status mosaic_compress(mosaic_cache *cache, const void *k, const void *v, int64_t seq_stride,
                               const int32_t *ctx_lens_host, const float *rot_k, const float *rot_v,
                               void *ws, size_t ws_bytes, void *stream);

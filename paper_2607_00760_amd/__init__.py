@@ -120,9 +120,12 @@ class MosaicCache:
     def seq_tokens(self, s):
         return int(self.lib.mosaic_seq_tokens(self._h, s))
 
-    def compress(self, k, v, ctx_lens, rot_k=None, rot_v=None):
+    def compress(self, k, v, ctx_lens, rot_k=None, rot_v=None, single_pass: bool = True):
         """k, v: [num_seqs][Hkv][seq_stride][128] (cache dtype); ctx_lens: host ints;
-        rot_k/rot_v: [num_seqs][Hkv][num_windows][128][128] fp32 or None."""
+        rot_k/rot_v: [num_seqs][Hkv][num_windows][128][128] fp32 or None.
+        single_pass: rotate each token once, packing through a transient
+        workspace (the library's worst-case segment slots); False: two passes,
+        no extra memory.  Both write the same bytes."""
         import torch
         _check_tensor(k, "k", self.elem, self.device)
         _check_tensor(v, "v", self.elem, self.device)
@@ -136,10 +139,15 @@ class MosaicCache:
             if tuple(rot_k.shape) != want or tuple(rot_v.shape) != want:
                 raise ValueError(f"rotation shape {tuple(rot_k.shape)} != {want}")
         lens = (C.c_int32 * self.num_seqs)(*[int(x) for x in ctx_lens])
+        ws = None
+        if single_pass:
+            n = C.c_size_t()
+            check(self.lib.mosaic_workspace_bytes(self._h, OP_COMPRESS, C.byref(n)))
+            ws = torch.empty(max(n.value, 16), dtype=torch.uint8, device=self.device)
         with torch.cuda.device(self.device):
             check(self.lib.mosaic_compress(self._h, _ptr(k), _ptr(v), k.shape[2], lens, _ptr(rot_k), _ptr(rot_v),
-                                           None, 0, _stream(self.device)))
-        self._keep = (k, v, rot_k, rot_v)      # alive until the enqueued work completes
+                                           _ptr(ws), 0 if ws is None else ws.numel(), _stream(self.device)))
+        self._keep = (k, v, rot_k, rot_v, ws)  # alive until the enqueued work completes
 
     def append(self, k_new, v_new):
         """k_new, v_new: [num_seqs][Hkv][128]."""

@@ -47,6 +47,7 @@ struct mosaic_cache {
     mosaic_params P;
     int num_seqs, max_tokens, rotated, npairs, GP, nw, max_desc, max_blocks, max_sel, max_splits;
     int maxrec, minb;
+    uint32_t slot_tok, slot_sc;  // single-pass compression: worst-case bytes of a segment's records
     mosaic_layout lay;
     mosaic_ws_layout wsl;
     uint64_t ctx_off;            // device int32 [num_seqs] (inside the arena)
@@ -213,6 +214,8 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     maxtok = std::max(maxtok, eb * params->default_keep + 16 / params->default_group);
     for (int i = 0; i < 3; ++i) minb = std::min(minb, params->block_cand[i]);
     c->maxrec = maxrec; c->minb = minb;
+    c->slot_tok = (uint32_t)(SEG * 2 * maxtok + 15) / 16 * 16;
+    c->slot_sc = (uint32_t)((SEG / minb) * maxrec + 15) / 16 * 16;
     // + 256: the decode kernels read whole 16-byte bitmaps and up to 2 * 128 bytes
     // of values past a vector (never used), which must stay inside the arena
     const uint64_t tok_bytes = (uint64_t)c->max_desc * SEG * 2 * maxtok + 256;
@@ -317,7 +320,8 @@ mosaic_status mosaic_decode_ws_layout(const mosaic_cache *c, mosaic_ws_layout *o
 
 mosaic_status mosaic_workspace_bytes(const mosaic_cache *c, int32_t op, size_t *bytes) {
     if (!c || !bytes) return fail(MOSAIC_ERR_INVALID, "NULL argument");
-    if (op == MOSAIC_OP_COMPRESS || op == MOSAIC_OP_APPEND) *bytes = 0;
+    if (op == MOSAIC_OP_COMPRESS) *bytes = (size_t)c->npairs * c->max_desc * ((size_t)c->slot_tok + c->slot_sc);
+    else if (op == MOSAIC_OP_APPEND) *bytes = 0;
     else if (op == MOSAIC_OP_DECODE) *bytes = c->wsl.total;
     else return fail(MOSAIC_ERR_INVALID, "unknown op %d", op);
     return ok();
@@ -331,7 +335,6 @@ int32_t mosaic_seq_tokens(const mosaic_cache *c, int32_t seq) {
 mosaic_status mosaic_compress(mosaic_cache *c, const void *k, const void *v, int64_t seq_stride,
                               const int32_t *ctx_lens_host, const float *rot_k, const float *rot_v, void *ws,
                               size_t ws_bytes, void *stream) {
-    (void)ws; (void)ws_bytes;
     if (!c) return fail(MOSAIC_ERR_INVALID, "NULL cache");
     if (!c->arena) return fail(MOSAIC_ERR_STATE, "cache not bound to an arena");
     if (!k || !v || !ctx_lens_host) return fail(MOSAIC_ERR_INVALID, "NULL k, v or ctx_lens_host");
@@ -349,13 +352,19 @@ mosaic_status mosaic_compress(mosaic_cache *c, const void *k, const void *v, int
     }
     if (seq_stride < maxL || seq_stride < 1) return fail(MOSAIC_ERR_INVALID, "seq_stride %lld < longest context %d",
                                                          (long long)seq_stride, maxL);
+    if (ws) {
+        const size_t need = (size_t)c->npairs * c->max_desc * ((size_t)c->slot_tok + c->slot_sc);
+        if (ws_bytes < need) return fail(MOSAIC_ERR_INVALID, "compress workspace %zu bytes < %zu required", ws_bytes, need);
+        if ((uintptr_t)ws % 16) return fail(MOSAIC_ERR_INVALID, "compress workspace not 16-byte aligned");
+    }
     hipStream_t s = (hipStream_t)stream;
     const Geom g = c->geom();
     int32_t *ctx_dev = (int32_t *)(c->arena + c->ctx_off);
     hipError_t e = launch_ctx_copy(ctx_dev, ctx_lens_host, c->num_seqs, s);
     if (e != hipSuccess) return hip_fail(e, "copy of context lengths");
     if (c->rotated && (e = launch_copy_rot(g, rot_k, rot_v, s)) != hipSuccess) return hip_fail(e, "rotation copy");
-    e = launch_compress(g, (const uint16_t *)k, (const uint16_t *)v, seq_stride, ctx_dev, maxL / SEG, any_tail, s);
+    e = launch_compress(g, (const uint16_t *)k, (const uint16_t *)v, seq_stride, ctx_dev, maxL / SEG, any_tail,
+                        (uint8_t *)ws, c->slot_tok, c->slot_sc, s);
     if (e != hipSuccess) return hip_fail(e, "compress launch");
     for (int q = 0; q < c->num_seqs; ++q) c->L[q] = ctx_lens_host[q];
     c->compressed = true;

@@ -379,8 +379,18 @@ __global__ void k_set_meta(Geom g, const int32_t *ctx) {
 }
 
 // mode 0: strategy selection of full prefill segments; mode 1: packing.
-__global__ void __launch_bounds__(256) k_prefill(Geom g, const uint16_t *k, const uint16_t *v, int64_t seq_stride,
-                                                 int mode) {
+// mode 0: choose the segment's strategy; mode 1: pack it at its descriptor's
+// offsets (both rotate the tokens); mode 2: both from one rotation, packing
+// into the segment's worst-case slot of the workspace (slot_tok + slot_sc
+// bytes per (pair, segment)), from where k_compact moves the records to their
+// offsets once the offsets are known.
+// (one instantiation per mode, so that each gets its own register budget:
+// three waves per SIMD)
+template <int MODE>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
+k_prefill(Geom g, const uint16_t *k, const uint16_t *v, int64_t seq_stride, uint8_t *ws, uint32_t slot_tok,
+          uint32_t slot_sc) {
+    constexpr int mode = MODE;
     constexpr int TPW = 16, NWV = 4;
     __shared__ SegSmem<NWV> sm;
     const int p = blockIdx.y, seg = blockIdx.x;
@@ -395,7 +405,26 @@ __global__ void __launch_bounds__(256) k_prefill(Geom g, const uint16_t *k, cons
     rotate_tile(k + base, SEG, rot, g.dtype, sm, yk);
     rotate_tile(v + base, SEG, rot ? rot + D * D : nullptr, g.dtype, sm, yv);
     const int wave = threadIdx.x >> 6;
-    if (mode == 0) {
+    if constexpr (MODE == 2) {
+        if (g.force) {
+            if (threadIdx.x == 0) { sm.strat[0] = g.def_keep; sm.strat[1] = ilog2i(g.def_group); sm.strat[2] = ilog2i(g.def_block); }
+        } else {
+            token_stats(g, yk, 0, sm, SEG);
+            token_stats(g, yv, 1, sm, SEG);
+            block_stats(g, yk, sm, SEG);
+            __syncthreads();
+            choose_strategy(g, sm);
+        }
+        __syncthreads();
+        const int r = sm.strat[0], l2g = sm.strat[1], l2b = sm.strat[2];
+        if (threadIdx.x == 0) {
+            desc->r = (uint8_t)r; desc->log2g = (uint8_t)l2g; desc->log2b = (uint8_t)l2b; desc->flags = 0;
+        }
+        uint8_t *slot = ws + ((uint64_t)p * g.max_desc + seg) * ((uint64_t)slot_tok + slot_sc);
+        pack_segment(yk, yv, r, l2g, l2b, g.trunc, g.dtype, g.fp8 != 0, slot, slot + slot_tok, SEG, sm.keys[wave], sm.x, 0);
+        return;
+    }
+    if constexpr (MODE == 0) {
         if (g.force) {
             if (threadIdx.x == 0) {
                 desc->r = (uint8_t)g.def_keep; desc->log2g = (uint8_t)ilog2i(g.def_group);
@@ -417,6 +446,23 @@ __global__ void __launch_bounds__(256) k_prefill(Geom g, const uint16_t *k, cons
         pack_segment(yk, yv, d.r, d.log2g, d.log2b, g.trunc, g.dtype, g.fp8 != 0, g.tok_of(p) + d.tok_off, g.sc_of(p) + d.sc_off,
                      SEG, sm.keys[wave], sm.x, 0);
     }
+}
+
+// The records of the single-pass compression from the segments' workspace
+// slots to their offsets (dword copies: every record run is a multiple of 4
+// bytes at a 4-byte aligned offset).
+__global__ void __launch_bounds__(256) k_compact(Geom g, const uint8_t *ws, uint32_t slot_tok, uint32_t slot_sc) {
+    const int p = blockIdx.y, seg = blockIdx.x;
+    const PairMeta *meta = g.meta_of(p);
+    if (seg >= meta->L / SEG) return;
+    const Desc d = g.desc_of(p)[seg];
+    const uint32_t tb = SEG * 2 * (uint32_t)tok_vec_bytes(d.r, d.log2g, g.trunc, g.fp8);
+    const uint32_t sb = (uint32_t)(SEG >> d.log2b) * (uint32_t)vec_bytes(d.r, d.log2g, g.trunc);
+    const uint8_t *slot = ws + ((uint64_t)p * g.max_desc + seg) * ((uint64_t)slot_tok + slot_sc);
+    const uint32_t *st = (const uint32_t *)slot, *ss = (const uint32_t *)(slot + slot_tok);
+    uint32_t *dt = (uint32_t *)(g.tok_of(p) + d.tok_off), *ds = (uint32_t *)(g.sc_of(p) + d.sc_off);
+    for (uint32_t i = threadIdx.x; i < tb / 4; i += 256) dt[i] = st[i];
+    for (uint32_t i = threadIdx.x; i < sb / 4; i += 256) ds[i] = ss[i];
 }
 
 // Exclusive scan of segment sizes per pair -> descriptor offsets and tails.
@@ -736,17 +782,21 @@ hipError_t launch_set_meta(const Geom &g, const int32_t *ctx_dev, hipStream_t s)
 }
 
 hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, int64_t seq_stride,
-                           const int32_t *ctx_dev, int max_full_segs, int any_tail, hipStream_t s) {
+                           const int32_t *ctx_dev, int max_full_segs, int any_tail, uint8_t *ws, uint32_t slot_tok,
+                           uint32_t slot_sc, hipStream_t s) {
     hipError_t e = launch_set_meta(g, ctx_dev, s);
     if (e != hipSuccess) return e;
+    const dim3 grid(max_full_segs, g.npairs);
     if (max_full_segs > 0) {
-        hipLaunchKernelGGL(k_prefill, dim3(max_full_segs, g.npairs), dim3(256), 0, s, g, k, v, seq_stride, 0);
+        if (ws) hipLaunchKernelGGL(k_prefill<2>, grid, dim3(256), 0, s, g, k, v, seq_stride, ws, slot_tok, slot_sc);
+        else hipLaunchKernelGGL(k_prefill<0>, grid, dim3(256), 0, s, g, k, v, seq_stride, ws, slot_tok, slot_sc);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     hipLaunchKernelGGL(k_scan, dim3(g.npairs), dim3(256), 0, s, g);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (max_full_segs > 0) {
-        hipLaunchKernelGGL(k_prefill, dim3(max_full_segs, g.npairs), dim3(256), 0, s, g, k, v, seq_stride, 1);
+        if (ws) hipLaunchKernelGGL(k_compact, grid, dim3(256), 0, s, g, (const uint8_t *)ws, slot_tok, slot_sc);
+        else hipLaunchKernelGGL(k_prefill<1>, grid, dim3(256), 0, s, g, k, v, seq_stride, ws, slot_tok, slot_sc);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (any_tail) {

@@ -199,8 +199,11 @@ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 // (implemented in the .hip files; all return hipError_t of the launch)
 hipError_t launch_ctx_copy(int32_t *dst_dev, const int32_t *src_host, int n, hipStream_t s);
 hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, hipStream_t s);
+// ws: NULL (two passes, each rotating the tokens) or the single-pass
+// workspace of slot_tok + slot_sc bytes per (pair, segment slot)
 hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, int64_t seq_stride,
-                           const int32_t *ctx_dev, int max_full_segs, int any_tail, hipStream_t s);
+                           const int32_t *ctx_dev, int max_full_segs, int any_tail, uint8_t *ws, uint32_t slot_tok,
+                           uint32_t slot_sc, hipStream_t s);
 hipError_t launch_set_meta(const Geom &g, const int32_t *ctx_dev, hipStream_t s);
 hipError_t launch_append(const Geom &g, const uint16_t *k, const uint16_t *v, hipStream_t s);
 // what: MAINT_FLUSH and / or MAINT_FINALIZE, the kernels to launch (each

@@ -39,8 +39,9 @@ hipError_t launch_copy_rot(const Geom &g, const float *, const float *, hipStrea
     return hipSuccess;
 }
 hipError_t launch_compress(const Geom &g, const uint16_t *, const uint16_t *, int64_t seq_stride, const int32_t *,
-                           int full_segs, int any_tail, hipStream_t) {
-    rec("compress npairs=%d stride=%lld segs=%d tail=%d", g.npairs, (long long)seq_stride, full_segs, any_tail);
+                           int full_segs, int any_tail, uint8_t *ws, uint32_t, uint32_t, hipStream_t) {
+    rec("compress npairs=%d stride=%lld segs=%d tail=%d%s", g.npairs, (long long)seq_stride, full_segs, any_tail,
+        ws ? " single-pass" : "");
     return hipSuccess;
 }
 hipError_t launch_set_meta(const Geom &g, const int32_t *, hipStream_t) {

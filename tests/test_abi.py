@@ -88,9 +88,12 @@ def test_layout_and_workspace():
         assert a % 256 == 0 and s % 256 == 0 and a + 6 * s <= b
     assert lay.rot_stride >= 2 * 3 * 128 * 128 * 4
     assert lay.token_stride >= (70000 // 64 + 1) * 64 * 2 * (2 * 48 + 16)
-    for op, pos in ((0, False), (1, False), (2, True)):
+    for op, pos in ((0, True), (1, False), (2, True)):
         assert L.mosaic_workspace_bytes(h, op, C.byref(n)) == 0
         assert (n.value > 0) == pos
+    # the optional single-pass compression workspace: a worst-case slot per (pair, segment)
+    assert L.mosaic_workspace_bytes(h, 0, C.byref(n)) == 0
+    assert n.value >= 6 * (70000 // 64 + 1) * 64 * 2 * (2 * 48 + 16)
     assert L.mosaic_workspace_bytes(h, 7, C.byref(n)) == -1
     wl = _lib.MosaicWsLayout()
     assert L.mosaic_decode_ws_layout(h, C.byref(wl)) == 0 and wl.gp == 8 and wl.max_splits > 0

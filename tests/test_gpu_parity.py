@@ -12,6 +12,7 @@ import torch
 
 from _parity import (D, assert_close, assert_state_equal, bits, gpu_cache, gpu_scores_sel, oracle_decode_all,
                      oracle_pairs, params_pair, scale_of)
+import paper_2607_00760_amd as M
 from oracle import oracle as O
 from workloads import gen
 
@@ -95,6 +96,24 @@ def test_compress_bit_exact(name):
     ops = oracle_pairs(op, spec, lay, cap)
     for p in range(spec.num_seqs * spec.hkv):
         assert_state_equal(c, p, ops[p], where=name)
+
+
+@pytest.mark.parametrize("name", ["c1", "mixed_strategies", "forced_norot_fp16", "truncated_64_g2", "fp8_search_bf16",
+                                  "ragged_bf16_w128"])
+def test_single_pass_compress_equals_two_pass(name):
+    """The single-pass compression (one rotation per token, records through
+    the workspace slots) writes the same arena as the two-pass one."""
+    spec, lay, lp, op, cap = _case(name)
+    caches = []
+    for single in (True, False):
+        c = M.MosaicCache(lp, spec.num_seqs, cap, rotated=lay["rot_k"] is not None, device="cuda")
+        c.arena.zero_()
+        rk = lay["rot_k"].cuda() if lay["rot_k"] is not None else None
+        rv = lay["rot_v"].cuda() if lay["rot_v"] is not None else None
+        c.compress(lay["k"].cuda(), lay["v"].cuda(), lay["ctx_lens"], rk, rv, single_pass=single)
+        caches.append(c)
+    torch.cuda.synchronize()
+    assert torch.equal(caches[0].arena, caches[1].arena), name
 
 
 @pytest.mark.parametrize("name", list(CASES))
