@@ -224,6 +224,68 @@ def test_c4_one_layer_full_size_properties():
     assert_close(out.cpu().numpy()[b, h * G:(h + 1) * G], want, "c4 attention over the GPU selection")
 
 
+@pytest.mark.parametrize("first", [0, 8, 16, 24])
+def test_c4_every_layer_sampled_segments(first):
+    """Eight of the 32 layers of the 1M-token workload per test, each built,
+    compressed and decoded on the GPU as the benchmark does: for each layer a
+    seeded 1 % of its segments (over all kv heads) are compressed by the oracle
+    as one-segment sequences under the segment's window rotation and must equal
+    the GPU's descriptor strategy, packed token records and block keys byte for
+    byte (a segment's records depend only on its tokens and rotation); and the
+    decode's selection of one kv head per layer is the token budget of the
+    GPU's own scores."""
+    spec = gen.spec("c4")
+    lp, op = params_pair(spec)
+    cap = spec.capacity
+    W = spec.rot_window
+    for layer in range(first, first + 8):
+        lay = gen.make_layer(spec, layer, device="cuda", capacity=cap)
+        c = gpu_cache(lp, spec, lay, cap)
+        q = gen.make_queries(spec, 0, layer).cuda()
+        c.decode(q, scale_of())
+        torch.cuda.synchronize()
+        nseg = spec.ctx[0] // 64
+        rng = np.random.default_rng(4040 + layer)
+        picks = sorted((int(pi), int(sg)) for pi, sg in zip(rng.integers(0, spec.hkv, nseg * spec.hkv // 100),
+                                                             rng.integers(0, nseg, nseg * spec.hkv // 100)))
+        descs = {pi: c.region("desc", pi, 16 * nseg).cpu().numpy().reshape(nseg, 16) for pi in set(p for p, _ in picks)}
+        kk, vv = lay["k"], lay["v"]
+
+        def one(job):
+            pi, sg = job
+            h = pi % spec.hkv
+            w = (sg * 64) // W
+            rk = lay["rot_k"][0, h, w:w + 1].cpu().numpy()
+            rv = lay["rot_v"][0, h, w:w + 1].cpu().numpy()
+            pr = O.Pair(op, 64, rk, rv)
+            pr.compress(bits(kk[0, h, sg * 64:(sg + 1) * 64]), bits(vv[0, h, sg * 64:(sg + 1) * 64]))
+            return pr.descriptor_bytes().reshape(-1, 16)[0], pr.token_arena(), pr.score_arena()
+
+        with cf.ThreadPoolExecutor(16) as ex:
+            want = list(ex.map(one, picks))
+        for (pi, sg), (od, ot, osc) in zip(picks, want):
+            d = descs[pi][sg]
+            assert np.array_equal(d[12:15], od[12:15]), f"c4 layer {layer} pair {pi} segment {sg}: strategy"
+            tok_off, sc_off = (int(x) for x in d[:8].view(np.uint32))
+            got_t = c.arena[c.layout.token_off + pi * c.layout.token_stride + tok_off:][:ot.size].cpu().numpy()
+            got_s = c.arena[c.layout.score_off + pi * c.layout.score_stride + sc_off:][:osc.size].cpu().numpy()
+            assert np.array_equal(got_t, ot), f"c4 layer {layer} pair {pi} segment {sg}: token records"
+            assert np.array_equal(got_s, osc), f"c4 layer {layer} pair {pi} segment {sg}: block keys"
+        # the selection of one kv head is the token budget of the GPU's scores
+        pi = int(rng.integers(0, spec.hkv))
+        nb = int(c.ws_region("wsel", pi, 4 * (c.layout.num_windows + 2)).cpu().numpy().view(np.int32)[-1])
+        gs, gsel, _ = gpu_scores_sel(c, pi, nb)
+        bs = 1 << c.ws_region("bsize", pi, nb).cpu().numpy().astype(np.int64)
+        budget = -(-int(bs.sum()) * spec.select[0] // spec.select[1])
+        key = np.where(gs == 0, 0.0, gs)
+        order = np.lexsort((np.arange(nb), -key.astype(np.float64)))
+        before = np.cumsum(bs[order]) - bs[order]
+        assert np.array_equal(gsel, np.sort(order[before < budget])), f"c4 layer {layer}: selection"
+        print(f"[fullsize] c4 layer {layer}: {len(picks)} segments byte-exact, selection ok", flush=True)
+        del c, lay
+        torch.cuda.empty_cache()
+
+
 def test_c3_quest_mode_full_size_sampled():
     """The quest mode (every channel kept, 16-token blocks, no rotation) on the
     full 8 x 131072 bf16 workload: sampled pairs against the oracle."""
