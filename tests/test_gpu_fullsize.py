@@ -4,12 +4,15 @@ benchmark times (one library call per step over every sequence and kv head).
 The GPU runs the whole workload; the oracle recomputes a seeded sample of
 (sequence, kv head) pairs one by one and must agree with it exactly on the
 packed bytes, descriptors, block scores and selections of those pairs, and
-within 2e-3 max-abs / 1e-3 rel-L2 on their outputs.  The 1M-token case (one
-layer of the 32) is too large for the oracle to compress whole in a test: it
-checks a prefix of the cache byte for byte, the scores of that prefix, that
-the selection is the token budget of the GPU's own scores, and the attention output
-against an independent fp64 evaluation over the GPU's selection (packed
-records decoded here, rotation merged back by R_v).
+within 2e-3 max-abs / 1e-3 rel-L2 on their outputs.  The 1M-token, 32-layer
+case is too large for the oracle to compress whole in a test.  Every layer is
+built on the GPU and a seeded 1 % of its (pair, segment) positions is checked
+byte for byte against the oracle's compression of that one segment (with its
+window's rotation), together with one kv head's selection per layer (the
+token budget of the GPU's own scores).  One layer is further checked on a
+prefix of the cache byte for byte, the scores of that prefix, and the
+attention output against an independent fp64 evaluation over the GPU's
+selection (packed records decoded here, rotation merged back by R_v).
 """
 import concurrent.futures as cf
 import math
