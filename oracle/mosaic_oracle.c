@@ -46,7 +46,12 @@
  * truncated bitmap of exactly T / g bits (R-19), FP8 values as OCP
  * E4M3 without a scale factor, block keys kept 16-bit (R-20), per-vector and
  * per-segment energies as pairwise trees over the 128 channels and the 64
- * tokens (R-22).
+ * tokens (R-22); with dynamic windows, a window of decode tokens closes after
+ * a segment when it holds the maximum length, or when the sum of its
+ * segments' losses (larger of K's and V's relative dropped energy under the
+ * provisional strategy) exceeds a threshold and it holds a minimum length;
+ * its rotation then comes from the caller and its segments are encoded
+ * again (R-23).
  *
  * Exactly-defined orders (so that integer and byte results are unique):
  *  chain(a, b)  : acc = 0; for i ascending: acc = fmaf(a_i, b_i, acc)
@@ -91,6 +96,11 @@ typedef struct {
     int32_t fp8;                     /* 1: K and V token values stored as OCP FP8 E4M3
                                         (Sec. 7, quantizing the compressed elements);
                                         block keys keep the 16-bit dtype (reading R-20) */
+    int32_t dyn;                     /* 1: windows of decode tokens close on their
+                                        accumulated compression loss (Sec. 4.3, Sec. 5.5;
+                                        reading R-23) instead of every rot_window tokens */
+    float tau_window;                /* accumulated loss above which a window closes */
+    int32_t min_window;              /* tokens a window holds at least before a loss close */
 } orc_params;
 
 typedef struct {
@@ -112,6 +122,11 @@ typedef struct {
     uint16_t bufk[32 * D], bufv[32 * D];   /* update buffer (raw dtype bits) */
     uint16_t stgk[64 * D], stgv[64 * D];   /* raw tokens of the trailing segment */
     float *rk, *rv;      /* [nw][D][D] or NULL (identity) */
+    /* windows closed by the compression loss (P.dyn; reading R-23) */
+    int32_t *wseg;       /* [nw + 1]: first segment of each window */
+    int32_t nwin;        /* windows in use; window nwin - 1 is open */
+    float wloss;         /* accumulated loss of the open window */
+    int32_t pend;        /* closed window awaiting its rotation, or -1 */
 } orc_pair;
 
 typedef struct {
@@ -440,10 +455,26 @@ static int min_block(const orc_params *P) {
     return m;
 }
 
-orc_pair *orc_pair_new(const orc_params *P, int cap, const float *rk, const float *rv, int nw) {
+/* Rotation windows a cache of cap tokens can hold: every closed window has at
+   least min_window tokens, so at most cap / min_window close, plus the open
+   one (reading R-23). */
+int orc_max_windows(const orc_params *P, int cap) {
+    int nw = (cap + P->rot_window - 1) / P->rot_window;
+    if (P->dyn && P->min_window > 0) {
+        int m = cap / P->min_window + 1;
+        if (m > nw) nw = m;
+    }
+    return nw > 0 ? nw : 1;
+}
+
+orc_pair *orc_pair_new(const orc_params *P, int cap, const float *rk, const float *rv, int nw_given) {
     orc_pair *p = (orc_pair *)calloc(1, sizeof(orc_pair));
     if (!p) return NULL;
+    int nw = nw_given;
+    if (P->dyn && rk && rv && nw_given > 0) { int m = orc_max_windows(P, cap); if (m > nw) nw = m; }
     p->P = *P; p->cap = cap; p->nw = nw;
+    p->pend = -1; p->nwin = 1;
+    p->wseg = (int32_t *)calloc((size_t)(nw > 0 ? nw : 1) + 1, sizeof(int32_t));
     int mv = max_vec_bytes(P), mb = min_block(P);
     int nseg = cap / P->seg_len + 2;
     p->tok_cap = (size_t)nseg * P->seg_len * 2 * mv;
@@ -455,20 +486,33 @@ orc_pair *orc_pair_new(const orc_params *P, int cap, const float *rk, const floa
     if (rk && rv && nw > 0) {
         p->rk = (float *)malloc((size_t)nw * D * D * sizeof(float));
         p->rv = (float *)malloc((size_t)nw * D * D * sizeof(float));
-        memcpy(p->rk, rk, (size_t)nw * D * D * sizeof(float));
-        memcpy(p->rv, rv, (size_t)nw * D * D * sizeof(float));
+        memcpy(p->rk, rk, (size_t)nw_given * D * D * sizeof(float));
+        memcpy(p->rv, rv, (size_t)nw_given * D * D * sizeof(float));
+        for (int w = nw_given; w < nw; ++w) {      /* slots of later windows: filled when they close */
+            memcpy(p->rk + (size_t)w * D * D, rk + (size_t)(nw_given - 1) * D * D, D * D * sizeof(float));
+            memcpy(p->rv + (size_t)w * D * D, rv + (size_t)(nw_given - 1) * D * D, D * D * sizeof(float));
+        }
     }
     return p;
 }
 
 void orc_pair_free(orc_pair *p) {
     if (!p) return;
-    free(p->tok); free(p->sc); free(p->desc); free(p->rk); free(p->rv); free(p);
+    free(p->tok); free(p->sc); free(p->desc); free(p->rk); free(p->rv); free(p->wseg); free(p);
+}
+
+/* Window of segment s: every rot_window tokens, or with dynamic windows the
+   last window of the table that starts at or before s. */
+static int win_of_seg(const orc_pair *p, int s) {
+    if (!p->P.dyn) return s * p->P.seg_len / p->P.rot_window;
+    int w = 0;
+    while (w + 1 < p->nwin && p->wseg[w + 1] <= s) ++w;
+    return w;
 }
 
 static const float *rot_of(const orc_pair *p, const float *R, int token_pos) {
     if (!R) return NULL;
-    int w = token_pos / p->P.rot_window;
+    int w = win_of_seg(p, token_pos / p->P.seg_len);
     if (w >= p->nw) w = p->nw - 1;
     return R + (size_t)w * D * D;
 }
@@ -486,23 +530,86 @@ static int state_nfinal(const orc_pair *p) { return p->L / p->P.seg_len; }
 static int state_prov(const orc_pair *p) { return (p->L % p->P.seg_len) >= p->P.update_buf; }
 static int state_nbuf(const orc_pair *p) { return (p->L % p->P.seg_len) - (state_prov(p) ? p->P.update_buf : 0); }
 
-/* finalize the trailing segment: staging holds S raw tokens */
-static void finalize_segment(orc_pair *p) {
+/* Compression loss of a segment under the strategy (r, g) (Sec. 4.3: the
+   loss of the current strategy on new vectors; Sec. 5.5: the channel-
+   compressed vectors compared with the original ones; reading R-23): the
+   larger of K's and V's relative dropped energy, each the segment's dropped
+   energy over its energy with the pairwise trees of the strategy search
+   (R-22), 0 for a part without energy.  fp32 with correctly rounded
+   divisions.  yk, yv: [n][D] rotated vectors, n == S == 64. */
+float orc_segment_loss(const orc_params *P, const float *yk, const float *yv, int n, int r, int g) {
+    const int T = trunc_of(P);
+    float tk[64], tv[64], dk[64], dv[64];
+    for (int t = 0; t < n; ++t) {
+        float ek[D], ev[D], mk[D], mv[D];
+        uint8_t kk[D], kv[D];
+        for (int c = 0; c < D; ++c) { ek[c] = yk[t * D + c] * yk[t * D + c]; ev[c] = yv[t * D + c] * yv[t * D + c]; }
+        keep_channels(yk + t * D, r, g, T, kk); keep_channels(yv + t * D, r, g, T, kv);
+        for (int c = 0; c < D; ++c) { mk[c] = kk[c] ? 0.0f : ek[c]; mv[c] = kv[c] ? 0.0f : ev[c]; }
+        tk[t] = orc_tree_sum(ek, D); tv[t] = orc_tree_sum(ev, D);
+        dk[t] = orc_tree_sum(mk, D); dv[t] = orc_tree_sum(mv, D);
+    }
+    float TK = orc_tree_sum(tk, n), TV = orc_tree_sum(tv, n), DK = orc_tree_sum(dk, n), DV = orc_tree_sum(dv, n);
+    float lk = TK > 0.0f ? DK / TK : 0.0f, lv = TV > 0.0f ? DV / TV : 0.0f;
+    return lk > lv ? lk : lv;
+}
+
+/* Segment s, finalized by the append path, belongs to the open window: add
+   its loss; the window closes after s when it holds rot_window tokens (the
+   maximum length), or when the accumulated loss exceeds tau_window and it
+   holds at least min_window tokens (Sec. 4.3; reading R-23).  The closed
+   window then awaits its own rotation (orc_pair_close), and the next
+   segment opens a new window. */
+static void window_update(orc_pair *p, int s, float loss) {
     const orc_params *P = &p->P;
-    int S = P->seg_len, nf = p->L / S - 1;   /* index of the segment being finalized */
-    float *yk = (float *)malloc((size_t)S * D * sizeof(float)), *yv = (float *)malloc((size_t)S * D * sizeof(float));
-    rotate_tokens(p, p->stgk, S, nf * S, p->rk, yk);
-    rotate_tokens(p, p->stgv, S, nf * S, p->rv, yv);
-    int r, g, B;
+    int w = p->nwin - 1;
+    int ntok = (s + 1 - p->wseg[w]) * P->seg_len;
+    float acc = p->wloss + loss;
+    int close = ntok >= P->rot_window || (acc > P->tau_window && ntok >= P->min_window);
+    if (close && p->nwin < p->nw) {
+        p->wseg[p->nwin] = s + 1;
+        p->nwin++;
+        p->pend = w;
+        p->wloss = 0.0f;
+    } else {
+        p->wloss = acc;
+    }
+}
+
+/* Segment s (S rotated tokens yk, yv) encoded with its own strategy at the
+   tails of the arenas. */
+static void encode_final(orc_pair *p, int s, const float *yk, const float *yv) {
+    const orc_params *P = &p->P;
+    int S = P->seg_len, r, g, B;
     orc_choose_strategy(P, yk, yv, S, &r, &g, &B);
     int rec = orc_vec_bytes_t(r, g, tok_eb(P), trunc_of(P)), srec = orc_vec_bytes_t(r, g, 2, trunc_of(P));
     encode_segment(yk, yv, S, r, g, B, P->dtype, trunc_of(P), tok_eb(P), p->tok + p->tok_tail, p->sc + p->sc_tail);
-    orc_desc *d = &p->desc[nf];
+    orc_desc *d = &p->desc[s];
     d->tok_off = p->tok_tail; d->sc_off = p->sc_tail; d->first_block = (uint32_t)p->nblk_final;
     d->r = (uint8_t)r; d->log2g = (uint8_t)ilog2(g); d->log2b = (uint8_t)ilog2(B); d->flags = 0;
     p->tok_tail += (uint32_t)(S * 2 * rec);
     p->sc_tail += (uint32_t)((S / B) * srec);
     p->nblk_final += S / B;
+}
+
+/* finalize the trailing segment: staging holds S raw tokens.  A segment
+   completed by an append also counts toward its window's loss, under the
+   provisional strategy (R-10) that new tokens were compressed with. */
+static void finalize_segment(orc_pair *p, int from_append) {
+    const orc_params *P = &p->P;
+    int S = P->seg_len, nf = p->L / S - 1;   /* index of the segment being finalized */
+    float *yk = (float *)malloc((size_t)S * D * sizeof(float)), *yv = (float *)malloc((size_t)S * D * sizeof(float));
+    rotate_tokens(p, p->stgk, S, nf * S, p->rk, yk);
+    rotate_tokens(p, p->stgv, S, nf * S, p->rv, yv);
+    float loss = 0.0f;
+    const int dyn = P->dyn && from_append;
+    if (dyn) {
+        int rp = P->def_keep, gp = P->def_group;
+        if (nf > 0) { rp = p->desc[nf - 1].r; gp = 1 << p->desc[nf - 1].log2g; }
+        loss = orc_segment_loss(P, yk, yv, S, rp, gp);
+    }
+    encode_final(p, nf, yk, yv);
+    if (dyn) window_update(p, nf, loss);
     free(yk); free(yv);
 }
 
@@ -524,17 +631,20 @@ static void flush_provisional(orc_pair *p) {
 }
 
 /* Append one token (Sec. 5.3 update buffer, Sec. 5.4 double buffering).
-   Returns 0, or -3 when the capacity is exhausted. */
+   Returns 0, -3 when the capacity is exhausted, or -4 (nothing appended)
+   when the token would compress the buffer while a closed window still
+   awaits its rotation. */
 int orc_pair_append(orc_pair *p, const uint16_t *k, const uint16_t *v) {
     const orc_params *P = &p->P;
     if (p->L >= p->cap) return -3;
     int S = P->seg_len, U = P->update_buf;
     int m = p->L % S, nb = state_nbuf(p);
+    if (p->pend >= 0 && nb + 1 == U) return -4;    /* a closed window awaits its rotation */
     memcpy(p->bufk + (size_t)nb * D, k, D * 2); memcpy(p->bufv + (size_t)nb * D, v, D * 2);
     memcpy(p->stgk + (size_t)m * D, k, D * 2); memcpy(p->stgv + (size_t)m * D, v, D * 2);
     p->L++;
     if (nb + 1 == U) {
-        if (p->L % S == 0) finalize_segment(p);
+        if (p->L % S == 0) finalize_segment(p, 1);
         else flush_provisional(p);
     }
     return 0;
@@ -548,15 +658,61 @@ int orc_pair_compress(orc_pair *p, const uint16_t *k, const uint16_t *v, int L) 
     if (L > p->cap || L < 0) return -3;
     p->L = 0; p->nblk_final = 0; p->tok_tail = 0; p->sc_tail = 0;
     int S = P->seg_len, nfull = L / S;
+    p->wloss = 0.0f; p->pend = -1; p->nwin = 1;
+    if (P->dyn) {
+        /* input tokens: fixed windows of rot_window tokens (Sec. 4.3); the
+           window holding the first token after the full segments stays open */
+        p->nwin = nfull * S / P->rot_window + 1;
+        if (p->nwin > p->nw) p->nwin = p->nw > 0 ? p->nw : 1;
+        for (int w = 0; w < p->nwin; ++w) p->wseg[w] = w * (P->rot_window / S);
+    }
     for (int s = 0; s < nfull; ++s) {
         memcpy(p->stgk, k + (size_t)s * S * D, (size_t)S * D * 2);
         memcpy(p->stgv, v + (size_t)s * S * D, (size_t)S * D * 2);
         p->L = (s + 1) * S;
-        finalize_segment(p);
+        finalize_segment(p, 0);
     }
     p->L = nfull * S;
     for (int t = nfull * S; t < L; ++t) orc_pair_append(p, k + (size_t)t * D, v + (size_t)t * D);
     return 0;
+}
+
+/* Close of the window awaiting its rotation (Sec. 4.3, Sec. 5.5): rk_new /
+   rv_new ([D][D], row j = rotated channel j), computed by the caller from the
+   window's raw tokens, replace its provisional rotation and become the
+   provisional rotation of the window the close opened; every segment of the
+   closed window is encoded again, with its own strategy, from its raw tokens
+   k, v ([n][D], the window's tokens from its first one).  The closed window
+   is the last compressed one (a buffer flush waits for the close), so the
+   new records start where its old ones did.  Returns 0, or -4 when no window
+   awaits a rotation. */
+int orc_pair_close(orc_pair *p, const float *rk_new, const float *rv_new, const uint16_t *k, const uint16_t *v) {
+    if (p->pend < 0 || !p->rk || !p->rv) return -4;
+    const orc_params *P = &p->P;
+    int w = p->pend, s0 = p->wseg[w], s1 = p->wseg[w + 1], S = P->seg_len;
+    for (int i = w; i <= w + 1 && i < p->nw; ++i) {
+        memcpy(p->rk + (size_t)i * D * D, rk_new, D * D * sizeof(float));
+        memcpy(p->rv + (size_t)i * D * D, rv_new, D * D * sizeof(float));
+    }
+    p->tok_tail = p->desc[s0].tok_off; p->sc_tail = p->desc[s0].sc_off;
+    p->nblk_final = (int32_t)p->desc[s0].first_block;
+    float *yk = (float *)malloc((size_t)S * D * sizeof(float)), *yv = (float *)malloc((size_t)S * D * sizeof(float));
+    for (int s = s0; s < s1; ++s) {
+        rotate_tokens(p, k + (size_t)(s - s0) * S * D, S, s * S, p->rk, yk);
+        rotate_tokens(p, v + (size_t)(s - s0) * S * D, S, s * S, p->rv, yv);
+        encode_final(p, s, yk, yv);
+    }
+    free(yk); free(yv);
+    p->pend = -1;
+    return 0;
+}
+
+/* Window state: windows in use, the window awaiting its rotation (-1: none),
+   the open window's accumulated loss, and the first segment of each window
+   (wseg, capacity nwin, may be NULL). */
+void orc_pair_windows(const orc_pair *p, int32_t *nwin, int32_t *pend, float *wloss, int32_t *wseg) {
+    *nwin = p->nwin; *pend = p->pend; *wloss = p->wloss;
+    if (wseg) for (int w = 0; w < p->nwin; ++w) wseg[w] = p->wseg[w];
 }
 
 void orc_pair_info(const orc_pair *p, orc_info *o) {
@@ -609,7 +765,7 @@ int orc_pair_scores(const orc_pair *p, const uint16_t *q, float *scores, int cap
     int cur_w = -1;
     for (int di = 0; di < inf.n_desc; ++di) {
         const orc_desc *d = &p->desc[di];
-        int pos = di * P->seg_len, w = pos / P->rot_window;
+        int pos = di * P->seg_len, w = win_of_seg(p, di);
         if (w != cur_w) { for (int h = 0; h < G; ++h) qrot32(p, q + (size_t)h * D, pos, qr[h]); cur_w = w; }
         const int T = trunc_of(P);
         int g = 1 << d->log2g, B = 1 << d->log2b, r = d->r, rec = orc_vec_bytes_t(r, g, 2, T), bmb = orc_bitmap_bytes_t(g, T);
@@ -729,7 +885,7 @@ int orc_pair_decode(const orc_pair *p, const uint16_t *q, float scale, double *o
     double qr[MAXG][D];
     for (int di = 0; di < inf.n_desc; ++di) {
         const orc_desc *d = &p->desc[di];
-        int pos = di * P->seg_len, w = pos / P->rot_window;
+        int pos = di * P->seg_len, w = win_of_seg(p, di);
         if (w != cur_w) {   /* q . R_k^T in fp64 for this window */
             const float *Rk = rot_of(p, p->rk, pos);
             for (int h = 0; h < G; ++h) for (int j = 0; j < D; ++j) {

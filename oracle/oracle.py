@@ -46,6 +46,7 @@ class OrcParams(C.Structure):
         ("tau_channel", C.c_float), ("tau_block", C.c_float),
         ("select_num", C.c_int32), ("select_den", C.c_int32), ("force_default", C.c_int32),
         ("trunc", C.c_int32), ("fp8", C.c_int32),
+        ("dyn", C.c_int32), ("tau_window", C.c_float), ("min_window", C.c_int32),
     ]
 
 
@@ -78,6 +79,9 @@ class Params:
     force_default: bool = False
     trunc: int = 128                # channels represented in the bitmap (Sec. 5.2 channel truncation)
     fp8: bool = False               # K/V token values as E4M3 (Sec. 7, combining with quantization)
+    dyn: bool = False               # decode windows closed by their accumulated loss (Sec. 4.3, R-23)
+    tau_window: float = 8.0
+    min_window: int = 1024
 
     def to_c(self) -> OrcParams:
         p = OrcParams()
@@ -94,6 +98,8 @@ class Params:
         p.force_default = 1 if self.force_default else 0
         p.trunc = self.trunc
         p.fp8 = 1 if self.fp8 else 0
+        p.dyn = 1 if self.dyn else 0
+        p.tau_window, p.min_window = self.tau_window, self.min_window
         return p
 
 
@@ -138,6 +144,11 @@ def lib():
                        ("orc_pair_stgk", u16p), ("orc_pair_stgv", u16p)):
             getattr(L, nm).argtypes = [C.c_void_p]; getattr(L, nm).restype = rt
         L.orc_pair_scores.argtypes = [C.c_void_p, u16p, fp, C.c_int]; L.orc_pair_scores.restype = C.c_int
+        L.orc_segment_loss.argtypes = [C.POINTER(OrcParams), fp, fp, C.c_int, C.c_int, C.c_int]
+        L.orc_segment_loss.restype = C.c_float
+        L.orc_max_windows.argtypes = [C.POINTER(OrcParams), C.c_int]; L.orc_max_windows.restype = C.c_int
+        L.orc_pair_close.argtypes = [C.c_void_p, fp, fp, u16p, u16p]; L.orc_pair_close.restype = C.c_int
+        L.orc_pair_windows.argtypes = [C.c_void_p, i32p, i32p, fp, i32p]; L.orc_pair_windows.restype = None
         L.orc_select_count.argtypes = [C.c_int, C.c_int, C.c_int]; L.orc_select_count.restype = C.c_int
         L.orc_select_budget.argtypes = [C.c_int, C.c_int, C.c_int]; L.orc_select_budget.restype = C.c_int
         L.orc_select_blocks.argtypes = [fp, i32p, C.c_int, C.c_int, u8p]; L.orc_select_blocks.restype = C.c_int
@@ -252,6 +263,19 @@ def choose_strategy(params: Params, yk, yv):
     return r.value, g.value, b.value
 
 
+def segment_loss(params: Params, yk, yv, r, g):
+    """Compression loss of a 64-token segment under (r, g) (R-23): the larger
+    of K's and V's relative dropped energy."""
+    yk, yv = _f32(yk).reshape(-1, D), _f32(yv).reshape(-1, D)
+    P = params.to_c()
+    return float(np.float32(lib().orc_segment_loss(C.byref(P), _p(yk, C.c_float), _p(yv, C.c_float), yk.shape[0], r, g)))
+
+
+def max_windows(params: Params, cap: int) -> int:
+    P = params.to_c()
+    return lib().orc_max_windows(C.byref(P), cap)
+
+
 def select_count(nblk, num, den):
     return lib().orc_select_count(nblk, num, den)
 
@@ -331,6 +355,29 @@ class Pair:
         rc = lib().orc_pair_append(self._h, _p(k, C.c_uint16), _p(v, C.c_uint16))
         if rc:
             raise ValueError("append: capacity")
+
+    def append_status(self, k, v) -> int:
+        """Append returning the oracle's status (0, -3 capacity, -4 a closed
+        window awaits its rotation) instead of raising."""
+        k, v = _u16(k).reshape(D), _u16(v).reshape(D)
+        return lib().orc_pair_append(self._h, _p(k, C.c_uint16), _p(v, C.c_uint16))
+
+    def windows(self):
+        """-> dict(nwin, pend, wloss, wseg list): the window table (R-23)."""
+        nwin, pend, wl = C.c_int32(), C.c_int32(), C.c_float()
+        lib().orc_pair_windows(self._h, C.byref(nwin), C.byref(pend), C.byref(wl), None)
+        ws = np.zeros(max(nwin.value, 1), np.int32)
+        lib().orc_pair_windows(self._h, C.byref(nwin), C.byref(pend), C.byref(wl), _p(ws, C.c_int32))
+        return dict(nwin=nwin.value, pend=pend.value, wloss=float(np.float32(wl.value)), wseg=ws[:nwin.value].tolist())
+
+    def close(self, rot_k, rot_v, k, v):
+        """Close of the window awaiting its rotation: new R (rows = channels)
+        and the window's raw tokens."""
+        rk, rv = _f32(rot_k).reshape(D, D), _f32(rot_v).reshape(D, D)
+        k, v = _u16(k).reshape(-1, D), _u16(v).reshape(-1, D)
+        rc = lib().orc_pair_close(self._h, _p(rk, C.c_float), _p(rv, C.c_float), _p(k, C.c_uint16), _p(v, C.c_uint16))
+        if rc:
+            raise ValueError("close: no window awaits a rotation")
 
     def info(self) -> OrcInfo:
         o = OrcInfo()
