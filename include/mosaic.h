@@ -15,7 +15,7 @@
  *  - The caller allocates and owns all device memory: inputs, the cache arena,
  *    workspaces and outputs.  It keeps them alive until the enqueued work
  *    completes.  The library never allocates device memory.  Only
- *    mosaic_cache_stats synchronizes.
+ *    mosaic_cache_stats and mosaic_window_poll synchronize.
  *  - `stream` is a hipStream_t (NULL = the null stream).  All work is enqueued
  *    on it, in order.
  *  - Validation happens before anything is enqueued.  On error nothing is
@@ -83,12 +83,22 @@ typedef struct {
                                   +-448, no scale factor); every kept count must then be a
                                   multiple of 4.  Block keys, the update buffer and the staging
                                   area keep the 16-bit dtype.  0 = 16-bit values */
+    int32_t dyn_windows;       /* 1: windows of decode tokens close on their accumulated
+                                  compression loss (Sec. 4.3 dynamic partitioning of output
+                                  tokens, Sec. 5.5 incremental strategy generation; see
+                                  mosaic_window_poll); needs rotated = 1.  0: every window
+                                  holds rot_window tokens */
+    float tau_window;          /* summed segment loss above which a window closes */
+    int32_t min_window;        /* tokens a window holds at least before it closes on its
+                                  loss; a multiple of 64 in [64, rot_window] (rot_window is
+                                  the maximum window length) */
 } mosaic_params;
 
 /* Fills *p with the paper's defaults (Sec. 5.5, Sec. 6.1): r in {16, 32, 48},
  * g in {4, 2, 1}, B in {16, 8, 4}, default (32, 1, 8), S = 64, U = 32,
  * W = 65536, tau = (0.30, 0.90), rho = 1/10, fp16, 8 kv heads, G = 4,
- * T = 128 (no truncation), 16-bit values. */
+ * T = 128 (no truncation), 16-bit values, fixed windows (dyn_windows = 0;
+ * tau_window = 8, min_window = 1024 when enabled). */
 void mosaic_params_default(mosaic_params *p);
 
 typedef struct mosaic_cache mosaic_cache;  /* host bookkeeping + bound arena */
@@ -96,9 +106,11 @@ typedef struct mosaic_cache mosaic_cache;  /* host bookkeeping + bound arena */
 /* Creates the host side of a cache for num_seqs sequences of up to max_tokens
  * tokens each.  rotated = 1 if mosaic_compress will receive rotation matrices
  * (Sec. 2.3); 0 for the identity rotation.  The handle owns host memory
- * only.  Errors: INVALID (parameters), UNSUPPORTED (head_dim != 128,
- * S != 64, U != 32), CAPACITY (a per-(sequence, kv head) arena would
- * exceed 4 GiB). */
+ * only.  With dyn_windows the cache holds max(ceil(max_tokens / W),
+ * max_tokens / min_window + 1) rotation windows per pair.  Errors: INVALID
+ * (parameters; dyn_windows without rotation), UNSUPPORTED (head_dim != 128,
+ * S != 64, U != 32, more than 1024 windows), CAPACITY (a per-(sequence,
+ * kv head) arena would exceed 4 GiB). */
 mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
                                   int32_t rotated, mosaic_cache **out);
 
@@ -113,7 +125,11 @@ mosaic_status mosaic_cache_destroy(mosaic_cache *cache);
  * off + p * stride.  Use it for inspection (tests, stats); the layout of a
  * region's contents is the packed format of Sec. 5.1:
  *   meta     : int32 tokens, int32 finalized blocks, uint32 token-arena
- *              bytes, uint32 score-arena bytes (finalized segments)
+ *              bytes, uint32 score-arena bytes (finalized segments); with
+ *              dyn_windows also int32 windows in use, fp32 loss summed in
+ *              the open window, int32 window awaiting its rotation (-1:
+ *              none), and from byte 64 the window table: int32
+ *              [num_windows + 1] first segment of each window in use
  *   desc     : 16-byte segment descriptors {uint32 token-arena offset,
  *              uint32 score-arena offset, uint32 first block, uint8 r,
  *              uint8 log2 g, uint8 log2 B, uint8 flags (bit 0 provisional)}
@@ -185,6 +201,9 @@ mosaic_status mosaic_decode_ws_layout(const mosaic_cache *cache, mosaic_ws_layou
  *               is rotated channel j, so y = x . R^T (Sec. 2.3).  Window w
  *               covers tokens [w W, (w+1) W); num_windows = ceil(max_tokens
  *               / W).  NULL (both) iff the cache was created with rotated = 0.
+ *               With dyn_windows the prefill's windows are these fixed ones;
+ *               the window holding the first token after the full segments
+ *               stays open for decode tokens (its rotation is the one given).
  *   Full segments get their own strategy.  The remaining ctx_len mod S tokens
  *   take the update path (buffer, provisional flush), as if appended.
  * Replaces any previous contents.
@@ -208,8 +227,55 @@ mosaic_status mosaic_compress(mosaic_cache *cache, const void *k, const void *v,
  * they are compressed with the previous finalized segment's strategy, as a
  * provisional chunk.  When its trailing segment reaches S tokens, the
  * segment gets its own strategy and is recompressed in place.
- * Errors: STATE (not compressed yet), CAPACITY (a sequence is full). */
+ * Errors: STATE (not compressed yet; with dyn_windows, a poll or a close is
+ * due first: see mosaic_window_poll), CAPACITY (a sequence is full). */
 mosaic_status mosaic_append(mosaic_cache *cache, const void *k_new, const void *v_new, void *stream);
+
+/* Windows closed by their compression loss (Sec. 4.3: output tokens are
+ * partitioned dynamically, a segment being closed once its compression loss
+ * passes a threshold, with a maximum length; Sec. 5.5: the loss of each new
+ * token compares its channel-compressed vectors with the original ones, and
+ * the closed segment's rotation comes from its covariance).  For caches
+ * created with dyn_windows = 1.  Every segment completed by mosaic_append
+ * adds its loss -- the larger of K's and V's relative dropped energy under
+ * the provisional strategy it was compressed with -- to the open window's
+ * sum.  After that segment the window closes if it holds rot_window tokens,
+ * or if the sum exceeds tau_window and it holds at least min_window tokens;
+ * the next segment opens a window whose provisional rotation is the closed
+ * window's.  A closed window keeps its provisional encoding until
+ * mosaic_window_close gives it its own rotation.
+ *
+ * mosaic_window_poll synchronizes `stream`, then reports for every pair p
+ * (= seq * num_kv_heads + kv_head) the window awaiting its rotation:
+ *   out_host[3 p]     : its index, -1 if none
+ *   out_host[3 p + 1] : its first token
+ *   out_host[3 p + 2] : its token count (a multiple of 64)
+ * and in *n_closed_host the number of such pairs.  Protocol: after an append
+ * that completed a segment, a poll must precede the next append that
+ * compresses an update buffer, and a window it reports must be closed before
+ * its sequence's buffer is compressed again (at most 32 appends later);
+ * mosaic_append fails with STATE, changing nothing, until then.  Decode may
+ * run at any time.  Errors: INVALID (NULL; no dynamic windows), STATE (not
+ * compressed). */
+mosaic_status mosaic_window_poll(mosaic_cache *cache, int32_t *out_host, int32_t *n_closed_host, void *stream);
+
+/* Closes every window the last poll reported.
+ *   rot_k, rot_v : [num_seqs][num_kv_heads][128][128] fp32: each such pair's
+ *                  rotation of its closed window (row j = rotated channel j),
+ *                  e.g. the eigenvectors of the window's K (V) covariance by
+ *                  descending eigenvalue; other pairs' entries are not read.
+ *   k, v         : [num_seqs][num_kv_heads][seq_stride][128] the closed
+ *                  windows' raw tokens (cache dtype), row 0 = the window's
+ *                  first token; seq_stride >= the longest closed window.
+ * The rotation replaces the window's provisional one and becomes the
+ * provisional rotation of the window the close opened; every segment of the
+ * closed window is encoded again from its tokens with its own strategy (two
+ * passes: strategy, then packing), in place (it is the last compressed
+ * window).  Nothing to close: OK, nothing enqueued.  Errors: INVALID (NULL,
+ * misaligned, seq_stride too small, no dynamic windows), STATE (a segment
+ * completed since the last poll). */
+mosaic_status mosaic_window_close(mosaic_cache *cache, const float *rot_k, const float *rot_v, const void *k,
+                                  const void *v, int64_t seq_stride, void *stream);
 
 /* One decode step of PackedAttention (Sec. 5.3) for every sequence.  Steps:
  * rotate q into each window (rotation merged into the query), score every

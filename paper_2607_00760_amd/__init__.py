@@ -36,6 +36,9 @@ class Params:
     force_default: bool = False
     trunc: int = 128                 # channels represented in the bitmaps (Sec. 5.2 channel truncation)
     fp8: bool = False                # K/V token values as E4M3 codes (Sec. 7, combining with quantization)
+    dyn_windows: bool = False        # decode windows closed by their compression loss (Sec. 4.3, Sec. 5.5)
+    tau_window: float = 8.0
+    min_window: int = 1024
 
     def to_c(self) -> MosaicParams:
         p = MosaicParams()
@@ -51,6 +54,8 @@ class Params:
         p.force_default_strategy = 1 if self.force_default else 0
         p.trunc_channels = self.trunc
         p.value_fp8 = 1 if self.fp8 else 0
+        p.dyn_windows = 1 if self.dyn_windows else 0
+        p.tau_window, p.min_window = self.tau_window, self.min_window
         return p
 
 
@@ -122,7 +127,7 @@ class MosaicCache:
 
     def compress(self, k, v, ctx_lens, rot_k=None, rot_v=None, single_pass: bool = True):
         """k, v: [num_seqs][Hkv][seq_stride][128] (cache dtype); ctx_lens: host ints;
-        rot_k/rot_v: [num_seqs][Hkv][num_windows][128][128] fp32 or None.
+        rot_k/rot_v: [num_seqs][Hkv][ceil(max_tokens / rot_window)][128][128] fp32 or None.
         single_pass: rotate each token once, packing through a transient
         workspace (the library's worst-case segment slots); False: two passes,
         no extra memory.  Both write the same bytes."""
@@ -135,7 +140,8 @@ class MosaicCache:
         if rot_k is not None:
             _check_tensor(rot_k, "rot_k", torch.float32, self.device)
             _check_tensor(rot_v, "rot_v", torch.float32, self.device)
-            want = (self.num_seqs, self.params.num_kv_heads, self.layout.num_windows, D, D)
+            nw = -(-self.max_tokens // self.params.rot_window)       # fixed windows of the prefill
+            want = (self.num_seqs, self.params.num_kv_heads, nw, D, D)
             if tuple(rot_k.shape) != want or tuple(rot_v.shape) != want:
                 raise ValueError(f"rotation shape {tuple(rot_k.shape)} != {want}")
         lens = (C.c_int32 * self.num_seqs)(*[int(x) for x in ctx_lens])
@@ -174,6 +180,36 @@ class MosaicCache:
             check(self.lib.mosaic_decode_attention(self._h, _ptr(q), _ptr(out), float(sm_scale), _ptr(self.workspace),
                                                    self.workspace.numel(), _stream(self.device)))
         return out
+
+    def window_poll(self):
+        """Windows closed by their loss and awaiting their rotation (synchronizes):
+        {pair: (window, first token, tokens)}."""
+        import torch
+        out = (C.c_int32 * (3 * self.num_pairs))()
+        n = C.c_int32()
+        with torch.cuda.device(self.device):
+            check(self.lib.mosaic_window_poll(self._h, out, C.byref(n), _stream(self.device)))
+        return {p: (out[3 * p], out[3 * p + 1], out[3 * p + 2]) for p in range(self.num_pairs) if out[3 * p] >= 0}
+
+    def window_close(self, rot_k, rot_v, k, v):
+        """rot_k, rot_v: [num_seqs][Hkv][128][128] fp32, each polled pair's new
+        rotation; k, v: [num_seqs][Hkv][stride][128] each closed window's raw
+        tokens from its first one."""
+        import torch
+        for t, nm in ((rot_k, "rot_k"), (rot_v, "rot_v")):
+            _check_tensor(t, nm, torch.float32, self.device)
+            if tuple(t.shape) != (self.num_seqs, self.params.num_kv_heads, D, D):
+                raise ValueError(f"{nm} shape {tuple(t.shape)}")
+        for t, nm in ((k, "k"), (v, "v")):
+            _check_tensor(t, nm, self.elem, self.device)
+            if t.dim() != 4 or tuple(t.shape[:2]) != (self.num_seqs, self.params.num_kv_heads) or t.shape[3] != D:
+                raise ValueError(f"{nm} shape {tuple(t.shape)}")
+        if k.shape != v.shape:
+            raise ValueError("k and v shapes differ")
+        with torch.cuda.device(self.device):
+            check(self.lib.mosaic_window_close(self._h, _ptr(rot_k), _ptr(rot_v), _ptr(k), _ptr(v), k.shape[2],
+                                               _stream(self.device)))
+        self._keep_close = (rot_k, rot_v, k, v)
 
     KERNELS = ("qrot", "score", "topk", "attn", "reduce")
 

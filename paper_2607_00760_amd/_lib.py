@@ -18,6 +18,7 @@ EXPORTED = [
     "mosaic_dense_decode_attention", "mosaic_cache_stats", "mosaic_seq_tokens", "mosaic_last_error",
     "mosaic_set_timing", "mosaic_decode_timing", "mosaic_rotation_workspace_bytes", "mosaic_compute_rotations",
     "mosaic_reorder_workspace_bytes", "mosaic_reorder_rotations", "mosaic_decode_attention_noalloc",
+    "mosaic_window_poll", "mosaic_window_close",
 ]
 
 
@@ -30,6 +31,7 @@ class MosaicParams(C.Structure):
         ("tau_channel", C.c_float), ("tau_block", C.c_float),
         ("select_num", C.c_int32), ("select_den", C.c_int32), ("force_default_strategy", C.c_int32),
         ("trunc_channels", C.c_int32), ("value_fp8", C.c_int32),
+        ("dyn_windows", C.c_int32), ("tau_window", C.c_float), ("min_window", C.c_int32),
     ]
 
 
@@ -99,6 +101,8 @@ def bind_signatures(L: C.CDLL) -> C.CDLL:
     L.mosaic_reorder_workspace_bytes.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, C.POINTER(sz)]
     L.mosaic_reorder_rotations.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, vp, vp, C.c_int64,
                                            C.POINTER(C.c_int32), vp, vp, vp, sz, vp]
+    L.mosaic_window_poll.argtypes = [vp, C.POINTER(C.c_int32), C.POINTER(C.c_int32), vp]
+    L.mosaic_window_close.argtypes = [vp, vp, vp, vp, vp, C.c_int64, vp]
     L.mosaic_set_timing.argtypes = [vp, C.c_int32]
     L.mosaic_decode_timing.argtypes = [vp, C.POINTER(C.c_float)]
     L.mosaic_seq_tokens.argtypes = [vp, C.c_int32]

@@ -56,6 +56,13 @@ struct mosaic_cache {
     bool timing = false, timed_once = false;
     hipEvent_t ev[6] = {};
     std::vector<int32_t> L;      // host mirror of each sequence's length
+    // dynamic windows: nw_src = rotations per pair mosaic_compress receives;
+    // poll_due = a segment completed since the last poll (a window may have
+    // closed); per pair the windows in use, the window awaiting its rotation
+    // and that window's token count, as of the last poll
+    bool dyn = false, poll_due = false;
+    int nw_src = 1;
+    std::vector<int32_t> nwin, pend, pend_len;
     Geom geom() const {
         Geom g{};
         g.npairs = npairs; g.hkv = P.num_kv_heads; g.G = P.group_size; g.GP = GP; g.dtype = P.dtype;
@@ -74,6 +81,7 @@ struct mosaic_cache {
         g.sel_num = P.select_num; g.sel_den = P.select_den; g.force = P.force_default_strategy;
         g.trunc = P.trunc_channels;
         g.fp8 = P.value_fp8;
+        g.dyn = dyn ? 1 : 0; g.min_win = P.min_window; g.tau_win = P.tau_window;
         return g;
     }
     WsGeom wsgeom(void *ws) const {
@@ -142,6 +150,9 @@ void mosaic_params_default(mosaic_params *p) {
     p->force_default_strategy = 0;
     p->trunc_channels = 128;
     p->value_fp8 = 0;
+    p->dyn_windows = 0;
+    p->tau_window = 8.0f;
+    p->min_window = 1024;
 }
 
 static mosaic_status check_params(const mosaic_params *p) {
@@ -182,6 +193,13 @@ static mosaic_status check_params(const mosaic_params *p) {
                 return fail(MOSAIC_ERR_INVALID, "keep_cand[%d] = %d: a multiple of 4 with value_fp8", i, p->keep_cand[i]);
         if (p->default_keep % 4) return fail(MOSAIC_ERR_INVALID, "default_keep %d: a multiple of 4 with value_fp8", p->default_keep);
     }
+    if (p->dyn_windows != 0 && p->dyn_windows != 1) return fail(MOSAIC_ERR_INVALID, "dyn_windows %d: 0 or 1", p->dyn_windows);
+    if (p->dyn_windows) {
+        if (!std::isfinite(p->tau_window) || p->tau_window < 0)
+            return fail(MOSAIC_ERR_INVALID, "tau_window must be finite and >= 0");
+        if (p->min_window < SEG || p->min_window % SEG || p->min_window > p->rot_window)
+            return fail(MOSAIC_ERR_INVALID, "min_window %d: a multiple of 64 in [64, rot_window]", p->min_window);
+    }
     return MOSAIC_OK;
 }
 
@@ -198,9 +216,20 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     c->npairs = num_seqs * params->num_kv_heads;
     c->GP = params->group_size <= 4 ? 4 : 8;
     c->nw = (max_tokens + params->rot_window - 1) / params->rot_window;
+    c->nw_src = c->nw;
+    c->dyn = params->dyn_windows != 0;
+    if (c->dyn) {
+        if (!c->rotated) {
+            delete c;
+            return fail(MOSAIC_ERR_INVALID, "dynamic windows need rotations (rotated = 1)");
+        }
+        // every closed window holds at least min_window tokens; one is open
+        c->nw = std::max(c->nw, max_tokens / params->min_window + 1);
+    }
     if (c->nw > MAX_WINDOWS) {
+        const int nw = c->nw;
         delete c;
-        return fail(MOSAIC_ERR_UNSUPPORTED, "%d rotation windows per sequence (at most %d)", (max_tokens + params->rot_window - 1) / params->rot_window, MAX_WINDOWS);
+        return fail(MOSAIC_ERR_UNSUPPORTED, "%d rotation windows per sequence (at most %d)", nw, MAX_WINDOWS);
     }
     c->max_desc = max_tokens / SEG + 2;
     int maxrec = 0, maxtok = 0, minb = params->default_block;
@@ -240,7 +269,8 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
         o = off;
         off = align256(off + stride * (uint64_t)c->npairs);
     };
-    region(l.meta_off, l.meta_stride, sizeof(PairMeta));
+    // meta: the counters, then (dynamic windows) the window table
+    region(l.meta_off, l.meta_stride, sizeof(PairMeta) + (c->dyn ? (uint64_t)(c->nw + 1) * 4 : 0));
     region(l.desc_off, l.desc_stride, (uint64_t)c->max_desc * sizeof(Desc));
     region(l.score_off, l.score_stride, sc_bytes);
     region(l.token_off, l.token_stride, tok_bytes);
@@ -279,6 +309,9 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     c->arena = nullptr;
     c->compressed = false;
     c->L.assign(num_seqs, 0);
+    c->nwin.assign(c->npairs, 1);
+    c->pend.assign(c->npairs, -1);
+    c->pend_len.assign(c->npairs, 0);
     *out = c;
     return ok();
 }
@@ -362,11 +395,17 @@ mosaic_status mosaic_compress(mosaic_cache *c, const void *k, const void *v, int
     int32_t *ctx_dev = (int32_t *)(c->arena + c->ctx_off);
     hipError_t e = launch_ctx_copy(ctx_dev, ctx_lens_host, c->num_seqs, s);
     if (e != hipSuccess) return hip_fail(e, "copy of context lengths");
-    if (c->rotated && (e = launch_copy_rot(g, rot_k, rot_v, s)) != hipSuccess) return hip_fail(e, "rotation copy");
+    if (c->rotated && (e = launch_copy_rot(g, rot_k, rot_v, c->nw_src, s)) != hipSuccess) return hip_fail(e, "rotation copy");
     e = launch_compress(g, (const uint16_t *)k, (const uint16_t *)v, seq_stride, ctx_dev, maxL / SEG, any_tail,
                         (uint8_t *)ws, c->slot_tok, c->slot_sc, s);
     if (e != hipSuccess) return hip_fail(e, "compress launch");
     for (int q = 0; q < c->num_seqs; ++q) c->L[q] = ctx_lens_host[q];
+    if (c->dyn)
+        for (int p = 0; p < c->npairs; ++p) {
+            c->nwin[p] = std::min((c->L[p / c->P.num_kv_heads] / SEG) / (c->P.rot_window / SEG) + 1, c->nw);
+            c->pend[p] = -1;
+        }
+    c->poll_due = false;
     c->compressed = true;
     return ok();
 }
@@ -379,7 +418,17 @@ mosaic_status mosaic_append(mosaic_cache *c, const void *k_new, const void *v_ne
     int due = 0;                            // MAINT_FLUSH / MAINT_FINALIZE of some sequence
     for (int q = 0; q < c->num_seqs; ++q) {
         if (c->L[q] + 1 > c->max_tokens) return fail(MOSAIC_ERR_CAPACITY, "sequence %d is full (%d tokens)", q, c->L[q]);
-        if ((c->L[q] + 1) % UBUF == 0) due |= ((c->L[q] + 1) % SEG == 0) ? MAINT_FINALIZE : MAINT_FLUSH;
+        if ((c->L[q] + 1) % UBUF == 0) {
+            due |= ((c->L[q] + 1) % SEG == 0) ? MAINT_FINALIZE : MAINT_FLUSH;
+            if (c->dyn && c->poll_due)
+                return fail(MOSAIC_ERR_STATE, "a segment completed since the last mosaic_window_poll: poll (and close "
+                                              "what it reports) before the buffer of sequence %d is compressed", q);
+            if (c->dyn)
+                for (int h = 0; h < c->P.num_kv_heads; ++h)
+                    if (c->pend[q * c->P.num_kv_heads + h] >= 0)
+                        return fail(MOSAIC_ERR_STATE, "sequence %d kv head %d: a closed window awaits its rotation "
+                                                      "(mosaic_window_close)", q, h);
+        }
     }
     hipStream_t s = (hipStream_t)stream;
     const Geom g = c->geom();
@@ -387,6 +436,7 @@ mosaic_status mosaic_append(mosaic_cache *c, const void *k_new, const void *v_ne
     if (e != hipSuccess) return hip_fail(e, "append launch");
     if (due && (e = launch_maintain(g, MAINT_APPEND, due, s)) != hipSuccess) return hip_fail(e, "flush/finalize launch");
     for (int q = 0; q < c->num_seqs; ++q) c->L[q] += 1;
+    if (c->dyn && (due & MAINT_FINALIZE)) c->poll_due = true;
     return ok();
 }
 
@@ -406,8 +456,17 @@ mosaic_status mosaic_decode_attention(mosaic_cache *c, const void *q, float *out
         max_desc = std::max(max_desc, L / SEG + ((L % SEG) >= UBUF ? 1 : 0));
         maxL = std::max(maxL, L);
     }
-    const int nwu = std::max(1, std::min(c->nw, (maxL + c->P.rot_window - 1) / c->P.rot_window));
-    hipError_t e = launch_decode(c->geom(), c->wsgeom(ws), (const uint16_t *)q, out, sm_scale, max_desc, nwu,
+    int nwu = std::max(1, std::min(c->nw, (maxL + c->P.rot_window - 1) / c->P.rot_window));
+    Geom g = c->geom();
+    if (c->dyn) {
+        // the windows in use as of the last poll: a window closed since then
+        // is still empty (nothing is compressed before the poll), so it adds
+        // nothing; the decode works on that many windows
+        nwu = 1;
+        for (int p = 0; p < c->npairs; ++p) nwu = std::max(nwu, c->nwin[p]);
+        g.nw = nwu;
+    }
+    hipError_t e = launch_decode(g, c->wsgeom(ws), (const uint16_t *)q, out, sm_scale, max_desc, nwu,
                                  (hipStream_t)stream, c->timing ? c->ev : nullptr);
     if (e != hipSuccess) return hip_fail(e, "decode launch");
     if (c->timing) c->timed_once = true;
@@ -595,9 +654,66 @@ mosaic_status mosaic_cache_stats(const mosaic_cache *c, mosaic_stats *out, void 
             }
             if (ri >= 0 && gi >= 0 && bi >= 0) out->strategy_hist[ri][gi][bi]++;
         }
-        if (c->rotated) out->rotation_bytes += (int64_t)((L + c->P.rot_window - 1) / c->P.rot_window) * 2 * D * D * 4;
+        if (c->rotated)
+            out->rotation_bytes += (int64_t)(c->dyn ? meta[p].nwin : (L + c->P.rot_window - 1) / c->P.rot_window) * 2 * D * D * 4;
     }
     out->dense_bytes = out->tokens * 2 * D * 2 * hkv;
+    return ok();
+}
+
+mosaic_status mosaic_window_poll(mosaic_cache *c, int32_t *out_host, int32_t *n_closed_host, void *stream) {
+    if (!c || !out_host || !n_closed_host) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    if (!c->dyn) return fail(MOSAIC_ERR_INVALID, "the cache was created without dynamic windows");
+    if (!c->arena || !c->compressed) return fail(MOSAIC_ERR_STATE, "poll before compress");
+    hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+    std::vector<uint8_t> meta((size_t)c->npairs * c->lay.meta_stride);
+    e = hipMemcpy(meta.data(), c->arena + c->lay.meta_off, meta.size(), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "meta copy");
+    int n = 0;
+    for (int p = 0; p < c->npairs; ++p) {
+        const uint8_t *m = meta.data() + (size_t)p * c->lay.meta_stride;
+        PairMeta pm;
+        std::memcpy(&pm, m, sizeof(pm));
+        const int32_t *wt = (const int32_t *)(m + sizeof(PairMeta));
+        if (pm.nwin < 1 || pm.nwin > c->nw || pm.pend < -1 || pm.pend >= pm.nwin - 1)
+            return fail(MOSAIC_ERR_STATE, "pair %d: window state out of range (%d windows, pending %d)", p, pm.nwin, pm.pend);
+        c->nwin[p] = pm.nwin;
+        c->pend[p] = pm.pend;
+        c->pend_len[p] = pm.pend >= 0 ? (wt[pm.pend + 1] - wt[pm.pend]) * SEG : 0;
+        out_host[3 * p] = pm.pend;
+        out_host[3 * p + 1] = pm.pend >= 0 ? wt[pm.pend] * SEG : 0;
+        out_host[3 * p + 2] = pm.pend >= 0 ? (wt[pm.pend + 1] - wt[pm.pend]) * SEG : 0;
+        n += pm.pend >= 0;
+    }
+    c->poll_due = false;
+    *n_closed_host = n;
+    return ok();
+}
+
+mosaic_status mosaic_window_close(mosaic_cache *c, const float *rot_k, const float *rot_v, const void *k, const void *v,
+                                  int64_t seq_stride, void *stream) {
+    if (!c) return fail(MOSAIC_ERR_INVALID, "NULL cache");
+    if (!c->dyn) return fail(MOSAIC_ERR_INVALID, "the cache was created without dynamic windows");
+    if (!c->arena || !c->compressed) return fail(MOSAIC_ERR_STATE, "close before compress");
+    if (c->poll_due) return fail(MOSAIC_ERR_STATE, "a segment completed since the last mosaic_window_poll");
+    if (!rot_k || !rot_v || !k || !v) return fail(MOSAIC_ERR_INVALID, "NULL rot_k, rot_v, k or v");
+    if (((uintptr_t)rot_k | (uintptr_t)rot_v | (uintptr_t)k | (uintptr_t)v) % 16)
+        return fail(MOSAIC_ERR_INVALID, "rot_k, rot_v, k and v must be 16-byte aligned");
+    int max_tok = 0, n = 0;
+    for (int p = 0; p < c->npairs; ++p) {
+        if (c->pend[p] < 0) continue;
+        ++n;
+        max_tok = std::max(max_tok, c->pend_len[p]);
+    }
+    if (n == 0) return ok();
+    if (seq_stride < max_tok)
+        return fail(MOSAIC_ERR_INVALID, "seq_stride %lld < longest closed window %d", (long long)seq_stride, max_tok);
+    const int max_segs = max_tok / SEG;
+    hipError_t e = launch_close(c->geom(), rot_k, rot_v, (const uint16_t *)k, (const uint16_t *)v, seq_stride, max_segs,
+                                (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "close launch");
+    for (int p = 0; p < c->npairs; ++p) { c->pend[p] = -1; c->pend_len[p] = 0; }
     return ok();
 }
 

@@ -356,12 +356,8 @@ __device__ __forceinline__ void stage_keys(const float (&yk)[TPW][2], SegSmem<NW
 
 // ------------------------------------------------------------------ kernels
 
-// R^T of K and V and R of V for every window of every pair, into the arena.
-__global__ void k_copy_rot(Geom g, const float *rk, const float *rv) {
-    const int p = blockIdx.y, w = blockIdx.x;
-    const float *Rk = rk + ((uint64_t)p * g.nw + w) * D * D;
-    const float *Rv = rv + ((uint64_t)p * g.nw + w) * D * D;
-    float *dst = g.rot_of(p, w);
+// R^T of K and V and R of V of one rotation into a window slot
+__device__ __forceinline__ void put_rot(float *dst, const float *Rk, const float *Rv) {
     for (int i = threadIdx.x; i < D * D; i += blockDim.x) {
         const int j = i / D, c = i % D;        // source R[j][c]
         dst[c * D + j] = Rk[i];
@@ -370,36 +366,61 @@ __global__ void k_copy_rot(Geom g, const float *rk, const float *rv) {
     }
 }
 
+// every window slot of every pair, from the caller's nw_src windows per pair
+// (slots past them take the last one: windows that close later get their own)
+__global__ void k_copy_rot(Geom g, const float *rk, const float *rv, int nw_src) {
+    const int p = blockIdx.y, w = blockIdx.x, ws = min(w, nw_src - 1);
+    put_rot(g.rot_of(p, w), rk + ((uint64_t)p * nw_src + ws) * D * D, rv + ((uint64_t)p * nw_src + ws) * D * D);
+}
+
 __global__ void k_set_meta(Geom g, const int32_t *ctx) {
     const int p = blockIdx.x * blockDim.x + threadIdx.x;
     if (p >= g.npairs) return;
     PairMeta *m = g.meta_of(p);
     m->L = ctx[p / g.hkv];
     m->nblk_final = 0; m->tok_tail = 0; m->sc_tail = 0;
+    m->nwin = 1; m->wloss = 0.0f; m->pend = -1;
+    if (g.dyn) {
+        // input tokens sit in fixed windows of W tokens (Sec. 4.3); the window
+        // holding the first token after the full segments stays open
+        const int spw = g.W / SEG, nwin = min((m->L / SEG) / spw + 1, g.nw);
+        int32_t *wt = g.wtab_of(p);
+        for (int w = 0; w < nwin; ++w) wt[w] = w * spw;
+        m->nwin = nwin;
+    }
 }
 
-// mode 0: strategy selection of full prefill segments; mode 1: packing.
 // mode 0: choose the segment's strategy; mode 1: pack it at its descriptor's
 // offsets (both rotate the tokens); mode 2: both from one rotation, packing
 // into the segment's worst-case slot of the workspace (slot_tok + slot_sc
 // bytes per (pair, segment)), from where k_compact moves the records to their
-// offsets once the offsets are known.
+// offsets once the offsets are known.  With close set (modes 0 and 1), the
+// segments are those of each pair's window awaiting its rotation, and the
+// input holds that window's tokens from its first one.
 // (one instantiation per mode, so that each gets its own register budget:
 // three waves per SIMD)
 template <int MODE>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
 k_prefill(Geom g, const uint16_t *k, const uint16_t *v, int64_t seq_stride, uint8_t *ws, uint32_t slot_tok,
-          uint32_t slot_sc) {
-    constexpr int mode = MODE;
+          uint32_t slot_sc, int close) {
     constexpr int TPW = 16, NWV = 4;
     __shared__ SegSmem<NWV> sm;
-    const int p = blockIdx.y, seg = blockIdx.x;
+    const int p = blockIdx.y;
     const PairMeta *meta = g.meta_of(p);
-    const int nfull = meta->L / SEG;
-    if (seg >= nfull) return;
-    const uint64_t base = ((uint64_t)p * seq_stride + (uint64_t)seg * SEG) * D;
+    int seg = blockIdx.x, win;
+    if (close) {
+        const int pw = meta->pend;
+        if (pw < 0) return;
+        const int32_t *wt = g.wtab_of(p);
+        seg += wt[pw];
+        if (seg >= wt[pw + 1]) return;
+        win = pw;
+    } else {
+        if (seg >= meta->L / SEG) return;
+        win = (seg * SEG) / g.W;
+    }
+    const uint64_t base = ((uint64_t)p * seq_stride + (uint64_t)blockIdx.x * SEG) * D;
     Desc *desc = g.desc_of(p) + seg;
-    const int win = (seg * SEG) / g.W;
     const float *rot = g.rotated ? g.rot_of(p, win) : nullptr;
     float yk[TPW][2], yv[TPW][2];
     rotate_tile(k + base, SEG, rot, g.dtype, sm, yk);
@@ -466,16 +487,27 @@ __global__ void __launch_bounds__(256) k_compact(Geom g, const uint8_t *ws, uint
 }
 
 // Exclusive scan of segment sizes per pair -> descriptor offsets and tails.
-__global__ void __launch_bounds__(256) k_scan(Geom g) {
+// With close set, the segments of the window awaiting its rotation, from the
+// offsets its first segment already has (every earlier segment is kept).
+__global__ void __launch_bounds__(256) k_scan(Geom g, int close) {
     __shared__ uint32_t s_tok[256], s_sc[256], s_blk[256];
     __shared__ uint32_t carry[3];
     const int p = blockIdx.x, tid = threadIdx.x;
     PairMeta *meta = g.meta_of(p);
-    const int nfull = meta->L / SEG;
+    int s_first = 0, nfull = meta->L / SEG;
+    if (close) {
+        const int pw = meta->pend;
+        if (pw < 0) return;
+        s_first = g.wtab_of(p)[pw];
+        nfull = g.wtab_of(p)[pw + 1];
+    }
     Desc *desc = g.desc_of(p);
-    if (tid == 0) { carry[0] = carry[1] = carry[2] = 0; }
+    if (tid == 0) {
+        if (close) { carry[0] = desc[s_first].tok_off; carry[1] = desc[s_first].sc_off; carry[2] = desc[s_first].first_block; }
+        else { carry[0] = carry[1] = carry[2] = 0; }
+    }
     __syncthreads();
-    for (int base = 0; base < nfull; base += 256) {
+    for (int base = s_first; base < nfull; base += 256) {
         const int s = base + tid;
         uint32_t tb = 0, sb = 0, nb = 0;
         if (s < nfull) {
@@ -547,8 +579,27 @@ __global__ void k_append(Geom g, const uint16_t *kn, const uint16_t *vn) {
 // the pair's update buffer, which is empty when a segment completes (every
 // buffered token belongs to it) and is next written by the following append.
 constexpr int MT_TPW = 2, MT_NWV = 8, MT_TOK = MT_TPW * MT_NWV, MT_THREADS = 64 * MT_NWV;
-constexpr int FST_N = 2 + 2 * NCAND + 3;           // per-token statistics: tot K/V, drop K/V x 9, bvar x 3
+// per-token statistics: tot K/V, drop K/V x 9, bvar x 3, and (dynamic
+// windows) the dropped energy of K/V under the provisional strategy
+constexpr int FST_PROV = 2 + 2 * NCAND + 3;
+constexpr int FST_N = FST_PROV + 2;
 static_assert(FST_N * SEG * 4 + 16 <= 2 * UBUF * D * 2, "finalize statistics and offsets fit the update buffer");
+
+// dropped energy of each of the wave's tokens under (r, 2^log2g), from lane 0
+// into out[t] (t = token within the workgroup's run)
+template <int TPW, int NWV>
+__device__ __forceinline__ void prov_drop(const Geom &g, const float (&y)[TPW][2], int r, int log2g,
+                                          SegSmem<NWV> &sm, float *out) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, t0 = wave * TPW;
+    const int n = r >> log2g;
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+        int rlo, rhi;
+        group_ranks(y[i][0], y[i][1], log2g, g.trunc >> log2g, sm.keys[wave], rlo, rhi);
+        const float d = tree128(rlo < n ? 0.0f : y[i][0] * y[i][0], rhi < n ? 0.0f : y[i][1] * y[i][1]);
+        if (lane == 0) out[t0 + i] = d;
+    }
+}
 
 __device__ __forceinline__ bool maint_due(const Geom &g, int mode, int L, bool fin) {
     const int m = L % SEG;
@@ -563,7 +614,8 @@ __device__ __forceinline__ bool maint_due(const Geom &g, int mode, int L, bool f
 // yv) and stage the rotated keys for blocks spanning several waves
 __device__ __forceinline__ void maint_rotate(const Geom &g, int p, int seg, int tb, int ntok, SegSmem<MT_NWV> &sm,
                                              float (&yk)[MT_TPW][2], float (&yv)[MT_TPW][2]) {
-    const int win = (seg * SEG) / g.W;
+    // the trailing segment belongs to the open window
+    const int win = g.dyn ? g.meta_of(p)->nwin - 1 : (seg * SEG) / g.W;
     const float *rot = g.rotated ? g.rot_of(p, win) : nullptr;
     const uint16_t *stg = g.stg_of(p) + (uint64_t)tb * D;
     rotate_tile(stg, ntok - tb, rot, g.dtype, sm, yk);
@@ -627,14 +679,22 @@ __global__ void __launch_bounds__(MT_THREADS) k_fin_stats(Geom g) {
         uint32_t *off = (uint32_t *)(st + FST_N * SEG);
         off[0] = meta->tok_tail; off[1] = meta->sc_tail; off[2] = (uint32_t)meta->nblk_final;
     }
-    if (g.force) return;
+    if (g.force && !g.dyn) return;
     float yk[MT_TPW][2], yv[MT_TPW][2];
     maint_rotate(g, p, seg, tb, SEG, sm, yk, yv);
     token_stats(g, yk, 0, sm, MT_TOK);
     token_stats(g, yv, 1, sm, MT_TOK);
     block_stats(g, yk, sm, MT_TOK);
+    if (g.dyn) {
+        // the segment's loss under the provisional strategy (the previous
+        // finalized segment's (r, g), else the default): dropped energy per token
+        int r = g.def_keep, log2g = ilog2i(g.def_group);
+        if (seg > 0) { const Desc pd = g.desc_of(p)[seg - 1]; r = pd.r; log2g = pd.log2g; }
+        prov_drop(g, yk, r, log2g, sm, st + FST_PROV * SEG + tb);
+        prov_drop(g, yv, r, log2g, sm, st + (FST_PROV + 1) * SEG + tb);
+    }
     __syncthreads();
-    for (int i = threadIdx.x; i < FST_N * MT_TOK; i += MT_THREADS) {
+    for (int i = threadIdx.x; i < FST_PROV * MT_TOK; i += MT_THREADS) {
         const int k = i / MT_TOK, t = i % MT_TOK;
         const float v = k < 2 ? sm.tot[k][t] : (k < 2 + 2 * NCAND ? sm.drop[(k - 2) / NCAND][(k - 2) % NCAND][t]
                                                                   : sm.bvar[k - 2 - 2 * NCAND][t]);
@@ -658,7 +718,7 @@ __global__ void __launch_bounds__(MT_THREADS) k_fin_pack(Geom g) {
     if (g.force) {
         r = g.def_keep; log2g = ilog2i(g.def_group); log2b = ilog2i(g.def_block);
     } else {
-        for (int i = threadIdx.x; i < FST_N * SEG; i += MT_THREADS) {
+        for (int i = threadIdx.x; i < FST_PROV * SEG; i += MT_THREADS) {
             const int k = i / SEG, t = i % SEG;
             const float v = st[i];
             if (k < 2) sm.tot[k][t] = v;
@@ -670,6 +730,56 @@ __global__ void __launch_bounds__(MT_THREADS) k_fin_pack(Geom g) {
         r = sm.strat[0]; log2g = sm.strat[1]; log2b = sm.strat[2];
     }
     maint_pack(g, p, seg, tb, SEG, true, r, log2g, log2b, off[0], off[1], (int)off[2], sm, yk, yv);
+}
+
+// Windows closed by their loss (Sec. 4.3 dynamic compression strategy,
+// Sec. 5.5 incremental strategy generation): after a finalize, a wave per
+// pair adds the segment's loss under the provisional strategy -- the larger of
+// K's and V's relative dropped energy, segment sums as 64-token pairwise trees
+// -- to its window's sum, and closes the window after this segment when it
+// holds W tokens, or when the sum exceeds tau_win and it holds min_win
+// tokens.  The closed window awaits its own rotation (pend); the next segment
+// opens a window.  Runs after k_fin_pack, which no longer reads the window.
+__global__ void __launch_bounds__(256) k_win_update(Geom g) {
+    const int p = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (p >= g.npairs) return;
+    PairMeta *meta = g.meta_of(p);
+    const int L = meta->L;
+    if (!maint_due(g, MAINT_APPEND, L, true)) return;
+    const float *st = (const float *)g.buf_of(p);
+    const float TK = tree64(st[lane]), TV = tree64(st[SEG + lane]);
+    const float DK = tree64(st[FST_PROV * SEG + lane]), DV = tree64(st[(FST_PROV + 1) * SEG + lane]);
+    if (lane != 0) return;
+    const float lk = TK > 0.0f ? DK / TK : 0.0f, lv = TV > 0.0f ? DV / TV : 0.0f;
+    const float loss = lk > lv ? lk : lv;
+    const int seg = L / SEG - 1, nwin = meta->nwin;
+    int32_t *wt = g.wtab_of(p);
+    const int ntok = (seg + 1 - wt[nwin - 1]) * SEG;
+    const float acc = meta->wloss + loss;
+    const bool close = ntok >= g.W || (acc > g.tau_win && ntok >= g.min_win);
+    if (close && nwin < g.nw) {
+        wt[nwin] = seg + 1;
+        meta->nwin = nwin + 1;
+        meta->pend = nwin - 1;
+        meta->wloss = 0.0f;
+    } else {
+        meta->wloss = acc;
+    }
+}
+
+// The new rotation of each pair's closed window into its slot and the next
+// one (the provisional rotation of the window the close opened).
+__global__ void k_close_rot(Geom g, const float *rk, const float *rv) {
+    const int p = blockIdx.y, pw = g.meta_of(p)->pend;
+    if (pw < 0) return;
+    const int w = pw + (int)blockIdx.x;
+    if (w >= g.nw) return;
+    put_rot(g.rot_of(p, w), rk + (uint64_t)p * D * D, rv + (uint64_t)p * D * D);
+}
+
+__global__ void k_close_done(Geom g) {
+    const int p = blockIdx.x * blockDim.x + threadIdx.x;
+    if (p < g.npairs) g.meta_of(p)->pend = -1;
 }
 
 // ------------------------------------------------------------------ channel reorder
@@ -771,8 +881,26 @@ hipError_t launch_ctx_copy(int32_t *dst_dev, const int32_t *src_host, int n, hip
     return hipMemcpyAsync(dst_dev, src_host, sizeof(int32_t) * (size_t)n, hipMemcpyHostToDevice, s);
 }
 
-hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, hipStream_t s) {
-    hipLaunchKernelGGL(k_copy_rot, dim3(g.nw, g.npairs), dim3(256), 0, s, g, rk, rv);
+hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, int nw_src, hipStream_t s) {
+    hipLaunchKernelGGL(k_copy_rot, dim3(g.nw, g.npairs), dim3(256), 0, s, g, rk, rv, nw_src);
+    return hipGetLastError();
+}
+
+hipError_t launch_close(const Geom &g, const float *rk, const float *rv, const uint16_t *k, const uint16_t *v,
+                        int64_t seq_stride, int max_segs, hipStream_t s) {
+    hipLaunchKernelGGL(k_close_rot, dim3(2, g.npairs), dim3(256), 0, s, g, rk, rv);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 grid(max_segs, g.npairs);
+    if (max_segs > 0) {
+        hipLaunchKernelGGL(k_prefill<0>, grid, dim3(256), 0, s, g, k, v, seq_stride, (uint8_t *)nullptr, 0u, 0u, 1);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(k_scan, dim3(g.npairs), dim3(256), 0, s, g, 1);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(k_prefill<1>, grid, dim3(256), 0, s, g, k, v, seq_stride, (uint8_t *)nullptr, 0u, 0u, 1);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_close_done, dim3(ceil_div(g.npairs, 256)), dim3(256), 0, s, g);
     return hipGetLastError();
 }
 
@@ -788,15 +916,15 @@ hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, 
     if (e != hipSuccess) return e;
     const dim3 grid(max_full_segs, g.npairs);
     if (max_full_segs > 0) {
-        if (ws) hipLaunchKernelGGL(k_prefill<2>, grid, dim3(256), 0, s, g, k, v, seq_stride, ws, slot_tok, slot_sc);
-        else hipLaunchKernelGGL(k_prefill<0>, grid, dim3(256), 0, s, g, k, v, seq_stride, ws, slot_tok, slot_sc);
+        if (ws) hipLaunchKernelGGL(k_prefill<2>, grid, dim3(256), 0, s, g, k, v, seq_stride, ws, slot_tok, slot_sc, 0);
+        else hipLaunchKernelGGL(k_prefill<0>, grid, dim3(256), 0, s, g, k, v, seq_stride, ws, slot_tok, slot_sc, 0);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(k_scan, dim3(g.npairs), dim3(256), 0, s, g);
+    hipLaunchKernelGGL(k_scan, dim3(g.npairs), dim3(256), 0, s, g, 0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (max_full_segs > 0) {
         if (ws) hipLaunchKernelGGL(k_compact, grid, dim3(256), 0, s, g, (const uint8_t *)ws, slot_tok, slot_sc);
-        else hipLaunchKernelGGL(k_prefill<1>, grid, dim3(256), 0, s, g, k, v, seq_stride, ws, slot_tok, slot_sc);
+        else hipLaunchKernelGGL(k_prefill<1>, grid, dim3(256), 0, s, g, k, v, seq_stride, ws, slot_tok, slot_sc, 0);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (any_tail) {
@@ -848,6 +976,10 @@ hipError_t launch_maintain(const Geom &g, int mode, int what, hipStream_t s) {
         if ((e = hipGetLastError()) != hipSuccess) return e;
         hipLaunchKernelGGL(k_fin_pack, dim3(g.npairs, SEG / MT_TOK), dim3(MT_THREADS), 0, s, g);
         if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (g.dyn) {
+            hipLaunchKernelGGL(k_win_update, dim3(ceil_div(g.npairs, 4)), dim3(256), 0, s, g);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
     }
     return hipSuccess;
 }

@@ -469,7 +469,8 @@ __device__ __forceinline__ void score_any(const PVec<RMAX> &x, int r, int l2g, u
 
 // grid (ceil(max segments / spw), pairs): a workgroup scores the block keys of
 // spw <= SCORE_SEGS consecutive segments, one lane per block key; spw is at
-// most a rotation window's segments, so a workgroup sees at most two windows.
+// most the segments of every window but a pair's last (W, or the least a
+// window closed by its loss holds), so a workgroup sees at most two windows.
 template <int DT, int GP, int RMAX, bool FR>
 __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
     __shared__ __align__(16) float qs[2][D * GP];
@@ -498,8 +499,10 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         plain = d.log2g == 0 && d.r <= 32 && (d.sc_off & 3u) == 0;
         dense = d.log2g == 0 && d.r == D && (d.sc_off & 15u) == 0;
     }
-    const int w0 = g.rotated ? (s0 * SEG) / g.W : 0;
-    const int w1 = g.rotated ? ((s0 + ns - 1) * SEG) / g.W : 0;
+    // the window of the first segment and the first segment of the next one
+    const int w0 = g.rotated ? win_of_seg(g, p, s0) : 0;
+    const int nxt = g.rotated ? win_first_seg(g, p, w0 + 1) : 0x7fffffff;
+    const int w1 = (s0 + ns - 1 >= nxt) ? w0 + 1 : w0;
     {
         const float4 *src = (const float4 *)(ws.qrot + (uint64_t)p * (ws.qrot_stride / 4));
         float4 *d0 = (float4 *)qs[0], *d1 = (float4 *)qs[1];
@@ -537,7 +540,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
                 uint4 t[D / 8];
 #pragma unroll
                 for (int k = 0; k < D / 8; ++k) t[k] = v4[k];
-                const uint32_t qa = lds_addr(qs) + ((g.rotated && ((s0 + i) * SEG) / g.W != w0) ? D * GP * 4 : 0);
+                const uint32_t qa = lds_addr(qs) + ((s0 + i >= nxt) ? D * GP * 4 : 0);
                 float acc[GP];
 #pragma unroll
                 for (int h = 0; h < GP; ++h) acc[h] = 0.0f;
@@ -598,7 +601,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
             load_pvec<RMAX, 1, false, 4>(xn, recn, recn + bmb, 32, true);
             __builtin_amdgcn_sched_barrier(0);
             if (g.trunc < D) mask_words(x.bw, g.trunc);       // a truncated bitmap's bytes past T bits are values
-            const uint32_t qoff = (g.rotated && ((s0 + i) * SEG) / g.W != w0) ? D * GP * 4 : 0;
+            const uint32_t qoff = (s0 + i >= nxt) ? D * GP * 4 : 0;
             float acc[GP];
 #pragma unroll
             for (int h = 0; h < GP; ++h) acc[h] = 0.0f;
@@ -626,7 +629,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
         const int j = b - (int)(d.first_block - fb0);
         const int r = valid ? d.r : 0, l2g = d.log2g;
         const uint8_t *rec = valid ? sc + d.sc_off + (uint32_t)j * (uint32_t)vec_bytes(r, l2g, g.trunc) : sc;
-        const uint32_t qoff = (g.rotated && ((s0 + i) * SEG) / g.W != w0) ? D * GP * 4 : 0;
+        const uint32_t qoff = (s0 + i >= nxt) ? D * GP * 4 : 0;
         const bool a16 = __all(!valid || (l2g == 0 && ((uintptr_t)rec & 15u) == 0 && g.trunc == D));
         PVec<RMAX> x;
         load_pvec<RMAX, -1, true>(x, rec, rec + bm_bytes(l2g, g.trunc), wave_max_i(r), a16);
@@ -783,10 +786,9 @@ constexpr int TOPK_MAXW = MAX_WINDOWS;                     // rotation windows t
 // first block of each of the first nwl rotation windows (windows past the
 // last segment start at nb)
 __device__ __forceinline__ void window_firsts(const Geom &g, int p, int nb, int ndesc, int nwl, int *fbw) {
-    const int segs_per_win = g.W / SEG;
     const Desc *gd = g.desc_of(p);
     for (int w = threadIdx.x; w < nwl; w += 1024) {
-        const int s0 = w * segs_per_win;
+        const int s0 = win_first_seg(g, p, w);
         fbw[w] = (s0 < ndesc) ? (int)gd[s0].first_block : nb;
     }
 }
@@ -2009,7 +2011,7 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w_in, const uint16_t *q
     if (e != hipSuccess) return e;
     if (ev) hipEventRecord(ev[1], s);
     if (max_desc_used > 0) {
-        const int spw = max(1, min(SCORE_SEGS, g.W / SEG));
+        const int spw = max(1, min(SCORE_SEGS, (g.dyn ? g.min_win : g.W) / SEG));
         const dim3 grid(ceil_div(max_desc_used, spw), g.npairs);
         if (fixed) hipLaunchKernelGGL((k_score<DT, GP, 48, true>), grid, dim3(256), 0, s, g, w, spw);
         else if (small) hipLaunchKernelGGL((k_score<DT, GP, 48, false>), grid, dim3(256), 0, s, g, w, spw);

@@ -32,7 +32,12 @@ struct PairMeta {             // per (sequence, kv head) device counters, 64 byt
     int32_t nblk_final;       // scoreable blocks of finalized segments
     uint32_t tok_tail;        // token-arena bytes of finalized segments
     uint32_t sc_tail;         // score-arena bytes of finalized segments
-    int32_t pad[12];
+    // windows closed by their loss (caches with dynamic windows only; the
+    // window table of int32 first segments follows this struct)
+    int32_t nwin;             // windows in use; window nwin - 1 is open
+    float wloss;              // accumulated loss of the open window
+    int32_t pend;             // closed window awaiting its rotation, -1 none
+    int32_t pad[9];
 };
 static_assert(sizeof(PairMeta) == 64, "meta size");
 
@@ -50,6 +55,9 @@ struct Geom {
     int sel_num, sel_den, force;
     int trunc;                        // channels represented in the bitmaps (T)
     int fp8;                          // K and V token values stored as E4M3 codes
+    int dyn;                          // windows of decode tokens closed by their loss
+    int min_win;                      // tokens a window holds before a loss close
+    float tau_win;                    // accumulated loss that closes a window
 
     __host__ __device__ PairMeta *meta_of(int p) const { return (PairMeta *)(meta + (uint64_t)p * meta_stride); }
     __host__ __device__ Desc *desc_of(int p) const { return (Desc *)(desc + (uint64_t)p * desc_stride); }
@@ -57,6 +65,10 @@ struct Geom {
     __host__ __device__ uint8_t *tok_of(int p) const { return tok + (uint64_t)p * tok_stride; }
     __host__ __device__ uint16_t *buf_of(int p) const { return (uint16_t *)((uint8_t *)buf + (uint64_t)p * buf_stride); }
     __host__ __device__ uint16_t *stg_of(int p) const { return (uint16_t *)((uint8_t *)stg + (uint64_t)p * stg_stride); }
+    // first segment of each window of pair p (dynamic windows)
+    __host__ __device__ int32_t *wtab_of(int p) const {
+        return (int32_t *)(meta + (uint64_t)p * meta_stride + sizeof(PairMeta));
+    }
     // rotation window w of pair p: [0] = R_k^T, [1] = R_v^T, [2] = R_v  (each D x D fp32)
     __host__ __device__ float *rot_of(int p, int w) const {
         if (w >= nw) w = nw - 1;
@@ -78,6 +90,24 @@ struct WsGeom {               // decode workspace
     int max_blocks, max_splits, max_sel;
     int split_slots;                        // attention workgroups resident at once on the device
 };
+
+// First segment of window w of pair p: every W tokens, or from the window
+// table (a window not in use starts past every segment).
+__device__ __forceinline__ int win_first_seg(const Geom &g, int p, int w) {
+    if (!g.dyn) return w * (g.W / SEG);
+    return w < g.meta_of(p)->nwin ? g.wtab_of(p)[w] : 0x7fffffff;
+}
+// Window of segment s of pair p: the last window starting at or before s.
+__device__ __forceinline__ int win_of_seg(const Geom &g, int p, int s) {
+    if (!g.dyn) return (s * SEG) / g.W;
+    const int32_t *wt = g.wtab_of(p);
+    int lo = 0, hi = g.meta_of(p)->nwin - 1;          // wt[0] = 0 <= s
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (wt[mid] <= s) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
 
 // a block's record: its byte offset in the pair's token arena, and
 // r << 8 | log2 g << 16 | log2 B << 20
@@ -198,7 +228,13 @@ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 // ---------------------------------------------------------------- launchers
 // (implemented in the .hip files; all return hipError_t of the launch)
 hipError_t launch_ctx_copy(int32_t *dst_dev, const int32_t *src_host, int n, hipStream_t s);
-hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, hipStream_t s);
+// nw_src: windows of rk / rv per pair; slots past them repeat the last one
+hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, int nw_src, hipStream_t s);
+// close of the windows awaiting their rotation (dynamic windows): the new
+// rotations rk / rv [pairs][D][D], the windows' raw tokens k / v
+// [pairs][seq_stride][D]; max_segs: segments of the longest closed window
+hipError_t launch_close(const Geom &g, const float *rk, const float *rv, const uint16_t *k, const uint16_t *v,
+                        int64_t seq_stride, int max_segs, hipStream_t s);
 // ws: NULL (two passes, each rotating the tokens) or the single-pass
 // workspace of slot_tok + slot_sc bytes per (pair, segment slot)
 hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, int64_t seq_stride,

@@ -34,8 +34,13 @@ hipError_t launch_ctx_copy(int32_t *, const int32_t *src_host, int n, hipStream_
     rec("%s", s.c_str());
     return hipSuccess;
 }
-hipError_t launch_copy_rot(const Geom &g, const float *, const float *, hipStream_t) {
-    rec("copy_rot npairs=%d nw=%d", g.npairs, g.nw);
+hipError_t launch_copy_rot(const Geom &g, const float *, const float *, int nw_src, hipStream_t) {
+    rec("copy_rot npairs=%d nw=%d src=%d", g.npairs, g.nw, nw_src);
+    return hipSuccess;
+}
+hipError_t launch_close(const Geom &g, const float *, const float *, const uint16_t *, const uint16_t *,
+                        int64_t seq_stride, int max_segs, hipStream_t) {
+    rec("close npairs=%d stride=%lld segs=%d", g.npairs, (long long)seq_stride, max_segs);
     return hipSuccess;
 }
 hipError_t launch_compress(const Geom &g, const uint16_t *, const uint16_t *, int64_t seq_stride, const int32_t *,

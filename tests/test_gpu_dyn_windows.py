@@ -1,0 +1,148 @@
+"""GPU parity of windows closed by their compression loss (Sec. 4.3 dynamic
+partitioning of output tokens, Sec. 5.5 incremental strategy generation).
+
+A C5-shaped batch (G = 7, bf16, ragged prefills, one of them longer than the
+maximum window and one with a remainder) appends 1500 drifting tokens per
+sequence through the C ABI.  Whenever the library refuses an append because a
+poll or a close is due, the test polls, checks that the windows the GPU
+closed are exactly the ones the oracle closed, computes each closed window's
+rotation from its raw tokens on the host (fp64 eigendecomposition) and hands
+the same rotation to both.  At checkpoints the whole state of every pair
+(arenas, descriptors, update buffer, staging, window table and the open
+window's loss bits) is byte-exact against the oracle, block scores and
+selections are bit-exact, and decode outputs agree within 2e-3 max-abs and
+1e-3 rel-L2.  Every pair must see at least two windows closed by their loss
+(shorter than the maximum length).
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_00760_amd as M
+from _parity import D, assert_close, assert_state_equal, bits, oracle_decode_all, scale_of
+from oracle import oracle as O
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+W, MINW, TAU, APPENDS = 2048, 256, 2.0, 1500
+CTX = (700, 1000, 1290, 2100)
+HKV, G = 2, 7
+CHECK_EVERY = 250
+
+
+def _stream(b, h, which):
+    n = CTX[b] + APPENDS
+    return gen.drift_tokens(f"dyn.{b}.{h}", n, which).to(torch.bfloat16)
+
+
+def _setup():
+    ns = len(CTX)
+    toks = {(b, h, w): _stream(b, h, w) for b in range(ns) for h in range(HKV) for w in ("k", "v")}
+    cap = max(CTX) + APPENDS
+    nw_src = -(-cap // W)
+    Lmax = max(CTX)
+    k = torch.zeros((ns, HKV, Lmax, D), dtype=torch.bfloat16)
+    v = torch.zeros_like(k)
+    rk = torch.empty((ns, HKV, nw_src, D, D))
+    rv = torch.empty_like(rk)
+    for b in range(ns):
+        for h in range(HKV):
+            L = CTX[b]
+            k[b, h, :L] = toks[(b, h, "k")][:L]
+            v[b, h, :L] = toks[(b, h, "v")][:L]
+            rk[b, h] = gen._rotations(k[b, h, :L].float(), L, W, nw_src, "cpu")
+            rv[b, h] = gen._rotations(v[b, h, :L].float(), L, W, nw_src, "cpu")
+    lp = M.Params(num_kv_heads=HKV, group_size=G, dtype="bf16", rot_window=W, dyn_windows=True, tau_window=TAU,
+                  min_window=MINW)
+    op = O.Params(group=G, dtype="bf16", rot_window=W, dyn=True, tau_window=TAU, min_window=MINW)
+    return toks, cap, k, v, rk, rv, lp, op
+
+
+def _gpu_windows(c, p, nwin_max):
+    raw = c.region("meta", p, 64 + 4 * (nwin_max + 1)).cpu().numpy()
+    m = raw[:64].view(np.int32)
+    nwin, pend = int(m[4]), int(m[6])
+    wloss = raw[20:24].view(np.float32)[0]
+    wseg = raw[64:64 + 4 * nwin].view(np.int32).tolist()
+    return dict(nwin=nwin, pend=pend, wloss=float(wloss), wseg=wseg)
+
+
+def test_loss_closed_windows_match_oracle():
+    toks, cap, k, v, rk, rv, lp, op = _setup()
+    ns, npairs = len(CTX), len(CTX) * HKV
+    print(f"[dyn] ctx={CTX} appends={APPENDS} W={W} min={MINW} tau={TAU}", flush=True)
+    c = M.MosaicCache(lp, ns, cap, rotated=True)
+    c.compress(k.cuda(), v.cuda(), list(CTX), rk.cuda(), rv.cuda())
+    ops = []
+    for p in range(npairs):
+        b, h = divmod(p, HKV)
+        pr = O.Pair(op, cap, rk[b, h].numpy(), rv[b, h].numpy())
+        pr.compress(bits(k[b, h, :CTX[b]]), bits(v[b, h, :CTX[b]]))
+        ops.append(pr)
+    kb = {key: bits(t) for key, t in toks.items()}
+    closes = {p: [] for p in range(npairs)}
+    sc = scale_of()
+    nslots = c.layout.num_windows
+    for t in range(APPENDS):
+        kn = torch.stack([torch.stack([toks[(b, h, "k")][CTX[b] + t] for h in range(HKV)]) for b in range(ns)])
+        vn = torch.stack([torch.stack([toks[(b, h, "v")][CTX[b] + t] for h in range(HKV)]) for b in range(ns)])
+        try:
+            c.append(kn.cuda(), vn.cuda())
+        except M.MosaicError as e:
+            assert e.status == -4, e
+            got = c.window_poll()
+            want = {}
+            for p, pr in enumerate(ops):
+                w = pr.windows()
+                if w["pend"] >= 0:
+                    a, bnd = w["wseg"][w["pend"]], w["wseg"][w["pend"] + 1]
+                    want[p] = (w["pend"], a * 64, (bnd - a) * 64)
+            assert got == want, f"step {t}: GPU closed {got}, oracle {want}"
+            if got:
+                maxlen = max(n for _, _, n in got.values())
+                Rk = torch.zeros((ns, HKV, D, D))
+                Rv = torch.zeros_like(Rk)
+                kw = torch.zeros((ns, HKV, maxlen, D), dtype=torch.bfloat16)
+                vw = torch.zeros_like(kw)
+                for p, (w, a, n) in got.items():
+                    b, h = divmod(p, HKV)
+                    kw[b, h, :n] = toks[(b, h, "k")][a:a + n]
+                    vw[b, h, :n] = toks[(b, h, "v")][a:a + n]
+                    Rk[b, h] = gen.window_rotation(kw[b, h, :n].float())
+                    Rv[b, h] = gen.window_rotation(vw[b, h, :n].float())
+                    ops[p].close(Rk[b, h].numpy(), Rv[b, h].numpy(), bits(kw[b, h, :n]), bits(vw[b, h, :n]))
+                    closes[p].append((w, a, n))
+                c.window_close(Rk.cuda(), Rv.cuda(), kw.cuda(), vw.cuda())
+                print(f"[dyn] step {t}: closed {sorted(got.items())}", flush=True)
+            c.append(kn.cuda(), vn.cuda())
+        for p, pr in enumerate(ops):
+            b, h = divmod(p, HKV)
+            assert pr.append_status(kb[(b, h, "k")][CTX[b] + t], kb[(b, h, "v")][CTX[b] + t]) == 0, (t, p)
+        if t % CHECK_EVERY == CHECK_EVERY - 1 or t == APPENDS - 1:
+            torch.cuda.synchronize()
+            for p, pr in enumerate(ops):
+                assert_state_equal(c, p, pr, where=f"step {t}")
+                gw, ow = _gpu_windows(c, p, nslots), pr.windows()
+                assert gw["nwin"] == ow["nwin"] and gw["pend"] == ow["pend"] and gw["wseg"] == ow["wseg"], (t, p, gw, ow)
+                assert np.float32(gw["wloss"]).view(np.uint32) == np.float32(ow["wloss"]).view(np.uint32), (t, p)
+            q = torch.randn((ns, HKV * G, D), generator=torch.Generator().manual_seed(t)).to(torch.bfloat16)
+            out = c.decode(q.cuda(), sc)
+            torch.cuda.synchronize()
+            want, sels, scores = oracle_decode_all(ops, gen.spec("c5", ctx=CTX, hkv=HKV, group=G), q, sc)
+            nwu = max(pr.windows()["nwin"] for pr in ops)
+            for p, pr in enumerate(ops):
+                nb = pr.info().nblk
+                gs = c.ws_region("score", p, 4 * nb).cpu().numpy().view(np.uint32)
+                assert np.array_equal(gs, scores[p].view(np.uint32)), (t, p)
+                wsel = c.ws_region("wsel", p, 4 * (nwu + 2)).cpu().numpy().view(np.int32)
+                kk = int(wsel[nwu])
+                gsel = c.ws_region("sel", p, 4 * max(kk, 1)).cpu().numpy().view(np.int32)[:kk]
+                assert np.array_equal(gsel, sels[p]), (t, p)
+            err = assert_close(out.cpu().numpy(), want, f"step {t}")
+            print(f"[dyn] step {t}: state byte-exact, windows {[pr.windows()['nwin'] for pr in ops]}, "
+                  f"max-abs {err[0]:.2e} rel-L2 {err[1]:.2e}", flush=True)
+    for p in range(npairs):
+        by_loss = [x for x in closes[p] if x[2] < W]
+        assert len(by_loss) >= 2, f"pair {p}: closes {closes[p]}"
+    print(f"[dyn] closes per pair {[len(closes[p]) for p in range(npairs)]}", flush=True)

@@ -163,8 +163,47 @@ def run_checks(path):
     assert L.mosaic_compress(h3, kv, kv, 130, ctx1, None, None, None, 0, None) == INVALID
     rot = sim.buf(2 * 128 * 128 * 4, 16)
     assert L.mosaic_compress(h3, kv, kv, 130, ctx1, rot, rot, None, 0, None) == OK
-    assert sim.log() == ["ctx_copy 130", "copy_rot npairs=1 nw=2", "compress npairs=1 stride=130 segs=2 tail=1"]
+    assert sim.log() == ["ctx_copy 130", "copy_rot npairs=1 nw=2 src=2", "compress npairs=1 stride=130 segs=2 tail=1"]
     assert L.mosaic_cache_destroy(h3) == OK
+    # ---- dynamic windows: parameters, window slots, and the poll-before-compress rule
+    for kw, st in [(dict(dyn_windows=2), INVALID), (dict(dyn_windows=1, min_window=100), INVALID),
+                   (dict(dyn_windows=1, min_window=0), INVALID), (dict(dyn_windows=1, tau_window=float("nan")), INVALID),
+                   (dict(dyn_windows=1, rot_window=256, min_window=512), INVALID)]:
+        pp = sim.params(**kw)
+        assert L.mosaic_cache_create(C.byref(pp), 1, 1000, 1, C.byref(h2)) == st, kw
+    pp = sim.params(dyn_windows=1)
+    assert L.mosaic_cache_create(C.byref(pp), 1, 1000, 0, C.byref(h2)) == INVALID         # needs rotations
+    pp = sim.params(dyn_windows=1, min_window=64)
+    assert L.mosaic_cache_create(C.byref(pp), 1, 70000, 1, C.byref(h2)) == UNSUPPORTED    # 1094 windows > 1024
+    h4, p4, arena4 = sim.cache(2, 1000, rotated=1, num_kv_heads=1, rot_window=512, dyn_windows=1, min_window=128)
+    lay = _lib.MosaicLayout()
+    assert L.mosaic_cache_layout(h4, C.byref(lay)) == OK
+    assert lay.num_windows == 1000 // 128 + 1 and lay.meta_stride >= 64 + 4 * (lay.num_windows + 1)
+    assert L.mosaic_cache_bind(h4, sim.buf(arena4), arena4) == OK
+    ctx4 = (C.c_int32 * 2)(62, 10)
+    rot4 = sim.buf(2 * 2 * 128 * 128 * 4, 16)
+    assert L.mosaic_compress(h4, kv, kv, 100, ctx4, rot4, rot4, None, 0, None) == OK
+    assert sim.log()[1] == "copy_rot npairs=2 nw=8 src=2"
+    closed = (C.c_int32 * 6)()
+    nclosed = C.c_int32()
+    h5, _, _ = sim.cache(1, 100)
+    assert L.mosaic_window_poll(h5, closed, C.byref(nclosed), None) == INVALID               # a fixed-window cache
+    assert L.mosaic_cache_destroy(h5) == OK
+    assert L.mosaic_window_close(h4, rot4, rot4, kv, kv, 64, None) == OK                     # nothing to close
+    assert sim.log() == []
+    assert L.mosaic_append(h4, kv, kv, None) == OK                                           # sequence 0: 63 tokens
+    assert L.mosaic_append(h4, kv, kv, None) == OK                                           # 64: finalize
+    assert sim.log()[-1] == "maintain mode=0 flush=0 finalize=1"
+    assert L.mosaic_window_close(h4, rot4, rot4, kv, kv, 64, None) == STATE                  # poll first
+    for _ in range(19):                                                                      # no compression due
+        assert L.mosaic_append(h4, kv, kv, None) == OK
+    # sequence 1 would reach 32 tokens: its buffer would be compressed before a poll
+    assert sim.tokens(h4, 2) == [83, 31]
+    sim.log()
+    assert L.mosaic_append(h4, kv, kv, None) == STATE
+    assert sim.log() == [] and sim.tokens(h4, 2) == [83, 31]
+    assert "poll" in L.mosaic_last_error().decode()
+    assert L.mosaic_cache_destroy(h4) == OK
     return True
 
 

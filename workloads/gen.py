@@ -204,6 +204,19 @@ def _plant(s: WorkloadSpec, k32, q_group, L, seq, kvh, device, target=0.80):
     return k32, mask, c
 
 
+def window_rotation(x32):
+    """[D][D] fp32 rotation of one window's vectors x32 [n][D]: rows are the
+    eigenvectors of the uncentered X^T X in fp64 by descending eigenvalue, each
+    signed so that its largest-magnitude component is positive."""
+    X = x32.double().cpu()
+    evals, evecs = torch.linalg.eigh(X.T @ X)
+    rows = evecs.T.flip(0)                                  # descending eigenvalue
+    amax = rows.abs().argmax(dim=1)
+    sign = torch.sign(rows[torch.arange(D), amax])
+    sign[sign == 0] = 1.0
+    return (rows * sign[:, None]).float()
+
+
 def _rotations(x32, L, W, nw, device):
     """[nw][D][D] fp32 rows = eigenvectors of X^T X (descending eigenvalue)."""
     R = torch.empty((nw, D, D), dtype=torch.float32, device=device)
@@ -211,17 +224,27 @@ def _rotations(x32, L, W, nw, device):
     for w in range(nw):
         a, b = w * W, min((w + 1) * W, L)
         if a < b:
-            X = x32[a:b].double()
-            cov = X.T @ X
-            evals, evecs = torch.linalg.eigh(cov.cpu())
-            rows = evecs.T.flip(0)                          # descending eigenvalue
-            amax = rows.abs().argmax(dim=1)
-            sign = torch.sign(rows[torch.arange(D), amax])
-            sign[sign == 0] = 1.0
-            rows = rows * sign[:, None]
-            last = rows.float().to(device)
+            last = window_rotation(x32[a:b]).to(device)
         R[w] = last if last is not None else torch.eye(D, device=device)
     return R
+
+
+def drift_tokens(seed, n, which, drift=0.05, device="cpu"):
+    """[n][D] fp32 anisotropic tokens whose principal directions turn slowly
+    (decode streams for windows closed by their loss): direction j has scale
+    4 exp(-j / 12) + 0.05, and the basis turns by a fixed small rotation every
+    16 tokens, so a window's rotation fits later tokens less and less well."""
+    g = _gen("cpu", seed, "drift", which)
+    Q, _ = torch.linalg.qr(torch.randn((D, D), generator=g, dtype=torch.float64))
+    A = torch.randn((D, D), generator=g, dtype=torch.float64) * drift
+    step = torch.linalg.matrix_exp((A - A.T) / 2)
+    scales = torch.exp(-torch.arange(D, dtype=torch.float64) / 12.0) * 4 + 0.05
+    z = torch.randn((n, D), generator=g, dtype=torch.float64) * scales
+    out = torch.empty((n, D), dtype=torch.float64)
+    for t0 in range(0, n, 16):
+        out[t0:t0 + 16] = z[t0:t0 + 16] @ Q.T
+        Q = step @ Q
+    return out.float().to(device)
 
 
 def make_layer(s: WorkloadSpec, layer: int = 0, device="cpu", queries=None, capacity=None):
