@@ -127,6 +127,7 @@ typedef struct {
     int32_t nwin;        /* windows in use; window nwin - 1 is open */
     float wloss;         /* accumulated loss of the open window */
     int32_t pend;        /* closed window awaiting its rotation, or -1 */
+    double *cov;         /* [2][2][D][D]: window w's uncentered K and V covariance in slot w % 2 */
 } orc_pair;
 
 typedef struct {
@@ -475,6 +476,7 @@ orc_pair *orc_pair_new(const orc_params *P, int cap, const float *rk, const floa
     p->P = *P; p->cap = cap; p->nw = nw;
     p->pend = -1; p->nwin = 1;
     p->wseg = (int32_t *)calloc((size_t)(nw > 0 ? nw : 1) + 1, sizeof(int32_t));
+    if (P->dyn) p->cov = (double *)calloc((size_t)4 * D * D, sizeof(double));
     int mv = max_vec_bytes(P), mb = min_block(P);
     int nseg = cap / P->seg_len + 2;
     p->tok_cap = (size_t)nseg * P->seg_len * 2 * mv;
@@ -498,7 +500,7 @@ orc_pair *orc_pair_new(const orc_params *P, int cap, const float *rk, const floa
 
 void orc_pair_free(orc_pair *p) {
     if (!p) return;
-    free(p->tok); free(p->sc); free(p->desc); free(p->rk); free(p->rv); free(p->wseg); free(p);
+    free(p->tok); free(p->sc); free(p->desc); free(p->rk); free(p->rv); free(p->wseg); free(p->cov); free(p);
 }
 
 /* Window of segment s: every rot_window tokens, or with dynamic windows the
@@ -554,6 +556,28 @@ float orc_segment_loss(const orc_params *P, const float *yk, const float *yv, in
     return lk > lv ? lk : lv;
 }
 
+/* Incremental covariance of a window (Sec. 5.5: the covariance is updated
+   with each new token's outer product, so that the rotation of a closed
+   window comes from it at once).  One segment's 64 raw tokens (k, v: [S][D])
+   are added to window w's uncentered K and V covariance: per entry (i, j),
+   the fp64 sum over the tokens in order of x_t[i] x_t[j] (each product exact
+   in fp64), then added to the window's running entry (which the window's
+   first segment replaces).  Windows alternate between two slots. */
+static void cov_add_segment(orc_pair *p, int w, const uint16_t *k, const uint16_t *v, int first) {
+    const int S = p->P.seg_len;
+    for (int which = 0; which < 2; ++which) {
+        const uint16_t *x = which ? v : k;
+        double *C = p->cov + ((size_t)(w & 1) * 2 + which) * D * D;
+        for (int i = 0; i < D; ++i)
+            for (int j = 0; j < D; ++j) {
+                double s = 0.0;
+                for (int t = 0; t < S; ++t)
+                    s = s + (double)to_f32(x[(size_t)t * D + i], p->P.dtype) * (double)to_f32(x[(size_t)t * D + j], p->P.dtype);
+                C[i * D + j] = (first ? 0.0 : C[i * D + j]) + s;
+            }
+    }
+}
+
 /* Segment s, finalized by the append path, belongs to the open window: add
    its loss; the window closes after s when it holds rot_window tokens (the
    maximum length), or when the accumulated loss exceeds tau_window and it
@@ -604,6 +628,8 @@ static void finalize_segment(orc_pair *p, int from_append) {
     float loss = 0.0f;
     const int dyn = P->dyn && from_append;
     if (dyn) {
+        const int w = p->nwin - 1;
+        cov_add_segment(p, w, p->stgk, p->stgv, nf == p->wseg[w]);
         int rp = P->def_keep, gp = P->def_group;
         if (nf > 0) { rp = p->desc[nf - 1].r; gp = 1 << p->desc[nf - 1].log2g; }
         loss = orc_segment_loss(P, yk, yv, S, rp, gp);
@@ -672,6 +698,11 @@ int orc_pair_compress(orc_pair *p, const uint16_t *k, const uint16_t *v, int L) 
         p->L = (s + 1) * S;
         finalize_segment(p, 0);
     }
+    if (P->dyn) {   /* the open window's covariance over its prefill segments */
+        const int w = p->nwin - 1;
+        for (int s = p->wseg[w]; s < nfull; ++s)
+            cov_add_segment(p, w, k + (size_t)s * S * D, v + (size_t)s * S * D, s == p->wseg[w]);
+    }
     p->L = nfull * S;
     for (int t = nfull * S; t < L; ++t) orc_pair_append(p, k + (size_t)t * D, v + (size_t)t * D);
     return 0;
@@ -713,6 +744,13 @@ int orc_pair_close(orc_pair *p, const float *rk_new, const float *rv_new, const 
 void orc_pair_windows(const orc_pair *p, int32_t *nwin, int32_t *pend, float *wloss, int32_t *wseg) {
     *nwin = p->nwin; *pend = p->pend; *wloss = p->wloss;
     if (wseg) for (int w = 0; w < p->nwin; ++w) wseg[w] = p->wseg[w];
+}
+
+/* Window w's incremental covariance (which: 0 K, 1 V) into out [D][D]; it
+   stays readable until the window two after it first accumulates. */
+void orc_pair_cov(const orc_pair *p, int w, int which, double *out) {
+    if (!p->cov) { memset(out, 0, (size_t)D * D * sizeof(double)); return; }
+    memcpy(out, p->cov + ((size_t)(w & 1) * 2 + which) * D * D, (size_t)D * D * sizeof(double));
 }
 
 void orc_pair_info(const orc_pair *p, orc_info *o) {

@@ -149,6 +149,7 @@ def lib():
         L.orc_max_windows.argtypes = [C.POINTER(OrcParams), C.c_int]; L.orc_max_windows.restype = C.c_int
         L.orc_pair_close.argtypes = [C.c_void_p, fp, fp, u16p, u16p]; L.orc_pair_close.restype = C.c_int
         L.orc_pair_windows.argtypes = [C.c_void_p, i32p, i32p, fp, i32p]; L.orc_pair_windows.restype = None
+        L.orc_pair_cov.argtypes = [C.c_void_p, C.c_int, C.c_int, f64p]; L.orc_pair_cov.restype = None
         L.orc_select_count.argtypes = [C.c_int, C.c_int, C.c_int]; L.orc_select_count.restype = C.c_int
         L.orc_select_budget.argtypes = [C.c_int, C.c_int, C.c_int]; L.orc_select_budget.restype = C.c_int
         L.orc_select_blocks.argtypes = [fp, i32p, C.c_int, C.c_int, u8p]; L.orc_select_blocks.restype = C.c_int
@@ -369,6 +370,15 @@ class Pair:
         ws = np.zeros(max(nwin.value, 1), np.int32)
         lib().orc_pair_windows(self._h, C.byref(nwin), C.byref(pend), C.byref(wl), _p(ws, C.c_int32))
         return dict(nwin=nwin.value, pend=pend.value, wloss=float(np.float32(wl.value)), wseg=ws[:nwin.value].tolist())
+
+    def cov(self, w):
+        """(K, V) incremental covariances [D][D] fp64 of window w (R-23)."""
+        out = []
+        for which in (0, 1):
+            a = np.zeros((D, D), np.float64)
+            lib().orc_pair_cov(self._h, w, which, _p(a, C.c_double))
+            out.append(a)
+        return tuple(out)
 
     def close(self, rot_k, rot_v, k, v):
         """Close of the window awaiting its rotation: new R (rows = channels)

@@ -382,3 +382,38 @@ def test_decode_over_loss_closed_windows_matches_numpy_decoder():
     out, sel = pr.decode(q, 0.125)
     assert len(sel) == pr.info().nblk
     assert np.max(np.abs(out - want)) < 1e-9
+
+
+# ---------------------------------------------------------------- the incremental covariance
+def test_incremental_covariance_is_window_gram_matrix():
+    """Integer tokens (every product and sum exact in fp64): at each close,
+    the window's incrementally accumulated covariance equals X^T X of its raw
+    tokens exactly -- the prefill part of the open window included (a prefill
+    of two fixed windows plus a remainder), and the slot of the window before
+    it untouched."""
+    r = np.random.default_rng(21)
+    P = dyn_params(rot_window=1024, tau_window=1.0, min_window=128)
+    L0, N = 1100, 2600
+    xk = r.integers(-4, 5, (N, D)).astype(np.float32)
+    xv = r.integers(-4, 5, (N, D)).astype(np.float32)
+    xk[:, :8] *= 3                                       # some structure: the first channels dominate
+    k, v = to_bits(xk), to_bits(xv)
+    pr = O.Pair(P, N, eye_rot(3), eye_rot(3))
+    pr.compress(k[:L0], v[:L0])
+    assert pr.windows()["wseg"] == [0, 16]               # window 1 holds tokens 1024..1087 so far
+    ck, cv = pr.cov(1)
+    assert np.array_equal(ck, xk[1024:1088].astype(np.float64).T @ xk[1024:1088].astype(np.float64))
+    checked = []
+
+    def closer(p, w, a, b):
+        ck, cv = p.cov(w)
+        X, Y = xk[a:b].astype(np.float64), xv[a:b].astype(np.float64)
+        assert np.array_equal(ck, X.T @ X) and np.array_equal(cv, Y.T @ Y), (w, a, b)
+        if w > 0:                                        # the previous window's slot is the other one
+            pk, _ = p.cov(w - 1)
+            assert not np.array_equal(pk, ck)
+        identity_closer(p, w, a, b, k, v)
+        checked.append((w, a, b))
+
+    drive(pr, k, v, closer, L0)
+    assert len(checked) >= 3 and checked[0][1] == 1024
