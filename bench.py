@@ -154,6 +154,52 @@ def update_path_us(M, gen, spec, params, dev):
             "append_with_finalize_us": med([x for t, x in enumerate(times) if kind(t) == 2]), "samples": n}
 
 
+def dyn_window_us(M, gen, spec, params, dev, reps=3):
+    """Windows closed by their loss (Sec. 4.3 dynamic partitioning of output
+    tokens, Sec. 5.5), c3 batch shape, 4096-token windows: a 4032-token
+    prefill per pair, so that the 64th append completes the window's last
+    segment and closes it (maximum length).  Times that append (finalize plus
+    the loss update) and mosaic_window_close (every pair's new rotation and the
+    re-encoding of its 4096 tokens, strategy and packing passes); medians over
+    `reps` fresh caches."""
+    import dataclasses
+    import torch
+    W = 4096
+    small = gen.spec(spec.name, ctx=(W - 64,) * spec.num_seqs, appends=64, rot_window=W)
+    lay = gen.make_layer(small, 0, device=dev, capacity=small.capacity)
+    dp = dataclasses.replace(params, rot_window=W, dyn_windows=True, min_window=1024, tau_window=1e30)
+    apps = [tuple(x.to(dev) for x in gen.make_appends(small, t)) for t in range(64)]
+    kw = torch.cat([lay["k"][:, :, :W - 64], torch.stack([a[0] for a in apps], dim=2)], dim=2).contiguous()
+    vw = torch.cat([lay["v"][:, :, :W - 64], torch.stack([a[1] for a in apps], dim=2)], dim=2).contiguous()
+    rk, rv = lay["rot_k"][:, :, 0].contiguous(), lay["rot_v"][:, :, 0].contiguous()
+    fin, close = [], []
+    for _ in range(reps):
+        cache = M.MosaicCache(dp, small.num_seqs, small.capacity, rotated=True, device=dev)
+        cache.compress(lay["k"], lay["v"], lay["ctx_lens"], lay["rot_k"], lay["rot_v"])
+        for t in range(63):
+            cache.append(*apps[t])
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record()
+        cache.append(*apps[63])
+        ev[1].record()
+        closed = cache.window_poll()                 # synchronizes
+        if len(closed) != cache.num_pairs or any(x[2] != W for x in closed.values()):
+            raise RuntimeError(f"expected every window to close at {W} tokens: {closed}")
+        ev[2].record()
+        cache.window_close(rk, rv, kw, vw)
+        ev[3].record()
+        torch.cuda.synchronize()
+        fin.append(1e3 * ev[0].elapsed_time(ev[1]))
+        close.append(1e3 * ev[2].elapsed_time(ev[3]))
+        del cache
+    med = lambda xs: float(sorted(xs)[len(xs) // 2])
+    pairs = small.num_seqs * small.hkv
+    return {"pairs": pairs, "window_tokens": W, "append_with_finalize_and_close_us": round(med(fin), 1),
+            "window_close_us": round(med(close), 1), "close_tokens_per_s": round(pairs * W / (med(close) * 1e-6)),
+            "reps": reps}
+
+
 def encoding_overlap(cache, lay, dev, compress_ms):
     """Compression of one layer on a second stream while a stand-in of the
     next layer's prefill compute runs on the first (Sec. 5.5 asynchronous
@@ -394,10 +440,14 @@ def main():
         log(f"reorder {reorder}")
 
     update_path = None
+    dyn_windows = None
     overlap = None
     if not args.no_extras and nlayers == 1 and not appends:
         update_path = update_path_us(M, gen, spec, params, dev)
         log(f"append {update_path}")
+        if spec.rotate:
+            dyn_windows = dyn_window_us(M, gen, spec, params, dev)
+            log(f"windows closed by their loss {dyn_windows}")
         overlap = encoding_overlap(cache, lay, dev, compress_ms)
         log(f"encoding overlap {overlap}")
 
@@ -696,7 +746,7 @@ def main():
         "compress_ms": round(compress_ms, 3), "memory_ratio": round(ratio, 4),
         "rotations_ms": None if rotations_ms is None else round(rotations_ms, 3),
         "channel_reorder": reorder,
-        "update_path": update_path, "encoding_overlap": overlap,
+        "update_path": update_path, "dyn_windows": dyn_windows, "encoding_overlap": overlap,
         "strategies": {f"{k[0]}/{k[1]}/{k[2]}": v for k, v in sorted(stats[0]["strategies"].items())},
         "cpu_baseline": cpu, "parity": parity, "datagen_s": round(t_gen, 1), "source_hash": source_hash(),
     }

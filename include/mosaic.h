@@ -138,6 +138,14 @@ mosaic_status mosaic_cache_destroy(mosaic_cache *cache);
  *   buffer   : update buffer [2 (K, V)][U][D] raw elements (Sec. 5.3)
  *   stage    : raw tokens of the trailing segment [2][S][D] (Sec. 5.4)
  *   rot      : per window {R_k^T, R_v^T, R_v} fp32 [3][D][D]
+ *   cov      : (dyn_windows) fp64 [2][2][D][D]: in slot w % 2 the uncentered
+ *              covariance X^T X of window w's K (then V) tokens, updated
+ *              segment by segment as segments are finalized (Sec. 5.5
+ *              incremental covariance); a closed window's stays in its slot
+ *              until the window after next accumulates, so it can be read
+ *              after mosaic_window_poll to compute the window's rotation.
+ *              Entry (i, j) is the fp64 sum over each segment's tokens in
+ *              order of x[i] x[j], added to the window's running entry.
  */
 typedef struct {
     uint64_t meta_off, meta_stride;
@@ -149,6 +157,7 @@ typedef struct {
     uint64_t rot_off, rot_stride;
     uint64_t total;
     int32_t num_pairs, max_desc, num_windows, reserved;
+    uint64_t cov_off, cov_stride;   /* dyn_windows only (else 0) */
 } mosaic_layout;
 mosaic_status mosaic_cache_layout(const mosaic_cache *cache, mosaic_layout *out);
 

@@ -211,6 +211,14 @@ class MosaicCache:
                                                _stream(self.device)))
         self._keep_close = (rot_k, rot_v, k, v)
 
+    def window_cov(self, pair: int, window: int):
+        """(K, V) incremental covariances [128][128] fp64 of a window of a pair
+        (dynamic windows; valid for the open window and the one before it)."""
+        import torch
+        base = self.layout.cov_off + pair * self.layout.cov_stride + (window & 1) * 2 * D * D * 8
+        raw = self.arena[base: base + 2 * D * D * 8].view(torch.float64).reshape(2, D, D)
+        return raw[0], raw[1]
+
     KERNELS = ("qrot", "score", "topk", "attn", "reduce")
 
     def set_timing(self, enable: bool = True):

@@ -39,7 +39,8 @@ class MosaicLayout(C.Structure):
     _fields_ = [(n, C.c_uint64) for n in (
         "meta_off", "meta_stride", "desc_off", "desc_stride", "score_off", "score_stride", "token_off",
         "token_stride", "buf_off", "buf_stride", "stage_off", "stage_stride", "rot_off", "rot_stride", "total")] + [
-        ("num_pairs", C.c_int32), ("max_desc", C.c_int32), ("num_windows", C.c_int32), ("reserved", C.c_int32)]
+        ("num_pairs", C.c_int32), ("max_desc", C.c_int32), ("num_windows", C.c_int32), ("reserved", C.c_int32),
+        ("cov_off", C.c_uint64), ("cov_stride", C.c_uint64)]
 
 
 class MosaicWsLayout(C.Structure):

@@ -73,6 +73,7 @@ struct mosaic_cache {
         g.meta_stride = lay.meta_stride; g.desc_stride = lay.desc_stride; g.sc_stride = lay.score_stride;
         g.tok_stride = lay.token_stride; g.buf_stride = lay.buf_stride; g.stg_stride = lay.stage_stride;
         g.rot_stride = lay.rot_stride;
+        g.cov = (double *)(arena + lay.cov_off); g.cov_stride = lay.cov_stride;
         for (int i = 0; i < 3; ++i) {
             g.keep_cand[i] = P.keep_cand[i]; g.group_cand[i] = P.group_cand[i]; g.block_cand[i] = P.block_cand[i];
         }
@@ -277,6 +278,7 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     region(l.buf_off, l.buf_stride, 2ull * UBUF * D * 2);
     region(l.stage_off, l.stage_stride, 2ull * SEG * D * 2);
     region(l.rot_off, l.rot_stride, c->rotated ? (uint64_t)c->nw * 3 * D * D * 4 : 0);
+    if (c->dyn) region(l.cov_off, l.cov_stride, 4ull * D * D * 8);
     c->ctx_off = off;
     off = align256(off + (uint64_t)num_seqs * 4);
     l.total = off;

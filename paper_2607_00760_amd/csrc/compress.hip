@@ -767,6 +767,51 @@ __global__ void __launch_bounds__(256) k_win_update(Geom g) {
     }
 }
 
+// Incremental covariance of the open window (Sec. 5.5: updated with each new
+// token's outer product; here segment by segment): grid (pairs, K / V, 8
+// blocks of 16 rows), 256 threads, thread t owning entries (16 b + t / 16,
+// 8 (t % 16) .. + 7).  Per segment, each entry is the fp64 sum over the 64
+// tokens in order of x[i] x[j] (products exact), added to the window's running
+// entry (replacing it at the window's first segment).  from_input = 0: the
+// segment an append just finalized (tokens in the staging area), for pairs
+// whose finalize ran; 1: after a prefill, the open window's full segments,
+// from the input x (pair p's token s at (p seq_stride + s) D).
+__global__ void __launch_bounds__(256) k_cov_seg(Geom g, const uint16_t *kin, const uint16_t *vin, int64_t seq_stride,
+                                                 int from_input) {
+    __shared__ float xs[SEG][D];
+    const int p = blockIdx.x, which = blockIdx.y, tid = threadIdx.x;
+    const PairMeta *meta = g.meta_of(p);
+    const int L = meta->L, w = meta->nwin - 1;
+    const int32_t *wt = g.wtab_of(p);
+    int s0, s1;
+    if (from_input) {
+        s0 = wt[w]; s1 = L / SEG;
+    } else {
+        if (!maint_due(g, MAINT_APPEND, L, true)) return;
+        s0 = L / SEG - 1; s1 = s0 + 1;
+    }
+    const int i = blockIdx.z * 16 + tid / 16, j0 = (tid % 16) * 8;
+    double *C = g.cov_of(p, w, which) + (uint64_t)i * D + j0;
+    for (int s = s0; s < s1; ++s) {
+        const uint16_t *src = from_input ? (which ? vin : kin) + ((uint64_t)p * seq_stride + (uint64_t)s * SEG) * D
+                                         : g.stg_of(p) + (uint64_t)which * SEG * D;
+        __syncthreads();
+        for (int e = tid; e < SEG * D; e += 256) xs[e / D][e % D] = h2f(src[e], g.dtype);
+        __syncthreads();
+        double acc[8];
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) acc[jj] = 0.0;
+        for (int t = 0; t < SEG; ++t) {
+            const double xi = (double)xs[t][i];
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj) acc[jj] = acc[jj] + xi * (double)xs[t][j0 + jj];
+        }
+        const bool first = s == wt[w];
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) C[jj] = (first ? 0.0 : C[jj]) + acc[jj];
+    }
+}
+
 // The new rotation of each pair's closed window into its slot and the next
 // one (the provisional rotation of the window the close opened).
 __global__ void k_close_rot(Geom g, const float *rk, const float *rv) {
@@ -914,6 +959,10 @@ hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, 
                            uint32_t slot_sc, hipStream_t s) {
     hipError_t e = launch_set_meta(g, ctx_dev, s);
     if (e != hipSuccess) return e;
+    if (g.dyn) {
+        hipLaunchKernelGGL(k_cov_seg, dim3(g.npairs, 2, D / 16), dim3(256), 0, s, g, k, v, seq_stride, 1);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     const dim3 grid(max_full_segs, g.npairs);
     if (max_full_segs > 0) {
         if (ws) hipLaunchKernelGGL(k_prefill<2>, grid, dim3(256), 0, s, g, k, v, seq_stride, ws, slot_tok, slot_sc, 0);
@@ -977,6 +1026,9 @@ hipError_t launch_maintain(const Geom &g, int mode, int what, hipStream_t s) {
         hipLaunchKernelGGL(k_fin_pack, dim3(g.npairs, SEG / MT_TOK), dim3(MT_THREADS), 0, s, g);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (g.dyn) {
+            hipLaunchKernelGGL(k_cov_seg, dim3(g.npairs, 2, D / 16), dim3(256), 0, s, g, (const uint16_t *)nullptr,
+                               (const uint16_t *)nullptr, (int64_t)0, 0);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
             hipLaunchKernelGGL(k_win_update, dim3(ceil_div(g.npairs, 4)), dim3(256), 0, s, g);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }

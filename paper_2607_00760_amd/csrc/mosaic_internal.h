@@ -48,6 +48,7 @@ struct Geom {
     uint8_t *meta, *desc, *sc, *tok;
     uint16_t *buf, *stg;
     float *rot;
+    double *cov; uint64_t cov_stride;   // dynamic windows: [2][2][D][D] per pair
     uint64_t meta_stride, desc_stride, sc_stride, tok_stride, buf_stride, stg_stride, rot_stride;
     int keep_cand[3], group_cand[3], block_cand[3];
     int def_keep, def_group, def_block;
@@ -65,6 +66,10 @@ struct Geom {
     __host__ __device__ uint8_t *tok_of(int p) const { return tok + (uint64_t)p * tok_stride; }
     __host__ __device__ uint16_t *buf_of(int p) const { return (uint16_t *)((uint8_t *)buf + (uint64_t)p * buf_stride); }
     __host__ __device__ uint16_t *stg_of(int p) const { return (uint16_t *)((uint8_t *)stg + (uint64_t)p * stg_stride); }
+    // slot of window w's K (which 0) or V (1) covariance, pair p
+    __host__ __device__ double *cov_of(int p, int w, int which) const {
+        return (double *)((uint8_t *)cov + (uint64_t)p * cov_stride) + ((uint64_t)(w & 1) * 2 + which) * D * D;
+    }
     // first segment of each window of pair p (dynamic windows)
     __host__ __device__ int32_t *wtab_of(int p) const {
         return (int32_t *)(meta + (uint64_t)p * meta_stride + sizeof(PairMeta));

@@ -5,11 +5,13 @@ A C5-shaped batch (G = 7, bf16, ragged prefills, one of them longer than the
 maximum window and one with a remainder) appends 1500 drifting tokens per
 sequence through the C ABI.  Whenever the library refuses an append because a
 poll or a close is due, the test polls, checks that the windows the GPU
-closed are exactly the ones the oracle closed, computes each closed window's
-rotation from its raw tokens on the host (fp64 eigendecomposition) and hands
-the same rotation to both.  At checkpoints the whole state of every pair
-(arenas, descriptors, update buffer, staging, window table and the open
-window's loss bits) is byte-exact against the oracle, block scores and
+closed are exactly the ones the oracle closed and that each closed window's
+incrementally accumulated covariance is bit-exact against the oracle's,
+computes the window's rotation from that covariance on the host (fp64
+eigendecomposition, Sec. 5.5) and hands the same rotation to both.  At
+checkpoints the whole state of every pair (arenas, descriptors, update
+buffer, staging, window table and the open window's loss bits) is
+byte-exact against the oracle, block scores and
 selections are bit-exact, and decode outputs agree within 2e-3 max-abs and
 1e-3 rel-L2.  Every pair must see at least two windows closed by their loss
 (shorter than the maximum length).
@@ -109,8 +111,16 @@ def test_loss_closed_windows_match_oracle():
                     b, h = divmod(p, HKV)
                     kw[b, h, :n] = toks[(b, h, "k")][a:a + n]
                     vw[b, h, :n] = toks[(b, h, "v")][a:a + n]
-                    Rk[b, h] = gen.window_rotation(kw[b, h, :n].float())
-                    Rv[b, h] = gen.window_rotation(vw[b, h, :n].float())
+                    # the window's incrementally accumulated covariance: bit-exact,
+                    # and the rotation both sides get comes from the oracle's
+                    ck, cv = ops[p].cov(w)
+                    gk, gv = (x.cpu().numpy() for x in c.window_cov(p, w))
+                    assert np.array_equal(gk.view(np.uint64), ck.view(np.uint64)), f"step {t} pair {p}: K covariance"
+                    assert np.array_equal(gv.view(np.uint64), cv.view(np.uint64)), f"step {t} pair {p}: V covariance"
+                    X = kw[b, h, :n].double()
+                    assert np.allclose(ck, (X.T @ X).numpy(), rtol=1e-12, atol=1e-9)
+                    Rk[b, h] = gen.rotation_from_cov(ck)
+                    Rv[b, h] = gen.rotation_from_cov(cv)
                     ops[p].close(Rk[b, h].numpy(), Rv[b, h].numpy(), bits(kw[b, h, :n]), bits(vw[b, h, :n]))
                     closes[p].append((w, a, n))
                 c.window_close(Rk.cuda(), Rv.cuda(), kw.cuda(), vw.cuda())

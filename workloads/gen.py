@@ -209,7 +209,12 @@ def window_rotation(x32):
     eigenvectors of the uncentered X^T X in fp64 by descending eigenvalue, each
     signed so that its largest-magnitude component is positive."""
     X = x32.double().cpu()
-    evals, evecs = torch.linalg.eigh(X.T @ X)
+    return rotation_from_cov(X.T @ X)
+
+
+def rotation_from_cov(cov):
+    """The same rotation from a given uncentered covariance [D][D] (fp64)."""
+    evals, evecs = torch.linalg.eigh(torch.as_tensor(cov, dtype=torch.float64).cpu())
     rows = evecs.T.flip(0)                                  # descending eigenvalue
     amax = rows.abs().argmax(dim=1)
     sign = torch.sign(rows[torch.arange(D), amax])
