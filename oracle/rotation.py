@@ -58,29 +58,60 @@ def rotations(x: np.ndarray, L: int, W: int, nw: int):
 
 
 # ---- selection-pattern channel reorder (Sec. 5.5) --------------------------
-# Reading R-21 (the paper names the goal, not the procedure): channels are
-# ordered by how often each is selected, i.e. among the r largest |y| of a
-# token's rotated vector (lowest channel first on ties), over the window's
-# tokens, most often first, lower current row first on equal counts; rows of R
-# follow.  Channels selected alike become neighbours and the least selected
-# come last, where a truncation of the bitmap drops them.  y is the
-# compressor's fp32 chain (oracle.rotate); x holds the 16-bit inputs as fp32.
-def selection_counts(x, R, r):
-    """x [n][D] fp32 (exact 16-bit values), R [D][D] fp32 -> counts [D] int64."""
+# Reading R-21 (the paper names the goal -- channels with similar selection
+# patterns become neighbours -- not the procedure).  A token selects the r
+# largest |y| of its rotated vector (lowest channel first on ties; y is the
+# compressor's fp32 chain, oracle.rotate; x holds the 16-bit inputs as fp32).
+# Over the window's tokens, n_c counts the tokens selecting channel c and
+# C[i][j] the tokens selecting both i and j (C[c][c] = n_c).  Channels are
+# placed in groups of four, the largest element group: a group starts with
+# the unplaced channel of the largest n (lowest channel on ties), then takes
+# three times the unplaced channel selected most often together with the
+# group so far (largest sum of C over its members), then the larger n, then
+# the lower channel.  Groups follow in the order formed, members in the order
+# taken; rows of R follow.  Groups of 2 and 4 then hold channels selected
+# together, and the least selected channels come last, where a truncation of
+# the bitmap drops them.
+def selection_masks(x, R, r):
+    """x [n][D] fp32 (exact 16-bit values), R [D][D] fp32 -> bool [n][D]: each
+    token's selected channels."""
     from oracle import oracle as O
     x = np.asarray(x, dtype=np.float32).reshape(-1, D)
-    counts = np.zeros(D, dtype=np.int64)
+    m = np.zeros((x.shape[0], D), dtype=bool)
     if x.shape[0] == 0:
-        return counts
+        return m
     y = O.rotate(x, np.asarray(R, dtype=np.float32))
     order = np.argsort(-np.abs(y), axis=1, kind="stable")   # equal magnitudes keep ascending channels
-    np.add.at(counts, order[:, :r].ravel(), 1)
-    return counts
+    np.put_along_axis(m, order[:, :r], True, axis=1)
+    return m
 
 
-def reorder_order(counts):
-    """New row order: descending count, ascending row on ties."""
-    return np.argsort(-np.asarray(counts), kind="stable")
+def selection_counts(x, R, r):
+    """-> n [D] int64: tokens selecting each channel."""
+    return selection_masks(x, R, r).sum(axis=0).astype(np.int64)
+
+
+def coselection_counts(x, R, r):
+    """-> C [D][D] int64: tokens selecting both channels (a library matmul of the
+    0/1 selection matrix with itself)."""
+    m = selection_masks(x, R, r).astype(np.int64)
+    return m.T @ m
+
+
+def reorder_order(C):
+    """New row order from co-selection counts C [D][D] (groups of four, above)."""
+    C = np.asarray(C, dtype=np.int64)
+    n = np.diagonal(C)
+    placed = np.zeros(D, dtype=bool)
+    order = []
+    while len(order) < D:
+        gsum = np.zeros(D, dtype=np.int64)
+        for _ in range(4):
+            j = max((c for c in range(D) if not placed[c]), key=lambda c: (gsum[c], n[c], -c))
+            order.append(j)
+            placed[j] = True
+            gsum += C[j]
+    return np.array(order, dtype=np.int64)
 
 
 def reorder_rotations(x, L, W, R, r):
@@ -95,7 +126,7 @@ def reorder_rotations(x, L, W, R, r):
     for w in range(nw):
         a, b = w * W, min((w + 1) * W, L)
         if a < b:
-            last = reorder_order(selection_counts(x[a:b], R[w], r))
+            last = reorder_order(coselection_counts(x[a:b], R[w], r))
         orders[w] = last
         out[w] = R[w][last]
     return out, orders

@@ -87,48 +87,97 @@ def test_selection_counts_brute_force():
     assert np.array_equal(got, want) and got.sum() == n * r
 
 
-def test_reorder_planted_frequencies():
-    """Identity rotation, channel c planted large in a known number of tokens:
-    the order is by descending planted count, ascending channel on ties."""
-    rng = np.random.default_rng(6)
-    r = 16
-    freq = rng.integers(0, 40, D)
-    freq[:r] = 50                                             # r channels planted in every token
-    n = 50
+def test_coselection_counts_brute_force():
+    """Co-selection counts against a per-token loop over the selected pairs,
+    on the same exact signed-permutation rotation with ties; the diagonal is
+    the selection count."""
+    rng = np.random.default_rng(15)
+    n, r = 120, 24
+    x = np.round(rng.standard_normal((n, D)) * 4) / 4
+    R = np.zeros((D, D))
+    R[np.arange(D), rng.permutation(D)] = rng.choice([-1.0, 1.0], D)
+    want = np.zeros((D, D), dtype=np.int64)
+    for t in range(n):
+        y = R @ x[t]
+        sel = sorted(range(D), key=lambda j: (-abs(y[j]), j))[:r]
+        for i in sel:
+            for j in sel:
+                want[i, j] += 1
+    got = RO.coselection_counts(x, R, r)
+    assert np.array_equal(got, want)
+    assert np.array_equal(np.diagonal(got), RO.selection_counts(x, R, r))
+
+
+def _feature_tokens(n, rng, scales=None, signs=False):
+    """Token t activates features t, t+5, t+11, t+19 (mod 32); feature f is
+    channels f, f+32, f+64, f+96, all active together.  Every channel is
+    selected equally often (identity rotation, r = 16), so only co-selection
+    tells the features apart."""
     x = np.zeros((n, D))
+    s = np.ones(D) if scales is None else scales
     for t in range(n):
-        big = [c for c in range(D) if t < freq[c]][:r]          # the first r channels planted at t
-        x[t, big] = 1.0 + 0.001 * np.arange(len(big))[::-1]
-    counts = RO.selection_counts(x, np.eye(D), r)
-    want = np.zeros(D, dtype=np.int64)
-    for t in range(n):
-        big = [c for c in range(D) if t < freq[c]][:r]
-        if len(big) < r:                                      # the rest are zeros: lowest channels fill in
-            big += [c for c in range(D) if c not in big][: r - len(big)]
-        want[big] += 1
-    assert np.array_equal(counts, want)
-    order = RO.reorder_order(counts)
-    assert np.array_equal(order, np.array(sorted(range(D), key=lambda c: (-want[c], c))))
+        for f in (t % 32, (t + 5) % 32, (t + 11) % 32, (t + 19) % 32):
+            for c in (f, f + 32, f + 64, f + 96):
+                x[t, c] = s[c] * (rng.choice([-1.0, 1.0]) if signs else 1.0)
+    return x
 
 
-def test_reorder_invariants_and_degenerate_cases():
-    rng = np.random.default_rng(7)
-    x = rng.standard_normal((700, D)).astype(np.float32)
-    Q, _ = np.linalg.qr(rng.standard_normal((D, D)))
-    R = np.stack([Q, Q.T, Q]).astype(np.float32)
-    Rp, orders = RO.reorder_rotations(x, 700, 256, R, 32)
-    for w in range(3):
-        assert np.array_equal(np.sort(orders[w]), np.arange(D))   # a permutation
-        assert np.array_equal(Rp[w], R[w][orders[w]])             # of the rows
-        a, b = w * 256, min((w + 1) * 256, 700)
-        c = RO.selection_counts(x[a:b], R[w], 32)[orders[w]]
-        assert np.all(np.diff(c) <= 0)                            # counts descend along the new order
-    # keeping every channel: equal counts, identity order
-    Rall, oall = RO.reorder_rotations(x, 700, 256, R, D)
-    assert np.array_equal(oall, np.tile(np.arange(D), (3, 1))) and np.array_equal(Rall, R)
-    # windows past the last token take the last order; no tokens at all: identity
-    R4 = np.stack([Q, Q.T, Q, Q]).astype(np.float32)
-    R4p, o4 = RO.reorder_rotations(x, 300, 256, R4, 32)
-    assert np.array_equal(o4[2], o4[1]) and np.array_equal(o4[3], o4[1])
-    R0p, o0 = RO.reorder_rotations(x, 0, 256, R4, 32)
-    assert np.array_equal(R0p, R4)
+def test_reorder_groups_coselected_channels():
+    """Equal selection counts: an order by count alone keeps the identity (and
+    groups of four would mix four features); the co-selection groups are the
+    features, lowest channel first: 0, 32, 64, 96, 1, 33, ..."""
+    rng = np.random.default_rng(16)
+    x = _feature_tokens(256, rng)
+    C = RO.coselection_counts(x, np.eye(D), 16)
+    n = np.diagonal(C)
+    assert np.all(n == n[0])                                  # every channel selected equally often
+    order = RO.reorder_order(C)
+    assert np.array_equal(order, np.array([f + 32 * k for f in range(32) for k in range(4)]))
+
+
+def test_reorder_order_seeds_and_tie_rules():
+    """Hand-made counts: the first group starts at the most selected channel;
+    a partner is the channel most co-selected with the whole group so far,
+    then the more selected, then the lower; the last groups take what is left
+    in index order when nothing else is co-selected."""
+    C = np.zeros((D, D), dtype=np.int64)
+    n = np.zeros(D, dtype=np.int64)
+    n[10], n[20], n[30], n[40], n[50] = 9, 5, 5, 4, 3
+    C[np.arange(D), np.arange(D)] = n
+    def co(i, j, v):
+        C[i, j] = C[j, i] = v
+    co(10, 20, 3); co(10, 30, 3)                               # tie on C with 10: both n = 5 -> lower (20)
+    co(20, 50, 2); co(10, 50, 1)                               # with {10, 20}: 50 has 3, 30 has 3 -> larger n (30)
+    co(40, 50, 1)
+    order = RO.reorder_order(C)
+    assert order[:4].tolist() == [10, 20, 30, 50]
+    assert order[4:8].tolist() == [40, 0, 1, 2]                # 40 is the most selected left; then index order
+    assert np.array_equal(np.sort(order), np.arange(D))
+
+
+def test_coselection_reorder_moves_the_ratio():
+    """Features with random signs and scales, under a rotation (an exact
+    signed permutation) that scatters each feature's channels: no group of 4
+    or 2 holds a feature, and the strategy search keeps single channels,
+    (16, 1); after the co-selection reorder each feature is one aligned group
+    and (16, 4) holds it losslessly, with a quarter of the bitmap bytes.  The
+    memory ratio rises (an order by selection count alone keeps the scattered
+    order here: every channel is selected equally often)."""
+    from oracle import oracle as O
+    rng = np.random.default_rng(17)
+    L = 1024
+    x = _feature_tokens(L, rng, scales=rng.uniform(1.0, 2.0, D), signs=True)
+    xb = O.f32_to_f16_bits(x).reshape(L, D)
+    xf = O.f16_bits_to_f32(xb).reshape(L, D)
+    R = np.zeros((D, D), np.float32)
+    R[np.arange(D), rng.permutation(D)] = rng.choice([-1.0, 1.0], D)
+    Rco, orders = RO.reorder_rotations(xf, L, L, R[None], 16)
+    P = O.Params(rot_window=L, default=(16, 4, 8))
+    used = {}
+    for name, Rw in (("given", R[None]), ("coselection", Rco)):
+        pr = O.Pair(P, L, Rw, Rw)
+        pr.compress(xb, xb)
+        used[name] = pr.info().used_bytes
+        used[name + "_rg"] = sorted({(d["r"], 1 << d["log2g"]) for d in pr.descriptors()})
+    assert used["given_rg"] == [(16, 1)] and used["coselection_rg"] == [(16, 4)], used
+    assert used["coselection"] < 0.8 * used["given"], used
