@@ -577,7 +577,7 @@ mosaic_status mosaic_reorder_workspace_bytes(const mosaic_params *params, int32_
     if (!bytes) return fail(MOSAIC_ERR_INVALID, "NULL argument");
     const mosaic_status st = rotation_shape(params, num_seqs, max_tokens, nw);
     if (st != MOSAIC_OK) return st;
-    *bytes = reorder_ws_bytes(num_seqs, params->num_kv_heads, nw);
+    *bytes = reorder_ws_bytes(num_seqs, params->num_kv_heads, nw, std::min(params->rot_window, max_tokens));
     return ok();
 }
 
@@ -603,14 +603,15 @@ mosaic_status mosaic_reorder_rotations(const mosaic_params *params, int32_t num_
     }
     if (seq_stride < maxL || seq_stride < 1) return fail(MOSAIC_ERR_INVALID, "seq_stride %lld < longest context %d",
                                                          (long long)seq_stride, maxL);
-    const size_t need = reorder_ws_bytes(num_seqs, params->num_kv_heads, nw);
+    const int wtok = std::min(params->rot_window, max_tokens);          // tokens of a window at most
+    const size_t need = reorder_ws_bytes(num_seqs, params->num_kv_heads, nw, wtok);
     if (ws_bytes < need) return fail(MOSAIC_ERR_INVALID, "workspace %zu < %zu", ws_bytes, need);
     hipStream_t s = (hipStream_t)stream;
     hipError_t e = hipMemcpyAsync(ws, ctx_lens_host, sizeof(int32_t) * num_seqs, hipMemcpyHostToDevice, s);
     if (e != hipSuccess) return hip_fail(e, "copy of context lengths");
     e = launch_reorder((const uint16_t *)k, (const uint16_t *)v, seq_stride, num_seqs, params->num_kv_heads,
-                       params->dtype, (const int32_t *)ws, params->rot_window, nw, params->default_keep, rot_k, rot_v,
-                       (uint8_t *)ws, s);
+                       params->dtype, (const int32_t *)ws, params->rot_window, nw, wtok, params->default_keep, rot_k,
+                       rot_v, (uint8_t *)ws, s);
     if (e != hipSuccess) return hip_fail(e, "reorder launch");
     return ok();
 }

@@ -829,10 +829,14 @@ __global__ void k_close_done(Geom g) {
 
 // ------------------------------------------------------------------ channel reorder
 // Selection-pattern reorder of the rotation rows (Sec. 5.5 asks for channels
-// selected alike to become neighbours): the rows of a window's R run by
-// descending count of the window's tokens that keep the channel among their
-// default_keep largest magnitudes, lower row first on equal counts.
-constexpr int SEL_SLICE = 4096;    // tokens per counting workgroup
+// selected alike to become neighbours).  Per window, K and V apart: each
+// token selects its default_keep largest magnitudes (the compressor's
+// rotation and ranks); C[i][j] counts the tokens selecting channels i and j;
+// the rows are then placed in groups of four, each started by the most
+// selected channel left and filled by the channels selected most often
+// together with the group so far.
+constexpr int SEL_SLICE = 4096;    // tokens per masking workgroup
+constexpr int CS_CHUNK = 512;      // token masks staged per round of the counting
 
 // R^T of every window of every pair, K and V (matrix (2 pair + which) nw + w),
 // for the compressor's rotation loop
@@ -847,17 +851,13 @@ __global__ void k_sel_transpose(const float *rk, const float *rv, int npairs, in
     }
 }
 
-__global__ void k_sel_zero(uint32_t *counts, int n) {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) counts[i] = 0u;
-}
-
 // grid (slices, windows, 2 pairs): every token of the slice rotated with the
-// window's R (the compressor's chain) and ranked; each channel counts the
-// tokens whose r largest magnitudes hold it (integer adds: exact in any order)
-__global__ void __launch_bounds__(256) k_sel_count(const uint16_t *k, const uint16_t *v, int64_t seq_stride, int hkv,
-                                                   int dtype, const int32_t *ctx, int W, int nw, int r,
-                                                   const float *rt, uint32_t *counts) {
+// window's R (the compressor's chain) and ranked; its selected channels (the
+// r largest magnitudes, lower channel first on ties) as a 128-bit mask at
+// masks[(m nw + w) wtok + token in window]
+__global__ void __launch_bounds__(256) k_sel_mask(const uint16_t *k, const uint16_t *v, int64_t seq_stride, int hkv,
+                                                  int dtype, const int32_t *ctx, int W, int nw, int r,
+                                                  const float *rt, uint4 *masks, int wtok) {
     constexpr int TPW = 16, NWV = 4;
     __shared__ SegSmem<NWV> sm;
     const int sl = blockIdx.x, w = blockIdx.y, m = blockIdx.z, pair = m >> 1, which = m & 1;
@@ -867,8 +867,8 @@ __global__ void __launch_bounds__(256) k_sel_count(const uint16_t *k, const uint
     if (a >= e) return;
     const uint16_t *src = (which ? v : k) + ((uint64_t)pair * seq_stride + (uint64_t)a) * D;
     const float *rtw = rt + ((uint64_t)m * nw + w) * D * D;
+    uint4 *dst = masks + ((uint64_t)m * nw + w) * (uint64_t)wtok + (uint64_t)sl * SEL_SLICE;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    uint32_t clo = 0, chi = 0;
     for (int64_t t0 = 0; t0 < e - a; t0 += SEG) {
         const int ntok = (int)min((int64_t)SEG, e - a - t0);
         float y[TPW][2];
@@ -878,37 +878,97 @@ __global__ void __launch_bounds__(256) k_sel_count(const uint16_t *k, const uint
             if (wave * TPW + i < ntok) {                     // wave-uniform
                 int rlo, rhi;
                 group_ranks(y[i][0], y[i][1], 0, D, sm.keys[wave], rlo, rhi);
-                clo += rlo < r ? 1u : 0u;
-                chi += rhi < r ? 1u : 0u;
+                const uint64_t mlo = __ballot(rlo < r), mhi = __ballot(rhi < r);
+                if (lane == 0)
+                    dst[t0 + wave * TPW + i] = make_uint4((uint32_t)mlo, (uint32_t)(mlo >> 32), (uint32_t)mhi,
+                                                          (uint32_t)(mhi >> 32));
             }
         }
     }
-    uint32_t *cnt = counts + ((uint64_t)m * nw + w) * D;
-    atomicAdd(&cnt[lane], clo);
-    atomicAdd(&cnt[lane + 64], chi);
 }
 
-// grid (windows, 2 pairs), 1024 threads: rows of R by descending count
-// (lower row first on ties), in place; a window without tokens takes the
-// order of the last window with tokens, and a pair with no tokens keeps R
+// grid (2 pairs x windows, 8 blocks of 16 rows), 256 threads: co-selection
+// counts of one window's tokens, thread t owning C[16 b + t / 16][8 (t % 16)
+// .. + 7]; the masks are staged in LDS 512 tokens at a time.  Integer counts:
+// exact in any order.  A window without tokens gets zeros.
+__global__ void __launch_bounds__(256) k_cosel(const uint4 *masks, int hkv, const int32_t *ctx, int W, int nw,
+                                               int wtok, uint32_t *cos) {
+    __shared__ uint32_t ms[CS_CHUNK][4];
+    const int mw = blockIdx.x, m = mw / nw, w = mw % nw, tid = threadIdx.x;
+    const int L = ctx[(m >> 1) / hkv];
+    const int ntok = (int)max((int64_t)0, min((int64_t)W, (int64_t)L - (int64_t)w * W));
+    const int i = blockIdx.y * 16 + tid / 16, j0 = (tid % 16) * 8;
+    const int wi = i >> 5, si = i & 31, wj = j0 >> 5, sj = j0 & 31;
+    const uint4 *src = masks + (uint64_t)mw * (uint64_t)wtok;
+    uint32_t cnt[8];
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) cnt[jj] = 0u;
+    for (int t0 = 0; t0 < ntok; t0 += CS_CHUNK) {
+        const int n = min(CS_CHUNK, ntok - t0);
+        __syncthreads();
+        for (int e = tid; e < n; e += 256) {
+            const uint4 x = src[t0 + e];
+            ms[e][0] = x.x; ms[e][1] = x.y; ms[e][2] = x.z; ms[e][3] = x.w;
+        }
+        __syncthreads();
+        for (int t = 0; t < n; ++t) {
+            const uint32_t sel = ((ms[t][wi] >> si) & 1u) ? (ms[t][wj] >> sj) : 0u;
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj) cnt[jj] += (sel >> jj) & 1u;
+        }
+    }
+    uint32_t *dst = cos + ((uint64_t)mw * D + i) * D + j0;
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) dst[jj] = cnt[jj];
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint64_t y = __shfl_xor(x, o);
+        x = x > y ? x : y;
+    }
+    return x;
+}
+
+// grid (windows, 2 pairs), 1024 threads: the new row order from the window's
+// co-selection counts, then the rows of R moved in place; a window without
+// tokens takes the order of the last window with tokens, and a pair with no
+// tokens keeps R.  Each of the 128 placements takes the unplaced channel of
+// the largest key (summed co-selection with the group so far, own count,
+// lower channel): threads 0..127 hold one candidate each and two waves'
+// maxima meet in LDS.
 __global__ void __launch_bounds__(1024) k_sel_permute(float *rk, float *rv, int hkv, const int32_t *ctx, int W, int nw,
-                                                      const uint32_t *counts) {
-    __shared__ uint32_t cnt[D];
+                                                      const uint32_t *cos) {
+    __shared__ uint32_t Cs[D * D];
+    __shared__ uint64_t best[2];
     __shared__ int pos[D];
     const int w = blockIdx.x, m = blockIdx.y, pair = m >> 1, which = m & 1, tid = threadIdx.x;
     const int L = ctx[pair / hkv];
     const int nwt = min(nw, (L + W - 1) / W);                 // windows with tokens
     if (nwt == 0) return;
     const int ws = min(w, nwt - 1);
-    if (tid < D) cnt[tid] = counts[((uint64_t)m * nw + ws) * D + tid];
+    const uint32_t *cw = cos + ((uint64_t)m * nw + ws) * D * D;
+    for (int e = tid; e < D * D; e += 1024) Cs[e] = cw[e];
     __syncthreads();
-    if (tid < D) {
-        const uint32_t mine = cnt[tid];
-        int rank = 0;
-        for (int c = 0; c < D; ++c) rank += (cnt[c] > mine || (cnt[c] == mine && c < tid)) ? 1 : 0;
-        pos[tid] = rank;
+    const bool cand = tid < D;
+    const uint32_t nj = cand ? Cs[tid * D + tid] : 0u;
+    uint32_t gsum = 0u;
+    bool placed = false;
+    for (int k = 0; k < D; ++k) {
+        if ((k & 3) == 0) gsum = 0u;                           // a new group of four
+        uint64_t key = (cand && !placed) ? (((uint64_t)gsum << 32) | ((uint64_t)nj << 8) | (uint64_t)(D - tid)) : 0ull;
+        key = wave_max_u64(key);
+        if (tid < D && (tid & 63) == 0) best[tid >> 6] = key;
+        __syncthreads();
+        const uint64_t b = best[0] > best[1] ? best[0] : best[1];
+        const int pick = D - (int)(b & 0xffu);
+        if (cand) {
+            if (tid == pick) { placed = true; pos[tid] = k; }
+            gsum += Cs[pick * D + tid];
+        }
+        __syncthreads();
     }
-    __syncthreads();
     float *R = (which ? rv : rk) + ((uint64_t)pair * nw + w) * D * D;
     const int row = tid >> 3, part = (tid & 7) * 16;        // 128 rows x 8 parts of 16 values
     float4 t[4];
@@ -984,28 +1044,30 @@ hipError_t launch_compress(const Geom &g, const uint16_t *k, const uint16_t *v, 
     return hipSuccess;
 }
 
-size_t reorder_ws_bytes(int num_seqs, int hkv, int nw) {
-    const size_t m = (size_t)num_seqs * hkv * 2 * nw;
-    return ((size_t)num_seqs * sizeof(int32_t) + 255) / 256 * 256 + (m * D * sizeof(uint32_t) + 255) / 256 * 256
-           + m * D * D * sizeof(float);
+// reorder workspace: context lengths, then per matrix (2 pairs x windows) the
+// token masks (wtok per window), the co-selection counts and R^T
+size_t reorder_ws_bytes(int num_seqs, int hkv, int nw, int wtok) {
+    const size_t mats = (size_t)num_seqs * hkv * 2 * nw;
+    return ((size_t)num_seqs * sizeof(int32_t) + 255) / 256 * 256 + (mats * wtok * 16 + 255) / 256 * 256 +
+           mats * D * D * sizeof(uint32_t) + mats * D * D * sizeof(float);
 }
 
 hipError_t launch_reorder(const uint16_t *k, const uint16_t *v, int64_t seq_stride, int num_seqs, int hkv, int dtype,
-                          const int32_t *ctx_dev, int W, int nw, int r, float *rot_k, float *rot_v, uint8_t *ws,
-                          hipStream_t s) {
+                          const int32_t *ctx_dev, int W, int nw, int wtok, int r, float *rot_k, float *rot_v,
+                          uint8_t *ws, hipStream_t s) {
     const int npairs = num_seqs * hkv, m = npairs * 2;
-    uint32_t *counts = (uint32_t *)(ws + ((size_t)num_seqs * sizeof(int32_t) + 255) / 256 * 256);
-    float *rt = (float *)((uint8_t *)counts + ((size_t)m * nw * D * sizeof(uint32_t) + 255) / 256 * 256);
-    const int ncnt = m * nw * D;
-    hipLaunchKernelGGL(k_sel_zero, dim3(ceil_div(ncnt, 256)), dim3(256), 0, s, counts, ncnt);
+    uint4 *masks = (uint4 *)(ws + ((size_t)num_seqs * sizeof(int32_t) + 255) / 256 * 256);
+    uint32_t *cos = (uint32_t *)((uint8_t *)masks + ((size_t)m * nw * wtok * 16 + 255) / 256 * 256);
+    float *rt = (float *)((uint8_t *)cos + (size_t)m * nw * D * D * sizeof(uint32_t));
+    hipLaunchKernelGGL(k_sel_transpose, dim3(m, nw), dim3(256), 0, s, rot_k, rot_v, npairs, nw, rt);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_sel_transpose, dim3(m, nw), dim3(256), 0, s, rot_k, rot_v, npairs, nw, rt);
+    hipLaunchKernelGGL(k_sel_mask, dim3(ceil_div(W < wtok ? W : wtok, SEL_SLICE), nw, m), dim3(256), 0, s, k, v,
+                       seq_stride, hkv, dtype, ctx_dev, W, nw, r, rt, masks, wtok);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_sel_count, dim3(ceil_div(W, SEL_SLICE), nw, m), dim3(256), 0, s, k, v, seq_stride, hkv, dtype,
-                       ctx_dev, W, nw, r, rt, counts);
+    hipLaunchKernelGGL(k_cosel, dim3(m * nw, D / 16), dim3(256), 0, s, masks, hkv, ctx_dev, W, nw, wtok, cos);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_sel_permute, dim3(nw, m), dim3(1024), 0, s, rot_k, rot_v, hkv, ctx_dev, W, nw, counts);
+    hipLaunchKernelGGL(k_sel_permute, dim3(nw, m), dim3(1024), 0, s, rot_k, rot_v, hkv, ctx_dev, W, nw, cos);
     return hipGetLastError();
 }
 

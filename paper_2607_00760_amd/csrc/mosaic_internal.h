@@ -259,10 +259,11 @@ hipError_t launch_dense(const uint16_t *q, const uint16_t *k, const uint16_t *v,
 size_t dense_part_bytes(int npairs, int G, int max_ctx);
 size_t rotation_ctx_bytes(int num_seqs);
 size_t rotation_ws_bytes(int num_seqs, int hkv, int nw, int W);
-size_t reorder_ws_bytes(int num_seqs, int hkv, int nw);
+// wtok = min(W, max_tokens): tokens of a window at most
+size_t reorder_ws_bytes(int num_seqs, int hkv, int nw, int wtok);
 hipError_t launch_reorder(const uint16_t *k, const uint16_t *v, int64_t seq_stride, int num_seqs, int hkv, int dtype,
-                          const int32_t *ctx_dev, int W, int nw, int r, float *rot_k, float *rot_v, uint8_t *ws,
-                          hipStream_t s);
+                          const int32_t *ctx_dev, int W, int nw, int wtok, int r, float *rot_k, float *rot_v,
+                          uint8_t *ws, hipStream_t s);
 hipError_t launch_rotations(const uint16_t *k, const uint16_t *v, int64_t seq_stride, int num_seqs, int hkv,
                             int dtype, const int32_t *ctx_dev, int W, int nw, float *rot_k, float *rot_v, float *ev_k,
                             float *ev_v, float *part, hipStream_t s);

@@ -73,7 +73,7 @@ hipError_t launch_dense(const uint16_t *, const uint16_t *, const uint16_t *, fl
     return hipSuccess;
 }
 hipError_t launch_reorder(const uint16_t *, const uint16_t *, int64_t, int, int, int, const int32_t *, int, int, int,
-                          float *, float *, uint8_t *, hipStream_t) {
+                          int, float *, float *, uint8_t *, hipStream_t) {
     rec("reorder");
     return hipSuccess;
 }
@@ -84,7 +84,7 @@ hipError_t launch_rotations(const uint16_t *, const uint16_t *, int64_t, int, in
 }
 // workspace sizes of the rotation, reorder and dense paths (not exercised here)
 size_t dense_part_bytes(int, int, int) { return 256; }
-size_t reorder_ws_bytes(int, int, int) { return 256; }
+size_t reorder_ws_bytes(int, int, int, int) { return 256; }
 size_t rotation_ws_bytes(int, int, int, int) { return 256; }
 size_t rotation_ctx_bytes(int) { return 256; }
 }  // namespace mosaic

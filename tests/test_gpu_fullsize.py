@@ -382,5 +382,5 @@ def test_c3_reorder_full_size_sampled():
             a, e = w * spec.rot_window, min((w + 1) * spec.rot_window, spec.ctx[b])
             R0 = lay["rot_" + which][b, h, w].cpu().numpy()
             x = lay[which][b, h, a:e].float().cpu().numpy()
-            order = RO.reorder_order(RO.selection_counts(x, R0, lp.default[0]))
+            order = RO.reorder_order(RO.coselection_counts(x, R0, lp.default[0]))
             assert np.array_equal(R[b, h, w].cpu().numpy(), R0[order]), f"{which} seq {b} head {h} window {w}"
