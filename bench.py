@@ -405,7 +405,7 @@ def main():
     # and Jacobi eigensolver; the caches above use the host's rotations)
     rotations_ms = None
     reorder = None
-    if spec.rotate and not args.no_rotations and nlayers == 1 and not appends:
+    if spec.rotate and not args.no_rotations and nlayers == 1:
         rk_g, rv_g = M.compute_rotations(params, lay["k"], lay["v"], lay["ctx_lens"], cap)
         n = C.c_size_t()
         M.load().mosaic_rotation_workspace_bytes(C.byref(params.to_c()), spec.num_seqs, cap, C.byref(n))

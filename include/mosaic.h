@@ -348,19 +348,23 @@ mosaic_status mosaic_compute_rotations(const mosaic_params *params, int32_t num_
                                        float *evals_v, void *ws, size_t ws_bytes, void *stream);
 
 /* Selection-pattern channel reorder (Sec. 5.5 asks for the rotated channels to be
- * reordered so that channels selected alike become neighbours, without fixing a
- * procedure; this is the one taken here).  For every rotation window of
- * every (sequence, kv head), K and V apart, counts how many of the window's tokens
- * keep each rotated channel among their default_keep largest magnitudes (y = x . R^T
- * by the compressor's own fp32 chain, lowest channel first on ties), then permutes
- * the rows of that window's R in place: most selected first, lower row first on
- * equal counts.  A window without tokens takes the order of the last window with
- * tokens; the windows of a sequence without tokens are left alone.  Eigenvalues
- * returned by mosaic_compute_rotations keep the old row order.
+ * reordered so that channels with similar selection patterns become neighbours,
+ * without fixing a procedure; this is the one taken here).  For every rotation
+ * window of every (sequence, kv head), K and V apart: each of the window's tokens
+ * selects its default_keep largest magnitudes (y = x . R^T by the compressor's own
+ * fp32 chain, lowest channel first on ties); n[c] counts the tokens selecting c and
+ * C[i][j] those selecting both i and j.  The rows of the window's R are then
+ * permuted in place, in groups of four: a group starts with the unplaced channel of
+ * the largest n (lowest on ties) and three times takes the unplaced channel with the
+ * largest sum of C over the group so far, then the larger n, then the lower channel.
+ * A window without tokens takes the order of the last window with tokens; the
+ * windows of a sequence without tokens are left alone.  Eigenvalues returned by
+ * mosaic_compute_rotations keep the old row order.
  *   k, v, seq_stride, ctx_lens_host, rot_k, rot_v: as mosaic_compute_rotations
  *                   (rot_k / rot_v are read and rewritten in place)
  *   ws            : at least mosaic_reorder_workspace_bytes bytes, 256-byte aligned
- *                   (context lengths, counts, transposed copies of R)
+ *                   (context lengths, every token's 16-byte selection mask, the
+ *                   co-selection counts, transposed copies of R)
  * Errors: INVALID (NULL, misaligned, bad shape, small workspace, default_keep out
  * of 1..128), CAPACITY (a context longer than max_tokens), UNSUPPORTED
  * (head_dim != 128). */

@@ -234,6 +234,34 @@ def _rotations(x32, L, W, nw, device):
     return R
 
 
+def feature_tokens(seed, n, device="cpu"):
+    """[n][D] fp32 tokens made of channel groups that are always active
+    together: token t activates features t, t+5, t+11, t+19 (mod 32),
+    feature f being channels f, f+32, f+64, f+96, each with an independent
+    random sign and a fixed per-channel scale in [1, 2]; the other channels
+    are 0.  Every channel is active in 1/8 of the tokens, so selection counts
+    alone do not tell the features apart; co-selection does."""
+    g = _gen("cpu", seed, "features")
+    scales = 1.0 + torch.rand(D, generator=g, dtype=torch.float64)
+    x = torch.zeros((n, D), dtype=torch.float64)
+    t = torch.arange(n)
+    for off in (0, 5, 11, 19):
+        f = (t + off) % 32
+        for k in range(4):
+            c = f + 32 * k
+            sign = torch.randint(0, 2, (n,), generator=g).double() * 2 - 1
+            x[t, c] = sign * scales[c]
+    return x.float().to(device)
+
+
+def signed_permutation(seed):
+    """[D][D] fp32 rotation that is a random signed permutation (exact)."""
+    g = _gen("cpu", seed, "signed-permutation")
+    R = torch.zeros((D, D))
+    R[torch.arange(D), torch.randperm(D, generator=g)] = torch.randint(0, 2, (D,), generator=g).float() * 2 - 1
+    return R
+
+
 def drift_tokens(seed, n, which, drift=0.05, device="cpu"):
     """[n][D] fp32 anisotropic tokens whose principal directions turn slowly
     (decode streams for windows closed by their loss): direction j has scale
