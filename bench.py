@@ -248,6 +248,19 @@ def encoding_overlap(cache, lay, dev, compress_ms):
             "hidden_fraction": round((serial - overlapped) / compress_ms, 3)}
 
 
+def arena_one_capacity(M, params, spec, cap):
+    """Arena bytes of the same cache with the longest capacity for every
+    sequence (host bookkeeping only, nothing allocated)."""
+    L = M.load()
+    h = C.c_void_p()
+    p = params.to_c()
+    M._lib.check(L.mosaic_cache_create(C.byref(p), spec.num_seqs, cap, int(spec.rotate), C.byref(h)))
+    n = C.c_size_t()
+    L.mosaic_cache_arena_bytes(h, C.byref(n))
+    L.mosaic_cache_destroy(h)
+    return int(n.value)
+
+
 def cpu_info():
     """(CPU model, cores this process may run on)."""
     model = None
@@ -354,6 +367,10 @@ def main():
     appends = spec.appends > 0                               # c2, c5: a step appends a token, then decodes
     nlayers = spec.layers if args.layers is None else args.layers
     cap = spec.max_ctx + (args.warmup + args.steps if appends else 0)
+    # ragged contexts: a capacity per sequence, so each pair's regions are
+    # sized for its own sequence (the rotations still cover the longest)
+    n_app = args.warmup + args.steps if appends else 0
+    caps = [L + n_app for L in spec.ctx] if len(set(spec.ctx)) > 1 else cap
     params = M.Params(num_kv_heads=spec.hkv, group_size=spec.group, dtype=spec.dtype, rot_window=spec.rot_window,
                       tau_channel=spec.tau_channel, tau_block=spec.tau_block, select=spec.select, **extra)
     flush = torch.empty(args.flush_mb << 20, dtype=torch.uint8, device=dev)
@@ -375,7 +392,7 @@ def main():
     for layer in range(nlayers):
         lay = gen.make_layer(spec, layer, device=dev, capacity=cap)
         q = lay["queries"] if lay["queries"] is not None else gen.make_queries(spec, 0, layer, device=dev)
-        cache = M.MosaicCache(params, spec.num_seqs, cap, rotated=spec.rotate, device=dev)
+        cache = M.MosaicCache(params, spec.num_seqs, caps, rotated=spec.rotate, device=dev)
         cache.compress(lay["k"], lay["v"], lay["ctx_lens"], lay["rot_k"], lay["rot_v"])
         if layer == 0:
             # the compression pass, timed once after one untimed pass
@@ -744,6 +761,7 @@ def main():
         "speedup_vs_dense_roofline": round(dense_roofline_us / value, 2),
         "wall_ms_per_step_incl_flush": round(1e3 * wall / args.steps, 3),
         "compress_ms": round(compress_ms, 3), "memory_ratio": round(ratio, 4),
+        "arena_bytes": int(caches[0].arena.numel()), "arena_bytes_one_capacity": arena_one_capacity(M, params, spec, cap),
         "rotations_ms": None if rotations_ms is None else round(rotations_ms, 3),
         "channel_reorder": reorder,
         "update_path": update_path, "dyn_windows": dyn_windows, "encoding_overlap": overlap,

@@ -114,6 +114,16 @@ typedef struct mosaic_cache mosaic_cache;  /* host bookkeeping + bound arena */
 mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
                                   int32_t rotated, mosaic_cache **out);
 
+/* The same with a capacity per sequence (max_tokens_host[num_seqs], each >= 1):
+ * the descriptor, score and token regions of each (sequence, kv head) pair are
+ * sized for its own sequence, so ragged batches do not reserve the longest
+ * sequence's worst case for every pair.  Rotation windows, workspaces and the
+ * other regions are sized for the longest.  Compress and append check each
+ * sequence against its own capacity.  The pair regions' offsets are then not a
+ * multiple of a stride (mosaic_cache_pair_regions). */
+mosaic_status mosaic_cache_create_ragged(const mosaic_params *params, int32_t num_seqs,
+                                         const int32_t *max_tokens_host, int32_t rotated, mosaic_cache **out);
+
 /* Bytes of device memory the cache needs (worst case over strategies).  The
  * caller allocates it, 256-byte aligned, and binds it once. */
 mosaic_status mosaic_cache_arena_bytes(const mosaic_cache *cache, size_t *bytes);
@@ -158,8 +168,17 @@ typedef struct {
     uint64_t total;
     int32_t num_pairs, max_desc, num_windows, reserved;
     uint64_t cov_off, cov_stride;   /* dyn_windows only (else 0) */
+    uint64_t pairs_off;             /* uint64 [num_pairs][4] device copy of the pair table below */
 } mosaic_layout;
 mosaic_status mosaic_cache_layout(const mosaic_cache *cache, mosaic_layout *out);
+
+/* Per pair p: out_host[4 p + 0..2] = byte offsets of its desc, score and token
+ * regions from desc_off, score_off and token_off, [4 p + 3] = its token region's
+ * bytes.  For caches of one capacity these are p * stride and token_stride; for
+ * ragged capacities (mosaic_cache_create_ragged) desc_stride, score_stride and
+ * token_stride are 0 and only this table locates the regions.  out_host holds
+ * 4 * num_pairs entries. */
+mosaic_status mosaic_cache_pair_regions(const mosaic_cache *cache, uint64_t *out_host);
 
 enum { MOSAIC_OP_COMPRESS = 0, MOSAIC_OP_APPEND = 1, MOSAIC_OP_DECODE = 2 };
 /* Workspace bytes an operation can use (0 if none).  Depends only on the

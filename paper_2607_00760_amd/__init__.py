@@ -85,18 +85,28 @@ def _check_tensor(t, name, dtype, device):
 class MosaicCache:
     """One layer's compressed KV cache for `num_seqs` sequences."""
 
-    def __init__(self, params: Params, num_seqs: int, max_tokens: int, rotated: bool = True, device="cuda"):
+    def __init__(self, params: Params, num_seqs: int, max_tokens, rotated: bool = True, device="cuda"):
+        """max_tokens: one capacity for every sequence, or a list of per-sequence
+        capacities (each pair's regions then sized for its own sequence)."""
         import torch
         self.lib = load()
         self.params = params
-        self.num_seqs, self.max_tokens, self.rotated = num_seqs, max_tokens, bool(rotated)
+        ragged = not isinstance(max_tokens, int)
+        caps = [int(x) for x in max_tokens] if ragged else None
+        if ragged and len(caps) != num_seqs:
+            raise ValueError(f"{len(caps)} capacities for {num_seqs} sequences")
+        self.num_seqs, self.max_tokens, self.rotated = num_seqs, (max(caps) if ragged else max_tokens), bool(rotated)
         self.device = torch.device(device)
         if self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
         self.elem = torch.bfloat16 if params.dtype == "bf16" else torch.float16
         self._p = params.to_c()
         h = C.c_void_p()
-        check(self.lib.mosaic_cache_create(C.byref(self._p), num_seqs, max_tokens, int(self.rotated), C.byref(h)))
+        if ragged:
+            check(self.lib.mosaic_cache_create_ragged(C.byref(self._p), num_seqs, (C.c_int32 * num_seqs)(*caps),
+                                                      int(self.rotated), C.byref(h)))
+        else:
+            check(self.lib.mosaic_cache_create(C.byref(self._p), num_seqs, max_tokens, int(self.rotated), C.byref(h)))
         self._h = h
         n = C.c_size_t()
         check(self.lib.mosaic_cache_arena_bytes(self._h, C.byref(n)))
@@ -108,6 +118,9 @@ class MosaicCache:
         check(self.lib.mosaic_cache_layout(self._h, C.byref(self.layout)))
         self.ws_layout = MosaicWsLayout()
         check(self.lib.mosaic_decode_ws_layout(self._h, C.byref(self.ws_layout)))
+        tab = (C.c_uint64 * (4 * self.num_pairs))()
+        check(self.lib.mosaic_cache_pair_regions(self._h, tab))
+        self.pair_regions = [tuple(tab[4 * p: 4 * p + 4]) for p in range(self.num_pairs)]
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -251,6 +264,12 @@ class MosaicCache:
     def region(self, name: str, pair: int, nbytes: int | None = None):
         off = getattr(self.layout, name + "_off")
         stride = getattr(self.layout, name + "_stride")
+        if name in ("desc", "score", "token"):            # located by the pair table
+            pos = off + self.pair_regions[pair][("desc", "score", "token").index(name)]
+            n = self.pair_regions[pair][3] if nbytes is None and name == "token" else nbytes
+            if n is None:
+                raise ValueError(f"give the bytes of the {name} region")
+            return self.arena[pos: pos + n]
         n = stride if nbytes is None else nbytes
         return self.arena[off + pair * stride: off + pair * stride + n]
 

@@ -18,7 +18,7 @@ EXPORTED = [
     "mosaic_dense_decode_attention", "mosaic_cache_stats", "mosaic_seq_tokens", "mosaic_last_error",
     "mosaic_set_timing", "mosaic_decode_timing", "mosaic_rotation_workspace_bytes", "mosaic_compute_rotations",
     "mosaic_reorder_workspace_bytes", "mosaic_reorder_rotations", "mosaic_decode_attention_noalloc",
-    "mosaic_window_poll", "mosaic_window_close",
+    "mosaic_window_poll", "mosaic_window_close", "mosaic_cache_create_ragged", "mosaic_cache_pair_regions",
 ]
 
 
@@ -40,7 +40,7 @@ class MosaicLayout(C.Structure):
         "meta_off", "meta_stride", "desc_off", "desc_stride", "score_off", "score_stride", "token_off",
         "token_stride", "buf_off", "buf_stride", "stage_off", "stage_stride", "rot_off", "rot_stride", "total")] + [
         ("num_pairs", C.c_int32), ("max_desc", C.c_int32), ("num_windows", C.c_int32), ("reserved", C.c_int32),
-        ("cov_off", C.c_uint64), ("cov_stride", C.c_uint64)]
+        ("cov_off", C.c_uint64), ("cov_stride", C.c_uint64), ("pairs_off", C.c_uint64)]
 
 
 class MosaicWsLayout(C.Structure):
@@ -82,6 +82,9 @@ def bind_signatures(L: C.CDLL) -> C.CDLL:
     L.mosaic_params_default.argtypes = [C.POINTER(MosaicParams)]
     L.mosaic_params_default.restype = None
     L.mosaic_cache_create.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.c_int32, C.c_int32, C.POINTER(vp)]
+    L.mosaic_cache_create_ragged.argtypes = [C.POINTER(MosaicParams), C.c_int32, C.POINTER(C.c_int32), C.c_int32,
+                                             C.POINTER(vp)]
+    L.mosaic_cache_pair_regions.argtypes = [vp, C.POINTER(C.c_uint64)]
     L.mosaic_cache_arena_bytes.argtypes = [vp, C.POINTER(sz)]
     L.mosaic_cache_bind.argtypes = [vp, vp, sz]
     L.mosaic_cache_destroy.argtypes = [vp]

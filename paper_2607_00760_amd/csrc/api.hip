@@ -63,6 +63,12 @@ struct mosaic_cache {
     bool dyn = false, poll_due = false;
     int nw_src = 1;
     std::vector<int32_t> nwin, pend, pend_len;
+    // capacities: per sequence; with ragged capacities the desc, score and
+    // token regions of a pair are sized for its sequence and located by the
+    // pair table [npairs][4] (offsets from each region's start, token bytes)
+    std::vector<int32_t> cap;
+    bool ragged = false;
+    std::vector<uint64_t> pairs;
     Geom geom() const {
         Geom g{};
         g.npairs = npairs; g.hkv = P.num_kv_heads; g.G = P.group_size; g.GP = GP; g.dtype = P.dtype;
@@ -74,6 +80,7 @@ struct mosaic_cache {
         g.tok_stride = lay.token_stride; g.buf_stride = lay.buf_stride; g.stg_stride = lay.stage_stride;
         g.rot_stride = lay.rot_stride;
         g.cov = (double *)(arena + lay.cov_off); g.cov_stride = lay.cov_stride;
+        g.ragged = ragged ? 1 : 0; g.poff = (const uint64_t *)(arena + lay.pairs_off);
         for (int i = 0; i < 3; ++i) {
             g.keep_cand[i] = P.keep_cand[i]; g.group_cand[i] = P.group_cand[i]; g.block_cand[i] = P.block_cand[i];
         }
@@ -204,16 +211,21 @@ static mosaic_status check_params(const mosaic_params *p) {
     return MOSAIC_OK;
 }
 
-mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
+static mosaic_status cache_create(const mosaic_params *params, int32_t num_seqs, const int32_t *caps, bool ragged,
                                   int32_t rotated, mosaic_cache **out) {
-    if (!params || !out) return fail(MOSAIC_ERR_INVALID, "NULL argument");
     mosaic_status st = check_params(params);
     if (st != MOSAIC_OK) return st;
-    if (num_seqs < 1 || max_tokens < 1) return fail(MOSAIC_ERR_INVALID, "num_seqs %d, max_tokens %d", num_seqs, max_tokens);
+    int max_tokens = 0;
+    for (int q = 0; q < num_seqs; ++q) {
+        if (caps[q] < 1) return fail(MOSAIC_ERR_INVALID, "max_tokens[%d] = %d < 1", q, caps[q]);
+        max_tokens = std::max(max_tokens, caps[q]);
+    }
     mosaic_cache *c = new (std::nothrow) mosaic_cache();
     if (!c) return fail(MOSAIC_ERR_INVALID, "out of host memory");
     c->P = *params;
     c->num_seqs = num_seqs; c->max_tokens = max_tokens; c->rotated = rotated ? 1 : 0;
+    c->cap.assign(caps, caps + num_seqs);
+    c->ragged = ragged;
     c->npairs = num_seqs * params->num_kv_heads;
     c->GP = params->group_size <= 4 ? 4 : 8;
     c->nw = (max_tokens + params->rot_window - 1) / params->rot_window;
@@ -272,13 +284,39 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     };
     // meta: the counters, then (dynamic windows) the window table
     region(l.meta_off, l.meta_stride, sizeof(PairMeta) + (c->dyn ? (uint64_t)(c->nw + 1) * 4 : 0));
-    region(l.desc_off, l.desc_stride, (uint64_t)c->max_desc * sizeof(Desc));
-    region(l.score_off, l.score_stride, sc_bytes);
-    region(l.token_off, l.token_stride, tok_bytes);
+    c->pairs.assign((size_t)c->npairs * 4, 0);
+    if (!ragged) {
+        region(l.desc_off, l.desc_stride, (uint64_t)c->max_desc * sizeof(Desc));
+        region(l.score_off, l.score_stride, sc_bytes);
+        region(l.token_off, l.token_stride, tok_bytes);
+        for (int p = 0; p < c->npairs; ++p) {
+            c->pairs[4 * p] = p * l.desc_stride; c->pairs[4 * p + 1] = p * l.score_stride;
+            c->pairs[4 * p + 2] = p * l.token_stride; c->pairs[4 * p + 3] = l.token_stride;
+        }
+    } else {
+        // each pair's regions sized for its own sequence, pair after pair
+        uint64_t *dst_off[3] = {&l.desc_off, &l.score_off, &l.token_off};
+        for (int r = 0; r < 3; ++r) {
+            *dst_off[r] = off;
+            uint64_t o = 0;
+            for (int p = 0; p < c->npairs; ++p) {
+                const uint64_t nd = (uint64_t)c->cap[p / params->num_kv_heads] / SEG + 2;
+                const uint64_t bytes = r == 0 ? nd * sizeof(Desc)
+                                     : r == 1 ? nd * (SEG / minb) * maxrec + 256 : nd * SEG * 2 * maxtok + 256;
+                c->pairs[4 * p + r] = o;
+                if (r == 2) c->pairs[4 * p + 3] = align256(bytes);
+                o += align256(bytes);
+            }
+            off = align256(off + o);
+        }
+        l.desc_stride = l.score_stride = l.token_stride = 0;
+    }
     region(l.buf_off, l.buf_stride, 2ull * UBUF * D * 2);
     region(l.stage_off, l.stage_stride, 2ull * SEG * D * 2);
     region(l.rot_off, l.rot_stride, c->rotated ? (uint64_t)c->nw * 3 * D * D * 4 : 0);
     if (c->dyn) region(l.cov_off, l.cov_stride, 4ull * D * D * 8);
+    l.pairs_off = off;
+    off = align256(off + (uint64_t)c->npairs * 4 * sizeof(uint64_t));
     c->ctx_off = off;
     off = align256(off + (uint64_t)num_seqs * 4);
     l.total = off;
@@ -315,6 +353,27 @@ mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs,
     c->pend.assign(c->npairs, -1);
     c->pend_len.assign(c->npairs, 0);
     *out = c;
+    return ok();
+}
+
+mosaic_status mosaic_cache_create(const mosaic_params *params, int32_t num_seqs, int32_t max_tokens,
+                                  int32_t rotated, mosaic_cache **out) {
+    if (!params || !out) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    if (num_seqs < 1 || max_tokens < 1) return fail(MOSAIC_ERR_INVALID, "num_seqs %d, max_tokens %d", num_seqs, max_tokens);
+    const std::vector<int32_t> caps((size_t)num_seqs, max_tokens);
+    return cache_create(params, num_seqs, caps.data(), false, rotated, out);
+}
+
+mosaic_status mosaic_cache_create_ragged(const mosaic_params *params, int32_t num_seqs,
+                                         const int32_t *max_tokens_host, int32_t rotated, mosaic_cache **out) {
+    if (!params || !out || !max_tokens_host) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    if (num_seqs < 1) return fail(MOSAIC_ERR_INVALID, "num_seqs %d", num_seqs);
+    return cache_create(params, num_seqs, max_tokens_host, true, rotated, out);
+}
+
+mosaic_status mosaic_cache_pair_regions(const mosaic_cache *c, uint64_t *out_host) {
+    if (!c || !out_host) return fail(MOSAIC_ERR_INVALID, "NULL argument");
+    std::memcpy(out_host, c->pairs.data(), c->pairs.size() * sizeof(uint64_t));
     return ok();
 }
 
@@ -381,7 +440,7 @@ mosaic_status mosaic_compress(mosaic_cache *c, const void *k, const void *v, int
     for (int s = 0; s < c->num_seqs; ++s) {
         const int L = ctx_lens_host[s];
         if (L < 0) return fail(MOSAIC_ERR_INVALID, "ctx_lens[%d] = %d < 0", s, L);
-        if (L > c->max_tokens) return fail(MOSAIC_ERR_CAPACITY, "ctx_lens[%d] = %d > max_tokens %d", s, L, c->max_tokens);
+        if (L > c->cap[s]) return fail(MOSAIC_ERR_CAPACITY, "ctx_lens[%d] = %d > max_tokens %d", s, L, c->cap[s]);
         maxL = std::max(maxL, L);
         any_tail |= (L % SEG) != 0;
     }
@@ -397,6 +456,9 @@ mosaic_status mosaic_compress(mosaic_cache *c, const void *k, const void *v, int
     int32_t *ctx_dev = (int32_t *)(c->arena + c->ctx_off);
     hipError_t e = launch_ctx_copy(ctx_dev, ctx_lens_host, c->num_seqs, s);
     if (e != hipSuccess) return hip_fail(e, "copy of context lengths");
+    if (c->ragged && (e = launch_pairs_copy((uint64_t *)(c->arena + c->lay.pairs_off), c->pairs.data(), c->npairs, s))
+                         != hipSuccess)
+        return hip_fail(e, "copy of the pair table");
     if (c->rotated && (e = launch_copy_rot(g, rot_k, rot_v, c->nw_src, s)) != hipSuccess) return hip_fail(e, "rotation copy");
     e = launch_compress(g, (const uint16_t *)k, (const uint16_t *)v, seq_stride, ctx_dev, maxL / SEG, any_tail,
                         (uint8_t *)ws, c->slot_tok, c->slot_sc, s);
@@ -419,7 +481,7 @@ mosaic_status mosaic_append(mosaic_cache *c, const void *k_new, const void *v_ne
     if (((uintptr_t)k_new | (uintptr_t)v_new) % 4) return fail(MOSAIC_ERR_INVALID, "k_new/v_new must be 4-byte aligned");
     int due = 0;                            // MAINT_FLUSH / MAINT_FINALIZE of some sequence
     for (int q = 0; q < c->num_seqs; ++q) {
-        if (c->L[q] + 1 > c->max_tokens) return fail(MOSAIC_ERR_CAPACITY, "sequence %d is full (%d tokens)", q, c->L[q]);
+        if (c->L[q] + 1 > c->cap[q]) return fail(MOSAIC_ERR_CAPACITY, "sequence %d is full (%d tokens)", q, c->L[q]);
         if ((c->L[q] + 1) % UBUF == 0) {
             due |= ((c->L[q] + 1) % SEG == 0) ? MAINT_FINALIZE : MAINT_FLUSH;
             if (c->dyn && c->poll_due)
@@ -634,8 +696,8 @@ mosaic_status mosaic_cache_stats(const mosaic_cache *c, mosaic_stats *out, void 
         const int L = meta[p].L, nf = L / SEG, rem = L % SEG, prov = rem >= UBUF, nbuf = rem - (prov ? UBUF : 0);
         const int nd = nf + prov;
         if (nd > 0) {
-            e = hipMemcpy(desc.data(), c->arena + c->lay.desc_off + (uint64_t)p * c->lay.desc_stride,
-                          sizeof(Desc) * nd, hipMemcpyDeviceToHost);
+            e = hipMemcpy(desc.data(), c->arena + c->lay.desc_off + c->pairs[4 * p], sizeof(Desc) * nd,
+                          hipMemcpyDeviceToHost);
             if (e != hipSuccess) return hip_fail(e, "descriptor copy");
         }
         int64_t used = (int64_t)meta[p].tok_tail + meta[p].sc_tail + 16ll * nd + (int64_t)nbuf * 2 * D * 2;

@@ -986,6 +986,10 @@ hipError_t launch_ctx_copy(int32_t *dst_dev, const int32_t *src_host, int n, hip
     return hipMemcpyAsync(dst_dev, src_host, sizeof(int32_t) * (size_t)n, hipMemcpyHostToDevice, s);
 }
 
+hipError_t launch_pairs_copy(uint64_t *dst_dev, const uint64_t *src_host, int npairs, hipStream_t s) {
+    return hipMemcpyAsync(dst_dev, src_host, sizeof(uint64_t) * 4 * (size_t)npairs, hipMemcpyHostToDevice, s);
+}
+
 hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, int nw_src, hipStream_t s) {
     hipLaunchKernelGGL(k_copy_rot, dim3(g.nw, g.npairs), dim3(256), 0, s, g, rk, rv, nw_src);
     return hipGetLastError();

@@ -1518,7 +1518,7 @@ k_attn(Geom g, WsGeom ws, float scale, const uint16_t *qraw) {
         if (on) {                                   // the entry's record offset and strategy (top-k wrote them)
             const uint2 si = ws.selinfo[(uint64_t)p * (ws.selinfo_stride / 8) + e0 + tid * estride];
             r = (int)((si.y >> 8) & 0xffu); l2g = (int)((si.y >> 16) & 3u); l2b = (int)min(max((si.y >> 20) & 7u, 2u), 4u);
-            goff = min(si.x, (uint32_t)g.tok_stride);      // keeps every read inside the arena
+            goff = min(si.x, (uint32_t)g.tok_size(p));     // keeps every read inside the arena
         }
         const int cls = on ? 4 - l2b : 3;
         const uint64_t m0 = __ballot(cls == 0), m1 = __ballot(cls == 1), m2 = __ballot(cls == 2);

@@ -49,6 +49,8 @@ struct Geom {
     uint16_t *buf, *stg;
     float *rot;
     double *cov; uint64_t cov_stride;   // dynamic windows: [2][2][D][D] per pair
+    int ragged;                         // per-sequence capacities: pair regions from poff
+    const uint64_t *poff;               // [npairs][4]: desc, score, token offsets; token bytes
     uint64_t meta_stride, desc_stride, sc_stride, tok_stride, buf_stride, stg_stride, rot_stride;
     int keep_cand[3], group_cand[3], block_cand[3];
     int def_keep, def_group, def_block;
@@ -61,9 +63,12 @@ struct Geom {
     float tau_win;                    // accumulated loss that closes a window
 
     __host__ __device__ PairMeta *meta_of(int p) const { return (PairMeta *)(meta + (uint64_t)p * meta_stride); }
-    __host__ __device__ Desc *desc_of(int p) const { return (Desc *)(desc + (uint64_t)p * desc_stride); }
-    __host__ __device__ uint8_t *sc_of(int p) const { return sc + (uint64_t)p * sc_stride; }
-    __host__ __device__ uint8_t *tok_of(int p) const { return tok + (uint64_t)p * tok_stride; }
+    __host__ __device__ Desc *desc_of(int p) const {
+        return (Desc *)(desc + (ragged ? poff[4 * p] : (uint64_t)p * desc_stride));
+    }
+    __host__ __device__ uint8_t *sc_of(int p) const { return sc + (ragged ? poff[4 * p + 1] : (uint64_t)p * sc_stride); }
+    __host__ __device__ uint8_t *tok_of(int p) const { return tok + (ragged ? poff[4 * p + 2] : (uint64_t)p * tok_stride); }
+    __host__ __device__ uint64_t tok_size(int p) const { return ragged ? poff[4 * p + 3] : tok_stride; }
     __host__ __device__ uint16_t *buf_of(int p) const { return (uint16_t *)((uint8_t *)buf + (uint64_t)p * buf_stride); }
     __host__ __device__ uint16_t *stg_of(int p) const { return (uint16_t *)((uint8_t *)stg + (uint64_t)p * stg_stride); }
     // slot of window w's K (which 0) or V (1) covariance, pair p
@@ -233,6 +238,8 @@ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 // ---------------------------------------------------------------- launchers
 // (implemented in the .hip files; all return hipError_t of the launch)
 hipError_t launch_ctx_copy(int32_t *dst_dev, const int32_t *src_host, int n, hipStream_t s);
+// the pair table of a cache with per-sequence capacities into its arena
+hipError_t launch_pairs_copy(uint64_t *dst_dev, const uint64_t *src_host, int npairs, hipStream_t s);
 // nw_src: windows of rk / rv per pair; slots past them repeat the last one
 hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, int nw_src, hipStream_t s);
 // close of the windows awaiting their rotation (dynamic windows): the new

@@ -34,6 +34,12 @@ hipError_t launch_ctx_copy(int32_t *, const int32_t *src_host, int n, hipStream_
     rec("%s", s.c_str());
     return hipSuccess;
 }
+hipError_t launch_pairs_copy(uint64_t *, const uint64_t *src_host, int npairs, hipStream_t) {
+    std::string s = "pairs_copy";
+    for (int i = 0; i < 4 * npairs; ++i) s += " " + std::to_string((unsigned long long)src_host[i]);
+    rec("%s", s.c_str());
+    return hipSuccess;
+}
 hipError_t launch_copy_rot(const Geom &g, const float *, const float *, int nw_src, hipStream_t) {
     rec("copy_rot npairs=%d nw=%d src=%d", g.npairs, g.nw, nw_src);
     return hipSuccess;

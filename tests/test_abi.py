@@ -176,3 +176,47 @@ def test_rotation_and_reorder_argument_checks():
     p.default_keep = 0
     assert L.mosaic_reorder_rotations(*args()) == -1
     assert "default_keep" in L.mosaic_last_error().decode()
+
+
+def test_ragged_capacities_layout():
+    """Per-sequence capacities: each pair's desc, score and token regions are
+    sized for its own sequence, 256-byte aligned, in pair order, disjoint and
+    inside the arena, located only by the pair table (strides 0); the arena is
+    smaller than with the longest capacity everywhere; uniform caches report
+    p * stride in the same table."""
+    L = _lib.load()
+    p = M.Params(num_kv_heads=2, group_size=4).to_c()
+    caps = (C.c_int32 * 3)(100, 5000, 70000)
+    h = C.c_void_p()
+    assert L.mosaic_cache_create_ragged(C.byref(p), 3, caps, 1, C.byref(h)) == 0
+    lay = _lib.MosaicLayout()
+    assert L.mosaic_cache_layout(h, C.byref(lay)) == 0
+    assert lay.desc_stride == lay.score_stride == lay.token_stride == 0 and lay.num_windows == 2
+    tab = (C.c_uint64 * 24)()
+    assert L.mosaic_cache_pair_regions(h, tab) == 0
+    rows = [tuple(tab[4 * q: 4 * q + 4]) for q in range(6)]
+    starts = (lay.desc_off, lay.score_off, lay.token_off)
+    for r, nxt in ((0, lay.score_off), (1, lay.token_off), (2, lay.buf_off)):
+        offs = [starts[r] + row[r] for row in rows]
+        assert all(o % 256 == 0 for o in offs) and offs == sorted(offs) and offs[0] == starts[r]
+        assert offs[-1] < nxt
+    tok = [rows[q][3] for q in range(6)]
+    assert tok[0] == tok[1] < tok[2] == tok[3] < tok[4] == tok[5]
+    assert tok[4] >= (70000 // 64 + 1) * 64 * 2 * (2 * 48 + 16) and tok[0] < (100 // 64 + 3) * 64 * 2 * (2 * 48 + 16) + 512
+    for q in range(5):
+        assert rows[q][2] + tok[q] <= rows[q + 1][2]
+    n_r, n_u = C.c_size_t(), C.c_size_t()
+    assert L.mosaic_cache_arena_bytes(h, C.byref(n_r)) == 0
+    st, hu = _create(num_seqs=3, max_tokens=70000, num_kv_heads=2, group_size=4)
+    assert st == 0 and L.mosaic_cache_arena_bytes(hu, C.byref(n_u)) == 0
+    assert n_r.value < 0.4 * n_u.value
+    lu = _lib.MosaicLayout()
+    assert L.mosaic_cache_layout(hu, C.byref(lu)) == 0 and L.mosaic_cache_pair_regions(hu, tab) == 0
+    assert [tuple(tab[4 * q: 4 * q + 4]) for q in range(6)] == \
+        [(q * lu.desc_stride, q * lu.score_stride, q * lu.token_stride, lu.token_stride) for q in range(6)]
+    L.mosaic_cache_destroy(h)
+    L.mosaic_cache_destroy(hu)
+    for bad in ((100, 0, 5), (100, -3, 5)):
+        assert L.mosaic_cache_create_ragged(C.byref(p), 3, (C.c_int32 * 3)(*bad), 1, C.byref(h)) == -1
+    assert L.mosaic_cache_create_ragged(C.byref(p), 3, None, 1, C.byref(h)) == -1
+    assert L.mosaic_cache_create_ragged(C.byref(p), 0, caps, 1, C.byref(h)) == -1

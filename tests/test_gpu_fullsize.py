@@ -102,7 +102,9 @@ def test_append_decode_full_size_sampled(name, per_seq, check_every):
     cap = spec.capacity
     lay = gen.make_layer(spec, 0, device="cuda", capacity=cap)
     lp, op = params_pair(spec)
-    c = gpu_cache(lp, spec, lay, cap)
+    # c5: a capacity per sequence (its context plus the appends), so each
+    # pair's regions are sized for its own sequence
+    c = gpu_cache(lp, spec, lay, [L + spec.appends for L in spec.ctx] if name == "c5" else cap)
     pairs = _spread(spec, per_seq, 7)               # c2: all 32 pairs; c5: one per sequence (16 of 64)
     ops = _oracle_pairs(op, spec, lay, cap, pairs)
     for pi, pr in ops.items():
@@ -270,8 +272,8 @@ def test_c4_every_layer_sampled_segments(first):
             d = descs[pi][sg]
             assert np.array_equal(d[12:15], od[12:15]), f"c4 layer {layer} pair {pi} segment {sg}: strategy"
             tok_off, sc_off = (int(x) for x in d[:8].view(np.uint32))
-            got_t = c.arena[c.layout.token_off + pi * c.layout.token_stride + tok_off:][:ot.size].cpu().numpy()
-            got_s = c.arena[c.layout.score_off + pi * c.layout.score_stride + sc_off:][:osc.size].cpu().numpy()
+            got_t = c.arena[c.layout.token_off + c.pair_regions[pi][2] + tok_off:][:ot.size].cpu().numpy()
+            got_s = c.arena[c.layout.score_off + c.pair_regions[pi][1] + sc_off:][:osc.size].cpu().numpy()
             assert np.array_equal(got_t, ot), f"c4 layer {layer} pair {pi} segment {sg}: token records"
             assert np.array_equal(got_s, osc), f"c4 layer {layer} pair {pi} segment {sg}: block keys"
         # the selection of one kv head is the token budget of the GPU's scores

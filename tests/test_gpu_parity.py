@@ -227,3 +227,46 @@ def test_decode_is_deterministic():
     c2 = gpu_cache(lp, spec, lay, cap)
     d = c2.decode(q, scale_of())
     assert torch.equal(a, b) and torch.equal(a, d)
+
+
+def test_ragged_capacities_parity():
+    """A capacity per sequence (context + 100): each pair's regions sized for
+    its own sequence and located through the pair table.  Prefill, 100
+    appends across flushes and finalizes, and decode are byte-exact /
+    within tolerance against the oracle, and the arena is smaller than with
+    the longest capacity everywhere."""
+    spec = gen.spec("c5", ctx=(1000, 64, 3000, 257), hkv=2, appends=100, rot_window=1024)
+    caps = [L + spec.appends for L in spec.ctx]
+    lay = gen.make_layer(spec, 0, capacity=max(caps))
+    lp, op = params_pair(spec)
+    print(f"[ragged] caps={caps}", flush=True)
+    c = gpu_cache(lp, spec, lay, caps)
+    uni = M.MosaicCache(lp, spec.num_seqs, max(caps), rotated=True)
+    tok_ragged = sum(r[3] for r in c.pair_regions)
+    assert tok_ragged < 0.5 * len(c.pair_regions) * uni.layout.token_stride      # 4721 of 4 x 3100 tokens
+    assert c.arena.numel() < uni.arena.numel()
+    del uni
+    ops = oracle_pairs(op, spec, lay, max(caps))
+    for p, pr in enumerate(ops):
+        assert_state_equal(c, p, pr, where="ragged prefill")
+    sc = scale_of()
+    for t in range(spec.appends):
+        kn, vn = gen.make_appends(spec, t)
+        c.append(kn.cuda(), vn.cuda())
+        kb, vb = bits(kn), bits(vn)
+        for p, pr in enumerate(ops):
+            b, h = divmod(p, spec.hkv)
+            pr.append(kb[b, h], vb[b, h])
+    with pytest.raises(M.MosaicError):                          # every sequence is full now
+        c.append(kn.cuda(), vn.cuda())
+    torch.cuda.synchronize()
+    for p, pr in enumerate(ops):
+        assert_state_equal(c, p, pr, where="ragged after appends")
+    q = gen.make_queries(spec, 7)
+    out = c.decode(q.cuda(), sc)
+    want, sels, _ = oracle_decode_all(ops, spec, q, sc)
+    for p in range(len(ops)):
+        _, gsel, _ = gpu_scores_sel(c, p, ops[p].info().nblk)
+        assert np.array_equal(gsel, sels[p]), f"pair {p}: selected blocks"
+    err = assert_close(out.cpu().numpy(), want, "ragged capacities")
+    print(f"[ragged] max-abs {err[0]:.2e} rel-L2 {err[1]:.2e}", flush=True)

@@ -204,6 +204,22 @@ def run_checks(path):
     assert sim.log() == [] and sim.tokens(h4, 2) == [83, 31]
     assert "poll" in L.mosaic_last_error().decode()
     assert L.mosaic_cache_destroy(h4) == OK
+    # ---- per-sequence capacities: each sequence checked against its own
+    pr = sim.params(num_kv_heads=1)
+    h6 = C.c_void_p()
+    assert L.mosaic_cache_create_ragged(C.byref(pr), 2, (C.c_int32 * 2)(40, 300), 0, C.byref(h6)) == OK
+    n6 = C.c_size_t()
+    assert L.mosaic_cache_arena_bytes(h6, C.byref(n6)) == OK
+    assert L.mosaic_cache_bind(h6, sim.buf(n6.value), n6.value) == OK
+    assert L.mosaic_compress(h6, kv, kv, 100, (C.c_int32 * 2)(41, 100), None, None, None, 0, None) == CAPACITY
+    assert sim.log() == []
+    assert L.mosaic_compress(h6, kv, kv, 100, (C.c_int32 * 2)(38, 100), None, None, None, 0, None) == OK
+    log = sim.log()
+    assert log[0] == "ctx_copy 38 100" and log[1].startswith("pairs_copy 0 ")
+    assert L.mosaic_append(h6, kv, kv, None) == OK and L.mosaic_append(h6, kv, kv, None) == OK
+    assert L.mosaic_append(h6, kv, kv, None) == CAPACITY                                     # sequence 0 holds 40
+    assert sim.tokens(h6, 2) == [40, 102]
+    assert L.mosaic_cache_destroy(h6) == OK
     return True
 
 
