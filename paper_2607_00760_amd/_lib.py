@@ -48,7 +48,8 @@ class MosaicWsLayout(C.Structure):
         "qrot_off", "qrot_stride", "score_off", "score_stride", "sel_off", "sel_stride", "wsel_off", "wsel_stride",
         "part_off", "part_stride", "tag_off", "tag_stride", "binfo_off", "binfo_stride", "bsize_off", "bsize_stride", "selinfo_off",
         "selinfo_stride", "wres_off", "wres_stride", "total")] + [
-        ("max_blocks", C.c_int32), ("max_splits", C.c_int32), ("gp", C.c_int32), ("reserved", C.c_int32)]
+        ("max_blocks", C.c_int32), ("max_splits", C.c_int32), ("gp", C.c_int32), ("reserved", C.c_int32),
+        ("tkx_off", C.c_uint64), ("tkx_stride", C.c_uint64)]
 
 
 class MosaicStats(C.Structure):

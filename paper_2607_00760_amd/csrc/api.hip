@@ -105,6 +105,7 @@ struct mosaic_cache {
         w.bsize = b + wsl.bsize_off; w.bsize_stride = wsl.bsize_stride;
         w.selinfo = (uint2 *)(b + wsl.selinfo_off); w.selinfo_stride = wsl.selinfo_stride;
         w.wres = (float *)(b + wsl.wres_off); w.wres_stride = wsl.wres_stride;
+        w.tkx = wsl.tkx_stride ? (uint32_t *)(b + wsl.tkx_off) : nullptr; w.tkx_stride = wsl.tkx_stride;
         w.max_blocks = max_blocks; w.max_splits = max_splits; w.max_sel = max_sel;
         return w;
     }
@@ -344,6 +345,12 @@ static mosaic_status cache_create(const mosaic_params *params, int32_t num_seqs,
     wregion(w.selinfo_off, w.selinfo_stride, (uint64_t)c->max_blocks * 8);
     // wres: each window's merged, back-rotated result per column block
     wregion(w.wres_off, w.wres_stride, (uint64_t)CMB_NCC * (c->nw + 1) * c->GP * CMB_RES * 4);
+    // pairs of more than 16 K blocks: the multi-workgroup top-k's histograms,
+    // radix states and per-chunk counts (chunks of 4096 blocks)
+    if (c->max_blocks > 16384) {
+        const uint64_t nch = ((uint64_t)c->max_blocks + 4095) / 4096;
+        wregion(w.tkx_off, w.tkx_stride, (3ull * 2048 + 16 + 2 * nch) * 4);
+    }
     w.total = off + 256;                     // whole 16-byte loads of the last pair's arrays stay inside
     w.max_blocks = c->max_blocks; w.max_splits = c->max_splits; w.gp = c->GP;
     c->arena = nullptr;

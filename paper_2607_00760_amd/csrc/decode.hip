@@ -130,6 +130,10 @@ __global__ void __launch_bounds__(256) k_qrot(Geom g, WsGeom ws, const uint16_t 
     constexpr int NCG = D / QROT_COLS;
     const int w = blockIdx.x / NCG, j0 = (blockIdx.x % NCG) * QROT_COLS;
     const int p = blockIdx.y, tid = threadIdx.x, G = g.G;
+    if (ws.tkx && blockIdx.x == 0) {        // the multi-workgroup top-k's histograms of this call
+        uint32_t *h = ws.tkx + (uint64_t)p * (ws.tkx_stride / 4);
+        for (int i = tid; i < 3 * 2048; i += 256) h[i] = 0u;
+    }
     if (g.rotated) {
         const float *src = g.rot_of(p, w);
         constexpr int PER = D * QROT_COLS / 4 / 256;       // 16-byte pieces per thread
@@ -1103,6 +1107,15 @@ __device__ __forceinline__ void topk_big(const Geom &g, const WsGeom &ws, int p,
     window_tail(g, nb, k, wsel);
 }
 
+// the token budget of pair p: ceil(rho * scoreable tokens), at least one
+// token (0 without scoreable blocks)
+__device__ __forceinline__ int pair_budget(const Geom &g, int nb, int nf, int prov) {
+    const int ntok = nf * SEG + prov * UBUF;
+    if (nb <= 0 || ntok <= 0) return 0;
+    const long long bb = ((long long)ntok * g.sel_num + g.sel_den - 1) / g.sel_den;
+    return (int)(bb < 1 ? 1 : (bb > ntok ? ntok : bb));
+}
+
 __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
     extern __shared__ __align__(16) uint32_t segw[];            // [TB_SMEM / 4] on the long-context path
     __shared__ uint32_t hist[2 * TOPK_BINS];
@@ -1113,15 +1126,210 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
     const int nb = pair_nblocks(g, p, meta);
     int nf, prov, nbuf;
     const int ndesc = pair_ndesc(meta, nf, prov, nbuf);
-    // the token budget: ceil(rho * scoreable tokens), at least one token
-    const int ntok = nf * SEG + prov * UBUF;
-    int budget = 0;
-    if (nb > 0 && ntok > 0) {
-        const long long bb = ((long long)ntok * g.sel_num + g.sel_den - 1) / g.sel_den;
-        budget = (int)(bb < 1 ? 1 : (bb > ntok ? ntok : bb));
-    }
+    const int budget = pair_budget(g, nb, nf, prov);
     if (nb <= 1024 * TOPK_KPT) topk_reg(g, ws, p, nb, ndesc, budget, hist, sbuf, fbw);
     else topk_big(g, ws, p, nb, ndesc, budget, segw, hist, sbuf, fbw);
+}
+
+// ------------------------------------------------------------------ top-k over many workgroups
+// Caches whose pairs can hold more than 16 K blocks: the same token-budget
+// selection, spread over workgroups of TKM_CHUNK consecutive blocks of a pair
+// and one kernel per phase, so that a long pair's keys are read by dozens of
+// CUs instead of one.  Three radix passes of 11, 11 and 10 bits over the
+// key: kernel k first takes the pick of pass k - 1 from the pair's histogram
+// of that pass (every workgroup the same, workgroup 0 records the state),
+// then adds its chunk's candidates' tokens to the pair's histogram of pass k
+// (per-chunk LDS bins, then integer atomics: exact in any order).  After the
+// last pick (threshold T, tokens still needed at T) one kernel sums the
+// tokens equal to T per chunk, the next counts each chunk's taken blocks
+// (blocks above T, and blocks equal to T while the equal tokens before them,
+// over the chunks before and the block order inside, are below the need), and
+// the last writes the list in block order and the windows' starts.  Chunk
+// prefixes are sums over the chunks before (a few dozen).
+// Per-pair state (WsGeom::tkx): hist[3][2048] | TkmHdr[4] | eq[nch] | tk[nch];
+// the three histograms are zeroed by k_qrot earlier in the same call.
+constexpr int TKM_CHUNK = 4096;                            // blocks per workgroup: 1024 threads x 4
+
+struct TkmHdr { uint32_t base, span, rem, done; };          // radix state after each pick
+
+__device__ __forceinline__ uint32_t *tkm_of(const WsGeom &ws, int p) { return ws.tkx + (uint64_t)p * (ws.tkx_stride / 4); }
+
+// this workgroup's view of pair p: blocks, budget, its chunk's keys (four
+// consecutive per thread) and the radix state after `npicks` picks
+struct TkmCtx {
+    int nb, ndesc, budget, i0, n_own;
+    Key4 x;
+    uint32_t *st;
+    __device__ __forceinline__ bool in(int e) const { return e < n_own; }
+};
+
+__device__ __forceinline__ bool tkm_setup(const Geom &g, const WsGeom &ws, int p, int c, TkmCtx &t) {
+    const PairMeta meta = *g.meta_of(p);
+    int nf, prov, nbuf;
+    t.ndesc = pair_ndesc(meta, nf, prov, nbuf);
+    t.nb = pair_nblocks(g, p, meta);
+    t.budget = pair_budget(g, t.nb, nf, prov);
+    t.st = tkm_of(ws, p);
+    t.i0 = c * TKM_CHUNK + 4 * (int)threadIdx.x;
+    t.n_own = max(0, min(4, t.nb - t.i0));
+    const float *sc = ws.score + (uint64_t)p * (ws.score_stride / 4);
+    const uint8_t *bz = ws.bsize + (uint64_t)p * ws.bsize_stride;
+    if (t.n_own > 0) t.x = load_key4(sc, bz, t.i0);
+    else { t.x.k[0] = t.x.k[1] = t.x.k[2] = t.x.k[3] = 0u; t.x.z = 0u; }
+    return c * TKM_CHUNK < t.nb;                             // the chunk holds blocks of the pair
+}
+
+// the state after pick `pass - 1` (pass >= 1) from the state before it and the
+// histogram of that pass; the initial state for pass 0.  hl, hd: 2048 words
+// of LDS each.
+__device__ __forceinline__ TkmHdr tkm_state(const TkmCtx &t, int pass, uint32_t *hl, uint32_t *hd, uint32_t *sbuf) {
+    TkmHdr h;
+    if (pass == 0) {
+        h.base = 0u; h.span = 0xffffffffu; h.rem = (uint32_t)max(t.budget, 0); h.done = t.budget <= 0;
+        return h;
+    }
+    h = ((const TkmHdr *)(t.st + 3 * TOPK_BINS))[pass - 1];
+    if (h.done) return h;
+    for (int i = threadIdx.x; i < TOPK_BINS; i += 1024) hl[i] = t.st[(pass - 1) * TOPK_BINS + i];
+    lds_barrier();
+    const int bits = 32 - (h.span ? __builtin_clz(h.span) : 32);
+    const int sh = bits > 11 ? bits - 11 : 0;
+    h.done = radix_pick(hl, hd, sbuf, sh, h.base, h.span, h.rem) ? 1u : 0u;
+    return h;
+}
+
+// grid (chunks, pairs): pass 0, 1 or 2 of the radix selection
+__global__ void __launch_bounds__(1024) k_tkm_pass(Geom g, WsGeom ws, int pass) {
+    __shared__ uint32_t hl[TOPK_BINS], hd[TOPK_BINS], sbuf[64];
+    const int p = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
+    TkmCtx t;
+    const bool mine = tkm_setup(g, ws, p, c, t);
+    const TkmHdr h = tkm_state(t, pass, hl, hd, sbuf);
+    if (c == 0 && tid == 0) ((TkmHdr *)(t.st + 3 * TOPK_BINS))[pass] = h;
+    if (h.done || !mine) return;
+    const int bits = 32 - (h.span ? __builtin_clz(h.span) : 32);
+    const int sh = bits > 11 ? bits - 11 : 0;
+    lds_barrier();                                          // hl (the previous pick's bins) is reused
+    for (int i = tid; i < TOPK_BINS; i += 1024) hl[i] = 0u;
+    lds_barrier();
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const uint32_t key = t.x.k[e], d = key - h.base;
+        if (t.in(e) && key >= h.base && d <= h.span) atomicAdd(&hl[d >> sh], t.x.tok(e));
+    }
+    lds_barrier();
+    uint32_t *hg = t.st + pass * TOPK_BINS;
+    for (int i = tid; i < TOPK_BINS; i += 1024)
+        if (hl[i]) atomicAdd(&hg[i], hl[i]);
+}
+
+// tokens equal to T among the chunk's blocks, in block order: v (this
+// thread's four blocks), then the exclusive prefix over the workgroup
+__device__ __forceinline__ uint32_t tkm_eq4(const TkmCtx &t, uint32_t T) {
+    uint32_t v = 0u;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v += (t.in(e) && t.x.k[e] == T) ? t.x.tok(e) : 0u;
+    return v;
+}
+
+// grid (chunks, pairs): the last pick (T = base, need = rem), then the tokens
+// equal to T per chunk
+__global__ void __launch_bounds__(1024) k_tkm_eq(Geom g, WsGeom ws, int nch) {
+    __shared__ uint32_t hl[TOPK_BINS], hd[TOPK_BINS], sbuf[64];
+    const int p = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
+    TkmCtx t;
+    const bool mine = tkm_setup(g, ws, p, c, t);
+    const TkmHdr h = tkm_state(t, 3, hl, hd, sbuf);
+    if (c == 0 && tid == 0) ((TkmHdr *)(t.st + 3 * TOPK_BINS))[3] = h;
+    if (!mine) return;
+    uint32_t v[1] = {t.budget > 0 ? tkm_eq4(t, h.base) : 0u}, tot[1];
+    block_excl_scan_1024<1>(v, tot, sbuf);
+    if (tid == 0) t.st[3 * TOPK_BINS + 16 + c] = tot[0];
+}
+
+// the taken mask (bit e: block i0 + e) of this thread's blocks
+__device__ __forceinline__ uint32_t tkm_taken(const TkmCtx &t, const TkmHdr &h, int c, uint32_t *sbuf) {
+    const uint32_t *eq = t.st + 3 * TOPK_BINS + 16;
+    uint32_t before = 0u;                                   // equal tokens of the chunks before
+    for (int i = 0; i < c; ++i) before += eq[i];
+    const uint32_t T = h.base, need = h.rem;
+    uint32_t v[1] = {t.budget > 0 ? tkm_eq4(t, T) : 0u}, tot[1];
+    block_excl_scan_1024<1>(v, tot, sbuf);
+    uint32_t acc = before + v[0], m = 0u;
+    if (t.budget > 0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t key = t.x.k[e];
+            const bool eqk = t.in(e) && key == T;
+            const bool tk = t.in(e) && (key > T || (eqk && acc < need));
+            acc += eqk ? t.x.tok(e) : 0u;
+            m |= tk ? (1u << e) : 0u;
+        }
+    }
+    return m;
+}
+
+// grid (chunks, pairs): each chunk's taken blocks
+__global__ void __launch_bounds__(1024) k_tkm_taken(Geom g, WsGeom ws, int nch) {
+    __shared__ uint32_t sbuf[64];
+    const int p = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
+    TkmCtx t;
+    if (!tkm_setup(g, ws, p, c, t)) return;
+    const TkmHdr h = ((const TkmHdr *)(t.st + 3 * TOPK_BINS))[3];
+    const uint32_t m = tkm_taken(t, h, c, sbuf);
+    uint32_t v[1] = {(uint32_t)__popc(m)}, tot[1];
+    block_excl_scan_1024<1>(v, tot, sbuf);
+    if (tid == 0) t.st[3 * TOPK_BINS + 16 + nch + c] = tot[0];
+}
+
+// grid (chunks, pairs): the list entries of each chunk in block order, their
+// record info, and the list position where each window starts
+__global__ void __launch_bounds__(1024) k_tkm_write(Geom g, WsGeom ws, int nch) {
+    __shared__ uint32_t sbuf[64], tpos[1024], tmk[1024];
+    __shared__ int fbw[TOPK_MAXW];
+    const int p = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
+    TkmCtx t;
+    const bool mine = tkm_setup(g, ws, p, c, t);
+    const int nvalid = (t.nb + TKM_CHUNK - 1) / TKM_CHUNK;  // chunks holding blocks
+    const uint32_t *tk = t.st + 3 * TOPK_BINS + 16 + nch;
+    uint32_t before = 0u, k = 0u;
+    for (int i = 0; i < nvalid; ++i) { k += tk[i]; before += i < c ? tk[i] : 0u; }
+    if (t.budget <= 0) k = 0u;
+    int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
+    const int nwl = min(g.nw, TOPK_MAXW);
+    if (c == 0) window_tail(g, t.nb, (int)k, wsel);
+    if (!mine && c != 0) return;
+    window_firsts(g, p, t.nb, t.ndesc, nwl, fbw);
+    const TkmHdr h = ((const TkmHdr *)(t.st + 3 * TOPK_BINS))[3];
+    const uint32_t m = mine ? tkm_taken(t, h, c, sbuf) : 0u;
+    uint32_t v[1] = {(uint32_t)__popc(m)}, tot[1];
+    block_excl_scan_1024<1>(v, tot, sbuf);                  // (its barriers also publish fbw)
+    const uint32_t pos0 = before + v[0];
+    int32_t *sel = ws.sel + (uint64_t)p * (ws.sel_stride / 4);
+    uint2 *sinfo = ws.selinfo + (uint64_t)p * (ws.selinfo_stride / 8);
+    const uint2 *bi = ws.binfo + (uint64_t)p * (ws.binfo_stride / 8);
+    uint2 br[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) br[e] = ((m >> e) & 1u) ? bi[t.i0 + e] : make_uint2(0u, 0u);
+    uint32_t pos = pos0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        if ((m >> e) & 1u) { sel[pos] = t.i0 + e; sinfo[pos] = br[e]; }
+        pos += (m >> e) & 1u;
+    }
+    tpos[tid] = pos0;
+    tmk[tid] = m;
+    lds_barrier();
+    const int lo = c * TKM_CHUNK, hi = min(lo + TKM_CHUNK, t.nb);
+    for (int w = tid; w < nwl; w += 1024) {
+        const int f = fbw[w];
+        if (f >= lo && f < hi) {
+            const int o = f - lo, th = o >> 2, e0 = o & 3;
+            wsel[w] = (int)(tpos[th] + (uint32_t)__popc(tmk[th] & ((1u << e0) - 1u)));
+        } else if (c == 0 && (f >= t.nb || t.budget <= 0)) {
+            wsel[w] = (int)k;
+        }
+    }
 }
 
 // ------------------------------------------------------------------ attention
@@ -2019,9 +2227,24 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w_in, const uint16_t *q
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev) hipEventRecord(ev[2], s);
-    const size_t topk_smem = w.max_blocks > 1024 * TOPK_KPT ? TB_SMEM : 0;
-    hipLaunchKernelGGL(k_topk, dim3(g.npairs), dim3(1024), topk_smem, s, g, w);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (w.tkx) {
+        const int nch = ceil_div(w.max_blocks, TKM_CHUNK);
+        const dim3 grid(nch, g.npairs);
+        for (int pass = 0; pass < 3; ++pass) {
+            hipLaunchKernelGGL(k_tkm_pass, grid, dim3(1024), 0, s, g, w, pass);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        hipLaunchKernelGGL(k_tkm_eq, grid, dim3(1024), 0, s, g, w, nch);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(k_tkm_taken, grid, dim3(1024), 0, s, g, w, nch);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(k_tkm_write, grid, dim3(1024), 0, s, g, w, nch);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    } else {
+        const size_t topk_smem = w.max_blocks > 1024 * TOPK_KPT ? TB_SMEM : 0;
+        hipLaunchKernelGGL(k_topk, dim3(g.npairs), dim3(1024), topk_smem, s, g, w);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     if (ev) hipEventRecord(ev[3], s);
     {
         // the plan has at most max(slots, selected blocks / SPLIT_MAX) splits

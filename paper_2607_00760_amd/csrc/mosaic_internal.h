@@ -97,6 +97,7 @@ struct WsGeom {               // decode workspace
     uint8_t *bsize; uint64_t bsize_stride;  // [max_blocks]: per block, log2 of its token count
     uint2 *selinfo; uint64_t selinfo_stride; // [max_blocks]: blk_info of each selected entry
     float *wres; uint64_t wres_stride;      // [CMB_NCC][nw + 1][GP][CMB_RES]: per-window merged results
+    uint32_t *tkx; uint64_t tkx_stride;     // multi-workgroup top-k state, or null (pairs of <= 16 K blocks)
     int max_blocks, max_splits, max_sel;
     int split_slots;                        // attention workgroups resident at once on the device
 };
