@@ -902,38 +902,6 @@ __device__ __forceinline__ void topk_reg(const Geom &g, const WsGeom &ws, int p,
     window_tail(g, nb, k, wsel);
 }
 
-// More keys (long contexts): each lane reads four consecutive keys (one
-// 16-byte score load, one 4-byte size load), a wave 256 consecutive keys, and
-// TB_UNROLL such groups are in flight per wave, so that a pass over the keys
-// is a few memory round trips.  The block order that the tie rule and the
-// list need is carried by 256-key segments, one wave's keys of one step: a
-// round of up to TB_SEGS segments scans their equal-key tokens, then their
-// taken counts, each with the carry of the rounds before; a segment's taken
-// blocks are four 64-bit masks (bit l of mask e: key 4 l + e).
-constexpr int TB_SEGS = 512;
-constexpr int TB_SEG_KEYS = 256;
-constexpr int TB_UNROLL = 8;
-constexpr size_t TB_SMEM = (size_t)TB_SEGS * (4 + 32);     // u32 prefixes + four u64 masks per segment
-
-// exclusive prefix sums (plus carry) of a[0 .. n) in place, n <= 4096, four
-// consecutive entries per thread; returns the total of the n entries
-__device__ __forceinline__ uint32_t seg_scan(uint32_t *a, int n, uint32_t carry, uint32_t *sbuf) {
-    const int tid = threadIdx.x;
-    uint32_t x[4], v[1], tot[1];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) x[e] = (4 * tid + e < n) ? a[4 * tid + e] : 0u;
-    v[0] = x[0] + x[1] + x[2] + x[3];
-    block_excl_scan_1024<1>(v, tot, sbuf);
-    uint32_t run = carry + v[0];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        if (4 * tid + e < n) a[4 * tid + e] = run;
-        run += x[e];
-    }
-    lds_barrier();
-    return tot[0];
-}
-
 // four consecutive keys and their log2 block sizes from index i (a multiple
 // of 4 below nb; the lanes past nb read the rest of the arrays' slack)
 struct Key4 {
@@ -949,164 +917,6 @@ __device__ __forceinline__ Key4 load_key4(const float *sc, const uint8_t *bz, in
     return r;
 }
 
-__device__ __forceinline__ void topk_big(const Geom &g, const WsGeom &ws, int p, int nb, int ndesc, int budget,
-                                         uint32_t *segw, uint32_t *hist, uint32_t *sbuf, int *fbw) {
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const float *sc = ws.score + (uint64_t)p * (ws.score_stride / 4);
-    const uint8_t *bz = ws.bsize + (uint64_t)p * ws.bsize_stride;
-    const uint2 *bi = ws.binfo + (uint64_t)p * (ws.binfo_stride / 8);
-    int32_t *sel = ws.sel + (uint64_t)p * (ws.sel_stride / 4);
-    int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
-    uint2 *sinfo = ws.selinfo + (uint64_t)p * (ws.selinfo_stride / 8);
-    uint64_t *segm = (uint64_t *)(segw + TB_SEGS);          // [TB_SEGS][4]
-    const int nwl = min(g.nw, TOPK_MAXW);
-    window_firsts(g, p, nb, ndesc, nwl, fbw);
-    for (int i = tid; i < TOPK_BINS; i += 1024) hist[i] = 0;
-    const int ng = (nb + 3) / 4;                            // groups of four keys
-    // the range of the keys (thread t: groups t, t + 1024, ...)
-    uint32_t kmin = 0xffffffffu, kmax = 0u;
-    for (int q0 = tid; q0 < ng; q0 += 1024 * TB_UNROLL) {
-        Key4 x[TB_UNROLL];
-#pragma unroll
-        for (int u = 0; u < TB_UNROLL; ++u) x[u] = load_key4(sc, bz, 4 * min(q0 + u * 1024, ng - 1));
-#pragma unroll
-        for (int u = 0; u < TB_UNROLL; ++u)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const bool in = 4 * min(q0 + u * 1024, ng - 1) + e < nb;   // (a clamped group repeats the last)
-                kmin = in ? min(kmin, x[u].k[e]) : kmin;
-                kmax = in ? max(kmax, x[u].k[e]) : kmax;
-            }
-    }
-    block_minmax_1024(kmin, kmax, sbuf);
-    uint32_t base = kmin, span = kmax - kmin, rem = (uint32_t)budget;
-    for (int pass = 0; budget > 0; ++pass) {
-        uint32_t *hc = hist + (pass & 1) * TOPK_BINS, *hn = hist + ((pass + 1) & 1) * TOPK_BINS;
-        const int bits = 32 - (span ? __builtin_clz(span) : 32);
-        const int sh = bits > 11 ? bits - 11 : 0;
-        for (int q0 = tid; q0 < ng; q0 += 1024 * TB_UNROLL) {
-            Key4 x[TB_UNROLL];
-#pragma unroll
-            for (int u = 0; u < TB_UNROLL; ++u) x[u] = load_key4(sc, bz, 4 * min(q0 + u * 1024, ng - 1));
-#pragma unroll
-            for (int u = 0; u < TB_UNROLL; ++u)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint32_t key = x[u].k[e], d = key - base;
-                    if (4 * (q0 + u * 1024) + e < nb && key >= base && d <= span) atomicAdd(&hc[d >> sh], x[u].tok(e));
-                }
-        }
-        lds_barrier();
-        if (radix_pick(hc, hn, sbuf, sh, base, span, rem)) break;
-    }
-    const uint32_t T = base, need = rem;
-    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    uint32_t eqc = 0, posc = 0;                             // carries: equal tokens, list positions
-    for (int r0 = 0; budget > 0 && r0 < nb; r0 += TB_SEGS * TB_SEG_KEYS) {
-        const int nk = min(nb - r0, TB_SEGS * TB_SEG_KEYS), ns = (nk + TB_SEG_KEYS - 1) / TB_SEG_KEYS;
-        // the lane's four keys of segment sg of this round (clamped to the
-        // round's last group); in(e): key e is one of the round's keys
-        auto fetch = [&](int sg) {
-            const int o = min(sg * TB_SEG_KEYS + 4 * lane, (nk - 1) & ~3);
-            return load_key4(sc, bz, r0 + o);
-        };
-        auto in = [&](int sg, int e) { return sg * TB_SEG_KEYS + 4 * lane + e < nk; };
-        // (a) tokens equal to T per segment -> their prefixes in block order
-        for (int s0 = wv; s0 < ns; s0 += 16 * TB_UNROLL) {
-            Key4 x[TB_UNROLL];
-#pragma unroll
-            for (int u = 0; u < TB_UNROLL; ++u) x[u] = fetch(s0 + 16 * u);
-#pragma unroll
-            for (int u = 0; u < TB_UNROLL; ++u) {
-                const int sg = s0 + 16 * u;
-                uint32_t e4 = 0;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) e4 += (in(sg, e) && x[u].k[e] == T) ? x[u].tok(e) : 0u;
-                const uint32_t tot = wave_scan_add(e4);
-                if (lane == 63 && sg < ns) segw[sg] = tot;
-            }
-        }
-        lds_barrier();
-        const uint32_t eq_round = seg_scan(segw, ns, eqc, sbuf);
-        eqc += eq_round;
-        // (b) taken blocks: four masks per segment and their count
-        for (int s0 = wv; s0 < ns; s0 += 16 * TB_UNROLL) {
-            Key4 x[TB_UNROLL];
-#pragma unroll
-            for (int u = 0; u < TB_UNROLL; ++u) x[u] = fetch(s0 + 16 * u);
-#pragma unroll
-            for (int u = 0; u < TB_UNROLL; ++u) {
-                const int sg = s0 + 16 * u;
-                uint32_t xe[4], e4 = 0;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    xe[e] = (in(sg, e) && x[u].k[e] == T) ? x[u].tok(e) : 0u;
-                    e4 += xe[e];
-                }
-                uint32_t pre = (sg < ns ? segw[sg] : 0u) + wave_scan_add(e4) - e4;
-                uint32_t cnt = 0;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint32_t key = x[u].k[e];
-                    const bool t = in(sg, e) && (key > T || (key == T && pre < need));
-                    pre += xe[e];
-                    const uint64_t m = __ballot(t);
-                    cnt += (uint32_t)__popcll(m);
-                    if (lane == 0 && sg < ns) segm[4 * sg + e] = m;
-                }
-                if (lane == 0 && sg < ns) segw[sg] = cnt;
-            }
-        }
-        lds_barrier();
-        const uint32_t taken_round = seg_scan(segw, ns, posc, sbuf);
-        posc += taken_round;
-        // (c) the list entries of the round, and the windows that start in it
-        for (int s0 = wv; s0 < ns; s0 += 16 * TB_UNROLL) {
-#pragma unroll
-            for (int u = 0; u < TB_UNROLL; ++u) {
-                const int sg = s0 + 16 * u;
-                if (sg < ns) {
-                    uint32_t pos = segw[sg];
-                    uint64_t m[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        m[e] = segm[4 * sg + e];
-                        pos += (uint32_t)__popcll(m[e] & below);    // taken keys of the lanes before
-                    }
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        if ((m[e] >> lane) & 1ull) {
-                            const int i = r0 + sg * TB_SEG_KEYS + 4 * lane + e;
-                            sel[pos] = i;
-                            sinfo[pos] = bi[i];
-                            ++pos;
-                        }
-                    }
-                }
-            }
-        }
-        for (int w = tid; w < nwl; w += 1024) {
-            const int f = fbw[w];
-            if (f >= r0 && f < r0 + nk) {
-                const int sg = (f - r0) / TB_SEG_KEYS, o = (f - r0) % TB_SEG_KEYS, l = o >> 2, e0 = o & 3;
-                const uint64_t bl = (l == 0) ? 0ull : (~0ull >> (64 - l));
-                uint32_t pos = segw[sg];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint64_t m = segm[4 * sg + e];
-                    pos += (uint32_t)__popcll(m & bl) + ((e < e0) ? (uint32_t)((m >> l) & 1ull) : 0u);
-                }
-                wsel[w] = (int)pos;
-            }
-        }
-        lds_barrier();                                     // the next round rewrites segw / segm
-    }
-    const int k = budget > 0 ? (int)posc : 0;
-    for (int w = tid; w < nwl; w += 1024)
-        if (budget <= 0 || fbw[w] >= nb) wsel[w] = k;
-    window_tail(g, nb, k, wsel);
-}
-
 // the token budget of pair p: ceil(rho * scoreable tokens), at least one
 // token (0 without scoreable blocks)
 __device__ __forceinline__ int pair_budget(const Geom &g, int nb, int nf, int prov) {
@@ -1116,8 +926,9 @@ __device__ __forceinline__ int pair_budget(const Geom &g, int nb, int nf, int pr
     return (int)(bb < 1 ? 1 : (bb > ntok ? ntok : bb));
 }
 
+// one workgroup per pair, for caches of at most 16 K blocks per pair (longer
+// ones take the multi-workgroup kernels below)
 __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
-    extern __shared__ __align__(16) uint32_t segw[];            // [TB_SMEM / 4] on the long-context path
     __shared__ uint32_t hist[2 * TOPK_BINS];
     __shared__ uint32_t sbuf[64];
     __shared__ int fbw[TOPK_MAXW];
@@ -1127,8 +938,7 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
     int nf, prov, nbuf;
     const int ndesc = pair_ndesc(meta, nf, prov, nbuf);
     const int budget = pair_budget(g, nb, nf, prov);
-    if (nb <= 1024 * TOPK_KPT) topk_reg(g, ws, p, nb, ndesc, budget, hist, sbuf, fbw);
-    else topk_big(g, ws, p, nb, ndesc, budget, segw, hist, sbuf, fbw);
+    topk_reg(g, ws, p, min(nb, 1024 * TOPK_KPT), ndesc, budget, hist, sbuf, fbw);
 }
 
 // ------------------------------------------------------------------ top-k over many workgroups
@@ -1204,6 +1014,7 @@ __global__ void __launch_bounds__(1024) k_tkm_pass(Geom g, WsGeom ws, int pass) 
     const int p = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
     TkmCtx t;
     const bool mine = tkm_setup(g, ws, p, c, t);
+    if (!mine && c != 0) return;                            // past the pair's blocks (workgroup 0 records the state)
     const TkmHdr h = tkm_state(t, pass, hl, hd, sbuf);
     if (c == 0 && tid == 0) ((TkmHdr *)(t.st + 3 * TOPK_BINS))[pass] = h;
     if (h.done || !mine) return;
@@ -1239,6 +1050,7 @@ __global__ void __launch_bounds__(1024) k_tkm_eq(Geom g, WsGeom ws, int nch) {
     const int p = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
     TkmCtx t;
     const bool mine = tkm_setup(g, ws, p, c, t);
+    if (!mine && c != 0) return;
     const TkmHdr h = tkm_state(t, 3, hl, hd, sbuf);
     if (c == 0 && tid == 0) ((TkmHdr *)(t.st + 3 * TOPK_BINS))[3] = h;
     if (!mine) return;
@@ -2241,8 +2053,7 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w_in, const uint16_t *q
         hipLaunchKernelGGL(k_tkm_write, grid, dim3(1024), 0, s, g, w, nch);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     } else {
-        const size_t topk_smem = w.max_blocks > 1024 * TOPK_KPT ? TB_SMEM : 0;
-        hipLaunchKernelGGL(k_topk, dim3(g.npairs), dim3(1024), topk_smem, s, g, w);
+        hipLaunchKernelGGL(k_topk, dim3(g.npairs), dim3(1024), 0, s, g, w);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev) hipEventRecord(ev[3], s);
