@@ -38,7 +38,10 @@ def _stream(b, h, which):
     return gen.drift_tokens(f"dyn.{b}.{h}", n, which).to(torch.bfloat16)
 
 
-def _setup():
+VARIANTS = {"default": {}, "fp8": dict(fp8=True), "trunc96": dict(trunc=96)}
+
+
+def _setup(variant="default"):
     ns = len(CTX)
     toks = {(b, h, w): _stream(b, h, w) for b in range(ns) for h in range(HKV) for w in ("k", "v")}
     cap = max(CTX) + APPENDS
@@ -55,9 +58,10 @@ def _setup():
             v[b, h, :L] = toks[(b, h, "v")][:L]
             rk[b, h] = gen._rotations(k[b, h, :L].float(), L, W, nw_src, "cpu")
             rv[b, h] = gen._rotations(v[b, h, :L].float(), L, W, nw_src, "cpu")
+    kw = VARIANTS[variant]
     lp = M.Params(num_kv_heads=HKV, group_size=G, dtype="bf16", rot_window=W, dyn_windows=True, tau_window=TAU,
-                  min_window=MINW)
-    op = O.Params(group=G, dtype="bf16", rot_window=W, dyn=True, tau_window=TAU, min_window=MINW)
+                  min_window=MINW, **kw)
+    op = O.Params(group=G, dtype="bf16", rot_window=W, dyn=True, tau_window=TAU, min_window=MINW, **kw)
     return toks, cap, k, v, rk, rv, lp, op
 
 
@@ -70,10 +74,13 @@ def _gpu_windows(c, p, nwin_max):
     return dict(nwin=nwin, pend=pend, wloss=float(wloss), wseg=wseg)
 
 
-def test_loss_closed_windows_match_oracle():
-    toks, cap, k, v, rk, rv, lp, op = _setup()
+@pytest.mark.parametrize("variant", list(VARIANTS))
+def test_loss_closed_windows_match_oracle(variant):
+    """Also with E4M3 token values and with 96-channel truncated bitmaps: the
+    loss, the close decisions and the re-encoding follow the same records."""
+    toks, cap, k, v, rk, rv, lp, op = _setup(variant)
     ns, npairs = len(CTX), len(CTX) * HKV
-    print(f"[dyn] ctx={CTX} appends={APPENDS} W={W} min={MINW} tau={TAU}", flush=True)
+    print(f"[dyn] {variant} ctx={CTX} appends={APPENDS} W={W} min={MINW} tau={TAU}", flush=True)
     c = M.MosaicCache(lp, ns, cap, rotated=True)
     c.compress(k.cuda(), v.cuda(), list(CTX), rk.cuda(), rv.cuda())
     ops = []
