@@ -219,7 +219,7 @@ typedef struct {
     uint64_t part_off, part_stride, tag_off, tag_stride, binfo_off, binfo_stride, bsize_off, bsize_stride,
              selinfo_off, selinfo_stride, wres_off, wres_stride, total;
     int32_t max_blocks, max_splits, gp, reserved;
-    uint64_t tkx_off, tkx_stride;   /* caches of more than 16384 blocks per pair: the
+    uint64_t tkx_off, tkx_stride;   /* caches of more than 32768 blocks per pair: the
                                        selection's per-pair state (histograms of three
                                        radix passes, their states, per-chunk counts of
                                        4096 blocks); else 0 */

@@ -345,9 +345,9 @@ static mosaic_status cache_create(const mosaic_params *params, int32_t num_seqs,
     wregion(w.selinfo_off, w.selinfo_stride, (uint64_t)c->max_blocks * 8);
     // wres: each window's merged, back-rotated result per column block
     wregion(w.wres_off, w.wres_stride, (uint64_t)CMB_NCC * (c->nw + 1) * c->GP * CMB_RES * 4);
-    // pairs of more than 16 K blocks: the multi-workgroup top-k's histograms,
+    // pairs of more than 32 K blocks: the multi-workgroup top-k's histograms,
     // radix states and per-chunk counts (chunks of 4096 blocks)
-    if (c->max_blocks > 16384) {
+    if (c->max_blocks > 32768) {
         const uint64_t nch = ((uint64_t)c->max_blocks + 4095) / 4096;
         wregion(w.tkx_off, w.tkx_stride, (3ull * 2048 + 16 + 2 * nch) * 4);
     }

@@ -15,9 +15,11 @@
 //            range [min, max] of the keys still in play, 2048 bins each, so
 //            the bins follow the keys that are present (at most three passes
 //            reach a single key), then an ordered compaction that breaks ties
-//            by the lowest block index.  Up to 16384 blocks per pair the keys
-//            stay in registers (16 per thread); scans and reductions use lane
-//            shifts inside the wave.
+//            by the lowest block index.  Up to 32768 blocks per pair the keys
+//            stay in registers (16 or 32 per thread, one workgroup per pair);
+//            scans and reductions use lane shifts inside the wave.  Longer
+//            pairs are spread over workgroups of 4096 blocks, one kernel per
+//            phase.
 //   attn   : split-K over the selected list (up to 128 blocks of one rotation
 //            window per split).  The split's blocks are ordered by size, so a
 //            64-token chunk never cuts a block and a token finds its block by
@@ -657,7 +659,7 @@ __global__ void __launch_bounds__(256) k_score(Geom g, WsGeom ws, int spw) {
 
 // ------------------------------------------------------------------ topk
 constexpr int TOPK_BINS = 2048;
-constexpr int TOPK_KPT = 16;                               // keys per thread held in registers
+constexpr int TOPK_KPT_MAX = 32;                           // keys per thread held in registers, at most
 
 // wave-level inclusive scans on the data-parallel-primitive lane shifts (no
 // LDS round trips): shifts by 1, 2, 4, 8 inside each 16-lane row, then the
@@ -802,8 +804,10 @@ __device__ __forceinline__ void window_tail(const Geom &g, int nb, int k, int32_
     if (threadIdx.x == 0) { wsel[g.nw] = k; wsel[g.nw + 1] = nb; }
 }
 
-// Up to 16 K keys: thread t owns the blocks [16 t, 16 t + 16); their keys
-// and sizes stay in registers and the taken ones are a 16-bit mask.
+// Up to 1024 KPT keys (KPT = 16 or 32): thread t owns the blocks [KPT t,
+// KPT t + KPT); their keys and sizes stay in registers and the taken ones are
+// a KPT-bit mask.
+template <int KPT>
 __device__ __forceinline__ void topk_reg(const Geom &g, const WsGeom &ws, int p, int nb, int ndesc, int budget,
                                          uint32_t *hist, uint32_t *sbuf, int *fbw) {
     const int tid = threadIdx.x;
@@ -812,26 +816,29 @@ __device__ __forceinline__ void topk_reg(const Geom &g, const WsGeom &ws, int p,
     int32_t *sel = ws.sel + (uint64_t)p * (ws.sel_stride / 4);
     int32_t *wsel = ws.wsel + (uint64_t)p * (ws.wsel_stride / 4);
     uint2 *sinfo = ws.selinfo + (uint64_t)p * (ws.selinfo_stride / 8);
-    const int i0 = min(nb, tid * TOPK_KPT), i1 = min(nb, i0 + TOPK_KPT), n_own = i1 - i0;
+    const int i0 = min(nb, tid * KPT), i1 = min(nb, i0 + KPT), n_own = i1 - i0;
     const int nwl = min(g.nw, TOPK_MAXW);
     window_firsts(g, p, nb, ndesc, nwl, fbw);              // published by the first barrier
     const uint8_t *bz = ws.bsize + (uint64_t)p * ws.bsize_stride;
-    uint32_t kr[TOPK_KPT];
-    uint32_t zr[TOPK_KPT / 4];                             // log2 block sizes, four per word
+    uint32_t kr[KPT];
+    uint32_t zr[KPT / 4];                             // log2 block sizes, four per word
     uint32_t kmin = 0xffffffffu, kmax = 0u;
     {
         const float4 *s4 = (const float4 *)(sc + i0);
-        const uint4 z4 = n_own > 0 ? *(const uint4 *)(bz + i0) : make_uint4(0u, 0u, 0u, 0u);
-        zr[0] = z4.x; zr[1] = z4.y; zr[2] = z4.z; zr[3] = z4.w;
 #pragma unroll
-        for (int q = 0; q < TOPK_KPT / 4; ++q) {
+        for (int h = 0; h < KPT / 16; ++h) {
+            const uint4 z4 = 16 * h < n_own ? *(const uint4 *)(bz + i0 + 16 * h) : make_uint4(0u, 0u, 0u, 0u);
+            zr[4 * h] = z4.x; zr[4 * h + 1] = z4.y; zr[4 * h + 2] = z4.z; zr[4 * h + 3] = z4.w;
+        }
+#pragma unroll
+        for (int q = 0; q < KPT / 4; ++q) {
             float4 f = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
             if (4 * q < n_own) f = s4[q];
             kr[4 * q] = score_key(f.x); kr[4 * q + 1] = score_key(f.y);
             kr[4 * q + 2] = score_key(f.z); kr[4 * q + 3] = score_key(f.w);
         }
 #pragma unroll
-        for (int j = 0; j < TOPK_KPT; ++j)
+        for (int j = 0; j < KPT; ++j)
             if (j < n_own) { kmin = min(kmin, kr[j]); kmax = max(kmax, kr[j]); }
     }
     // tokens of owned block j: 2^(log2 size)
@@ -846,7 +853,7 @@ __device__ __forceinline__ void topk_reg(const Geom &g, const WsGeom &ws, int p,
         const int bits = 32 - (span ? __builtin_clz(span) : 32);
         const int sh = bits > 11 ? bits - 11 : 0;                 // (span >> sh) < 2048
 #pragma unroll
-        for (int j = 0; j < TOPK_KPT; ++j) {
+        for (int j = 0; j < KPT; ++j) {
             const uint32_t d = kr[j] - base;
             if (j < n_own && kr[j] >= base && d <= span) atomicAdd(&hc[d >> sh], tok_reg(j));
         }
@@ -858,7 +865,7 @@ __device__ __forceinline__ void topk_reg(const Geom &g, const WsGeom &ws, int p,
     uint32_t v[1] = {0u}, tot[1];
     if (budget > 0) {                                      // this thread's tokens equal to T
 #pragma unroll
-        for (int j = 0; j < TOPK_KPT; ++j) v[0] += (j < n_own && kr[j] == T) ? tok_reg(j) : 0u;
+        for (int j = 0; j < KPT; ++j) v[0] += (j < n_own && kr[j] == T) ? tok_reg(j) : 0u;
     }
     block_excl_scan_1024<1>(v, tot, sbuf);                 // -> equal tokens before this thread
     // taken blocks: above T, or equal to T while the equal tokens before are below need
@@ -866,7 +873,7 @@ __device__ __forceinline__ void topk_reg(const Geom &g, const WsGeom &ws, int p,
     if (budget > 0) {
         uint32_t acc = v[0];
 #pragma unroll
-        for (int j = 0; j < TOPK_KPT; ++j) {
+        for (int j = 0; j < KPT; ++j) {
             const bool eq = j < n_own && kr[j] == T;
             const bool t = j < n_own && (kr[j] > T || (eq && acc < need));
             acc += eq ? tok_reg(j) : 0u;
@@ -878,12 +885,12 @@ __device__ __forceinline__ void topk_reg(const Geom &g, const WsGeom &ws, int p,
     const uint32_t pos0 = v[0];
     const int k = budget > 0 ? (int)tot[0] : 0;            // blocks selected
     // the record info of the taken blocks only: all loads issued, then the stores
-    uint2 br[TOPK_KPT];
+    uint2 br[KPT];
 #pragma unroll
-    for (int j = 0; j < TOPK_KPT; ++j) br[j] = ((tmask >> j) & 1u) ? bi[i0 + j] : make_uint2(0u, 0u);
+    for (int j = 0; j < KPT; ++j) br[j] = ((tmask >> j) & 1u) ? bi[i0 + j] : make_uint2(0u, 0u);
     uint32_t pos = pos0;
 #pragma unroll
-    for (int j = 0; j < TOPK_KPT; ++j) {
+    for (int j = 0; j < KPT; ++j) {
         if ((tmask >> j) & 1u) { sel[pos] = i0 + j; sinfo[pos] = br[j]; }
         pos += (tmask >> j) & 1u;
     }
@@ -896,7 +903,7 @@ __device__ __forceinline__ void topk_reg(const Geom &g, const WsGeom &ws, int p,
     for (int w = tid; w < nwl; w += 1024) {
         const int f = fbw[w];
         if (f >= nb) { wsel[w] = k; continue; }
-        const int t = f / TOPK_KPT, off = f % TOPK_KPT;
+        const int t = f / KPT, off = f % KPT;
         wsel[w] = (int)(tpos[t] + (uint32_t)__popc(tmk[t] & ((1u << off) - 1u)));
     }
     window_tail(g, nb, k, wsel);
@@ -926,8 +933,9 @@ __device__ __forceinline__ int pair_budget(const Geom &g, int nb, int nf, int pr
     return (int)(bb < 1 ? 1 : (bb > ntok ? ntok : bb));
 }
 
-// one workgroup per pair, for caches of at most 16 K blocks per pair (longer
-// ones take the multi-workgroup kernels below)
+// one workgroup per pair, for calls whose pairs hold at most 32 K blocks
+// (longer ones take the multi-workgroup kernels below): 16 keys per thread
+// when the pair's blocks fit, else 32
 __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
     __shared__ uint32_t hist[2 * TOPK_BINS];
     __shared__ uint32_t sbuf[64];
@@ -938,11 +946,12 @@ __global__ void __launch_bounds__(1024) k_topk(Geom g, WsGeom ws) {
     int nf, prov, nbuf;
     const int ndesc = pair_ndesc(meta, nf, prov, nbuf);
     const int budget = pair_budget(g, nb, nf, prov);
-    topk_reg(g, ws, p, min(nb, 1024 * TOPK_KPT), ndesc, budget, hist, sbuf, fbw);
+    if (nb <= 1024 * 16) topk_reg<16>(g, ws, p, nb, ndesc, budget, hist, sbuf, fbw);
+    else topk_reg<32>(g, ws, p, min(nb, 1024 * TOPK_KPT_MAX), ndesc, budget, hist, sbuf, fbw);
 }
 
 // ------------------------------------------------------------------ top-k over many workgroups
-// Caches whose pairs can hold more than 16 K blocks: the same token-budget
+// Calls whose pairs can hold more than 32 K blocks: the same token-budget
 // selection, spread over workgroups of TKM_CHUNK consecutive blocks of a pair
 // and one kernel per phase, so that a long pair's keys are read by dozens of
 // CUs instead of one.  Three radix passes of 11, 11 and 10 bits over the
@@ -2039,7 +2048,13 @@ hipError_t launch_decode_dt(const Geom &g, const WsGeom &w_in, const uint16_t *q
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev) hipEventRecord(ev[2], s);
-    if (w.tkx) {
+    // blocks of a pair at most in this call: its segments times the most
+    // blocks a segment can have
+    int minb = g.def_block;
+    for (int i = 0; i < 3; ++i) minb = min(minb, g.block_cand[i]);
+    const long long maxb = (long long)max_desc_used * (SEG / minb);
+    if (maxb > 1024 * TOPK_KPT_MAX) {
+        if (!w.tkx) return hipErrorInvalidValue;               // the workspace has no multi-workgroup state
         const int nch = ceil_div(w.max_blocks, TKM_CHUNK);
         const dim3 grid(nch, g.npairs);
         for (int pass = 0; pass < 3; ++pass) {

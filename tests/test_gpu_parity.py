@@ -58,10 +58,14 @@ CASES = {
     # K and V for the byte-exact compression, K only for the decode (unit-scale
     # values keep the outputs O(1) under the same absolute bound)
     "fp8_wide_range": (gen.spec("c3", ctx=(1500, 700), hkv=2, kind="gauss"), dict(fp8=True)),
-    # more than 16 K blocks in a pair: the top-k's long-context path (strided
-    # passes, 64-key segments), over two rounds of segments for the first pair
+    # more than 32 K blocks in a pair: the multi-workgroup top-k (18 chunks of
+    # 4096 blocks for the first pair, 5 for the second)
     "long_topk_b4": (gen.spec("c1", ctx=(290000, 70000), hkv=1, rotate=False), dict(force_default=True,
                                                                                    default=(32, 1, 4))),
+    # 16 K to 32 K blocks in the first pair: the single-workgroup top-k with 32
+    # keys per thread, beside a short pair on 16 keys per thread
+    "mid_topk_b4": (gen.spec("c1", ctx=(100000, 3000), hkv=1, rotate=False), dict(force_default=True,
+                                                                                 default=(32, 1, 4))),
 }
 
 
@@ -160,11 +164,12 @@ def test_append_flush_finalize_parity(name):
             assert_close(out.cpu().numpy(), want, f"{name} step {t}")
 
 
-def test_long_topk_all_ties():
+@pytest.mark.parametrize("name", ["long_topk_b4", "mid_topk_b4"])
+def test_long_topk_all_ties(name):
     """A zero query scores every block 0: the selection is the first blocks in
-    block order up to the token budget, on the long-context top-k path, where
-    the equal-token prefix carries from one round of segments to the next."""
-    spec, lay, lp, op, cap = _case("long_topk_b4")
+    block order up to the token budget, on the multi-workgroup top-k (where
+    the equal-token prefix carries across chunks) and on the 32-key path."""
+    spec, lay, lp, op, cap = _case(name)
     c = gpu_cache(lp, spec, lay, cap)
     ops = oracle_pairs(op, spec, lay, cap)
     q = torch.zeros((spec.num_seqs, spec.hq, D), dtype=spec.torch_dtype)
