@@ -168,7 +168,9 @@ typedef struct {
     uint64_t total;
     int32_t num_pairs, max_desc, num_windows, reserved;
     uint64_t cov_off, cov_stride;   /* dyn_windows only (else 0) */
-    uint64_t pairs_off;             /* uint64 [num_pairs][4] device copy of the pair table below */
+    uint64_t pairs_off;             /* uint64 [num_pairs][4] device copy of the pair table below
+                                       (written by mosaic_compress; the kernels locate the pair
+                                       regions through it) */
 } mosaic_layout;
 mosaic_status mosaic_cache_layout(const mosaic_cache *cache, mosaic_layout *out);
 

@@ -80,7 +80,7 @@ struct mosaic_cache {
         g.tok_stride = lay.token_stride; g.buf_stride = lay.buf_stride; g.stg_stride = lay.stage_stride;
         g.rot_stride = lay.rot_stride;
         g.cov = (double *)(arena + lay.cov_off); g.cov_stride = lay.cov_stride;
-        g.ragged = ragged ? 1 : 0; g.poff = (const uint64_t *)(arena + lay.pairs_off);
+        g.poff = (const uint64_t *)(arena + lay.pairs_off);
         for (int i = 0; i < 3; ++i) {
             g.keep_cand[i] = P.keep_cand[i]; g.group_cand[i] = P.group_cand[i]; g.block_cand[i] = P.block_cand[i];
         }
@@ -463,8 +463,7 @@ mosaic_status mosaic_compress(mosaic_cache *c, const void *k, const void *v, int
     int32_t *ctx_dev = (int32_t *)(c->arena + c->ctx_off);
     hipError_t e = launch_ctx_copy(ctx_dev, ctx_lens_host, c->num_seqs, s);
     if (e != hipSuccess) return hip_fail(e, "copy of context lengths");
-    if (c->ragged && (e = launch_pairs_copy((uint64_t *)(c->arena + c->lay.pairs_off), c->pairs.data(), c->npairs, s))
-                         != hipSuccess)
+    if ((e = launch_pairs_copy((uint64_t *)(c->arena + c->lay.pairs_off), c->pairs.data(), c->npairs, s)) != hipSuccess)
         return hip_fail(e, "copy of the pair table");
     if (c->rotated && (e = launch_copy_rot(g, rot_k, rot_v, c->nw_src, s)) != hipSuccess) return hip_fail(e, "rotation copy");
     e = launch_compress(g, (const uint16_t *)k, (const uint16_t *)v, seq_stride, ctx_dev, maxL / SEG, any_tail,

@@ -49,7 +49,6 @@ struct Geom {
     uint16_t *buf, *stg;
     float *rot;
     double *cov; uint64_t cov_stride;   // dynamic windows: [2][2][D][D] per pair
-    int ragged;                         // per-sequence capacities: pair regions from poff
     const uint64_t *poff;               // [npairs][4]: desc, score, token offsets; token bytes
     uint64_t meta_stride, desc_stride, sc_stride, tok_stride, buf_stride, stg_stride, rot_stride;
     int keep_cand[3], group_cand[3], block_cand[3];
@@ -63,12 +62,12 @@ struct Geom {
     float tau_win;                    // accumulated loss that closes a window
 
     __host__ __device__ PairMeta *meta_of(int p) const { return (PairMeta *)(meta + (uint64_t)p * meta_stride); }
-    __host__ __device__ Desc *desc_of(int p) const {
-        return (Desc *)(desc + (ragged ? poff[4 * p] : (uint64_t)p * desc_stride));
-    }
-    __host__ __device__ uint8_t *sc_of(int p) const { return sc + (ragged ? poff[4 * p + 1] : (uint64_t)p * sc_stride); }
-    __host__ __device__ uint8_t *tok_of(int p) const { return tok + (ragged ? poff[4 * p + 2] : (uint64_t)p * tok_stride); }
-    __host__ __device__ uint64_t tok_size(int p) const { return ragged ? poff[4 * p + 3] : tok_stride; }
+    // a pair's descriptor, score and token regions, from the pair table (one
+    // read each; the table serves caches of one capacity and ragged ones alike)
+    __host__ __device__ Desc *desc_of(int p) const { return (Desc *)(desc + poff[4 * p]); }
+    __host__ __device__ uint8_t *sc_of(int p) const { return sc + poff[4 * p + 1]; }
+    __host__ __device__ uint8_t *tok_of(int p) const { return tok + poff[4 * p + 2]; }
+    __host__ __device__ uint64_t tok_size(int p) const { return poff[4 * p + 3]; }
     __host__ __device__ uint16_t *buf_of(int p) const { return (uint16_t *)((uint8_t *)buf + (uint64_t)p * buf_stride); }
     __host__ __device__ uint16_t *stg_of(int p) const { return (uint16_t *)((uint8_t *)stg + (uint64_t)p * stg_stride); }
     // slot of window w's K (which 0) or V (1) covariance, pair p

@@ -35,8 +35,8 @@ hipError_t launch_ctx_copy(int32_t *, const int32_t *src_host, int n, hipStream_
     return hipSuccess;
 }
 hipError_t launch_pairs_copy(uint64_t *, const uint64_t *src_host, int npairs, hipStream_t) {
-    std::string s = "pairs_copy";
-    for (int i = 0; i < 4 * npairs; ++i) s += " " + std::to_string((unsigned long long)src_host[i]);
+    std::string s = "pairs_copy npairs=" + std::to_string(npairs) + " tok";
+    for (int i = 0; i < npairs && i < 16; ++i) s += " " + std::to_string((unsigned long long)src_host[4 * i + 2]);
     rec("%s", s.c_str());
     return hipSuccess;
 }

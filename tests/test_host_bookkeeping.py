@@ -111,7 +111,9 @@ def run_checks(path):
         assert L.mosaic_last_error()
     assert sim.log() == []
     assert L.mosaic_compress(h, kv, kv, 100, ctx, None, None, None, 0, None) == OK
-    assert sim.log() == ["ctx_copy 0 31 100", f"compress npairs={ns * hkv} stride=100 segs=1 tail=1"]
+    log = sim.log()
+    assert log[0] == "ctx_copy 0 31 100" and log[1].startswith(f"pairs_copy npairs={ns * hkv} tok 0 ")
+    assert log[2:] == [f"compress npairs={ns * hkv} stride=100 segs=1 tail=1"]
     lengths = [0, 31, 100]
     assert sim.tokens(h, ns) == lengths
     # ---- the append schedule over 320 appends (ragged lengths cross U and S at different steps)
@@ -163,7 +165,8 @@ def run_checks(path):
     assert L.mosaic_compress(h3, kv, kv, 130, ctx1, None, None, None, 0, None) == INVALID
     rot = sim.buf(2 * 128 * 128 * 4, 16)
     assert L.mosaic_compress(h3, kv, kv, 130, ctx1, rot, rot, None, 0, None) == OK
-    assert sim.log() == ["ctx_copy 130", "copy_rot npairs=1 nw=2 src=2", "compress npairs=1 stride=130 segs=2 tail=1"]
+    assert sim.log() == ["ctx_copy 130", "pairs_copy npairs=1 tok 0", "copy_rot npairs=1 nw=2 src=2",
+                         "compress npairs=1 stride=130 segs=2 tail=1"]
     assert L.mosaic_cache_destroy(h3) == OK
     # ---- dynamic windows: parameters, window slots, and the poll-before-compress rule
     for kw, st in [(dict(dyn_windows=2), INVALID), (dict(dyn_windows=1, min_window=100), INVALID),
@@ -183,7 +186,7 @@ def run_checks(path):
     ctx4 = (C.c_int32 * 2)(62, 10)
     rot4 = sim.buf(2 * 2 * 128 * 128 * 4, 16)
     assert L.mosaic_compress(h4, kv, kv, 100, ctx4, rot4, rot4, None, 0, None) == OK
-    assert sim.log()[1] == "copy_rot npairs=2 nw=8 src=2"
+    assert sim.log()[2] == "copy_rot npairs=2 nw=8 src=2"
     closed = (C.c_int32 * 6)()
     nclosed = C.c_int32()
     h5, _, _ = sim.cache(1, 100)
@@ -215,7 +218,9 @@ def run_checks(path):
     assert sim.log() == []
     assert L.mosaic_compress(h6, kv, kv, 100, (C.c_int32 * 2)(38, 100), None, None, None, 0, None) == OK
     log = sim.log()
-    assert log[0] == "ctx_copy 38 100" and log[1].startswith("pairs_copy 0 ")
+    tok = [int(x) for x in log[1].split(" tok ")[1].split()]
+    assert log[0] == "ctx_copy 38 100" and log[1].startswith("pairs_copy npairs=2 tok 0 ")
+    assert 0 < tok[1] < 8 * 64 * 2 * 112        # the short sequence's token slot: (40 / 64 + 2) segments
     assert L.mosaic_append(h6, kv, kv, None) == OK and L.mosaic_append(h6, kv, kv, None) == OK
     assert L.mosaic_append(h6, kv, kv, None) == CAPACITY                                     # sequence 0 holds 40
     assert sim.tokens(h6, 2) == [40, 102]
