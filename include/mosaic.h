@@ -182,7 +182,7 @@ mosaic_status mosaic_cache_layout(const mosaic_cache *cache, mosaic_layout *out)
  * 4 * num_pairs entries. */
 mosaic_status mosaic_cache_pair_regions(const mosaic_cache *cache, uint64_t *out_host);
 
-enum { MOSAIC_OP_COMPRESS = 0, MOSAIC_OP_APPEND = 1, MOSAIC_OP_DECODE = 2 };
+enum { MOSAIC_OP_COMPRESS = 0, MOSAIC_OP_APPEND = 1, MOSAIC_OP_DECODE = 2, MOSAIC_OP_WINDOW_ROTATIONS = 3 };
 /* Workspace bytes an operation can use (0 if none).  Depends only on the
  * cache's shape and capacity, so one allocation serves every call.  DECODE
  * requires its workspace; COMPRESS's is optional (see mosaic_compress): a
@@ -292,6 +292,22 @@ mosaic_status mosaic_append(mosaic_cache *cache, const void *k_new, const void *
  * run at any time.  Errors: INVALID (NULL; no dynamic windows), STATE (not
  * compressed). */
 mosaic_status mosaic_window_poll(mosaic_cache *cache, int32_t *out_host, int32_t *n_closed_host, void *stream);
+
+/* Rotations of the windows the last poll reported, on the GPU, from their
+ * incremental covariances (Sec. 5.5: with the covariance kept up to date the
+ * closed segment's rotation follows directly from it): each K and V
+ * covariance is cast to fp32 and solved by the cyclic Jacobi eigensolver of
+ * mosaic_compute_rotations (rows by descending eigenvalue, each signed so that
+ * its largest-magnitude component is positive).
+ *   rot_k, rot_v : [num_seqs][num_kv_heads][128][128] fp32 outputs, in the
+ *                  layout mosaic_window_close takes; pairs with nothing to
+ *                  close get the identity.
+ *   ws           : at least mosaic_workspace_bytes(MOSAIC_OP_WINDOW_ROTATIONS)
+ *                  bytes, 256-byte aligned.
+ * Errors: INVALID (NULL, misaligned, small workspace, no dynamic windows),
+ * STATE (a segment completed since the last poll). */
+mosaic_status mosaic_window_rotations(mosaic_cache *cache, float *rot_k, float *rot_v, void *ws, size_t ws_bytes,
+                                      void *stream);
 
 /* Closes every window the last poll reported.
  *   rot_k, rot_v : [num_seqs][num_kv_heads][128][128] fp32: each such pair's

@@ -10,7 +10,7 @@ from __future__ import annotations
 import ctypes as C
 from dataclasses import dataclass
 
-from ._lib import (OP_APPEND, OP_COMPRESS, OP_DECODE, MosaicError, MosaicLayout, MosaicParams, MosaicStats,
+from ._lib import (OP_APPEND, OP_COMPRESS, OP_DECODE, OP_WINDOW_ROTATIONS, MosaicError, MosaicLayout, MosaicParams, MosaicStats,
                    MosaicWsLayout, check, load)
 
 __all__ = ["Params", "MosaicCache", "dense_decode", "MosaicError", "load"]
@@ -203,6 +203,22 @@ class MosaicCache:
         with torch.cuda.device(self.device):
             check(self.lib.mosaic_window_poll(self._h, out, C.byref(n), _stream(self.device)))
         return {p: (out[3 * p], out[3 * p + 1], out[3 * p + 2]) for p in range(self.num_pairs) if out[3 * p] >= 0}
+
+    def window_rotations(self):
+        """Rotations of the polled windows from their incremental covariances,
+        on the GPU: (rot_k, rot_v) [num_seqs][Hkv][128][128] fp32 (identity for
+        pairs with nothing to close)."""
+        import torch
+        n = C.c_size_t()
+        check(self.lib.mosaic_workspace_bytes(self._h, OP_WINDOW_ROTATIONS, C.byref(n)))
+        ws = torch.empty(max(n.value, 256), dtype=torch.uint8, device=self.device)
+        rk = torch.empty((self.num_seqs, self.params.num_kv_heads, D, D), dtype=torch.float32, device=self.device)
+        rv = torch.empty_like(rk)
+        with torch.cuda.device(self.device):
+            check(self.lib.mosaic_window_rotations(self._h, _ptr(rk), _ptr(rv), _ptr(ws), ws.numel(),
+                                                   _stream(self.device)))
+        self._keep_wrot = ws
+        return rk, rv
 
     def window_close(self, rot_k, rot_v, k, v):
         """rot_k, rot_v: [num_seqs][Hkv][128][128] fp32, each polled pair's new

@@ -9,7 +9,7 @@ LIB_PATH = os.path.join(HERE, "libmosaic.so")
 
 MOSAIC_OK = 0
 STATUS_NAMES = {0: "OK", -1: "INVALID", -2: "UNSUPPORTED", -3: "CAPACITY", -4: "STATE", -5: "HIP"}
-OP_COMPRESS, OP_APPEND, OP_DECODE = 0, 1, 2
+OP_COMPRESS, OP_APPEND, OP_DECODE, OP_WINDOW_ROTATIONS = 0, 1, 2, 3
 
 EXPORTED = [
     "mosaic_params_default", "mosaic_cache_create", "mosaic_cache_arena_bytes", "mosaic_cache_bind",
@@ -19,6 +19,7 @@ EXPORTED = [
     "mosaic_set_timing", "mosaic_decode_timing", "mosaic_rotation_workspace_bytes", "mosaic_compute_rotations",
     "mosaic_reorder_workspace_bytes", "mosaic_reorder_rotations", "mosaic_decode_attention_noalloc",
     "mosaic_window_poll", "mosaic_window_close", "mosaic_cache_create_ragged", "mosaic_cache_pair_regions",
+    "mosaic_window_rotations",
 ]
 
 
@@ -108,6 +109,7 @@ def bind_signatures(L: C.CDLL) -> C.CDLL:
                                            C.POINTER(C.c_int32), vp, vp, vp, sz, vp]
     L.mosaic_window_poll.argtypes = [vp, C.POINTER(C.c_int32), C.POINTER(C.c_int32), vp]
     L.mosaic_window_close.argtypes = [vp, vp, vp, vp, vp, C.c_int64, vp]
+    L.mosaic_window_rotations.argtypes = [vp, vp, vp, vp, sz, vp]
     L.mosaic_set_timing.argtypes = [vp, C.c_int32]
     L.mosaic_decode_timing.argtypes = [vp, C.POINTER(C.c_float)]
     L.mosaic_seq_tokens.argtypes = [vp, C.c_int32]

@@ -39,6 +39,8 @@ mosaic_status hip_fail(hipError_t e, const char *what) {
 }
 
 uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
+// window rotations: int32 [pairs] flags, then fp32 [pairs][K, V][D][D]
+size_t window_rot_ws_bytes(int npairs) { return align256((uint64_t)npairs * 4) + (size_t)npairs * 2 * D * D * 4; }
 int ilog2(int v) { int l = 0; while ((1 << l) < v) ++l; return l; }
 
 }  // namespace
@@ -424,6 +426,7 @@ mosaic_status mosaic_workspace_bytes(const mosaic_cache *c, int32_t op, size_t *
     if (op == MOSAIC_OP_COMPRESS) *bytes = (size_t)c->npairs * c->max_desc * ((size_t)c->slot_tok + c->slot_sc);
     else if (op == MOSAIC_OP_APPEND) *bytes = 0;
     else if (op == MOSAIC_OP_DECODE) *bytes = c->wsl.total;
+    else if (op == MOSAIC_OP_WINDOW_ROTATIONS) *bytes = c->dyn ? window_rot_ws_bytes(c->npairs) : 0;
     else return fail(MOSAIC_ERR_INVALID, "unknown op %d", op);
     return ok();
 }
@@ -759,6 +762,23 @@ mosaic_status mosaic_window_poll(mosaic_cache *c, int32_t *out_host, int32_t *n_
     }
     c->poll_due = false;
     *n_closed_host = n;
+    return ok();
+}
+
+mosaic_status mosaic_window_rotations(mosaic_cache *c, float *rot_k, float *rot_v, void *ws, size_t ws_bytes,
+                                      void *stream) {
+    if (!c) return fail(MOSAIC_ERR_INVALID, "NULL cache");
+    if (!c->dyn) return fail(MOSAIC_ERR_INVALID, "the cache was created without dynamic windows");
+    if (!c->arena || !c->compressed) return fail(MOSAIC_ERR_STATE, "rotations before compress");
+    if (c->poll_due) return fail(MOSAIC_ERR_STATE, "a segment completed since the last mosaic_window_poll");
+    if (!rot_k || !rot_v || !ws) return fail(MOSAIC_ERR_INVALID, "NULL rot_k, rot_v or ws");
+    if (((uintptr_t)rot_k | (uintptr_t)rot_v) % 16 || (uintptr_t)ws % 256)
+        return fail(MOSAIC_ERR_INVALID, "rot_k and rot_v must be 16-byte aligned, ws 256-byte aligned");
+    if (ws_bytes < window_rot_ws_bytes(c->npairs))
+        return fail(MOSAIC_ERR_INVALID, "workspace %zu bytes < %zu required", ws_bytes, window_rot_ws_bytes(c->npairs));
+    float *part = (float *)((uint8_t *)ws + align256((uint64_t)c->npairs * 4));
+    hipError_t e = launch_window_rotations(c->geom(), rot_k, rot_v, part, (int32_t *)ws, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "window rotation launch");
     return ok();
 }
 

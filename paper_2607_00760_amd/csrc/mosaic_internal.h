@@ -242,6 +242,10 @@ hipError_t launch_ctx_copy(int32_t *dst_dev, const int32_t *src_host, int n, hip
 hipError_t launch_pairs_copy(uint64_t *dst_dev, const uint64_t *src_host, int npairs, hipStream_t s);
 // nw_src: windows of rk / rv per pair; slots past them repeat the last one
 hipError_t launch_copy_rot(const Geom &g, const float *rk, const float *rv, int nw_src, hipStream_t s);
+// rotations of the windows awaiting them, from their incremental covariances
+// (dynamic windows): part = pairs * 2 * D * D floats, one_tok = pairs int32
+hipError_t launch_window_rotations(const Geom &g, float *rot_k, float *rot_v, float *part, int32_t *one_tok,
+                                   hipStream_t s);
 // close of the windows awaiting their rotation (dynamic windows): the new
 // rotations rk / rv [pairs][D][D], the windows' raw tokens k / v
 // [pairs][seq_stride][D]; max_segs: segments of the longest closed window

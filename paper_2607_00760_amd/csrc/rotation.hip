@@ -263,7 +263,38 @@ __global__ void __launch_bounds__(JT) k_jacobi(const int32_t *ctx, int hkv, int 
     }
 }
 
+// grid (pairs * 2), 256 threads: the incremental covariance of each pair's
+// window awaiting its rotation (K for z even, V for z odd), cast to fp32 and
+// symmetrized from the upper triangle as the solver expects, into the
+// solver's partials (one window, one slice); one_tok[pair] = 1 if the pair has
+// such a window (the solver then treats it as one window with a token), else
+// 0 (the solver writes the identity)
+__global__ void __launch_bounds__(256) k_cov_gather(Geom g, float *part, int32_t *one_tok) {
+    const int z = blockIdx.x, p = z >> 1, kv = z & 1, tid = threadIdx.x;
+    const int pw = g.meta_of(p)->pend;
+    if (tid == 0 && kv == 0) one_tok[p] = pw >= 0 ? 1 : 0;
+    if (pw < 0) return;
+    const double *C = g.cov_of(p, pw, kv);
+    float *dst = part + (uint64_t)z * D * D;
+    for (int i = tid; i < D * D; i += 256) {
+        const int r = i / D, c = i % D;
+        dst[i] = (float)C[min(r, c) * D + max(r, c)];
+    }
+}
+
 }  // namespace
+
+hipError_t launch_window_rotations(const Geom &g, float *rot_k, float *rot_v, float *part, int32_t *one_tok,
+                                   hipStream_t s) {
+    hipLaunchKernelGGL(k_cov_gather, dim3(g.npairs * 2), dim3(256), 0, s, g, part, one_tok);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const size_t smem = (size_t)2 * D * JP * sizeof(float);
+    // one "sequence" per pair, one window of one token when a window awaits
+    hipLaunchKernelGGL(k_jacobi, dim3(1, g.npairs * 2), dim3(JT), smem, s, (const int32_t *)one_tok, 1, 1, 1, 1,
+                       (const float *)part, rot_k, rot_v, (float *)nullptr, (float *)nullptr);
+    return hipGetLastError();
+}
 
 // workspace: the context lengths (int32 [num_seqs], padded to 256 bytes), then
 // the covariance partials [pairs][K, V][windows][slices][D][D] fp32

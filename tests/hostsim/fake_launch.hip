@@ -44,6 +44,10 @@ hipError_t launch_copy_rot(const Geom &g, const float *, const float *, int nw_s
     rec("copy_rot npairs=%d nw=%d src=%d", g.npairs, g.nw, nw_src);
     return hipSuccess;
 }
+hipError_t launch_window_rotations(const Geom &g, float *, float *, float *, int32_t *, hipStream_t) {
+    rec("window_rotations npairs=%d", g.npairs);
+    return hipSuccess;
+}
 hipError_t launch_close(const Geom &g, const float *, const float *, const uint16_t *, const uint16_t *,
                         int64_t seq_stride, int max_segs, hipStream_t) {
     rec("close npairs=%d stride=%lld segs=%d", g.npairs, (long long)seq_stride, max_segs);

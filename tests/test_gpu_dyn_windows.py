@@ -8,7 +8,9 @@ poll or a close is due, the test polls, checks that the windows the GPU
 closed are exactly the ones the oracle closed and that each closed window's
 incrementally accumulated covariance is bit-exact against the oracle's,
 computes the window's rotation from that covariance on the host (fp64
-eigendecomposition, Sec. 5.5) and hands the same rotation to both.  At
+eigendecomposition, Sec. 5.5) and hands the same rotation to both (the
+rotations the GPU computes from its own covariances are checked by their
+defining properties).  At
 checkpoints the whole state of every pair (arenas, descriptors, update
 buffer, staging, window table and the open window's loss bits) is
 byte-exact against the oracle, block scores and
@@ -74,6 +76,32 @@ def _gpu_windows(c, p, nwin_max):
     return dict(nwin=nwin, pend=pend, wloss=float(wloss), wseg=wseg)
 
 
+def _check_gpu_rotations(c, ops, got, ns):
+    """mosaic_window_rotations: the closed windows' rotations computed on the
+    GPU from their incremental covariances, checked by the properties that
+    define them against the oracle's fp64 covariance (eigenvectors of close
+    eigenvalues are not unique): orthonormal rows, R C R^T diagonal with the
+    eigenvalues in descending order, the sign rule; the identity for pairs
+    with nothing to close."""
+    rk, rv = (x.cpu().numpy() for x in c.window_rotations())
+    for p in range(ns * HKV):
+        b, h = divmod(p, HKV)
+        for R, which in ((rk[b, h], 0), (rv[b, h], 1)):
+            if p not in got:
+                assert np.array_equal(R, np.eye(D, dtype=np.float32)), p
+                continue
+            Cw = ops[p].cov(got[p][0])[which]
+            lam = np.linalg.eigvalsh(Cw)[::-1]
+            Rd = R.astype(np.float64)
+            assert np.abs(Rd @ Rd.T - np.eye(D)).max() < 1e-4, p
+            A = Rd @ Cw @ Rd.T
+            off = A - np.diag(np.diag(A))
+            assert np.sqrt((off ** 2).sum()) < 5e-5 * lam[0] * D, p
+            assert np.abs(np.diag(A) - lam).max() < 5e-5 * lam[0], p
+            idx = np.argmax(np.abs(Rd), axis=1)
+            assert np.all(Rd[np.arange(D), idx] > 0), p
+
+
 @pytest.mark.parametrize("variant", list(VARIANTS))
 def test_loss_closed_windows_match_oracle(variant):
     """Also with E4M3 token values and with 96-channel truncated bitmaps: the
@@ -109,6 +137,7 @@ def test_loss_closed_windows_match_oracle(variant):
                     want[p] = (w["pend"], a * 64, (bnd - a) * 64)
             assert got == want, f"step {t}: GPU closed {got}, oracle {want}"
             if got:
+                _check_gpu_rotations(c, ops, got, ns)
                 maxlen = max(n for _, _, n in got.values())
                 Rk = torch.zeros((ns, HKV, D, D))
                 Rv = torch.zeros_like(Rk)

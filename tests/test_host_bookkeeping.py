@@ -198,6 +198,11 @@ def run_checks(path):
     assert L.mosaic_append(h4, kv, kv, None) == OK                                           # 64: finalize
     assert sim.log()[-1] == "maintain mode=0 flush=0 finalize=1"
     assert L.mosaic_window_close(h4, rot4, rot4, kv, kv, 64, None) == STATE                  # poll first
+    wrb = C.c_size_t()
+    assert L.mosaic_workspace_bytes(h4, 3, C.byref(wrb)) == OK and wrb.value >= 2 * 2 * 128 * 128 * 4
+    wr = sim.buf(wrb.value)
+    assert L.mosaic_window_rotations(h4, rot4, rot4, wr, wrb.value, None) == STATE           # poll first too
+    assert L.mosaic_window_rotations(h4, rot4, rot4, wr, wrb.value - 1, None) == STATE
     for _ in range(19):                                                                      # no compression due
         assert L.mosaic_append(h4, kv, kv, None) == OK
     # sequence 1 would reach 32 tokens: its buffer would be compressed before a poll
