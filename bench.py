@@ -159,9 +159,11 @@ def dyn_window_us(M, gen, spec, params, dev, reps=3):
     tokens, Sec. 5.5), c3 batch shape, 4096-token windows: a 4032-token
     prefill per pair, so that the 64th append completes the window's last
     segment and closes it (maximum length).  Times that append (finalize plus
-    the loss update) and mosaic_window_close (every pair's new rotation and the
-    re-encoding of its 4096 tokens, strategy and packing passes); medians over
-    `reps` fresh caches."""
+    the loss update), mosaic_window_rotations (every pair's K and V rotation
+    from the window's incremental covariance, Jacobi on the GPU) and
+    mosaic_window_close (the new rotations and the re-encoding of each pair's
+    4096 tokens, strategy and packing passes); medians over `reps` fresh
+    caches."""
     import dataclasses
     import torch
     W = 4096
@@ -171,15 +173,14 @@ def dyn_window_us(M, gen, spec, params, dev, reps=3):
     apps = [tuple(x.to(dev) for x in gen.make_appends(small, t)) for t in range(64)]
     kw = torch.cat([lay["k"][:, :, :W - 64], torch.stack([a[0] for a in apps], dim=2)], dim=2).contiguous()
     vw = torch.cat([lay["v"][:, :, :W - 64], torch.stack([a[1] for a in apps], dim=2)], dim=2).contiguous()
-    rk, rv = lay["rot_k"][:, :, 0].contiguous(), lay["rot_v"][:, :, 0].contiguous()
-    fin, close = [], []
+    fin, rot, close = [], [], []
     for _ in range(reps):
         cache = M.MosaicCache(dp, small.num_seqs, small.capacity, rotated=True, device=dev)
         cache.compress(lay["k"], lay["v"], lay["ctx_lens"], lay["rot_k"], lay["rot_v"])
         for t in range(63):
             cache.append(*apps[t])
         torch.cuda.synchronize()
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
         ev[0].record()
         cache.append(*apps[63])
         ev[1].record()
@@ -187,16 +188,20 @@ def dyn_window_us(M, gen, spec, params, dev, reps=3):
         if len(closed) != cache.num_pairs or any(x[2] != W for x in closed.values()):
             raise RuntimeError(f"expected every window to close at {W} tokens: {closed}")
         ev[2].record()
-        cache.window_close(rk, rv, kw, vw)
+        rk, rv = cache.window_rotations()
         ev[3].record()
+        ev[4].record()
+        cache.window_close(rk, rv, kw, vw)
+        ev[5].record()
         torch.cuda.synchronize()
         fin.append(1e3 * ev[0].elapsed_time(ev[1]))
-        close.append(1e3 * ev[2].elapsed_time(ev[3]))
+        rot.append(1e3 * ev[2].elapsed_time(ev[3]))
+        close.append(1e3 * ev[4].elapsed_time(ev[5]))
         del cache
     med = lambda xs: float(sorted(xs)[len(xs) // 2])
     pairs = small.num_seqs * small.hkv
     return {"pairs": pairs, "window_tokens": W, "append_with_finalize_and_close_us": round(med(fin), 1),
-            "window_close_us": round(med(close), 1), "close_tokens_per_s": round(pairs * W / (med(close) * 1e-6)),
+            "window_rotations_us": round(med(rot), 1), "window_close_us": round(med(close), 1), "close_tokens_per_s": round(pairs * W / (med(close) * 1e-6)),
             "reps": reps}
 
 
