@@ -111,6 +111,9 @@ def test_loss_closed_windows_match_oracle(variant):
     print(f"[dyn] {variant} ctx={CTX} appends={APPENDS} W={W} min={MINW} tau={TAU}", flush=True)
     c = M.MosaicCache(lp, ns, cap, rotated=True)
     c.compress(k.cuda(), v.cuda(), list(CTX), rk.cuda(), rv.cuda())
+    # no window awaits a close yet: every pair's rotations are the identity
+    for R in c.window_rotations():
+        assert torch.equal(R.cpu(), torch.eye(D).expand(ns, HKV, D, D)), "rotations before any close"
     ops = []
     for p in range(npairs):
         b, h = divmod(p, HKV)
