@@ -1111,6 +1111,12 @@ __global__ void __launch_bounds__(1024) k_tkm_write(Geom g, WsGeom ws, int nch) 
     const int p = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
     TkmCtx t;
     const bool mine = tkm_setup(g, ws, p, c, t);
+    // the record info of this thread's four blocks, loaded with the keys
+    // (taken or not): it is not waited on until the list is written
+    const uint2 *bi = ws.binfo + (uint64_t)p * (ws.binfo_stride / 8);
+    uint2 br[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) br[e] = t.in(e) ? bi[t.i0 + e] : make_uint2(0u, 0u);
     const int nvalid = (t.nb + TKM_CHUNK - 1) / TKM_CHUNK;  // chunks holding blocks
     const uint32_t *tk = t.st + 3 * TOPK_BINS + 16 + nch;
     uint32_t before = 0u, k = 0u;
@@ -1128,10 +1134,6 @@ __global__ void __launch_bounds__(1024) k_tkm_write(Geom g, WsGeom ws, int nch) 
     const uint32_t pos0 = before + v[0];
     int32_t *sel = ws.sel + (uint64_t)p * (ws.sel_stride / 4);
     uint2 *sinfo = ws.selinfo + (uint64_t)p * (ws.selinfo_stride / 8);
-    const uint2 *bi = ws.binfo + (uint64_t)p * (ws.binfo_stride / 8);
-    uint2 br[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) br[e] = ((m >> e) & 1u) ? bi[t.i0 + e] : make_uint2(0u, 0u);
     uint32_t pos = pos0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -1978,9 +1980,11 @@ __global__ void __launch_bounds__(CMB_THREADS) k_combine(Geom g, WsGeom ws, floa
 }
 
 // one thread per output (pair, head, column): the log-sum-exp merge of its
-// window slots' results, in slot order
+// window slots' results, in slot order; the slots are read eight per round
+// trip (a long context has dozens of windows)
 template <int GP>
 __global__ void __launch_bounds__(256) k_merge(Geom g, WsGeom ws, float *out) {
+    constexpr int MU = 8;
     const int i = blockIdx.x * 256 + threadIdx.x;
     const int p = i / (GP * D), h = (i / D) % GP, j = i % D;
     if (p >= g.npairs || h >= g.G) return;
@@ -1988,15 +1992,25 @@ __global__ void __launch_bounds__(256) k_merge(Geom g, WsGeom ws, float *out) {
     const float *r = ws.wres + (uint64_t)p * (ws.wres_stride / 4) + (uint64_t)cc * (g.nw + 1) * (GP * CMB_RES)
                      + h * CMB_RES;
     float M = -INFINITY, Lsum = 0.0f, o = 0.0f;
-    for (int x = 0; x <= g.nw; ++x, r += GP * CMB_RES) {
-        const float wm = r[0];
-        if (wm == -INFINITY) continue;
-        const float wl = r[1], y = r[2 + jj];
-        const float mn = fmaxf(M, wm);
-        const float a = __expf(M - mn), b = __expf(wm - mn);    // M = -inf: a = 0
-        o = o * a + y * b;
-        Lsum = Lsum * a + wl * b;
-        M = mn;
+    for (int x0 = 0; x0 <= g.nw; x0 += MU) {
+        float wm[MU], wl[MU], y[MU];
+#pragma unroll
+        for (int u = 0; u < MU; ++u) {
+            wm[u] = -INFINITY; wl[u] = 0.0f; y[u] = 0.0f;
+            if (x0 + u <= g.nw) {
+                const float *rr = r + (uint64_t)(x0 + u) * (GP * CMB_RES);
+                wm[u] = rr[0]; wl[u] = rr[1]; y[u] = rr[2 + jj];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < MU; ++u) {
+            if (wm[u] == -INFINITY) continue;
+            const float mn = fmaxf(M, wm[u]);
+            const float a = __expf(M - mn), b = __expf(wm[u] - mn);    // M = -inf: a = 0
+            o = o * a + y[u] * b;
+            Lsum = Lsum * a + wl[u] * b;
+            M = mn;
+        }
     }
     out[((uint64_t)p * g.G + h) * D + j] = (Lsum > 0.0f) ? o / Lsum : 0.0f;
 }
